@@ -1,0 +1,217 @@
+/*
+ * qf.h -- C ABI of libqf: deployment-aligned simulated ("fake") quantization and the
+ * quantization-aware linear layer with a straight-through backward, for AMD MI355X (gfx950).
+ *
+ * Method: QATFactory, Sec. 3.2 "Deployment-aligned simulated quantization".
+ *   Q(X) -> (C, theta), Q^-1(C, theta) -> X_hat                         Eq. quantize-dequantize
+ *   W_hat = Q^-1(Q(W)), A_hat = Q^-1(Q(A)), O = W_hat A_hat              Eq. fakequant
+ *   dL/dW ~= dL/dO A_hat^T                                               Eq. ste
+ *   dL/dA ~= W_hat^T dL/dO                                               Eq. activation-ste
+ * Formats (Sec. 3.2.3, Tab. formats): NVFP4 (E2M1 + E4M3 per 16 + FP32 tensor scale),
+ * MXFP4 (E2M1 + E8M0 per 32), Q4_K (uint4 + 6-bit scales/mins per 32 + FP16 per 256).
+ *
+ * Conventions (all entry points)
+ *  - Tensors are row-major.  Activations are [M, K] (tokens x in-features), weights follow
+ *    nn.Linear: [N, K] (out x in), outputs [M, N].  Quantization blocks run along K.
+ *  - bf16 / fp16 tensors are passed as raw 16-bit words (uint16_t), little-endian.
+ *  - Every tensor pointer is DEVICE memory owned by the caller.  The library allocates no
+ *    device memory; scratch comes from the caller's workspace (qf_workspace_size).
+ *  - Calls are asynchronous on `stream` (a hipStream_t; 0 = the null stream).  Inputs must
+ *    stay valid and outputs must not be read until the stream reaches that point.
+ *  - Every call returns a qf_status.  Validation is done on the host before any launch:
+ *    on error nothing is launched and qf_last_error() returns a message (thread-local).
+ *    Non-finite data is never an error; it propagates as each format defines.
+ *  - Alignment: every tensor base pointer must be 16-byte aligned and every leading
+ *    dimension a multiple of 8 elements (QF_EALIGN otherwise).
+ *  - Nibble order: two 4-bit codes per byte, element 2i in the LOW nibble.  Code layout:
+ *    bit 3 = sign, bits 0-2 = E2M1 magnitude index into {0, .5, 1, 1.5, 2, 3, 4, 6}.
+ *  - Scale layout: plain row-major [R, K/block] bytes (E4M3 for NVFP4, E8M0 for MXFP4).
+ */
+#ifndef QF_H
+#define QF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef void* qf_stream_t; /* a hipStream_t */
+
+typedef enum {
+    QF_OK = 0,
+    QF_EINVAL = 1,   /* null required pointer, bad enum, aliasing that the call forbids */
+    QF_ESHAPE = 2,   /* negative size, K not a multiple of the format's block, ld < K   */
+    QF_EALIGN = 3,   /* pointer not 16-byte aligned or ld not a multiple of 8          */
+    QF_ENOTSUP = 4,  /* valid request that this build does not implement               */
+    QF_EDEVICE = 5   /* a HIP launch failed (message carries the HIP error string)      */
+} qf_status;
+
+typedef enum {
+    QF_FMT_NONE = 0,   /* no quantization: the tensor is used as is (W4A16 activations)  */
+    QF_FMT_NVFP4 = 1,
+    QF_FMT_MXFP4 = 2,
+    QF_FMT_Q4K = 3     /* weights only (Tab. formats: W4A16)                              */
+} qf_format;
+
+typedef enum {
+    QF_AMAX_COMPUTE = 0, /* the call computes g = max|x| and stores it in *amax             */
+    QF_AMAX_GIVEN = 1    /* *amax already holds g (running activation amax, Sec. 3.2.3
+                            NVFP4 paragraph; or a tied-group max, "Engine-specific scale
+                            sharing")                                                    */
+} qf_amax_mode;
+
+/* Library version (major*10000 + minor*100 + patch) and the last error on this thread. */
+int qf_version(void);
+const char* qf_last_error(void);
+
+/*
+ * qf_amax -- tensor amax g = max |x| over a bf16 [R, K] tensor (Sec. 3.2.1: scales derive
+ * from the maximum absolute value).  `amax` is a device FP32 scalar.
+ *   accumulate = 0: *amax = g.   accumulate = 1: *amax = max(*amax, g) -- the running
+ *   activation amax of Sec. 3.2.3 (NVFP4 paragraph), and the way to build a tied-scale group
+ *   ("Engine-specific scale sharing": call once per member).
+ * NaN inputs make *amax NaN.  R = 0 or K = 0 leaves a zero (accumulate = 0) or unchanged value.
+ */
+qf_status qf_amax(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, float* amax,
+                  int accumulate, qf_stream_t stream);
+
+/*
+ * qf_fakequant_nvfp4 -- NVFP4 quantize + dequantize (Eqs. nvfp4, nvfp4-dequant).
+ *   x       bf16 [R, K] (row stride ldx elements), K % 16 == 0.
+ *   amax    device FP32 scalar, required.  amax_mode = QF_AMAX_COMPUTE: the call writes g;
+ *           QF_AMAX_GIVEN: the call reads g.
+ *   s_out   device FP32 scalar or NULL: receives the tensor decode scale S = g / 2688
+ *           (2688 = 6 * 448, largest E2M1 times largest E4M3).  Must not alias `amax`.
+ *   codes   [R, K/2] bytes or NULL;  scales [R, K/16] E4M3 bytes or NULL;
+ *   xhat    bf16 [R, K] (row stride K) or NULL.
+ * Per block of 16: t = a_b / (6 S) rounded to the nearest E4M3 (saturating at 448),
+ * D_b = S * s_E4M3, codes = nearest E2M1 to |x| * (1 / D_b) (ties to even, saturating),
+ * x_hat = bf16(+-V * D_b).  g = 0 gives all-zero scales and codes carrying only the sign.
+ */
+qf_status qf_fakequant_nvfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
+                             float* amax, int amax_mode, float* s_out, uint8_t* codes,
+                             uint8_t* scales, uint16_t* xhat, qf_stream_t stream);
+
+/*
+ * qf_fakequant_mxfp4 -- MXFP4 quantize + dequantize (Eqs. mxfp4, mxfp4-dequant).
+ *   x bf16 [R, K], K % 32 == 0.  codes [R, K/2] or NULL; scales [R, K/32] E8M0 or NULL;
+ *   xhat bf16 [R, K] or NULL.
+ * Per block of 32: p = floor(log2 max|x|) - 2 clamped to [-127, 127] (code p + 127),
+ * codes = nearest E2M1 to |x| / 2^p (ties to even, saturating at 6), x_hat = +-V * 2^p.
+ * All-zero block: code 0.  Block holding Inf/NaN: scale 0xFF, codes 0, x_hat NaN (0x7FC0).
+ */
+qf_status qf_fakequant_mxfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
+                             uint8_t* codes, uint8_t* scales, uint16_t* xhat,
+                             qf_stream_t stream);
+
+/*
+ * qf_fakequant_q4k -- Q4_K quantize + dequantize + llama.cpp block packing
+ * (Eqs. q4k, q4k-dequant; Sec. 3.5 engine-native export).
+ *   x bf16 [R, K], K % 256 == 0.  packed [R, K/256, 144] bytes or NULL; xhat bf16 [R, K] or NULL.
+ * Block of 144 bytes: FP16 d, FP16 dmin, 12 bytes of 6-bit scales/mins, 128 bytes of codes
+ * (byte 32c+l: code 64c+l in the low nibble, code 64c+32+l in the high nibble).
+ * Scale search ("min-max"): per sub-block of 32 the range [min(0, min x), max x] is split
+ * into 15 steps; d, dmin = FP16(max step / 63), FP16(max offset / 63); 6-bit scale and min =
+ * nearest integers; code = nearest integer to (x + dmin*m6) / (d*s6) clamped to [0, 15];
+ * x_hat = bf16(d*s6*code - dmin*m6).  Signed zeros in x count as +0.
+ */
+qf_status qf_fakequant_q4k(const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
+                           uint8_t* packed, uint16_t* xhat, qf_stream_t stream);
+
+/* ---------------------------------------------------------------------------------------
+ * Quantization-aware linear layer (Eqs. fakequant, ste, activation-ste)
+ * ------------------------------------------------------------------------------------ */
+
+/* flags */
+#define QF_FLAG_REUSE_WS 1u /* backward: the workspace still holds W_hat / A_hat written by the
+                               forward on the same X, W, desc (skips re-quantization; the
+                               bits are identical either way) */
+
+typedef struct {
+    int64_t M, N, K;      /* X [M, K], W [N, K], Y [M, N]                                  */
+    int64_t ldx, ldw, ldy;/* row strides (elements) of X / dX, W, Y / dY; 0 means dense     */
+    int32_t wfmt;         /* qf_format of the weight                                       */
+    int32_t afmt;         /* qf_format of the activation (QF_FMT_NONE = W4A16 training)    */
+    float* w_amax;        /* NVFP4 weight: device FP32 scalar or NULL.  NULL: g computed
+                             from W every call (Sec. 3.2.1, per-forward re-quantization).
+                             Non-NULL: holds the tied-group g (read only).                 */
+    float* a_amax;        /* NVFP4 activation: device FP32 scalar holding the running
+                             amax (read only).  Required when afmt == QF_FMT_NVFP4.       */
+    uint32_t flags;       /* QF_FLAG_*                                                     */
+} qf_qlinear_desc;
+
+/* Bytes of device workspace qf_qlinear_fwd / qf_qlinear_bwd_ste need for `d` (host only). */
+qf_status qf_workspace_size(const qf_qlinear_desc* d, size_t* bytes);
+
+/*
+ * qf_qlinear_fwd -- Y = A_hat W_hat^T (bf16 output, FP32 accumulation on MFMA).
+ *   X bf16 [M, K], W bf16 [N, K], Y bf16 [M, N]; ws >= qf_workspace_size bytes, 256-aligned.
+ * The workspace receives W_hat (and A_hat when afmt != NONE) as bf16.
+ */
+qf_status qf_qlinear_fwd(const qf_qlinear_desc* d, const uint16_t* X, const uint16_t* W,
+                         uint16_t* Y, void* ws, size_t ws_bytes, qf_stream_t stream);
+
+/*
+ * qf_qlinear_bwd_ste -- straight-through backward.
+ *   dX = dY W_hat      bf16 [M, K]  (Eq. activation-ste)        dX may be NULL
+ *   dW = dY^T A_hat    FP32 [N, K]  (Eq. ste; A_hat = X when afmt == NONE)  dW may be NULL
+ * dY is bf16 [M, N] and is not quantized.  dW is overwritten (not accumulated).
+ */
+qf_status qf_qlinear_bwd_ste(const qf_qlinear_desc* d, const uint16_t* dY, const uint16_t* X,
+                             const uint16_t* W, uint16_t* dX, float* dW, void* ws,
+                             size_t ws_bytes, qf_stream_t stream);
+
+/* ---------------------------------------------------------------------------------------
+ * Grouped (mixture-of-experts) variant (Sec. 3.3 "Mixture-of-experts adaptation")
+ * ------------------------------------------------------------------------------------ */
+typedef struct {
+    int64_t E;            /* experts                                                       */
+    int64_t T;            /* rows of X / Y: tokens x top-k, sorted by expert               */
+    int64_t N, K;         /* per-expert weight [N, K]                                      */
+    int32_t wfmt, afmt;   /* afmt must be QF_FMT_NONE or QF_FMT_MXFP4                       */
+    float* w_amax;        /* NVFP4: device FP32 [E] or NULL (NULL: per-expert g computed)  */
+    uint32_t flags;
+} qf_grouped_desc;
+
+qf_status qf_grouped_workspace_size(const qf_grouped_desc* d, size_t* bytes);
+
+/*
+ * qf_qlinear_grouped_fwd -- for every expert e, rows [off[e], off[e+1]) of X:
+ *   Y_e = A_hat_e W_hat_e^T with W_hat_e = Q^-1(Q(W[e])), one tensor scale per expert.
+ *   group_offsets: DEVICE int64 [E+1], non-decreasing, off[0] = 0, off[E] = T (the host never
+ *   reads it).  X bf16 [T, K], W bf16 [E, N, K], Y bf16 [T, N].
+ */
+qf_status qf_qlinear_grouped_fwd(const qf_grouped_desc* d, const int64_t* group_offsets,
+                                 const uint16_t* X, const uint16_t* W, uint16_t* Y, void* ws,
+                                 size_t ws_bytes, qf_stream_t stream);
+
+/*
+ * qf_qlinear_grouped_bwd_ste -- per expert: dX_e = dY_e W_hat_e (bf16 [T, K], may be NULL),
+ *   dW_e = dY_e^T A_hat_e (FP32 [E, N, K], may be NULL; experts with no rows get zeros).
+ */
+qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int64_t* group_offsets,
+                                     const uint16_t* dY, const uint16_t* X, const uint16_t* W,
+                                     uint16_t* dX, float* dW, void* ws, size_t ws_bytes,
+                                     qf_stream_t stream);
+
+/* ---------------------------------------------------------------------------------------
+ * Plain BF16 GEMMs on the same MFMA kernels (building blocks of the layer calls above)
+ * ------------------------------------------------------------------------------------ */
+/*
+ * qf_gemm_bf16 -- C[M, N] = sum_k opA(m, k) * opB(n, k), FP32 accumulation.
+ *   a_kmajor = 1: A stored [M, K] (k contiguous, row stride lda); 0: stored [K, M].
+ *   b_kmajor = 1: B stored [N, K] (k contiguous, row stride ldb); 0: stored [K, N].
+ *   c_f32 = 1: C is FP32, else bf16; row stride ldc.
+ * Forward = (1, 1); dX = dY W_hat is (1, 0); dW = dY^T A_hat is (0, 0).
+ */
+qf_status qf_gemm_bf16(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
+                       int a_kmajor, const uint16_t* B, int64_t ldb, int b_kmajor, void* C,
+                       int64_t ldc, int c_f32, qf_stream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QF_H */

@@ -390,9 +390,11 @@ void or_q4k_unpack_block(const uint8_t* in, uint16_t* dh, uint16_t* mh, int* ls,
 /*
  * Reading ("min-max"; the paper fixes the representation and the decode equation, not the
  * scale search):
- *  per sub-block j of 32: lo_j = min(0, min x), hi_j = max x,
- *     a_j = fl(fl(hi_j - lo_j) / 15), mu_j = -lo_j   (the unsigned min m_6 is subtracted,
- *     so the offset is never positive)
+ *  per sub-block j of 32: lo_j = min(0, min x), hi_j = max x, signed zeros counted as +0
+ *     (the sign of a zero plays no part in an unsigned-code format, and this keeps the
+ *     extremes independent of element order),
+ *     a_j = fl(fl(hi_j - lo_j) / 15), mu_j = fl(0 - lo_j)   (the unsigned min m_6 is
+ *     subtracted, so the offset is never positive)
  *  per super-block of 256: s_FP16 = h(fl(max a_j / 63)), m_FP16 = h(fl(max mu_j / 63))
  *  s_6,j = clamp(rne(fl(a_j / s_FP16)), 0, 63), m_6,j = clamp(rne(fl(mu_j / m_FP16)), 0, 63)
  *     (0 when the FP16 value is 0)
@@ -408,15 +410,15 @@ void or_q4k_quant(const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
             const uint16_t* xs = x + r * ldx + sb * 256;
             float a[8], mu[8];
             for (int j = 0; j < 8; ++j) {
-                float lo = 0.0f, hi = or_bf16_to_f32(xs[32 * j]);
+                float lo = 0.0f, hi = or_bf16_to_f32(xs[32 * j]) + 0.0f;   /* -0 -> +0 */
                 for (int i = 0; i < 32; ++i) {
-                    float v = or_bf16_to_f32(xs[32 * j + i]);
+                    float v = or_bf16_to_f32(xs[32 * j + i]) + 0.0f;
                     if (v < lo) lo = v;
                     if (v > hi) hi = v;
                 }
                 float range = hi - lo;
                 a[j] = range / 15.0f;
-                mu[j] = -lo;
+                mu[j] = 0.0f - lo;
             }
             float amx = a[0], mmx = mu[0];
             for (int j = 1; j < 8; ++j) {

@@ -413,3 +413,19 @@ def test_effective_bits_per_weight_match_paper_table():
     assert 8 * qk["packed"].nbytes / n == rows["q4k"][3]
     assert K // nv["scales"].shape[1] == rows["nvfp4"][0]
     assert K // mx["scales"].shape[1] == rows["mxfp4"][0]
+
+
+def test_q4k_signed_zeros_count_as_positive_zero():
+    # Reading of Eq. q4k: codes are unsigned, so the sign of a zero input carries no
+    # information; -0 and +0 inputs give the same packed block and x_hat.
+    x = _q4k_inputs(seed=6, R=4, K=256)
+    x[:, :32] = 0x0000
+    x[:, 40:60] = 0x0000
+    y = x.copy()
+    y[:, :32] = 0x8000
+    y[:, 40:60:2] = 0x8000
+    a, b = oracle.q4k(x), oracle.q4k(y)
+    np.testing.assert_array_equal(a["packed"], b["packed"])
+    np.testing.assert_array_equal(a["xhat"], b["xhat"])
+    d, m, ls, lm, qq = _q4k_fields(a["packed"])
+    assert np.all(np.signbit(m) == False)
