@@ -1,0 +1,200 @@
+"""Benchmark: one quantization-aware linear layer step (fake quant + BF16 MFMA GEMMs,
+forward + straight-through backward) on one MI355X.
+
+Workload (default): the 8B-class MLP up-projection with MXFP4 weights and activations,
+X [8192, 4096], W [14336, 4096], dY [8192, 14336] (seeded synthetic bf16, see workloads/).
+One step is the whole hot path, in the order the layer runs it:
+    forward:  Q(W) -> W_hat, Q(X) -> X_hat (MXFP4 quantize-dequantize), Y = X_hat W_hat^T
+    backward: Q(W), Q(X) again (the quantized tensors are transient, as in the paper),
+              dX = dY W_hat, dW = dY^T X_hat (FP32)
+`value` is the step's throughput in TFLOP/s over the three GEMMs' 3 * 2MNK flops, with the
+quantization time inside the step.  Each launch is bracketed by HIP events on the stream it
+runs on, which gives per-kernel durations for the roofline record.  The fake-quant kernel
+bandwidth is measured separately over rotating input buffers (>1 GB) so the 256 MB MALL
+cannot serve repeated reads.
+
+Prints ONE JSON line.  Only --gpus 1 is supported.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense BF16 MFMA
+PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-rows", type=int, default=256,
+                   help="token rows in the CPU oracle's bounded sample of the step")
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU path is "
+              "not part of this build", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2609_39223_amd as qf
+    import workloads
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    qf.lib()
+    w = workloads.mlp_up(seed=0)
+    M, N, K = w["M"], w["N"], w["K"]
+
+    def up(a):
+        return torch.from_numpy(a.view(np.int16)).to(dev)
+
+    X, W, dY = up(w["X"]), up(w["W"]), up(w["dY"])
+    what = torch.empty(N, K, dtype=torch.int16, device=dev)
+    xhat = torch.empty(M, K, dtype=torch.int16, device=dev)
+    Y = torch.empty(M, N, dtype=torch.int16, device=dev)
+    dX = torch.empty(M, K, dtype=torch.int16, device=dev)
+    dW = torch.empty(N, K, dtype=torch.float32, device=dev)
+
+    phases = ["quant_W", "quant_X", "gemm_fwd", "requant_W", "gemm_dX", "requant_X", "gemm_dW"]
+
+    def step(ev=None):
+        def mark(i):
+            if ev is not None:
+                ev[i].record()
+        mark(0)
+        qf.fakequant_mxfp4(W, None, None, what)
+        mark(1)
+        qf.fakequant_mxfp4(X, None, None, xhat)
+        mark(2)
+        qf.gemm_bf16(M, N, K, xhat, K, 1, what, K, 1, Y, N, 0)
+        mark(3)
+        qf.fakequant_mxfp4(W, None, None, what)
+        mark(4)
+        qf.gemm_bf16(M, K, N, dY, N, 1, what, K, 0, dX, K, 0)
+        mark(5)
+        qf.fakequant_mxfp4(X, None, None, xhat)
+        mark(6)
+        qf.gemm_bf16(N, K, M, dY, N, 0, xhat, K, 0, dW, K, 1)
+        mark(7)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(phases) + 1)]
+              for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(events[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_phase = np.zeros(len(phases))
+    step_ms = []
+    for ev in events:
+        d = [ev[i].elapsed_time(ev[i + 1]) for i in range(len(phases))]
+        per_phase += d
+        step_ms.append(ev[0].elapsed_time(ev[-1]))
+    per_phase /= args.steps
+    ms_step = float(np.mean(step_ms))
+    gemm_flops = 2.0 * M * N * K
+    tflops = 3 * gemm_flops / (ms_step * 1e-3) / 1e12
+    gemm_ms = {p: float(per_phase[i]) for i, p in enumerate(phases) if p.startswith("gemm")}
+    dom = max(gemm_ms, key=gemm_ms.get)
+    achieved = gemm_flops / (gemm_ms[dom] * 1e-3) / 1e12
+
+    # ---- fake-quant bandwidth over rotating buffers (W-shaped, > 1 GB in total) -----------
+    nbuf = 10
+    bufs = [torch.empty_like(W) for _ in range(nbuf)]
+    for b in bufs:   # finite bf16 payloads of N(0, 0.02)-like magnitude
+        b.copy_((torch.randn(N, K, device=dev) * 0.02).to(torch.bfloat16).view(torch.int16))
+    codes = torch.empty(N, K // 2, dtype=torch.uint8, device=dev)
+    scales = torch.empty(N, K // 32, dtype=torch.uint8, device=dev)
+    outs = torch.empty(N, K, dtype=torch.int16, device=dev)
+    for b in bufs[:2]:
+        qf.fakequant_mxfp4(b, codes, scales, outs)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 3 * nbuf
+    e0.record()
+    for i in range(reps):
+        qf.fakequant_mxfp4(bufs[i % nbuf], codes, scales, outs)
+    e1.record()
+    torch.cuda.synchronize()
+    q_ms = e0.elapsed_time(e1) / reps
+    q_bytes = N * K * (2 + 2 + 0.5 + 1.0 / 32)
+    q_gbps = q_bytes / (q_ms * 1e-3) / 1e9
+    del bufs
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, args.cpu_rows)
+
+    out = {
+        "metric": "fake-quant GB/s and fused fake-quant+BF16 GEMM TFLOP/s (fwd+bwd), 1 MI355X",
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) activations with 41 outlier channels x20, N(0,0.02) weights)",
+        "config": {"workload": "mlp_up_mxfp4_w4a4: X 8192x4096, W 14336x4096, fwd + STE bwd",
+                   "M": M, "N": N, "K": K, "wfmt": "mxfp4", "afmt": "mxfp4"},
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None},
+        "phases_ms": {p: round(float(per_phase[i]), 4) for i, p in enumerate(phases)},
+        "fakequant": {"kernel": "mxfp4 (codes+scales+x_hat)", "tensor": f"{N}x{K}",
+                      "GBps": round(q_gbps, 1), "frac_hbm": round(q_gbps / PEAK_HBM_GBPS, 4),
+                      "us": round(q_ms * 1e3, 2), "bytes_per_elem": 4.53125},
+        "wall_s_timed": round(wall, 3),
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(w, rows):
+    """The CPU oracle on a bounded sample of the same step: `rows` token rows of X and dY
+    (full W): MXFP4 fake quant of W and of the sampled X rows, then the three FP64 products
+    restricted to those rows.  Throughput counts the sample's 3 * 2 * rows * N * K flops."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = 1
+    M, N, K = w["M"], w["N"], w["K"]
+    Xs, dYs = w["X"][:rows], w["dY"][:rows]
+    t0 = time.perf_counter()
+    wq = oracle.mxfp4(w["W"])["xhat"]
+    xq = oracle.mxfp4(Xs)["xhat"]
+    oracle.linear_fwd(xq, wq)
+    oracle.linear_dx(dYs, wq)
+    oracle.linear_dw(dYs, xq)
+    dt = time.perf_counter() - t0
+    flops = 3 * 2.0 * rows * N * K
+    return {"value": round(flops / dt / 1e12, 5), "unit": "TFLOP/s", "cores": int(cores),
+            "kind": "oracle", "seconds": round(dt, 2),
+            "sample": f"{rows} of {M} token rows (full {N}x{K} weight quantized), MXFP4 W4A4 "
+                      "fwd + dX + dW in FP64"}
+
+
+if __name__ == "__main__":
+    main()

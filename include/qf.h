@@ -37,6 +37,12 @@
 extern "C" {
 #endif
 
+#if defined(__GNUC__)
+#define QF_API __attribute__((visibility("default")))
+#else
+#define QF_API
+#endif
+
 typedef void* qf_stream_t; /* a hipStream_t */
 
 typedef enum {
@@ -63,8 +69,8 @@ typedef enum {
 } qf_amax_mode;
 
 /* Library version (major*10000 + minor*100 + patch) and the last error on this thread. */
-int qf_version(void);
-const char* qf_last_error(void);
+QF_API int qf_version(void);
+QF_API const char* qf_last_error(void);
 
 /*
  * qf_amax -- tensor amax g = max |x| over a bf16 [R, K] tensor (Sec. 3.2.1: scales derive
@@ -74,7 +80,7 @@ const char* qf_last_error(void);
  *   ("Engine-specific scale sharing": call once per member).
  * NaN inputs make *amax NaN.  R = 0 or K = 0 leaves a zero (accumulate = 0) or unchanged value.
  */
-qf_status qf_amax(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, float* amax,
+QF_API qf_status qf_amax(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, float* amax,
                   int accumulate, qf_stream_t stream);
 
 /*
@@ -90,7 +96,7 @@ qf_status qf_amax(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, float* a
  * D_b = S * s_E4M3, codes = nearest E2M1 to |x| * (1 / D_b) (ties to even, saturating),
  * x_hat = bf16(+-V * D_b).  g = 0 gives all-zero scales and codes carrying only the sign.
  */
-qf_status qf_fakequant_nvfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
+QF_API qf_status qf_fakequant_nvfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
                              float* amax, int amax_mode, float* s_out, uint8_t* codes,
                              uint8_t* scales, uint16_t* xhat, qf_stream_t stream);
 
@@ -102,7 +108,7 @@ qf_status qf_fakequant_nvfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ld
  * codes = nearest E2M1 to |x| / 2^p (ties to even, saturating at 6), x_hat = +-V * 2^p.
  * All-zero block: code 0.  Block holding Inf/NaN: scale 0xFF, codes 0, x_hat NaN (0x7FC0).
  */
-qf_status qf_fakequant_mxfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
+QF_API qf_status qf_fakequant_mxfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
                              uint8_t* codes, uint8_t* scales, uint16_t* xhat,
                              qf_stream_t stream);
 
@@ -117,7 +123,7 @@ qf_status qf_fakequant_mxfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ld
  * nearest integers; code = nearest integer to (x + dmin*m6) / (d*s6) clamped to [0, 15];
  * x_hat = bf16(d*s6*code - dmin*m6).  Signed zeros in x count as +0.
  */
-qf_status qf_fakequant_q4k(const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
+QF_API qf_status qf_fakequant_q4k(const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
                            uint8_t* packed, uint16_t* xhat, qf_stream_t stream);
 
 /* ---------------------------------------------------------------------------------------
@@ -143,14 +149,14 @@ typedef struct {
 } qf_qlinear_desc;
 
 /* Bytes of device workspace qf_qlinear_fwd / qf_qlinear_bwd_ste need for `d` (host only). */
-qf_status qf_workspace_size(const qf_qlinear_desc* d, size_t* bytes);
+QF_API qf_status qf_workspace_size(const qf_qlinear_desc* d, size_t* bytes);
 
 /*
  * qf_qlinear_fwd -- Y = A_hat W_hat^T (bf16 output, FP32 accumulation on MFMA).
  *   X bf16 [M, K], W bf16 [N, K], Y bf16 [M, N]; ws >= qf_workspace_size bytes, 256-aligned.
  * The workspace receives W_hat (and A_hat when afmt != NONE) as bf16.
  */
-qf_status qf_qlinear_fwd(const qf_qlinear_desc* d, const uint16_t* X, const uint16_t* W,
+QF_API qf_status qf_qlinear_fwd(const qf_qlinear_desc* d, const uint16_t* X, const uint16_t* W,
                          uint16_t* Y, void* ws, size_t ws_bytes, qf_stream_t stream);
 
 /*
@@ -159,7 +165,7 @@ qf_status qf_qlinear_fwd(const qf_qlinear_desc* d, const uint16_t* X, const uint
  *   dW = dY^T A_hat    FP32 [N, K]  (Eq. ste; A_hat = X when afmt == NONE)  dW may be NULL
  * dY is bf16 [M, N] and is not quantized.  dW is overwritten (not accumulated).
  */
-qf_status qf_qlinear_bwd_ste(const qf_qlinear_desc* d, const uint16_t* dY, const uint16_t* X,
+QF_API qf_status qf_qlinear_bwd_ste(const qf_qlinear_desc* d, const uint16_t* dY, const uint16_t* X,
                              const uint16_t* W, uint16_t* dX, float* dW, void* ws,
                              size_t ws_bytes, qf_stream_t stream);
 
@@ -175,7 +181,7 @@ typedef struct {
     uint32_t flags;
 } qf_grouped_desc;
 
-qf_status qf_grouped_workspace_size(const qf_grouped_desc* d, size_t* bytes);
+QF_API qf_status qf_grouped_workspace_size(const qf_grouped_desc* d, size_t* bytes);
 
 /*
  * qf_qlinear_grouped_fwd -- for every expert e, rows [off[e], off[e+1]) of X:
@@ -183,7 +189,7 @@ qf_status qf_grouped_workspace_size(const qf_grouped_desc* d, size_t* bytes);
  *   group_offsets: DEVICE int64 [E+1], non-decreasing, off[0] = 0, off[E] = T (the host never
  *   reads it).  X bf16 [T, K], W bf16 [E, N, K], Y bf16 [T, N].
  */
-qf_status qf_qlinear_grouped_fwd(const qf_grouped_desc* d, const int64_t* group_offsets,
+QF_API qf_status qf_qlinear_grouped_fwd(const qf_grouped_desc* d, const int64_t* group_offsets,
                                  const uint16_t* X, const uint16_t* W, uint16_t* Y, void* ws,
                                  size_t ws_bytes, qf_stream_t stream);
 
@@ -191,7 +197,7 @@ qf_status qf_qlinear_grouped_fwd(const qf_grouped_desc* d, const int64_t* group_
  * qf_qlinear_grouped_bwd_ste -- per expert: dX_e = dY_e W_hat_e (bf16 [T, K], may be NULL),
  *   dW_e = dY_e^T A_hat_e (FP32 [E, N, K], may be NULL; experts with no rows get zeros).
  */
-qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int64_t* group_offsets,
+QF_API qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int64_t* group_offsets,
                                      const uint16_t* dY, const uint16_t* X, const uint16_t* W,
                                      uint16_t* dX, float* dW, void* ws, size_t ws_bytes,
                                      qf_stream_t stream);
@@ -206,7 +212,7 @@ qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int64_t* gr
  *   c_f32 = 1: C is FP32, else bf16; row stride ldc.
  * Forward = (1, 1); dX = dY W_hat is (1, 0); dW = dY^T A_hat is (0, 0).
  */
-qf_status qf_gemm_bf16(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
+QF_API qf_status qf_gemm_bf16(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
                        int a_kmajor, const uint16_t* B, int64_t ldb, int b_kmajor, void* C,
                        int64_t ldc, int c_f32, qf_stream_t stream);
 

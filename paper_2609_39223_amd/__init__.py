@@ -1,0 +1,207 @@
+"""Python binding of libqf (C ABI in include/qf.h): argument marshalling only.
+
+Every function takes torch tensors that live on the GPU, passes their device pointers and
+the current HIP stream to the C entry point of the same name, and raises ``QFError`` when
+the call returns a non-OK status.  All arithmetic runs in the library's HIP kernels; there
+is no fallback path.  bf16 tensors may be ``torch.bfloat16`` or raw 16-bit integer tensors.
+
+Tensor conventions follow nn.Linear: X [M, K], W [N, K], Y [M, N]; dW is FP32 [N, K].
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libqf.so")
+
+FMT = {"none": 0, "nvfp4": 1, "mxfp4": 2, "q4k": 3}
+AMAX_COMPUTE, AMAX_GIVEN = 0, 1
+FLAG_REUSE_WS = 1
+STATUS = {0: "QF_OK", 1: "QF_EINVAL", 2: "QF_ESHAPE", 3: "QF_EALIGN", 4: "QF_ENOTSUP",
+          5: "QF_EDEVICE"}
+
+
+class QFError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class QLinearDesc(ctypes.Structure):
+    _fields_ = [("M", ctypes.c_int64), ("N", ctypes.c_int64), ("K", ctypes.c_int64),
+                ("ldx", ctypes.c_int64), ("ldw", ctypes.c_int64), ("ldy", ctypes.c_int64),
+                ("wfmt", ctypes.c_int32), ("afmt", ctypes.c_int32),
+                ("w_amax", ctypes.c_void_p), ("a_amax", ctypes.c_void_p),
+                ("flags", ctypes.c_uint32)]
+
+
+class GroupedDesc(ctypes.Structure):
+    _fields_ = [("E", ctypes.c_int64), ("T", ctypes.c_int64), ("N", ctypes.c_int64),
+                ("K", ctypes.c_int64), ("wfmt", ctypes.c_int32), ("afmt", ctypes.c_int32),
+                ("w_amax", ctypes.c_void_p), ("flags", ctypes.c_uint32)]
+
+
+_lib = None
+_P = ctypes.c_void_p
+_I = ctypes.c_int64
+
+
+def lib() -> ctypes.CDLL:
+    """Load libqf.so (built in-tree by ``__graft_entry__.build()``); no fallback."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+        torch.cuda.init()  # bind the process's HIP runtime before the library loads
+        L = ctypes.CDLL(LIB_PATH)
+        sig = {
+            "qf_version": ([], ctypes.c_int),
+            "qf_last_error": ([], ctypes.c_char_p),
+            "qf_amax": ([_P, _I, _I, _I, _P, ctypes.c_int, _P], ctypes.c_int),
+            "qf_fakequant_nvfp4": ([_P, _I, _I, _I, _P, ctypes.c_int, _P, _P, _P, _P, _P],
+                                   ctypes.c_int),
+            "qf_fakequant_mxfp4": ([_P, _I, _I, _I, _P, _P, _P, _P], ctypes.c_int),
+            "qf_fakequant_q4k": ([_P, _I, _I, _I, _P, _P, _P], ctypes.c_int),
+            "qf_workspace_size": ([ctypes.POINTER(QLinearDesc), ctypes.POINTER(ctypes.c_size_t)],
+                                  ctypes.c_int),
+            "qf_qlinear_fwd": ([ctypes.POINTER(QLinearDesc), _P, _P, _P, _P, ctypes.c_size_t, _P],
+                               ctypes.c_int),
+            "qf_qlinear_bwd_ste": ([ctypes.POINTER(QLinearDesc), _P, _P, _P, _P, _P, _P,
+                                    ctypes.c_size_t, _P], ctypes.c_int),
+            "qf_grouped_workspace_size": ([ctypes.POINTER(GroupedDesc),
+                                           ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
+            "qf_qlinear_grouped_fwd": ([ctypes.POINTER(GroupedDesc), _P, _P, _P, _P, _P,
+                                        ctypes.c_size_t, _P], ctypes.c_int),
+            "qf_qlinear_grouped_bwd_ste": ([ctypes.POINTER(GroupedDesc), _P, _P, _P, _P, _P, _P,
+                                            _P, ctypes.c_size_t, _P], ctypes.c_int),
+            "qf_gemm_bf16": ([_I, _I, _I, _P, _I, ctypes.c_int, _P, _I, ctypes.c_int, _P, _I,
+                              ctypes.c_int, _P], ctypes.c_int),
+        }
+        for name, (args, res) in sig.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = res
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != 0:
+        raise QFError(status, lib().qf_last_error().decode())
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("expected a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError("tensor must be on the GPU")
+    return t.data_ptr()
+
+
+def _stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _bf16(t):
+    if t is not None and t.element_size() != 2:
+        raise TypeError("bf16 operand must have 2-byte elements")
+    return t
+
+
+def _rows(x):
+    if x.dim() != 2:
+        raise ValueError("expected a 2-D tensor")
+    if x.stride(1) != 1:
+        raise ValueError("rows must be contiguous")
+    return x.shape[0], x.shape[1], x.stride(0)
+
+
+def version() -> int:
+    return lib().qf_version()
+
+
+# ----------------------------------------------------------------------------- quantizers
+def amax(x, out, accumulate: bool = False):
+    R, K, ld = _rows(_bf16(x))
+    _check(lib().qf_amax(_ptr(x), R, K, ld, _ptr(out), int(accumulate), _stream()))
+    return out
+
+
+def fakequant_nvfp4(x, amax, amax_mode=AMAX_COMPUTE, s_out=None, codes=None, scales=None,
+                    xhat=None):
+    R, K, ld = _rows(_bf16(x))
+    _check(lib().qf_fakequant_nvfp4(_ptr(x), R, K, ld, _ptr(amax), int(amax_mode), _ptr(s_out),
+                                    _ptr(codes), _ptr(scales), _ptr(xhat), _stream()))
+
+
+def fakequant_mxfp4(x, codes=None, scales=None, xhat=None):
+    R, K, ld = _rows(_bf16(x))
+    _check(lib().qf_fakequant_mxfp4(_ptr(x), R, K, ld, _ptr(codes), _ptr(scales), _ptr(xhat),
+                                    _stream()))
+
+
+def fakequant_q4k(x, packed=None, xhat=None):
+    R, K, ld = _rows(_bf16(x))
+    _check(lib().qf_fakequant_q4k(_ptr(x), R, K, ld, _ptr(packed), _ptr(xhat), _stream()))
+
+
+# --------------------------------------------------------------------------- linear layer
+def qlinear_desc(M, N, K, wfmt="nvfp4", afmt="none", w_amax=None, a_amax=None, flags=0,
+                 ldx=0, ldw=0, ldy=0) -> QLinearDesc:
+    return QLinearDesc(M, N, K, ldx, ldw, ldy, FMT[wfmt], FMT[afmt], _ptr(w_amax),
+                       _ptr(a_amax), flags)
+
+
+def workspace_size(desc: QLinearDesc) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().qf_workspace_size(ctypes.byref(desc), ctypes.byref(n)))
+    return n.value
+
+
+def workspace(desc: QLinearDesc, device="cuda"):
+    return torch.empty(max(workspace_size(desc), 256), dtype=torch.uint8, device=device)
+
+
+def qlinear_fwd(desc, X, W, Y, ws):
+    _check(lib().qf_qlinear_fwd(ctypes.byref(desc), _ptr(_bf16(X)), _ptr(_bf16(W)),
+                                _ptr(_bf16(Y)), _ptr(ws), ws.numel(), _stream()))
+    return Y
+
+
+def qlinear_bwd_ste(desc, dY, X, W, dX, dW, ws):
+    _check(lib().qf_qlinear_bwd_ste(ctypes.byref(desc), _ptr(_bf16(dY)), _ptr(_bf16(X)),
+                                    _ptr(_bf16(W)), _ptr(_bf16(dX)), _ptr(dW), _ptr(ws),
+                                    ws.numel(), _stream()))
+
+
+def grouped_desc(E, T, N, K, wfmt="nvfp4", afmt="none", w_amax=None, flags=0) -> GroupedDesc:
+    return GroupedDesc(E, T, N, K, FMT[wfmt], FMT[afmt], _ptr(w_amax), flags)
+
+
+def grouped_workspace(desc: GroupedDesc, device="cuda"):
+    n = ctypes.c_size_t()
+    _check(lib().qf_grouped_workspace_size(ctypes.byref(desc), ctypes.byref(n)))
+    return torch.empty(max(n.value, 256), dtype=torch.uint8, device=device)
+
+
+def qlinear_grouped_fwd(desc, offsets, X, W, Y, ws):
+    _check(lib().qf_qlinear_grouped_fwd(ctypes.byref(desc), _ptr(offsets), _ptr(_bf16(X)),
+                                        _ptr(_bf16(W)), _ptr(_bf16(Y)), _ptr(ws), ws.numel(),
+                                        _stream()))
+
+
+def qlinear_grouped_bwd_ste(desc, offsets, dY, X, W, dX, dW, ws):
+    _check(lib().qf_qlinear_grouped_bwd_ste(ctypes.byref(desc), _ptr(offsets), _ptr(_bf16(dY)),
+                                            _ptr(_bf16(X)), _ptr(_bf16(W)), _ptr(_bf16(dX)),
+                                            _ptr(dW), _ptr(ws), ws.numel(), _stream()))
+
+
+def gemm_bf16(M, N, K, A, lda, a_kmajor, B, ldb, b_kmajor, C, ldc, c_f32):
+    _check(lib().qf_gemm_bf16(M, N, K, _ptr(_bf16(A)), lda, int(a_kmajor), _ptr(_bf16(B)), ldb,
+                              int(b_kmajor), _ptr(C), ldc, int(c_f32), _stream()))
+    return C

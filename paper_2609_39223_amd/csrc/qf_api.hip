@@ -1,0 +1,466 @@
+// C ABI of libqf (declared in include/qf.h): host-side validation, workspace layout and the
+// launch sequence of each call.  No call allocates device memory or synchronizes; every
+// kernel goes on the caller's stream.
+#include <hip/hip_runtime.h>
+#include <stdarg.h>
+#include <stdint.h>
+#include <stdio.h>
+
+#include "qf.h"
+#include "qf_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+qf_status fail(qf_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+qf_status ok() {
+  g_err[0] = 0;
+  return QF_OK;
+}
+
+qf_status dev(hipError_t e, const char* what) {
+  if (e == hipSuccess) return QF_OK;
+  return fail(QF_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define QF_TRY(expr)                      \
+  do {                                    \
+    qf_status _st = (expr);               \
+    if (_st != QF_OK) return _st;         \
+  } while (0)
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// A 2-D bf16 operand: rows x cols with row stride ld (elements).
+qf_status check_mat(const char* name, const void* p, int64_t rows, int64_t cols, int64_t ld,
+                    bool required) {
+  if (rows < 0 || cols < 0) return fail(QF_ESHAPE, "%s: negative shape", name);
+  if (rows == 0 || cols == 0) return QF_OK;
+  if (!p) {
+    if (required) return fail(QF_EINVAL, "%s: null pointer", name);
+    return QF_OK;
+  }
+  if (ld < cols) return fail(QF_ESHAPE, "%s: row stride %lld < %lld columns", name,
+                             (long long)ld, (long long)cols);
+  if (!aligned16(p)) return fail(QF_EALIGN, "%s: pointer not 16-byte aligned", name);
+  if (ld % 8) return fail(QF_EALIGN, "%s: row stride %lld not a multiple of 8", name,
+                          (long long)ld);
+  return QF_OK;
+}
+
+qf_status check_out(const char* name, const void* p) {
+  if (p && !aligned16(p)) return fail(QF_EALIGN, "%s: pointer not 16-byte aligned", name);
+  return QF_OK;
+}
+
+qf_status check_quant_input(const char* fn, const uint16_t* x, int64_t R, int64_t K,
+                            int64_t ldx, int64_t block) {
+  if (R < 0 || K < 0) return fail(QF_ESHAPE, "%s: negative shape", fn);
+  if (K % block) return fail(QF_ESHAPE, "%s: K=%lld is not a multiple of the block size %lld",
+                             fn, (long long)K, (long long)block);
+  return check_mat(fn, x, R, K, ldx, true);
+}
+
+inline hipStream_t S(qf_stream_t s) { return reinterpret_cast<hipStream_t>(s); }
+
+constexpr size_t kAlign = 256;
+inline size_t up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+bool fmt_valid(int f) { return f >= QF_FMT_NONE && f <= QF_FMT_Q4K; }
+
+int64_t block_of(int f) {
+  switch (f) {
+    case QF_FMT_NVFP4: return 16;
+    case QF_FMT_MXFP4: return 32;
+    case QF_FMT_Q4K: return 256;
+    default: return 8;
+  }
+}
+
+// x_hat-only fake quantization of a [R, K] bf16 tensor into out (row stride K).
+// NVFP4: g_given (device) when non-null, else computed into g_scratch.
+qf_status fakequant_to(int fmt, const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
+                       const float* g_given, float* g_scratch, uint16_t* out, hipStream_t s) {
+  switch (fmt) {
+    case QF_FMT_NVFP4: {
+      const float* g = g_given;
+      if (!g) {
+        QF_TRY(dev(qf::launch_fill_f32(g_scratch, 1, 0.0f, s), "amax init"));
+        QF_TRY(dev(qf::launch_amax(x, R, K, ldx, g_scratch, s), "amax"));
+        g = g_scratch;
+      }
+      return dev(qf::launch_nvfp4(x, R, K, ldx, g, nullptr, nullptr, nullptr, out, s), "nvfp4");
+    }
+    case QF_FMT_MXFP4:
+      return dev(qf::launch_mxfp4(x, R, K, ldx, nullptr, nullptr, out, s), "mxfp4");
+    case QF_FMT_Q4K:
+      return dev(qf::launch_q4k(x, R, K, ldx, nullptr, out, s), "q4k");
+    default:
+      return fail(QF_EINVAL, "bad format %d", fmt);
+  }
+}
+
+struct LinearWs {
+  float* scal;      // [0]: weight amax scratch
+  uint16_t* what;   // [N, K] or null
+  uint16_t* ahat;   // [M, K] or null
+};
+
+size_t linear_ws_bytes(const qf_qlinear_desc* d) {
+  size_t b = kAlign;
+  if (d->wfmt != QF_FMT_NONE) b += up((size_t)d->N * d->K * 2);
+  if (d->afmt != QF_FMT_NONE) b += up((size_t)d->M * d->K * 2);
+  return b;
+}
+
+LinearWs linear_ws(const qf_qlinear_desc* d, void* ws) {
+  char* p = static_cast<char*>(ws);
+  LinearWs w{};
+  w.scal = reinterpret_cast<float*>(p);
+  p += kAlign;
+  if (d->wfmt != QF_FMT_NONE) {
+    w.what = reinterpret_cast<uint16_t*>(p);
+    p += up((size_t)d->N * d->K * 2);
+  }
+  if (d->afmt != QF_FMT_NONE) w.ahat = reinterpret_cast<uint16_t*>(p);
+  return w;
+}
+
+struct Dims {
+  int64_t ldx, ldw, ldy;
+};
+
+qf_status check_desc(const char* fn, const qf_qlinear_desc* d, Dims* dm) {
+  if (!d) return fail(QF_EINVAL, "%s: null descriptor", fn);
+  if (d->M < 0 || d->N < 0 || d->K < 0) return fail(QF_ESHAPE, "%s: negative shape", fn);
+  if (!fmt_valid(d->wfmt) || !fmt_valid(d->afmt))
+    return fail(QF_EINVAL, "%s: bad format (wfmt=%d afmt=%d)", fn, d->wfmt, d->afmt);
+  if (d->afmt == QF_FMT_Q4K)
+    return fail(QF_ENOTSUP, "%s: Q4_K is a weight-only format (W4A16)", fn);
+  if (d->afmt == QF_FMT_NVFP4 && !d->a_amax)
+    return fail(QF_EINVAL, "%s: NVFP4 activations need a_amax (the running amax)", fn);
+  const int64_t need = block_of(d->wfmt) > block_of(d->afmt) ? block_of(d->wfmt)
+                                                              : block_of(d->afmt);
+  if (d->K % need)
+    return fail(QF_ESHAPE, "%s: K=%lld is not a multiple of %lld", fn, (long long)d->K,
+                (long long)need);
+  if (d->N % 8) return fail(QF_ESHAPE, "%s: N=%lld is not a multiple of 8", fn, (long long)d->N);
+  dm->ldx = d->ldx ? d->ldx : d->K;
+  dm->ldw = d->ldw ? d->ldw : d->K;
+  dm->ldy = d->ldy ? d->ldy : d->N;
+  return QF_OK;
+}
+
+qf_status check_ws(const char* fn, size_t need, void* ws, size_t ws_bytes) {
+  if (ws_bytes < need)
+    return fail(QF_EINVAL, "%s: workspace %zu bytes < required %zu", fn, ws_bytes, need);
+  if (!ws) return fail(QF_EINVAL, "%s: null workspace", fn);
+  if ((uintptr_t)ws % kAlign) return fail(QF_EALIGN, "%s: workspace not 256-byte aligned", fn);
+  return QF_OK;
+}
+
+// Quantize W (and X when afmt != NONE) into the workspace; returns the GEMM operands.
+qf_status quantize_operands(const qf_qlinear_desc* d, const Dims& dm, const uint16_t* X,
+                            const uint16_t* W, const LinearWs& w, bool do_w, bool do_a,
+                            const uint16_t** Wop, int64_t* ldw_op, const uint16_t** Aop,
+                            int64_t* lda_op, hipStream_t s) {
+  *Wop = W; *ldw_op = dm.ldw;
+  *Aop = X; *lda_op = dm.ldx;
+  if (d->wfmt != QF_FMT_NONE) {
+    if (do_w) QF_TRY(fakequant_to(d->wfmt, W, d->N, d->K, dm.ldw, d->w_amax, w.scal, w.what, s));
+    *Wop = w.what; *ldw_op = d->K;
+  }
+  if (d->afmt != QF_FMT_NONE) {
+    if (do_a) QF_TRY(fakequant_to(d->afmt, X, d->M, d->K, dm.ldx, d->a_amax, nullptr, w.ahat, s));
+    *Aop = w.ahat; *lda_op = d->K;
+  }
+  return QF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int qf_version(void) { return 100; }
+
+const char* qf_last_error(void) { return g_err; }
+
+qf_status qf_amax(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, float* amax,
+                  int accumulate, qf_stream_t stream) {
+  QF_TRY(check_mat("qf_amax: x", x, R, K, ldx, true));
+  if (!amax) return fail(QF_EINVAL, "qf_amax: null amax");
+  if (accumulate != 0 && accumulate != 1) return fail(QF_EINVAL, "qf_amax: accumulate must be 0/1");
+  if (!accumulate) QF_TRY(dev(qf::launch_fill_f32(amax, 1, 0.0f, S(stream)), "amax init"));
+  QF_TRY(dev(qf::launch_amax(x, R, K, ldx, amax, S(stream)), "amax"));
+  return ok();
+}
+
+qf_status qf_fakequant_nvfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, float* amax,
+                             int amax_mode, float* s_out, uint8_t* codes, uint8_t* scales,
+                             uint16_t* xhat, qf_stream_t stream) {
+  QF_TRY(check_quant_input("qf_fakequant_nvfp4", x, R, K, ldx, 16));
+  if (!amax) return fail(QF_EINVAL, "qf_fakequant_nvfp4: null amax");
+  if (amax_mode != QF_AMAX_COMPUTE && amax_mode != QF_AMAX_GIVEN)
+    return fail(QF_EINVAL, "qf_fakequant_nvfp4: bad amax_mode %d", amax_mode);
+  if (s_out && s_out == amax) return fail(QF_EINVAL, "qf_fakequant_nvfp4: s_out aliases amax");
+  QF_TRY(check_out("qf_fakequant_nvfp4: codes", codes));
+  QF_TRY(check_out("qf_fakequant_nvfp4: scales", scales));
+  QF_TRY(check_out("qf_fakequant_nvfp4: xhat", xhat));
+  hipStream_t s = S(stream);
+  if (amax_mode == QF_AMAX_COMPUTE) {
+    QF_TRY(dev(qf::launch_fill_f32(amax, 1, 0.0f, s), "amax init"));
+    QF_TRY(dev(qf::launch_amax(x, R, K, ldx, amax, s), "amax"));
+  }
+  if (R == 0 || K == 0) {
+    if (s_out) QF_TRY(dev(qf::launch_fill_f32(s_out, 1, 0.0f, s), "S"));
+    return ok();
+  }
+  QF_TRY(dev(qf::launch_nvfp4(x, R, K, ldx, amax, s_out, codes, scales, xhat, s), "nvfp4"));
+  return ok();
+}
+
+qf_status qf_fakequant_mxfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
+                             uint8_t* codes, uint8_t* scales, uint16_t* xhat,
+                             qf_stream_t stream) {
+  QF_TRY(check_quant_input("qf_fakequant_mxfp4", x, R, K, ldx, 32));
+  QF_TRY(check_out("qf_fakequant_mxfp4: codes", codes));
+  QF_TRY(check_out("qf_fakequant_mxfp4: scales", scales));
+  QF_TRY(check_out("qf_fakequant_mxfp4: xhat", xhat));
+  QF_TRY(dev(qf::launch_mxfp4(x, R, K, ldx, codes, scales, xhat, S(stream)), "mxfp4"));
+  return ok();
+}
+
+qf_status qf_fakequant_q4k(const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
+                           uint8_t* packed, uint16_t* xhat, qf_stream_t stream) {
+  QF_TRY(check_quant_input("qf_fakequant_q4k", x, R, K, ldx, 256));
+  QF_TRY(check_out("qf_fakequant_q4k: packed", packed));
+  QF_TRY(check_out("qf_fakequant_q4k: xhat", xhat));
+  QF_TRY(dev(qf::launch_q4k(x, R, K, ldx, packed, xhat, S(stream)), "q4k"));
+  return ok();
+}
+
+qf_status qf_workspace_size(const qf_qlinear_desc* d, size_t* bytes) {
+  Dims dm;
+  QF_TRY(check_desc("qf_workspace_size", d, &dm));
+  if (!bytes) return fail(QF_EINVAL, "qf_workspace_size: null output");
+  *bytes = linear_ws_bytes(d);
+  return ok();
+}
+
+qf_status qf_qlinear_fwd(const qf_qlinear_desc* d, const uint16_t* X, const uint16_t* W,
+                         uint16_t* Y, void* ws, size_t ws_bytes, qf_stream_t stream) {
+  Dims dm;
+  QF_TRY(check_desc("qf_qlinear_fwd", d, &dm));
+  QF_TRY(check_mat("qf_qlinear_fwd: X", X, d->M, d->K, dm.ldx, true));
+  QF_TRY(check_mat("qf_qlinear_fwd: W", W, d->N, d->K, dm.ldw, true));
+  QF_TRY(check_mat("qf_qlinear_fwd: Y", Y, d->M, d->N, dm.ldy, true));
+  QF_TRY(check_ws("qf_qlinear_fwd", linear_ws_bytes(d), ws, ws_bytes));
+  hipStream_t s = S(stream);
+  LinearWs w = linear_ws(d, ws);
+  const uint16_t *Wop, *Aop;
+  int64_t ldw_op, lda_op;
+  QF_TRY(quantize_operands(d, dm, X, W, w, true, true, &Wop, &ldw_op, &Aop, &lda_op, s));
+  QF_TRY(dev(qf::launch_gemm(d->M, d->N, d->K, Aop, lda_op, 1, Wop, ldw_op, 1, Y, dm.ldy, 0, s),
+             "forward gemm"));
+  return ok();
+}
+
+qf_status qf_qlinear_bwd_ste(const qf_qlinear_desc* d, const uint16_t* dY, const uint16_t* X,
+                             const uint16_t* W, uint16_t* dX, float* dW, void* ws,
+                             size_t ws_bytes, qf_stream_t stream) {
+  Dims dm;
+  QF_TRY(check_desc("qf_qlinear_bwd_ste", d, &dm));
+  QF_TRY(check_mat("qf_qlinear_bwd_ste: dY", dY, d->M, d->N, dm.ldy, true));
+  QF_TRY(check_mat("qf_qlinear_bwd_ste: X", X, d->M, d->K, dm.ldx, dW != nullptr));
+  QF_TRY(check_mat("qf_qlinear_bwd_ste: W", W, d->N, d->K, dm.ldw, dX != nullptr));
+  QF_TRY(check_mat("qf_qlinear_bwd_ste: dX", dX, d->M, d->K, dm.ldx, false));
+  QF_TRY(check_out("qf_qlinear_bwd_ste: dW", dW));
+  QF_TRY(check_ws("qf_qlinear_bwd_ste", linear_ws_bytes(d), ws, ws_bytes));
+  hipStream_t s = S(stream);
+  LinearWs w = linear_ws(d, ws);
+  const bool reuse = (d->flags & QF_FLAG_REUSE_WS) != 0;
+  const uint16_t *Wop, *Aop;
+  int64_t ldw_op, lda_op;
+  QF_TRY(quantize_operands(d, dm, X, W, w, !reuse && dX != nullptr, !reuse && dW != nullptr,
+                           &Wop, &ldw_op, &Aop, &lda_op, s));
+  if (dX) {  // dX[M, K] = dY[M, N] W_hat[N, K]: contraction over N, W_hat is [K-out][N]-major
+    QF_TRY(dev(qf::launch_gemm(d->M, d->K, d->N, dY, dm.ldy, 1, Wop, ldw_op, 0, dX, dm.ldx, 0, s),
+               "dX gemm"));
+  }
+  if (dW) {  // dW[N, K] = dY^T A_hat: contraction over M, both operands stored [M][...]
+    QF_TRY(dev(qf::launch_gemm(d->N, d->K, d->M, dY, dm.ldy, 0, Aop, lda_op, 0, dW, d->K, 1, s),
+               "dW gemm"));
+  }
+  return ok();
+}
+
+// ------------------------------------------------------------------------------ grouped
+namespace {
+
+struct GroupedWs {
+  int* tile_start;  // [E+1]
+  int* order;       // [E]
+  float* wamax;     // [E]
+  uint16_t* what;   // [E, N, K]
+  uint16_t* ahat;   // [T, K]
+};
+
+size_t grouped_ws_bytes(const qf_grouped_desc* d) {
+  size_t b = up((size_t)(d->E + 1) * 4) + up((size_t)d->E * 4) + up((size_t)d->E * 4);
+  if (d->wfmt != QF_FMT_NONE) b += up((size_t)d->E * d->N * d->K * 2);
+  if (d->afmt != QF_FMT_NONE) b += up((size_t)d->T * d->K * 2);
+  return b;
+}
+
+GroupedWs grouped_ws(const qf_grouped_desc* d, void* ws) {
+  char* p = static_cast<char*>(ws);
+  GroupedWs g{};
+  g.tile_start = reinterpret_cast<int*>(p); p += up((size_t)(d->E + 1) * 4);
+  g.order = reinterpret_cast<int*>(p); p += up((size_t)d->E * 4);
+  g.wamax = reinterpret_cast<float*>(p); p += up((size_t)d->E * 4);
+  if (d->wfmt != QF_FMT_NONE) { g.what = reinterpret_cast<uint16_t*>(p); p += up((size_t)d->E * d->N * d->K * 2); }
+  if (d->afmt != QF_FMT_NONE) g.ahat = reinterpret_cast<uint16_t*>(p);
+  return g;
+}
+
+qf_status check_grouped(const char* fn, const qf_grouped_desc* d, const int64_t* off) {
+  if (!d) return fail(QF_EINVAL, "%s: null descriptor", fn);
+  if (d->E < 0 || d->T < 0 || d->N < 0 || d->K < 0) return fail(QF_ESHAPE, "%s: negative shape", fn);
+  if (d->E > 1024) return fail(QF_ENOTSUP, "%s: more than 1024 experts", fn);
+  if (!fmt_valid(d->wfmt) || !fmt_valid(d->afmt)) return fail(QF_EINVAL, "%s: bad format", fn);
+  if (d->afmt != QF_FMT_NONE && d->afmt != QF_FMT_MXFP4)
+    return fail(QF_ENOTSUP, "%s: grouped activations support NONE or MXFP4", fn);
+  const int64_t need = block_of(d->wfmt) > block_of(d->afmt) ? block_of(d->wfmt) : block_of(d->afmt);
+  if (d->K % need) return fail(QF_ESHAPE, "%s: K=%lld is not a multiple of %lld", fn, (long long)d->K, (long long)need);
+  if (d->N % 8) return fail(QF_ESHAPE, "%s: N not a multiple of 8", fn);
+  if (d->E > 0 && !off) return fail(QF_EINVAL, "%s: null group_offsets", fn);
+  return QF_OK;
+}
+
+qf_status grouped_quantize(const qf_grouped_desc* d, const uint16_t* X, const uint16_t* W,
+                           const GroupedWs& g, bool do_w, bool do_a, const uint16_t** Wop,
+                           const uint16_t** Aop, hipStream_t s) {
+  *Wop = W;
+  *Aop = X;
+  const int64_t R = d->N, K = d->K;
+  if (d->wfmt != QF_FMT_NONE) {
+    if (do_w) {
+      switch (d->wfmt) {
+        case QF_FMT_NVFP4: {
+          const float* gp = d->w_amax;
+          if (!gp) {
+            QF_TRY(dev(qf::launch_fill_f32(g.wamax, d->E, 0.0f, s), "amax init"));
+            QF_TRY(dev(qf::launch_amax_batched(W, d->E, R, K, g.wamax, s), "amax"));
+            gp = g.wamax;
+          }
+          QF_TRY(dev(qf::launch_nvfp4_batched(W, d->E, R, K, gp, g.what, s), "nvfp4"));
+          break;
+        }
+        case QF_FMT_MXFP4:
+          QF_TRY(dev(qf::launch_mxfp4(W, d->E * R, K, K, nullptr, nullptr, g.what, s), "mxfp4"));
+          break;
+        case QF_FMT_Q4K:
+          QF_TRY(dev(qf::launch_q4k(W, d->E * R, K, K, nullptr, g.what, s), "q4k"));
+          break;
+      }
+    }
+    *Wop = g.what;
+  }
+  if (d->afmt == QF_FMT_MXFP4) {
+    if (do_a) QF_TRY(dev(qf::launch_mxfp4(X, d->T, K, K, nullptr, nullptr, g.ahat, s), "mxfp4"));
+    *Aop = g.ahat;
+  }
+  return QF_OK;
+}
+
+}  // namespace
+
+qf_status qf_grouped_workspace_size(const qf_grouped_desc* d, size_t* bytes) {
+  QF_TRY(check_grouped("qf_grouped_workspace_size", d, (const int64_t*)1));
+  if (!bytes) return fail(QF_EINVAL, "qf_grouped_workspace_size: null output");
+  *bytes = grouped_ws_bytes(d);
+  return ok();
+}
+
+qf_status qf_qlinear_grouped_fwd(const qf_grouped_desc* d, const int64_t* group_offsets,
+                                 const uint16_t* X, const uint16_t* W, uint16_t* Y, void* ws,
+                                 size_t ws_bytes, qf_stream_t stream) {
+  QF_TRY(check_grouped("qf_qlinear_grouped_fwd", d, group_offsets));
+  QF_TRY(check_mat("qf_qlinear_grouped_fwd: X", X, d->T, d->K, d->K, true));
+  QF_TRY(check_mat("qf_qlinear_grouped_fwd: W", W, d->E * d->N, d->K, d->K, true));
+  QF_TRY(check_mat("qf_qlinear_grouped_fwd: Y", Y, d->T, d->N, d->N, true));
+  QF_TRY(check_ws("qf_qlinear_grouped_fwd", grouped_ws_bytes(d), ws, ws_bytes));
+  if (d->E == 0) return ok();
+  hipStream_t s = S(stream);
+  GroupedWs g = grouped_ws(d, ws);
+  const uint16_t *Wop, *Aop;
+  QF_TRY(grouped_quantize(d, X, W, g, true, true, &Wop, &Aop, s));
+  QF_TRY(dev(qf::launch_grouped_prep(group_offsets, d->E, g.tile_start, g.order, s), "prep"));
+  QF_TRY(dev(qf::launch_grouped_rows_ws(d->E, d->T, d->N, d->K, group_offsets, g.tile_start, Aop,
+                                        d->K, Wop, d->K, d->N * d->K, 1, Y, d->N, s),
+             "grouped forward"));
+  return ok();
+}
+
+qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int64_t* group_offsets,
+                                     const uint16_t* dY, const uint16_t* X, const uint16_t* W,
+                                     uint16_t* dX, float* dW, void* ws, size_t ws_bytes,
+                                     qf_stream_t stream) {
+  QF_TRY(check_grouped("qf_qlinear_grouped_bwd_ste", d, group_offsets));
+  QF_TRY(check_mat("qf_qlinear_grouped_bwd_ste: dY", dY, d->T, d->N, d->N, true));
+  QF_TRY(check_mat("qf_qlinear_grouped_bwd_ste: X", X, d->T, d->K, d->K, dW != nullptr));
+  QF_TRY(check_mat("qf_qlinear_grouped_bwd_ste: W", W, d->E * d->N, d->K, d->K, dX != nullptr));
+  QF_TRY(check_mat("qf_qlinear_grouped_bwd_ste: dX", dX, d->T, d->K, d->K, false));
+  QF_TRY(check_out("qf_qlinear_grouped_bwd_ste: dW", dW));
+  QF_TRY(check_ws("qf_qlinear_grouped_bwd_ste", grouped_ws_bytes(d), ws, ws_bytes));
+  if (d->E == 0) return ok();
+  hipStream_t s = S(stream);
+  GroupedWs g = grouped_ws(d, ws);
+  const bool reuse = (d->flags & QF_FLAG_REUSE_WS) != 0;
+  const uint16_t *Wop, *Aop;
+  QF_TRY(grouped_quantize(d, X, W, g, !reuse && dX, !reuse && dW, &Wop, &Aop, s));
+  QF_TRY(dev(qf::launch_grouped_prep(group_offsets, d->E, g.tile_start, g.order, s), "prep"));
+  if (dX) {
+    QF_TRY(dev(qf::launch_grouped_rows_ws(d->E, d->T, d->K, d->N, group_offsets, g.tile_start, dY,
+                                          d->N, Wop, d->K, d->N * d->K, 0, dX, d->K, s),
+               "grouped dX"));
+  }
+  if (dW) {
+    QF_TRY(dev(qf::launch_grouped_wgrad_ws(d->E, d->T, d->N, d->K, group_offsets, g.order, dY,
+                                           d->N, Aop, d->K, dW, s),
+               "grouped dW"));
+  }
+  return ok();
+}
+
+qf_status qf_gemm_bf16(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
+                       int a_kmajor, const uint16_t* B, int64_t ldb, int b_kmajor, void* C,
+                       int64_t ldc, int c_f32, qf_stream_t stream) {
+  if (M < 0 || N < 0 || K < 0) return fail(QF_ESHAPE, "qf_gemm_bf16: negative shape");
+  if ((a_kmajor | b_kmajor | c_f32) & ~1) return fail(QF_EINVAL, "qf_gemm_bf16: flags must be 0/1");
+  if (a_kmajor ? false : (M % 8 != 0)) return fail(QF_ESHAPE, "qf_gemm_bf16: M must be a multiple of 8 for [K][M] A");
+  if (b_kmajor ? false : (N % 8 != 0)) return fail(QF_ESHAPE, "qf_gemm_bf16: N must be a multiple of 8 for [K][N] B");
+  if ((a_kmajor || b_kmajor) && K % 8) return fail(QF_ESHAPE, "qf_gemm_bf16: K must be a multiple of 8");
+  QF_TRY(a_kmajor ? check_mat("qf_gemm_bf16: A", A, M, K, lda, true)
+                  : check_mat("qf_gemm_bf16: A", A, K, M, lda, true));
+  QF_TRY(b_kmajor ? check_mat("qf_gemm_bf16: B", B, N, K, ldb, true)
+                  : check_mat("qf_gemm_bf16: B", B, K, N, ldb, true));
+  if (M > 0 && N > 0) {
+    if (!C) return fail(QF_EINVAL, "qf_gemm_bf16: null C");
+    if (ldc < N) return fail(QF_ESHAPE, "qf_gemm_bf16: ldc < N");
+    if (!aligned16(C)) return fail(QF_EALIGN, "qf_gemm_bf16: C not 16-byte aligned");
+  }
+  QF_TRY(dev(qf::launch_gemm(M, N, K, A, lda, a_kmajor, B, ldb, b_kmajor, C, ldc, c_f32, S(stream)),
+             "gemm"));
+  return ok();
+}
+
+}  // extern "C"

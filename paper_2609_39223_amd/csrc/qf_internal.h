@@ -1,0 +1,53 @@
+// Internal launch interface shared by the C ABI (qf_api.hip) and the kernel files.
+// Host-side validation happens in qf_api.hip; the launchers below assume valid arguments.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace qf {
+
+// ---- quantizers (qf_quant.hip) ----------------------------------------------------------
+// Writes v to p[0..n) with a kernel (no memset nodes, so callers may capture it in a graph).
+hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s);
+hipError_t launch_amax(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, float* amax,
+                       hipStream_t s);
+// g: device scalar holding the tensor amax to use; s_out may be null.
+hipError_t launch_nvfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, const float* g,
+                        float* s_out, uint8_t* codes, uint8_t* scales, uint16_t* xhat,
+                        hipStream_t s);
+hipError_t launch_mxfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, uint8_t* codes,
+                        uint8_t* scales, uint16_t* xhat, hipStream_t s);
+hipError_t launch_q4k(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, uint8_t* packed,
+                      uint16_t* xhat, hipStream_t s);
+
+// Batched variants over E equally shaped tensors (expert weights), one tensor scale each.
+hipError_t launch_amax_batched(const uint16_t* x, int64_t E, int64_t R, int64_t K,
+                               float* amax, hipStream_t s);
+hipError_t launch_nvfp4_batched(const uint16_t* x, int64_t E, int64_t R, int64_t K,
+                                const float* g, uint16_t* xhat, hipStream_t s);
+
+// ---- GEMMs (qf_gemm.hip) ------------------------------------------------------------------
+// C[M,N] = sum_k A(m,k) B(n,k).  a_kmajor: A stored [M][K] (else [K][M]); likewise B.
+hipError_t launch_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
+                       int a_kmajor, const uint16_t* B, int64_t ldb, int b_kmajor, void* C,
+                       int64_t ldc, int c_f32, hipStream_t s);
+
+// Grouped over experts (rows [off[e], off[e+1]) of the token-major operands belong to
+// expert e; the host never reads off).  launch_grouped_prep fills two small device arrays:
+// tile_start[E+1] (prefix of per-expert 256-row tile counts) and order[E] (experts by
+// decreasing row count).
+hipError_t launch_grouped_prep(const int64_t* off, int64_t E, int* tile_start, int* order,
+                               hipStream_t s);
+// Forward / dX shape: C[t, n] = sum_k A[t, k] B_e(n, k) for t in expert e's rows.
+// b_kmajor: B_e stored [N][K] (forward) or [K][N] (dX); bstride = elements per expert.
+hipError_t launch_grouped_rows_ws(int64_t E, int64_t T, int64_t N, int64_t K, const int64_t* off,
+                                  const int* tile_start, const uint16_t* A, int64_t lda,
+                                  const uint16_t* B, int64_t ldb, int64_t bstride, int b_kmajor,
+                                  uint16_t* C, int64_t ldc, hipStream_t s);
+// dW shape: C_e[n, k] = sum over expert e's rows t of dY[t, n] X[t, k]  (FP32, [E][N][K]).
+hipError_t launch_grouped_wgrad_ws(int64_t E, int64_t T, int64_t N, int64_t K, const int64_t* off,
+                                   const int* order, const uint16_t* dY, int64_t ldy,
+                                   const uint16_t* X, int64_t ldx, float* C, hipStream_t s);
+
+}  // namespace qf

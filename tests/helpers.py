@@ -66,3 +66,25 @@ def unpack_nibbles(codes, K):
     out[:, 0::2] = codes & 15
     out[:, 1::2] = codes >> 4
     return out
+
+
+# ------------------------------------------------------------------ GPU marshalling helpers
+def to_dev(a, dev="cuda"):
+    """Upload a numpy array (raw bits for bf16) to the GPU without changing its bytes."""
+    import torch
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    return torch.from_numpy(a).to(dev)
+
+
+def from_dev(t, dtype=None):
+    arr = t.detach().cpu().numpy()
+    if arr.dtype == np.int16:
+        arr = arr.view(np.uint16)
+    return arr if dtype is None else arr.astype(dtype)
+
+
+def empty_bf16(shape, dev="cuda"):
+    import torch
+    return torch.empty(shape, dtype=torch.int16, device=dev)

@@ -1,0 +1,105 @@
+"""Host-only checks of the C ABI library: it loads, exports every symbol include/qf.h
+declares, and rejects invalid arguments before touching the GPU (no kernel is launched
+by any call here: each one fails host validation)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "qf.h")
+LIB = os.path.join(ROOT, "paper_2609_39223_amd", "libqf.so")
+
+QF_OK, QF_EINVAL, QF_ESHAPE, QF_EALIGN, QF_ENOTSUP = 0, 1, 2, 3, 4
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"QF_API\s+[\w\s\*]*?\b(qf_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(LIB):
+        pytest.skip("libqf.so not built (run __graft_entry__.build())")
+    import torch  # noqa: F401  (same HIP runtime as the GPU path)
+    lib = ctypes.CDLL(LIB)
+    lib.qf_last_error.restype = ctypes.c_char_p
+    return lib
+
+
+def test_header_declares_the_boundary():
+    syms = declared_symbols()
+    for s in ["qf_fakequant_nvfp4", "qf_fakequant_mxfp4", "qf_fakequant_q4k", "qf_amax",
+              "qf_qlinear_fwd", "qf_qlinear_bwd_ste", "qf_qlinear_grouped_fwd",
+              "qf_qlinear_grouped_bwd_ste", "qf_workspace_size", "qf_last_error", "qf_version"]:
+        assert s in syms
+
+
+def test_library_exports_every_declared_symbol(L):
+    for s in declared_symbols():
+        assert hasattr(L, s), s
+    assert L.qf_version() >= 100
+
+
+I64 = ctypes.c_int64
+P = ctypes.c_void_p
+
+
+def test_quantizer_validation(L):
+    f = L.qf_fakequant_mxfp4
+    assert f(P(256), I64(4), I64(40), I64(40), None, None, None, None) == QF_ESHAPE
+    assert b"multiple" in L.qf_last_error()
+    assert f(None, I64(4), I64(64), I64(64), None, None, None, None) == QF_EINVAL
+    assert f(P(258), I64(4), I64(64), I64(64), None, None, None, None) == QF_EALIGN
+    assert f(P(256), I64(4), I64(64), I64(60), None, None, None, None) == QF_ESHAPE
+    assert f(P(256), I64(4), I64(64), I64(68), None, None, None, None) == QF_EALIGN
+    assert f(P(256), I64(-1), I64(64), I64(64), None, None, None, None) == QF_ESHAPE
+    g = L.qf_fakequant_nvfp4
+    assert g(P(256), I64(4), I64(24), I64(24), P(512), 0, None, None, None, None, None) == QF_ESHAPE
+    assert g(P(256), I64(4), I64(32), I64(32), None, 0, None, None, None, None, None) == QF_EINVAL
+    assert g(P(256), I64(4), I64(32), I64(32), P(512), 7, None, None, None, None, None) == QF_EINVAL
+    assert g(P(256), I64(4), I64(32), I64(32), P(512), 0, P(512), None, None, None, None) == QF_EINVAL
+    h = L.qf_fakequant_q4k
+    assert h(P(256), I64(4), I64(128), I64(128), None, None, None) == QF_ESHAPE
+    assert h(P(256), I64(4), I64(256), I64(256), P(7), None, None) == QF_EALIGN
+
+
+class Desc(ctypes.Structure):
+    _fields_ = [("M", ctypes.c_int64), ("N", ctypes.c_int64), ("K", ctypes.c_int64),
+                ("ldx", ctypes.c_int64), ("ldw", ctypes.c_int64), ("ldy", ctypes.c_int64),
+                ("wfmt", ctypes.c_int32), ("afmt", ctypes.c_int32),
+                ("w_amax", ctypes.c_void_p), ("a_amax", ctypes.c_void_p),
+                ("flags", ctypes.c_uint32)]
+
+
+def test_workspace_size_and_desc_validation(L):
+    n = ctypes.c_size_t()
+    d = Desc(256, 512, 512, 0, 0, 0, 1, 0, None, None, 0)
+    assert L.qf_workspace_size(ctypes.byref(d), ctypes.byref(n)) == QF_OK
+    assert n.value >= 512 * 512 * 2
+    d2 = Desc(256, 512, 512, 0, 0, 0, 2, 2, None, None, 0)
+    assert L.qf_workspace_size(ctypes.byref(d2), ctypes.byref(n)) == QF_OK
+    assert n.value >= (512 + 256) * 512 * 2
+    bad = [Desc(256, 512, 500, 0, 0, 0, 1, 0, None, None, 0),   # K % 16
+           Desc(256, 512, 512, 0, 0, 0, 3, 3, None, None, 0),   # Q4_K activations
+           Desc(256, 512, 512, 0, 0, 0, 1, 1, None, None, 0),   # NVFP4 act without a_amax
+           Desc(256, 512, 512, 0, 0, 0, 9, 0, None, None, 0),   # bad enum
+           Desc(-1, 512, 512, 0, 0, 0, 1, 0, None, None, 0)]
+    want = [QF_ESHAPE, QF_ENOTSUP, QF_EINVAL, QF_EINVAL, QF_ESHAPE]
+    for dd, w in zip(bad, want):
+        assert L.qf_workspace_size(ctypes.byref(dd), ctypes.byref(n)) == w
+    # too-small workspace is rejected before any launch
+    assert L.qf_qlinear_fwd(ctypes.byref(d), P(256), P(256), P(256), P(256), ctypes.c_size_t(16),
+                            None) == QF_EINVAL
+    assert b"workspace" in L.qf_last_error()
+
+
+def test_gemm_validation(L):
+    f = L.qf_gemm_bf16
+    args = lambda M, N, K, lda, ak, ldb, bk: f(I64(M), I64(N), I64(K), P(256), I64(lda), ak, P(256),
+                                               I64(ldb), bk, P(256), I64(N), 0, None)
+    assert args(64, 64, 60, 60, 1, 60, 1) == QF_ESHAPE      # K % 8 for k-major operands
+    assert args(60, 64, 64, 64, 0, 64, 1) == QF_ESHAPE      # M % 8 for [K][M] A
+    assert args(64, 64, 64, 32, 1, 64, 1) == QF_ESHAPE      # lda < K

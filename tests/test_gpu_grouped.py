@@ -1,0 +1,79 @@
+"""GPU parity of the grouped (mixture-of-experts) layer: per-expert fake quantization and
+grouped GEMMs over device-resident row offsets equal looping the dense layer per expert."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from tests.helpers import assert_close, bf16_to_f64, empty_bf16, from_dev, to_dev
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def qf():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_39223_amd as qf
+    qf.lib()
+    return qf
+
+
+def run_grouped(qf, offsets, X, W, dY, wfmt, afmt):
+    E, N, K = W.shape
+    T = X.shape[0]
+    d = qf.grouped_desc(E, T, N, K, wfmt, afmt)
+    ws = qf.grouped_workspace(d)
+    off = torch.from_numpy(offsets.astype(np.int64)).cuda()
+    Xd, Wd, dYd = to_dev(X), to_dev(W.reshape(E * N, K)), to_dev(dY)
+    Y, dX = empty_bf16((T, N)), empty_bf16((T, K))
+    dW = torch.full((E, N, K), 7.0, dtype=torch.float32, device="cuda")
+    qf.qlinear_grouped_fwd(d, off, Xd, Wd, Y, ws)
+    qf.qlinear_grouped_bwd_ste(d, off, dYd, Xd, Wd, dX, dW, ws)
+    torch.cuda.synchronize()
+    return from_dev(Y), from_dev(dX), from_dev(dW)
+
+
+@pytest.mark.parametrize("wfmt,afmt", [("nvfp4", "none"), ("mxfp4", "mxfp4"), ("q4k", "none")])
+def test_grouped_matches_per_expert_loop(qf, wfmt, afmt):
+    rng = np.random.default_rng(0)
+    E, N, K = 6, 264, 512
+    counts = np.array([0, 300, 1, 513, 0, 77])          # empty, ragged, single-row experts
+    offsets = np.concatenate([[0], np.cumsum(counts)])
+    T = int(offsets[-1])
+    X = workloads.normal_bf16(rng, (T, K))
+    W = np.stack([workloads.normal_bf16(rng, (N, K), 0.02 * (e + 1)) for e in range(E)])
+    dY = workloads.normal_bf16(rng, (T, N))
+    Y, dX, dW = run_grouped(qf, offsets, X, W, dY, wfmt, afmt)
+    ahat = oracle.fakequant(X, afmt)
+    for e in range(E):
+        r0, r1 = offsets[e], offsets[e + 1]
+        what = oracle.fakequant(W[e], wfmt)              # one tensor scale per expert
+        if r1 > r0:
+            assert_close(bf16_to_f64(Y[r0:r1]), oracle.linear_fwd(ahat[r0:r1], what), f"Y e={e}")
+            assert_close(bf16_to_f64(dX[r0:r1]), oracle.linear_dx(dY[r0:r1], what), f"dX e={e}")
+            assert_close(dW[e].astype(np.float64), oracle.linear_dw(dY[r0:r1], ahat[r0:r1]),
+                         f"dW e={e}")
+        else:
+            assert np.all(dW[e] == 0.0)
+
+
+def test_grouped_zipf_routing_sampled(qf):
+    """128 experts, top-8 Zipf(1.1) routing (reduced token count and width), sampled."""
+    tok, offsets = workloads.moe_routing(seed=0, tokens=2048, experts=128, topk=8)
+    rng = np.random.default_rng(1)
+    E, N, K = 128, 384, 256
+    T = int(offsets[-1])
+    Xtok = workloads.normal_bf16(rng, (2048, K))
+    X = Xtok[tok]
+    W = workloads.normal_bf16(rng, (E * N, K), 0.02).reshape(E, N, K)
+    dY = workloads.normal_bf16(rng, (T, N))
+    Y, dX, dW = run_grouped(qf, offsets, X, W, dY, "nvfp4", "none")
+    for e in [0, 1, 5, 64, 127]:
+        r0, r1 = offsets[e], offsets[e + 1]
+        what = oracle.nvfp4(W[e])["xhat"]
+        assert_close(bf16_to_f64(Y[r0:r1]), oracle.linear_fwd(X[r0:r1], what), f"Y e={e}")
+        assert_close(bf16_to_f64(dX[r0:r1]), oracle.linear_dx(dY[r0:r1], what), f"dX e={e}")
+        assert_close(dW[e].astype(np.float64), oracle.linear_dw(dY[r0:r1], X[r0:r1]), f"dW e={e}")

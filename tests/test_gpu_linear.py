@@ -1,0 +1,196 @@
+"""GPU parity of the MFMA GEMMs and the quantization-aware linear layer (forward +
+straight-through backward) against the FP64 oracle on the same fake-quantized operands.
+
+Tolerance (FP32 accumulation, bf16 outputs): per entry |y - r| / max(|r|, 1e-3 rms(r)),
+max <= 2e-2 and mean <= 2e-3 (bf16 output rounding alone gives max 2^-9 ~ 1.95e-3).
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from tests.helpers import assert_close, bf16_to_f64, empty_bf16, from_dev, to_dev
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def qf():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_39223_amd as qf
+    qf.lib()
+    return qf
+
+
+def _rand_bf16(rng, shape, std=1.0):
+    return workloads.normal_bf16(rng, shape, std)
+
+
+# ---------------------------------------------------------------------------- plain GEMMs
+@pytest.mark.parametrize("a_km,b_km,c32", [(1, 1, 0), (1, 0, 0), (0, 0, 1), (1, 1, 1),
+                                           (0, 1, 0), (0, 0, 0), (1, 0, 1), (0, 1, 1)])
+@pytest.mark.parametrize("M,N,K", [(256, 256, 64), (300, 264, 136), (8, 520, 1000),
+                                   (513, 8, 72), (1, 16, 8)])
+def test_gemm_layouts_ragged(qf, a_km, b_km, c32, M, N, K):
+    if (not a_km and M % 8) or (not b_km and N % 8):
+        pytest.skip("mn-major operands need a multiple of 8 along the contiguous axis")
+    rng = np.random.default_rng(M * 7 + N * 3 + K)
+    A = _rand_bf16(rng, (M, K))              # logical A(m, k)
+    B = _rand_bf16(rng, (N, K))              # logical B(n, k)
+    As = A if a_km else np.ascontiguousarray(A.T)
+    Bs = B if b_km else np.ascontiguousarray(B.T)
+    C = torch.empty(M, N, dtype=torch.float32 if c32 else torch.int16, device="cuda")
+    qf.gemm_bf16(M, N, K, to_dev(As), As.shape[1], a_km, to_dev(Bs), Bs.shape[1], b_km, C, N, c32)
+    torch.cuda.synchronize()
+    got = from_dev(C).astype(np.float64) if c32 else bf16_to_f64(from_dev(C))
+    assert_close(got, oracle.linear_fwd(A, B), f"gemm a_km={a_km} b_km={b_km}")
+
+
+def test_gemm_zero_depth_writes_zeros(qf):
+    C = torch.full((64, 64), 7.0, dtype=torch.float32, device="cuda")
+    A = torch.zeros(64, 8, dtype=torch.int16, device="cuda")
+    qf.gemm_bf16(64, 64, 0, A, 8, 1, A, 8, 1, C, 64, 1)
+    torch.cuda.synchronize()
+    assert float(C.abs().max().item()) == 0.0
+
+
+def test_gemm_strided_output_leaves_padding(qf):
+    rng = np.random.default_rng(11)
+    M, N, K, ldc = 200, 136, 96, 152
+    A, B = _rand_bf16(rng, (M, K)), _rand_bf16(rng, (N, K))
+    C = torch.full((M, ldc), -3.0, dtype=torch.float32, device="cuda")
+    qf.gemm_bf16(M, N, K, to_dev(A), K, 1, to_dev(B), K, 1, C, ldc, 1)
+    torch.cuda.synchronize()
+    c = from_dev(C)
+    assert np.all(c[:, N:] == -3.0)
+    assert_close(c[:, :N], oracle.linear_fwd(A, B), "strided C")
+
+
+# --------------------------------------------------------------------------- linear layer
+def _layer(qf, w, wfmt, afmt, flags=0, w_amax=None, a_amax=None, reuse=False):
+    M, N, K = w["X"].shape[0], w["W"].shape[0], w["W"].shape[1]
+    X, W, dY = to_dev(w["X"]), to_dev(w["W"]), to_dev(w["dY"])
+    d = qf.qlinear_desc(M, N, K, wfmt, afmt, w_amax=w_amax, a_amax=a_amax, flags=0)
+    ws = qf.workspace(d)
+    Y, dX = empty_bf16((M, N)), empty_bf16((M, K))
+    dW = torch.empty(N, K, dtype=torch.float32, device="cuda")
+    qf.qlinear_fwd(d, X, W, Y, ws)
+    if reuse:
+        d = qf.qlinear_desc(M, N, K, wfmt, afmt, w_amax=w_amax, a_amax=a_amax,
+                            flags=qf.FLAG_REUSE_WS)
+    qf.qlinear_bwd_ste(d, dY, X, W, dX, dW, ws)
+    torch.cuda.synchronize()
+    return from_dev(Y), from_dev(dX), from_dev(dW)
+
+
+def test_single_linear_nvfp4_full(qf):
+    w = workloads.single_linear(seed=0)
+    Y, dX, dW = _layer(qf, w, "nvfp4", "none")
+    what = oracle.nvfp4(w["W"])["xhat"]
+    assert_close(bf16_to_f64(Y), oracle.linear_fwd(w["X"], what), "Y")
+    assert_close(bf16_to_f64(dX), oracle.linear_dx(w["dY"], what), "dX")
+    assert_close(dW.astype(np.float64), oracle.linear_dw(w["dY"], w["X"]), "dW")
+    # saving the quantized operands for the backward gives the same bits as re-quantizing
+    Y2, dX2, dW2 = _layer(qf, w, "nvfp4", "none", reuse=True)
+    assert np.array_equal(Y, Y2) and np.array_equal(dX, dX2) and np.array_equal(dW, dW2)
+
+
+@pytest.mark.parametrize("wfmt,afmt", [("mxfp4", "mxfp4"), ("q4k", "none"), ("none", "none"),
+                                       ("nvfp4", "mxfp4"), ("mxfp4", "none")])
+def test_linear_formats_small(qf, wfmt, afmt):
+    rng = np.random.default_rng(5)
+    M, N, K = 384, 264, 512
+    w = {"X": _rand_bf16(rng, (M, K)), "W": _rand_bf16(rng, (N, K), 0.02),
+         "dY": _rand_bf16(rng, (M, N))}
+    Y, dX, dW = _layer(qf, w, wfmt, afmt)
+    what = oracle.fakequant(w["W"], wfmt)
+    ahat = oracle.fakequant(w["X"], afmt)
+    assert_close(bf16_to_f64(Y), oracle.linear_fwd(ahat, what), "Y")
+    assert_close(bf16_to_f64(dX), oracle.linear_dx(w["dY"], what), "dX")
+    assert_close(dW.astype(np.float64), oracle.linear_dw(w["dY"], ahat), "dW")
+
+
+def test_nvfp4_activations_with_running_amax(qf):
+    rng = np.random.default_rng(6)
+    M, N, K = 256, 256, 256
+    w = {"X": _rand_bf16(rng, (M, K)), "W": _rand_bf16(rng, (N, K), 0.02),
+         "dY": _rand_bf16(rng, (M, N))}
+    run = float(np.float32(1.25 * oracle.amax(w["X"])))      # running amax above this batch
+    a_amax = torch.tensor([run], dtype=torch.float32, device="cuda")
+    Y, dX, dW = _layer(qf, w, "nvfp4", "nvfp4", a_amax=a_amax)
+    what = oracle.nvfp4(w["W"])["xhat"]
+    ahat = oracle.nvfp4(w["X"], amax_in=run)["xhat"]
+    assert_close(bf16_to_f64(Y), oracle.linear_fwd(ahat, what), "Y")
+    assert_close(dW.astype(np.float64), oracle.linear_dw(w["dY"], ahat), "dW")
+
+
+def test_tied_qkv_scale(qf):
+    # Engine-specific scale sharing: one tensor scale for the fused Q, K, V weights, built
+    # with qf_amax(accumulate) over the members and passed as w_amax.
+    rng = np.random.default_rng(7)
+    K = 512
+    parts = [_rand_bf16(rng, (n, K), s) for n, s in ((512, 0.02), (128, 0.05), (128, 0.01))]
+    Wqkv = np.concatenate(parts)
+    g = torch.zeros(1, dtype=torch.float32, device="cuda")
+    for i, p in enumerate(parts):
+        qf.amax(to_dev(p), g, accumulate=i > 0)
+    torch.cuda.synchronize()
+    gval = float(g.item())
+    assert gval == max(oracle.amax(p) for p in parts)
+    w = {"X": _rand_bf16(rng, (256, K)), "W": Wqkv, "dY": _rand_bf16(rng, (256, Wqkv.shape[0]))}
+    Y, dX, dW = _layer(qf, w, "nvfp4", "none", w_amax=g)
+    what = oracle.nvfp4(Wqkv, amax_in=gval)["xhat"]
+    assert_close(bf16_to_f64(Y), oracle.linear_fwd(w["X"], what), "Y")
+
+
+def test_activation_gradient_decomposition_on_gpu(qf):
+    # dW(W4A4) - dW(W4A16) = dO eps_A^T (Eq. activation-gradient-error), to FP32 accuracy
+    rng = np.random.default_rng(8)
+    M, N, K = 512, 256, 256
+    w = {"X": _rand_bf16(rng, (M, K)), "W": _rand_bf16(rng, (N, K), 0.02),
+         "dY": _rand_bf16(rng, (M, N))}
+    _, _, dW44 = _layer(qf, w, "mxfp4", "mxfp4")
+    _, _, dW416 = _layer(qf, w, "mxfp4", "none")
+    eps = bf16_to_f64(oracle.mxfp4(w["X"])["xhat"]) - bf16_to_f64(w["X"])
+    want = bf16_to_f64(w["dY"]).T @ eps
+    scale = np.abs(bf16_to_f64(w["dY"])).T @ np.abs(bf16_to_f64(w["X"]))
+    assert np.all(np.abs((dW44.astype(np.float64) - dW416) - want) <= 1e-5 * scale + 1e-6)
+
+
+def test_mlp_up_mxfp4_full_size_sampled(qf):
+    """The benchmarked workload (8192 x 14336 x 4096, MXFP4 weights and activations) in the
+    launch configuration the benchmark times, checked on sampled entries + whole rows."""
+    w = workloads.mlp_up(seed=0)
+    M, N, K = w["M"], w["N"], w["K"]
+    Y, dX, dW = _layer(qf, w, "mxfp4", "mxfp4")
+    xq = oracle.mxfp4(w["X"])["xhat"]
+    wq = oracle.mxfp4(w["W"])["xhat"]
+    rng = np.random.default_rng(9)
+    n = 1 << 14
+    # Y[i, j] = sum_k xq[i, k] wq[j, k]
+    i, j = rng.integers(0, M, n), rng.integers(0, N, n)
+    assert_close(bf16_to_f64(Y[i, j]), oracle.dot_rows(xq, i, wq, j), "Y sampled")
+    r = rng.integers(0, M, 2)
+    assert_close(bf16_to_f64(Y[r]), oracle.linear_fwd(xq[r], wq), "Y rows")
+    # dX[i, k] = sum_n dY[i, n] wq[n, k]
+    wqT = np.ascontiguousarray(wq.T)
+    i, k = rng.integers(0, M, n), rng.integers(0, K, n)
+    assert_close(bf16_to_f64(dX[i, k]), oracle.dot_rows(w["dY"], i, wqT, k), "dX sampled")
+    # dW[j, k] = sum_m dY[m, j] xq[m, k]
+    dYT = np.ascontiguousarray(w["dY"].T)
+    xqT = np.ascontiguousarray(xq.T)
+    j, k = rng.integers(0, N, n // 4), rng.integers(0, K, n // 4)
+    assert_close(dW[j, k].astype(np.float64), oracle.dot_rows(dYT, j, xqT, k), "dW sampled")
+
+
+def test_linear_determinism(qf):
+    rng = np.random.default_rng(10)
+    w = {"X": _rand_bf16(rng, (512, 1024)), "W": _rand_bf16(rng, (768, 1024), 0.02),
+         "dY": _rand_bf16(rng, (512, 768))}
+    a = _layer(qf, w, "nvfp4", "none")
+    b = _layer(qf, w, "nvfp4", "none")
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)

@@ -1,0 +1,218 @@
+"""GPU parity of the fake-quantization kernels against the CPU oracle: bit-exact codes,
+scales, tensor scale and dequantized bf16 on seeded inputs (LLM-shaped tensors at full size,
+wide-range and edge-case tensors, exhaustive bf16 inputs, ragged rows / strides)."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from tests.helpers import empty_bf16, from_dev, to_dev, wide_range_bf16
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def qf():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_39223_amd as qf
+    qf.lib()
+    return qf
+
+
+def _strided(x, ld):
+    """Embed [R, K] into an [R, ld] buffer (row stride ld) and return (buffer view, base)."""
+    R, K = x.shape
+    buf = np.full((R, ld), 0x7FC0, np.uint16)   # NaN padding: must never be read
+    buf[:, :K] = x
+    return buf
+
+
+def run_mxfp4(qf, x, ld=None):
+    R, K = x.shape
+    if ld is None:
+        xd = to_dev(x)
+    else:
+        xd = to_dev(_strided(x, ld))[:, :K]
+    codes = torch.empty(R, K // 2, dtype=torch.uint8, device="cuda")
+    scales = torch.empty(R, K // 32, dtype=torch.uint8, device="cuda")
+    xhat = empty_bf16((R, K))
+    qf.fakequant_mxfp4(xd, codes, scales, xhat)
+    torch.cuda.synchronize()
+    return {"codes": from_dev(codes), "scales": from_dev(scales), "xhat": from_dev(xhat)}
+
+
+def run_nvfp4(qf, x, amax_in=None, ld=None):
+    R, K = x.shape
+    xd = to_dev(x) if ld is None else to_dev(_strided(x, ld))[:, :K]
+    amax = torch.tensor([0.0 if amax_in is None else amax_in], dtype=torch.float32, device="cuda")
+    s_out = torch.zeros(1, dtype=torch.float32, device="cuda")
+    codes = torch.empty(R, K // 2, dtype=torch.uint8, device="cuda")
+    scales = torch.empty(R, K // 16, dtype=torch.uint8, device="cuda")
+    xhat = empty_bf16((R, K))
+    mode = qf.AMAX_COMPUTE if amax_in is None else qf.AMAX_GIVEN
+    qf.fakequant_nvfp4(xd, amax, mode, s_out, codes, scales, xhat)
+    torch.cuda.synchronize()
+    return {"codes": from_dev(codes), "scales": from_dev(scales), "xhat": from_dev(xhat),
+            "S": float(s_out.item()), "amax": float(amax.item())}
+
+
+def run_q4k(qf, x, ld=None):
+    R, K = x.shape
+    xd = to_dev(x) if ld is None else to_dev(_strided(x, ld))[:, :K]
+    packed = torch.empty(R, K // 256, 144, dtype=torch.uint8, device="cuda")
+    xhat = empty_bf16((R, K))
+    qf.fakequant_q4k(xd, packed, xhat)
+    torch.cuda.synchronize()
+    return {"packed": from_dev(packed), "xhat": from_dev(xhat)}
+
+
+def assert_same(got, want, keys, what=""):
+    for k in keys:
+        g, w = np.asarray(got[k]), np.asarray(want[k])
+        if not np.array_equal(g, w):
+            bad = np.argwhere(g != w)
+            i = tuple(bad[0])
+            raise AssertionError(f"{what} {k}: {len(bad)} mismatches, first at {i}: "
+                                 f"got {g[i]} want {w[i]}")
+
+
+def all_bf16_blocks(block, finite_only=False, seed=None):
+    v = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    if finite_only:
+        v = v[(v & 0x7F80) != 0x7F80]
+    if seed is not None:
+        v = np.random.default_rng(seed).permutation(v)
+    n = len(v) // block * block
+    return v[:n].reshape(-1, block)
+
+
+# ------------------------------------------------------------------------------- MXFP4
+def test_mxfp4_exhaustive_bf16_inputs(qf):
+    for seed in (None, 1):
+        x = all_bf16_blocks(32, seed=seed).reshape(-1, 256)
+        assert_same(run_mxfp4(qf, x), oracle.mxfp4(x), ("codes", "scales", "xhat"), "mxfp4")
+
+
+def test_mxfp4_wide_range_and_ragged(qf):
+    rng = np.random.default_rng(0)
+    for R, K, ld in [(1, 32, None), (3, 96, None), (37, 2080, None), (130, 4096, 4160),
+                     (5, 8192, None)]:
+        x = wide_range_bf16(rng, (R, K), lo_exp=-140, hi_exp=126)
+        assert_same(run_mxfp4(qf, x, ld), oracle.mxfp4(x), ("codes", "scales", "xhat"),
+                    f"mxfp4 {R}x{K}")
+
+
+def test_mxfp4_full_size_mlp_up_operands(qf):
+    w = workloads.mlp_up(seed=0)
+    for name in ("W", "X"):
+        assert_same(run_mxfp4(qf, w[name]), oracle.mxfp4(w[name]), ("codes", "scales", "xhat"),
+                    "mxfp4 " + name)
+
+
+# ------------------------------------------------------------------------------- NVFP4
+def test_nvfp4_exhaustive_finite_bf16_inputs(qf):
+    for seed in (None, 2):
+        x = all_bf16_blocks(16, finite_only=True, seed=seed).reshape(-1, 64)
+        want = oracle.nvfp4(x)
+        got = run_nvfp4(qf, x)
+        assert_same(got, want, ("codes", "scales", "xhat"), "nvfp4 computed g")
+        assert got["S"] == want["S"]
+        # the same inputs under several supplied (running / tied) amax values
+        for g in [1.0, 3.0e-3, 2.5e5, 1.0e-30, 3.0e38]:
+            g32 = float(np.float32(g))
+            assert_same(run_nvfp4(qf, x[:64], amax_in=g32), oracle.nvfp4(x[:64], amax_in=g32),
+                        ("codes", "scales", "xhat"), f"nvfp4 g={g}")
+
+
+def test_nvfp4_wide_range_ragged_and_amax(qf):
+    rng = np.random.default_rng(3)
+    for R, K, ld in [(1, 16, None), (7, 48, None), (33, 4112, None), (64, 1024, 1040)]:
+        for spread in (3, 30):
+            x = wide_range_bf16(rng, (R, K), lo_exp=-spread, hi_exp=spread)
+            want = oracle.nvfp4(x)
+            got = run_nvfp4(qf, x, ld=ld)
+            assert_same(got, want, ("codes", "scales", "xhat"), f"nvfp4 {R}x{K}")
+            assert got["S"] == want["S"] and got["amax"] == oracle.amax(x)
+
+
+def test_nvfp4_zero_tensor(qf):
+    x = np.zeros((4, 64), np.uint16)
+    x[2, 5] = 0x8000
+    got = run_nvfp4(qf, x)
+    assert_same(got, oracle.nvfp4(x), ("codes", "scales", "xhat"), "nvfp4 zeros")
+    assert got["S"] == 0.0
+
+
+def test_nvfp4_full_size_weights(qf):
+    w = workloads.single_linear(seed=0)
+    assert_same(run_nvfp4(qf, w["W"]), oracle.nvfp4(w["W"]), ("codes", "scales", "xhat", "S"),
+                "nvfp4 512x512")
+    rng = np.random.default_rng(4)
+    W = workloads.normal_bf16(rng, (24576, 4096), 0.02)     # fused gate/up of the 9B layer
+    assert_same(run_nvfp4(qf, W), oracle.nvfp4(W), ("codes", "scales", "xhat", "S"),
+                "nvfp4 24576x4096")
+
+
+# -------------------------------------------------------------------------------- Q4_K
+def test_q4k_wide_range_edge_blocks_and_ragged(qf):
+    rng = np.random.default_rng(5)
+    for R, K, ld in [(1, 256, None), (9, 768, None), (40, 4096, 4352), (3, 8448, None)]:
+        x = wide_range_bf16(rng, (R, K), lo_exp=-20, hi_exp=10, zero_frac=0.05)
+        x[0, :32] = 0                                  # all-zero sub-block
+        x[-1, 32:64] = 0x8000                          # all -0 sub-block
+        x[-1, 64:96] = np.abs(x[-1, 64:96].astype(np.int32)).astype(np.uint16) | 0x8000
+        assert_same(run_q4k(qf, x, ld), oracle.q4k(x), ("packed", "xhat"), f"q4k {R}x{K}")
+
+
+def test_q4k_exhaustive_bf16_inputs_below_limits(qf):
+    # every bf16 pattern with magnitude below 2^100 (super-block ranges stay finite in FP32),
+    # then every pattern below 2^14 (scales inside the FP16 range), in shuffled blocks
+    v = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    for lim, seed in ((2.0 ** 100, 7), (2.0 ** 14, 8)):
+        mag = np.abs((v.astype(np.uint32) << 16).view(np.float32))
+        sel = np.random.default_rng(seed).permutation(v[mag < lim])
+        x = sel[: len(sel) // 256 * 256].reshape(-1, 256)
+        assert_same(run_q4k(qf, x), oracle.q4k(x), ("packed", "xhat"), f"q4k below {lim}")
+
+
+def test_q4k_full_size_export_weight(qf):
+    w = workloads.q4k_weight(seed=0, scale=64)
+    assert_same(run_q4k(qf, w["W"]), oracle.q4k(w["W"]), ("packed", "xhat"), "q4k 14336x4096")
+
+
+# ------------------------------------------------------------------------------- amax
+def test_amax_and_running_accumulate(qf):
+    rng = np.random.default_rng(6)
+    a = wide_range_bf16(rng, (100, 1024), lo_exp=-5, hi_exp=5)
+    b = wide_range_bf16(rng, (60, 1024), lo_exp=-5, hi_exp=9)
+    out = torch.zeros(1, dtype=torch.float32, device="cuda")
+    qf.amax(to_dev(a), out, accumulate=False)
+    torch.cuda.synchronize()
+    assert float(out.item()) == oracle.amax(a)
+    qf.amax(to_dev(b), out, accumulate=True)
+    torch.cuda.synchronize()
+    assert float(out.item()) == max(oracle.amax(a), oracle.amax(b))
+    qf.amax(to_dev(a), out, accumulate=True)
+    torch.cuda.synchronize()
+    assert float(out.item()) == max(oracle.amax(a), oracle.amax(b))
+
+
+def test_determinism_two_runs(qf):
+    w = workloads.mlp_up(seed=1, scale=8, n_scale=8)
+    a = run_nvfp4(qf, w["X"])
+    b = run_nvfp4(qf, w["X"])
+    assert_same(a, b, ("codes", "scales", "xhat", "S"), "repeat")
+
+
+def test_empty_inputs_are_no_ops(qf):
+    x = torch.zeros(0, 64, dtype=torch.int16, device="cuda")
+    xhat = torch.zeros(0, 64, dtype=torch.int16, device="cuda")
+    qf.fakequant_mxfp4(x, None, None, xhat)
+    amax = torch.full((1,), 5.0, device="cuda")
+    s_out = torch.full((1,), 5.0, device="cuda")
+    qf.fakequant_nvfp4(x, amax, qf.AMAX_COMPUTE, s_out, None, None, xhat)
+    torch.cuda.synchronize()
+    assert float(amax.item()) == 0.0 and float(s_out.item()) == 0.0
