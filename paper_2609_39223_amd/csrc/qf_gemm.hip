@@ -67,68 +67,230 @@ __device__ __forceinline__ uint32_t bf16_rne(float f) {
   return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
 }
 
-// Operand tile [256 mn][64 k] read from global into registers.
-// k-major: element (mn, k) at P[mn * ld + k]; lane t reads chunks (r = 32 i + t / 8, c = t % 8).
-// mn-major: element (mn, k) at P[k * ld + mn]; lane t reads rows k = 8 (t / 32) + i of the
-//   8 mn values starting at 8 (t % 32), to be transposed in registers before the LDS store.
+// LDS layout (128 KB): [A stage buffer 0 | A buffer 1 | B buffer 0 | B buffer 1], 32 KB each.
+constexpr int kLdsB = 2 * kTileBytes;
+
+// One operand's staging state for the block.
+// k-major: element (mn, k) at P[mn * ld + k]; lane t owns chunks (row 32 i + t / 8, chunk t % 8).
+// mn-major: element (mn, k) at P[k * ld + mn]; lane t owns the 8 x 8 block of rows
+//   k = 8 (t / 32) + i and columns mn = 8 (t % 32) + j, transposed in registers so that LDS
+//   holds it k-contiguous like the k-major operand.
+// `base` (uniform) is the tile origin at the block's first k; a 64-deep step advances it by
+// `step` bytes; `off` are per-lane byte offsets (rows past the matrix end are clamped to the
+// last row: they only feed outputs that are never stored).  `wr` are per-lane LDS offsets.
 template <bool KMAJOR>
-struct Stage {
+struct Operand {
+  const char* base;
+  int64_t step;
+  uint32_t off[8];
+  int wr[8];
   uint4 v[8];
 
-  __device__ __forceinline__ void load(const uint16_t* __restrict__ P, int64_t ld, int64_t mn0,
-                                       int64_t mn_end, int64_t k0, int64_t k_end, int tid) {
+  __device__ __forceinline__ void init(const uint16_t* P, int64_t ld, int64_t mn0,
+                                       int64_t mn_end, int64_t kb, int tid) {
     if (KMAJOR) {
+      base = reinterpret_cast<const char*>(P + mn0 * ld + kb);
+      step = (int64_t)BK * 2;
       const int c = tid & 7;
-      const int64_t k = k0 + c * 8;
+      const int64_t lim = mn_end - mn0 - 1;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const int64_t mn = mn0 + i * 32 + (tid >> 3);
-        v[i] = make_uint4(0, 0, 0, 0);
-        if (mn < mn_end && k < k_end) v[i] = *reinterpret_cast<const uint4*>(P + mn * ld + k);
+        const int rel = i * 32 + (tid >> 3);
+        const int64_t rc = rel < lim ? rel : lim;
+        off[i] = (uint32_t)((rc * ld + c * 8) * 2);
+        wr[i] = lds_off(rel, c);
       }
     } else {
-      const int64_t mn = mn0 + (tid & 31) * 8;
-      const int64_t kb = k0 + (tid >> 5) * 8;
+      base = reinterpret_cast<const char*>(P + kb * ld + mn0);
+      step = (int64_t)BK * ld * 2;
+      const int mg = tid & 31, kg = tid >> 5;
+      const int64_t lim = mn_end - mn0 - 8;
+      const int64_t cc = mg * 8 < lim ? mg * 8 : lim;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        v[i] = make_uint4(0, 0, 0, 0);
-        if (mn < mn_end && kb + i < k_end)
-          v[i] = *reinterpret_cast<const uint4*>(P + (kb + i) * ld + mn);
+        off[i] = (uint32_t)(((int64_t)(kg * 8 + i) * ld + cc) * 2);
+        wr[i] = lds_off(mg * 8 + i, kg);
       }
     }
   }
 
-  __device__ __forceinline__ void store(char* __restrict__ lds, int tid) const {
+  __device__ __forceinline__ void load(int i, int64_t s) {
+    v[i] = *reinterpret_cast<const uint4*>(base + s * step + off[i]);
+  }
+  __device__ __forceinline__ void load_all(int64_t s) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) load(i, s);
+  }
+  // Partial last step: contraction indices >= krem (relative to the step) read as zero.
+  __device__ __forceinline__ void load_tail(int64_t s, int64_t krem, int tid) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int64_t k = KMAJOR ? (tid & 7) * 8 : (tid >> 5) * 8 + i;
+      v[i] = make_uint4(0, 0, 0, 0);
+      if (k < krem) load(i, s);
+    }
+  }
+  // k-major: chunk i -> its LDS slot.
+  __device__ __forceinline__ void write(int i, char* lds) const {
+    *reinterpret_cast<uint4*>(lds + wr[i]) = v[i];
+  }
+  // mn-major: transpose the 8 x 8 bf16 block and store the 8 k-contiguous chunks.
+  __device__ __forceinline__ void write_transposed(char* lds) const {
+    uint32_t w[8][4];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      w[i][0] = v[i].x; w[i][1] = v[i].y; w[i][2] = v[i].z; w[i][3] = v[i].w;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      uint32_t o[4];
+#pragma unroll
+      for (int d = 0; d < 4; ++d) {
+        const uint32_t lo = w[2 * d][j >> 1], hi = w[2 * d + 1][j >> 1];
+        o[d] = (j & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
+      }
+      *reinterpret_cast<uint4*>(lds + wr[j]) = make_uint4(o[0], o[1], o[2], o[3]);
+    }
+  }
+  __device__ __forceinline__ void write_all(char* lds) const {
     if (KMAJOR) {
-      const int c = tid & 7;
 #pragma unroll
-      for (int i = 0; i < 8; ++i)
-        *reinterpret_cast<uint4*>(lds + lds_off(i * 32 + (tid >> 3), c)) = v[i];
+      for (int i = 0; i < 8; ++i) write(i, lds);
     } else {
-      const int mg = tid & 31, kg = tid >> 5;
-      uint32_t w[8][4];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        w[i][0] = v[i].x; w[i][1] = v[i].y; w[i][2] = v[i].z; w[i][3] = v[i].w;
-      }
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        uint32_t o[4];
-#pragma unroll
-        for (int d = 0; d < 4; ++d) {
-          const uint32_t lo = w[2 * d][j >> 1], hi = w[2 * d + 1][j >> 1];
-          o[d] = (j & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
-        }
-        *reinterpret_cast<uint4*>(lds + lds_off(mg * 8 + j, kg)) = make_uint4(o[0], o[1], o[2], o[3]);
-      }
+      write_transposed(lds);
     }
   }
 };
+
+// Which chunks of an operand are written to LDS in which k-slice of a step (see the pipeline
+// below).  k-major operands spread their 8 chunks as pairs over slices 3, 0, 1, 2; mn-major
+// operands write all 8 at once (the transpose needs all eight rows): A in slice 3, B in 0.
+template <bool KMAJOR, bool IS_A>
+__device__ __forceinline__ constexpr bool writes_in(int slice, int i) {
+  return KMAJOR ? ((i >> 1) == ((slice + 1) & 3)) : (slice == (IS_A ? 3 : 0));
+}
+
+template <bool KMAJOR, bool IS_A>
+__device__ __forceinline__ void stage_slice(Operand<KMAJOR>& op, int slice, char* wbuf,
+                                            int64_t load_stage) {
+  if (KMAJOR) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if (writes_in<KMAJOR, IS_A>(slice, i)) { op.write(i, wbuf); op.load(i, load_stage); }
+  } else if (writes_in<KMAJOR, IS_A>(slice, 0)) {
+    op.write_transposed(wbuf);
+    op.load_all(load_stage);
+  }
+}
+
+// Per-lane LDS byte offsets of this wave's MFMA fragments: fragment i of k-slice kk sits at
+// frag_off[kk][i & 1] + i * 4096 (row 32 i further; the swizzle term (row >> 3) & 7 flips by
+// 4 for odd i).
+__device__ __forceinline__ void frag_offsets(int rbase, int lane, int fo[4][2]) {
+  const int r = rbase + (lane & 31);
+  const int g = (lane >> 5) ^ (r & 7) ^ ((r >> 3) & 7);
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    fo[kk][0] = r * 128 + ((g ^ (2 * kk)) << 4);
+    fo[kk][1] = r * 128 + ((g ^ (2 * kk) ^ 4) << 4);
+  }
+}
+
+__device__ __forceinline__ void read_frags(const char* __restrict__ a, const char* __restrict__ b,
+                                           const int fa[2], const int fb[2], bf16x8_t af[4],
+                                           bf16x8_t bfr[4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    af[i] = *reinterpret_cast<const bf16x8_t*>(a + fa[i & 1] + i * 4096);
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+    bfr[j] = *reinterpret_cast<const bf16x8_t*>(b + fb[j & 1] + j * 4096);
+}
+
+__device__ __forceinline__ void mfma16(f32x16_t acc[4][4], const bf16x8_t af[4],
+                                       const bf16x8_t bfr[4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+}
+
+// Scheduling-group masks (AMDGPU backend): MFMA, DS read, DS write, VMEM read.
+#define QF_SG(mask, n) __builtin_amdgcn_sched_group_barrier(mask, n, 0)
+constexpr int kSgMfma = 0x008, kSgDsRead = 0x100, kSgDsWrite = 0x200, kSgVmemRead = 0x020;
+
+// Interleave one k-slice: 16 MFMAs with 8 fragment reads and this slice's LDS writes and
+// global loads.
+__device__ __forceinline__ void sched_slice(int nw) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    QF_SG(kSgMfma, 1);
+    QF_SG(kSgDsRead, 1);
+    if (i < nw) { QF_SG(kSgDsWrite, 1); QF_SG(kSgVmemRead, 1); }
+    QF_SG(kSgMfma, 1);
+    if (i + 8 < nw) { QF_SG(kSgDsWrite, 1); QF_SG(kSgVmemRead, 1); }
+  }
+}
+
+template <bool KM>
+__device__ __forceinline__ constexpr int nwrites(int slice, bool is_a) {
+  return KM ? 2 : ((slice == (is_a ? 3 : 0)) ? 8 : 0);
+}
 
 __device__ __forceinline__ int remap_xcd(int bid, int nb) {
   const int full = nb - nb % kXcds;
   if (bid >= full) return bid;
   return (bid % kXcds) * (full / kXcds) + bid / kXcds;
+}
+
+// Software pipeline over 64-deep k steps, one barrier per step, LDS double buffer.
+// During step kt (reading stage kt from buffer kt&1):
+//   slices 0-2: MFMAs on slices 0-2 of stage kt; fragment reads of slices 1-3; LDS writes of
+//               the slice-0..2 chunks of stage kt+1 into buffer (kt+1)&1, each followed by the
+//               global load of the same chunk of stage kt+2 into the freed registers
+//   barrier   : stage kt+1 is complete in LDS; every wave is done reading buffer kt&1
+//   slice 3   : MFMAs on slice 3; fragment reads of slice 0 of stage kt+1; LDS writes of the
+//               slice-3 chunks of stage kt+2 into buffer kt&1, then loads of stage kt+3
+// Every chunk is therefore loaded one full step before it is written to LDS.  Loads past the
+// last full stage re-read the last stage (uniform clamp) and are never used.
+template <bool A_KM, bool B_KM, int CUR>
+__device__ __forceinline__ void pipeline_step(int64_t kt, int64_t last, Operand<A_KM>& A,
+                                              Operand<B_KM>& B, char* smem, const int fa[4][2],
+                                              const int fb[4][2], bf16x8_t af0[4],
+                                              bf16x8_t bf0[4], bf16x8_t af1[4], bf16x8_t bf1[4],
+                                              f32x16_t acc[4][4]) {
+  char* aCur = smem + CUR * kTileBytes;
+  char* aNxt = smem + (1 - CUR) * kTileBytes;
+  char* bCur = smem + kLdsB + CUR * kTileBytes;
+  char* bNxt = smem + kLdsB + (1 - CUR) * kTileBytes;
+  const int64_t s2 = kt + 2 <= last ? kt + 2 : last;
+  const int64_t s3 = kt + 3 <= last ? kt + 3 : last;
+  // slice 0
+  read_frags(aCur, bCur, fa[1], fb[1], af1, bf1);
+  stage_slice<A_KM, true>(A, 0, aNxt, s2);
+  stage_slice<B_KM, false>(B, 0, bNxt, s2);
+  mfma16(acc, af0, bf0);
+  sched_slice(nwrites<A_KM>(0, true) + nwrites<B_KM>(0, false));
+  // slice 1
+  read_frags(aCur, bCur, fa[2], fb[2], af0, bf0);
+  stage_slice<A_KM, true>(A, 1, aNxt, s2);
+  stage_slice<B_KM, false>(B, 1, bNxt, s2);
+  mfma16(acc, af1, bf1);
+  sched_slice(nwrites<A_KM>(1, true) + nwrites<B_KM>(1, false));
+  // slice 2
+  read_frags(aCur, bCur, fa[3], fb[3], af1, bf1);
+  stage_slice<A_KM, true>(A, 2, aNxt, s2);
+  stage_slice<B_KM, false>(B, 2, bNxt, s2);
+  mfma16(acc, af0, bf0);
+  sched_slice(nwrites<A_KM>(2, true) + nwrites<B_KM>(2, false));
+  __syncthreads();
+  // slice 3
+  read_frags(aNxt, bNxt, fa[0], fb[0], af0, bf0);
+  stage_slice<A_KM, true>(A, 3, aCur, s3);
+  stage_slice<B_KM, false>(B, 3, bCur, s3);
+  mfma16(acc, af1, bf1);
+  sched_slice(nwrites<A_KM>(3, true) + nwrites<B_KM>(3, false));
 }
 
 template <bool A_KM, bool B_KM, bool C_F32, int MODE>
@@ -181,49 +343,53 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmArgs p) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
 
-  const int64_t nk = ke > kb ? (ke - kb + BK - 1) / BK : 0;
-  Stage<A_KM> sa;
-  Stage<B_KM> sb;
-  if (nk > 0) {
-    sa.load(Ap, p.lda, m0, m_end, kb, ke, tid);
-    sb.load(Bp, p.ldb, n0, n_end, kb, ke, tid);
-    sa.store(smem, tid);
-    sb.store(smem + kTileBytes, tid);
-  }
-  __syncthreads();
+  Operand<A_KM> A;
+  Operand<B_KM> B;
+  A.init(Ap, p.lda, m0, m_end, kb, tid);
+  B.init(Bp, p.ldb, n0, n_end, kb, tid);
+  int fa[4][2], fb[4][2];
+  frag_offsets(wm * 128, lane, fa);
+  frag_offsets(wn * 128, lane, fb);
+  bf16x8_t af0[4], bf0[4], af1[4], bf1[4];
+  const int64_t depth = ke > kb ? ke - kb : 0;
+  const int64_t nfull = depth / BK;
+  const int64_t krem = depth % BK;
 
-  for (int64_t kt = 0; kt < nk; ++kt) {
-    char* cur = smem + (kt & 1) * 2 * kTileBytes;
-    char* nxt = smem + ((kt + 1) & 1) * 2 * kTileBytes;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      const int64_t k0 = kb + (kt + 1) * BK;
-      sa.load(Ap, p.lda, m0, m_end, k0, ke, tid);
-      sb.load(Bp, p.ldb, n0, n_end, k0, ke, tid);
-    }
-    const char* As = cur;
-    const char* Bs = cur + kTileBytes;
-#pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      const int c = kk * 2 + (lane >> 5);
-      bf16x8_t af[4], bfr[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        af[i] = *reinterpret_cast<const bf16x8_t*>(As + lds_off(wm * 128 + i * 32 + (lane & 31), c));
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8_t*>(Bs + lds_off(wn * 128 + j * 32 + (lane & 31), c));
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-    }
-    if (more) {
-      sa.store(nxt, tid);
-      sb.store(nxt + kTileBytes, tid);
-    }
+  if (nfull > 0) {
+    const int64_t last = nfull - 1;
+    // prologue: stage 0 -> buffer 0; stage 1's slice-3 chunks -> buffer 1; registers hold
+    // stage 1 for slices 0-2 and stage 2 for slice 3.
+    A.load_all(0);
+    B.load_all(0);
+    A.write_all(smem);
+    B.write_all(smem + kLdsB);
+    A.load_all(last < 1 ? last : 1);
+    B.load_all(last < 1 ? last : 1);
+    stage_slice<A_KM, true>(A, 3, smem + kTileBytes, last < 2 ? last : 2);
+    stage_slice<B_KM, false>(B, 3, smem + kLdsB + kTileBytes, last < 2 ? last : 2);
     __syncthreads();
+    read_frags(smem, smem + kLdsB, fa[0], fb[0], af0, bf0);
+    int64_t kt = 0;
+    for (; kt + 1 < nfull; kt += 2) {
+      pipeline_step<A_KM, B_KM, 0>(kt, last, A, B, smem, fa, fb, af0, bf0, af1, bf1, acc);
+      pipeline_step<A_KM, B_KM, 1>(kt + 1, last, A, B, smem, fa, fb, af0, bf0, af1, bf1, acc);
+    }
+    if (kt < nfull)
+      pipeline_step<A_KM, B_KM, 0>(kt, last, A, B, smem, fa, fb, af0, bf0, af1, bf1, acc);
+  }
+  if (krem > 0) {
+    // partial last step, outside the pipeline: masked loads straight into buffer 0
+    __syncthreads();
+    A.load_tail(nfull, krem, tid);
+    B.load_tail(nfull, krem, tid);
+    A.write_all(smem);
+    B.write_all(smem + kLdsB);
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      read_frags(smem, smem + kLdsB, fa[kk], fb[kk], af0, bf0);
+      mfma16(acc, af0, bf0);
+    }
   }
 
   // ---- epilogue: accumulator (row 8(v/4) + 4(lane/32) + v%4, col lane%32) -> C -------------
