@@ -6,6 +6,7 @@ X [8192, 4096], W [14336, 4096], dY [8192, 14336] (seeded synthetic bf16, see wo
 One step is the whole hot path, in the order the layer runs it:
     forward:  Q(W) -> W_hat, Q(X) -> X_hat (MXFP4 quantize-dequantize), Y = X_hat W_hat^T
     backward: Q(W), Q(X) again (the quantized tensors are transient, as in the paper),
+              W_hat^T, X_hat^T, dY^T (transposes into the NT GEMM's operand form),
               dX = dY W_hat, dW = dY^T X_hat (FP32)
 `value` is the step's throughput in TFLOP/s over the three GEMMs' 3 * 2MNK flops, with the
 quantization time inside the step.  Each launch is bracketed by HIP events on the stream it
@@ -38,7 +39,23 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-rows", type=int, default=256,
                    help="token rows in the CPU oracle's bounded sample of the step")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="only run a plain 1 GiB device-to-device copy (reference for the "
+                        "HBM byte counters) and exit")
     return p.parse_args()
+
+
+def copy_calibration():
+    """A plain copy of known size: 2^30 bytes read and 2^30 bytes written, 5 times."""
+    import torch
+    a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": 1 << 30, "repeats": 5}), flush=True)
 
 
 def main():
@@ -47,6 +64,9 @@ def main():
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU path is "
               "not part of this build", file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
     import torch
     import paper_2609_39223_amd as qf
     import workloads
@@ -63,31 +83,37 @@ def main():
     X, W, dY = up(w["X"]), up(w["W"]), up(w["dY"])
     what = torch.empty(N, K, dtype=torch.int16, device=dev)
     xhat = torch.empty(M, K, dtype=torch.int16, device=dev)
+    whatt = torch.empty(K, N, dtype=torch.int16, device=dev)
+    xhatt = torch.empty(K, M, dtype=torch.int16, device=dev)
+    dYt = torch.empty(N, M, dtype=torch.int16, device=dev)
     Y = torch.empty(M, N, dtype=torch.int16, device=dev)
     dX = torch.empty(M, K, dtype=torch.int16, device=dev)
     dW = torch.empty(N, K, dtype=torch.float32, device=dev)
 
-    phases = ["quant_W", "quant_X", "gemm_fwd", "requant_W", "gemm_dX", "requant_X", "gemm_dW"]
+    # The launches qf_qlinear_fwd + qf_qlinear_bwd_ste issue for this layer, one by one so
+    # each can be bracketed by events.  All three products run as NT GEMMs.
+    phases = ["quant_W", "quant_X", "gemm_fwd", "requant_W", "transpose_W_hat", "gemm_dX",
+              "requant_X", "transpose_X_hat", "transpose_dY", "gemm_dW"]
+    calls = [
+        lambda: qf.fakequant_mxfp4(W, None, None, what),
+        lambda: qf.fakequant_mxfp4(X, None, None, xhat),
+        lambda: qf.gemm_bf16(M, N, K, xhat, K, 1, what, K, 1, Y, N, 0),
+        lambda: qf.fakequant_mxfp4(W, None, None, what),
+        lambda: qf.transpose_bf16(what, whatt),
+        lambda: qf.gemm_bf16(M, K, N, dY, N, 1, whatt, N, 1, dX, K, 0),
+        lambda: qf.fakequant_mxfp4(X, None, None, xhat),
+        lambda: qf.transpose_bf16(xhat, xhatt),
+        lambda: qf.transpose_bf16(dY, dYt),
+        lambda: qf.gemm_bf16(N, K, M, dYt, M, 1, xhatt, M, 1, dW, K, 1),
+    ]
 
     def step(ev=None):
-        def mark(i):
+        for i, c in enumerate(calls):
             if ev is not None:
                 ev[i].record()
-        mark(0)
-        qf.fakequant_mxfp4(W, None, None, what)
-        mark(1)
-        qf.fakequant_mxfp4(X, None, None, xhat)
-        mark(2)
-        qf.gemm_bf16(M, N, K, xhat, K, 1, what, K, 1, Y, N, 0)
-        mark(3)
-        qf.fakequant_mxfp4(W, None, None, what)
-        mark(4)
-        qf.gemm_bf16(M, K, N, dY, N, 1, what, K, 0, dX, K, 0)
-        mark(5)
-        qf.fakequant_mxfp4(X, None, None, xhat)
-        mark(6)
-        qf.gemm_bf16(N, K, M, dY, N, 0, xhat, K, 0, dW, K, 1)
-        mark(7)
+            c()
+        if ev is not None:
+            ev[len(calls)].record()
 
     for _ in range(args.warmup):
         step()

@@ -154,7 +154,9 @@ QF_API qf_status qf_workspace_size(const qf_qlinear_desc* d, size_t* bytes);
 /*
  * qf_qlinear_fwd -- Y = A_hat W_hat^T (bf16 output, FP32 accumulation on MFMA).
  *   X bf16 [M, K], W bf16 [N, K], Y bf16 [M, N]; ws >= qf_workspace_size bytes, 256-aligned.
- * The workspace receives W_hat (and A_hat when afmt != NONE) as bf16.
+ * The workspace receives W_hat (and A_hat when afmt != NONE) as bf16; it also holds the
+ * transposed operands the backward builds (W_hat^T, A_hat^T, dY^T), so one workspace serves
+ * both calls.
  */
 QF_API qf_status qf_qlinear_fwd(const qf_qlinear_desc* d, const uint16_t* X, const uint16_t* W,
                          uint16_t* Y, void* ws, size_t ws_bytes, qf_stream_t stream);
@@ -205,6 +207,14 @@ QF_API qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int6
 /* ---------------------------------------------------------------------------------------
  * Plain BF16 GEMMs on the same MFMA kernels (building blocks of the layer calls above)
  * ------------------------------------------------------------------------------------ */
+/*
+ * qf_transpose_bf16 -- out[c][r] = in[r][c] for a bf16 [R, C] matrix (row strides ldi, ldo);
+ * R and C must be multiples of 8.  The backward uses it to put dY and the quantized operands
+ * in the k-contiguous form of the NT GEMM.
+ */
+QF_API qf_status qf_transpose_bf16(const uint16_t* in, int64_t R, int64_t C, int64_t ldi,
+                                   uint16_t* out, int64_t ldo, qf_stream_t stream);
+
 /*
  * qf_gemm_bf16 -- C[M, N] = sum_k opA(m, k) * opB(n, k), FP32 accumulation.
  *   a_kmajor = 1: A stored [M, K] (k contiguous, row stride lda); 0: stored [K, M].

@@ -79,6 +79,7 @@ def lib() -> ctypes.CDLL:
                                             _P, ctypes.c_size_t, _P], ctypes.c_int),
             "qf_gemm_bf16": ([_I, _I, _I, _P, _I, ctypes.c_int, _P, _I, ctypes.c_int, _P, _I,
                               ctypes.c_int, _P], ctypes.c_int),
+            "qf_transpose_bf16": ([_P, _I, _I, _I, _P, _I, _P], ctypes.c_int),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -205,3 +206,12 @@ def gemm_bf16(M, N, K, A, lda, a_kmajor, B, ldb, b_kmajor, C, ldc, c_f32):
     _check(lib().qf_gemm_bf16(M, N, K, _ptr(_bf16(A)), lda, int(a_kmajor), _ptr(_bf16(B)), ldb,
                               int(b_kmajor), _ptr(C), ldc, int(c_f32), _stream()))
     return C
+
+
+def transpose_bf16(x, out):
+    """out[c][r] = x[r][c] (bf16, R and C multiples of 8)."""
+    R, C, ld = _rows(_bf16(x))
+    if out.dim() != 2 or out.shape[0] != C or out.shape[1] < R or out.stride(1) != 1:
+        raise ValueError("out must be a [C, >=R] row-contiguous tensor")
+    _check(lib().qf_transpose_bf16(_ptr(x), R, C, ld, _ptr(_bf16(out)), out.stride(0), _stream()))
+    return out

@@ -35,8 +35,19 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError("hipcc failed:\n" + err)
     if verbose and err.strip():
         print(err)
+    check_stubs(tmp)
     os.replace(tmp, LIB)
     return LIB
+
+
+def check_stubs(path: str) -> None:
+    """Fail if a kernel's host launch stub is left undefined (the library would load-fail)."""
+    r = subprocess.run(["nm", "--undefined-only", path], capture_output=True, text=True)
+    if r.returncode != 0:
+        return
+    bad = [l.split()[-1] for l in r.stdout.splitlines() if "__device_stub" in l]
+    if bad:
+        raise RuntimeError("undefined kernel launch stubs in %s: %s" % (path, bad))
 
 
 if __name__ == "__main__":

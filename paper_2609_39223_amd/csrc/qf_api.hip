@@ -108,29 +108,42 @@ qf_status fakequant_to(int fmt, const uint16_t* x, int64_t R, int64_t K, int64_t
   }
 }
 
+// Workspace of one linear layer (256-byte aligned regions):
+//   scal   256 B   weight amax scratch
+//   what   [N, K]  W_hat (forward operand), when wfmt != NONE
+//   ahat   [M, K]  A_hat, when afmt != NONE
+//   whatt  [K, N]  W_hat^T (or W^T): right operand of dX = dY W_hat in NT form
+//   ahatt  [K, M]  A_hat^T (or X^T): right operand of dW = dY^T A_hat in NT form
+//   dyt    [N, M]  dY^T: left operand of dW
 struct LinearWs {
-  float* scal;      // [0]: weight amax scratch
-  uint16_t* what;   // [N, K] or null
-  uint16_t* ahat;   // [M, K] or null
+  float* scal;
+  uint16_t* what;
+  uint16_t* ahat;
+  uint16_t* whatt;
+  uint16_t* ahatt;
+  uint16_t* dyt;
 };
 
 size_t linear_ws_bytes(const qf_qlinear_desc* d) {
+  const size_t M = d->M, N = d->N, K = d->K;
   size_t b = kAlign;
-  if (d->wfmt != QF_FMT_NONE) b += up((size_t)d->N * d->K * 2);
-  if (d->afmt != QF_FMT_NONE) b += up((size_t)d->M * d->K * 2);
+  if (d->wfmt != QF_FMT_NONE) b += up(N * K * 2);
+  if (d->afmt != QF_FMT_NONE) b += up(M * K * 2);
+  b += up(K * N * 2) + up(K * M * 2) + up(N * M * 2);
   return b;
 }
 
 LinearWs linear_ws(const qf_qlinear_desc* d, void* ws) {
+  const size_t M = d->M, N = d->N, K = d->K;
   char* p = static_cast<char*>(ws);
   LinearWs w{};
   w.scal = reinterpret_cast<float*>(p);
   p += kAlign;
-  if (d->wfmt != QF_FMT_NONE) {
-    w.what = reinterpret_cast<uint16_t*>(p);
-    p += up((size_t)d->N * d->K * 2);
-  }
-  if (d->afmt != QF_FMT_NONE) w.ahat = reinterpret_cast<uint16_t*>(p);
+  if (d->wfmt != QF_FMT_NONE) { w.what = reinterpret_cast<uint16_t*>(p); p += up(N * K * 2); }
+  if (d->afmt != QF_FMT_NONE) { w.ahat = reinterpret_cast<uint16_t*>(p); p += up(M * K * 2); }
+  w.whatt = reinterpret_cast<uint16_t*>(p); p += up(K * N * 2);
+  w.ahatt = reinterpret_cast<uint16_t*>(p); p += up(K * M * 2);
+  w.dyt = reinterpret_cast<uint16_t*>(p);
   return w;
 }
 
@@ -268,7 +281,7 @@ qf_status qf_qlinear_fwd(const qf_qlinear_desc* d, const uint16_t* X, const uint
   const uint16_t *Wop, *Aop;
   int64_t ldw_op, lda_op;
   QF_TRY(quantize_operands(d, dm, X, W, w, true, true, &Wop, &ldw_op, &Aop, &lda_op, s));
-  QF_TRY(dev(qf::launch_gemm(d->M, d->N, d->K, Aop, lda_op, 1, Wop, ldw_op, 1, Y, dm.ldy, 0, s),
+  QF_TRY(dev(qf::launch_gemm_nt(d->M, d->N, d->K, Aop, lda_op, Wop, ldw_op, Y, dm.ldy, 0, s),
              "forward gemm"));
   return ok();
 }
@@ -291,13 +304,32 @@ qf_status qf_qlinear_bwd_ste(const qf_qlinear_desc* d, const uint16_t* dY, const
   int64_t ldw_op, lda_op;
   QF_TRY(quantize_operands(d, dm, X, W, w, !reuse && dX != nullptr, !reuse && dW != nullptr,
                            &Wop, &ldw_op, &Aop, &lda_op, s));
-  if (dX) {  // dX[M, K] = dY[M, N] W_hat[N, K]: contraction over N, W_hat is [K-out][N]-major
-    QF_TRY(dev(qf::launch_gemm(d->M, d->K, d->N, dY, dm.ldy, 1, Wop, ldw_op, 0, dX, dm.ldx, 0, s),
-               "dX gemm"));
-  }
-  if (dW) {  // dW[N, K] = dY^T A_hat: contraction over M, both operands stored [M][...]
-    QF_TRY(dev(qf::launch_gemm(d->N, d->K, d->M, dY, dm.ldy, 0, Aop, lda_op, 0, dW, d->K, 1, s),
-               "dW gemm"));
+  if (d->M % 8 == 0) {
+    // NT form: transposed operands through the workspace.
+    if (dX) {  // dX[M, K] = dY[M, N] (W_hat^T)[K, N]^T
+      QF_TRY(dev(qf::launch_transpose_bf16(Wop, d->N, d->K, ldw_op, w.whatt, d->N, 1, 0, 0, s),
+                 "transpose W_hat"));
+      QF_TRY(dev(qf::launch_gemm_nt(d->M, d->K, d->N, dY, dm.ldy, w.whatt, d->N, dX, dm.ldx, 0, s),
+                 "dX gemm"));
+    }
+    if (dW) {  // dW[N, K] = (dY^T)[N, M] (A_hat^T)[K, M]^T
+      QF_TRY(dev(qf::launch_transpose_bf16(dY, d->M, d->N, dm.ldy, w.dyt, d->M, 1, 0, 0, s),
+                 "transpose dY"));
+      QF_TRY(dev(qf::launch_transpose_bf16(Aop, d->M, d->K, lda_op, w.ahatt, d->M, 1, 0, 0, s),
+                 "transpose A_hat"));
+      QF_TRY(dev(qf::launch_gemm_nt(d->N, d->K, d->M, w.dyt, d->M, w.ahatt, d->M, dW, d->K, 1, s),
+                 "dW gemm"));
+    }
+  } else {
+    // M not a multiple of 8: the generic kernel reads the [M, *] operands directly.
+    if (dX) {
+      QF_TRY(dev(qf::launch_gemm(d->M, d->K, d->N, dY, dm.ldy, 1, Wop, ldw_op, 0, dX, dm.ldx, 0, s),
+                 "dX gemm"));
+    }
+    if (dW) {
+      QF_TRY(dev(qf::launch_gemm(d->N, d->K, d->M, dY, dm.ldy, 0, Aop, lda_op, 0, dW, d->K, 1, s),
+                 "dW gemm"));
+    }
   }
   return ok();
 }
@@ -311,12 +343,14 @@ struct GroupedWs {
   float* wamax;     // [E]
   uint16_t* what;   // [E, N, K]
   uint16_t* ahat;   // [T, K]
+  uint16_t* whatt;  // [E, K, N]: per-expert W_hat^T, right operand of dX in NT form
 };
 
 size_t grouped_ws_bytes(const qf_grouped_desc* d) {
   size_t b = up((size_t)(d->E + 1) * 4) + up((size_t)d->E * 4) + up((size_t)d->E * 4);
   if (d->wfmt != QF_FMT_NONE) b += up((size_t)d->E * d->N * d->K * 2);
   if (d->afmt != QF_FMT_NONE) b += up((size_t)d->T * d->K * 2);
+  b += up((size_t)d->E * d->N * d->K * 2);
   return b;
 }
 
@@ -327,7 +361,8 @@ GroupedWs grouped_ws(const qf_grouped_desc* d, void* ws) {
   g.order = reinterpret_cast<int*>(p); p += up((size_t)d->E * 4);
   g.wamax = reinterpret_cast<float*>(p); p += up((size_t)d->E * 4);
   if (d->wfmt != QF_FMT_NONE) { g.what = reinterpret_cast<uint16_t*>(p); p += up((size_t)d->E * d->N * d->K * 2); }
-  if (d->afmt != QF_FMT_NONE) g.ahat = reinterpret_cast<uint16_t*>(p);
+  if (d->afmt != QF_FMT_NONE) { g.ahat = reinterpret_cast<uint16_t*>(p); p += up((size_t)d->T * d->K * 2); }
+  g.whatt = reinterpret_cast<uint16_t*>(p);
   return g;
 }
 
@@ -404,8 +439,8 @@ qf_status qf_qlinear_grouped_fwd(const qf_grouped_desc* d, const int64_t* group_
   const uint16_t *Wop, *Aop;
   QF_TRY(grouped_quantize(d, X, W, g, true, true, &Wop, &Aop, s));
   QF_TRY(dev(qf::launch_grouped_prep(group_offsets, d->E, g.tile_start, g.order, s), "prep"));
-  QF_TRY(dev(qf::launch_grouped_rows_ws(d->E, d->T, d->N, d->K, group_offsets, g.tile_start, Aop,
-                                        d->K, Wop, d->K, d->N * d->K, 1, Y, d->N, s),
+  QF_TRY(dev(qf::launch_grouped_nt_rows(d->E, d->T, d->N, d->K, group_offsets, g.tile_start, Aop,
+                                        d->K, Wop, d->K, d->N * d->K, Y, d->N, s),
              "grouped forward"));
   return ok();
 }
@@ -429,8 +464,11 @@ qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int64_t* gr
   QF_TRY(grouped_quantize(d, X, W, g, !reuse && dX, !reuse && dW, &Wop, &Aop, s));
   QF_TRY(dev(qf::launch_grouped_prep(group_offsets, d->E, g.tile_start, g.order, s), "prep"));
   if (dX) {
-    QF_TRY(dev(qf::launch_grouped_rows_ws(d->E, d->T, d->K, d->N, group_offsets, g.tile_start, dY,
-                                          d->N, Wop, d->K, d->N * d->K, 0, dX, d->K, s),
+    QF_TRY(dev(qf::launch_transpose_bf16(Wop, d->N, d->K, d->K, g.whatt, d->N, d->E, d->N * d->K,
+                                         d->N * d->K, s),
+               "transpose expert W_hat"));
+    QF_TRY(dev(qf::launch_grouped_nt_rows(d->E, d->T, d->K, d->N, group_offsets, g.tile_start, dY,
+                                          d->N, g.whatt, d->N, d->N * d->K, dX, d->K, s),
                "grouped dX"));
   }
   if (dW) {
@@ -458,8 +496,21 @@ qf_status qf_gemm_bf16(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64
     if (ldc < N) return fail(QF_ESHAPE, "qf_gemm_bf16: ldc < N");
     if (!aligned16(C)) return fail(QF_EALIGN, "qf_gemm_bf16: C not 16-byte aligned");
   }
-  QF_TRY(dev(qf::launch_gemm(M, N, K, A, lda, a_kmajor, B, ldb, b_kmajor, C, ldc, c_f32, S(stream)),
-             "gemm"));
+  if (a_kmajor && b_kmajor)
+    QF_TRY(dev(qf::launch_gemm_nt(M, N, K, A, lda, B, ldb, C, ldc, c_f32, S(stream)), "gemm"));
+  else
+    QF_TRY(dev(qf::launch_gemm(M, N, K, A, lda, a_kmajor, B, ldb, b_kmajor, C, ldc, c_f32, S(stream)),
+               "gemm"));
+  return ok();
+}
+
+qf_status qf_transpose_bf16(const uint16_t* in, int64_t R, int64_t C, int64_t ldi, uint16_t* out,
+                            int64_t ldo, qf_stream_t stream) {
+  if (R < 0 || C < 0) return fail(QF_ESHAPE, "qf_transpose_bf16: negative shape");
+  if (R % 8 || C % 8) return fail(QF_ESHAPE, "qf_transpose_bf16: R and C must be multiples of 8");
+  QF_TRY(check_mat("qf_transpose_bf16: in", in, R, C, ldi, true));
+  QF_TRY(check_mat("qf_transpose_bf16: out", out, C, R, ldo, true));
+  QF_TRY(dev(qf::launch_transpose_bf16(in, R, C, ldi, out, ldo, 1, 0, 0, S(stream)), "transpose"));
   return ok();
 }
 

@@ -103,3 +103,12 @@ def test_gemm_validation(L):
     assert args(64, 64, 60, 60, 1, 60, 1) == QF_ESHAPE      # K % 8 for k-major operands
     assert args(60, 64, 64, 64, 0, 64, 1) == QF_ESHAPE      # M % 8 for [K][M] A
     assert args(64, 64, 64, 32, 1, 64, 1) == QF_ESHAPE      # lda < K
+
+
+def test_library_has_no_undefined_kernel_stubs():
+    import shutil
+    import subprocess
+    if not os.path.exists(LIB) or shutil.which("nm") is None:
+        pytest.skip("needs the built library and nm")
+    out = subprocess.run(["nm", "--undefined-only", LIB], capture_output=True, text=True).stdout
+    assert "__device_stub" not in out

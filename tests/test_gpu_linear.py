@@ -194,3 +194,44 @@ def test_linear_determinism(qf):
     b = _layer(qf, w, "nvfp4", "none")
     for x, y in zip(a, b):
         assert np.array_equal(x, y)
+
+
+@pytest.mark.parametrize("R,C,ldi", [(64, 256, 256), (8, 8, 8), (136, 520, 528), (8192, 72, 72)])
+def test_transpose_exact(qf, R, C, ldi):
+    rng = np.random.default_rng(R + C)
+    x = rng.integers(0, 65536, size=(R, ldi), dtype=np.uint32).astype(np.uint16)
+    xd = to_dev(x)[:, :C]
+    out = torch.full((C, R + 8), 1234, dtype=torch.int16, device="cuda")[:, :R]
+    qf.transpose_bf16(xd, out)
+    torch.cuda.synchronize()
+    got = from_dev(out.contiguous())
+    np.testing.assert_array_equal(got, x[:, :C].T)
+
+
+def test_layer_backward_with_m_not_multiple_of_8(qf):
+    # M % 8 != 0 takes the kernel that reads the [M, *] operands directly (no transposes)
+    rng = np.random.default_rng(12)
+    M, N, K = 300, 136, 256
+    w = {"X": _rand_bf16(rng, (M, K)), "W": _rand_bf16(rng, (N, K), 0.02),
+         "dY": _rand_bf16(rng, (M, N))}
+    Y, dX, dW = _layer(qf, w, "mxfp4", "mxfp4")
+    what = oracle.mxfp4(w["W"])["xhat"]
+    ahat = oracle.mxfp4(w["X"])["xhat"]
+    assert_close(bf16_to_f64(Y), oracle.linear_fwd(ahat, what), "Y")
+    assert_close(bf16_to_f64(dX), oracle.linear_dx(w["dY"], what), "dX")
+    assert_close(dW.astype(np.float64), oracle.linear_dw(w["dY"], ahat), "dW")
+
+
+def test_nt_gemm_pipeline_depths(qf):
+    # K from below one stage to many stages, with and without a partial last stage
+    rng = np.random.default_rng(13)
+    M, N = 264, 520
+    A = _rand_bf16(rng, (M, 4096))
+    B = _rand_bf16(rng, (N, 4096))
+    for K in [8, 32, 40, 64, 96, 128, 160, 200, 512, 1016, 4096]:
+        C = torch.empty(M, N, dtype=torch.float32, device="cuda")
+        qf.gemm_bf16(M, N, K, to_dev(A), 4096, 1, to_dev(B), 4096, 1, C, N, 1)
+        torch.cuda.synchronize()
+        assert_close(from_dev(C).astype(np.float64),
+                     oracle.linear_fwd(np.ascontiguousarray(A[:, :K]), np.ascontiguousarray(B[:, :K])),
+                     f"K={K}")
