@@ -412,153 +412,6 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmArgs p) {
   }
 }
 
-// ------------------------------------------------------------------------------------------
-// 8-wavefront variant: the same 256 x 256 x 64 block tile with 512 lanes, two wavefronts per
-// SIMD.  Each wavefront owns a 128 x 64 sub-tile (4 x 2 accumulators, 128 AGPRs), so the
-// second wavefront on a SIMD issues MFMAs while the first waits on LDS or the barrier.
-// Wavefronts 0-3 stage the A operand, wavefronts 4-7 the B operand (8 chunks per lane, the
-// same per-lane layout as the 4-wavefront kernel), so a lane holds one operand's registers.
-template <bool KM>
-struct Stager {
-  Operand<KM> op;
-};
-
-template <bool A_KM, bool B_KM, bool C_F32, int MODE>
-__global__ __launch_bounds__(512, 1) void gemm8_kernel(GemmArgs p) {
-  __shared__ __attribute__((aligned(16))) char smem[4 * kTileBytes];
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, w = tid >> 6, wm = w >> 2, wn = w & 3;
-  const bool grpB = w >= 4;
-  const int st = tid & 255;
-  const int bid = remap_xcd(blockIdx.x, gridDim.x);
-
-  const uint16_t* Ap = p.A;
-  const uint16_t* Bp = p.B;
-  char* Cp = reinterpret_cast<char*>(p.C);
-  int64_t m0, m_end, n0, n_end = p.N, kb = 0, ke = p.K;
-  if (MODE == kDense) {
-    const int per_group = kGroupM * p.tiles_n;
-    const int g = bid / per_group;
-    const int first = g * kGroupM;
-    const int gs = min(p.tiles_m - first, kGroupM);
-    const int tm = first + (bid % per_group) % gs;
-    const int tn = (bid % per_group) / gs;
-    m0 = (int64_t)tm * BM; m_end = p.M;
-    n0 = (int64_t)tn * BN;
-  } else if (MODE == kGroupRows) {
-    const int mt = bid / p.tiles_n, tn = bid % p.tiles_n;
-    if (mt >= p.tile_start[p.E]) return;
-    int lo = 0, hi = p.E;
-    while (hi - lo > 1) {
-      const int mid = (lo + hi) >> 1;
-      if (p.tile_start[mid] <= mt) lo = mid; else hi = mid;
-    }
-    const int e = lo;
-    m0 = p.off[e] + (int64_t)(mt - p.tile_start[e]) * BM;
-    m_end = p.off[e + 1];
-    n0 = (int64_t)tn * BN;
-    Bp += (int64_t)e * p.bstride;
-  } else {
-    const int tpe = p.tiles_m * p.tiles_n;
-    const int e = p.order[bid / tpe];
-    const int t = bid % tpe;
-    m0 = (int64_t)(t / p.tiles_n) * BM; m_end = p.M;
-    n0 = (int64_t)(t % p.tiles_n) * BN;
-    kb = p.off[e]; ke = p.off[e + 1];
-    Cp += (int64_t)e * p.cstride * (C_F32 ? 4 : 2);
-  }
-
-  f32x16_t acc[4][2];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16_t{};
-
-  // One operand per lane: A for wavefronts 0-3, B for 4-7.  When both operands share a
-  // layout the staging code is identical and only the base pointer differs.
-  constexpr bool same = A_KM == B_KM;
-  Operand<A_KM> SA;
-  Operand<B_KM> SB;
-  if (same || !grpB) SA.init(grpB ? reinterpret_cast<const uint16_t*>(Bp) : Ap, grpB ? p.ldb : p.lda,
-                             grpB ? n0 : m0, grpB ? n_end : m_end, kb, st);
-  if (!same && grpB) SB.init(Bp, p.ldb, n0, n_end, kb, st);
-  char* myLds = smem + (grpB ? kLdsB : 0);
-
-  int fa[4][2], fb[4][2];
-  frag_offsets(wm * 128, lane, fa);
-  frag_offsets(wn * 64, lane, fb);
-  bf16x8_t af[4], bfr[2];
-  const int64_t depth = ke > kb ? ke - kb : 0;
-  const int64_t nfull = depth / BK;
-  const int64_t krem = depth % BK;
-
-#define QF8_STAGE(expr_a, expr_b) \
-  do { if (same || !grpB) { SA.expr_a; } else { SB.expr_b; } } while (0)
-
-  auto slice = [&](const char* a, const char* b, int kk) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      af[i] = *reinterpret_cast<const bf16x8_t*>(a + fa[kk][i & 1] + i * 4096);
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-      bfr[j] = *reinterpret_cast<const bf16x8_t*>(b + fb[kk][j & 1] + j * 4096);
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-  };
-
-  if (nfull > 0) {
-    const int64_t last = nfull - 1;
-    QF8_STAGE(load_all(0), load_all(0));
-    QF8_STAGE(write_all(myLds), write_all(myLds));
-    QF8_STAGE(load_all(last < 1 ? last : 1), load_all(last < 1 ? last : 1));
-    __syncthreads();
-    for (int64_t kt = 0; kt < nfull; ++kt) {
-      const int cur = (int)(kt & 1);
-      const char* aC = smem + cur * kTileBytes;
-      const char* bC = smem + kLdsB + cur * kTileBytes;
-      char* wN = myLds + (1 - cur) * kTileBytes;
-      const int64_t s2 = kt + 2 <= last ? kt + 2 : last;
-      slice(aC, bC, 0);
-      slice(aC, bC, 1);
-      QF8_STAGE(write_all(wN), write_all(wN));
-      QF8_STAGE(load_all(s2), load_all(s2));
-      slice(aC, bC, 2);
-      slice(aC, bC, 3);
-      __syncthreads();
-    }
-  }
-  if (krem > 0) {
-    __syncthreads();
-    QF8_STAGE(load_tail(nfull, krem, st), load_tail(nfull, krem, st));
-    QF8_STAGE(write_all(myLds), write_all(myLds));
-    __syncthreads();
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) slice(smem, smem + kLdsB, kk);
-  }
-#undef QF8_STAGE
-
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int64_t col = n0 + wn * 64 + j * 32 + (lane & 31);
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int64_t row = m0 + wm * 128 + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-        if (row < m_end && col < n_end) {
-          if (C_F32)
-            reinterpret_cast<float*>(Cp)[row * p.ldc + col] = acc[i][j][v];
-          else
-            reinterpret_cast<uint16_t*>(Cp)[row * p.ldc + col] = (uint16_t)bf16_rne(acc[i][j][v]);
-        }
-      }
-    }
-  }
-}
-
 // Per-expert tile prefix (grouped rows) and experts ordered by decreasing row count (grouped
 // wgrad, so the longest contractions start first).  One block, E <= 1024 lanes.
 __global__ void grouped_prep_kernel(const int64_t* __restrict__ off, int E, int* tile_start,
@@ -584,16 +437,9 @@ __global__ void grouped_prep_kernel(const int64_t* __restrict__ off, int E, int*
   }
 }
 
-#ifndef QF_GEMM_WAVES
-#define QF_GEMM_WAVES 4
-#endif
-
 template <bool A_KM, bool B_KM, bool C_F32, int MODE>
 hipError_t launch(const GemmArgs& a, int blocks, hipStream_t s) {
-  if (QF_GEMM_WAVES == 8)
-    hipLaunchKernelGGL((gemm8_kernel<A_KM, B_KM, C_F32, MODE>), dim3(blocks), dim3(512), 0, s, a);
-  else
-    hipLaunchKernelGGL((gemm_kernel<A_KM, B_KM, C_F32, MODE>), dim3(blocks), dim3(NTHR), 0, s, a);
+  hipLaunchKernelGGL((gemm_kernel<A_KM, B_KM, C_F32, MODE>), dim3(blocks), dim3(NTHR), 0, s, a);
   return hipGetLastError();
 }
 

@@ -14,8 +14,8 @@
 //    staging registers and no ds_write instructions.  Wavefronts 0-3 load A, 4-7 load B.
 //  - The k loop runs in 32-deep stages through a 5-stage ring (5 x 32 KB = the whole 160 KB
 //    LDS).  Loads for stage s+4 are issued at step s, three steps before they are needed, so
-//    L2-miss latency is hidden; each wavefront waits only for its own loads of stage s+1
-//    (s_waitcnt vmcnt(8)) before the one barrier per step.
+//    L2-miss latency is hidden; before the one barrier per step each wavefront waits only for
+//    its own loads of stage s+2 (s_waitcnt vmcnt(8)).
 //  - After the barrier every wavefront prefetches the first fragments of the next stage
 //    while the current stage's MFMAs run, so no fragment read waits behind the barrier.
 //  - LDS rows hold 32 bf16 (4 chunks of 16 bytes); chunk c of row r is stored at slot
@@ -41,6 +41,7 @@ constexpr int kGroupM = 8;
 constexpr int kXcds = 8;
 
 enum Mode { kDense = 0, kGroupRows = 1 };
+constexpr int kNtWaves = 8;   // wavefronts per block (the 4-wavefront form is kept compilable)
 
 struct NtArgs {
   const uint16_t* A;
@@ -54,10 +55,6 @@ struct NtArgs {
   const int* tile_start;  // grouped rows: [E+1] per-expert tile prefix
   int E;
 };
-
-#ifndef QF_NT_WAVES
-#define QF_NT_WAVES 8
-#endif
 
 #define QF_LDS(p) ((__attribute__((address_space(3))) void*)(p))
 
@@ -276,8 +273,8 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, in
   a.tiles_m = (int)((M + BM - 1) / BM);
   a.tiles_n = (int)((N + BN - 1) / BN);
   const dim3 grid((unsigned)(a.tiles_m * a.tiles_n));
-  if (c_f32) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, QF_NT_WAVES>), grid, dim3(QF_NT_WAVES * 64), 0, s, a);
-  else hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, QF_NT_WAVES>), grid, dim3(QF_NT_WAVES * 64), 0, s, a);
+  if (c_f32) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, kNtWaves>), grid, dim3(kNtWaves * 64), 0, s, a);
+  else hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, kNtWaves>), grid, dim3(kNtWaves * 64), 0, s, a);
   return hipGetLastError();
 }
 
@@ -292,7 +289,7 @@ hipError_t launch_grouped_nt_rows(int64_t E, int64_t T, int64_t N, int64_t K, co
   a.tiles_n = (int)((N + BN - 1) / BN);
   a.tiles_m = (int)((T + BM - 1) / BM + E);
   const dim3 grid((unsigned)(a.tiles_m * a.tiles_n));
-  hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRows, QF_NT_WAVES>), grid, dim3(QF_NT_WAVES * 64), 0, s, a);
+  hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRows, kNtWaves>), grid, dim3(kNtWaves * 64), 0, s, a);
   return hipGetLastError();
 }
 
