@@ -47,6 +47,22 @@ def parse():
     return p.parse_args()
 
 
+def measured_traffic(launch):
+    """HBM bytes per launch of `launch` from the committed FETCH_SIZE/WRITE_SIZE counter summary
+    (copy-calibrated), or None when no summary covers it or the kernel source has changed since
+    the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "gemm_nt_wgrad_mlp_up_traffic.json")
+    try:
+        rec = json.load(open(path))
+        src = open(os.path.join(ROOT, rec["source"]), "rb").read()
+    except (OSError, ValueError, KeyError):
+        return None
+    if rec.get("launch") != launch or hashlib.sha256(src).hexdigest() != rec["source_sha256"]:
+        return None
+    return rec["bytes"]
+
+
 def copy_calibration():
     """A plain copy of known size: 2^30 bytes read and 2^30 bytes written, 5 times."""
     import torch
@@ -191,7 +207,8 @@ def main():
                    "M": M, "N": N, "K": K, "wfmt": "mxfp4", "afmt": "mxfp4"},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None},
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": measured_traffic(dom), "traffic_unit": "bytes per launch"},
         "phases_ms": {p: round(float(per_phase[i]), 4) for i, p in enumerate(phases)},
         "fakequant": {"kernel": "mxfp4 (codes+scales+x_hat)", "tensor": f"{N}x{K}",
                       "GBps": round(q_gbps, 1), "frac_hbm": round(q_gbps / PEAK_HBM_GBPS, 4),
