@@ -1,30 +1,38 @@
 // NT BF16 MFMA GEMM for gfx950: C[m, n] = sum_k A[m, k] * B[n, k], both operands k-contiguous.
 //
 // Every product of the quantization-aware layer is issued in this form (the backward's
-// transposed operands come from the transposing quantizer / transpose kernels), so this is
-// the one kernel that carries the layer's FLOPs:
+// transposed operands come from the transpose kernel), so this is the one kernel that carries
+// the layer's FLOPs:
 //   forward  Y  = A_hat W_hat^T        A = A_hat [M, K],   B = W_hat [N, K]
 //   dX          = dY W_hat             A = dY [M, N],      B = W_hat^T [K, N]
 //   dW          = dY^T A_hat           A = dY^T [N, M],    B = A_hat^T [K, M]
 //
 // Design (256 x 256 block tile, 512 lanes = 8 wavefronts, two per SIMD):
-//  - Each wavefront owns a 128 x 64 sub-tile as 4 x 2 v_mfma_f32_32x32x16_bf16 accumulators
-//    (128 AGPRs); the second wavefront on a SIMD issues MFMAs while the first waits.
-//  - Operands move global -> LDS with direct-to-LDS loads (global_load_lds_dwordx4): no
-//    staging registers and no ds_write instructions.  Wavefronts 0-3 load A, 4-7 load B.
-//  - The k loop runs in 32-deep stages through a 5-stage ring (5 x 32 KB = the whole 160 KB
-//    LDS).  Loads for stage s+4 are issued at step s, three steps before they are needed, so
-//    L2-miss latency is hidden; before the one barrier per step each wavefront waits only for
-//    its own loads of stage s+2 (s_waitcnt vmcnt(8)).
-//  - After the barrier every wavefront prefetches the first fragments of the next stage
-//    while the current stage's MFMAs run, so no fragment read waits behind the barrier.
-//  - LDS rows hold 32 bf16 (4 chunks of 16 bytes); chunk c of row r is stored at slot
-//    c ^ ((r >> 2) & 3), which keeps 16 consecutive fragment rows on 16 distinct bank groups.
+//  - Each wavefront owns a 128 x 64 sub-tile as 4 x 2 v_mfma_f32_32x32x16_bf16 accumulators;
+//    the second wavefront on a SIMD issues MFMAs while the first waits.
+//  - K advances in 64-deep stages, double-buffered in LDS (2 x 64 KB).  A stage row is 128
+//    bytes, so every global request is a whole 128-byte cache line (32-deep stages fetch half
+//    lines and double the L2 request count).
+//  - Operands move global -> LDS with direct-to-LDS loads (no staging registers, no ds_write):
+//    wavefronts 0-3 load A, 4-7 load B, 8 loads of 8 rows each per wavefront and stage.  The
+//    loads of stage s+1 are issued during the first slice of step s and have three of the
+//    step's four 16-deep MFMA slices to land.
+//  - Each MFMA is followed by one fragment read for the next slice (and, in the first slice,
+//    one direct-to-LDS load), so the LDS and memory pipes work while the MFMA pipe is busy.
+//    One barrier per step, before the last slice: it publishes stage s+1 (all loads waited)
+//    and retires every read of stage s (so step s+1 may overwrite that buffer).
+//  - LDS rows hold 64 bf16 (8 chunks of 16 bytes); chunk c of row r sits at slot
+//    c ^ ((r >> 1) & 7), so the 16 rows a fragment read serves in one pass fall on 16
+//    distinct 16-byte bank groups.
 //  - Rows past the matrix edge load the last valid row (their outputs are never stored); a
-//    partial last k stage goes through a masked register path after the ring drains.
+//    partial last k stage goes through a masked register path.
+//  - The epilogue stages the tile through LDS (rows padded so both half-waves of a write hit
+//    different banks) and writes whole rows with 16-byte stores; FP32 tiles go in two halves.
 //  - Block ids are remapped so each XCD (own L2) works on a contiguous group of tiles.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 #include "qf_internal.h"
 
@@ -34,14 +42,21 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-constexpr int BM = 256, BN = 256, BK = 32, NSTAGE = 5;
-constexpr int kOpStage = BM * BK * 2;            // 16 KB: one operand, one stage
-constexpr int kStage = 2 * kOpStage;             // 32 KB: A then B
+constexpr int BM = 256, BN = 256, BK = 64;
+constexpr int kRow = BK * 2;                     // 128 bytes per LDS row
+constexpr int kOpStage = BM * kRow;              // 32 KB: one operand, one stage
+constexpr int kStage = 2 * kOpStage;             // 64 KB: A then B
 constexpr int kGroupM = 8;
 constexpr int kXcds = 8;
+constexpr int kWaves = 8;
+constexpr int NJ = 2;                            // 32-column accumulator blocks per wavefront
+constexpr int NLD = 8;                           // direct-to-LDS loads per wavefront per stage
+constexpr int kPitch16 = BN * 2 + 16;            // epilogue LDS row pitch, bf16 tile (528 B)
+constexpr int kPitch32 = BN * 4 + 32;            // epilogue LDS row pitch, FP32 half tile
+constexpr int kSmemEpi = (BM * kPitch16 > 128 * kPitch32) ? BM * kPitch16 : 128 * kPitch32;
+constexpr int kSmem = (2 * kStage > kSmemEpi) ? 2 * kStage : kSmemEpi;
 
 enum Mode { kDense = 0, kGroupRows = 1 };
-constexpr int kNtWaves = 8;   // wavefronts per block (the 4-wavefront form is kept compilable)
 
 struct NtArgs {
   const uint16_t* A;
@@ -54,18 +69,31 @@ struct NtArgs {
   const int64_t* off;     // grouped rows: [E+1] row offsets
   const int* tile_start;  // grouped rows: [E+1] per-expert tile prefix
   int E;
+  int vec_store;          // C and ldc allow 16-byte stores
 };
 
 #define QF_LDS(p) ((__attribute__((address_space(3))) void*)(p))
 
-// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
-#define QF_WAIT_VMCNT(n) \
-  __builtin_amdgcn_s_waitcnt(((n) & 15) | (7 << 4) | (15 << 8) | ((((n) >> 4) & 3) << 14))
-
-// 16-byte direct-to-LDS load: lane l's 16 bytes land at lds + 16 l (lds wave-uniform).
-// (A plain function: device builtins with template-dependent operands keep the host pass
-// from emitting the kernel's launch stub.)
-__device__ __forceinline__ void dma16(const void* g, void* lds) {
+// 16-byte direct-to-LDS loads: lane l's 16 bytes land at lds + 16 l (lds wave-uniform).
+// The buffer form (buffer_load_dwordx4 ... lds) reads at voff + soff from a resource whose
+// range ends at the operand's last valid byte (reads past it return zeros).  The global form
+// is plain pointer arithmetic, but the compiler counts it as an LDS access of unknown order,
+// which turns the fine-grained lgkmcnt waits of the fragment reads that follow into full
+// waits.  (Plain functions: device builtins with template-dependent operands keep the host
+// pass from emitting the kernel's launch stub.)
+#ifndef QF_NT_GLOBAL_LDS
+#define QF_NT_GLOBAL_LDS 0
+#endif
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
+  const int64_t n = bytes < 0xFFFFFFFFll ? bytes : 0xFFFFFFFFll;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)(uint32_t)n,
+                                           0x00020000);
+}
+__device__ __forceinline__ void dma16_buf(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff,
+                                          void* lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, QF_LDS(lds), 16, (int)voff, (int)soff, 0, 0);
+}
+__device__ __forceinline__ void dma16_global(const void* g, void* lds) {
   __builtin_amdgcn_global_load_lds(g, QF_LDS(lds), 16, 0, 0);
 }
 
@@ -81,17 +109,13 @@ __device__ __forceinline__ int remap_xcd(int bid, int nb) {
   return (bid % kXcds) * (full / kXcds) + bid / kXcds;
 }
 
-// NW = 8: two wavefronts per SIMD, 128 x 64 each, wavefronts 0-3 load A and 4-7 load B.
-// NW = 4: one wavefront per SIMD, 128 x 128 each, every wavefront loads both operands.
-template <bool C_F32, int MODE, int NW>
-__global__ __launch_bounds__(NW * 64, 1) void gemm_nt_kernel(NtArgs p) {
-  constexpr int NJ = NW == 8 ? 2 : 4;            // 32-column accumulator blocks per wave
-  constexpr int WN = NJ * 32;                    // columns per wavefront
-  constexpr int NLD = NW == 8 ? 4 : 8;           // direct-to-LDS loads per wave per stage
-  __shared__ __attribute__((aligned(16))) char smem[NSTAGE * kStage];
+template <bool C_F32, int MODE>
+__global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
+  __shared__ __attribute__((aligned(16))) char smem[kSmem];
   const int tid = threadIdx.x;
-  const int lane = tid & 63, w = tid >> 6;
-  const int wm = NW == 8 ? w >> 2 : w >> 1, wn = NW == 8 ? w & 3 : w & 1;
+  const int lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (scalar) index
+  const int wm = w >> 2, wn = w & 3;
   const int bid = remap_xcd(blockIdx.x, gridDim.x);
 
   const uint16_t* Bp = p.B;
@@ -119,42 +143,37 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_nt_kernel(NtArgs p) {
   }
   const int64_t n_end = p.N, K = p.K;
 
-  // ---- this lane's loads: direct-to-LDS instructions of 16 rows each ------------------------
-  // Load q of wavefront w fills LDS rows R0 = (4 (w & 3) + (q & 3)) * 16 .. R0 + 15 of operand
-  // (NW == 8 ? w >> 2 : q >> 2); lane l lands at row R0 + l / 4, slot l % 4, which holds
-  // logical chunk (l % 4) ^ ((l / 16) % 4).
-  const int lw = w & 3;
-  const int chunk = (lane & 3) ^ ((lane >> 4) & 3);
-  const char* gbase[2];
+  // ---- this lane's loads ----------------------------------------------------------------------
+  // Wavefront w loads operand w >> 2, tile rows 64 (w & 3) .. + 63; load q covers rows
+  // R = 64 (w & 3) + 8 q .. R + 7, lane l lands at row R + l / 8, slot l % 8, and so fetches
+  // logical chunk (l % 8) ^ ((row >> 1) % 8) = (l % 8) ^ ((4 (q % 2) + l / 16) % 8).
+  const int op = w >> 2, lw = w & 3;
+  const int64_t ld = op ? p.ldb : p.lda;
+  const int64_t r0 = op ? n0 : m0;
+  const int64_t rlim = (op ? n_end : m_end) - r0 - 1;   // last valid row of the tile
+  const char* gbase = reinterpret_cast<const char*>((op ? Bp : p.A) + r0 * ld);
+  const __amdgpu_buffer_rsrc_t rsrc = make_rsrc(gbase, (rlim * ld + K) * 2);
   uint32_t goff[NLD];
-  int lofs[NLD];
-#pragma unroll
-  for (int op = 0; op < 2; ++op) {
-    const uint16_t* P = op ? Bp : p.A;
-    const int64_t r0 = op ? n0 : m0;
-    gbase[op] = reinterpret_cast<const char*>(P + r0 * (op ? p.ldb : p.lda));
-  }
 #pragma unroll
   for (int q = 0; q < NLD; ++q) {
-    const int op = NW == 8 ? (w >> 2) : (q >> 2);
-    const int64_t ld = op ? p.ldb : p.lda;
-    const int64_t rlim = (op ? n_end : m_end) - (op ? n0 : m0) - 1;
-    const int64_t row = (lw * 4 + (q & 3)) * 16 + (lane >> 2);
+    const int64_t row = lw * 64 + q * 8 + (lane >> 3);
     const int64_t rc = row < rlim ? row : rlim;
-    goff[q] = (uint32_t)((rc * ld + chunk * 8) * 2);
-    lofs[q] = op * kOpStage + (lw * 4 + (q & 3)) * 1024;
+    const int c = (lane & 7) ^ ((4 * (q & 1) + (lane >> 4)) & 7);
+    goff[q] = (uint32_t)((rc * ld + c * 8) * 2);
   }
-  const int gsel = NW == 8 ? (w >> 2) : 0;
+  const int lbase = op * kOpStage + lw * 64 * kRow;     // load q adds 8 q rows
 
-  // ---- fragment offsets: slice kk, fragment i at fo[kk] + i * 2048 (32 rows of 64 bytes) -----
-  int foa[2], fob[2];
+  // ---- fragment offsets: slice kk, fragment i at fo[kk] + i * 4096 (32 rows of 128 bytes) -----
+  // Fragment rows start 32-aligned, so the swizzle term (row >> 1) & 7 is (lane >> 1) & 7.
+  int foa[4], fob[4];
   {
-    const int ra = wm * 128 + (lane & 31), rb = wn * WN + (lane & 31);
+    const int ra = wm * 128 + (lane & 31), rb = wn * 64 + (lane & 31);
+    const int sw = (lane >> 1) & 7;
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
+    for (int kk = 0; kk < 4; ++kk) {
       const int c = 2 * kk + (lane >> 5);
-      foa[kk] = ra * 64 + ((c ^ ((ra >> 2) & 3)) << 4);
-      fob[kk] = kOpStage + rb * 64 + ((c ^ ((rb >> 2) & 3)) << 4);
+      foa[kk] = ra * kRow + ((c ^ sw) << 4);
+      fob[kk] = kOpStage + rb * kRow + ((c ^ sw) << 4);
     }
   }
 
@@ -163,102 +182,182 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_nt_kernel(NtArgs p) {
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < NJ; ++j) acc[i][j] = f32x16_t{};
-  bf16x8_t a0[4], b0[NJ], a1[4], b1[NJ];
+  bf16x8_t fa[2][4], fb[2][NJ];
 
-  auto issue = [&](int64_t s, int buf) {
-    char* l = smem + buf * kStage;
+  auto dma = [&](int64_t s, int buf, int q) {
+    char* l = smem + buf * kStage + lbase + q * 8 * kRow;
+    if (QF_NT_GLOBAL_LDS) dma16_global(gbase + s * kRow + goff[q], l);
+    else dma16_buf(rsrc, goff[q], (uint32_t)(s * kRow), l);
+  };
+  // Fragment read r of a slice, in the order the slice's MFMAs consume them: A0, B0, B1, A1..A3.
+  auto read_one = [&](const char* st, int kk, int r, bf16x8_t* a, bf16x8_t* b) {
+    if (r == 0) a[0] = *reinterpret_cast<const bf16x8_t*>(st + foa[kk]);
+    else if (r <= NJ) b[r - 1] = *reinterpret_cast<const bf16x8_t*>(st + fob[kk] + (r - 1) * 4096);
+    else a[r - NJ] = *reinterpret_cast<const bf16x8_t*>(st + foa[kk] + (r - NJ) * 4096);
+  };
+  auto read_all = [&](const char* st, int kk, bf16x8_t* a, bf16x8_t* b) {
 #pragma unroll
-    for (int q = 0; q < NLD; ++q) {
-      const char* g = gbase[NW == 8 ? gsel : (q >> 2)] + s * (BK * 2);
-      dma16(g + goff[q], l + lofs[q]);
+    for (int r = 0; r < 4 + NJ; ++r) read_one(st, kk, r, a, b);
+  };
+  // One 16-deep slice of MFMAs from (a, b), with the fragment reads of the next slice (from
+  // rst / rkk into ra, rb) and, if LOADS, the direct-to-LDS loads of stage ls into buffer
+  // lbuf, issued one per MFMA.  The scheduling fences keep that interleave.
+  auto slice = [&](auto reads, auto loads, const bf16x8_t* a, const bf16x8_t* b,
+                   const char* rst, int rkk, bf16x8_t* ra, bf16x8_t* rb, int64_t ls, int lbuf) {
+    constexpr bool READS = decltype(reads)::value, LOADS = decltype(loads)::value;
+    constexpr int NM = 4 * NJ, NR = 4 + NJ;
+#pragma unroll
+    for (int t = 0; t < NM; ++t) {
+      acc[t / NJ][t % NJ] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[t / NJ], b[t % NJ],
+                                                                    acc[t / NJ][t % NJ], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (READS && t < NR) read_one(rst, rkk, t, ra, rb);
+      if (LOADS) {
+        constexpr int per = (NLD + NM - 1) / NM;
+#pragma unroll
+        for (int q = t * per; q < (t + 1) * per && q < NLD; ++q) dma(ls, lbuf, q);
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
-  auto frags = [&](const char* st, int kk, bf16x8_t* a, bf16x8_t* b) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) a[i] = *reinterpret_cast<const bf16x8_t*>(st + foa[kk] + i * 2048);
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) b[j] = *reinterpret_cast<const bf16x8_t*>(st + fob[kk] + j * 2048);
-  };
-  auto mfma = [&](const bf16x8_t* a, const bf16x8_t* b) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < NJ; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+  // One 64-deep step on stage s (buffer s & 1); unless LAST, stage s+1 is loaded into the
+  // other buffer and its first fragments are read during the last slice.
+  auto step = [&](int64_t s, auto last) {
+    constexpr bool LAST = decltype(last)::value;
+    const int cur = (int)(s & 1), nxt = cur ^ 1;
+    const char* cs = smem + cur * kStage;
+    slice(std::true_type{}, std::integral_constant<bool, !LAST>{}, fa[0], fb[0], cs, 1, fa[1],
+          fb[1], s + 1, nxt);
+    slice(std::true_type{}, std::false_type{}, fa[1], fb[1], cs, 2, fa[0], fb[0], 0, 0);
+    slice(std::true_type{}, std::false_type{}, fa[0], fb[0], cs, 3, fa[1], fb[1], 0, 0);
+    // Stage s+1 has landed everywhere and every read of stage s has returned: after this
+    // barrier the next step may overwrite stage s's buffer.
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    slice(std::integral_constant<bool, !LAST>{}, std::false_type{}, fa[1], fb[1],
+          smem + nxt * kStage, 0, fa[0], fb[0], 0, 0);
   };
 
   const int64_t nfull = K / BK;
   const int64_t krem = K % BK;
   if (nfull > 0) {
-    const int64_t last = nfull - 1;
-    // Ring slot of stage s is s % NSTAGE.  Stage s+4 is issued at the top of step s into the
-    // slot stage s-1 used; the barrier that ends step s-1 guarantees every wavefront has
-    // consumed that slot.  The barrier that ends step s guarantees stage s+2 has landed, so
-    // step s+1 may prefetch its fragments.  Each wavefront issues exactly 4 loads per step
-    // (stages past the end re-load the last stage into a slot nobody reads again), so
-    // "stages up to t landed" is always "at most 8 loads outstanding" at the barrier.
 #pragma unroll
-    for (int s = 0; s < NSTAGE - 1; ++s) issue(s < last ? s : last, s);
-    QF_WAIT_VMCNT(2 * NLD);
+    for (int q = 0; q < NLD; ++q) dma(0, 0, q);
+    __builtin_amdgcn_s_waitcnt(0);               // stage 0 landed (every counter drained)
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    frags(smem, 0, a0, b0);
-    int buf = 0;
-    for (int64_t s = 0; s < nfull; ++s) {
-      const int64_t s4 = s + NSTAGE - 1;
-      const int bufp = buf == 0 ? NSTAGE - 1 : buf - 1;
-      const int bufn = buf == NSTAGE - 1 ? 0 : buf + 1;
-      issue(s4 < last ? s4 : last, bufp);
-      frags(smem + buf * kStage, 1, a1, b1);
-      mfma(a0, b0);
-      frags(smem + bufn * kStage, 0, a0, b0);      // next stage, slice 0
-      mfma(a1, b1);
-      QF_WAIT_VMCNT(2 * NLD);                            // own loads of stage s+2 landed
-      __builtin_amdgcn_s_barrier();
-      __builtin_amdgcn_sched_barrier(0);
-      buf = bufn;
-    }
-    QF_WAIT_VMCNT(0);                              // drain the ring before LDS is reused
+    read_all(smem, 0, fa[0], fb[0]);
+    for (int64_t s = 0; s < nfull - 1; ++s) step(s, std::false_type{});
+    step(nfull - 1, std::true_type{});
   }
   if (krem > 0) {
-    // Partial last stage: masked loads through registers into ring slot 0.
-    QF_WAIT_VMCNT(0);
+    // Partial last stage: masked loads through registers into buffer 0.  The wait + barrier
+    // retires every earlier read of that buffer.
+    __builtin_amdgcn_s_waitcnt(0);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    const int64_t k0 = nfull * BK + chunk * 8;
 #pragma unroll
     for (int q = 0; q < NLD; ++q) {
+      const int c = (lane & 7) ^ ((4 * (q & 1) + (lane >> 4)) & 7);
       uint4 v = make_uint4(0, 0, 0, 0);
-      const char* g = gbase[NW == 8 ? gsel : (q >> 2)] + nfull * (BK * 2);
-      if (k0 < K) v = *reinterpret_cast<const uint4*>(g + goff[q]);
-      *reinterpret_cast<uint4*>(smem + lofs[q] + lane * 16) = v;
+      if (nfull * BK + c * 8 < K)
+        v = *reinterpret_cast<const uint4*>(gbase + nfull * kRow + goff[q]);
+      *reinterpret_cast<uint4*>(smem + lbase + q * 8 * kRow + lane * 16) = v;
     }
     __syncthreads();
-    frags(smem, 0, a0, b0);
-    frags(smem, 1, a1, b1);
-    mfma(a0, b0);
-    mfma(a1, b1);
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      if (kk * 16 >= krem) break;                // uniform: the rest of the stage is zeros
+      read_all(smem, kk, fa[0], fb[0]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < NJ; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[0][i], fb[0][j], acc[i][j], 0, 0, 0);
+    }
   }
 
-  // ---- epilogue: accumulator element v sits at row 8(v/4) + 4(lane/32) + v%4, col lane%32 ----
+  // ---- epilogue: the tile goes through LDS and leaves as whole-row 16-byte stores ----------
+  // Accumulator element v of block (i, j) sits at row 8 (v / 4) + 4 (lane / 32) + v % 4, column
+  // lane % 32 of that 32 x 32 block.  Rows are padded so that the two half-waves of a write
+  // (rows 4 apart) land 16 banks apart.
+  __syncthreads();                               // every wavefront is done with the operands
   char* Cp = reinterpret_cast<char*>(p.C);
+  const int64_t ldc = p.ldc;
+  if (!C_F32) {
+    char* wbase = smem + (wm * 128 + 4 * (lane >> 5)) * kPitch16 + (wn * 64 + (lane & 31)) * 2;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int64_t col = n0 + wn * WN + j * 32 + (lane & 31);
+      for (int j = 0; j < NJ; ++j)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int64_t row = m0 + wm * 128 + i * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-        if (row < m_end && col < n_end) {
-          if (C_F32)
-            reinterpret_cast<float*>(Cp)[row * p.ldc + col] = acc[i][j][v];
-          else
-            reinterpret_cast<uint16_t*>(Cp)[row * p.ldc + col] = (uint16_t)bf16_rne(acc[i][j][v]);
+        for (int v = 0; v < 16; ++v)
+          *reinterpret_cast<uint16_t*>(wbase + (i * 32 + 8 * (v >> 2) + (v & 3)) * kPitch16 +
+                                       j * 64) = (uint16_t)bf16_rne(acc[i][j][v]);
+    __syncthreads();
+    const int c8 = (tid & 31) * 8;
+    const int64_t gcol = n0 + c8;
+#pragma unroll 4
+    for (int it = 0; it < BM / 16; ++it) {
+      const int r = it * 16 + (tid >> 5);
+      const int64_t grow = m0 + r;
+      if (grow >= m_end || gcol >= n_end) continue;
+      const uint4 v = *reinterpret_cast<const uint4*>(smem + r * kPitch16 + c8 * 2);
+      uint16_t* dst = reinterpret_cast<uint16_t*>(Cp) + grow * ldc + gcol;
+      if (p.vec_store && gcol + 8 <= n_end) {
+        *reinterpret_cast<uint4*>(dst) = v;
+      } else {
+        const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+        for (int e = 0; e < 8 && gcol + e < n_end; ++e)
+          dst[e] = (uint16_t)(wv[e >> 1] >> (16 * (e & 1)));
+      }
+    }
+  } else {
+    // FP32 tile (256 KB) in two halves of 128 rows: the wavefronts with wm == h write half h.
+    char* wbase = smem + 4 * (lane >> 5) * kPitch32 + (wn * 64 + (lane & 31)) * 4;
+    const int c4 = (tid & 63) * 4;
+    const int64_t gcol = n0 + c4;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if (h) __syncthreads();                    // half 0 has been read out
+      if (wm == h) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < NJ; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+              *reinterpret_cast<float*>(wbase + (i * 32 + 8 * (v >> 2) + (v & 3)) * kPitch32 +
+                                        j * 128) = acc[i][j][v];
+      }
+      __syncthreads();
+#pragma unroll 4
+      for (int it = 0; it < 128 / 8; ++it) {
+        const int r = it * 8 + (tid >> 6);
+        const int64_t grow = m0 + h * 128 + r;
+        if (grow >= m_end || gcol >= n_end) continue;
+        const uint4 v = *reinterpret_cast<const uint4*>(smem + r * kPitch32 + c4 * 4);
+        float* dst = reinterpret_cast<float*>(Cp) + grow * ldc + gcol;
+        if (p.vec_store && gcol + 4 <= n_end) {
+          *reinterpret_cast<uint4*>(dst) = v;
+        } else {
+          const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+          for (int e = 0; e < 4 && gcol + e < n_end; ++e) dst[e] = __uint_as_float(wv[e]);
         }
       }
     }
   }
+}
+
+// The loads address a 256-row tile with 32-bit byte offsets from the tile's first row.
+bool nt_offsets_fit(int64_t K, int64_t lda, int64_t ldb) {
+  const int64_t lim = (int64_t)1 << 31;
+  return K * 2 < lim && (int64_t)BM * lda * 2 < lim && (int64_t)BN * ldb * 2 < lim;
+}
+
+int vec_store_ok(const void* C, int64_t ldc, int esize) {
+  return (reinterpret_cast<uintptr_t>(C) % 16 == 0) && ((ldc * esize) % 16 == 0);
 }
 
 }  // namespace
@@ -267,14 +366,16 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, in
                           const uint16_t* B, int64_t ldb, void* C, int64_t ldc, int c_f32,
                           hipStream_t s) {
   if (M == 0 || N == 0) return hipSuccess;
+  if (!nt_offsets_fit(K, lda, ldb)) return hipErrorInvalidValue;
   NtArgs a{};
   a.A = A; a.B = B; a.C = C; a.lda = lda; a.ldb = ldb; a.ldc = ldc;
   a.M = M; a.N = N; a.K = K;
+  a.vec_store = vec_store_ok(C, ldc, c_f32 ? 4 : 2);
   a.tiles_m = (int)((M + BM - 1) / BM);
   a.tiles_n = (int)((N + BN - 1) / BN);
   const dim3 grid((unsigned)(a.tiles_m * a.tiles_n));
-  if (c_f32) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, kNtWaves>), grid, dim3(kNtWaves * 64), 0, s, a);
-  else hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, kNtWaves>), grid, dim3(kNtWaves * 64), 0, s, a);
+  if (c_f32) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense>), grid, dim3(kWaves * 64), 0, s, a);
+  else hipLaunchKernelGGL((gemm_nt_kernel<false, kDense>), grid, dim3(kWaves * 64), 0, s, a);
   return hipGetLastError();
 }
 
@@ -283,13 +384,15 @@ hipError_t launch_grouped_nt_rows(int64_t E, int64_t T, int64_t N, int64_t K, co
                                   const uint16_t* B, int64_t ldb, int64_t bstride, uint16_t* C,
                                   int64_t ldc, hipStream_t s) {
   if (T == 0 || N == 0 || E == 0) return hipSuccess;
+  if (!nt_offsets_fit(K, lda, ldb)) return hipErrorInvalidValue;
   NtArgs a{};
   a.A = A; a.B = B; a.C = C; a.lda = lda; a.ldb = ldb; a.ldc = ldc; a.bstride = bstride;
   a.M = T; a.N = N; a.K = K; a.off = off; a.tile_start = tile_start; a.E = (int)E;
+  a.vec_store = vec_store_ok(C, ldc, 2);
   a.tiles_n = (int)((N + BN - 1) / BN);
   a.tiles_m = (int)((T + BM - 1) / BM + E);
   const dim3 grid((unsigned)(a.tiles_m * a.tiles_n));
-  hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRows, kNtWaves>), grid, dim3(kNtWaves * 64), 0, s, a);
+  hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRows>), grid, dim3(kWaves * 64), 0, s, a);
   return hipGetLastError();
 }
 
