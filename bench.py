@@ -3,16 +3,17 @@ forward + straight-through backward) on one MI355X.
 
 Workload (default): the 8B-class MLP up-projection with MXFP4 weights and activations,
 X [8192, 4096], W [14336, 4096], dY [8192, 14336] (seeded synthetic bf16, see workloads/).
-One step is the whole hot path, in the order the layer runs it:
+One step is the layer's two C-ABI calls, qf_qlinear_fwd then qf_qlinear_bwd_ste, which run
+the whole hot path:
     forward:  Q(W) -> W_hat, Q(X) -> X_hat (MXFP4 quantize-dequantize), Y = X_hat W_hat^T
-    backward: Q(W), Q(X) again (the quantized tensors are transient, as in the paper),
-              W_hat^T, X_hat^T, dY^T (transposes into the NT GEMM's operand form),
-              dX = dY W_hat, dW = dY^T X_hat (FP32)
+    backward: Q(W) -> W_hat^T and Q(X) -> X_hat^T (transposing quantizer: the quantized
+              tensors are transient, as in the paper), dY^T, dX = dY W_hat,
+              dW = dY^T X_hat (FP32); all three products are NT GEMMs
 `value` is the step's throughput in TFLOP/s over the three GEMMs' 3 * 2MNK flops, with the
-quantization time inside the step.  Each launch is bracketed by HIP events on the stream it
-runs on, which gives per-kernel durations for the roofline record.  The fake-quant kernel
-bandwidth is measured separately over rotating input buffers (>1 GB) so the 256 MB MALL
-cannot serve repeated reads.
+quantization time inside the step.  A second pass issues the same kernels one C-ABI call at a
+time, each bracketed by HIP events on the stream it runs on: that gives the per-kernel
+durations of the roofline record.  The fake-quant kernel bandwidth is measured separately
+over rotating input buffers (>1 GB) so the 256 MB MALL cannot serve repeated reads.
 
 Prints ONE JSON line.  Only --gpus 1 is supported.
 """
@@ -99,29 +100,52 @@ def main():
         return torch.from_numpy(a.view(np.int16)).to(dev)
 
     X, W, dY = up(w["X"]), up(w["W"]), up(w["dY"])
+    Y = torch.empty(M, N, dtype=torch.int16, device=dev)
+    dX = torch.empty(M, K, dtype=torch.int16, device=dev)
+    dW = torch.empty(N, K, dtype=torch.float32, device=dev)
+
+    # ---- the timed step: the layer's two C-ABI calls, forward then STE backward ------------
+    desc = qf.qlinear_desc(M, N, K, "mxfp4", "mxfp4")
+    ws = qf.workspace(desc)
+
+    def layer_step():
+        qf.qlinear_fwd(desc, X, W, Y, ws)
+        qf.qlinear_bwd_ste(desc, dY, X, W, dX, dW, ws)
+
+    for _ in range(args.warmup):
+        layer_step()
+    torch.cuda.synchronize()
+    sev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    t0 = time.perf_counter()
+    sev[0].record()
+    for i in range(args.steps):
+        layer_step()
+        sev[i + 1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    step_ms = [sev[i].elapsed_time(sev[i + 1]) for i in range(args.steps)]
+    ms_step = float(np.mean(step_ms))
+    gemm_flops = 2.0 * M * N * K
+    tflops = 3 * gemm_flops / (ms_step * 1e-3) / 1e12
+    del ws
+
+    # ---- per-launch breakdown: the same kernels the two calls issue, one C-ABI call each, so
+    # every launch is bracketed by HIP events on the stream it runs on ------------------------
     what = torch.empty(N, K, dtype=torch.int16, device=dev)
     xhat = torch.empty(M, K, dtype=torch.int16, device=dev)
     whatt = torch.empty(K, N, dtype=torch.int16, device=dev)
     xhatt = torch.empty(K, M, dtype=torch.int16, device=dev)
     dYt = torch.empty(N, M, dtype=torch.int16, device=dev)
-    Y = torch.empty(M, N, dtype=torch.int16, device=dev)
-    dX = torch.empty(M, K, dtype=torch.int16, device=dev)
-    dW = torch.empty(N, K, dtype=torch.float32, device=dev)
-
-    # The launches qf_qlinear_fwd + qf_qlinear_bwd_ste issue for this layer, one by one so
-    # each can be bracketed by events.  All three products run as NT GEMMs.
-    phases = ["quant_W", "quant_X", "gemm_fwd", "requant_W", "transpose_W_hat", "gemm_dX",
-              "requant_X", "transpose_X_hat", "transpose_dY", "gemm_dW"]
+    phases = ["quant_W", "quant_X", "gemm_fwd", "quant_W_transposed", "gemm_dX", "transpose_dY",
+              "quant_X_transposed", "gemm_dW"]
     calls = [
         lambda: qf.fakequant_mxfp4(W, None, None, what),
         lambda: qf.fakequant_mxfp4(X, None, None, xhat),
         lambda: qf.gemm_bf16(M, N, K, xhat, K, 1, what, K, 1, Y, N, 0),
-        lambda: qf.fakequant_mxfp4(W, None, None, what),
-        lambda: qf.transpose_bf16(what, whatt),
+        lambda: qf.fakequant_transposed(W, "mxfp4", whatt),
         lambda: qf.gemm_bf16(M, K, N, dY, N, 1, whatt, N, 1, dX, K, 0),
-        lambda: qf.fakequant_mxfp4(X, None, None, xhat),
-        lambda: qf.transpose_bf16(xhat, xhatt),
         lambda: qf.transpose_bf16(dY, dYt),
+        lambda: qf.fakequant_transposed(X, "mxfp4", xhatt),
         lambda: qf.gemm_bf16(N, K, M, dYt, M, 1, xhatt, M, 1, dW, K, 1),
     ]
 
@@ -136,25 +160,15 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(phases) + 1)]
               for _ in range(args.steps)]
+    for s_ in range(args.steps):
+        step(events[s_])
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for s in range(args.steps):
-        step(events[s])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
     per_phase = np.zeros(len(phases))
-    step_ms = []
     for ev in events:
-        d = [ev[i].elapsed_time(ev[i + 1]) for i in range(len(phases))]
-        per_phase += d
-        step_ms.append(ev[0].elapsed_time(ev[-1]))
+        per_phase += [ev[i].elapsed_time(ev[i + 1]) for i in range(len(phases))]
     per_phase /= args.steps
-    ms_step = float(np.mean(step_ms))
-    gemm_flops = 2.0 * M * N * K
-    tflops = 3 * gemm_flops / (ms_step * 1e-3) / 1e12
     gemm_ms = {p: float(per_phase[i]) for i, p in enumerate(phases) if p.startswith("gemm")}
     dom = max(gemm_ms, key=gemm_ms.get)
     achieved = gemm_flops / (gemm_ms[dom] * 1e-3) / 1e12
@@ -210,6 +224,7 @@ def main():
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic(dom), "traffic_unit": "bytes per launch"},
         "phases_ms": {p: round(float(per_phase[i]), 4) for i, p in enumerate(phases)},
+        "phases_sum_ms": round(float(per_phase.sum()), 4),
         "fakequant": {"kernel": "mxfp4 (codes+scales+x_hat)", "tensor": f"{N}x{K}",
                       "GBps": round(q_gbps, 1), "frac_hbm": round(q_gbps / PEAK_HBM_GBPS, 4),
                       "us": round(q_ms * 1e3, 2), "bytes_per_elem": 4.53125},

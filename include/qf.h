@@ -204,6 +204,20 @@ QF_API qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int6
                                      uint16_t* dX, float* dW, void* ws, size_t ws_bytes,
                                      qf_stream_t stream);
 
+/*
+ * qf_fakequant_transposed -- quantize + dequantize with transposed output: out[k][r] =
+ * x_hat[r][k], the x_hat of qf_fakequant_nvfp4 / _mxfp4 / _q4k bit for bit (same per-block
+ * equations; blocks run along the rows of x).  The backward of the layer uses it to produce
+ * W_hat^T and A_hat^T, the NT-form operands of dX and dW, in one pass.
+ *   fmt   QF_FMT_NVFP4, QF_FMT_MXFP4 or QF_FMT_Q4K.
+ *   x     bf16 [R, K] (row stride ldx); R % 8 == 0; K a multiple of the format block.
+ *   amax  NVFP4: device FP32 tensor amax g, read only (required); ignored otherwise.
+ *   out   bf16 [K, R] with row stride ldo >= R (ldo % 8 == 0), 16-byte aligned.
+ */
+QF_API qf_status qf_fakequant_transposed(int fmt, const uint16_t* x, int64_t R, int64_t K,
+                                         int64_t ldx, const float* amax, uint16_t* out,
+                                         int64_t ldo, qf_stream_t stream);
+
 /* ---------------------------------------------------------------------------------------
  * Plain BF16 GEMMs on the same MFMA kernels (building blocks of the layer calls above)
  * ------------------------------------------------------------------------------------ */

@@ -80,6 +80,8 @@ def lib() -> ctypes.CDLL:
             "qf_gemm_bf16": ([_I, _I, _I, _P, _I, ctypes.c_int, _P, _I, ctypes.c_int, _P, _I,
                               ctypes.c_int, _P], ctypes.c_int),
             "qf_transpose_bf16": ([_P, _I, _I, _I, _P, _I, _P], ctypes.c_int),
+            "qf_fakequant_transposed": ([ctypes.c_int, _P, _I, _I, _I, _P, _P, _I, _P],
+                                        ctypes.c_int),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -149,6 +151,16 @@ def fakequant_mxfp4(x, codes=None, scales=None, xhat=None):
 def fakequant_q4k(x, packed=None, xhat=None):
     R, K, ld = _rows(_bf16(x))
     _check(lib().qf_fakequant_q4k(_ptr(x), R, K, ld, _ptr(packed), _ptr(xhat), _stream()))
+
+
+def fakequant_transposed(x, fmt, out, amax=None):
+    """out[k][r] = x_hat[r][k] for x [R, K]; out is a [K, >=R] row-contiguous bf16 tensor."""
+    R, K, ld = _rows(_bf16(x))
+    if out.dim() != 2 or out.shape[0] != K or out.shape[1] < R or out.stride(1) != 1:
+        raise ValueError("out must be a [K, >=R] row-contiguous tensor")
+    _check(lib().qf_fakequant_transposed(FMT[fmt], _ptr(x), R, K, ld, _ptr(amax),
+                                         _ptr(_bf16(out)), out.stride(0), _stream()))
+    return out
 
 
 # --------------------------------------------------------------------------- linear layer

@@ -260,6 +260,23 @@ qf_status qf_fakequant_q4k(const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
   return ok();
 }
 
+qf_status qf_fakequant_transposed(int fmt, const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
+                                  const float* amax, uint16_t* out, int64_t ldo,
+                                  qf_stream_t stream) {
+  const char* fn = "qf_fakequant_transposed";
+  if (fmt != QF_FMT_NVFP4 && fmt != QF_FMT_MXFP4 && fmt != QF_FMT_Q4K)
+    return fail(QF_EINVAL, "%s: bad format %d", fn, fmt);
+  QF_TRY(check_quant_input(fn, x, R, K, ldx, block_of(fmt)));
+  if (R % 8) return fail(QF_ESHAPE, "%s: R=%lld is not a multiple of 8", fn, (long long)R);
+  if (R == 0 || K == 0) return ok();
+  if (fmt == QF_FMT_NVFP4 && !amax) return fail(QF_EINVAL, "%s: NVFP4 needs amax", fn);
+  if (!out) return fail(QF_EINVAL, "%s: null output", fn);
+  QF_TRY(check_mat("qf_fakequant_transposed: out", out, K, R, ldo, true));
+  QF_TRY(dev(qf::launch_quant_t(fmt, x, R, K, ldx, 1, 0, amax, out, ldo, 0, S(stream)),
+             "quantize (transposed)"));
+  return ok();
+}
+
 qf_status qf_workspace_size(const qf_qlinear_desc* d, size_t* bytes) {
   Dims dm;
   QF_TRY(check_desc("qf_workspace_size", d, &dm));
@@ -302,25 +319,46 @@ qf_status qf_qlinear_bwd_ste(const qf_qlinear_desc* d, const uint16_t* dY, const
   const bool reuse = (d->flags & QF_FLAG_REUSE_WS) != 0;
   const uint16_t *Wop, *Aop;
   int64_t ldw_op, lda_op;
-  QF_TRY(quantize_operands(d, dm, X, W, w, !reuse && dX != nullptr, !reuse && dW != nullptr,
-                           &Wop, &ldw_op, &Aop, &lda_op, s));
   if (d->M % 8 == 0) {
-    // NT form: transposed operands through the workspace.
+    // NT form: transposed operands through the workspace.  Without saved x_hat operands the
+    // transposed ones come straight from the transposing quantizer (one pass over W and X).
     if (dX) {  // dX[M, K] = dY[M, N] (W_hat^T)[K, N]^T
-      QF_TRY(dev(qf::launch_transpose_bf16(Wop, d->N, d->K, ldw_op, w.whatt, d->N, 1, 0, 0, s),
-                 "transpose W_hat"));
+      if (d->wfmt != QF_FMT_NONE && !reuse) {
+        const float* g = d->w_amax;
+        if (d->wfmt == QF_FMT_NVFP4 && !g) {
+          QF_TRY(dev(qf::launch_fill_f32(w.scal, 1, 0.0f, s), "amax init"));
+          QF_TRY(dev(qf::launch_amax(W, d->N, d->K, dm.ldw, w.scal, s), "amax"));
+          g = w.scal;
+        }
+        QF_TRY(dev(qf::launch_quant_t(d->wfmt, W, d->N, d->K, dm.ldw, 1, 0, g, w.whatt, d->N, 0,
+                                      s), "quantize W (transposed)"));
+      } else {
+        const uint16_t* src = d->wfmt != QF_FMT_NONE ? w.what : W;
+        const int64_t ld = d->wfmt != QF_FMT_NONE ? d->K : dm.ldw;
+        QF_TRY(dev(qf::launch_transpose_bf16(src, d->N, d->K, ld, w.whatt, d->N, 1, 0, 0, s),
+                   "transpose W_hat"));
+      }
       QF_TRY(dev(qf::launch_gemm_nt(d->M, d->K, d->N, dY, dm.ldy, w.whatt, d->N, dX, dm.ldx, 0, s),
                  "dX gemm"));
     }
     if (dW) {  // dW[N, K] = (dY^T)[N, M] (A_hat^T)[K, M]^T
       QF_TRY(dev(qf::launch_transpose_bf16(dY, d->M, d->N, dm.ldy, w.dyt, d->M, 1, 0, 0, s),
                  "transpose dY"));
-      QF_TRY(dev(qf::launch_transpose_bf16(Aop, d->M, d->K, lda_op, w.ahatt, d->M, 1, 0, 0, s),
-                 "transpose A_hat"));
+      if (d->afmt != QF_FMT_NONE && !reuse) {
+        QF_TRY(dev(qf::launch_quant_t(d->afmt, X, d->M, d->K, dm.ldx, 1, 0, d->a_amax, w.ahatt,
+                                      d->M, 0, s), "quantize X (transposed)"));
+      } else {
+        const uint16_t* src = d->afmt != QF_FMT_NONE ? w.ahat : X;
+        const int64_t ld = d->afmt != QF_FMT_NONE ? d->K : dm.ldx;
+        QF_TRY(dev(qf::launch_transpose_bf16(src, d->M, d->K, ld, w.ahatt, d->M, 1, 0, 0, s),
+                   "transpose A_hat"));
+      }
       QF_TRY(dev(qf::launch_gemm_nt(d->N, d->K, d->M, w.dyt, d->M, w.ahatt, d->M, dW, d->K, 1, s),
                  "dW gemm"));
     }
   } else {
+    QF_TRY(quantize_operands(d, dm, X, W, w, !reuse && dX != nullptr, !reuse && dW != nullptr,
+                             &Wop, &ldw_op, &Aop, &lda_op, s));
     // M not a multiple of 8: the generic kernel reads the [M, *] operands directly.
     if (dX) {
       QF_TRY(dev(qf::launch_gemm(d->M, d->K, d->N, dY, dm.ldy, 1, Wop, ldw_op, 0, dX, dm.ldx, 0, s),
@@ -460,13 +498,27 @@ qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int64_t* gr
   hipStream_t s = S(stream);
   GroupedWs g = grouped_ws(d, ws);
   const bool reuse = (d->flags & QF_FLAG_REUSE_WS) != 0;
+  // Without a saved W_hat, the experts' W_hat^T comes straight from the transposing quantizer.
+  const bool fuse_w = dX && d->wfmt != QF_FMT_NONE && !reuse;
   const uint16_t *Wop, *Aop;
-  QF_TRY(grouped_quantize(d, X, W, g, !reuse && dX, !reuse && dW, &Wop, &Aop, s));
+  QF_TRY(grouped_quantize(d, X, W, g, !reuse && dX && !fuse_w, !reuse && dW, &Wop, &Aop, s));
   QF_TRY(dev(qf::launch_grouped_prep(group_offsets, d->E, g.tile_start, g.order, s), "prep"));
   if (dX) {
-    QF_TRY(dev(qf::launch_transpose_bf16(Wop, d->N, d->K, d->K, g.whatt, d->N, d->E, d->N * d->K,
-                                         d->N * d->K, s),
-               "transpose expert W_hat"));
+    if (fuse_w) {
+      const float* gp = d->w_amax;
+      if (d->wfmt == QF_FMT_NVFP4 && !gp) {
+        QF_TRY(dev(qf::launch_fill_f32(g.wamax, d->E, 0.0f, s), "amax init"));
+        QF_TRY(dev(qf::launch_amax_batched(W, d->E, d->N, d->K, g.wamax, s), "amax"));
+        gp = g.wamax;
+      }
+      QF_TRY(dev(qf::launch_quant_t(d->wfmt, W, d->N, d->K, d->K, d->E, d->N * d->K, gp, g.whatt,
+                                    d->N, d->N * d->K, s),
+                 "quantize expert W (transposed)"));
+    } else {
+      QF_TRY(dev(qf::launch_transpose_bf16(Wop, d->N, d->K, d->K, g.whatt, d->N, d->E,
+                                           d->N * d->K, d->N * d->K, s),
+                 "transpose expert W_hat"));
+    }
     QF_TRY(dev(qf::launch_grouped_nt_rows(d->E, d->T, d->K, d->N, group_offsets, g.tile_start, dY,
                                           d->N, g.whatt, d->N, d->N * d->K, dX, d->K, s),
                "grouped dX"));

@@ -27,6 +27,13 @@ hipError_t launch_amax_batched(const uint16_t* x, int64_t E, int64_t R, int64_t 
 hipError_t launch_nvfp4_batched(const uint16_t* x, int64_t E, int64_t R, int64_t K,
                                 const float* g, uint16_t* xhat, hipStream_t s);
 
+// Quantize-dequantize with transposed output: out[k][r] = x_hat[r][k] (bf16, row stride ldo)
+// for `batch` tensors spaced xbs / obs elements apart (NVFP4: tensor amax g[z] per tensor).
+// R and K multiples of 8, K a multiple of the format block.
+hipError_t launch_quant_t(int fmt, const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
+                          int64_t batch, int64_t xbs, const float* g, uint16_t* out, int64_t ldo,
+                          int64_t obs, hipStream_t s);
+
 // ---- GEMMs (qf_gemm.hip) ------------------------------------------------------------------
 // C[M,N] = sum_k A(m,k) B(n,k).  a_kmajor: A stored [M][K] (else [K][M]); likewise B.
 hipError_t launch_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,

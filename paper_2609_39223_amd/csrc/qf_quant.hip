@@ -15,6 +15,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "qf.h"
 #include "qf_internal.h"
 
 namespace qf {
@@ -169,6 +170,116 @@ __global__ __launch_bounds__(kThreads) void amax_kernel(const uint16_t* __restri
   }
 }
 
+// ======================================================================= per-chunk codecs
+// Each function quantizes and dequantizes this lane's 8 elements h[] (bf16 bits); the lanes
+// of one format block must run it together (cross-lane reductions).
+
+// NVFP4 (16-block = this lane and lane ^ 1): 4-bit codes cw (element k in nibble k), E4M3
+// block scale sc, x_hat bits xh.  S is the FP32 tensor scale g / (6 * 448), six_s = 6 S.
+__device__ __forceinline__ void nvfp4_chunk(const uint32_t h[8], float S, float six_s,
+                                            uint32_t& cw, uint32_t& sc, uint32_t xh[8]) {
+  uint32_t ab = max_abs_bits8(h);
+  const uint32_t o = xor1_u32(ab);         // partner lane holds the other 8 of the 16-block
+  ab = o > ab ? o : ab;
+  sc = 0;
+  if (S != 0.0f) {
+    const float t = as_f32(ab << 16) / six_s;   // t_b = a_b / (6 S)
+    sc = e4m3_code(t);
+  }
+  const float D = S * e4m3_value(sc);       // block decode scale s_FP32 * s_E4M3,b
+  const float rcp = D != 0.0f ? 1.0f / D : 0.0f;
+  cw = 0;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const uint32_t sign = h[k] >> 15;
+    uint32_t m = 0;
+    if (D != 0.0f) m = e2m1_code(as_f32((h[k] & 0x7FFFu) << 16) * rcp);
+    cw |= ((sign << 3) | m) << (4 * k);
+    const float mag = e2m1_value(m) * D;
+    xh[k] = bf16_rne(sign ? -mag : mag);
+  }
+}
+
+// MXFP4 (32-block = the 4 lanes of a quad): codes cw, E8M0 scale code e (0xFF for a block
+// holding Inf / NaN, whose x_hat is NaN and codes 0), x_hat bits xh.
+__device__ __forceinline__ void mxfp4_chunk(const uint32_t h[8], uint32_t& cw, uint32_t& scale,
+                                            uint32_t xh[8]) {
+  uint32_t ab = max_abs_bits8(h);
+  uint32_t o = xor1_u32(ab);
+  ab = o > ab ? o : ab;
+  o = xor2_u32(ab);
+  ab = o > ab ? o : ab;                     // max |x| of the 32-block (4 lanes)
+  const bool nonfinite = ab >= 0x7F80u;     // Inf or NaN somewhere in the block
+  const uint32_t E = ab >> 7;               // biased exponent of the block max
+  const uint32_t e = E >= 2u ? E - 2u : 0u; // scale code: floor(log2 a) - 2, clamped
+  const float up = as_f32((254u - e) << 23);  // 2^(127 - e): divides by the scale exactly
+  cw = 0;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const uint32_t sign = h[k] >> 15;
+    const uint32_t m = e2m1_code(as_f32((h[k] & 0x7FFFu) << 16) * up);
+    // x_hat = +-V(m) * 2^(e-127) written directly as bf16 bits
+    uint32_t b;
+    if (m == 0u) b = 0u;
+    else if (e < 2u && m < 4u) b = m << (e + 5u);             // bf16 subnormal range
+    else b = (e << 7) - 128u + (m >= 2u ? 64u * m : 0u);
+    cw |= ((sign << 3) | m) << (4 * k);
+    xh[k] = b | (sign << 15);
+  }
+  scale = e;
+  if (nonfinite) {
+    cw = 0;
+    scale = 0xFFu;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) xh[k] = 0x7FC0u;
+  }
+}
+
+// Q4_K (32 lanes per 256-element super-block; lane L holds elements 8L..8L+7, sub-block L/4):
+// FP16 bits of d and dmin, this sub-block's 6-bit scale / min, the 4-bit codes of this
+// lane (qlo: elements 0-3, qhi: 4-7, one per byte) and x_hat bits xh.
+struct Q4kChunk {
+  uint32_t dh, mh, ls, lm, qlo, qhi;
+};
+__device__ __forceinline__ void q4k_chunk(const uint32_t h[8], Q4kChunk& r, uint32_t xh[8]) {
+  float xv[8];
+  float lo = 0.0f, hi = -__builtin_huge_valf();
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    xv[k] = as_f32(h[k] << 16) + 0.0f;      // signed zeros count as +0
+    lo = fminf(lo, xv[k]);
+    hi = fmaxf(hi, xv[k]);
+  }
+  lo = fminf(lo, xor1_f(lo)); hi = fmaxf(hi, xor1_f(hi));
+  lo = fminf(lo, xor2_f(lo)); hi = fmaxf(hi, xor2_f(hi));
+  const float a = (hi - lo) / 15.0f;        // step of the sub-block
+  const float mu = 0.0f - lo;               // offset (subtracted), never negative
+  float A = a, Mx = mu;
+  A = fmaxf(A, xor_swz_f<4>(A)); Mx = fmaxf(Mx, xor_swz_f<4>(Mx));
+  A = fmaxf(A, xor_swz_f<8>(A)); Mx = fmaxf(Mx, xor_swz_f<8>(Mx));
+  A = fmaxf(A, xor_swz_f<16>(A)); Mx = fmaxf(Mx, xor_swz_f<16>(Mx));
+  r.dh = f16_rne_sat(A / 63.0f);
+  r.mh = f16_rne_sat(Mx / 63.0f);
+  const float d = f16_value(r.dh), dmin = f16_value(r.mh);
+  r.ls = 0;
+  r.lm = 0;
+  if (d != 0.0f) r.ls = (uint32_t)fminf(fmaxf(__builtin_rintf(a / d), 0.0f), 63.0f);
+  if (dmin != 0.0f) r.lm = (uint32_t)fminf(fmaxf(__builtin_rintf(mu / dmin), 0.0f), 63.0f);
+  const float t1 = d * (float)r.ls;
+  const float t2 = dmin * (float)r.lm;
+  r.qlo = 0;
+  r.qhi = 0;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    uint32_t q = 0;
+    if (t1 != 0.0f) q = (uint32_t)fminf(fmaxf(__builtin_rintf((xv[k] + t2) / t1), 0.0f), 15.0f);
+    if (k < 4) r.qlo |= q << (8 * k);
+    else r.qhi |= q << (8 * (k - 4));
+    const float prod = t1 * (float)q;
+    xh[k] = bf16_rne(prod - t2);
+  }
+}
+
 // ============================================================================= NVFP4
 // grid.z indexes batched tensors (expert weights): tensor z uses g[z] and element offset
 // z * tstride (input) / z * R * K (outputs).
@@ -193,28 +304,9 @@ __global__ __launch_bounds__(kThreads) void nvfp4_kernel(
     const bool ok = col_ok && r < R;
     uint4 v = make_uint4(0, 0, 0, 0);
     if (ok) v = *reinterpret_cast<const uint4*>(xt + r * ldx + c * 8);
-    uint32_t h[8];
+    uint32_t h[8], cw, sc, xh[8];
     unpack8(v, h);
-    uint32_t ab = max_abs_bits8(h);
-    uint32_t o = xor1_u32(ab);              // partner lane holds the other 8 of the 16-block
-    ab = o > ab ? o : ab;
-    uint32_t sc = 0;
-    if (S != 0.0f) {
-      float t = as_f32(ab << 16) / six_s;   // t_b = a_b / (6 S)
-      sc = e4m3_code(t);
-    }
-    const float D = S * e4m3_value(sc);     // block decode scale s_FP32 * s_E4M3,b
-    const float rcp = D != 0.0f ? 1.0f / D : 0.0f;
-    uint32_t cw = 0, xh[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const uint32_t sign = h[k] >> 15;
-      uint32_t m = 0;
-      if (D != 0.0f) m = e2m1_code(as_f32((h[k] & 0x7FFFu) << 16) * rcp);
-      cw |= ((sign << 3) | m) << (4 * k);
-      const float mag = e2m1_value(m) * D;
-      xh[k] = bf16_rne(sign ? -mag : mag);
-    }
+    nvfp4_chunk(h, S, six_s, cw, sc, xh);
     if (ok) {
       if (codes) *reinterpret_cast<uint32_t*>(codes + obase / 2 + r * (K / 2) + c * 4) = cw;
       if (scales && (c & 1) == 0) scales[obase / 16 + r * (K / 16) + c / 2] = (uint8_t)sc;
@@ -237,38 +329,12 @@ __global__ __launch_bounds__(kThreads) void mxfp4_kernel(
     const bool ok = col_ok && r < R;
     uint4 v = make_uint4(0, 0, 0, 0);
     if (ok) v = *reinterpret_cast<const uint4*>(x + r * ldx + c * 8);
-    uint32_t h[8];
+    uint32_t h[8], cw, e, xh[8];
     unpack8(v, h);
-    uint32_t ab = max_abs_bits8(h);
-    uint32_t o = xor1_u32(ab);
-    ab = o > ab ? o : ab;
-    o = xor2_u32(ab);
-    ab = o > ab ? o : ab;                   // max |x| of the 32-block (4 lanes)
-    const bool nonfinite = ab >= 0x7F80u;   // Inf or NaN somewhere in the block
-    const uint32_t E = ab >> 7;             // biased exponent of the block max
-    const uint32_t e = E >= 2u ? E - 2u : 0u;   // scale code: floor(log2 a) - 2, clamped
-    const float up = as_f32((254u - e) << 23);  // 2^(127 - e): divides by the scale exactly
-    uint32_t cw = 0, xh[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const uint32_t sign = h[k] >> 15;
-      const uint32_t m = e2m1_code(as_f32((h[k] & 0x7FFFu) << 16) * up);
-      // x_hat = +-V(m) * 2^(e-127) written directly as bf16 bits
-      uint32_t b;
-      if (m == 0u) b = 0u;
-      else if (e < 2u && m < 4u) b = m << (e + 5u);             // bf16 subnormal range
-      else b = (e << 7) - 128u + (m >= 2u ? 64u * m : 0u);
-      cw |= ((sign << 3) | m) << (4 * k);
-      xh[k] = b | (sign << 15);
-    }
-    if (nonfinite) {
-      cw = 0;
-#pragma unroll
-      for (int k = 0; k < 8; ++k) xh[k] = 0x7FC0u;
-    }
+    mxfp4_chunk(h, cw, e, xh);
     if (ok) {
       if (codes) *reinterpret_cast<uint32_t*>(codes + r * (K / 2) + c * 4) = cw;
-      if (scales && (c & 3) == 0) scales[r * (K / 32) + c / 4] = (uint8_t)(nonfinite ? 0xFFu : e);
+      if (scales && (c & 3) == 0) scales[r * (K / 32) + c / 4] = (uint8_t)e;
       if (xhat) *reinterpret_cast<uint4*>(xhat + r * K + c * 8) = pack8(xh);
     }
   }
@@ -294,42 +360,11 @@ __global__ __launch_bounds__(kThreads) void q4k_kernel(const uint16_t* __restric
     const bool ok = col_ok && r < R;
     uint4 v = make_uint4(0, 0, 0, 0);
     if (ok) v = *reinterpret_cast<const uint4*>(x + r * ldx + c * 8);
-    uint32_t h[8];
+    uint32_t h[8], xh[8];
     unpack8(v, h);
-    float xv[8];
-    float lo = 0.0f, hi = -__builtin_huge_valf();
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      xv[k] = as_f32(h[k] << 16) + 0.0f;    // signed zeros count as +0
-      lo = fminf(lo, xv[k]);
-      hi = fmaxf(hi, xv[k]);
-    }
-    lo = fminf(lo, xor1_f(lo)); hi = fmaxf(hi, xor1_f(hi));
-    lo = fminf(lo, xor2_f(lo)); hi = fmaxf(hi, xor2_f(hi));
-    const float a = (hi - lo) / 15.0f;      // step of the sub-block
-    const float mu = 0.0f - lo;             // offset (subtracted), never negative
-    float A = a, Mx = mu;
-    A = fmaxf(A, xor_swz_f<4>(A)); Mx = fmaxf(Mx, xor_swz_f<4>(Mx));
-    A = fmaxf(A, xor_swz_f<8>(A)); Mx = fmaxf(Mx, xor_swz_f<8>(Mx));
-    A = fmaxf(A, xor_swz_f<16>(A)); Mx = fmaxf(Mx, xor_swz_f<16>(Mx));
-    const uint32_t dh = f16_rne_sat(A / 63.0f);
-    const uint32_t mh = f16_rne_sat(Mx / 63.0f);
-    const float d = f16_value(dh), dmin = f16_value(mh);
-    uint32_t ls = 0, lm = 0;
-    if (d != 0.0f) ls = (uint32_t)fminf(fmaxf(__builtin_rintf(a / d), 0.0f), 63.0f);
-    if (dmin != 0.0f) lm = (uint32_t)fminf(fmaxf(__builtin_rintf(mu / dmin), 0.0f), 63.0f);
-    const float t1 = d * (float)ls;
-    const float t2 = dmin * (float)lm;
-    uint32_t qlo = 0, qhi = 0, xh[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      uint32_t q = 0;
-      if (t1 != 0.0f) q = (uint32_t)fminf(fmaxf(__builtin_rintf((xv[k] + t2) / t1), 0.0f), 15.0f);
-      if (k < 4) qlo |= q << (8 * k);
-      else qhi |= q << (8 * (k - 4));
-      const float prod = t1 * (float)q;
-      xh[k] = bf16_rne(prod - t2);
-    }
+    Q4kChunk q;
+    q4k_chunk(h, q, xh);
+    const uint32_t ls = q.ls, lm = q.lm, qlo = q.qlo, qhi = q.qhi, dh = q.dh, mh = q.mh;
     // gather the eight 6-bit scales / mins at lane 0 of the super-block
     uint32_t LS[8], LM[8];
     const int base = (threadIdx.x & 63) & ~31;
@@ -364,6 +399,79 @@ __global__ __launch_bounds__(kThreads) void q4k_kernel(const uint16_t* __restric
       }
     }
     if (ok && xhat) *reinterpret_cast<uint4*>(xhat + r * K + c * 8) = pack8(xh);
+  }
+}
+
+// ===================================================== quantize-dequantize, transposed output
+// out[k][r] = x_hat[r][k]: the backward's NT GEMMs take W_hat^T and A_hat^T, which this
+// writes in one pass instead of x_hat followed by a transpose.  A block quantizes a 64 x 256
+// tile (thread t: row 8 i + t / 32, chunk t % 32, so each 32-lane half-wave holds one full
+// 256-element row -- every format block, the Q4_K super-block included, stays inside one
+// half-wave), parks x_hat in LDS (chunk c of row r at slot c ^ (((r >> 3) & 7) << 1)), then
+// every lane transposes an 8 x 8 block in registers and writes 8 output rows of 16 bytes.
+// grid.z indexes batched tensors; NVFP4 tensor z uses the tensor amax g[z].  R and K are
+// multiples of 8; K a multiple of the format block.
+constexpr int kTR = 64, kTC = 256;
+
+__device__ __forceinline__ int tslot(int r, int c) { return c ^ (((r >> 3) & 7) << 1); }
+
+template <int FMT>
+__global__ __launch_bounds__(kThreads) void quant_t_kernel(const uint16_t* __restrict__ x,
+                                                           int64_t R, int64_t K, int64_t ldx,
+                                                           int64_t xbs, const float* __restrict__ g,
+                                                           uint16_t* __restrict__ out,
+                                                           int64_t ldo, int64_t obs) {
+  __shared__ uint4 tile[kTR * (kTC / 8)];
+  const int t = threadIdx.x;
+  const int64_t r0 = (int64_t)blockIdx.y * kTR, c0 = (int64_t)blockIdx.x * kTC;
+  x += (int64_t)blockIdx.z * xbs;
+  out += (int64_t)blockIdx.z * obs;
+  float S = 0.0f, six_s = 0.0f;
+  if (FMT == QF_FMT_NVFP4) {
+    S = g[blockIdx.z] / 2688.0f;            // g maps to 6 * 448
+    six_s = 6.0f * S;
+  }
+#pragma unroll 2
+  for (int i = 0; i < 8; ++i) {
+    const int row = i * 8 + (t >> 5), cc = t & 31;
+    const int64_t gr = r0 + row, gc = c0 + cc * 8;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (gr < R && gc < K) v = *reinterpret_cast<const uint4*>(x + gr * ldx + gc);
+    uint32_t h[8], xh[8];
+    unpack8(v, h);
+    if (FMT == QF_FMT_NVFP4) {
+      uint32_t cw, sc;
+      nvfp4_chunk(h, S, six_s, cw, sc, xh);
+    } else if (FMT == QF_FMT_MXFP4) {
+      uint32_t cw, e;
+      mxfp4_chunk(h, cw, e, xh);
+    } else {
+      Q4kChunk q;
+      q4k_chunk(h, q, xh);
+    }
+    tile[row * 32 + tslot(row, cc)] = pack8(xh);
+  }
+  __syncthreads();
+  const int rb = t & 7, cb = t >> 3;
+  uint32_t w[8][4];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int row = rb * 8 + i;
+    const uint4 v = tile[row * 32 + tslot(row, cb)];
+    w[i][0] = v.x; w[i][1] = v.y; w[i][2] = v.z; w[i][3] = v.w;
+  }
+  const int64_t orow0 = c0 + cb * 8, ocol = r0 + rb * 8;
+  if (ocol >= R) return;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    if (orow0 + j >= K) break;
+    uint32_t o[4];
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      const uint32_t lo = w[2 * d][j >> 1], hi = w[2 * d + 1][j >> 1];
+      o[d] = (j & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
+    }
+    *reinterpret_cast<uint4*>(out + (orow0 + j) * ldo + ocol) = make_uint4(o[0], o[1], o[2], o[3]);
   }
 }
 
@@ -446,6 +554,31 @@ hipError_t launch_q4k(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, uint
   if (R == 0 || K == 0) return hipSuccess;
   hipLaunchKernelGGL(q4k_kernel<2>, row_grid(R, K, 2), dim3(kThreads), 0, s, x, R, K, ldx,
                      packed, xhat);
+  return hipGetLastError();
+}
+
+hipError_t launch_quant_t(int fmt, const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
+                          int64_t batch, int64_t xbs, const float* g, uint16_t* out, int64_t ldo,
+                          int64_t obs, hipStream_t s) {
+  if (R == 0 || K == 0 || batch == 0) return hipSuccess;
+  const dim3 grid((unsigned)((K + kTC - 1) / kTC), (unsigned)((R + kTR - 1) / kTR),
+                  (unsigned)batch);
+  switch (fmt) {
+    case QF_FMT_NVFP4:
+      hipLaunchKernelGGL(quant_t_kernel<QF_FMT_NVFP4>, grid, dim3(kThreads), 0, s, x, R, K, ldx,
+                         xbs, g, out, ldo, obs);
+      break;
+    case QF_FMT_MXFP4:
+      hipLaunchKernelGGL(quant_t_kernel<QF_FMT_MXFP4>, grid, dim3(kThreads), 0, s, x, R, K, ldx,
+                         xbs, g, out, ldo, obs);
+      break;
+    case QF_FMT_Q4K:
+      hipLaunchKernelGGL(quant_t_kernel<QF_FMT_Q4K>, grid, dim3(kThreads), 0, s, x, R, K, ldx,
+                         xbs, g, out, ldo, obs);
+      break;
+    default:
+      return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

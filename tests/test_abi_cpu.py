@@ -64,6 +64,15 @@ def test_quantizer_validation(L):
     h = L.qf_fakequant_q4k
     assert h(P(256), I64(4), I64(128), I64(128), None, None, None) == QF_ESHAPE
     assert h(P(256), I64(4), I64(256), I64(256), P(7), None, None) == QF_EALIGN
+    t = L.qf_fakequant_transposed
+    t.argtypes = [ctypes.c_int, P, I64, I64, I64, P, P, I64, P]
+    assert t(0, P(256), 8, 64, 64, None, P(256), 8, None) == QF_EINVAL         # format NONE
+    assert t(2, P(256), 12, 64, 64, None, P(256), 16, None) == QF_ESHAPE       # R % 8
+    assert t(2, P(256), 8, 48, 48, None, P(256), 8, None) == QF_ESHAPE         # K % 32
+    assert t(1, P(256), 8, 64, 64, None, P(256), 8, None) == QF_EINVAL         # NVFP4 amax
+    assert t(2, P(256), 8, 64, 64, None, None, 8, None) == QF_EINVAL           # no output
+    assert t(2, P(256), 8, 64, 64, None, P(256), 4, None) == QF_ESHAPE         # ldo < R
+    assert t(3, P(256), 8, 256, 256, None, P(264), 8, None) == QF_EALIGN       # out alignment
 
 
 class Desc(ctypes.Structure):

@@ -21,7 +21,7 @@ def qf():
     return qf
 
 
-def run_grouped(qf, offsets, X, W, dY, wfmt, afmt):
+def run_grouped(qf, offsets, X, W, dY, wfmt, afmt, reuse=False):
     E, N, K = W.shape
     T = X.shape[0]
     d = qf.grouped_desc(E, T, N, K, wfmt, afmt)
@@ -31,6 +31,8 @@ def run_grouped(qf, offsets, X, W, dY, wfmt, afmt):
     Y, dX = empty_bf16((T, N)), empty_bf16((T, K))
     dW = torch.full((E, N, K), 7.0, dtype=torch.float32, device="cuda")
     qf.qlinear_grouped_fwd(d, off, Xd, Wd, Y, ws)
+    if reuse:
+        d = qf.grouped_desc(E, T, N, K, wfmt, afmt, flags=qf.FLAG_REUSE_WS)
     qf.qlinear_grouped_bwd_ste(d, off, dYd, Xd, Wd, dX, dW, ws)
     torch.cuda.synchronize()
     return from_dev(Y), from_dev(dX), from_dev(dW)
@@ -77,3 +79,21 @@ def test_grouped_zipf_routing_sampled(qf):
         assert_close(bf16_to_f64(Y[r0:r1]), oracle.linear_fwd(X[r0:r1], what), f"Y e={e}")
         assert_close(bf16_to_f64(dX[r0:r1]), oracle.linear_dx(dY[r0:r1], what), f"dX e={e}")
         assert_close(dW[e].astype(np.float64), oracle.linear_dw(dY[r0:r1], X[r0:r1]), f"dW e={e}")
+
+
+@pytest.mark.parametrize("wfmt", ["nvfp4", "mxfp4", "q4k"])
+def test_grouped_transposing_quantizer_matches_saved_operands(qf, wfmt):
+    """Expert W_hat^T straight from the transposing quantizer (per-expert NVFP4 scales) equals
+    transposing the forward's saved W_hat: bit-identical dX."""
+    rng = np.random.default_rng(13)
+    E, N, K = 4, 136, 768
+    counts = np.array([70, 0, 258, 9])
+    offsets = np.concatenate([[0], np.cumsum(counts)])
+    T = int(offsets[-1])
+    X = workloads.normal_bf16(rng, (T, K))
+    W = np.stack([workloads.normal_bf16(rng, (N, K), 0.02 * (e + 1)) for e in range(E)])
+    dY = workloads.normal_bf16(rng, (T, N))
+    _, dX, dW = run_grouped(qf, offsets, X, W, dY, wfmt, "none")
+    _, dX2, dW2 = run_grouped(qf, offsets, X, W, dY, wfmt, "none", reuse=True)
+    assert np.array_equal(dX.view(np.uint16), dX2.view(np.uint16))
+    assert np.array_equal(dW.view(np.uint32), dW2.view(np.uint32))

@@ -235,3 +235,25 @@ def test_nt_gemm_pipeline_depths(qf):
         assert_close(from_dev(C).astype(np.float64),
                      oracle.linear_fwd(np.ascontiguousarray(A[:, :K]), np.ascontiguousarray(B[:, :K])),
                      f"K={K}")
+
+
+@pytest.mark.parametrize("wfmt,afmt,M,K", [("nvfp4", "none", 392, 544), ("mxfp4", "mxfp4", 392, 544),
+                                           ("q4k", "none", 264, 768), ("nvfp4", "nvfp4", 200, 512),
+                                           ("mxfp4", "none", 8, 256)])
+def test_transposing_quantizer_matches_saved_operands(qf, wfmt, afmt, M, K):
+    """The backward quantizes W (and X) straight into the transposed NT operands; with
+    QF_FLAG_REUSE_WS it instead transposes the forward's saved x_hat.  Both routes feed the
+    same GEMMs, so dX and dW must agree bit for bit (ragged tiles in every direction)."""
+    rng = np.random.default_rng(12)
+    N = 264
+    w = {"X": _rand_bf16(rng, (M, K)), "W": _rand_bf16(rng, (N, K), 0.02),
+         "dY": _rand_bf16(rng, (M, N))}
+    a_amax = None
+    if afmt == "nvfp4":
+        a_amax = torch.tensor([float(np.float32(1.1 * oracle.amax(w["X"])))],
+                              dtype=torch.float32, device="cuda")
+    Y, dX, dW = _layer(qf, w, wfmt, afmt, a_amax=a_amax)
+    Y2, dX2, dW2 = _layer(qf, w, wfmt, afmt, a_amax=a_amax, reuse=True)
+    assert np.array_equal(Y, Y2)
+    assert np.array_equal(dX.view(np.uint16), dX2.view(np.uint16))
+    assert np.array_equal(dW.view(np.uint32), dW2.view(np.uint32))

@@ -216,3 +216,31 @@ def test_empty_inputs_are_no_ops(qf):
     qf.fakequant_nvfp4(x, amax, qf.AMAX_COMPUTE, s_out, None, None, xhat)
     torch.cuda.synchronize()
     assert float(amax.item()) == 0.0 and float(s_out.item()) == 0.0
+
+
+@pytest.mark.parametrize("fmt,R,K,ldo", [("mxfp4", 8, 32, None), ("mxfp4", 72, 2080, 80),
+                                         ("nvfp4", 136, 528, None), ("nvfp4", 64, 256, 200),
+                                         ("q4k", 200, 768, None), ("q4k", 8, 256, 16)])
+def test_transposed_fakequant_bit_exact(qf, fmt, R, K, ldo):
+    """out[k][r] = x_hat[r][k]: ragged 64 x 256 tiles both ways, padded output rows kept."""
+    rng = np.random.default_rng(21)
+    if fmt == "q4k":
+        x = wide_range_bf16(rng, (R, K), lo_exp=-20, hi_exp=12)
+    else:
+        x = wide_range_bf16(rng, (R, K), lo_exp=-140, hi_exp=126)
+    if fmt == "mxfp4":
+        x[1, 5] = 0x7FC0                           # NaN block
+        x[3, min(40, K - 1)] = 0xFF80              # -Inf block
+    ldo = ldo or R
+    amax_in = None
+    amax = None
+    if fmt == "nvfp4":
+        amax_in = float(np.float32(oracle.amax(x)))
+        amax = torch.tensor([amax_in], dtype=torch.float32, device="cuda")
+    out = torch.full((K, ldo), 0x1234, dtype=torch.int16, device="cuda")
+    qf.fakequant_transposed(to_dev(x), fmt, out, amax)
+    torch.cuda.synchronize()
+    got = from_dev(out)
+    want = oracle.fakequant(x, fmt, amax_in)
+    assert np.array_equal(got[:, :R], np.ascontiguousarray(want.T)), fmt
+    assert np.all(got[:, R:] == 0x1234)
