@@ -136,6 +136,7 @@ def main():
     whatt = torch.empty(K, N, dtype=torch.int16, device=dev)
     xhatt = torch.empty(K, M, dtype=torch.int16, device=dev)
     dYt = torch.empty(N, M, dtype=torch.int16, device=dev)
+    gws = qf.gemm_workspace(N, K, 1)        # dW's split last round, as in the layer call
     phases = ["quant_W", "quant_X", "gemm_fwd", "quant_W_transposed", "gemm_dX", "transpose_dY",
               "quant_X_transposed", "gemm_dW"]
     calls = [
@@ -146,7 +147,7 @@ def main():
         lambda: qf.gemm_bf16(M, K, N, dY, N, 1, whatt, N, 1, dX, K, 0),
         lambda: qf.transpose_bf16(dY, dYt),
         lambda: qf.fakequant_transposed(X, "mxfp4", xhatt),
-        lambda: qf.gemm_bf16(N, K, M, dYt, M, 1, xhatt, M, 1, dW, K, 1),
+        lambda: qf.gemm_bf16(N, K, M, dYt, M, 1, xhatt, M, 1, dW, K, 1, ws=gws),
     ]
 
     def step(ev=None):
@@ -196,7 +197,7 @@ def main():
     q_gbps = q_bytes / (q_ms * 1e-3) / 1e9
     del bufs
 
-    del X, W, dY, what, xhat, whatt, xhatt, dYt, Y, dX, dW
+    del X, W, dY, what, xhat, whatt, xhatt, dYt, Y, dX, dW, gws
     torch.cuda.empty_cache()
     rows = None if args.main_only else other_rows(qf, torch, dev)
 

@@ -240,6 +240,21 @@ QF_API qf_status qf_gemm_bf16(int64_t M, int64_t N, int64_t K, const uint16_t* A
                        int a_kmajor, const uint16_t* B, int64_t ldb, int b_kmajor, void* C,
                        int64_t ldc, int c_f32, qf_stream_t stream);
 
+/*
+ * qf_gemm_workspace_size / qf_gemm_bf16_ws -- qf_gemm_bf16 with a caller workspace.  With
+ * k-contiguous A and B and an FP32 C (the dW product), a last round of output tiles that
+ * would leave at least half of the compute units idle is computed as two K-halves into the
+ * workspace and summed in a fixed order (deterministic; the summation order differs from the
+ * unsplit call by that one split).  Other layouts ignore the workspace.  ws: device memory,
+ * 256-byte aligned, at least the returned size (0 when no split can happen); ownership stays
+ * with the caller.
+ */
+QF_API qf_status qf_gemm_workspace_size(int64_t M, int64_t N, int c_f32, size_t* bytes);
+QF_API qf_status qf_gemm_bf16_ws(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
+                                 int a_kmajor, const uint16_t* B, int64_t ldb, int b_kmajor,
+                                 void* C, int64_t ldc, int c_f32, void* ws, size_t ws_bytes,
+                                 qf_stream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -80,6 +80,10 @@ def lib() -> ctypes.CDLL:
             "qf_gemm_bf16": ([_I, _I, _I, _P, _I, ctypes.c_int, _P, _I, ctypes.c_int, _P, _I,
                               ctypes.c_int, _P], ctypes.c_int),
             "qf_transpose_bf16": ([_P, _I, _I, _I, _P, _I, _P], ctypes.c_int),
+            "qf_gemm_workspace_size": ([_I, _I, ctypes.c_int, ctypes.POINTER(ctypes.c_size_t)],
+                                       ctypes.c_int),
+            "qf_gemm_bf16_ws": ([_I, _I, _I, _P, _I, ctypes.c_int, _P, _I, ctypes.c_int, _P, _I,
+                                 ctypes.c_int, _P, ctypes.c_size_t, _P], ctypes.c_int),
             "qf_fakequant_transposed": ([ctypes.c_int, _P, _I, _I, _I, _P, _P, _I, _P],
                                         ctypes.c_int),
         }
@@ -214,10 +218,21 @@ def qlinear_grouped_bwd_ste(desc, offsets, dY, X, W, dX, dW, ws):
                                             _ptr(dW), _ptr(ws), ws.numel(), _stream()))
 
 
-def gemm_bf16(M, N, K, A, lda, a_kmajor, B, ldb, b_kmajor, C, ldc, c_f32):
-    _check(lib().qf_gemm_bf16(M, N, K, _ptr(_bf16(A)), lda, int(a_kmajor), _ptr(_bf16(B)), ldb,
-                              int(b_kmajor), _ptr(C), ldc, int(c_f32), _stream()))
+def gemm_bf16(M, N, K, A, lda, a_kmajor, B, ldb, b_kmajor, C, ldc, c_f32, ws=None):
+    if ws is None:
+        _check(lib().qf_gemm_bf16(M, N, K, _ptr(_bf16(A)), lda, int(a_kmajor), _ptr(_bf16(B)),
+                                  ldb, int(b_kmajor), _ptr(C), ldc, int(c_f32), _stream()))
+    else:
+        _check(lib().qf_gemm_bf16_ws(M, N, K, _ptr(_bf16(A)), lda, int(a_kmajor), _ptr(_bf16(B)),
+                                     ldb, int(b_kmajor), _ptr(C), ldc, int(c_f32), _ptr(ws),
+                                     ws.numel() * ws.element_size(), _stream()))
     return C
+
+
+def gemm_workspace(M, N, c_f32, device="cuda"):
+    n = ctypes.c_size_t()
+    _check(lib().qf_gemm_workspace_size(M, N, int(c_f32), ctypes.byref(n)))
+    return torch.empty(max(n.value, 256), dtype=torch.uint8, device=device)
 
 
 def transpose_bf16(x, out):

@@ -115,6 +115,7 @@ qf_status fakequant_to(int fmt, const uint16_t* x, int64_t R, int64_t K, int64_t
 //   whatt  [K, N]  W_hat^T (or W^T): right operand of dX = dY W_hat in NT form
 //   ahatt  [K, M]  A_hat^T (or X^T): right operand of dW = dY^T A_hat in NT form
 //   dyt    [N, M]  dY^T: left operand of dW
+//   part   FP32 partial tiles of the dW GEMM's split last round (qf::gemm_nt_split_bytes)
 struct LinearWs {
   float* scal;
   uint16_t* what;
@@ -122,6 +123,7 @@ struct LinearWs {
   uint16_t* whatt;
   uint16_t* ahatt;
   uint16_t* dyt;
+  float* part;
 };
 
 size_t linear_ws_bytes(const qf_qlinear_desc* d) {
@@ -130,6 +132,7 @@ size_t linear_ws_bytes(const qf_qlinear_desc* d) {
   if (d->wfmt != QF_FMT_NONE) b += up(N * K * 2);
   if (d->afmt != QF_FMT_NONE) b += up(M * K * 2);
   b += up(K * N * 2) + up(K * M * 2) + up(N * M * 2);
+  b += up(qf::gemm_nt_split_bytes(d->N, d->K));
   return b;
 }
 
@@ -143,7 +146,8 @@ LinearWs linear_ws(const qf_qlinear_desc* d, void* ws) {
   if (d->afmt != QF_FMT_NONE) { w.ahat = reinterpret_cast<uint16_t*>(p); p += up(M * K * 2); }
   w.whatt = reinterpret_cast<uint16_t*>(p); p += up(K * N * 2);
   w.ahatt = reinterpret_cast<uint16_t*>(p); p += up(K * M * 2);
-  w.dyt = reinterpret_cast<uint16_t*>(p);
+  w.dyt = reinterpret_cast<uint16_t*>(p); p += up(N * M * 2);
+  w.part = reinterpret_cast<float*>(p);
   return w;
 }
 
@@ -298,7 +302,8 @@ qf_status qf_qlinear_fwd(const qf_qlinear_desc* d, const uint16_t* X, const uint
   const uint16_t *Wop, *Aop;
   int64_t ldw_op, lda_op;
   QF_TRY(quantize_operands(d, dm, X, W, w, true, true, &Wop, &ldw_op, &Aop, &lda_op, s));
-  QF_TRY(dev(qf::launch_gemm_nt(d->M, d->N, d->K, Aop, lda_op, Wop, ldw_op, Y, dm.ldy, 0, s),
+  QF_TRY(dev(qf::launch_gemm_nt(d->M, d->N, d->K, Aop, lda_op, Wop, ldw_op, Y, dm.ldy, 0,
+                                nullptr, s),
              "forward gemm"));
   return ok();
 }
@@ -338,7 +343,8 @@ qf_status qf_qlinear_bwd_ste(const qf_qlinear_desc* d, const uint16_t* dY, const
         QF_TRY(dev(qf::launch_transpose_bf16(src, d->N, d->K, ld, w.whatt, d->N, 1, 0, 0, s),
                    "transpose W_hat"));
       }
-      QF_TRY(dev(qf::launch_gemm_nt(d->M, d->K, d->N, dY, dm.ldy, w.whatt, d->N, dX, dm.ldx, 0, s),
+      QF_TRY(dev(qf::launch_gemm_nt(d->M, d->K, d->N, dY, dm.ldy, w.whatt, d->N, dX, dm.ldx, 0,
+                                    nullptr, s),
                  "dX gemm"));
     }
     if (dW) {  // dW[N, K] = (dY^T)[N, M] (A_hat^T)[K, M]^T
@@ -353,7 +359,8 @@ qf_status qf_qlinear_bwd_ste(const qf_qlinear_desc* d, const uint16_t* dY, const
         QF_TRY(dev(qf::launch_transpose_bf16(src, d->M, d->K, ld, w.ahatt, d->M, 1, 0, 0, s),
                    "transpose A_hat"));
       }
-      QF_TRY(dev(qf::launch_gemm_nt(d->N, d->K, d->M, w.dyt, d->M, w.ahatt, d->M, dW, d->K, 1, s),
+      QF_TRY(dev(qf::launch_gemm_nt(d->N, d->K, d->M, w.dyt, d->M, w.ahatt, d->M, dW, d->K, 1,
+                                    w.part, s),
                  "dW gemm"));
     }
   } else {
@@ -531,9 +538,9 @@ qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int64_t* gr
   return ok();
 }
 
-qf_status qf_gemm_bf16(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
-                       int a_kmajor, const uint16_t* B, int64_t ldb, int b_kmajor, void* C,
-                       int64_t ldc, int c_f32, qf_stream_t stream) {
+qf_status qf_gemm_bf16_ws(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
+                          int a_kmajor, const uint16_t* B, int64_t ldb, int b_kmajor, void* C,
+                          int64_t ldc, int c_f32, void* ws, size_t ws_bytes, qf_stream_t stream) {
   if (M < 0 || N < 0 || K < 0) return fail(QF_ESHAPE, "qf_gemm_bf16: negative shape");
   if ((a_kmajor | b_kmajor | c_f32) & ~1) return fail(QF_EINVAL, "qf_gemm_bf16: flags must be 0/1");
   if (a_kmajor ? false : (M % 8 != 0)) return fail(QF_ESHAPE, "qf_gemm_bf16: M must be a multiple of 8 for [K][M] A");
@@ -548,11 +555,34 @@ qf_status qf_gemm_bf16(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64
     if (ldc < N) return fail(QF_ESHAPE, "qf_gemm_bf16: ldc < N");
     if (!aligned16(C)) return fail(QF_EALIGN, "qf_gemm_bf16: C not 16-byte aligned");
   }
+  float* part = nullptr;
+  if (ws != nullptr && a_kmajor && b_kmajor && c_f32) {
+    if ((uintptr_t)ws % kAlign) return fail(QF_EALIGN, "qf_gemm_bf16_ws: workspace not 256-byte aligned");
+    if (ws_bytes < qf::gemm_nt_split_bytes(M, N))
+      return fail(QF_EINVAL, "qf_gemm_bf16_ws: workspace %zu bytes < required %zu", ws_bytes,
+                  qf::gemm_nt_split_bytes(M, N));
+    part = static_cast<float*>(ws);
+  }
   if (a_kmajor && b_kmajor)
-    QF_TRY(dev(qf::launch_gemm_nt(M, N, K, A, lda, B, ldb, C, ldc, c_f32, S(stream)), "gemm"));
+    QF_TRY(dev(qf::launch_gemm_nt(M, N, K, A, lda, B, ldb, C, ldc, c_f32, part, S(stream)),
+               "gemm"));
   else
     QF_TRY(dev(qf::launch_gemm(M, N, K, A, lda, a_kmajor, B, ldb, b_kmajor, C, ldc, c_f32, S(stream)),
                "gemm"));
+  return ok();
+}
+
+qf_status qf_gemm_bf16(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
+                       int a_kmajor, const uint16_t* B, int64_t ldb, int b_kmajor, void* C,
+                       int64_t ldc, int c_f32, qf_stream_t stream) {
+  return qf_gemm_bf16_ws(M, N, K, A, lda, a_kmajor, B, ldb, b_kmajor, C, ldc, c_f32, nullptr, 0,
+                         stream);
+}
+
+qf_status qf_gemm_workspace_size(int64_t M, int64_t N, int c_f32, size_t* bytes) {
+  if (!bytes) return fail(QF_EINVAL, "qf_gemm_workspace_size: null output");
+  if (M < 0 || N < 0) return fail(QF_ESHAPE, "qf_gemm_workspace_size: negative shape");
+  *bytes = c_f32 ? qf::gemm_nt_split_bytes(M, N) : 0;
   return ok();
 }
 

@@ -32,6 +32,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <type_traits>
 
 #include "qf_internal.h"
@@ -51,6 +52,7 @@ constexpr int kXcds = 8;
 constexpr int kWaves = 8;
 constexpr int NJ = 2;                            // 32-column accumulator blocks per wavefront
 constexpr int NLD = 8;                           // direct-to-LDS loads per wavefront per stage
+constexpr int64_t kMaxSplitTiles = 128;          // split tiles of the last round, at most
 constexpr int kPitch16 = BN * 2 + 16;            // epilogue LDS row pitch, bf16 tile (528 B)
 constexpr int kPitch32 = BN * 4 + 32;            // epilogue LDS row pitch, FP32 half tile
 constexpr int kSmemEpi = (BM * kPitch16 > 128 * kPitch32) ? BM * kPitch16 : 128 * kPitch32;
@@ -70,6 +72,14 @@ struct NtArgs {
   const int* tile_start;  // grouped rows: [E+1] per-expert tile prefix
   int E;
   int vec_store;          // C and ldc allow 16-byte stores
+  // FP32 split of the last partial round.  Tiles [split_from, tiles) are computed as two
+  // K-halves (stages [0, split_stage) and the rest); half h of tile split_from + i writes its
+  // 256 x 256 FP32 partial to part[2 i + h].  Work items are laid out per XCD (each XCD runs
+  // a contiguous range, see remap_xcd): full_per_xcd whole tiles, then split_per_xcd tiles as
+  // 2 halves each, so every XCD ends with a full round of half-length items.
+  float* part;
+  int split_from, full_per_xcd, split_per_xcd;
+  int64_t split_stage;
 };
 
 #define QF_LDS(p) ((__attribute__((address_space(3))) void*)(p))
@@ -116,7 +126,20 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
   const int lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (scalar) index
   const int wm = w >> 2, wn = w & 3;
-  const int bid = remap_xcd(blockIdx.x, gridDim.x);
+  const int item = remap_xcd(blockIdx.x, gridDim.x);
+  int bid = item, half = -1, pidx = 0;
+  if (MODE == kDense && C_F32 && p.part != nullptr) {
+    const int per_xcd = p.full_per_xcd + 2 * p.split_per_xcd;
+    const int x = item / per_xcd, j = item % per_xcd;
+    if (j < p.full_per_xcd) {
+      bid = x * p.full_per_xcd + j;
+    } else {
+      const int i = x * p.split_per_xcd + ((j - p.full_per_xcd) >> 1);
+      bid = p.split_from + i;
+      half = (j - p.full_per_xcd) & 1;
+      pidx = 2 * i + half;
+    }
+  }
 
   const uint16_t* Bp = p.B;
   int64_t m0, m_end, n0;
@@ -240,16 +263,18 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
   };
 
   const int64_t nfull = K / BK;
-  const int64_t krem = K % BK;
-  if (nfull > 0) {
+  const int64_t krem = half == 0 ? 0 : K % BK;   // the K tail belongs to the second half
+  const int64_t s0 = half == 1 ? p.split_stage : 0;
+  const int64_t s1 = half == 0 ? p.split_stage : nfull;
+  if (s1 > s0) {
 #pragma unroll
-    for (int q = 0; q < NLD; ++q) dma(0, 0, q);
-    __builtin_amdgcn_s_waitcnt(0);               // stage 0 landed (every counter drained)
+    for (int q = 0; q < NLD; ++q) dma(s0, (int)(s0 & 1), q);
+    __builtin_amdgcn_s_waitcnt(0);               // first stage landed (every counter drained)
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    read_all(smem, 0, fa[0], fb[0]);
-    for (int64_t s = 0; s < nfull - 1; ++s) step(s, std::false_type{});
-    step(nfull - 1, std::true_type{});
+    read_all(smem + (s0 & 1) * kStage, 0, fa[0], fb[0]);
+    for (int64_t s = s0; s < s1 - 1; ++s) step(s, std::false_type{});
+    step(s1 - 1, std::true_type{});
   }
   if (krem > 0) {
     // Partial last stage: masked loads through registers into buffer 0.  The wait + barrier
@@ -283,8 +308,14 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
   // lane % 32 of that 32 x 32 block.  Rows are padded so that the two half-waves of a write
   // (rows 4 apart) land 16 banks apart.
   __syncthreads();                               // every wavefront is done with the operands
+  // Destination: the output tile, or (split halves) a dense 256 x 256 FP32 partial.
   char* Cp = reinterpret_cast<char*>(p.C);
-  const int64_t ldc = p.ldc;
+  int64_t ldc = p.ldc, em0 = m0, em_end = m_end, en0 = n0, en_end = n_end;
+  int vec = p.vec_store;
+  if (half >= 0) {
+    Cp = reinterpret_cast<char*>(p.part + (int64_t)pidx * BM * BN);
+    ldc = BN; em0 = 0; em_end = BM; en0 = 0; en_end = BN; vec = 1;
+  }
   if (!C_F32) {
     char* wbase = smem + (wm * 128 + 4 * (lane >> 5)) * kPitch16 + (wn * 64 + (lane & 31)) * 2;
 #pragma unroll
@@ -297,19 +328,19 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
                                        j * 64) = (uint16_t)bf16_rne(acc[i][j][v]);
     __syncthreads();
     const int c8 = (tid & 31) * 8;
-    const int64_t gcol = n0 + c8;
+    const int64_t gcol = en0 + c8;
 #pragma unroll 4
     for (int it = 0; it < BM / 16; ++it) {
       const int r = it * 16 + (tid >> 5);
-      const int64_t grow = m0 + r;
-      if (grow >= m_end || gcol >= n_end) continue;
+      const int64_t grow = em0 + r;
+      if (grow >= em_end || gcol >= en_end) continue;
       const uint4 v = *reinterpret_cast<const uint4*>(smem + r * kPitch16 + c8 * 2);
       uint16_t* dst = reinterpret_cast<uint16_t*>(Cp) + grow * ldc + gcol;
-      if (p.vec_store && gcol + 8 <= n_end) {
+      if (vec && gcol + 8 <= en_end) {
         *reinterpret_cast<uint4*>(dst) = v;
       } else {
         const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
-        for (int e = 0; e < 8 && gcol + e < n_end; ++e)
+        for (int e = 0; e < 8 && gcol + e < en_end; ++e)
           dst[e] = (uint16_t)(wv[e >> 1] >> (16 * (e & 1)));
       }
     }
@@ -317,7 +348,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
     // FP32 tile (256 KB) in two halves of 128 rows: the wavefronts with wm == h write half h.
     char* wbase = smem + 4 * (lane >> 5) * kPitch32 + (wn * 64 + (lane & 31)) * 4;
     const int c4 = (tid & 63) * 4;
-    const int64_t gcol = n0 + c4;
+    const int64_t gcol = en0 + c4;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       if (h) __syncthreads();                    // half 0 has been read out
@@ -335,19 +366,56 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
 #pragma unroll 4
       for (int it = 0; it < 128 / 8; ++it) {
         const int r = it * 8 + (tid >> 6);
-        const int64_t grow = m0 + h * 128 + r;
-        if (grow >= m_end || gcol >= n_end) continue;
+        const int64_t grow = em0 + h * 128 + r;
+        if (grow >= em_end || gcol >= en_end) continue;
         const uint4 v = *reinterpret_cast<const uint4*>(smem + r * kPitch32 + c4 * 4);
         float* dst = reinterpret_cast<float*>(Cp) + grow * ldc + gcol;
-        if (p.vec_store && gcol + 4 <= n_end) {
+        if (vec && gcol + 4 <= en_end) {
           *reinterpret_cast<uint4*>(dst) = v;
         } else {
           const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
-          for (int e = 0; e < 4 && gcol + e < n_end; ++e) dst[e] = __uint_as_float(wv[e]);
+          for (int e = 0; e < 4 && gcol + e < en_end; ++e) dst[e] = __uint_as_float(wv[e]);
         }
       }
     }
   }
+}
+
+// C[tile] = part[2 i] + part[2 i + 1] for the split tiles split_from + i (dense mode, FP32):
+// four consecutive columns per lane.  The two halves are added in a fixed order, so the
+// result does not depend on which half finished first.
+__global__ __launch_bounds__(256) void split_reduce_kernel(NtArgs p) {
+  const int i = blockIdx.y;
+  const int t = p.split_from + i;
+  const int per_group = kGroupM * p.tiles_n;
+  const int g = t / per_group;
+  const int first = g * kGroupM;
+  const int gs = min(p.tiles_m - first, kGroupM);
+  const int64_t m0 = (int64_t)(first + (t % per_group) % gs) * BM;
+  const int64_t n0 = (int64_t)((t % per_group) / gs) * BN;
+  const int e = (blockIdx.x * 256 + threadIdx.x) * 4;      // element of the 256 x 256 tile
+  const int r = e / BN, c = e % BN;
+  const int64_t grow = m0 + r, gcol = n0 + c;
+  if (grow >= p.M || gcol >= p.N) return;
+  const float4 a = *reinterpret_cast<const float4*>(p.part + (int64_t)(2 * i) * BM * BN + e);
+  const float4 b = *reinterpret_cast<const float4*>(p.part + (int64_t)(2 * i + 1) * BM * BN + e);
+  const float sum[4] = {a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w};
+  float* dst = reinterpret_cast<float*>(p.C) + grow * p.ldc + gcol;
+  if (p.vec_store && gcol + 4 <= p.N) {
+    *reinterpret_cast<float4*>(dst) = make_float4(sum[0], sum[1], sum[2], sum[3]);
+  } else {
+    for (int k = 0; k < 4 && gcol + k < p.N; ++k) dst[k] = sum[k];
+  }
+}
+
+// Blocks resident at once: one 512-lane block per CU.
+int64_t resident_blocks() {
+  int dev = 0, ncu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      ncu <= 0)
+    return 256;
+  return ncu;
 }
 
 // The loads address a 256-row tile with 32-bit byte offsets from the tile's first row.
@@ -362,9 +430,14 @@ int vec_store_ok(const void* C, int64_t ldc, int esize) {
 
 }  // namespace
 
+size_t gemm_nt_split_bytes(int64_t M, int64_t N) {
+  const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+  return (size_t)(2 * std::min<int64_t>(tiles, kMaxSplitTiles)) * BM * BN * sizeof(float);
+}
+
 hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
                           const uint16_t* B, int64_t ldb, void* C, int64_t ldc, int c_f32,
-                          hipStream_t s) {
+                          float* part, hipStream_t s) {
   if (M == 0 || N == 0) return hipSuccess;
   if (!nt_offsets_fit(K, lda, ldb)) return hipErrorInvalidValue;
   NtArgs a{};
@@ -373,9 +446,28 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, in
   a.vec_store = vec_store_ok(C, ldc, c_f32 ? 4 : 2);
   a.tiles_m = (int)((M + BM - 1) / BM);
   a.tiles_n = (int)((N + BN - 1) / BN);
-  const dim3 grid((unsigned)(a.tiles_m * a.tiles_n));
+  const int64_t tiles = (int64_t)a.tiles_m * a.tiles_n;
+  int64_t items = tiles;
+  // A last round that would leave at least half the CUs idle runs as K-halves instead (FP32
+  // output only; needs a partial buffer and at least two full stages).
+  // The split is decided per XCD: each runs tiles / 8 tiles on cus / 8 CUs.
+  const int64_t cus = resident_blocks();
+  const int64_t rem = tiles % cus;
+  if (c_f32 && part != nullptr && tiles % kXcds == 0 && cus % kXcds == 0 && rem > 0 &&
+      2 * rem <= cus && rem <= kMaxSplitTiles && K / BK >= 2) {
+    a.part = part;
+    a.split_from = (int)(tiles - rem);
+    a.full_per_xcd = (int)((tiles - rem) / kXcds);
+    a.split_per_xcd = (int)(rem / kXcds);
+    a.split_stage = (K / BK) / 2;
+    items = tiles + rem;
+  }
+  const dim3 grid((unsigned)items);
   if (c_f32) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense>), grid, dim3(kWaves * 64), 0, s, a);
   else hipLaunchKernelGGL((gemm_nt_kernel<false, kDense>), grid, dim3(kWaves * 64), 0, s, a);
+  if (a.part != nullptr)
+    hipLaunchKernelGGL(split_reduce_kernel, dim3(BM * BN / (256 * 4), (unsigned)rem), dim3(256),
+                       0, s, a);
   return hipGetLastError();
 }
 

@@ -44,7 +44,10 @@ hipError_t launch_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64
 // contiguous (row strides lda, ldb multiples of 8, K multiple of 8).
 hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
                           const uint16_t* B, int64_t ldb, void* C, int64_t ldc, int c_f32,
-                          hipStream_t s);
+                          float* part, hipStream_t s);
+// Bytes of the FP32 partial buffer `part` an [M, N] FP32-output launch may use (a K-split
+// of the last partial round of tiles).  part may be null: no split.
+size_t gemm_nt_split_bytes(int64_t M, int64_t N);
 // Grouped NT: rows [off[e], off[e+1]) of A use B + e * bstride ([N][K], k contiguous).
 hipError_t launch_grouped_nt_rows(int64_t E, int64_t T, int64_t N, int64_t K, const int64_t* off,
                                   const int* tile_start, const uint16_t* A, int64_t lda,

@@ -257,3 +257,27 @@ def test_transposing_quantizer_matches_saved_operands(qf, wfmt, afmt, M, K):
     assert np.array_equal(Y, Y2)
     assert np.array_equal(dX.view(np.uint16), dX2.view(np.uint16))
     assert np.array_equal(dW.view(np.uint32), dW2.view(np.uint32))
+
+
+@pytest.mark.parametrize("M,N,K,ldc", [(264, 1000, 136, 1004), (8, 2048, 1000, 2048),
+                                       (2048, 12, 200, 16), (512, 1024, 128, 1024),
+                                       (300, 264, 136, 264)])
+def test_gemm_split_last_round(qf, M, N, K, ldc):
+    """FP32 NT GEMM with a workspace: grids of 8 tiles (one per XCD, all in the last, partial
+    round) run as two K-halves plus a fixed-order sum; ragged edges, K tails, a strided C, and
+    one shape (4 tiles) that does not split."""
+    rng = np.random.default_rng(M + N + K)
+    A, B = _rand_bf16(rng, (M, K)), _rand_bf16(rng, (N, K))
+    C = torch.full((M, ldc), -3.0, dtype=torch.float32, device="cuda")
+    ws = qf.gemm_workspace(M, N, 1)
+    qf.gemm_bf16(M, N, K, to_dev(A), K, 1, to_dev(B), K, 1, C, ldc, 1, ws=ws)
+    torch.cuda.synchronize()
+    c = from_dev(C)
+    assert np.all(c[:, N:] == -3.0)
+    want = oracle.linear_fwd(A, B)
+    assert_close(c[:, :N].astype(np.float64), want, "split gemm")
+    # the same call again gives the same bits
+    C2 = torch.full((M, ldc), -3.0, dtype=torch.float32, device="cuda")
+    qf.gemm_bf16(M, N, K, to_dev(A), K, 1, to_dev(B), K, 1, C2, ldc, 1, ws=ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(c.view(np.uint32), from_dev(C2).view(np.uint32))
