@@ -28,7 +28,8 @@
 //    partial last k stage goes through a masked register path.
 //  - The epilogue stages the tile through LDS (rows padded so both half-waves of a write hit
 //    different banks) and writes whole rows with 16-byte stores; FP32 tiles go in two halves.
-//  - Block ids are remapped so each XCD (own L2) works on a contiguous group of tiles.
+//  - Block ids are remapped so each XCD (own L2) works on a contiguous group of tiles, and
+//    each XCD walks K from its own rotated start (HBM channel spread).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -207,10 +208,22 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
     for (int j = 0; j < NJ; ++j) acc[i][j] = f32x16_t{};
   bf16x8_t fa[2][4], fb[2][NJ];
 
+  // K order: the stages of this item's range [ks0, ks1) are visited rotated by an offset that
+  // depends on the XCD (blockIdx.x % 8).  The 32 CUs of an XCD stay in step, so the panels
+  // they share still meet in its L2, but the eight XCDs stream from eight different k offsets:
+  // with row strides that are large powers of two, k-aligned requests from all CUs otherwise
+  // pile onto the same HBM channels.  Each tile's sum order is fixed, so results are
+  // deterministic.
+  const int64_t ks0 = half == 1 ? p.split_stage : 0;
+  const int64_t ks1 = half == 0 ? p.split_stage : K / BK;
+  const int64_t klen = ks1 > ks0 ? ks1 - ks0 : 1;
+  const int64_t krot = (int64_t)(blockIdx.x % kXcds) * (klen / kXcds);
   auto dma = [&](int64_t s, int buf, int q) {
+    int64_t se = s + krot;
+    if (se >= ks1) se -= klen;
     char* l = smem + buf * kStage + lbase + q * 8 * kRow;
-    if (QF_NT_GLOBAL_LDS) dma16_global(gbase + s * kRow + goff[q], l);
-    else dma16_buf(rsrc, goff[q], (uint32_t)(s * kRow), l);
+    if (QF_NT_GLOBAL_LDS) dma16_global(gbase + se * kRow + goff[q], l);
+    else dma16_buf(rsrc, goff[q], (uint32_t)(se * kRow), l);
   };
   // Fragment read r of a slice, in the order the slice's MFMAs consume them: A0, B0, B1, A1..A3.
   auto read_one = [&](const char* st, int kk, int r, bf16x8_t* a, bf16x8_t* b) {
