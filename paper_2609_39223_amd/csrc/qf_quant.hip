@@ -141,17 +141,26 @@ __global__ void fill_f32_kernel(float* p, int64_t n, float v) {
 __global__ __launch_bounds__(kThreads) void amax_kernel(const uint16_t* __restrict__ x, int64_t R,
                                                         int64_t K, int64_t ldx, int64_t tstride,
                                                         float* __restrict__ amax) {
+  constexpr int RPT = 8;                      // rows per pass: 8 independent 16-byte loads
   const int64_t chunks = K >> 3;
   const uint16_t* xt = x + (int64_t)blockIdx.z * tstride;
   uint32_t m = 0;
-  for (int64_t r = blockIdx.y; r < R; r += gridDim.y) {
-    for (int64_t c = (int64_t)blockIdx.x * kThreads + threadIdx.x; c < chunks;
-         c += (int64_t)gridDim.x * kThreads) {
-      uint4 v = *reinterpret_cast<const uint4*>(xt + r * ldx + c * 8);
-      uint32_t h[8];
-      unpack8(v, h);
-      uint32_t a = max_abs_bits8(h);
-      m = a > m ? a : m;
+  for (int64_t c = (int64_t)blockIdx.x * kThreads + threadIdx.x; c < chunks;
+       c += (int64_t)gridDim.x * kThreads) {
+    for (int64_t r0 = (int64_t)blockIdx.y * RPT; r0 < R; r0 += (int64_t)gridDim.y * RPT) {
+      uint4 v[RPT];
+#pragma unroll
+      for (int i = 0; i < RPT; ++i) {
+        v[i] = make_uint4(0, 0, 0, 0);
+        if (r0 + i < R) v[i] = *reinterpret_cast<const uint4*>(xt + (r0 + i) * ldx + c * 8);
+      }
+#pragma unroll
+      for (int i = 0; i < RPT; ++i) {
+        uint32_t h[8];
+        unpack8(v[i], h);
+        const uint32_t a = max_abs_bits8(h);
+        m = a > m ? a : m;
+      }
     }
   }
 #pragma unroll
@@ -298,14 +307,19 @@ __global__ __launch_bounds__(kThreads) void nvfp4_kernel(
   if (s_out && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0) s_out[z] = S;
   const uint16_t* xt = x + z * tstride;
   const int64_t obase = z * R * K;
+  uint4 vin[RPT];
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {           // all loads first: RPT requests in flight
+    const int64_t r = (int64_t)blockIdx.y * RPT + i;
+    vin[i] = make_uint4(0, 0, 0, 0);
+    if (col_ok && r < R) vin[i] = *reinterpret_cast<const uint4*>(xt + r * ldx + c * 8);
+  }
 #pragma unroll
   for (int i = 0; i < RPT; ++i) {
     const int64_t r = (int64_t)blockIdx.y * RPT + i;
     const bool ok = col_ok && r < R;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (ok) v = *reinterpret_cast<const uint4*>(xt + r * ldx + c * 8);
     uint32_t h[8], cw, sc, xh[8];
-    unpack8(v, h);
+    unpack8(vin[i], h);
     nvfp4_chunk(h, S, six_s, cw, sc, xh);
     if (ok) {
       if (codes) *reinterpret_cast<uint32_t*>(codes + obase / 2 + r * (K / 2) + c * 4) = cw;
@@ -323,14 +337,19 @@ __global__ __launch_bounds__(kThreads) void mxfp4_kernel(
   const int64_t chunks = K >> 3;
   const int64_t c = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   const bool col_ok = c < chunks;
+  uint4 vin[RPT];
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {           // all loads first: RPT requests in flight
+    const int64_t r = (int64_t)blockIdx.y * RPT + i;
+    vin[i] = make_uint4(0, 0, 0, 0);
+    if (col_ok && r < R) vin[i] = *reinterpret_cast<const uint4*>(x + r * ldx + c * 8);
+  }
 #pragma unroll
   for (int i = 0; i < RPT; ++i) {
     const int64_t r = (int64_t)blockIdx.y * RPT + i;
     const bool ok = col_ok && r < R;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (ok) v = *reinterpret_cast<const uint4*>(x + r * ldx + c * 8);
     uint32_t h[8], cw, e, xh[8];
-    unpack8(v, h);
+    unpack8(vin[i], h);
     mxfp4_chunk(h, cw, e, xh);
     if (ok) {
       if (codes) *reinterpret_cast<uint32_t*>(codes + r * (K / 2) + c * 4) = cw;
@@ -431,14 +450,18 @@ __global__ __launch_bounds__(kThreads) void quant_t_kernel(const uint16_t* __res
     S = g[blockIdx.z] / 2688.0f;            // g maps to 6 * 448
     six_s = 6.0f * S;
   }
-#pragma unroll 2
+  uint4 vin[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {             // all eight loads first
+    const int64_t gr = r0 + i * 8 + (t >> 5), gc = c0 + (t & 31) * 8;
+    vin[i] = make_uint4(0, 0, 0, 0);
+    if (gr < R && gc < K) vin[i] = *reinterpret_cast<const uint4*>(x + gr * ldx + gc);
+  }
+#pragma unroll
   for (int i = 0; i < 8; ++i) {
     const int row = i * 8 + (t >> 5), cc = t & 31;
-    const int64_t gr = r0 + row, gc = c0 + cc * 8;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (gr < R && gc < K) v = *reinterpret_cast<const uint4*>(x + gr * ldx + gc);
     uint32_t h[8], xh[8];
-    unpack8(v, h);
+    unpack8(vin[i], h);
     if (FMT == QF_FMT_NVFP4) {
       uint32_t cw, sc;
       nvfp4_chunk(h, S, six_s, cw, sc, xh);
@@ -489,11 +512,14 @@ hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s) {
   return hipGetLastError();
 }
 
+// At most ~1000 blocks (one atomic each) for one tensor: 8 rows per pass, grid-strided.
 static dim3 amax_grid(int64_t R, int64_t K, int64_t E) {
   const int64_t chunks = K >> 3;
   int64_t gx = (chunks + kThreads - 1) / kThreads;
   if (gx > 64) gx = 64;
-  int64_t gy = R < 1024 ? R : 1024;
+  int64_t gy = (R + 7) / 8;
+  const int64_t cap = (1024 + gx - 1) / gx;
+  if (gy > cap) gy = cap;
   if (gy < 1) gy = 1;
   return dim3((unsigned)gx, (unsigned)gy, (unsigned)E);
 }
@@ -509,9 +535,9 @@ hipError_t launch_amax(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, flo
 hipError_t launch_amax_batched(const uint16_t* x, int64_t E, int64_t R, int64_t K, float* amax,
                                hipStream_t s) {
   if (E == 0 || R == 0 || K == 0) return hipSuccess;
-  int64_t gy = R < 64 ? R : 64;
   dim3 grid = amax_grid(R, K, E);
-  grid.y = (unsigned)gy;
+  const int64_t gy = (R + 7) / 8 < 16 ? (R + 7) / 8 : 16;
+  grid.y = (unsigned)(gy < 1 ? 1 : gy);
   hipLaunchKernelGGL(amax_kernel, grid, dim3(kThreads), 0, s, x, R, K, K, R * K, amax);
   return hipGetLastError();
 }
