@@ -389,13 +389,22 @@ struct GroupedWs {
   uint16_t* what;   // [E, N, K]
   uint16_t* ahat;   // [T, K]
   uint16_t* whatt;  // [E, K, N]: per-expert W_hat^T, right operand of dX in NT form
+  int* kstart;      // [E+1]: expert e's tokens at padded columns [64 kstart[e], 64 kstart[e+1])
+  int* korder;      // [E]: experts in XCD-balanced order for the dW launch
+  uint16_t* dyt;    // [N, Tpad]: dY^T, each expert's tokens padded to a multiple of 64
+  uint16_t* at;     // [K, Tpad]: A_hat^T, same padding (dW operands in NT form)
 };
+
+// Padded token count: each expert's rows rounded up to a multiple of 64.
+int64_t grouped_tpad(const qf_grouped_desc* d) { return (d->T + 63 * d->E + 63) / 64 * 64; }
 
 size_t grouped_ws_bytes(const qf_grouped_desc* d) {
   size_t b = up((size_t)(d->E + 1) * 4) + up((size_t)d->E * 4) + up((size_t)d->E * 4);
   if (d->wfmt != QF_FMT_NONE) b += up((size_t)d->E * d->N * d->K * 2);
   if (d->afmt != QF_FMT_NONE) b += up((size_t)d->T * d->K * 2);
   b += up((size_t)d->E * d->N * d->K * 2);
+  b += up((size_t)(d->E + 1) * 4) + up((size_t)d->E * 4);
+  b += up((size_t)d->N * grouped_tpad(d) * 2) + up((size_t)d->K * grouped_tpad(d) * 2);
   return b;
 }
 
@@ -407,7 +416,11 @@ GroupedWs grouped_ws(const qf_grouped_desc* d, void* ws) {
   g.wamax = reinterpret_cast<float*>(p); p += up((size_t)d->E * 4);
   if (d->wfmt != QF_FMT_NONE) { g.what = reinterpret_cast<uint16_t*>(p); p += up((size_t)d->E * d->N * d->K * 2); }
   if (d->afmt != QF_FMT_NONE) { g.ahat = reinterpret_cast<uint16_t*>(p); p += up((size_t)d->T * d->K * 2); }
-  g.whatt = reinterpret_cast<uint16_t*>(p);
+  g.whatt = reinterpret_cast<uint16_t*>(p); p += up((size_t)d->E * d->N * d->K * 2);
+  g.kstart = reinterpret_cast<int*>(p); p += up((size_t)(d->E + 1) * 4);
+  g.korder = reinterpret_cast<int*>(p); p += up((size_t)d->E * 4);
+  g.dyt = reinterpret_cast<uint16_t*>(p); p += up((size_t)d->N * grouped_tpad(d) * 2);
+  g.at = reinterpret_cast<uint16_t*>(p);
   return g;
 }
 
@@ -483,7 +496,9 @@ qf_status qf_qlinear_grouped_fwd(const qf_grouped_desc* d, const int64_t* group_
   GroupedWs g = grouped_ws(d, ws);
   const uint16_t *Wop, *Aop;
   QF_TRY(grouped_quantize(d, X, W, g, true, true, &Wop, &Aop, s));
-  QF_TRY(dev(qf::launch_grouped_prep(group_offsets, d->E, g.tile_start, g.order, s), "prep"));
+  QF_TRY(dev(qf::launch_grouped_prep(group_offsets, d->E, g.tile_start, g.order, g.kstart,
+                                    g.korder, s),
+             "prep"));
   QF_TRY(dev(qf::launch_grouped_nt_rows(d->E, d->T, d->N, d->K, group_offsets, g.tile_start, Aop,
                                         d->K, Wop, d->K, d->N * d->K, Y, d->N, s),
              "grouped forward"));
@@ -508,8 +523,10 @@ qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int64_t* gr
   // Without a saved W_hat, the experts' W_hat^T comes straight from the transposing quantizer.
   const bool fuse_w = dX && d->wfmt != QF_FMT_NONE && !reuse;
   const uint16_t *Wop, *Aop;
-  QF_TRY(grouped_quantize(d, X, W, g, !reuse && dX && !fuse_w, !reuse && dW, &Wop, &Aop, s));
-  QF_TRY(dev(qf::launch_grouped_prep(group_offsets, d->E, g.tile_start, g.order, s), "prep"));
+  QF_TRY(grouped_quantize(d, X, W, g, !reuse && dX && !fuse_w, false, &Wop, &Aop, s));
+  QF_TRY(dev(qf::launch_grouped_prep(group_offsets, d->E, g.tile_start, g.order, g.kstart,
+                                    g.korder, s),
+             "prep"));
   if (dX) {
     if (fuse_w) {
       const float* gp = d->w_amax;
@@ -531,8 +548,18 @@ qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int64_t* gr
                "grouped dX"));
   }
   if (dW) {
-    QF_TRY(dev(qf::launch_grouped_wgrad_ws(d->E, d->T, d->N, d->K, group_offsets, g.order, dY,
-                                           d->N, Aop, d->K, dW, s),
+    // dW_e = dY_e^T A_hat_e as one NT launch over padded, transposed token columns: expert e
+    // contracts over its own 64-aligned column range (zeros past its last token).
+    const int64_t tp = grouped_tpad(d);
+    QF_TRY(dev(qf::launch_quant_t_grouped(QF_FMT_NONE, dY, d->T, d->N, group_offsets, g.kstart,
+                                          d->E, g.dyt, tp, s),
+               "transpose dY (grouped)"));
+    const bool saved = d->afmt != QF_FMT_NONE && reuse;
+    QF_TRY(dev(qf::launch_quant_t_grouped(saved ? QF_FMT_NONE : d->afmt, saved ? g.ahat : X, d->T,
+                                          d->K, group_offsets, g.kstart, d->E, g.at, tp, s),
+               "quantize A (grouped, transposed)"));
+    QF_TRY(dev(qf::launch_grouped_nt_k(d->E, d->N, d->K, tp, g.kstart, g.korder, g.dyt, tp, g.at,
+                                       tp, dW, d->K, d->N * d->K, s),
                "grouped dW"));
   }
   return ok();

@@ -2,11 +2,11 @@
 //
 //   C[m, n] = sum_k A(m, k) * B(n, k)        FP32 accumulation, bf16 or FP32 output
 //
-// Each operand is either k-major (stored [MN][K], contraction contiguous: X, W, dY in the
-// forward and dX GEMMs) or mn-major (stored [K][MN]: W_hat as the right operand of
-// dX = dY W_hat, and both operands of dW = dY^T A_hat).  The three products of the layer
-// (Eqs. fakequant, ste, activation-ste) are the three layout combinations (k,k), (k,mn),
-// (mn,mn) of one kernel template.
+// Each operand is either k-major (stored [MN][K], contraction contiguous) or mn-major
+// (stored [K][MN]).  The layer's products run on the NT kernel (qf_gemm_nt.hip) with both
+// operands k-major; this template covers the other layouts of the plain GEMM entry point and
+// the layer backward when the token count is not a multiple of 8 (dX = dY W_hat as (k,mn),
+// dW = dY^T A_hat as (mn,mn)), reading mn-major operands in place.
 //
 // Block tile 256 x 256 x 64, 256 lanes = 4 wavefronts in a 2 x 2 grid, each wavefront
 // owning a 128 x 128 sub-tile as 4 x 4 v_mfma_f32_32x32x16_bf16 accumulators (256 AGPRs).
@@ -40,21 +40,15 @@ constexpr int kTileBytes = BM * BK * 2;   // one operand stage: 32 KB
 constexpr int kGroupM = 8;
 constexpr int kXcds = 8;
 
-enum Mode { kDense = 0, kGroupRows = 1, kGroupWgrad = 2 };
+enum Mode { kDense = 0 };
 
 struct GemmArgs {
   const uint16_t* A;
   const uint16_t* B;
   void* C;
   int64_t lda, ldb, ldc;
-  int64_t bstride;   // grouped: elements between consecutive experts' B
-  int64_t cstride;   // grouped wgrad: elements between consecutive experts' C
   int64_t M, N, K;
   int tiles_m, tiles_n;
-  const int64_t* off;      // grouped: device [E+1] row offsets
-  const int* tile_start;   // grouped rows: [E+1] prefix of per-expert m-tile counts
-  const int* order;        // grouped wgrad: experts by decreasing row count
-  int E;
 };
 
 __device__ __forceinline__ int lds_off(int r, int c) {
@@ -314,27 +308,6 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmArgs p) {
     const int tn = (bid % per_group) / gs;
     m0 = (int64_t)tm * BM; m_end = p.M;
     n0 = (int64_t)tn * BN;
-  } else if (MODE == kGroupRows) {
-    const int mt = bid / p.tiles_n, tn = bid % p.tiles_n;
-    if (mt >= p.tile_start[p.E]) return;        // uniform over the block
-    int lo = 0, hi = p.E;                       // find e: tile_start[e] <= mt < tile_start[e+1]
-    while (hi - lo > 1) {
-      const int mid = (lo + hi) >> 1;
-      if (p.tile_start[mid] <= mt) lo = mid; else hi = mid;
-    }
-    const int e = lo;
-    m0 = p.off[e] + (int64_t)(mt - p.tile_start[e]) * BM;
-    m_end = p.off[e + 1];
-    n0 = (int64_t)tn * BN;
-    Bp += (int64_t)e * p.bstride;
-  } else {
-    const int tpe = p.tiles_m * p.tiles_n;
-    const int e = p.order[bid / tpe];
-    const int t = bid % tpe;
-    m0 = (int64_t)(t / p.tiles_n) * BM; m_end = p.M;
-    n0 = (int64_t)(t % p.tiles_n) * BN;
-    kb = p.off[e]; ke = p.off[e + 1];
-    Cp += (int64_t)e * p.cstride * (C_F32 ? 4 : 2);
   }
 
   f32x16_t acc[4][4];
@@ -415,17 +388,23 @@ __global__ __launch_bounds__(NTHR, 1) void gemm_kernel(GemmArgs p) {
 // Per-expert tile prefix (grouped rows) and experts ordered by decreasing row count (grouped
 // wgrad, so the longest contractions start first).  One block, E <= 1024 lanes.
 __global__ void grouped_prep_kernel(const int64_t* __restrict__ off, int E, int* tile_start,
-                                    int* order) {
-  __shared__ int cnt[1024];
+                                    int* order, int* kstart, int* korder) {
+  __shared__ int cnt[1024], cnt64[1024];
   const int e = threadIdx.x;
   int64_t rows = 0;
   if (e < E) rows = off[e + 1] - off[e];
   if (e < E) cnt[e] = (int)((rows + BM - 1) / BM);
+  if (e < E) cnt64[e] = (int)((rows + 63) / 64);
   __syncthreads();
   if (e == 0) {
     int s = 0;
     for (int i = 0; i < E; ++i) { tile_start[i] = s; s += cnt[i]; }
     tile_start[E] = s;
+  }
+  if (e == 0 && kstart) {                        // 64-row units: padded k ranges of dW
+    int s = 0;
+    for (int i = 0; i < E; ++i) { kstart[i] = s; s += cnt64[i]; }
+    kstart[E] = s;
   }
   if (e < E && order) {
     int rank = 0;
@@ -434,6 +413,18 @@ __global__ void grouped_prep_kernel(const int64_t* __restrict__ off, int E, int*
       rank += (ri > rows) || (ri == rows && i < e);
     }
     order[rank] = e;
+    if (korder) {
+      // Balanced over the 8 XCDs for launches whose items run as 8 contiguous ranges (one per
+      // XCD): ranks are dealt in a snake (0..7 to XCDs 0..7, 8..15 to XCDs 7..0, ...), and
+      // each XCD's experts stay in decreasing order.  Needs E % 8 == 0 (else the plain order).
+      int pos = rank;
+      if (E % 8 == 0) {
+        const int k = rank / 8, i = rank % 8;
+        const int x = (k & 1) ? 7 - i : i;
+        pos = x * (E / 8) + k;
+      }
+      korder[pos] = e;
+    }
   }
 }
 
@@ -469,38 +460,10 @@ hipError_t launch_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64
 }
 
 hipError_t launch_grouped_prep(const int64_t* off, int64_t E, int* tile_start, int* order,
-                               hipStream_t s) {
+                               int* kstart, int* korder, hipStream_t s) {
   hipLaunchKernelGGL(grouped_prep_kernel, dim3(1), dim3(1024), 0, s, off, (int)E, tile_start,
-                     order);
+                     order, kstart, korder);
   return hipGetLastError();
-}
-
-hipError_t launch_grouped_rows_ws(int64_t E, int64_t T, int64_t N, int64_t K, const int64_t* off,
-                                  const int* tile_start, const uint16_t* A, int64_t lda,
-                                  const uint16_t* B, int64_t ldb, int64_t bstride, int b_kmajor,
-                                  uint16_t* C, int64_t ldc, hipStream_t s) {
-  if (T == 0 || N == 0 || E == 0) return hipSuccess;
-  GemmArgs a{};
-  a.A = A; a.B = B; a.C = C; a.lda = lda; a.ldb = ldb; a.ldc = ldc; a.bstride = bstride;
-  a.M = T; a.N = N; a.K = K; a.off = off; a.tile_start = tile_start; a.E = (int)E;
-  a.tiles_n = (int)((N + BN - 1) / BN);
-  a.tiles_m = (int)((T + BM - 1) / BM + E);   // upper bound on sum_e ceil(M_e / BM)
-  const int blocks = a.tiles_m * a.tiles_n;
-  if (b_kmajor) return launch<true, true, false, kGroupRows>(a, blocks, s);
-  return launch<true, false, false, kGroupRows>(a, blocks, s);
-}
-
-hipError_t launch_grouped_wgrad_ws(int64_t E, int64_t T, int64_t N, int64_t K, const int64_t* off,
-                                   const int* order, const uint16_t* dY, int64_t ldy,
-                                   const uint16_t* X, int64_t ldx, float* C, hipStream_t s) {
-  if (E == 0 || N == 0 || K == 0) return hipSuccess;
-  GemmArgs a{};
-  a.A = dY; a.B = X; a.C = C; a.lda = ldy; a.ldb = ldx; a.ldc = K; a.cstride = N * K;
-  a.M = N; a.N = K; a.K = T; a.off = off; a.order = order; a.E = (int)E;
-  a.tiles_m = (int)((N + BM - 1) / BM);
-  a.tiles_n = (int)((K + BN - 1) / BN);
-  const int blocks = a.tiles_m * a.tiles_n * (int)E;
-  return launch<false, false, true, kGroupWgrad>(a, blocks, s);
 }
 
 }  // namespace qf

@@ -59,7 +59,7 @@ constexpr int kPitch32 = BN * 4 + 32;            // epilogue LDS row pitch, FP32
 constexpr int kSmemEpi = (BM * kPitch16 > 128 * kPitch32) ? BM * kPitch16 : 128 * kPitch32;
 constexpr int kSmem = (2 * kStage > kSmemEpi) ? 2 * kStage : kSmemEpi;
 
-enum Mode { kDense = 0, kGroupRows = 1 };
+enum Mode { kDense = 0, kGroupRows = 1, kGroupK = 2 };
 
 struct NtArgs {
   const uint16_t* A;
@@ -72,6 +72,12 @@ struct NtArgs {
   const int64_t* off;     // grouped rows: [E+1] row offsets
   const int* tile_start;  // grouped rows: [E+1] per-expert tile prefix
   int E;
+  // grouped K (per-expert weight gradient): expert e contracts over k in
+  // [BK kstart[e], BK kstart[e+1]) and writes C + e cstride; order[] lists experts by
+  // decreasing work, so the largest start first.
+  const int* kstart;
+  const int* order;
+  int64_t cstride;
   int vec_store;          // C and ldc allow 16-byte stores
   // FP32 split of the last partial round.  Tiles [split_from, tiles) are computed as two
   // K-halves (stages [0, split_stage) and the rest); half h of tile split_from + i writes its
@@ -144,14 +150,25 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
 
   const uint16_t* Bp = p.B;
   int64_t m0, m_end, n0;
-  if (MODE == kDense) {
+  int64_t ks0 = 0, ks1 = p.K / BK;               // stage range of this item
+  int64_t cofs = 0;                              // element offset of this item's C
+  if (MODE == kDense || MODE == kGroupK) {
+    int t = bid;
+    if (MODE == kGroupK) {
+      const int tpe = p.tiles_m * p.tiles_n;
+      const int e = p.order[bid / tpe];
+      t = bid % tpe;
+      ks0 = p.kstart[e];
+      ks1 = p.kstart[e + 1];
+      cofs = (int64_t)e * p.cstride;
+    }
     const int per_group = kGroupM * p.tiles_n;
-    const int g = bid / per_group;
+    const int g = t / per_group;
     const int first = g * kGroupM;
     const int gs = min(p.tiles_m - first, kGroupM);
-    m0 = (int64_t)(first + (bid % per_group) % gs) * BM;
+    m0 = (int64_t)(first + (t % per_group) % gs) * BM;
     m_end = p.M;
-    n0 = (int64_t)((bid % per_group) / gs) * BN;
+    n0 = (int64_t)((t % per_group) / gs) * BN;
   } else {
     const int mt = bid / p.tiles_n, tn = bid % p.tiles_n;
     if (mt >= p.tile_start[p.E]) return;         // uniform over the block
@@ -214,8 +231,8 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
   // with row strides that are large powers of two, k-aligned requests from all CUs otherwise
   // pile onto the same HBM channels.  Each tile's sum order is fixed, so results are
   // deterministic.
-  const int64_t ks0 = half == 1 ? p.split_stage : 0;
-  const int64_t ks1 = half == 0 ? p.split_stage : K / BK;
+  if (half == 1) ks0 = p.split_stage;
+  if (half == 0) ks1 = p.split_stage;
   const int64_t klen = ks1 > ks0 ? ks1 - ks0 : 1;
   const int64_t krot = (int64_t)(blockIdx.x % kXcds) * (klen / kXcds);
   auto dma = [&](int64_t s, int buf, int q) {
@@ -275,10 +292,9 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
           smem + nxt * kStage, 0, fa[0], fb[0], 0, 0);
   };
 
-  const int64_t nfull = K / BK;
-  const int64_t krem = half == 0 ? 0 : K % BK;   // the K tail belongs to the second half
-  const int64_t s0 = half == 1 ? p.split_stage : 0;
-  const int64_t s1 = half == 0 ? p.split_stage : nfull;
+  const int64_t nfull = K / BK;                 // the K tail (dense, second half) follows it
+  const int64_t krem = (half == 0 || MODE == kGroupK) ? 0 : K % BK;
+  const int64_t s0 = ks0, s1 = ks1;
   if (s1 > s0) {
 #pragma unroll
     for (int q = 0; q < NLD; ++q) dma(s0, (int)(s0 & 1), q);
@@ -322,7 +338,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
   // (rows 4 apart) land 16 banks apart.
   __syncthreads();                               // every wavefront is done with the operands
   // Destination: the output tile, or (split halves) a dense 256 x 256 FP32 partial.
-  char* Cp = reinterpret_cast<char*>(p.C);
+  char* Cp = reinterpret_cast<char*>(p.C) + cofs * (C_F32 ? 4 : 2);
   int64_t ldc = p.ldc, em0 = m0, em_end = m_end, en0 = n0, en_end = n_end;
   int vec = p.vec_store;
   if (half >= 0) {
@@ -498,6 +514,23 @@ hipError_t launch_grouped_nt_rows(int64_t E, int64_t T, int64_t N, int64_t K, co
   a.tiles_m = (int)((T + BM - 1) / BM + E);
   const dim3 grid((unsigned)(a.tiles_m * a.tiles_n));
   hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRows>), grid, dim3(kWaves * 64), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_grouped_nt_k(int64_t E, int64_t M, int64_t N, int64_t Kpad, const int* kstart,
+                                const int* order, const uint16_t* A, int64_t lda,
+                                const uint16_t* B, int64_t ldb, float* C, int64_t ldc,
+                                int64_t cstride, hipStream_t s) {
+  if (E == 0 || M == 0 || N == 0) return hipSuccess;
+  if (!nt_offsets_fit(Kpad, lda, ldb)) return hipErrorInvalidValue;
+  NtArgs a{};
+  a.A = A; a.B = B; a.C = C; a.lda = lda; a.ldb = ldb; a.ldc = ldc; a.cstride = cstride;
+  a.M = M; a.N = N; a.K = Kpad; a.kstart = kstart; a.order = order; a.E = (int)E;
+  a.vec_store = vec_store_ok(C, ldc, 4) && (cstride * 4) % 16 == 0;
+  a.tiles_m = (int)((M + BM - 1) / BM);
+  a.tiles_n = (int)((N + BN - 1) / BN);
+  const dim3 grid((unsigned)(a.tiles_m * a.tiles_n * E));
+  hipLaunchKernelGGL((gemm_nt_kernel<true, kGroupK>), grid, dim3(kWaves * 64), 0, s, a);
   return hipGetLastError();
 }
 

@@ -33,6 +33,12 @@ hipError_t launch_nvfp4_batched(const uint16_t* x, int64_t E, int64_t R, int64_t
 hipError_t launch_quant_t(int fmt, const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
                           int64_t batch, int64_t xbs, const float* g, uint16_t* out, int64_t ldo,
                           int64_t obs, hipStream_t s);
+// Grouped, transposed, 64-padded: rows [off[e], off[e+1]) of x [T, K] (fmt NONE or MXFP4)
+// land as columns [64 kstart[e], 64 kstart[e+1]) of out [K, ldo] (x_hat^T), zeros past each
+// expert's last row.  kstart from launch_grouped_prep.
+hipError_t launch_quant_t_grouped(int fmt, const uint16_t* x, int64_t T, int64_t K,
+                                  const int64_t* off, const int* kstart, int64_t E,
+                                  uint16_t* out, int64_t ldo, hipStream_t s);
 
 // ---- GEMMs (qf_gemm.hip) ------------------------------------------------------------------
 // C[M,N] = sum_k A(m,k) B(n,k).  a_kmajor: A stored [M][K] (else [K][M]); likewise B.
@@ -48,6 +54,12 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, in
 // Bytes of the FP32 partial buffer `part` an [M, N] FP32-output launch may use (a K-split
 // of the last partial round of tiles).  part may be null: no split.
 size_t gemm_nt_split_bytes(int64_t M, int64_t N);
+// Grouped-K NT (per-expert weight gradient): C + e cstride [M, N] = A[:, k] B[:, k]^T over
+// k in [64 kstart[e], 64 kstart[e+1]) of the padded operands A [M][Kpad], B [N][Kpad].
+hipError_t launch_grouped_nt_k(int64_t E, int64_t M, int64_t N, int64_t Kpad, const int* kstart,
+                                const int* order, const uint16_t* A, int64_t lda,
+                                const uint16_t* B, int64_t ldb, float* C, int64_t ldc,
+                                int64_t cstride, hipStream_t s);
 // Grouped NT: rows [off[e], off[e+1]) of A use B + e * bstride ([N][K], k contiguous).
 hipError_t launch_grouped_nt_rows(int64_t E, int64_t T, int64_t N, int64_t K, const int64_t* off,
                                   const int* tile_start, const uint16_t* A, int64_t lda,
@@ -60,20 +72,10 @@ hipError_t launch_transpose_bf16(const uint16_t* in, int64_t R, int64_t C, int64
                                  int64_t obs, hipStream_t s);
 
 // Grouped over experts (rows [off[e], off[e+1]) of the token-major operands belong to
-// expert e; the host never reads off).  launch_grouped_prep fills two small device arrays:
-// tile_start[E+1] (prefix of per-expert 256-row tile counts) and order[E] (experts by
-// decreasing row count).
+// expert e; the host never reads off).  launch_grouped_prep fills small device arrays:
+// tile_start[E+1] (prefix of per-expert 256-row tile counts), order[E] (experts by
+// decreasing row count) and, when non-null, kstart[E+1] (prefix of per-expert 64-row counts)
+// and korder[E] (the same experts dealt over 8 XCD ranges; see grouped_prep_kernel).
 hipError_t launch_grouped_prep(const int64_t* off, int64_t E, int* tile_start, int* order,
-                               hipStream_t s);
-// Forward / dX shape: C[t, n] = sum_k A[t, k] B_e(n, k) for t in expert e's rows.
-// b_kmajor: B_e stored [N][K] (forward) or [K][N] (dX); bstride = elements per expert.
-hipError_t launch_grouped_rows_ws(int64_t E, int64_t T, int64_t N, int64_t K, const int64_t* off,
-                                  const int* tile_start, const uint16_t* A, int64_t lda,
-                                  const uint16_t* B, int64_t ldb, int64_t bstride, int b_kmajor,
-                                  uint16_t* C, int64_t ldc, hipStream_t s);
-// dW shape: C_e[n, k] = sum over expert e's rows t of dY[t, n] X[t, k]  (FP32, [E][N][K]).
-hipError_t launch_grouped_wgrad_ws(int64_t E, int64_t T, int64_t N, int64_t K, const int64_t* off,
-                                   const int* order, const uint16_t* dY, int64_t ldy,
-                                   const uint16_t* X, int64_t ldx, float* C, hipStream_t s);
-
+                               int* kstart, int* korder, hipStream_t s);
 }  // namespace qf

@@ -434,15 +434,33 @@ constexpr int kTR = 64, kTC = 256;
 
 __device__ __forceinline__ int tslot(int r, int c) { return c ^ (((r >> 3) & 7) << 1); }
 
-template <int FMT>
+template <int FMT, bool GROUPED>
 __global__ __launch_bounds__(kThreads) void quant_t_kernel(const uint16_t* __restrict__ x,
                                                            int64_t R, int64_t K, int64_t ldx,
                                                            int64_t xbs, const float* __restrict__ g,
                                                            uint16_t* __restrict__ out,
-                                                           int64_t ldo, int64_t obs) {
+                                                           int64_t ldo, int64_t obs,
+                                                           const int64_t* __restrict__ off,
+                                                           const int* __restrict__ kstart, int E) {
   __shared__ uint4 tile[kTR * (kTC / 8)];
   const int t = threadIdx.x;
-  const int64_t r0 = (int64_t)blockIdx.y * kTR, c0 = (int64_t)blockIdx.x * kTC;
+  const int64_t c0 = (int64_t)blockIdx.x * kTC;
+  // Input rows [r0, r_end) of this tile; output columns start at oc0.
+  int64_t r0 = (int64_t)blockIdx.y * kTR, r_end = R, oc0 = r0;
+  if (GROUPED) {
+    // Expert e's rows [off[e], off[e+1]) go to the 64-aligned output columns starting at
+    // 64 kstart[e]; the columns past its last row are written as zeros.
+    const int y = blockIdx.y;
+    if (y >= kstart[E]) return;                  // uniform over the block
+    int lo = 0, hi = E;                          // kstart[e] <= y < kstart[e+1]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (kstart[mid] <= y) lo = mid; else hi = mid;
+    }
+    r0 = off[lo] + (int64_t)(y - kstart[lo]) * kTR;
+    r_end = off[lo + 1];
+    oc0 = (int64_t)y * kTR;
+  }
   x += (int64_t)blockIdx.z * xbs;
   out += (int64_t)blockIdx.z * obs;
   float S = 0.0f, six_s = 0.0f;
@@ -455,7 +473,7 @@ __global__ __launch_bounds__(kThreads) void quant_t_kernel(const uint16_t* __res
   for (int i = 0; i < 8; ++i) {             // all eight loads first
     const int64_t gr = r0 + i * 8 + (t >> 5), gc = c0 + (t & 31) * 8;
     vin[i] = make_uint4(0, 0, 0, 0);
-    if (gr < R && gc < K) vin[i] = *reinterpret_cast<const uint4*>(x + gr * ldx + gc);
+    if (gr < r_end && gc < K) vin[i] = *reinterpret_cast<const uint4*>(x + gr * ldx + gc);
   }
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
@@ -468,9 +486,12 @@ __global__ __launch_bounds__(kThreads) void quant_t_kernel(const uint16_t* __res
     } else if (FMT == QF_FMT_MXFP4) {
       uint32_t cw, e;
       mxfp4_chunk(h, cw, e, xh);
-    } else {
+    } else if (FMT == QF_FMT_Q4K) {
       Q4kChunk q;
       q4k_chunk(h, q, xh);
+    } else {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) xh[k] = h[k];
     }
     tile[row * 32 + tslot(row, cc)] = pack8(xh);
   }
@@ -483,8 +504,8 @@ __global__ __launch_bounds__(kThreads) void quant_t_kernel(const uint16_t* __res
     const uint4 v = tile[row * 32 + tslot(row, cb)];
     w[i][0] = v.x; w[i][1] = v.y; w[i][2] = v.z; w[i][3] = v.w;
   }
-  const int64_t orow0 = c0 + cb * 8, ocol = r0 + rb * 8;
-  if (ocol >= R) return;
+  const int64_t orow0 = c0 + cb * 8, ocol = oc0 + rb * 8;
+  if (!GROUPED && ocol >= R) return;
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     if (orow0 + j >= K) break;
@@ -583,29 +604,43 @@ hipError_t launch_q4k(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, uint
   return hipGetLastError();
 }
 
-hipError_t launch_quant_t(int fmt, const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
-                          int64_t batch, int64_t xbs, const float* g, uint16_t* out, int64_t ldo,
-                          int64_t obs, hipStream_t s) {
-  if (R == 0 || K == 0 || batch == 0) return hipSuccess;
-  const dim3 grid((unsigned)((K + kTC - 1) / kTC), (unsigned)((R + kTR - 1) / kTR),
-                  (unsigned)batch);
+template <bool GROUPED>
+hipError_t launch_quant_t_impl(int fmt, const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
+                               int64_t batch, int64_t xbs, const float* g, uint16_t* out,
+                               int64_t ldo, int64_t obs, const int64_t* off, const int* kstart,
+                               int E, int64_t ytiles, hipStream_t s) {
+  const dim3 grid((unsigned)((K + kTC - 1) / kTC), (unsigned)ytiles, (unsigned)batch);
   switch (fmt) {
-    case QF_FMT_NVFP4:
-      hipLaunchKernelGGL(quant_t_kernel<QF_FMT_NVFP4>, grid, dim3(kThreads), 0, s, x, R, K, ldx,
-                         xbs, g, out, ldo, obs);
-      break;
-    case QF_FMT_MXFP4:
-      hipLaunchKernelGGL(quant_t_kernel<QF_FMT_MXFP4>, grid, dim3(kThreads), 0, s, x, R, K, ldx,
-                         xbs, g, out, ldo, obs);
-      break;
-    case QF_FMT_Q4K:
-      hipLaunchKernelGGL(quant_t_kernel<QF_FMT_Q4K>, grid, dim3(kThreads), 0, s, x, R, K, ldx,
-                         xbs, g, out, ldo, obs);
-      break;
+#define QF_QT(F)                                                                            \
+  hipLaunchKernelGGL((quant_t_kernel<F, GROUPED>), grid, dim3(kThreads), 0, s, x, R, K, ldx, \
+                     xbs, g, out, ldo, obs, off, kstart, E);                                 \
+  break;
+    case QF_FMT_NONE: QF_QT(QF_FMT_NONE)
+    case QF_FMT_NVFP4: QF_QT(QF_FMT_NVFP4)
+    case QF_FMT_MXFP4: QF_QT(QF_FMT_MXFP4)
+    case QF_FMT_Q4K: QF_QT(QF_FMT_Q4K)
+#undef QF_QT
     default:
       return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+hipError_t launch_quant_t(int fmt, const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
+                          int64_t batch, int64_t xbs, const float* g, uint16_t* out, int64_t ldo,
+                          int64_t obs, hipStream_t s) {
+  if (R == 0 || K == 0 || batch == 0) return hipSuccess;
+  return launch_quant_t_impl<false>(fmt, x, R, K, ldx, batch, xbs, g, out, ldo, obs, nullptr,
+                                    nullptr, 0, (R + kTR - 1) / kTR, s);
+}
+
+hipError_t launch_quant_t_grouped(int fmt, const uint16_t* x, int64_t T, int64_t K,
+                                  const int64_t* off, const int* kstart, int64_t E,
+                                  uint16_t* out, int64_t ldo, hipStream_t s) {
+  if (T == 0 || K == 0 || E == 0) return hipSuccess;
+  // 64-row tiles: at most sum_e ceil(T_e / 64) <= T / 64 + E
+  return launch_quant_t_impl<true>(fmt, x, T, K, K, 1, 0, nullptr, out, ldo, 0, off, kstart,
+                                   (int)E, (T + kTR - 1) / kTR + E, s);
 }
 
 }  // namespace qf
