@@ -15,10 +15,12 @@
 //    lines and double the L2 request count).
 //  - Operands move global -> LDS with direct-to-LDS loads (no staging registers, no ds_write):
 //    wavefronts 0-3 load A, 4-7 load B, 8 loads of 8 rows each per wavefront and stage.  The
-//    loads of stage s+1 are issued during the first slice of step s and have three of the
-//    step's four 16-deep MFMA slices to land.
-//  - Each MFMA is followed by one fragment read for the next slice (and, in the first slice,
-//    one direct-to-LDS load), so the LDS and memory pipes work while the MFMA pipe is busy.
+//    loads of stage s+1 are spread over four slices (the last of step s-1, right after the
+//    barrier that frees its buffer, and the first two of step s), so the memory pipe sees a
+//    steady stream rather than a burst, and the last of them has a full slice to land.
+//  - Each MFMA is followed by one fragment read for the next slice (and, in three slices of
+//    four, up to one direct-to-LDS load), so the LDS and memory pipes work while the MFMA pipe
+//    is busy.
 //    One barrier per step, before the last slice: it publishes stage s+1 (all loads waited)
 //    and retires every read of stage s (so step s+1 may overwrite that buffer).
 //  - LDS rows hold 64 bf16 (8 chunks of 16 bytes); chunk c of row r sits at slot
@@ -256,7 +258,8 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
   // rst / rkk into ra, rb) and, if LOADS, the direct-to-LDS loads of stage ls into buffer
   // lbuf, issued one per MFMA.  The scheduling fences keep that interleave.
   auto slice = [&](auto reads, auto loads, const bf16x8_t* a, const bf16x8_t* b,
-                   const char* rst, int rkk, bf16x8_t* ra, bf16x8_t* rb, int64_t ls, int lbuf) {
+                   const char* rst, int rkk, bf16x8_t* ra, bf16x8_t* rb, int64_t ls, int lbuf,
+                   int qa = 0, int nq = 0) {
     constexpr bool READS = decltype(reads)::value, LOADS = decltype(loads)::value;
     constexpr int NM = 4 * NJ, NR = 4 + NJ;
 #pragma unroll
@@ -266,30 +269,31 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
       __builtin_amdgcn_sched_barrier(0);
       if (READS && t < NR) read_one(rst, rkk, t, ra, rb);
       if (LOADS) {
-        constexpr int per = (NLD + NM - 1) / NM;
-#pragma unroll
-        for (int q = t * per; q < (t + 1) * per && q < NLD; ++q) dma(ls, lbuf, q);
+        // loads [qa, qa + nq) of stage ls, one per MFMA from the first
+        if (t < nq) dma(ls, lbuf, qa + t);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
   };
-  // One 64-deep step on stage s (buffer s & 1); unless LAST, stage s+1 is loaded into the
-  // other buffer and its first fragments are read during the last slice.
-  auto step = [&](int64_t s, auto last) {
+  // Loads are spread over the step: stage s+1's eight loads per wavefront go out 3 in the
+  // last slice of step s-1 (right after its barrier freed stage s-1's buffer), 3 in slice 0
+  // and 2 in slice 1 of step s; the barrier before slice 3 waits for them.
+  auto step = [&](int64_t s, int64_t s_end, auto last) {
     constexpr bool LAST = decltype(last)::value;
-    const int cur = (int)(s & 1), nxt = cur ^ 1;
+    const int cur = (int)((s - ks0) & 1), nxt = cur ^ 1;
     const char* cs = smem + cur * kStage;
-    slice(std::true_type{}, std::integral_constant<bool, !LAST>{}, fa[0], fb[0], cs, 1, fa[1],
-          fb[1], s + 1, nxt);
-    slice(std::true_type{}, std::false_type{}, fa[1], fb[1], cs, 2, fa[0], fb[0], 0, 0);
+    // Stages past the end are clamped to the last one: their copies land in a buffer that is
+    // not read again, and the epilogue's barrier drains them.
+    const int64_t n1 = s + 1 < s_end ? s + 1 : s_end - 1;
+    const int64_t n2 = s + 2 < s_end ? s + 2 : s_end - 1;
+    slice(std::true_type{}, std::true_type{}, fa[0], fb[0], cs, 1, fa[1], fb[1], n1, nxt, 3, 3);
+    slice(std::true_type{}, std::true_type{}, fa[1], fb[1], cs, 2, fa[0], fb[0], n1, nxt, 6, 2);
     slice(std::true_type{}, std::false_type{}, fa[0], fb[0], cs, 3, fa[1], fb[1], 0, 0);
-    // Stage s+1 has landed everywhere and every read of stage s has returned: after this
-    // barrier the next step may overwrite stage s's buffer.
     __builtin_amdgcn_s_waitcnt(0);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    slice(std::integral_constant<bool, !LAST>{}, std::false_type{}, fa[1], fb[1],
-          smem + nxt * kStage, 0, fa[0], fb[0], 0, 0);
+    slice(std::integral_constant<bool, !LAST>{}, std::true_type{}, fa[1], fb[1],
+          smem + nxt * kStage, 0, fa[0], fb[0], n2, cur, 0, 3);
   };
 
   const int64_t nfull = K / BK;                 // the K tail (dense, second half) follows it
@@ -297,13 +301,17 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
   const int64_t s0 = ks0, s1 = ks1;
   if (s1 > s0) {
 #pragma unroll
-    for (int q = 0; q < NLD; ++q) dma(s0, (int)(s0 & 1), q);
-    __builtin_amdgcn_s_waitcnt(0);               // first stage landed (every counter drained)
+    for (int q = 0; q < NLD; ++q) dma(s0, 0, q);
+    if (s0 + 1 < s1) {
+#pragma unroll
+      for (int q = 0; q < 3; ++q) dma(s0 + 1, 1, q);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    read_all(smem + (s0 & 1) * kStage, 0, fa[0], fb[0]);
-    for (int64_t s = s0; s < s1 - 1; ++s) step(s, std::false_type{});
-    step(s1 - 1, std::true_type{});
+    read_all(smem, 0, fa[0], fb[0]);
+    for (int64_t s = s0; s < s1 - 1; ++s) step(s, s1, std::false_type{});
+    step(s1 - 1, s1, std::true_type{});
   }
   if (krem > 0) {
     // Partial last stage: masked loads through registers into buffer 0.  The wait + barrier
