@@ -302,7 +302,7 @@ qf_status qf_qlinear_fwd(const qf_qlinear_desc* d, const uint16_t* X, const uint
   const uint16_t *Wop, *Aop;
   int64_t ldw_op, lda_op;
   QF_TRY(quantize_operands(d, dm, X, W, w, true, true, &Wop, &ldw_op, &Aop, &lda_op, s));
-  QF_TRY(dev(qf::launch_gemm_nt(d->M, d->N, d->K, Aop, lda_op, Wop, ldw_op, Y, dm.ldy, 0,
+  QF_TRY(dev(qf::launch_gemm_nt(d->M, d->N, d->K, Aop, lda_op, 0, Wop, ldw_op, 0, Y, dm.ldy, 0,
                                 nullptr, s),
              "forward gemm"));
   return ok();
@@ -343,8 +343,8 @@ qf_status qf_qlinear_bwd_ste(const qf_qlinear_desc* d, const uint16_t* dY, const
         QF_TRY(dev(qf::launch_transpose_bf16(src, d->N, d->K, ld, w.whatt, d->N, 1, 0, 0, s),
                    "transpose W_hat"));
       }
-      QF_TRY(dev(qf::launch_gemm_nt(d->M, d->K, d->N, dY, dm.ldy, w.whatt, d->N, dX, dm.ldx, 0,
-                                    nullptr, s),
+      QF_TRY(dev(qf::launch_gemm_nt(d->M, d->K, d->N, dY, dm.ldy, 0, w.whatt, d->N, 0, dX,
+                                    dm.ldx, 0, nullptr, s),
                  "dX gemm"));
     }
     if (dW) {  // dW[N, K] = (dY^T)[N, M] (A_hat^T)[K, M]^T
@@ -359,22 +359,24 @@ qf_status qf_qlinear_bwd_ste(const qf_qlinear_desc* d, const uint16_t* dY, const
         QF_TRY(dev(qf::launch_transpose_bf16(src, d->M, d->K, ld, w.ahatt, d->M, 1, 0, 0, s),
                    "transpose A_hat"));
       }
-      QF_TRY(dev(qf::launch_gemm_nt(d->N, d->K, d->M, w.dyt, d->M, w.ahatt, d->M, dW, d->K, 1,
-                                    w.part, s),
+      QF_TRY(dev(qf::launch_gemm_nt(d->N, d->K, d->M, w.dyt, d->M, 0, w.ahatt, d->M, 0, dW, d->K,
+                                    1, w.part, s),
                  "dW gemm"));
     }
   } else {
+    // Token count not a multiple of 8 (no 16-byte transposed rows): the NT kernel reads
+    // W_hat [N, K], dY [M, N] and A_hat [M, K] in place as operands stored [K'][*], through
+    // transposing LDS reads (slower than the transposed operands, correct for any M).
     QF_TRY(quantize_operands(d, dm, X, W, w, !reuse && dX != nullptr, !reuse && dW != nullptr,
                              &Wop, &ldw_op, &Aop, &lda_op, s));
-    // M not a multiple of 8: the generic kernel reads the [M, *] operands directly.
-    if (dX) {
-      QF_TRY(dev(qf::launch_gemm(d->M, d->K, d->N, dY, dm.ldy, 1, Wop, ldw_op, 0, dX, dm.ldx, 0, s),
+    if (dX)  // dX[M, K] = dY[M, N] W_hat[N, K]
+      QF_TRY(dev(qf::launch_gemm_nt(d->M, d->K, d->N, dY, dm.ldy, 0, Wop, ldw_op, 1, dX, dm.ldx,
+                                    0, nullptr, s),
                  "dX gemm"));
-    }
-    if (dW) {
-      QF_TRY(dev(qf::launch_gemm(d->N, d->K, d->M, dY, dm.ldy, 0, Aop, lda_op, 0, dW, d->K, 1, s),
+    if (dW)  // dW[N, K] = dY[M, N]^T A_hat[M, K]
+      QF_TRY(dev(qf::launch_gemm_nt(d->N, d->K, d->M, dY, dm.ldy, 1, Aop, lda_op, 1, dW, d->K, 1,
+                                    w.part, s),
                  "dW gemm"));
-    }
   }
   return ok();
 }
@@ -500,7 +502,7 @@ qf_status qf_qlinear_grouped_fwd(const qf_grouped_desc* d, const int64_t* group_
                                     g.korder, s),
              "prep"));
   QF_TRY(dev(qf::launch_grouped_nt_rows(d->E, d->T, d->N, d->K, group_offsets, g.tile_start, Aop,
-                                        d->K, Wop, d->K, d->N * d->K, Y, d->N, s),
+                                        d->K, Wop, d->K, 0, d->N * d->K, Y, d->N, s),
              "grouped forward"));
   return ok();
 }
@@ -544,7 +546,7 @@ qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int64_t* gr
                  "transpose expert W_hat"));
     }
     QF_TRY(dev(qf::launch_grouped_nt_rows(d->E, d->T, d->K, d->N, group_offsets, g.tile_start, dY,
-                                          d->N, g.whatt, d->N, d->N * d->K, dX, d->K, s),
+                                          d->N, g.whatt, d->N, 0, d->N * d->K, dX, d->K, s),
                "grouped dX"));
   }
   if (dW) {
@@ -583,19 +585,16 @@ qf_status qf_gemm_bf16_ws(int64_t M, int64_t N, int64_t K, const uint16_t* A, in
     if (!aligned16(C)) return fail(QF_EALIGN, "qf_gemm_bf16: C not 16-byte aligned");
   }
   float* part = nullptr;
-  if (ws != nullptr && a_kmajor && b_kmajor && c_f32) {
+  if (ws != nullptr && c_f32) {
     if ((uintptr_t)ws % kAlign) return fail(QF_EALIGN, "qf_gemm_bf16_ws: workspace not 256-byte aligned");
     if (ws_bytes < qf::gemm_nt_split_bytes(M, N))
       return fail(QF_EINVAL, "qf_gemm_bf16_ws: workspace %zu bytes < required %zu", ws_bytes,
                   qf::gemm_nt_split_bytes(M, N));
     part = static_cast<float*>(ws);
   }
-  if (a_kmajor && b_kmajor)
-    QF_TRY(dev(qf::launch_gemm_nt(M, N, K, A, lda, B, ldb, C, ldc, c_f32, part, S(stream)),
-               "gemm"));
-  else
-    QF_TRY(dev(qf::launch_gemm(M, N, K, A, lda, a_kmajor, B, ldb, b_kmajor, C, ldc, c_f32, S(stream)),
-               "gemm"));
+  QF_TRY(dev(qf::launch_gemm_nt(M, N, K, A, lda, !a_kmajor, B, ldb, !b_kmajor, C, ldc, c_f32,
+                                part, S(stream)),
+             "gemm"));
   return ok();
 }
 

@@ -44,6 +44,8 @@ namespace qf {
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef short v8i16 __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int BM = 256, BN = 256, BK = 64;
@@ -116,6 +118,12 @@ __device__ __forceinline__ void dma16_global(const void* g, void* lds) {
   __builtin_amdgcn_global_load_lds(g, QF_LDS(lds), 16, 0, 0);
 }
 
+// ds_read_b64_tr_b16 (gfx950): transposing 4 x 16-bit LDS read, see the fragment offsets.
+__device__ __forceinline__ v4i16 lds_tr16(const char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) v4i16*)(__attribute__((address_space(3))) char*)(p));
+}
+
 __device__ __forceinline__ uint32_t bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);
   if ((u & 0x7FFFFFFFu) > 0x7F800000u) return 0x7FC0u;
@@ -128,7 +136,7 @@ __device__ __forceinline__ int remap_xcd(int bid, int nb) {
   return (bid % kXcds) * (full / kXcds) + bid / kXcds;
 }
 
-template <bool C_F32, int MODE>
+template <bool C_F32, int MODE, bool A_MN, bool B_MN>
 __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
   __shared__ __attribute__((aligned(16))) char smem[kSmem];
   const int tid = threadIdx.x;
@@ -187,36 +195,71 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
   const int64_t n_end = p.N, K = p.K;
 
   // ---- this lane's loads ----------------------------------------------------------------------
-  // Wavefront w loads operand w >> 2, tile rows 64 (w & 3) .. + 63; load q covers rows
-  // R = 64 (w & 3) + 8 q .. R + 7, lane l lands at row R + l / 8, slot l % 8, and so fetches
+  // Wavefront w loads operand w >> 2 (8 loads of 1 KB per stage, LDS offsets lbase + 1 KB q).
+  // k-major operand ([rows][K], a stage is 256 rows x 128 B): load q covers tile rows
+  // R = 64 (w & 3) + 8 q .. R + 7, lane l lands at row R + l / 8, slot l % 8 and so fetches
   // logical chunk (l % 8) ^ ((row >> 1) % 8) = (l % 8) ^ ((4 (q % 2) + l / 16) % 8).
+  // mn-major operand ([K][rows], a stage is 64 k-rows x 512 B): load q covers k-rows
+  // 16 (w & 3) + 2 q + {0, 1}; lane l lands at k-row 16 (w & 3) + 2 q + l / 32, 16-byte slot
+  // l % 32, and fetches logical chunk (l % 32) ^ (4 (k-row % 4)) (chunk c = columns 8c..8c+7).
   const int op = w >> 2, lw = w & 3;
+  const bool mn = op ? B_MN : A_MN;              // wave-uniform
   const int64_t ld = op ? p.ldb : p.lda;
   const int64_t r0 = op ? n0 : m0;
-  const int64_t rlim = (op ? n_end : m_end) - r0 - 1;   // last valid row of the tile
-  const char* gbase = reinterpret_cast<const char*>((op ? Bp : p.A) + r0 * ld);
-  const __amdgpu_buffer_rsrc_t rsrc = make_rsrc(gbase, (rlim * ld + K) * 2);
+  const int64_t rlim = (op ? n_end : m_end) - r0 - 1;   // last valid tile row (k-major) / column
+  const char* gbase;
+  __amdgpu_buffer_rsrc_t rsrc;
+  int64_t sstride;                               // bytes from one stage to the next
   uint32_t goff[NLD];
+  if (!mn) {
+    gbase = reinterpret_cast<const char*>((op ? Bp : p.A) + r0 * ld);
+    rsrc = make_rsrc(gbase, (rlim * ld + K) * 2);
+    sstride = kRow;
 #pragma unroll
-  for (int q = 0; q < NLD; ++q) {
-    const int64_t row = lw * 64 + q * 8 + (lane >> 3);
-    const int64_t rc = row < rlim ? row : rlim;
-    const int c = (lane & 7) ^ ((4 * (q & 1) + (lane >> 4)) & 7);
-    goff[q] = (uint32_t)((rc * ld + c * 8) * 2);
+    for (int q = 0; q < NLD; ++q) {
+      const int64_t row = lw * 64 + q * 8 + (lane >> 3);
+      const int64_t rc = row < rlim ? row : rlim;
+      const int c = (lane & 7) ^ ((4 * (q & 1) + (lane >> 4)) & 7);
+      goff[q] = (uint32_t)((rc * ld + c * 8) * 2);
+    }
+  } else {
+    gbase = reinterpret_cast<const char*>((op ? Bp : p.A) + r0);
+    rsrc = make_rsrc(gbase, ((K - 1) * ld + rlim + 1) * 2);
+    sstride = (int64_t)BK * ld * 2;
+    const int clim = (int)(rlim / 8);            // last chunk holding valid columns
+#pragma unroll
+    for (int q = 0; q < NLD; ++q) {
+      const int kr = lw * 16 + q * 2 + (lane >> 5);
+      int c = (lane & 31) ^ (4 * (kr & 3));
+      c = c < clim ? c : clim;
+      goff[q] = (uint32_t)(((int64_t)kr * ld + c * 8) * 2);
+    }
   }
-  const int lbase = op * kOpStage + lw * 64 * kRow;     // load q adds 8 q rows
+  const int lbase = op * kOpStage + lw * 8192;   // load q adds 1 KB q
 
-  // ---- fragment offsets: slice kk, fragment i at fo[kk] + i * 4096 (32 rows of 128 bytes) -----
-  // Fragment rows start 32-aligned, so the swizzle term (row >> 1) & 7 is (lane >> 1) & 7.
+  // ---- fragment offsets ----------------------------------------------------------------------
+  // k-major: slice kk, fragment i at fo[kk] + i * 4096 (32 rows of 128 bytes); fragment rows
+  // start 32-aligned, so the swizzle term (row >> 1) & 7 is (lane >> 1) & 7.
+  // mn-major: two ds_read_b64_tr_b16 per fragment (k 0-3 and 4-7 of the lane's 8).  Within
+  // each group of 16 lanes that instruction hands output lane L element j of source lane
+  // 4 j + L / 4 (element L % 4), so source lane 4 j + a points at k-row kb + j, columns
+  // c0 + 4 a .. +3: output lane L then holds k-rows kb .. kb+3 of column c0 + L.  Lane l
+  // (group g = l / 16) serves MFMA lane rows 16 (g % 2) + L and k-half g / 2; fragment f's base
+  // is fo[f], plus (16 kk + 4 h) * 512 bytes for slice kk, half h.
   int foa[4], fob[4];
   {
     const int ra = wm * 128 + (lane & 31), rb = wn * 64 + (lane & 31);
     const int sw = (lane >> 1) & 7;
+    const int g = lane >> 4, j = (lane >> 2) & 3, a = lane & 3;
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int c = 2 * kk + (lane >> 5);
-      foa[kk] = ra * kRow + ((c ^ sw) << 4);
-      fob[kk] = kOpStage + rb * kRow + ((c ^ sw) << 4);
+    for (int x = 0; x < 4; ++x) {
+      const int c = 2 * x + (lane >> 5);
+      // mn-major fragment x: columns start at (wm * 128 or wn * 64) + 32 x
+      const int rowj = 8 * (g >> 1) + j;
+      if (A_MN) foa[x] = rowj * 512 + ((4 * ((wm * 4 + x) ^ j) + 2 * (g & 1) + (a >> 1)) << 4) + 8 * (a & 1);
+      else foa[x] = ra * kRow + ((c ^ sw) << 4);
+      if (B_MN) fob[x] = kOpStage + rowj * 512 + ((4 * ((wn * 2 + x) ^ j) + 2 * (g & 1) + (a >> 1)) << 4) + 8 * (a & 1);
+      else fob[x] = kOpStage + rb * kRow + ((c ^ sw) << 4);
     }
   }
 
@@ -240,15 +283,27 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
   auto dma = [&](int64_t s, int buf, int q) {
     int64_t se = s + krot;
     if (se >= ks1) se -= klen;
-    char* l = smem + buf * kStage + lbase + q * 8 * kRow;
-    if (QF_NT_GLOBAL_LDS) dma16_global(gbase + se * kRow + goff[q], l);
-    else dma16_buf(rsrc, goff[q], (uint32_t)(se * kRow), l);
+    char* l = smem + buf * kStage + lbase + q * 1024;
+    if (QF_NT_GLOBAL_LDS) dma16_global(gbase + se * sstride + goff[q], l);
+    else dma16_buf(rsrc, goff[q], (uint32_t)(se * sstride), l);
   };
   // Fragment read r of a slice, in the order the slice's MFMAs consume them: A0, B0, B1, A1..A3.
+  auto frag = [&](const char* st, int kk, int f, bool is_b) -> bf16x8_t {
+    const bool mnf = is_b ? B_MN : A_MN;
+    if (!mnf) {
+      const int* fo = is_b ? fob : foa;
+      return *reinterpret_cast<const bf16x8_t*>(st + fo[kk] + f * 4096);
+    }
+    const char* base = st + (is_b ? fob[f] : foa[f]) + kk * 16 * 512;
+    const v4i16 lo = lds_tr16(base);
+    const v4i16 hi = lds_tr16(base + 4 * 512);
+    const v8i16 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_bit_cast(bf16x8_t, v);
+  };
   auto read_one = [&](const char* st, int kk, int r, bf16x8_t* a, bf16x8_t* b) {
-    if (r == 0) a[0] = *reinterpret_cast<const bf16x8_t*>(st + foa[kk]);
-    else if (r <= NJ) b[r - 1] = *reinterpret_cast<const bf16x8_t*>(st + fob[kk] + (r - 1) * 4096);
-    else a[r - NJ] = *reinterpret_cast<const bf16x8_t*>(st + foa[kk] + (r - NJ) * 4096);
+    if (r == 0) a[0] = frag(st, kk, 0, false);
+    else if (r <= NJ) b[r - 1] = frag(st, kk, r - 1, true);
+    else a[r - NJ] = frag(st, kk, r - NJ, false);
   };
   auto read_all = [&](const char* st, int kk, bf16x8_t* a, bf16x8_t* b) {
 #pragma unroll
@@ -321,11 +376,16 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int q = 0; q < NLD; ++q) {
-      const int c = (lane & 7) ^ ((4 * (q & 1) + (lane >> 4)) & 7);
+      bool valid;
+      if (!mn) {
+        const int c = (lane & 7) ^ ((4 * (q & 1) + (lane >> 4)) & 7);
+        valid = nfull * BK + c * 8 < K;
+      } else {
+        valid = nfull * BK + lw * 16 + q * 2 + (lane >> 5) < K;
+      }
       uint4 v = make_uint4(0, 0, 0, 0);
-      if (nfull * BK + c * 8 < K)
-        v = *reinterpret_cast<const uint4*>(gbase + nfull * kRow + goff[q]);
-      *reinterpret_cast<uint4*>(smem + lbase + q * 8 * kRow + lane * 16) = v;
+      if (valid) v = *reinterpret_cast<const uint4*>(gbase + nfull * sstride + goff[q]);
+      *reinterpret_cast<uint4*>(smem + lbase + q * 1024 + lane * 16) = v;
     }
     __syncthreads();
 #pragma unroll
@@ -455,10 +515,12 @@ int64_t resident_blocks() {
   return ncu;
 }
 
-// The loads address a 256-row tile with 32-bit byte offsets from the tile's first row.
-bool nt_offsets_fit(int64_t K, int64_t lda, int64_t ldb) {
+// The loads address a tile with 32-bit byte offsets from its first element: a k-major operand
+// spans 256 rows, an mn-major one all K rows.
+bool nt_offsets_fit(int64_t K, int64_t lda, int64_t ldb, bool a_mn = false, bool b_mn = false) {
   const int64_t lim = (int64_t)1 << 31;
-  return K * 2 < lim && (int64_t)BM * lda * 2 < lim && (int64_t)BN * ldb * 2 < lim;
+  const int64_t ra = a_mn ? K + BK : BM, rb = b_mn ? K + BK : BN;
+  return K * 2 < lim && ra * lda * 2 < lim && rb * ldb * 2 < lim;
 }
 
 int vec_store_ok(const void* C, int64_t ldc, int esize) {
@@ -473,10 +535,10 @@ size_t gemm_nt_split_bytes(int64_t M, int64_t N) {
 }
 
 hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
-                          const uint16_t* B, int64_t ldb, void* C, int64_t ldc, int c_f32,
-                          float* part, hipStream_t s) {
+                          int a_mn, const uint16_t* B, int64_t ldb, int b_mn, void* C,
+                          int64_t ldc, int c_f32, float* part, hipStream_t s) {
   if (M == 0 || N == 0) return hipSuccess;
-  if (!nt_offsets_fit(K, lda, ldb)) return hipErrorInvalidValue;
+  if (!nt_offsets_fit(K, lda, ldb, a_mn, b_mn)) return hipErrorInvalidValue;
   NtArgs a{};
   a.A = A; a.B = B; a.C = C; a.lda = lda; a.ldb = ldb; a.ldc = ldc;
   a.M = M; a.N = N; a.K = K;
@@ -500,8 +562,18 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, in
     items = tiles + rem;
   }
   const dim3 grid((unsigned)items);
-  if (c_f32) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense>), grid, dim3(kWaves * 64), 0, s, a);
-  else hipLaunchKernelGGL((gemm_nt_kernel<false, kDense>), grid, dim3(kWaves * 64), 0, s, a);
+  const dim3 blk(kWaves * 64);
+  if (c_f32) {
+    if (a_mn && b_mn) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, true, true>), grid, blk, 0, s, a);
+    else if (b_mn) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, false, true>), grid, blk, 0, s, a);
+    else if (a_mn) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, true, false>), grid, blk, 0, s, a);
+    else hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, false, false>), grid, blk, 0, s, a);
+  } else {
+    if (a_mn && b_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, true, true>), grid, blk, 0, s, a);
+    else if (b_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, false, true>), grid, blk, 0, s, a);
+    else if (a_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, true, false>), grid, blk, 0, s, a);
+    else hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, false, false>), grid, blk, 0, s, a);
+  }
   if (a.part != nullptr)
     hipLaunchKernelGGL(split_reduce_kernel, dim3(BM * BN / (256 * 4), (unsigned)rem), dim3(256),
                        0, s, a);
@@ -510,10 +582,10 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, in
 
 hipError_t launch_grouped_nt_rows(int64_t E, int64_t T, int64_t N, int64_t K, const int64_t* off,
                                   const int* tile_start, const uint16_t* A, int64_t lda,
-                                  const uint16_t* B, int64_t ldb, int64_t bstride, uint16_t* C,
-                                  int64_t ldc, hipStream_t s) {
+                                  const uint16_t* B, int64_t ldb, int b_mn, int64_t bstride,
+                                  uint16_t* C, int64_t ldc, hipStream_t s) {
   if (T == 0 || N == 0 || E == 0) return hipSuccess;
-  if (!nt_offsets_fit(K, lda, ldb)) return hipErrorInvalidValue;
+  if (!nt_offsets_fit(K, lda, ldb, false, b_mn)) return hipErrorInvalidValue;
   NtArgs a{};
   a.A = A; a.B = B; a.C = C; a.lda = lda; a.ldb = ldb; a.ldc = ldc; a.bstride = bstride;
   a.M = T; a.N = N; a.K = K; a.off = off; a.tile_start = tile_start; a.E = (int)E;
@@ -521,7 +593,8 @@ hipError_t launch_grouped_nt_rows(int64_t E, int64_t T, int64_t N, int64_t K, co
   a.tiles_n = (int)((N + BN - 1) / BN);
   a.tiles_m = (int)((T + BM - 1) / BM + E);
   const dim3 grid((unsigned)(a.tiles_m * a.tiles_n));
-  hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRows>), grid, dim3(kWaves * 64), 0, s, a);
+  if (b_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRows, false, true>), grid, dim3(kWaves * 64), 0, s, a);
+  else hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRows, false, false>), grid, dim3(kWaves * 64), 0, s, a);
   return hipGetLastError();
 }
 
@@ -538,7 +611,7 @@ hipError_t launch_grouped_nt_k(int64_t E, int64_t M, int64_t N, int64_t Kpad, co
   a.tiles_m = (int)((M + BM - 1) / BM);
   a.tiles_n = (int)((N + BN - 1) / BN);
   const dim3 grid((unsigned)(a.tiles_m * a.tiles_n * E));
-  hipLaunchKernelGGL((gemm_nt_kernel<true, kGroupK>), grid, dim3(kWaves * 64), 0, s, a);
+  hipLaunchKernelGGL((gemm_nt_kernel<true, kGroupK, false, false>), grid, dim3(kWaves * 64), 0, s, a);
   return hipGetLastError();
 }
 

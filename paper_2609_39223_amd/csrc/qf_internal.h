@@ -40,17 +40,13 @@ hipError_t launch_quant_t_grouped(int fmt, const uint16_t* x, int64_t T, int64_t
                                   const int64_t* off, const int* kstart, int64_t E,
                                   uint16_t* out, int64_t ldo, hipStream_t s);
 
-// ---- GEMMs (qf_gemm.hip) ------------------------------------------------------------------
-// C[M,N] = sum_k A(m,k) B(n,k).  a_kmajor: A stored [M][K] (else [K][M]); likewise B.
-hipError_t launch_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
-                       int a_kmajor, const uint16_t* B, int64_t ldb, int b_kmajor, void* C,
-                       int64_t ldc, int c_f32, hipStream_t s);
-
-// NT GEMM (qf_gemm_nt.hip): C[m, n] = sum_k A[m, k] B[n, k], A [M][K] and B [N][K] with k
-// contiguous (row strides lda, ldb multiples of 8, K multiple of 8).
+// ---- GEMMs --------------------------------------------------------------------------------
+// NT GEMM (qf_gemm_nt.hip): C[m, n] = sum_k A(m, k) B(n, k).  A is [M][K] (k contiguous) or,
+// with a_mn, [K][M] (m contiguous); likewise B [N][K] or [K][N] with b_mn.  Row strides and
+// K multiples of 8.
 hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
-                          const uint16_t* B, int64_t ldb, void* C, int64_t ldc, int c_f32,
-                          float* part, hipStream_t s);
+                          int a_mn, const uint16_t* B, int64_t ldb, int b_mn, void* C,
+                          int64_t ldc, int c_f32, float* part, hipStream_t s);
 // Bytes of the FP32 partial buffer `part` an [M, N] FP32-output launch may use (a K-split
 // of the last partial round of tiles).  part may be null: no split.
 size_t gemm_nt_split_bytes(int64_t M, int64_t N);
@@ -60,18 +56,19 @@ hipError_t launch_grouped_nt_k(int64_t E, int64_t M, int64_t N, int64_t Kpad, co
                                 const int* order, const uint16_t* A, int64_t lda,
                                 const uint16_t* B, int64_t ldb, float* C, int64_t ldc,
                                 int64_t cstride, hipStream_t s);
-// Grouped NT: rows [off[e], off[e+1]) of A use B + e * bstride ([N][K], k contiguous).
+// Grouped NT: rows [off[e], off[e+1]) of A use B + e * bstride ([N][K], k contiguous, or
+// [K][N] with b_mn).
 hipError_t launch_grouped_nt_rows(int64_t E, int64_t T, int64_t N, int64_t K, const int64_t* off,
                                   const int* tile_start, const uint16_t* A, int64_t lda,
-                                  const uint16_t* B, int64_t ldb, int64_t bstride, uint16_t* C,
-                                  int64_t ldc, hipStream_t s);
+                                  const uint16_t* B, int64_t ldb, int b_mn, int64_t bstride,
+                                  uint16_t* C, int64_t ldc, hipStream_t s);
 // bf16 transpose (qf_transpose.hip): out[c][r] = in[r][c] for `batch` matrices spaced ibs / obs
 // elements apart; R and C multiples of 8.
 hipError_t launch_transpose_bf16(const uint16_t* in, int64_t R, int64_t C, int64_t ldi,
                                  uint16_t* out, int64_t ldo, int64_t batch, int64_t ibs,
                                  int64_t obs, hipStream_t s);
 
-// Grouped over experts (rows [off[e], off[e+1]) of the token-major operands belong to
+// Grouped over experts (qf_grouped.hip; rows [off[e], off[e+1]) of the token-major operands belong to
 // expert e; the host never reads off).  launch_grouped_prep fills small device arrays:
 // tile_start[E+1] (prefix of per-expert 256-row tile counts), order[E] (experts by
 // decreasing row count) and, when non-null, kstart[E+1] (prefix of per-expert 64-row counts)
