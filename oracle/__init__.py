@@ -9,11 +9,18 @@ Contents
 * ``qf_oracle.c`` (built to ``_build/liboracle.so`` by :func:`oracle.build.build`):
   plain C codecs for E2M1, E4M3, E8M0, bfloat16, float16 and the three quantizers
   NVFP4 / MXFP4 / Q4_K (QATFactory Sec. 3.2.3, Tab. formats; Eqs. nvfp4-dequant,
-  mxfp4-dequant, q4k-dequant), plus Q4_K block packing (Sec. 3.5, engine-native export).
+  mxfp4-dequant, q4k-dequant), plus Q4_K block packing (Sec. 3.5, engine-native export)
+  and the LoRA merge W + s B A in binary32 (Sec. 3.3, Eqs. qad-lora, export-lora).
 * FP64 linear-layer references in this module: the forward O = A_hat W_hat^T
   (Eq. fakequant, written for row-major activations) and the straight-through backward
   dA = dO W_hat (Eq. activation-ste), dW = dO^T A_hat (Eqs. ste, activation-gradient-error).
   A numpy float64 matmul is the only library primitive used.
+* LoRA-QAD (Sec. 3.3): the merged fake quant W_hat = Q^-1(Q(W + s B A)) (Eq. qad-lora), its
+  export codes Q(W + s B A) (Eq. export-lora), and the FP64 STE gradients of the factors:
+  with G = dO^T A_hat the straight-through gradient of the merged weight (Eq. ste),
+  dB = s G A^T and dA = s B^T G (chain rule through W + s B A).  The MoE variants apply
+  these per expert (Sec. 3.3 "Mixture-of-experts adaptation": unshared factors, or one
+  factor shared by every expert, whose gradient is then the sum over experts).
 """
 from __future__ import annotations
 
@@ -78,6 +85,9 @@ def lib():
         L.or_q4k_unpack_block.argtypes = [_u8p, ctypes.POINTER(ctypes.c_uint16),
                                           ctypes.POINTER(ctypes.c_uint16), ip, ip, ip]
         L.or_q4k_unpack_block.restype = None
+        L.or_lora_merge.argtypes = [_u16p, _i64, _i64, _i64, _f32p, _f32p, _i64, ctypes.c_float,
+                                    _u16p]
+        L.or_lora_merge.restype = None
         _lib = L
     return _lib
 
@@ -259,3 +269,94 @@ def dot_rows(a: np.ndarray, ai, b: np.ndarray, bi) -> np.ndarray:
     A = bf16_array_to_f64(a[np.asarray(ai)])
     B = bf16_array_to_f64(b[np.asarray(bi)])
     return (A * B).sum(axis=1)
+
+
+# ------------------------------------------------------------------------------ LoRA-QAD
+def lora_merge(w: np.ndarray, B: np.ndarray, A: np.ndarray, scale: float = 1.0) -> np.ndarray:
+    """bf16 bits of W + scale * B A (Sec. 3.3, Eq. qad-lora): binary32 merge, one fused
+    multiply-add per rank term in increasing rank order, rounded once to bf16 (the C
+    function or_lora_merge states the reading)."""
+    w, N, K = _rows(w)
+    B = np.ascontiguousarray(B, dtype=np.float32)
+    A = np.ascontiguousarray(A, dtype=np.float32)
+    r = A.shape[0]
+    assert B.shape == (N, r) and A.shape == (r, K)
+    out = np.zeros((N, K), np.uint16)
+    lib().or_lora_merge(_ptr(w, _u16p), N, K, K, _ptr(B, _f32p), _ptr(A, _f32p), r,
+                        float(np.float32(scale)), _ptr(out, _u16p))
+    return out
+
+
+def lora_quant(w: np.ndarray, B: np.ndarray, A: np.ndarray, scale: float, fmt: str,
+               amax_in: float | None = None) -> dict:
+    """Q(W + s B A) with its dequantization (Eqs. qad-lora, export-lora): the quantizer of
+    `fmt` applied to the merged bf16 weight; for NVFP4 the tensor amax is that of the merged
+    weight unless amax_in (a tied-group value) is given.  Returns the quantizer's dict plus
+    'merged' (the bf16 merged weight)."""
+    m = lora_merge(w, B, A, scale)
+    if fmt == "nvfp4":
+        out = nvfp4(m, amax_in)
+        out["amax"] = amax(m) if amax_in is None else float(np.float32(amax_in))
+    elif fmt == "mxfp4":
+        out = mxfp4(m)
+    elif fmt == "q4k":
+        out = q4k(m)
+    else:
+        raise ValueError(fmt)
+    out["merged"] = m
+    return out
+
+
+def lora_grads(dy: np.ndarray, aop: np.ndarray, B: np.ndarray, A: np.ndarray,
+               scale: float = 1.0):
+    """FP64 STE gradients of the LoRA factors (Sec. 3.3 with Eq. ste): G = dO^T A_hat is the
+    straight-through gradient of the merged weight W + s B A, so dB = s G A^T [N, r] and
+    dA = s B^T G [r, K].  Returns (dA, dB)."""
+    G = linear_dw(dy, aop)
+    B64 = np.asarray(B, np.float64)
+    A64 = np.asarray(A, np.float64)
+    s = float(np.float32(scale))
+    return s * (B64.T @ G), s * (G @ A64.T)
+
+
+def _expert_factor(F: np.ndarray, e: int, per_expert_ndim: int) -> np.ndarray:
+    """Expert e's slice of an unshared factor stack, or the shared factor itself."""
+    return F[e] if F.ndim == per_expert_ndim else F
+
+
+def lora_grads_grouped(dy: np.ndarray, aop: np.ndarray, offsets, B: np.ndarray, A: np.ndarray,
+                       scale: float = 1.0):
+    """FP64 factor gradients of the MoE LoRA layer (Sec. 3.3 "Mixture-of-experts adaptation").
+    Rows [off[e], off[e+1]) of dy [T, N] and aop [T, K] belong to expert e.  A is [E, r, K]
+    (one factor per expert) or [r, K] (shared by all experts); B is [E, N, r] or [N, r].
+    Expert e's merged-weight gradient is G_e = dO_e^T A_hat_e; an unshared factor gets its
+    expert's term, a shared factor the sum of the terms over experts in expert order.
+    Returns (dA, dB) shaped like A and B."""
+    off = np.asarray(offsets, np.int64)
+    E = len(off) - 1
+    s = float(np.float32(scale))
+    dA = np.zeros(A.shape, np.float64)
+    dB = np.zeros(B.shape, np.float64)
+    for e in range(E):
+        G = linear_dw(dy[off[e]:off[e + 1]], aop[off[e]:off[e + 1]])
+        Ae = np.asarray(_expert_factor(A, e, 3), np.float64)
+        Be = np.asarray(_expert_factor(B, e, 3), np.float64)
+        ga, gb = s * (Be.T @ G), s * (G @ Ae.T)
+        if A.ndim == 3:
+            dA[e] = ga
+        else:
+            dA += ga
+        if B.ndim == 3:
+            dB[e] = gb
+        else:
+            dB += gb
+    return dA, dB
+
+
+def lora_quant_grouped(w: np.ndarray, B: np.ndarray, A: np.ndarray, scale: float, fmt: str):
+    """Per-expert W_hat_e = Q^-1(Q(W_e + s B_e A_e)) for W [E, N, K] (Sec. 3.3: each expert's
+    merged weight is quantized on its own, with its own NVFP4 tensor amax).  A / B as in
+    lora_grads_grouped.  Returns x_hat [E, N, K]."""
+    E = w.shape[0]
+    return np.stack([lora_quant(w[e], _expert_factor(B, e, 3), _expert_factor(A, e, 3), scale,
+                                fmt)["xhat"] for e in range(E)])

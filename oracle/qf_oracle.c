@@ -470,4 +470,32 @@ void or_q4k_dequant(const uint8_t* packed, int64_t R, int64_t K, uint16_t* xhat)
         }
 }
 
+/* ------------------------------------------------------------------------- */
+/* LoRA merge (Sec. 3.3, Eqs. qad-lora and export-lora): W + s * B A            */
+/* ------------------------------------------------------------------------- */
+/*
+ * The merged weight that LoRA-QAD quantizes in the forward pass and that the exporter
+ * quantizes into the checkpoint.  W is bf16 [N, K] (nn.Linear layout), B is FP32 [N, r],
+ * A is FP32 [r, K] (the trainable low-rank factors), s a scalar multiplier (1 for the
+ * paper's W + BA; LoRA's alpha / r otherwise).
+ * Reading (the paper fixes neither the precision nor the order of the merge):
+ *  1. acc = sum over j = 0, 1, ..., r-1 of B[n][j] * A[j][k] in binary32, one fused
+ *     multiply-add (a single rounding) per rank term, starting from +0;
+ *  2. t = fl(s * acc);  m = fl(W[n][k] + t);
+ *  3. the merged element is bf16(m) (round to nearest even): the merged weight has the
+ *     base weight's type, so the quantizer sees the same input type as without adapters.
+ * IEEE rules apply throughout: W = -0 with t = +0 merges to +0; NaN and Inf propagate.
+ */
+void or_lora_merge(const uint16_t* w, int64_t N, int64_t K, int64_t ldw, const float* B,
+                   const float* A, int64_t r, float s, uint16_t* out) {
+    for (int64_t n = 0; n < N; ++n)
+        for (int64_t k = 0; k < K; ++k) {
+            float acc = 0.0f;
+            for (int64_t j = 0; j < r; ++j) acc = fmaf(B[n * r + j], A[j * K + k], acc);
+            float t = s * acc;
+            float m = or_bf16_to_f32(w[n * ldw + k]) + t;
+            out[n * K + k] = or_bf16_from_f32(m);
+        }
+}
+
 int or_version(void) { return 1; }

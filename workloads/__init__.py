@@ -21,6 +21,11 @@ tensor shapes and value distributions of the layers it quantizes (Sec. 3.2, Sec.
                         popularity (Gumbel-top-8 sampling), hidden 3072, expert intermediate
                         1536: W_gu [128][3072][3072], W_d [128][3072][1536] ~ N(0,0.02).
 * ``q4k_weight``        W [14336,4096] ~ N(0,0.02) x per-row log-normal(0,0.5), X [4096,4096] ~ N(0,1).
+* ``lora_factors``      LoRA-QAD adapters of rank r on an [N, K] weight (Sec. 3.3; the paper's
+                        ranks are 4, 16, 64, 256 and its memory table uses 16): FP32
+                        A [r, K] ~ N(0, 1/K) and B [N, r] ~ N(0, (0.001 sqrt(K/r))^2), so a
+                        trained-like update s B A with s = alpha / r = 2 has std 0.002, a tenth
+                        of the N(0, 0.02) base weight (enough to move many quantization codes).
 
 Draws use ``numpy.random.default_rng(seed)`` in float32, in the order listed.  Large
 tensors are drawn in row chunks from the same generator, so the bytes depend only on the
@@ -156,3 +161,12 @@ def moe_experts(seed: int = 0, tokens: int = 32768, experts: int = 128, hidden: 
     dYd = normal_bf16(rng, (T, hidden), 1.0)
     return {"offsets": offsets, "X": X, "Wgu": Wgu, "Wd": Wd, "Xd": Xd, "dYgu": dYgu,
             "dYd": dYd, "E": experts, "T": T, "hidden": hidden, "inter": inter}
+
+
+def lora_factors(seed: int, N: int, K: int, r: int = 16, alpha: float | None = None) -> dict:
+    """FP32 LoRA factors A [r, K], B [N, r] and the multiplier s = alpha / r (alpha = 2r)."""
+    rng = np.random.default_rng(seed)
+    A = (rng.standard_normal((r, K), dtype=np.float32) * np.float32(1.0 / np.sqrt(K)))
+    B = (rng.standard_normal((N, r), dtype=np.float32) * np.float32(0.001 * np.sqrt(K / r)))
+    a = 2.0 * r if alpha is None else float(alpha)
+    return {"A": A.astype(np.float32), "B": B.astype(np.float32), "r": r, "scale": a / r}
