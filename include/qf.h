@@ -255,6 +255,95 @@ QF_API qf_status qf_gemm_bf16_ws(int64_t M, int64_t N, int64_t K, const uint16_t
                                  void* C, int64_t ldc, int c_f32, void* ws, size_t ws_bytes,
                                  qf_stream_t stream);
 
+/* ---------------------------------------------------------------------------------------
+ * LoRA-QAD (Sec. 3.3 "Full-parameter vs. LoRA-QAD", Eqs. qad-lora and export-lora;
+ * "Mixture-of-experts adaptation")
+ * ------------------------------------------------------------------------------------ */
+/*
+ * Low-rank adapters of a frozen bf16 weight W [N, K]: the student's weight is the merged
+ * W + scale * B A, quantized as a whole (W_hat = Q^-1(Q(W + scale B A)), Eq. qad-lora); the
+ * exporter quantizes the same merged weight (Eq. export-lora).
+ *   A      FP32 [r, K] (row stride K), device, 16-byte aligned.
+ *   B      FP32 [N, r] (row stride r), device, 16-byte aligned.
+ *   r      rank, 1 <= r <= 4096.
+ *   scale  multiplies B A (1 for the paper's W + B A; LoRA's alpha / r otherwise).
+ *   a_shared, b_shared  grouped (MoE) calls only: 0 = one factor per expert (A [E, r, K],
+ *          B [E, N, r]), 1 = one factor shared by every expert (A [r, K] / B [N, r]); the
+ *          paper's hybrid layout shares A for gate/up and B for down.  Ignored elsewhere.
+ * Merge arithmetic (exactly what the library computes): per element, acc = sum over
+ * j = 0..r-1 of B[n][j] A[j][k] in binary32 with one fused multiply-add per term in rising
+ * j, then bf16(W[n][k] + fl(scale * acc)) rounded to nearest even.  The merged weight is
+ * never written to memory by the layer calls.
+ */
+typedef struct {
+    const float* A;
+    const float* B;
+    int64_t r;
+    float scale;
+    int32_t a_shared, b_shared;
+} qf_lora;
+
+/*
+ * qf_lora_amax -- g = max |W + scale B A| over the merged bf16 weight (the NVFP4 tensor
+ * amax of Eq. qad-lora); accumulate as in qf_amax (tied groups: call once per member).
+ */
+QF_API qf_status qf_lora_amax(const uint16_t* W, int64_t N, int64_t K, int64_t ldw,
+                              const qf_lora* lora, float* amax, int accumulate,
+                              qf_stream_t stream);
+
+/*
+ * qf_lora_fakequant -- quantize + dequantize the merged weight W + scale B A (Eqs. qad-lora,
+ * export-lora) with the per-block equations of qf_fakequant_nvfp4 / _mxfp4 / _q4k.
+ *   fmt     QF_FMT_NONE (xhat = the merged bf16 weight), NVFP4, MXFP4 or Q4K.
+ *   amax, amax_mode, s_out   NVFP4 only, as in qf_fakequant_nvfp4 (COMPUTE: g of the merged
+ *           weight); ignored (may be NULL) for the other formats.
+ *   codes [N, K/2], scales [N, K/16 | K/32]   NVFP4 / MXFP4 export outputs, or NULL.
+ *   packed [N, K/256, 144]   Q4_K export blocks, or NULL.
+ *   xhat  bf16 [N, K] (row stride K), or NULL.
+ * An output that the format does not produce must be NULL (QF_EINVAL otherwise).
+ */
+QF_API qf_status qf_lora_fakequant(int fmt, const uint16_t* W, int64_t N, int64_t K,
+                                   int64_t ldw, const qf_lora* lora, float* amax, int amax_mode,
+                                   float* s_out, uint8_t* codes, uint8_t* scales,
+                                   uint8_t* packed, uint16_t* xhat, qf_stream_t stream);
+
+/*
+ * qf_lora_fakequant_transposed -- out[k][n] = x_hat[n][k] of qf_lora_fakequant, bit for bit
+ * (the dX operand of the backward in NT form).  fmt NVFP4 / MXFP4 / Q4K (or NONE: the
+ * merged weight transposed); amax: NVFP4 tensor amax (read only, required for NVFP4).
+ * N % 8 == 0; out bf16 [K, N] with row stride ldo >= N (ldo % 8 == 0).
+ */
+QF_API qf_status qf_lora_fakequant_transposed(int fmt, const uint16_t* W, int64_t N, int64_t K,
+                                              int64_t ldw, const qf_lora* lora,
+                                              const float* amax, uint16_t* out, int64_t ldo,
+                                              qf_stream_t stream);
+
+/* Workspace bytes of qf_qlinear_lora_fwd / _bwd_ste for (d, lora) (host only). */
+QF_API qf_status qf_lora_workspace_size(const qf_qlinear_desc* d, const qf_lora* lora,
+                                        size_t* bytes);
+
+/*
+ * qf_qlinear_lora_fwd -- Y = A_hat W_hat^T with W_hat = Q^-1(Q(W + scale B A)) (Eq. qad-lora;
+ * A_hat as in qf_qlinear_fwd).  d as for qf_qlinear_fwd (wfmt may be NONE: bf16 LoRA);
+ * NVFP4 with d->w_amax == NULL uses g of the merged weight.  W is the frozen base weight.
+ * The workspace keeps W_hat and A_hat for a backward with QF_FLAG_REUSE_WS.
+ */
+QF_API qf_status qf_qlinear_lora_fwd(const qf_qlinear_desc* d, const qf_lora* lora,
+                                     const uint16_t* X, const uint16_t* W, uint16_t* Y, void* ws,
+                                     size_t ws_bytes, qf_stream_t stream);
+
+/*
+ * qf_qlinear_lora_bwd_ste -- straight-through backward of the LoRA layer.  The merged weight's
+ * STE gradient is G = dY^T A_hat (Eq. ste); the frozen W gets none, the factors get
+ *   dB = scale G A^T    FP32 [N, r]       dA = scale B^T G    FP32 [r, K]
+ * (overwritten; either may be NULL), and dX = dY W_hat (Eq. activation-ste; bf16 [M, K], may
+ * be NULL).  G itself is never formed: dB = scale dY^T (A_hat A^T), dA = scale (dY B)^T A_hat.
+ */
+QF_API qf_status qf_qlinear_lora_bwd_ste(const qf_qlinear_desc* d, const qf_lora* lora,
+                                         const uint16_t* dY, const uint16_t* X,
+                                         const uint16_t* W, uint16_t* dX, float* dA, float* dB,
+                                         void* ws, size_t ws_bytes, qf_stream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -38,6 +38,12 @@ class QLinearDesc(ctypes.Structure):
                 ("flags", ctypes.c_uint32)]
 
 
+class LoRA(ctypes.Structure):
+    _fields_ = [("A", ctypes.c_void_p), ("B", ctypes.c_void_p), ("r", ctypes.c_int64),
+                ("scale", ctypes.c_float), ("a_shared", ctypes.c_int32),
+                ("b_shared", ctypes.c_int32)]
+
+
 class GroupedDesc(ctypes.Structure):
     _fields_ = [("E", ctypes.c_int64), ("T", ctypes.c_int64), ("N", ctypes.c_int64),
                 ("K", ctypes.c_int64), ("wfmt", ctypes.c_int32), ("afmt", ctypes.c_int32),
@@ -85,6 +91,19 @@ def lib() -> ctypes.CDLL:
             "qf_gemm_bf16_ws": ([_I, _I, _I, _P, _I, ctypes.c_int, _P, _I, ctypes.c_int, _P, _I,
                                  ctypes.c_int, _P, ctypes.c_size_t, _P], ctypes.c_int),
             "qf_fakequant_transposed": ([ctypes.c_int, _P, _I, _I, _I, _P, _P, _I, _P],
+                                        ctypes.c_int),
+            "qf_lora_amax": ([_P, _I, _I, _I, ctypes.POINTER(LoRA), _P, ctypes.c_int, _P],
+                             ctypes.c_int),
+            "qf_lora_fakequant": ([ctypes.c_int, _P, _I, _I, _I, ctypes.POINTER(LoRA), _P,
+                                   ctypes.c_int, _P, _P, _P, _P, _P, _P], ctypes.c_int),
+            "qf_lora_fakequant_transposed": ([ctypes.c_int, _P, _I, _I, _I, ctypes.POINTER(LoRA),
+                                              _P, _P, _I, _P], ctypes.c_int),
+            "qf_lora_workspace_size": ([ctypes.POINTER(QLinearDesc), ctypes.POINTER(LoRA),
+                                        ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
+            "qf_qlinear_lora_fwd": ([ctypes.POINTER(QLinearDesc), ctypes.POINTER(LoRA), _P, _P,
+                                     _P, _P, ctypes.c_size_t, _P], ctypes.c_int),
+            "qf_qlinear_lora_bwd_ste": ([ctypes.POINTER(QLinearDesc), ctypes.POINTER(LoRA), _P,
+                                         _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P],
                                         ctypes.c_int),
         }
         for name, (args, res) in sig.items():
@@ -242,3 +261,63 @@ def transpose_bf16(x, out):
         raise ValueError("out must be a [C, >=R] row-contiguous tensor")
     _check(lib().qf_transpose_bf16(_ptr(x), R, C, ld, _ptr(_bf16(out)), out.stride(0), _stream()))
     return out
+
+
+# --------------------------------------------------------------------------- LoRA-QAD
+def lora(A, B, scale=1.0, a_shared=False, b_shared=False) -> LoRA:
+    """Adapter descriptor: A FP32 [r, K] (or [E, r, K]), B FP32 [N, r] (or [E, N, r]).
+    The descriptor holds references to A and B, so the device memory it points to stays
+    allocated while the descriptor is alive."""
+    for t in (A, B):
+        if t.dtype != torch.float32 or not t.is_contiguous():
+            raise TypeError("LoRA factors must be contiguous float32 tensors")
+    r = A.shape[-2]
+    if B.shape[-1] != r:
+        raise ValueError("A is [.., r, K] and B is [.., N, r]")
+    lo = LoRA(_ptr(A), _ptr(B), r, float(scale), int(a_shared), int(b_shared))
+    lo._factors = (A, B)
+    return lo
+
+
+def lora_amax(W, lo: LoRA, out, accumulate: bool = False):
+    N, K, ld = _rows(_bf16(W))
+    _check(lib().qf_lora_amax(_ptr(W), N, K, ld, ctypes.byref(lo), _ptr(out), int(accumulate),
+                              _stream()))
+    return out
+
+
+def lora_fakequant(W, lo: LoRA, fmt, amax=None, amax_mode=AMAX_COMPUTE, s_out=None, codes=None,
+                   scales=None, packed=None, xhat=None):
+    N, K, ld = _rows(_bf16(W))
+    _check(lib().qf_lora_fakequant(FMT[fmt], _ptr(W), N, K, ld, ctypes.byref(lo), _ptr(amax),
+                                   amax_mode, _ptr(s_out), _ptr(codes), _ptr(scales),
+                                   _ptr(packed), _ptr(_bf16(xhat)), _stream()))
+
+
+def lora_fakequant_transposed(W, lo: LoRA, fmt, out, amax=None):
+    N, K, ld = _rows(_bf16(W))
+    if out.dim() != 2 or out.shape[0] != K or out.shape[1] < N or out.stride(1) != 1:
+        raise ValueError("out must be a [K, >=N] row-contiguous tensor")
+    _check(lib().qf_lora_fakequant_transposed(FMT[fmt], _ptr(W), N, K, ld, ctypes.byref(lo),
+                                              _ptr(amax), _ptr(_bf16(out)), out.stride(0),
+                                              _stream()))
+    return out
+
+
+def lora_workspace(desc: QLinearDesc, lo: LoRA, device="cuda"):
+    n = ctypes.c_size_t()
+    _check(lib().qf_lora_workspace_size(ctypes.byref(desc), ctypes.byref(lo), ctypes.byref(n)))
+    return torch.empty(max(n.value, 256), dtype=torch.uint8, device=device)
+
+
+def qlinear_lora_fwd(desc, lo: LoRA, X, W, Y, ws):
+    _check(lib().qf_qlinear_lora_fwd(ctypes.byref(desc), ctypes.byref(lo), _ptr(_bf16(X)),
+                                     _ptr(_bf16(W)), _ptr(_bf16(Y)), _ptr(ws), ws.numel(),
+                                     _stream()))
+    return Y
+
+
+def qlinear_lora_bwd_ste(desc, lo: LoRA, dY, X, W, dX, dA, dB, ws):
+    _check(lib().qf_qlinear_lora_bwd_ste(ctypes.byref(desc), ctypes.byref(lo), _ptr(_bf16(dY)),
+                                         _ptr(_bf16(X)), _ptr(_bf16(W)), _ptr(_bf16(dX)),
+                                         _ptr(dA), _ptr(dB), _ptr(ws), ws.numel(), _stream()))

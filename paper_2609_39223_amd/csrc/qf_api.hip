@@ -622,4 +622,250 @@ qf_status qf_transpose_bf16(const uint16_t* in, int64_t R, int64_t C, int64_t ld
   return ok();
 }
 
+// ------------------------------------------------------------------------------- LoRA-QAD
+namespace {
+
+constexpr int64_t kMaxRank = 4096;
+
+qf_status check_lora(const char* fn, const qf_lora* L, int64_t N, int64_t K) {
+  if (!L) return fail(QF_EINVAL, "%s: null lora", fn);
+  if (L->r < 1 || L->r > kMaxRank)
+    return fail(QF_ESHAPE, "%s: rank %lld outside [1, %lld]", fn, (long long)L->r,
+                (long long)kMaxRank);
+  if (N > 0 && K > 0) {
+    if (!L->A || !L->B) return fail(QF_EINVAL, "%s: null LoRA factor", fn);
+    if (!aligned16(L->A) || !aligned16(L->B))
+      return fail(QF_EALIGN, "%s: LoRA factors must be 16-byte aligned", fn);
+  }
+  return QF_OK;
+}
+
+qf::LoraOperand lora_op(const qf_lora* L) {
+  return qf::LoraOperand{L->A, 0, L->B, 0, L->r, L->scale};
+}
+
+// Workspace of the LoRA layer (256-byte aligned regions):
+//   scal  256 B    merged-weight amax scratch
+//   what  [N, K]   W_hat of the merged weight (forward operand; kept for a REUSE backward)
+//   ahat  [M, K]   A_hat, when afmt != NONE
+//   whatt [K, N]   W_hat^T: right operand of dX = dY W_hat in NT form
+//   bt    [r, N]   B^T (FP32)
+//   u, v  [M, rp]  A_hat A^T and dY B (FP32, rp = r rounded up to 16, zeros past r)
+//   part           FP32 row-split partials of the column sums
+struct LoraWs {
+  float* scal;
+  uint16_t* what;
+  uint16_t* ahat;
+  uint16_t* whatt;
+  float* bt;
+  float* u;
+  float* v;
+  float* part;
+};
+
+size_t lora_ws_bytes(const qf_qlinear_desc* d, int64_t r) {
+  const size_t M = d->M, N = d->N, K = d->K, R = r;
+  size_t b = kAlign + up(N * K * 2);
+  if (d->afmt != QF_FMT_NONE) b += up(M * K * 2);
+  const size_t RP = (R + 15) / 16 * 16;
+  b += up(K * N * 2) + up(R * N * 4) + 2 * up(M * RP * 4);
+  const size_t p1 = qf::lora_colsum_part_bytes(d->M, d->N, r);
+  const size_t p2 = qf::lora_colsum_part_bytes(d->M, d->K, r);
+  return b + up(p1 > p2 ? p1 : p2);
+}
+
+LoraWs lora_ws(const qf_qlinear_desc* d, int64_t r, void* ws) {
+  const size_t M = d->M, N = d->N, K = d->K, R = r, RP = (R + 15) / 16 * 16;
+  char* p = static_cast<char*>(ws);
+  LoraWs w{};
+  w.scal = reinterpret_cast<float*>(p); p += kAlign;
+  w.what = reinterpret_cast<uint16_t*>(p); p += up(N * K * 2);
+  if (d->afmt != QF_FMT_NONE) { w.ahat = reinterpret_cast<uint16_t*>(p); p += up(M * K * 2); }
+  w.whatt = reinterpret_cast<uint16_t*>(p); p += up(K * N * 2);
+  w.bt = reinterpret_cast<float*>(p); p += up(R * N * 4);
+  w.u = reinterpret_cast<float*>(p); p += up(M * RP * 4);
+  w.v = reinterpret_cast<float*>(p); p += up(M * RP * 4);
+  w.part = reinterpret_cast<float*>(p);
+  return w;
+}
+
+// NVFP4 tensor amax of the merged weight: the caller's tied-group value, else computed.
+qf_status lora_weight_amax(const qf_qlinear_desc* d, const qf::LoraOperand& L, const uint16_t* W,
+                           int64_t ldw, float* scratch, const float** g, hipStream_t s) {
+  *g = d->w_amax;
+  if (d->wfmt != QF_FMT_NVFP4 || *g) return QF_OK;
+  QF_TRY(dev(qf::launch_fill_f32(scratch, 1, 0.0f, s), "amax init"));
+  QF_TRY(dev(qf::launch_lora_amax(L, W, d->N, d->K, ldw, 1, 0, scratch, s), "merged amax"));
+  *g = scratch;
+  return QF_OK;
+}
+
+}  // namespace
+
+qf_status qf_lora_amax(const uint16_t* W, int64_t N, int64_t K, int64_t ldw, const qf_lora* lora,
+                       float* amax, int accumulate, qf_stream_t stream) {
+  const char* fn = "qf_lora_amax";
+  QF_TRY(check_quant_input(fn, W, N, K, ldw, 8));
+  QF_TRY(check_lora(fn, lora, N, K));
+  if (!amax) return fail(QF_EINVAL, "%s: null amax", fn);
+  if (accumulate != 0 && accumulate != 1) return fail(QF_EINVAL, "%s: accumulate must be 0/1", fn);
+  hipStream_t s = S(stream);
+  if (!accumulate) QF_TRY(dev(qf::launch_fill_f32(amax, 1, 0.0f, s), "amax init"));
+  QF_TRY(dev(qf::launch_lora_amax(lora_op(lora), W, N, K, ldw, 1, 0, amax, s), "merged amax"));
+  return ok();
+}
+
+qf_status qf_lora_fakequant(int fmt, const uint16_t* W, int64_t N, int64_t K, int64_t ldw,
+                            const qf_lora* lora, float* amax, int amax_mode, float* s_out,
+                            uint8_t* codes, uint8_t* scales, uint8_t* packed, uint16_t* xhat,
+                            qf_stream_t stream) {
+  const char* fn = "qf_lora_fakequant";
+  if (!fmt_valid(fmt)) return fail(QF_EINVAL, "%s: bad format %d", fn, fmt);
+  QF_TRY(check_quant_input(fn, W, N, K, ldw, block_of(fmt)));
+  QF_TRY(check_lora(fn, lora, N, K));
+  const bool fp4 = fmt == QF_FMT_NVFP4 || fmt == QF_FMT_MXFP4;
+  if ((codes || scales) && !fp4) return fail(QF_EINVAL, "%s: codes/scales are NVFP4/MXFP4 outputs", fn);
+  if (packed && fmt != QF_FMT_Q4K) return fail(QF_EINVAL, "%s: packed is the Q4_K output", fn);
+  QF_TRY(check_out("qf_lora_fakequant: codes", codes));
+  QF_TRY(check_out("qf_lora_fakequant: scales", scales));
+  QF_TRY(check_out("qf_lora_fakequant: packed", packed));
+  QF_TRY(check_out("qf_lora_fakequant: xhat", xhat));
+  hipStream_t s = S(stream);
+  const qf::LoraOperand L = lora_op(lora);
+  if (fmt == QF_FMT_NVFP4) {
+    if (!amax) return fail(QF_EINVAL, "%s: NVFP4 needs amax", fn);
+    if (amax_mode != QF_AMAX_COMPUTE && amax_mode != QF_AMAX_GIVEN)
+      return fail(QF_EINVAL, "%s: bad amax_mode %d", fn, amax_mode);
+    if (s_out && s_out == amax) return fail(QF_EINVAL, "%s: s_out aliases amax", fn);
+    if (amax_mode == QF_AMAX_COMPUTE) {
+      QF_TRY(dev(qf::launch_fill_f32(amax, 1, 0.0f, s), "amax init"));
+      QF_TRY(dev(qf::launch_lora_amax(L, W, N, K, ldw, 1, 0, amax, s), "merged amax"));
+    }
+    if ((N == 0 || K == 0) && s_out) QF_TRY(dev(qf::launch_fill_f32(s_out, 1, 0.0f, s), "S"));
+  } else if (s_out) {
+    return fail(QF_EINVAL, "%s: s_out is an NVFP4 output", fn);
+  }
+  QF_TRY(dev(qf::launch_lora_quant(fmt, L, W, N, K, ldw, 1, 0, amax, s_out, codes, scales, packed,
+                                   xhat, s),
+             "merged quantize"));
+  return ok();
+}
+
+qf_status qf_lora_fakequant_transposed(int fmt, const uint16_t* W, int64_t N, int64_t K,
+                                       int64_t ldw, const qf_lora* lora, const float* amax,
+                                       uint16_t* out, int64_t ldo, qf_stream_t stream) {
+  const char* fn = "qf_lora_fakequant_transposed";
+  if (!fmt_valid(fmt)) return fail(QF_EINVAL, "%s: bad format %d", fn, fmt);
+  QF_TRY(check_quant_input(fn, W, N, K, ldw, block_of(fmt)));
+  QF_TRY(check_lora(fn, lora, N, K));
+  if (N % 8) return fail(QF_ESHAPE, "%s: N=%lld is not a multiple of 8", fn, (long long)N);
+  if (N == 0 || K == 0) return ok();
+  if (fmt == QF_FMT_NVFP4 && !amax) return fail(QF_EINVAL, "%s: NVFP4 needs amax", fn);
+  if (!out) return fail(QF_EINVAL, "%s: null output", fn);
+  QF_TRY(check_mat("qf_lora_fakequant_transposed: out", out, K, N, ldo, true));
+  QF_TRY(dev(qf::launch_lora_quant_t(fmt, lora_op(lora), W, N, K, ldw, 1, 0, amax, out, ldo, 0,
+                                     S(stream)),
+             "merged quantize (transposed)"));
+  return ok();
+}
+
+qf_status qf_lora_workspace_size(const qf_qlinear_desc* d, const qf_lora* lora, size_t* bytes) {
+  Dims dm;
+  QF_TRY(check_desc("qf_lora_workspace_size", d, &dm));
+  QF_TRY(check_lora("qf_lora_workspace_size", lora, 0, 0));
+  if (!bytes) return fail(QF_EINVAL, "qf_lora_workspace_size: null output");
+  *bytes = lora_ws_bytes(d, lora->r);
+  return ok();
+}
+
+qf_status qf_qlinear_lora_fwd(const qf_qlinear_desc* d, const qf_lora* lora, const uint16_t* X,
+                              const uint16_t* W, uint16_t* Y, void* ws, size_t ws_bytes,
+                              qf_stream_t stream) {
+  const char* fn = "qf_qlinear_lora_fwd";
+  Dims dm;
+  QF_TRY(check_desc(fn, d, &dm));
+  QF_TRY(check_lora(fn, lora, d->N, d->K));
+  QF_TRY(check_mat("qf_qlinear_lora_fwd: X", X, d->M, d->K, dm.ldx, true));
+  QF_TRY(check_mat("qf_qlinear_lora_fwd: W", W, d->N, d->K, dm.ldw, true));
+  QF_TRY(check_mat("qf_qlinear_lora_fwd: Y", Y, d->M, d->N, dm.ldy, true));
+  QF_TRY(check_ws(fn, lora_ws_bytes(d, lora->r), ws, ws_bytes));
+  hipStream_t s = S(stream);
+  LoraWs w = lora_ws(d, lora->r, ws);
+  const qf::LoraOperand L = lora_op(lora);
+  const float* g;
+  QF_TRY(lora_weight_amax(d, L, W, dm.ldw, w.scal, &g, s));
+  QF_TRY(dev(qf::launch_lora_quant(d->wfmt, L, W, d->N, d->K, dm.ldw, 1, 0, g, nullptr, nullptr,
+                                   nullptr, nullptr, w.what, s),
+             "merged quantize"));
+  const uint16_t* Aop = X;
+  int64_t lda = dm.ldx;
+  if (d->afmt != QF_FMT_NONE) {
+    QF_TRY(fakequant_to(d->afmt, X, d->M, d->K, dm.ldx, d->a_amax, nullptr, w.ahat, s));
+    Aop = w.ahat;
+    lda = d->K;
+  }
+  QF_TRY(dev(qf::launch_gemm_nt(d->M, d->N, d->K, Aop, lda, 0, w.what, d->K, 0, Y, dm.ldy, 0,
+                                nullptr, s),
+             "forward gemm"));
+  return ok();
+}
+
+qf_status qf_qlinear_lora_bwd_ste(const qf_qlinear_desc* d, const qf_lora* lora,
+                                  const uint16_t* dY, const uint16_t* X, const uint16_t* W,
+                                  uint16_t* dX, float* dA, float* dB, void* ws, size_t ws_bytes,
+                                  qf_stream_t stream) {
+  const char* fn = "qf_qlinear_lora_bwd_ste";
+  Dims dm;
+  QF_TRY(check_desc(fn, d, &dm));
+  QF_TRY(check_lora(fn, lora, d->N, d->K));
+  const bool grads = dA || dB;
+  QF_TRY(check_mat("qf_qlinear_lora_bwd_ste: dY", dY, d->M, d->N, dm.ldy, true));
+  QF_TRY(check_mat("qf_qlinear_lora_bwd_ste: X", X, d->M, d->K, dm.ldx, grads));
+  QF_TRY(check_mat("qf_qlinear_lora_bwd_ste: W", W, d->N, d->K, dm.ldw, dX != nullptr));
+  QF_TRY(check_mat("qf_qlinear_lora_bwd_ste: dX", dX, d->M, d->K, dm.ldx, false));
+  QF_TRY(check_out("qf_qlinear_lora_bwd_ste: dA", dA));
+  QF_TRY(check_out("qf_qlinear_lora_bwd_ste: dB", dB));
+  QF_TRY(check_ws(fn, lora_ws_bytes(d, lora->r), ws, ws_bytes));
+  hipStream_t s = S(stream);
+  LoraWs w = lora_ws(d, lora->r, ws);
+  const qf::LoraOperand L = lora_op(lora);
+  const bool reuse = (d->flags & QF_FLAG_REUSE_WS) != 0;
+  const int64_t M = d->M, N = d->N, K = d->K, r = lora->r, rp = (r + 15) / 16 * 16;
+  if (dX && M > 0 && K > 0) {  // dX[M, K] = dY[M, N] (W_hat^T)[K, N]^T
+    if (reuse) {
+      QF_TRY(dev(qf::launch_transpose_bf16(w.what, N, K, K, w.whatt, N, 1, 0, 0, s),
+                 "transpose W_hat"));
+    } else {
+      const float* g;
+      QF_TRY(lora_weight_amax(d, L, W, dm.ldw, w.scal, &g, s));
+      QF_TRY(dev(qf::launch_lora_quant_t(d->wfmt, L, W, N, K, dm.ldw, 1, 0, g, w.whatt, N, 0, s),
+                 "merged quantize (transposed)"));
+    }
+    QF_TRY(dev(qf::launch_gemm_nt(M, K, N, dY, dm.ldy, 0, w.whatt, N, 0, dX, dm.ldx, 0, nullptr,
+                                  s),
+               "dX gemm"));
+  }
+  if (!grads) return ok();
+  const uint16_t* Aop = X;
+  int64_t lda = dm.ldx;
+  if (d->afmt != QF_FMT_NONE) {
+    if (!reuse && M > 0)
+      QF_TRY(fakequant_to(d->afmt, X, M, K, dm.ldx, d->a_amax, nullptr, w.ahat, s));
+    Aop = w.ahat;
+    lda = K;
+  }
+  if (dB) {  // dB = scale dY^T (A_hat A^T)
+    QF_TRY(dev(qf::launch_lora_rowdot(Aop, M, K, lda, L.A, K, r, w.u, rp, s), "A_hat A^T"));
+    QF_TRY(dev(qf::launch_lora_colsum(dY, M, N, dm.ldy, w.u, rp, r, L.scale, w.part, 0, dB, s),
+               "dB"));
+  }
+  if (dA) {  // dA = scale (dY B)^T A_hat
+    QF_TRY(dev(qf::launch_transpose_f32(L.B, N, r, w.bt, s), "B^T"));
+    QF_TRY(dev(qf::launch_lora_rowdot(dY, M, N, dm.ldy, w.bt, N, r, w.v, rp, s), "dY B"));
+    QF_TRY(dev(qf::launch_lora_colsum(Aop, M, K, lda, w.v, rp, r, L.scale, w.part, 1, dA, s),
+               "dA"));
+  }
+  return ok();
+}
+
 }  // extern "C"

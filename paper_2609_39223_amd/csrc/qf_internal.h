@@ -75,4 +75,45 @@ hipError_t launch_transpose_bf16(const uint16_t* in, int64_t R, int64_t C, int64
 // and korder[E] (the same experts dealt over 8 XCD ranges; see grouped_prep_kernel).
 hipError_t launch_grouped_prep(const int64_t* off, int64_t E, int* tile_start, int* order,
                                int* kstart, int* korder, hipStream_t s);
+
+// ---- LoRA-QAD (qf_lora.hip) ------------------------------------------------------------------
+// Low-rank factors of a merged weight W + scale * B A: A FP32 [r, K] (row stride K), B FP32
+// [N, r] (row stride r); for `batch` tensors, tensor z uses A + z * a_stride and
+// B + z * b_stride (a stride of 0 shares the factor).  A and B 16-byte aligned.
+struct LoraOperand {
+  const float* A;
+  int64_t a_stride;
+  const float* B;
+  int64_t b_stride;
+  int64_t r;
+  float scale;
+};
+// amax of the merged bf16 tensors folded into amax[z] (bit-pattern atomic max; initialize).
+hipError_t launch_lora_amax(const LoraOperand& L, const uint16_t* w, int64_t N, int64_t K,
+                            int64_t ldw, int64_t batch, int64_t wbs, float* amax, hipStream_t s);
+// Quantize-dequantize of the merged tensors (fmt NONE: the merged bf16 tensor itself).  Row
+// outputs per tensor z at z * N * (K/2 | K/block | (K/256) * 144 | K); g: NVFP4 amax per tensor.
+hipError_t launch_lora_quant(int fmt, const LoraOperand& L, const uint16_t* w, int64_t N,
+                             int64_t K, int64_t ldw, int64_t batch, int64_t wbs, const float* g,
+                             float* s_out, uint8_t* codes, uint8_t* scales, uint8_t* packed,
+                             uint16_t* xhat, hipStream_t s);
+// Same with transposed bf16 output out[k][n] (row stride ldo, tensor z at out + z * obs).
+hipError_t launch_lora_quant_t(int fmt, const LoraOperand& L, const uint16_t* w, int64_t N,
+                               int64_t K, int64_t ldw, int64_t batch, int64_t wbs, const float* g,
+                               uint16_t* out, int64_t ldo, int64_t obs, hipStream_t s);
+// P[m][j] = sum_k X[m][k] F[j][k]: X bf16 [M, K] (ldx), F FP32 [r, K] (ldf, multiple of 4,
+// 16-byte aligned), P FP32 [M, ldp] with ldp = r rounded up to 16 (zeros past r).  K a
+// multiple of 8.
+hipError_t launch_lora_rowdot(const uint16_t* X, int64_t M, int64_t K, int64_t ldx, const float* F,
+                              int64_t ldf, int64_t r, float* P, int64_t ldp, hipStream_t s);
+// out = scale * sum_m Big[m][c] Sm[m][j] as out[c][j] (or out[j][c] when transposed): Big bf16
+// [M, C] (ldb, C a multiple of 4), Sm FP32 [M, lds_] as the row-dot writes it (lds_ = r
+// rounded up to 16, zeros past r, 16-byte aligned); `part` holds
+// lora_colsum_part_bytes(M, C, r) bytes of row-split partials (summed in a fixed order).
+size_t lora_colsum_part_bytes(int64_t M, int64_t C, int64_t r);
+hipError_t launch_lora_colsum(const uint16_t* Big, int64_t M, int64_t C, int64_t ldb,
+                              const float* Sm, int64_t lds_, int64_t r, float scale,
+                              float* part, int transposed, float* out, hipStream_t s);
+// Ft [r, N] = F^T for FP32 F [N, r].
+hipError_t launch_transpose_f32(const float* F, int64_t N, int64_t r, float* Ft, hipStream_t s);
 }  // namespace qf

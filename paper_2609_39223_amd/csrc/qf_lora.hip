@@ -1,0 +1,486 @@
+// LoRA-QAD kernels for gfx950 (QATFactory Sec. 3.3, Eqs. qad-lora and export-lora).
+//
+// Forward / export: W_hat = Q^-1(Q(W + s B A)) with the rank-r update merged inside the
+// quantizer's tile load, so the merged weight never goes to HBM.  W is bf16 [N, K], A FP32
+// [r, K], B FP32 [N, r].  Each merged element is
+//     acc = sum_j B[n][j] A[j][k]   (binary32, one fused multiply-add per rank term, j rising)
+//     m   = bf16(W[n][k] + fl(s * acc))
+// and then goes through the same per-chunk codec as an unmerged tensor.
+//
+// Backward (straight-through, Eq. ste): the merged weight's gradient G = dY^T A_hat is never
+// formed; the factor gradients are regrouped around the rank-r products
+//     dB = s G A^T = s dY^T (A_hat A^T),      dA = s B^T G = s (dY B)^T A_hat,
+// i.e. two row-dot products (U = A_hat A^T, V = dY B: [M, r], contraction over the
+// contiguous axis) and two column sums (dY^T U: [N, r], V^T A_hat: [r, K], contraction over
+// the M rows).  All four stream a bf16 matrix once from HBM against a small FP32 factor
+// held on chip; the column sums split M into row ranges whose FP32 partials are added in a
+// fixed order (deterministic results).
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "qf.h"
+#include "qf_codecs.h"
+#include "qf_internal.h"
+
+namespace qf {
+namespace {
+
+using namespace codec;
+
+constexpr int kThreads = 256;
+constexpr int kRC = 16;   // rank terms staged per pass (B rows in LDS; row-dot outputs)
+
+// ====================================================================== merged quantizer
+enum { kOutRows = 0, kOutTransposed = 1, kOutAmax = 2 };
+
+struct MergeArgs {
+  const uint16_t* w;      // [N, K] row stride ldw; tensor z at w + z * wbs
+  int64_t N, K, ldw, wbs;
+  const float* A;         // [r, K] (row stride K); tensor z at A + z * abs (0: shared)
+  int64_t abs;
+  const float* B;         // [N, r] (row stride r); tensor z at B + z * bbs (0: shared)
+  int64_t bbs;
+  int r;
+  float scale;
+  const float* g;         // NVFP4 tensor amax per tensor (read)
+  float* amax;            // kOutAmax: running max per tensor (bit-pattern atomic max)
+  float* s_out;           // NVFP4 decode scale per tensor, or null
+  uint8_t* codes;         // [N, K/2] per tensor, or null
+  uint8_t* scales;        // [N, K/16] E4M3 or [N, K/32] E8M0 per tensor, or null
+  uint8_t* packed;        // Q4_K [N, K/256, 144] per tensor, or null
+  uint16_t* xhat;         // [N, K] per tensor, or null
+  uint16_t* out;          // kOutTransposed: [K, N] row stride ldo, tensor z at out + z * obs
+  int64_t ldo, obs;
+};
+
+// One 64 x 256 tile of tensor blockIdx.z (the tile layout of store_tile_transposed: lane t
+// owns chunk t % 32 of rows 8 i + t / 32).
+template <int FMT, int OUT>
+__global__ __launch_bounds__(kThreads) void lora_quant_kernel(MergeArgs p) {
+  __shared__ float bs[kTR * kRC];                     // B rows of the tile, one rank pass
+  __shared__ uint4 tile[OUT == kOutTransposed ? kTR * (kTC / 8) : 1];
+  const int t = threadIdx.x, cc = t & 31, rs = t >> 5;
+  const int64_t z = blockIdx.z;
+  const int64_t c0 = (int64_t)blockIdx.x * kTC, r0 = (int64_t)blockIdx.y * kTR;
+  const int64_t col = c0 + cc * 8;
+  const int64_t N = p.N, K = p.K;
+  const bool col_ok = col < K;
+  const uint16_t* w = p.w + z * p.wbs;
+  const float* A = p.A + z * p.abs;
+  const float* B = p.B + z * p.bbs;
+
+  uint4 vin[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {                       // the W tile's loads go out first
+    const int64_t row = r0 + 8 * i + rs;
+    vin[i] = make_uint4(0, 0, 0, 0);
+    if (row < N && col_ok) vin[i] = *reinterpret_cast<const uint4*>(w + row * p.ldw + col);
+  }
+
+  float acc[8][8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[i][k] = 0.0f;
+
+  for (int j0 = 0; j0 < p.r; j0 += kRC) {
+    const int nj = p.r - j0 < kRC ? p.r - j0 : kRC;
+    __syncthreads();                                  // previous pass's reads of bs are done
+    for (int idx = t; idx < kTR * kRC; idx += kThreads) {
+      const int rr = idx / kRC, jj = idx % kRC;
+      const int64_t row = r0 + rr;
+      bs[idx] = (row < N && jj < nj) ? B[row * p.r + j0 + jj] : 0.0f;
+    }
+    __syncthreads();
+#pragma unroll 2
+    for (int jj = 0; jj < nj; ++jj) {
+      float a[8];
+      if (col_ok) {
+        const float4 lo = *reinterpret_cast<const float4*>(A + (int64_t)(j0 + jj) * K + col);
+        const float4 hi = *reinterpret_cast<const float4*>(A + (int64_t)(j0 + jj) * K + col + 4);
+        a[0] = lo.x; a[1] = lo.y; a[2] = lo.z; a[3] = lo.w;
+        a[4] = hi.x; a[5] = hi.y; a[6] = hi.z; a[7] = hi.w;
+      } else {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) a[k] = 0.0f;
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float b = bs[(8 * i + rs) * kRC + jj];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) acc[i][k] = __builtin_fmaf(b, a[k], acc[i][k]);
+      }
+    }
+  }
+
+  float S = 0.0f, six_s = 0.0f;
+  if (FMT == QF_FMT_NVFP4 && OUT != kOutAmax) {
+    S = p.g[z] / 2688.0f;                             // g maps to 6 * 448
+    six_s = 6.0f * S;
+    if (OUT == kOutRows && p.s_out && blockIdx.x == 0 && blockIdx.y == 0 && t == 0) p.s_out[z] = S;
+  }
+  uint32_t mx = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int64_t row = r0 + 8 * i + rs;
+    const bool ok = row < N && col_ok;
+    uint32_t h[8], xh[8];
+    unpack8(vin[i], h);
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {                     // m = bf16(W + fl(s * acc))
+      const float upd = p.scale * acc[i][k];
+      h[k] = bf16_rne(as_f32(h[k] << 16) + upd);
+    }
+    if (OUT == kOutAmax) {
+      const uint32_t a = ok ? max_abs_bits8(h) : 0u;
+      mx = a > mx ? a : mx;
+      continue;
+    }
+    uint32_t cw = 0, sc = 0;
+    if (FMT == QF_FMT_NVFP4) {
+      nvfp4_chunk(h, S, six_s, cw, sc, xh);
+    } else if (FMT == QF_FMT_MXFP4) {
+      mxfp4_chunk(h, cw, sc, xh);
+    } else if (FMT == QF_FMT_Q4K) {
+      Q4kChunk q;
+      q4k_chunk(h, q, xh);
+      if (OUT == kOutRows && p.packed) {
+        const int64_t kb = K / 256;
+        q4k_store(q, cc, ok, p.packed + ((z * N + row) * kb + col / 256) * 144);
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) xh[k] = h[k];
+    }
+    if (OUT == kOutTransposed) {
+      const int lr = 8 * i + rs;
+      tile[lr * 32 + tslot(lr, cc)] = pack8(xh);
+    } else if (ok) {
+      const int64_t e = (z * N + row) * K + col;      // element index of this chunk
+      if (FMT == QF_FMT_NVFP4 || FMT == QF_FMT_MXFP4) {
+        if (p.codes) *reinterpret_cast<uint32_t*>(p.codes + e / 2) = cw;
+        constexpr int kBlk = FMT == QF_FMT_NVFP4 ? 16 : 32;
+        if (p.scales && (cc & (kBlk / 8 - 1)) == 0) p.scales[e / kBlk] = (uint8_t)sc;
+      }
+      if (p.xhat) *reinterpret_cast<uint4*>(p.xhat + e) = pack8(xh);
+    }
+  }
+  if (OUT == kOutAmax) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      const uint32_t o = (uint32_t)__shfl_xor((int)mx, off, 64);
+      mx = o > mx ? o : mx;
+    }
+    __shared__ uint32_t wmax[kThreads / 64];
+    if ((t & 63) == 0) wmax[t >> 6] = mx;
+    __syncthreads();
+    if (t == 0) {
+      uint32_t b = wmax[0];
+      for (int i = 1; i < kThreads / 64; ++i) b = wmax[i] > b ? wmax[i] : b;
+      if (b != 0u) atomicMax(reinterpret_cast<unsigned int*>(p.amax + z), b << 16);
+    }
+  }
+  if (OUT == kOutTransposed) {
+    __syncthreads();
+    store_tile_transposed(tile, t, p.out + z * p.obs, p.ldo, c0, r0, K, N);
+  }
+}
+
+// ============================================================================ row-dot
+// P[m][j0 + jj] = sum_k X[m][k] F[j0 + jj][k] for jj < 16: X bf16 [M, K] (row stride ldx),
+// F FP32 [r, K] (row stride ldf), P FP32 [M, ldp] with ldp >= r rounded up to 16 (the ranks
+// past r get zeros).  A block of 4 waves takes
+// 16 rows (4 per wave); each step covers 512 columns (8 per lane): the F slab [16][512] is
+// staged in LDS in two planes of 4 columns so every lane's 16-byte reads are contiguous
+// across the wave.  After the K loop each lane holds 4 x 16 partial sums, which a
+// recursive-halving exchange (63 shuffles, fixed pairing) reduces so that lane l ends with
+// output l = (row l / 16, rank l % 16).
+constexpr int kRowsPerWave = 4;
+constexpr int kStepK = 512;
+
+__global__ __launch_bounds__(kThreads) void lora_rowdot_kernel(const uint16_t* __restrict__ X,
+                                                               int64_t M, int64_t K, int64_t ldx,
+                                                               const float* __restrict__ F,
+                                                               int64_t ldf, int r,
+                                                               float* __restrict__ P,
+                                                               int64_t ldp) {
+  __shared__ float4 fs[kRC * 2 * 64];                 // [jj][plane][lane] x 4 columns
+  const int t = threadIdx.x, lane = t & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int j0 = blockIdx.y * kRC;
+  const int nj = r - j0 < kRC ? r - j0 : kRC;
+  const int64_t m0 = (int64_t)blockIdx.x * (4 * kRowsPerWave) + wv * kRowsPerWave;
+  float acc[kRowsPerWave][kRC];
+#pragma unroll
+  for (int i = 0; i < kRowsPerWave; ++i)
+#pragma unroll
+    for (int j = 0; j < kRC; ++j) acc[i][j] = 0.0f;
+
+  for (int64_t k0 = 0; k0 < K; k0 += kStepK) {
+    const int64_t kc = k0 + lane * 8;
+    uint4 xv[kRowsPerWave];
+#pragma unroll
+    for (int i = 0; i < kRowsPerWave; ++i) {
+      xv[i] = make_uint4(0, 0, 0, 0);
+      if (m0 + i < M && kc < K) xv[i] = *reinterpret_cast<const uint4*>(X + (m0 + i) * ldx + kc);
+    }
+    __syncthreads();                                  // previous slab fully read
+#pragma unroll
+    for (int q = 0; q < (kRC * 2 * 64) / kThreads; ++q) {
+      const int idx = t + q * kThreads;               // (jj, lane', plane) in global order
+      const int jj = idx >> 7, l = (idx >> 1) & 63, pl = idx & 1;
+      const int64_t kk = k0 + l * 8 + pl * 4;
+      float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      if (jj < nj && kk < K) v = *reinterpret_cast<const float4*>(F + (int64_t)(j0 + jj) * ldf + kk);
+      fs[(jj * 2 + pl) * 64 + l] = v;
+    }
+    __syncthreads();
+    float xf[kRowsPerWave][8];
+#pragma unroll
+    for (int i = 0; i < kRowsPerWave; ++i) {
+      uint32_t h[8];
+      unpack8(xv[i], h);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) xf[i][k] = as_f32(h[k] << 16);
+    }
+#pragma unroll
+    for (int jj = 0; jj < kRC; ++jj) {
+      const float4 lo = fs[(jj * 2) * 64 + lane], hi = fs[(jj * 2 + 1) * 64 + lane];
+      const float f[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+#pragma unroll
+      for (int i = 0; i < kRowsPerWave; ++i)
+#pragma unroll
+        for (int k = 0; k < 8; ++k) acc[i][jj] = __builtin_fmaf(xf[i][k], f[k], acc[i][jj]);
+    }
+  }
+  // recursive halving over the 64 lanes: value index v = 16 i + jj
+  float* v = &acc[0][0];
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const bool upper = (lane & o) != 0;
+#pragma unroll
+    for (int q = 0; q < o; ++q) {
+      const float send = upper ? v[q] : v[q + o];
+      const float keep = upper ? v[q + o] : v[q];
+      v[q] = keep + __shfl_xor(send, o, 64);
+    }
+  }
+  const int64_t m = m0 + (lane >> 4);
+  const int jj = lane & 15;
+  if (m < M) P[m * ldp + j0 + jj] = v[0];          // ranks past r: zeros (F rows read as 0)
+}
+
+// ======================================================================== column sums
+// part[s][j0 + jj][c] = sum over rows m of split s of Big[m][c] Sm[m][j0 + jj], jj < 16:
+// Big bf16 [M, C] (row stride ldb), Sm FP32 [M, lds_].  A block covers 256 columns (4 per
+// lane) of one row split; each of its 4 waves takes every fourth group of 4 rows (4 loads in
+// flight per lane), and the waves' partials are added in wave order through LDS, 8 ranks at a
+// time.  part is [splits][r][C] FP32.  Sm's row stride is a multiple of 16 with zeros past
+// rank r (as the row-dot writes it), so a rank pass reads 16 values unconditionally.
+constexpr int kColRows = 4;
+
+__global__ __launch_bounds__(kThreads) void lora_colsum_kernel(const uint16_t* __restrict__ Big,
+                                                               int64_t M, int64_t C, int64_t ldb,
+                                                               const float* __restrict__ Sm,
+                                                               int64_t lds_, int r,
+                                                               int64_t rows_per_split,
+                                                               float* __restrict__ part) {
+  __shared__ float4 red[4 * 8 * 64];                  // [wave][rank of the half][lane] x 4 cols
+  const int t = threadIdx.x, lane = t & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(t >> 6);
+  const int j0 = blockIdx.z * kRC;
+  const int nj = r - j0 < kRC ? r - j0 : kRC;
+  const int64_t s = blockIdx.y;
+  const int64_t cb = (int64_t)blockIdx.x * 256;
+  const int64_t c = cb + lane * 4;
+  const bool c_ok = c < C;
+  const int64_t mb = s * rows_per_split;
+  const int64_t me = mb + rows_per_split < M ? mb + rows_per_split : M;
+  float acc[4][kRC];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < kRC; ++j) acc[i][j] = 0.0f;
+  for (int64_t m0 = mb + wv * kColRows; m0 < me; m0 += 4 * kColRows) {
+    uint2 bv[kColRows];
+#pragma unroll
+    for (int q = 0; q < kColRows; ++q) {
+      bv[q] = make_uint2(0, 0);
+      if (c_ok && m0 + q < me) bv[q] = *reinterpret_cast<const uint2*>(Big + (m0 + q) * ldb + c);
+    }
+#pragma unroll
+    for (int q = 0; q < kColRows; ++q) {
+      if (m0 + q >= me) break;                        // uniform over the wave
+      const float x[4] = {as_f32(bv[q].x << 16), as_f32(bv[q].x & 0xFFFF0000u),
+                          as_f32(bv[q].y << 16), as_f32(bv[q].y & 0xFFFF0000u)};
+      const float4* sm = reinterpret_cast<const float4*>(Sm + (m0 + q) * lds_ + j0);
+      float sv[kRC];
+#pragma unroll
+      for (int u = 0; u < kRC / 4; ++u) {
+        const float4 f = sm[u];
+        sv[4 * u] = f.x; sv[4 * u + 1] = f.y; sv[4 * u + 2] = f.z; sv[4 * u + 3] = f.w;
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < kRC; ++j) acc[i][j] = __builtin_fmaf(x[i], sv[j], acc[i][j]);
+    }
+  }
+  // wave partials -> LDS (4 columns per lane as one 16-byte write), then thread t sums column
+  // cb + t over the waves in order, 8 ranks per half
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    if (h) __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      red[(wv * 8 + j) * 64 + lane] =
+          make_float4(acc[0][8 * h + j], acc[1][8 * h + j], acc[2][8 * h + j], acc[3][8 * h + j]);
+    __syncthreads();
+    const float* rf = reinterpret_cast<const float*>(red);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int jj = 8 * h + j;
+      float v = rf[(0 * 8 + j) * 256 + t];
+#pragma unroll
+      for (int w = 1; w < 4; ++w) v += rf[(w * 8 + j) * 256 + t];
+      if (jj < nj && cb + t < C) part[(s * r + j0 + jj) * C + cb + t] = v;
+    }
+  }
+}
+
+// out = scale * sum_s part[s] in split order (part [splits][r][C]); out[c][j] (row stride r)
+// or, transposed, out[j][c] (row stride C).
+__global__ void lora_finish_kernel(const float* __restrict__ part, int64_t splits, int64_t C,
+                                   int r, float scale, int transposed, float* __restrict__ out) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // j * C + c
+  if (idx >= C * r) return;
+  float acc = 0.0f;
+  for (int64_t s = 0; s < splits; ++s) acc += part[s * C * r + idx];
+  const float v = scale * acc;
+  const int64_t j = idx / C, c = idx % C;
+  if (transposed) out[idx] = v;
+  else out[c * r + j] = v;
+}
+
+// Ft[j][n] = F[n][j] for a small FP32 [N, r] matrix.
+__global__ void transpose_f32_kernel(const float* __restrict__ F, int64_t N, int r,
+                                     float* __restrict__ Ft) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= N * r) return;
+  const int64_t n = idx / r, j = idx % r;
+  Ft[j * N + n] = F[idx];
+}
+
+inline dim3 tile_grid(int64_t N, int64_t K, int64_t batch) {
+  return dim3((unsigned)((K + kTC - 1) / kTC), (unsigned)((N + kTR - 1) / kTR), (unsigned)batch);
+}
+
+template <int OUT>
+hipError_t launch_merge(int fmt, const MergeArgs& a, int64_t batch, hipStream_t s) {
+  const dim3 grid = tile_grid(a.N, a.K, batch);
+  switch (fmt) {
+#define QF_LQ(F)                                                                      \
+  hipLaunchKernelGGL((lora_quant_kernel<F, OUT>), grid, dim3(kThreads), 0, s, a); \
+  break;
+    case QF_FMT_NONE: QF_LQ(QF_FMT_NONE)
+    case QF_FMT_NVFP4: QF_LQ(QF_FMT_NVFP4)
+    case QF_FMT_MXFP4: QF_LQ(QF_FMT_MXFP4)
+    case QF_FMT_Q4K: QF_LQ(QF_FMT_Q4K)
+#undef QF_LQ
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+MergeArgs merge_args(const LoraOperand& L, const uint16_t* w, int64_t N, int64_t K, int64_t ldw,
+                     int64_t wbs) {
+  MergeArgs a{};
+  a.w = w; a.N = N; a.K = K; a.ldw = ldw; a.wbs = wbs;
+  a.A = L.A; a.abs = L.a_stride;
+  a.B = L.B; a.bbs = L.b_stride;
+  a.r = (int)L.r; a.scale = L.scale;
+  return a;
+}
+
+}  // namespace
+
+// ================================================================================ launchers
+hipError_t launch_lora_amax(const LoraOperand& L, const uint16_t* w, int64_t N, int64_t K,
+                            int64_t ldw, int64_t batch, int64_t wbs, float* amax, hipStream_t s) {
+  if (N == 0 || K == 0 || batch == 0) return hipSuccess;
+  MergeArgs a = merge_args(L, w, N, K, ldw, wbs);
+  a.amax = amax;
+  return launch_merge<kOutAmax>(QF_FMT_NONE, a, batch, s);
+}
+
+hipError_t launch_lora_quant(int fmt, const LoraOperand& L, const uint16_t* w, int64_t N,
+                             int64_t K, int64_t ldw, int64_t batch, int64_t wbs, const float* g,
+                             float* s_out, uint8_t* codes, uint8_t* scales, uint8_t* packed,
+                             uint16_t* xhat, hipStream_t s) {
+  if (N == 0 || K == 0 || batch == 0) return hipSuccess;
+  MergeArgs a = merge_args(L, w, N, K, ldw, wbs);
+  a.g = g; a.s_out = s_out; a.codes = codes; a.scales = scales; a.packed = packed; a.xhat = xhat;
+  return launch_merge<kOutRows>(fmt, a, batch, s);
+}
+
+hipError_t launch_lora_quant_t(int fmt, const LoraOperand& L, const uint16_t* w, int64_t N,
+                               int64_t K, int64_t ldw, int64_t batch, int64_t wbs, const float* g,
+                               uint16_t* out, int64_t ldo, int64_t obs, hipStream_t s) {
+  if (N == 0 || K == 0 || batch == 0) return hipSuccess;
+  MergeArgs a = merge_args(L, w, N, K, ldw, wbs);
+  a.g = g; a.out = out; a.ldo = ldo; a.obs = obs;
+  return launch_merge<kOutTransposed>(fmt, a, batch, s);
+}
+
+hipError_t launch_lora_rowdot(const uint16_t* X, int64_t M, int64_t K, int64_t ldx, const float* F,
+                              int64_t ldf, int64_t r, float* P, int64_t ldp, hipStream_t s) {
+  if (M == 0 || r == 0) return hipSuccess;
+  const dim3 grid((unsigned)((M + 4 * kRowsPerWave - 1) / (4 * kRowsPerWave)),
+                  (unsigned)((r + kRC - 1) / kRC));
+  hipLaunchKernelGGL(lora_rowdot_kernel, grid, dim3(kThreads), 0, s, X, M, K, ldx, F, ldf, (int)r,
+                     P, ldp);
+  return hipGetLastError();
+}
+
+int64_t lora_colsum_splits(int64_t M, int64_t C) {
+  const int64_t cblocks = (C + 255) / 256;
+  int64_t sp = (1024 + cblocks - 1) / cblocks;       // ~1024 workgroups
+  const int64_t by_rows = (M + 127) / 128;           // at least 128 rows per split
+  if (sp > by_rows) sp = by_rows;
+  return sp < 1 ? 1 : sp;
+}
+
+size_t lora_colsum_part_bytes(int64_t M, int64_t C, int64_t r) {
+  return (size_t)lora_colsum_splits(M, C) * (size_t)C * (size_t)r * 4;
+}
+
+hipError_t launch_lora_colsum(const uint16_t* Big, int64_t M, int64_t C, int64_t ldb,
+                              const float* Sm, int64_t lds_, int64_t r, float scale,
+                              float* part, int transposed, float* out, hipStream_t s) {
+  if (C == 0 || r == 0) return hipSuccess;
+  int64_t splits = 0;
+  if (M > 0) {
+    splits = lora_colsum_splits(M, C);
+    const int64_t rps = (M + splits - 1) / splits;
+    const dim3 grid((unsigned)((C + 255) / 256), (unsigned)splits, (unsigned)((r + kRC - 1) / kRC));
+    hipLaunchKernelGGL(lora_colsum_kernel, grid, dim3(kThreads), 0, s, Big, M, C, ldb, Sm, lds_,
+                       (int)r, rps, part);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  const int64_t n = C * r;
+  hipLaunchKernelGGL(lora_finish_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, part,
+                     splits, C, (int)r, scale, transposed, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_transpose_f32(const float* F, int64_t N, int64_t r, float* Ft, hipStream_t s) {
+  const int64_t n = N * r;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(transpose_f32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, F,
+                     N, (int)r, Ft);
+  return hipGetLastError();
+}
+
+}  // namespace qf

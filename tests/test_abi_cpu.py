@@ -121,3 +121,39 @@ def test_library_has_no_undefined_kernel_stubs():
         pytest.skip("needs the built library and nm")
     out = subprocess.run(["nm", "--undefined-only", LIB], capture_output=True, text=True).stdout
     assert "__device_stub" not in out
+
+
+class LoRA(ctypes.Structure):
+    _fields_ = [("A", ctypes.c_void_p), ("B", ctypes.c_void_p), ("r", ctypes.c_int64),
+                ("scale", ctypes.c_float), ("a_shared", ctypes.c_int32),
+                ("b_shared", ctypes.c_int32)]
+
+
+def test_lora_validation(L):
+    f = L.qf_lora_fakequant
+    lo = LoRA(256, 512, 16, 1.0, 0, 0)
+    args = lambda fmt, lo_, codes=None, scales=None, packed=None, s_out=None, K=64: f(
+        fmt, P(256), I64(8), I64(K), I64(K), ctypes.byref(lo_) if lo_ is not None else None,
+        P(1024), 0, s_out, codes, scales, packed, None, None)
+    assert args(2, None) == QF_EINVAL                                   # null descriptor
+    assert args(2, LoRA(256, 512, 0, 1.0, 0, 0)) == QF_ESHAPE           # rank 0
+    assert args(2, LoRA(256, 512, 5000, 1.0, 0, 0)) == QF_ESHAPE        # rank too large
+    assert args(2, LoRA(None, 512, 4, 1.0, 0, 0)) == QF_EINVAL          # null factor
+    assert args(2, LoRA(260, 512, 4, 1.0, 0, 0)) == QF_EALIGN           # misaligned factor
+    assert args(3, lo, codes=P(256), K=256) == QF_EINVAL                # codes with Q4_K
+    assert args(2, lo, packed=P(256)) == QF_EINVAL                      # packed with MXFP4
+    assert args(2, lo, s_out=P(256)) == QF_EINVAL                       # s_out with MXFP4
+    assert args(2, lo, K=48) == QF_ESHAPE                               # K % 32
+    assert args(9, lo) == QF_EINVAL                                     # bad format
+    t = L.qf_lora_fakequant_transposed
+    assert t(2, P(256), I64(12), I64(64), I64(64), ctypes.byref(lo), None, P(256), I64(16),
+             None) == QF_ESHAPE                                         # N % 8
+    assert t(1, P(256), I64(8), I64(64), I64(64), ctypes.byref(lo), None, P(256), I64(8),
+             None) == QF_EINVAL                                         # NVFP4 without amax
+    n = ctypes.c_size_t()
+    d = Desc(256, 512, 512, 0, 0, 0, 2, 2, None, None, 0)
+    assert L.qf_lora_workspace_size(ctypes.byref(d), ctypes.byref(lo), ctypes.byref(n)) == QF_OK
+    assert n.value >= (2 * 512 * 512 + 256 * 512) * 2                   # W_hat, W_hat^T, A_hat
+    assert L.qf_qlinear_lora_fwd(ctypes.byref(d), ctypes.byref(lo), P(256), P(256), P(256),
+                                 P(256), ctypes.c_size_t(16), None) == QF_EINVAL
+    assert b"workspace" in L.qf_last_error()
