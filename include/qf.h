@@ -344,6 +344,31 @@ QF_API qf_status qf_qlinear_lora_bwd_ste(const qf_qlinear_desc* d, const qf_lora
                                          const uint16_t* W, uint16_t* dX, float* dA, float* dB,
                                          void* ws, size_t ws_bytes, qf_stream_t stream);
 
+/*
+ * Grouped LoRA-QAD (Sec. 3.3 "Mixture-of-experts adaptation"): expert e's weight is the merged
+ * W[e] + scale B_e A_e, quantized per expert (its own NVFP4 tensor amax unless d->w_amax holds
+ * tied values [E]).  lora->a_shared / b_shared select one factor for all experts (A [r, K] /
+ * B [N, r]) instead of one per expert (A [E, r, K] / B [E, N, r]); the paper's hybrid layout
+ * shares A for gate/up and B for down.  group_offsets, X, W, Y, d as for the grouped layer
+ * (afmt NONE or MXFP4).  The merged weights are never written to memory.
+ * Backward: dX = dY_e W_hat_e per expert (bf16 [T, K], may be NULL); dA, dB FP32 shaped like
+ * A, B (overwritten; may be NULL): an unshared factor gets its expert's gradient
+ * (dB_e = scale dY_e^T A_hat_e A_e^T, dA_e = scale B_e^T dY_e^T A_hat_e; zeros for an expert
+ * with no rows), a shared factor the sum over experts.
+ */
+QF_API qf_status qf_grouped_lora_workspace_size(const qf_grouped_desc* d, const qf_lora* lora,
+                                                size_t* bytes);
+QF_API qf_status qf_qlinear_grouped_lora_fwd(const qf_grouped_desc* d, const qf_lora* lora,
+                                             const int64_t* group_offsets, const uint16_t* X,
+                                             const uint16_t* W, uint16_t* Y, void* ws,
+                                             size_t ws_bytes, qf_stream_t stream);
+QF_API qf_status qf_qlinear_grouped_lora_bwd_ste(const qf_grouped_desc* d, const qf_lora* lora,
+                                                 const int64_t* group_offsets,
+                                                 const uint16_t* dY, const uint16_t* X,
+                                                 const uint16_t* W, uint16_t* dX, float* dA,
+                                                 float* dB, void* ws, size_t ws_bytes,
+                                                 qf_stream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -105,6 +105,13 @@ def lib() -> ctypes.CDLL:
             "qf_qlinear_lora_bwd_ste": ([ctypes.POINTER(QLinearDesc), ctypes.POINTER(LoRA), _P,
                                          _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P],
                                         ctypes.c_int),
+            "qf_grouped_lora_workspace_size": ([ctypes.POINTER(GroupedDesc), ctypes.POINTER(LoRA),
+                                                ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
+            "qf_qlinear_grouped_lora_fwd": ([ctypes.POINTER(GroupedDesc), ctypes.POINTER(LoRA), _P,
+                                             _P, _P, _P, _P, ctypes.c_size_t, _P], ctypes.c_int),
+            "qf_qlinear_grouped_lora_bwd_ste": ([ctypes.POINTER(GroupedDesc), ctypes.POINTER(LoRA),
+                                                 _P, _P, _P, _P, _P, _P, _P, _P, ctypes.c_size_t,
+                                                 _P], ctypes.c_int),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -321,3 +328,23 @@ def qlinear_lora_bwd_ste(desc, lo: LoRA, dY, X, W, dX, dA, dB, ws):
     _check(lib().qf_qlinear_lora_bwd_ste(ctypes.byref(desc), ctypes.byref(lo), _ptr(_bf16(dY)),
                                          _ptr(_bf16(X)), _ptr(_bf16(W)), _ptr(_bf16(dX)),
                                          _ptr(dA), _ptr(dB), _ptr(ws), ws.numel(), _stream()))
+
+
+def grouped_lora_workspace(desc: GroupedDesc, lo: LoRA, device="cuda"):
+    n = ctypes.c_size_t()
+    _check(lib().qf_grouped_lora_workspace_size(ctypes.byref(desc), ctypes.byref(lo),
+                                                ctypes.byref(n)))
+    return torch.empty(max(n.value, 256), dtype=torch.uint8, device=device)
+
+
+def qlinear_grouped_lora_fwd(desc, lo: LoRA, offsets, X, W, Y, ws):
+    _check(lib().qf_qlinear_grouped_lora_fwd(ctypes.byref(desc), ctypes.byref(lo), _ptr(offsets),
+                                             _ptr(_bf16(X)), _ptr(_bf16(W)), _ptr(_bf16(Y)),
+                                             _ptr(ws), ws.numel(), _stream()))
+
+
+def qlinear_grouped_lora_bwd_ste(desc, lo: LoRA, offsets, dY, X, W, dX, dA, dB, ws):
+    _check(lib().qf_qlinear_grouped_lora_bwd_ste(ctypes.byref(desc), ctypes.byref(lo),
+                                                 _ptr(offsets), _ptr(_bf16(dY)), _ptr(_bf16(X)),
+                                                 _ptr(_bf16(W)), _ptr(_bf16(dX)), _ptr(dA),
+                                                 _ptr(dB), _ptr(ws), ws.numel(), _stream()))

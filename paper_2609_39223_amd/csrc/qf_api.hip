@@ -855,14 +855,213 @@ qf_status qf_qlinear_lora_bwd_ste(const qf_qlinear_desc* d, const qf_lora* lora,
     lda = K;
   }
   if (dB) {  // dB = scale dY^T (A_hat A^T)
-    QF_TRY(dev(qf::launch_lora_rowdot(Aop, M, K, lda, L.A, K, r, w.u, rp, s), "A_hat A^T"));
-    QF_TRY(dev(qf::launch_lora_colsum(dY, M, N, dm.ldy, w.u, rp, r, L.scale, w.part, 0, dB, s),
+    QF_TRY(dev(qf::launch_lora_rowdot(Aop, M, K, lda, L.A, K, r, w.u, rp, nullptr, nullptr, 0, 0, s), "A_hat A^T"));
+    QF_TRY(dev(qf::launch_lora_colsum(dY, M, N, dm.ldy, w.u, rp, r, L.scale, w.part, 0, dB, nullptr,
+                                          nullptr, 0, 0, s),
                "dB"));
   }
   if (dA) {  // dA = scale (dY B)^T A_hat
-    QF_TRY(dev(qf::launch_transpose_f32(L.B, N, r, w.bt, s), "B^T"));
-    QF_TRY(dev(qf::launch_lora_rowdot(dY, M, N, dm.ldy, w.bt, N, r, w.v, rp, s), "dY B"));
-    QF_TRY(dev(qf::launch_lora_colsum(Aop, M, K, lda, w.v, rp, r, L.scale, w.part, 1, dA, s),
+    QF_TRY(dev(qf::launch_transpose_f32(L.B, N, r, 1, w.bt, s), "B^T"));
+    QF_TRY(dev(qf::launch_lora_rowdot(dY, M, N, dm.ldy, w.bt, N, r, w.v, rp, nullptr, nullptr, 0, 0, s), "dY B"));
+    QF_TRY(dev(qf::launch_lora_colsum(Aop, M, K, lda, w.v, rp, r, L.scale, w.part, 1, dA, nullptr,
+                                          nullptr, 0, 0, s),
+               "dA"));
+  }
+  return ok();
+}
+
+// -------------------------------------------------------------------- grouped LoRA-QAD (MoE)
+namespace {
+
+// Workspace of the grouped LoRA layer (256-byte aligned regions):
+//   tile_start, order  [E+1], [E]   grouped NT row tiles (launch_grouped_prep)
+//   pre16, prech       [E+1] x 2    row-dot / column-sum chunk prefixes
+//   wamax              [E]          per-expert merged amax (NVFP4)
+//   what               [E, N, K]    per-expert W_hat of the merged weights
+//   ahat               [T, K]       A_hat (afmt MXFP4)
+//   whatt              [E, K, N]    per-expert W_hat^T (dX operand in NT form)
+//   bt                 [Eb, r, N]   B^T per expert (Eb = 1 when B is shared)
+//   u, v               [T, rp]      A_hat A_e^T and dY B_e (FP32)
+//   part                            column-sum chunk partials
+struct GroupedLoraWs {
+  int* tile_start;
+  int* order;
+  int* pre16;
+  int* prech;
+  float* wamax;
+  uint16_t* what;
+  uint16_t* ahat;
+  uint16_t* whatt;
+  float* bt;
+  float* u;
+  float* v;
+  float* part;
+};
+
+size_t glora_ws_bytes(const qf_grouped_desc* d, int64_t r, int b_shared) {
+  const size_t E = d->E, T = d->T, N = d->N, K = d->K, R = r, RP = (R + 15) / 16 * 16;
+  const size_t Eb = b_shared ? 1 : E;
+  size_t b = up((E + 1) * 4) + up(E * 4) + 2 * up((E + 1) * 4) + up(E * 4);
+  b += up(E * N * K * 2);
+  if (d->afmt != QF_FMT_NONE) b += up(T * K * 2);
+  b += up(E * K * N * 2) + up(Eb * R * N * 4) + 2 * up(T * RP * 4);
+  const size_t p1 = qf::lora_colsum_grouped_part_bytes(d->T, d->E, d->N, r);
+  const size_t p2 = qf::lora_colsum_grouped_part_bytes(d->T, d->E, d->K, r);
+  return b + up(p1 > p2 ? p1 : p2);
+}
+
+GroupedLoraWs glora_ws(const qf_grouped_desc* d, int64_t r, int b_shared, void* ws) {
+  const size_t E = d->E, T = d->T, N = d->N, K = d->K, R = r, RP = (R + 15) / 16 * 16;
+  const size_t Eb = b_shared ? 1 : E;
+  char* p = static_cast<char*>(ws);
+  GroupedLoraWs g{};
+  g.tile_start = reinterpret_cast<int*>(p); p += up((E + 1) * 4);
+  g.order = reinterpret_cast<int*>(p); p += up(E * 4);
+  g.pre16 = reinterpret_cast<int*>(p); p += up((E + 1) * 4);
+  g.prech = reinterpret_cast<int*>(p); p += up((E + 1) * 4);
+  g.wamax = reinterpret_cast<float*>(p); p += up(E * 4);
+  g.what = reinterpret_cast<uint16_t*>(p); p += up(E * N * K * 2);
+  if (d->afmt != QF_FMT_NONE) { g.ahat = reinterpret_cast<uint16_t*>(p); p += up(T * K * 2); }
+  g.whatt = reinterpret_cast<uint16_t*>(p); p += up(E * K * N * 2);
+  g.bt = reinterpret_cast<float*>(p); p += up(Eb * R * N * 4);
+  g.u = reinterpret_cast<float*>(p); p += up(T * RP * 4);
+  g.v = reinterpret_cast<float*>(p); p += up(T * RP * 4);
+  g.part = reinterpret_cast<float*>(p);
+  return g;
+}
+
+qf_status check_glora(const char* fn, const qf_grouped_desc* d, const int64_t* off,
+                      const qf_lora* L) {
+  QF_TRY(check_grouped(fn, d, off));
+  QF_TRY(check_lora(fn, L, d->N, d->K));
+  if ((L->a_shared & ~1) || (L->b_shared & ~1))
+    return fail(QF_EINVAL, "%s: a_shared / b_shared must be 0 or 1", fn);
+  return QF_OK;
+}
+
+qf::LoraOperand glora_op(const qf_grouped_desc* d, const qf_lora* L) {
+  return qf::LoraOperand{L->A, L->a_shared ? 0 : L->r * d->K, L->B,
+                         L->b_shared ? 0 : d->N * L->r, L->r, L->scale};
+}
+
+// Per-expert NVFP4 amax of the merged weights (or the caller's tied values).
+qf_status glora_amax(const qf_grouped_desc* d, const qf::LoraOperand& L, const uint16_t* W,
+                     float* scratch, const float** g, hipStream_t s) {
+  *g = d->w_amax;
+  if (d->wfmt != QF_FMT_NVFP4 || *g) return QF_OK;
+  QF_TRY(dev(qf::launch_fill_f32(scratch, d->E, 0.0f, s), "amax init"));
+  QF_TRY(dev(qf::launch_lora_amax(L, W, d->N, d->K, d->K, d->E, d->N * d->K, scratch, s),
+             "merged amax"));
+  *g = scratch;
+  return QF_OK;
+}
+
+}  // namespace
+
+qf_status qf_grouped_lora_workspace_size(const qf_grouped_desc* d, const qf_lora* lora,
+                                         size_t* bytes) {
+  QF_TRY(check_glora("qf_grouped_lora_workspace_size", d, (const int64_t*)1, lora));
+  if (!bytes) return fail(QF_EINVAL, "qf_grouped_lora_workspace_size: null output");
+  *bytes = glora_ws_bytes(d, lora->r, lora->b_shared);
+  return ok();
+}
+
+qf_status qf_qlinear_grouped_lora_fwd(const qf_grouped_desc* d, const qf_lora* lora,
+                                      const int64_t* group_offsets, const uint16_t* X,
+                                      const uint16_t* W, uint16_t* Y, void* ws, size_t ws_bytes,
+                                      qf_stream_t stream) {
+  const char* fn = "qf_qlinear_grouped_lora_fwd";
+  QF_TRY(check_glora(fn, d, group_offsets, lora));
+  QF_TRY(check_mat("qf_qlinear_grouped_lora_fwd: X", X, d->T, d->K, d->K, true));
+  QF_TRY(check_mat("qf_qlinear_grouped_lora_fwd: W", W, d->E * d->N, d->K, d->K, true));
+  QF_TRY(check_mat("qf_qlinear_grouped_lora_fwd: Y", Y, d->T, d->N, d->N, true));
+  QF_TRY(check_ws(fn, glora_ws_bytes(d, lora->r, lora->b_shared), ws, ws_bytes));
+  if (d->E == 0) return ok();
+  hipStream_t s = S(stream);
+  GroupedLoraWs g = glora_ws(d, lora->r, lora->b_shared, ws);
+  const qf::LoraOperand L = glora_op(d, lora);
+  const float* gp;
+  QF_TRY(glora_amax(d, L, W, g.wamax, &gp, s));
+  QF_TRY(dev(qf::launch_lora_quant(d->wfmt, L, W, d->N, d->K, d->K, d->E, d->N * d->K, gp,
+                                   nullptr, nullptr, nullptr, nullptr, g.what, s),
+             "merged quantize (experts)"));
+  const uint16_t* Aop = X;
+  if (d->afmt == QF_FMT_MXFP4) {
+    QF_TRY(dev(qf::launch_mxfp4(X, d->T, d->K, d->K, nullptr, nullptr, g.ahat, s), "mxfp4"));
+    Aop = g.ahat;
+  }
+  QF_TRY(dev(qf::launch_grouped_prep(group_offsets, d->E, g.tile_start, g.order, nullptr, nullptr,
+                                    s),
+             "prep"));
+  QF_TRY(dev(qf::launch_grouped_nt_rows(d->E, d->T, d->N, d->K, group_offsets, g.tile_start, Aop,
+                                        d->K, g.what, d->K, 0, d->N * d->K, Y, d->N, s),
+             "grouped forward"));
+  return ok();
+}
+
+qf_status qf_qlinear_grouped_lora_bwd_ste(const qf_grouped_desc* d, const qf_lora* lora,
+                                          const int64_t* group_offsets, const uint16_t* dY,
+                                          const uint16_t* X, const uint16_t* W, uint16_t* dX,
+                                          float* dA, float* dB, void* ws, size_t ws_bytes,
+                                          qf_stream_t stream) {
+  const char* fn = "qf_qlinear_grouped_lora_bwd_ste";
+  QF_TRY(check_glora(fn, d, group_offsets, lora));
+  const bool grads = dA || dB;
+  QF_TRY(check_mat("qf_qlinear_grouped_lora_bwd_ste: dY", dY, d->T, d->N, d->N, true));
+  QF_TRY(check_mat("qf_qlinear_grouped_lora_bwd_ste: X", X, d->T, d->K, d->K, grads));
+  QF_TRY(check_mat("qf_qlinear_grouped_lora_bwd_ste: W", W, d->E * d->N, d->K, d->K, dX != nullptr));
+  QF_TRY(check_mat("qf_qlinear_grouped_lora_bwd_ste: dX", dX, d->T, d->K, d->K, false));
+  QF_TRY(check_out("qf_qlinear_grouped_lora_bwd_ste: dA", dA));
+  QF_TRY(check_out("qf_qlinear_grouped_lora_bwd_ste: dB", dB));
+  QF_TRY(check_ws(fn, glora_ws_bytes(d, lora->r, lora->b_shared), ws, ws_bytes));
+  if (d->E == 0) return ok();
+  hipStream_t s = S(stream);
+  GroupedLoraWs g = glora_ws(d, lora->r, lora->b_shared, ws);
+  const qf::LoraOperand L = glora_op(d, lora);
+  const bool reuse = (d->flags & QF_FLAG_REUSE_WS) != 0;
+  const int64_t E = d->E, T = d->T, N = d->N, K = d->K, r = lora->r, rp = (r + 15) / 16 * 16;
+  if (dX) {
+    QF_TRY(dev(qf::launch_grouped_prep(group_offsets, E, g.tile_start, g.order, nullptr, nullptr,
+                                      s),
+               "prep"));
+    if (reuse) {
+      QF_TRY(dev(qf::launch_transpose_bf16(g.what, N, K, K, g.whatt, N, E, N * K, N * K, s),
+                 "transpose expert W_hat"));
+    } else {
+      const float* gp;
+      QF_TRY(glora_amax(d, L, W, g.wamax, &gp, s));
+      QF_TRY(dev(qf::launch_lora_quant_t(d->wfmt, L, W, N, K, K, E, N * K, gp, g.whatt, N, N * K,
+                                         s),
+                 "merged quantize (experts, transposed)"));
+    }
+    QF_TRY(dev(qf::launch_grouped_nt_rows(E, T, K, N, group_offsets, g.tile_start, dY, N, g.whatt,
+                                          N, 0, N * K, dX, K, s),
+               "grouped dX"));
+  }
+  if (!grads) return ok();
+  const uint16_t* Aop = X;
+  if (d->afmt == QF_FMT_MXFP4) {
+    if (!reuse && T > 0)
+      QF_TRY(dev(qf::launch_mxfp4(X, T, K, K, nullptr, nullptr, g.ahat, s), "mxfp4"));
+    Aop = g.ahat;
+  }
+  QF_TRY(dev(qf::launch_group_prefix(group_offsets, E, 16, g.pre16, s), "row prefix"));
+  QF_TRY(dev(qf::launch_group_prefix(group_offsets, E, 1024, g.prech, s), "chunk prefix"));
+  if (dB) {  // dB_e = scale dY_e^T (A_hat_e A_e^T); shared B: summed over experts
+    QF_TRY(dev(qf::launch_lora_rowdot(Aop, T, K, K, L.A, K, r, g.u, rp, group_offsets, g.pre16, E,
+                                      L.a_stride, s),
+               "A_hat A_e^T"));
+    QF_TRY(dev(qf::launch_lora_colsum(dY, T, N, N, g.u, rp, r, L.scale, g.part, 0, dB,
+                                      group_offsets, g.prech, E, !lora->b_shared, s),
+               "dB"));
+  }
+  if (dA) {  // dA_e = scale (dY_e B_e)^T A_hat_e; shared A: summed over experts
+    QF_TRY(dev(qf::launch_transpose_f32(L.B, N, r, lora->b_shared ? 1 : E, g.bt, s), "B^T"));
+    QF_TRY(dev(qf::launch_lora_rowdot(dY, T, N, N, g.bt, N, r, g.v, rp, group_offsets, g.pre16, E,
+                                      lora->b_shared ? 0 : r * N, s),
+               "dY B_e"));
+    QF_TRY(dev(qf::launch_lora_colsum(Aop, T, K, K, g.v, rp, r, L.scale, g.part, 1, dA,
+                                      group_offsets, g.prech, E, !lora->a_shared, s),
                "dA"));
   }
   return ok();

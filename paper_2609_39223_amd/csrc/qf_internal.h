@@ -101,19 +101,30 @@ hipError_t launch_lora_quant(int fmt, const LoraOperand& L, const uint16_t* w, i
 hipError_t launch_lora_quant_t(int fmt, const LoraOperand& L, const uint16_t* w, int64_t N,
                                int64_t K, int64_t ldw, int64_t batch, int64_t wbs, const float* g,
                                uint16_t* out, int64_t ldo, int64_t obs, hipStream_t s);
+// Grouped (mixture-of-experts) mode of the two kernels below: off [E+1] (device) splits the M
+// rows into experts and pre [E+1] (device, launch_group_prefix with the kernel's chunk: 16
+// rows for the row-dot, 1024 for the column sum) deals expert-aligned chunks to blocks; off
+// null = one group.  pre[e] = sum over experts before e of ceil(rows / q).
+hipError_t launch_group_prefix(const int64_t* off, int64_t E, int q, int* pre, hipStream_t s);
 // P[m][j] = sum_k X[m][k] F[j][k]: X bf16 [M, K] (ldx), F FP32 [r, K] (ldf, multiple of 4,
-// 16-byte aligned), P FP32 [M, ldp] with ldp = r rounded up to 16 (zeros past r).  K a
-// multiple of 8.
+// 16-byte aligned; grouped: expert e uses F + e * fstride), P FP32 [M, ldp] with ldp = r
+// rounded up to 16 (zeros past r).  K a multiple of 8.
 hipError_t launch_lora_rowdot(const uint16_t* X, int64_t M, int64_t K, int64_t ldx, const float* F,
-                              int64_t ldf, int64_t r, float* P, int64_t ldp, hipStream_t s);
+                              int64_t ldf, int64_t r, float* P, int64_t ldp, const int64_t* off,
+                              const int* pre, int64_t E, int64_t fstride, hipStream_t s);
 // out = scale * sum_m Big[m][c] Sm[m][j] as out[c][j] (or out[j][c] when transposed): Big bf16
 // [M, C] (ldb, C a multiple of 4), Sm FP32 [M, lds_] as the row-dot writes it (lds_ = r
-// rounded up to 16, zeros past r, 16-byte aligned); `part` holds
-// lora_colsum_part_bytes(M, C, r) bytes of row-split partials (summed in a fixed order).
+// rounded up to 16, zeros past r, 16-byte aligned); `part` holds lora_colsum_part_bytes(M, C,
+// r) bytes (grouped: lora_colsum_grouped_part_bytes) of row-chunk partials, summed in a fixed
+// order.  Grouped with per_group: out + e * C * r receives expert e's rows only; grouped
+// without: the sum over all rows.
 size_t lora_colsum_part_bytes(int64_t M, int64_t C, int64_t r);
+size_t lora_colsum_grouped_part_bytes(int64_t T, int64_t E, int64_t C, int64_t r);
 hipError_t launch_lora_colsum(const uint16_t* Big, int64_t M, int64_t C, int64_t ldb,
                               const float* Sm, int64_t lds_, int64_t r, float scale,
-                              float* part, int transposed, float* out, hipStream_t s);
-// Ft [r, N] = F^T for FP32 F [N, r].
-hipError_t launch_transpose_f32(const float* F, int64_t N, int64_t r, float* Ft, hipStream_t s);
+                              float* part, int transposed, float* out, const int64_t* off,
+                              const int* pre, int64_t E, int per_group, hipStream_t s);
+// Ft [z][r][N] = F[z]^T for `batch` FP32 [N, r] matrices stored back to back.
+hipError_t launch_transpose_f32(const float* F, int64_t N, int64_t r, int64_t batch, float* Ft,
+                                hipStream_t s);
 }  // namespace qf

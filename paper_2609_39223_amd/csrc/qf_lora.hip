@@ -29,6 +29,7 @@ using namespace codec;
 
 constexpr int kThreads = 256;
 constexpr int kRC = 16;   // rank terms staged per pass (B rows in LDS; row-dot outputs)
+constexpr int64_t kGroupChunk = 1024;   // rows per column-sum chunk in grouped mode
 
 // ====================================================================== merged quantizer
 enum { kOutRows = 0, kOutTransposed = 1, kOutAmax = 2 };
@@ -186,6 +187,39 @@ __global__ __launch_bounds__(kThreads) void lora_quant_kernel(MergeArgs p) {
   }
 }
 
+// ======================================================================== expert groups
+// Grouped (mixture-of-experts) mode of the row-dot and column-sum kernels: rows
+// [off[e], off[e+1]) belong to expert e, and blocks are dealt expert-aligned row chunks:
+// block y covers chunk y - pre[e] of expert e, where pre[e] <= y < pre[e+1] and pre is the
+// prefix of ceil(rows_e / chunk) (group_prefix_kernel).  The host never reads off or pre, so
+// grids are sized for the worst case (T / chunk + E) and blocks past pre[E] exit.
+struct Groups {
+  const int64_t* off;   // null: one group of M rows (dense)
+  const int* pre;
+  int E;
+};
+
+__device__ __forceinline__ int find_group(const int* pre, int E, int y) {
+  int lo = 0, hi = E;                                 // pre[lo] <= y < pre[hi]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (pre[mid] <= y) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+// pre[e] = sum over experts before e of ceil(rows / q); one thread (E <= 1024).
+__global__ void group_prefix_kernel(const int64_t* __restrict__ off, int E, int q,
+                                    int* __restrict__ pre) {
+  if (threadIdx.x != 0) return;
+  int acc = 0;
+  pre[0] = 0;
+  for (int e = 0; e < E; ++e) {
+    acc += (int)((off[e + 1] - off[e] + q - 1) / q);
+    pre[e + 1] = acc;
+  }
+}
+
 // ============================================================================ row-dot
 // P[m][j0 + jj] = sum_k X[m][k] F[j0 + jj][k] for jj < 16: X bf16 [M, K] (row stride ldx),
 // F FP32 [r, K] (row stride ldf), P FP32 [M, ldp] with ldp >= r rounded up to 16 (the ranks
@@ -194,22 +228,32 @@ __global__ __launch_bounds__(kThreads) void lora_quant_kernel(MergeArgs p) {
 // staged in LDS in two planes of 4 columns so every lane's 16-byte reads are contiguous
 // across the wave.  After the K loop each lane holds 4 x 16 partial sums, which a
 // recursive-halving exchange (63 shuffles, fixed pairing) reduces so that lane l ends with
-// output l = (row l / 16, rank l % 16).
+// output l = (row l / 16, rank l % 16).  Grouped: a block's 16 rows come from one expert's
+// chunk and use F + e * fstride.
 constexpr int kRowsPerWave = 4;
 constexpr int kStepK = 512;
 
 __global__ __launch_bounds__(kThreads) void lora_rowdot_kernel(const uint16_t* __restrict__ X,
                                                                int64_t M, int64_t K, int64_t ldx,
-                                                               const float* __restrict__ F,
+                                                               const float* F,
                                                                int64_t ldf, int r,
                                                                float* __restrict__ P,
-                                                               int64_t ldp) {
+                                                               int64_t ldp, Groups g,
+                                                               int64_t fstride) {
   __shared__ float4 fs[kRC * 2 * 64];                 // [jj][plane][lane] x 4 columns
   const int t = threadIdx.x, lane = t & 63;
   const int wv = __builtin_amdgcn_readfirstlane(t >> 6);
   const int j0 = blockIdx.y * kRC;
   const int nj = r - j0 < kRC ? r - j0 : kRC;
-  const int64_t m0 = (int64_t)blockIdx.x * (4 * kRowsPerWave) + wv * kRowsPerWave;
+  int64_t m0 = (int64_t)blockIdx.x * (4 * kRowsPerWave) + wv * kRowsPerWave;
+  if (g.off) {                                        // uniform over the block
+    const int y = blockIdx.x;
+    if (y >= g.pre[g.E]) return;
+    const int e = find_group(g.pre, g.E, y);
+    m0 = g.off[e] + (int64_t)(y - g.pre[e]) * (4 * kRowsPerWave) + wv * kRowsPerWave;
+    M = g.off[e + 1];
+    F += e * fstride;
+  }
   float acc[kRowsPerWave][kRC];
 #pragma unroll
   for (int i = 0; i < kRowsPerWave; ++i)
@@ -277,6 +321,7 @@ __global__ __launch_bounds__(kThreads) void lora_rowdot_kernel(const uint16_t* _
 // flight per lane), and the waves' partials are added in wave order through LDS, 8 ranks at a
 // time.  part is [splits][r][C] FP32.  Sm's row stride is a multiple of 16 with zeros past
 // rank r (as the row-dot writes it), so a rank pass reads 16 values unconditionally.
+// Grouped: split y is chunk y - pre[e] (rows_per_split rows) of expert e.
 constexpr int kColRows = 4;
 
 __global__ __launch_bounds__(kThreads) void lora_colsum_kernel(const uint16_t* __restrict__ Big,
@@ -284,7 +329,8 @@ __global__ __launch_bounds__(kThreads) void lora_colsum_kernel(const uint16_t* _
                                                                const float* __restrict__ Sm,
                                                                int64_t lds_, int r,
                                                                int64_t rows_per_split,
-                                                               float* __restrict__ part) {
+                                                               float* __restrict__ part,
+                                                               Groups g) {
   __shared__ float4 red[4 * 8 * 64];                  // [wave][rank of the half][lane] x 4 cols
   const int t = threadIdx.x, lane = t & 63;
   const int wv = __builtin_amdgcn_readfirstlane(t >> 6);
@@ -294,8 +340,14 @@ __global__ __launch_bounds__(kThreads) void lora_colsum_kernel(const uint16_t* _
   const int64_t cb = (int64_t)blockIdx.x * 256;
   const int64_t c = cb + lane * 4;
   const bool c_ok = c < C;
-  const int64_t mb = s * rows_per_split;
-  const int64_t me = mb + rows_per_split < M ? mb + rows_per_split : M;
+  int64_t mb = s * rows_per_split, end = M;
+  if (g.off) {                                        // uniform over the block
+    if (s >= g.pre[g.E]) return;
+    const int e = find_group(g.pre, g.E, (int)s);
+    mb = g.off[e] + (s - g.pre[e]) * rows_per_split;
+    end = g.off[e + 1];
+  }
+  const int64_t me = mb + rows_per_split < end ? mb + rows_per_split : end;
   float acc[4][kRC];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -349,26 +401,36 @@ __global__ __launch_bounds__(kThreads) void lora_colsum_kernel(const uint16_t* _
 }
 
 // out = scale * sum_s part[s] in split order (part [splits][r][C]); out[c][j] (row stride r)
-// or, transposed, out[j][c] (row stride C).
+// or, transposed, out[j][c] (row stride C).  Grouped with per_group: output e = blockIdx.y
+// (at out + e * C * r) sums splits [pre[e], pre[e+1]); grouped without: all pre[E] splits.
 __global__ void lora_finish_kernel(const float* __restrict__ part, int64_t splits, int64_t C,
-                                   int r, float scale, int transposed, float* __restrict__ out) {
+                                   int r, float scale, int transposed, float* __restrict__ out,
+                                   Groups g, int per_group) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // j * C + c
   if (idx >= C * r) return;
+  int64_t s0 = 0, s1 = splits;
+  if (g.off) {
+    const int e = blockIdx.y;
+    s0 = per_group ? g.pre[e] : 0;
+    s1 = per_group ? g.pre[e + 1] : g.pre[g.E];
+    out += (int64_t)e * C * r;
+  }
   float acc = 0.0f;
-  for (int64_t s = 0; s < splits; ++s) acc += part[s * C * r + idx];
+  for (int64_t s = s0; s < s1; ++s) acc += part[s * C * r + idx];
   const float v = scale * acc;
   const int64_t j = idx / C, c = idx % C;
   if (transposed) out[idx] = v;
   else out[c * r + j] = v;
 }
 
-// Ft[j][n] = F[n][j] for a small FP32 [N, r] matrix.
+// Ft[z][j][n] = F[z][n][j] for small FP32 [N, r] matrices (batch z = blockIdx.y).
 __global__ void transpose_f32_kernel(const float* __restrict__ F, int64_t N, int r,
                                      float* __restrict__ Ft) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= N * r) return;
+  const int64_t z = blockIdx.y;
   const int64_t n = idx / r, j = idx % r;
-  Ft[j * N + n] = F[idx];
+  Ft[z * N * r + j * N + n] = F[z * N * r + idx];
 }
 
 inline dim3 tile_grid(int64_t N, int64_t K, int64_t batch) {
@@ -433,13 +495,20 @@ hipError_t launch_lora_quant_t(int fmt, const LoraOperand& L, const uint16_t* w,
   return launch_merge<kOutTransposed>(fmt, a, batch, s);
 }
 
+hipError_t launch_group_prefix(const int64_t* off, int64_t E, int q, int* pre, hipStream_t s) {
+  hipLaunchKernelGGL(group_prefix_kernel, dim3(1), dim3(64), 0, s, off, (int)E, q, pre);
+  return hipGetLastError();
+}
+
 hipError_t launch_lora_rowdot(const uint16_t* X, int64_t M, int64_t K, int64_t ldx, const float* F,
-                              int64_t ldf, int64_t r, float* P, int64_t ldp, hipStream_t s) {
+                              int64_t ldf, int64_t r, float* P, int64_t ldp, const int64_t* off,
+                              const int* pre, int64_t E, int64_t fstride, hipStream_t s) {
   if (M == 0 || r == 0) return hipSuccess;
-  const dim3 grid((unsigned)((M + 4 * kRowsPerWave - 1) / (4 * kRowsPerWave)),
-                  (unsigned)((r + kRC - 1) / kRC));
+  constexpr int64_t rows = 4 * kRowsPerWave;
+  const int64_t blocks = off ? M / rows + E : (M + rows - 1) / rows;
+  const dim3 grid((unsigned)blocks, (unsigned)((r + kRC - 1) / kRC));
   hipLaunchKernelGGL(lora_rowdot_kernel, grid, dim3(kThreads), 0, s, X, M, K, ldx, F, ldf, (int)r,
-                     P, ldp);
+                     P, ldp, Groups{off, pre, (int)E}, fstride);
   return hipGetLastError();
 }
 
@@ -455,31 +524,44 @@ size_t lora_colsum_part_bytes(int64_t M, int64_t C, int64_t r) {
   return (size_t)lora_colsum_splits(M, C) * (size_t)C * (size_t)r * 4;
 }
 
+size_t lora_colsum_grouped_part_bytes(int64_t T, int64_t E, int64_t C, int64_t r) {
+  return (size_t)(T / kGroupChunk + E) * (size_t)C * (size_t)r * 4;
+}
+
 hipError_t launch_lora_colsum(const uint16_t* Big, int64_t M, int64_t C, int64_t ldb,
                               const float* Sm, int64_t lds_, int64_t r, float scale,
-                              float* part, int transposed, float* out, hipStream_t s) {
+                              float* part, int transposed, float* out, const int64_t* off,
+                              const int* pre, int64_t E, int per_group, hipStream_t s) {
   if (C == 0 || r == 0) return hipSuccess;
-  int64_t splits = 0;
-  if (M > 0) {
+  const Groups g{off, pre, (int)E};
+  int64_t splits = 0, rps = 0;
+  if (off) {
+    splits = M / kGroupChunk + E;
+    rps = kGroupChunk;
+  } else if (M > 0) {
     splits = lora_colsum_splits(M, C);
-    const int64_t rps = (M + splits - 1) / splits;
+    rps = (M + splits - 1) / splits;
+  }
+  if (splits > 0 && M > 0) {
     const dim3 grid((unsigned)((C + 255) / 256), (unsigned)splits, (unsigned)((r + kRC - 1) / kRC));
     hipLaunchKernelGGL(lora_colsum_kernel, grid, dim3(kThreads), 0, s, Big, M, C, ldb, Sm, lds_,
-                       (int)r, rps, part);
+                       (int)r, rps, part, g);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   const int64_t n = C * r;
-  hipLaunchKernelGGL(lora_finish_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, part,
-                     splits, C, (int)r, scale, transposed, out);
+  const unsigned outs = off && per_group ? (unsigned)E : 1u;
+  hipLaunchKernelGGL(lora_finish_kernel, dim3((unsigned)((n + 255) / 256), outs), dim3(256), 0, s,
+                     part, M > 0 ? splits : 0, C, (int)r, scale, transposed, out, g, per_group);
   return hipGetLastError();
 }
 
-hipError_t launch_transpose_f32(const float* F, int64_t N, int64_t r, float* Ft, hipStream_t s) {
+hipError_t launch_transpose_f32(const float* F, int64_t N, int64_t r, int64_t batch, float* Ft,
+                                hipStream_t s) {
   const int64_t n = N * r;
-  if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(transpose_f32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, F,
-                     N, (int)r, Ft);
+  if (n == 0 || batch == 0) return hipSuccess;
+  hipLaunchKernelGGL(transpose_f32_kernel, dim3((unsigned)((n + 255) / 256), (unsigned)batch),
+                     dim3(256), 0, s, F, N, (int)r, Ft);
   return hipGetLastError();
 }
 

@@ -283,3 +283,88 @@ def test_lora_mlp_up_full_size_sampled(qf):
         V[m0:m0 + 1024] = bf16_to_f64(w["dY"][m0:m0 + 1024]) @ B64
     ks = rng.integers(0, K, 64)
     assert_close(dA[:, ks].astype(np.float64), s * (V.T @ xf[:, ks]), "dA sampled columns")
+
+
+# ------------------------------------------------------------------------ grouped (MoE)
+def _grouped_case(seed, E, N, K, counts):
+    rng = np.random.default_rng(seed)
+    off = np.zeros(E + 1, np.int64)
+    off[1:] = np.cumsum(counts)
+    T = int(off[-1])
+    X = workloads.normal_bf16(rng, (max(T, 1), K))[:T]
+    W = workloads.normal_bf16(rng, (E * N, K), 0.02).reshape(E, N, K)
+    dY = workloads.normal_bf16(rng, (max(T, 1), N))[:T]
+    return off, T, X, W, dY
+
+
+@pytest.mark.parametrize("wfmt,afmt,shared,r", [
+    ("mxfp4", "mxfp4", "none", 16),
+    ("nvfp4", "none", "A", 8),          # gate/up layout: A shared, per-expert tensor amax
+    ("nvfp4", "mxfp4", "B", 20),        # down layout: B shared
+    ("q4k", "none", "none", 3),
+])
+def test_grouped_lora_layer(qf, wfmt, afmt, shared, r):
+    E, N, K = 6, 264, 512
+    counts = [37, 0, 300, 5, 1100, 64]     # an empty expert, chunks past 1024 rows, tiny ones
+    off, T, X, W, dY = _grouped_case(r, E, N, K, counts)
+    rng = np.random.default_rng(100 + r)
+    A = (rng.standard_normal((r, K) if shared == "A" else (E, r, K)) / np.sqrt(K)).astype(np.float32)
+    B = (rng.standard_normal((N, r) if shared == "B" else (E, N, r)) * 0.01).astype(np.float32)
+    s = 2.0
+    lo = qf.lora(_dev_f32(A), _dev_f32(B), s, a_shared=shared == "A", b_shared=shared == "B")
+    offd = torch.from_numpy(off).cuda()
+    Xd, Wd, dYd = to_dev(X), to_dev(W.reshape(E * N, K)), to_dev(dY)
+
+    def run(reuse):
+        d = qf.grouped_desc(E, T, N, K, wfmt, afmt)
+        ws = qf.grouped_lora_workspace(d, lo)
+        Y, dX = empty_bf16((T, N)), empty_bf16((T, K))
+        dA = torch.full(A.shape, 7.0, dtype=torch.float32, device="cuda")
+        dB = torch.full(B.shape, 7.0, dtype=torch.float32, device="cuda")
+        qf.qlinear_grouped_lora_fwd(d, lo, offd, Xd, Wd, Y, ws)
+        if reuse:
+            d = qf.grouped_desc(E, T, N, K, wfmt, afmt, flags=qf.FLAG_REUSE_WS)
+        qf.qlinear_grouped_lora_bwd_ste(d, lo, offd, dYd, Xd, Wd, dX, dA, dB, ws)
+        torch.cuda.synchronize()
+        return from_dev(Y), from_dev(dX), from_dev(dA), from_dev(dB)
+
+    Y, dX, dA, dB = run(False)
+    xh = oracle.lora_quant_grouped(W, B, A, s, wfmt) if wfmt != "none" else None
+    ahat = oracle.fakequant(X, afmt)
+    Yr = np.zeros((T, N))
+    dXr = np.zeros((T, K))
+    for e in range(E):
+        rows = slice(off[e], off[e + 1])
+        Yr[rows] = oracle.linear_fwd(ahat[rows], xh[e])
+        dXr[rows] = oracle.linear_dx(dY[rows], xh[e])
+    assert_close(bf16_to_f64(Y), Yr, "Y")
+    assert_close(bf16_to_f64(dX), dXr, "dX")
+    rA, rB = oracle.lora_grads_grouped(dY, ahat, off, B, A, s)
+    assert_close(dA.astype(np.float64), rA, "dA")
+    assert_close(dB.astype(np.float64), rB, "dB")
+    if shared != "A":
+        assert np.all(dA[1] == 0.0)        # expert 1 has no rows
+    if shared != "B":
+        assert np.all(dB[1] == 0.0)
+    again = run(True)
+    for a, b in zip((Y, dX, dA, dB), again):
+        assert np.array_equal(a, b)
+
+
+def test_grouped_lora_no_tokens(qf):
+    E, N, K, r = 3, 64, 256, 4
+    off = np.zeros(E + 1, np.int64)
+    W = workloads.normal_bf16(np.random.default_rng(1), (E * N, K), 0.02)
+    A = np.ones((E, r, K), np.float32)
+    B = np.ones((E, N, r), np.float32)
+    lo = qf.lora(_dev_f32(A), _dev_f32(B), 1.0)
+    d = qf.grouped_desc(E, 0, N, K, "mxfp4", "none")
+    ws = qf.grouped_lora_workspace(d, lo)
+    dA = torch.full(A.shape, 7.0, dtype=torch.float32, device="cuda")
+    dB = torch.full(B.shape, 7.0, dtype=torch.float32, device="cuda")
+    e0 = torch.empty(0, K, dtype=torch.int16, device="cuda")
+    e1 = torch.empty(0, N, dtype=torch.int16, device="cuda")
+    qf.qlinear_grouped_lora_bwd_ste(d, lo, torch.from_numpy(off).cuda(), e1, e0, to_dev(W), None,
+                                    dA, dB, ws)
+    torch.cuda.synchronize()
+    assert np.all(from_dev(dA) == 0.0) and np.all(from_dev(dB) == 0.0)
