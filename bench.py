@@ -265,7 +265,8 @@ def other_rows(qf, torch, dev):
     data drawn on the GPU): every quantizer and the amax pass over W-shaped tensors through
     rotating buffers, the transpose, the 9B-class dense layer at 32K tokens (NVFP4 weights,
     tied QKV and gate/up scales), the 128-expert grouped layer (NVFP4 weights, Zipf(1.1)
-    top-8 routing) and the Q4_K export packing + forward GEMM."""
+    top-8 routing), the LoRA-QAD layer (rank-16 adapter on the MLP up-projection) and the
+    Q4_K export packing + forward GEMM."""
     import workloads
     gen = torch.Generator(device="cuda")
     gen.manual_seed(0)
@@ -362,6 +363,41 @@ def other_rows(qf, torch, dev):
     del glayers
     torch.cuda.empty_cache()
 
+    # ---- LoRA-QAD: the MXFP4 W4A4 MLP up-projection with a rank-16 adapter -------------------
+    out["lora_mlp_up_r16"] = lora_row(qf, torch, dev, gen)
+
+    # ---- MoE LoRA-QAD: the same 128 experts with rank-16 adapters in the hybrid layout ------
+    _, offsets = workloads.moe_routing(seed=0, tokens=32768, experts=128, topk=8)
+    off = torch.from_numpy(offsets).to(dev)
+    r = 16
+    glayers = []
+    for n, k, shared in ((2 * I, H, "A"), (H, I, "B")):
+        Xg = _randn_bf16(torch, gen, (Tm, k))
+        Wg = _randn_bf16(torch, gen, (E * n, k), 0.02)
+        dYg = _randn_bf16(torch, gen, (Tm, n))
+        Ag = torch.randn((r, k) if shared == "A" else (E, r, k), generator=gen, device=dev) / np.sqrt(k)
+        Bg = torch.randn((n, r) if shared == "B" else (E, n, r), generator=gen, device=dev) * (0.001 * np.sqrt(k / r))
+        lo = qf.lora(Ag.contiguous(), Bg.contiguous(), 2.0, a_shared=shared == "A",
+                     b_shared=shared == "B")
+        d = qf.grouped_desc(E, Tm, n, k, "nvfp4", "none")
+        glayers.append((d, lo, Xg, Wg, dYg, torch.empty(Tm, n, dtype=torch.bfloat16, device=dev),
+                        torch.empty(Tm, k, dtype=torch.bfloat16, device=dev),
+                        torch.empty_like(Ag), torch.empty_like(Bg), qf.grouped_lora_workspace(d, lo)))
+
+    def moe_lora_step():
+        for d, lo, Xg, Wg, dYg, Yg, dXg, dAg, dBg, ws in glayers:
+            qf.qlinear_grouped_lora_fwd(d, lo, off, Xg, Wg, Yg, ws)
+            qf.qlinear_grouped_lora_bwd_ste(d, lo, off, dYg, Xg, Wg, dXg, dAg, dBg, ws)
+
+    ms = _time(torch, moe_lora_step, reps=3, warm=1)
+    gf = 2 * 2.0 * Tm * (2 * I * H + H * I)
+    out["moe_lora_nvfp4_r16"] = {"ms": round(ms, 3), "TFLOPs": round(gf / (ms * 1e-3) / 1e12, 1),
+                                 "work": "the 128-expert layer above with frozen expert weights and "
+                                         "rank-16 adapters (gate/up: A shared, down: B shared), fwd + "
+                                         "STE bwd (dX, dA, dB); TFLOPs counts fwd + dX GEMMs"}
+    del glayers
+    torch.cuda.empty_cache()
+
     # ---- Q4_K export: quantize + pack W [14336, 4096], then the forward GEMM at M = 4096 ----
     Wq = _randn_bf16(torch, gen, (N, K), 0.02, row_scale=torch.exp(0.5 * torch.randn(N, generator=gen, device=dev)))
     Xq = _randn_bf16(torch, gen, (4096, K))
@@ -378,6 +414,53 @@ def other_rows(qf, torch, dev):
         "forward_TFLOPs": round(2.0 * 4096 * N * K / (ms_fwd * 1e-3) / 1e12, 1),
         "work": "W 14336x4096 (per-row log-normal scale) -> 144-byte blocks; Y = X Q(W)^T, X 4096x4096"}
     return out
+
+
+def lora_row(qf, torch, dev, gen):
+    """LoRA-QAD step on the MLP up-projection shape (X 8192x4096, frozen W 14336x4096, rank-16
+    FP32 factors, scale 2): the layer's two C-ABI calls (merged quantize + forward GEMM; merged
+    transposed quantize + dX GEMM + dA, dB), and each backward output on its own."""
+    M, N, K, r = 8192, 14336, 4096, 16
+    X = _randn_bf16(torch, gen, (M, K))
+    W = _randn_bf16(torch, gen, (N, K), 0.02)
+    dY = _randn_bf16(torch, gen, (M, N))
+    A = torch.randn(r, K, generator=gen, device=dev) * (1.0 / np.sqrt(K))
+    B = torch.randn(N, r, generator=gen, device=dev) * (0.001 * np.sqrt(K / r))
+    lo = qf.lora(A.contiguous(), B.contiguous(), 2.0)
+    d = qf.qlinear_desc(M, N, K, "mxfp4", "mxfp4")
+    ws = qf.lora_workspace(d, lo)
+    Y = torch.empty(M, N, dtype=torch.bfloat16, device=dev)
+    dX = torch.empty(M, K, dtype=torch.bfloat16, device=dev)
+    dA = torch.empty(r, K, dtype=torch.float32, device=dev)
+    dB = torch.empty(N, r, dtype=torch.float32, device=dev)
+    xh = torch.empty(N, K, dtype=torch.bfloat16, device=dev)
+    tr = torch.empty(K, N, dtype=torch.bfloat16, device=dev)
+
+    def step():
+        qf.qlinear_lora_fwd(d, lo, X, W, Y, ws)
+        qf.qlinear_lora_bwd_ste(d, lo, dY, X, W, dX, dA, dB, ws)
+
+    ms = _time(torch, step, reps=10, warm=2)
+    ms_fwd = _time(torch, lambda: qf.qlinear_lora_fwd(d, lo, X, W, Y, ws), reps=10)
+    ms_dx = _time(torch, lambda: qf.qlinear_lora_bwd_ste(d, lo, dY, X, W, dX, None, None, ws), reps=10)
+    ms_da = _time(torch, lambda: qf.qlinear_lora_bwd_ste(d, lo, dY, X, W, None, dA, None, ws), reps=10)
+    ms_db = _time(torch, lambda: qf.qlinear_lora_bwd_ste(d, lo, dY, X, W, None, None, dB, ws), reps=10)
+    ms_q = _time(torch, lambda: qf.lora_fakequant(W, lo, "mxfp4", xhat=xh), reps=20)
+    ms_qt = _time(torch, lambda: qf.lora_fakequant_transposed(W, lo, "mxfp4", tr), reps=20)
+    gemm = 2.0 * M * N * K
+    lora_flops = 2 * (2.0 * N * K * r) + 2 * (2.0 * M * K * r) + 2 * (2.0 * M * N * r)
+    merge_gflop = 2.0 * N * K * r / 1e9
+    return {
+        "ms": round(ms, 4),
+        "TFLOPs": round((2 * gemm + lora_flops) / (ms * 1e-3) / 1e12, 1),
+        "fwd_ms": round(ms_fwd, 4), "bwd_dX_only_ms": round(ms_dx, 4),
+        "bwd_dA_only_ms": round(ms_da, 4), "bwd_dB_only_ms": round(ms_db, 4),
+        "merged_quant_us": round(ms_q * 1e3, 2),
+        "merged_quant_GBps": round(N * K * 4.0 / (ms_q * 1e-3) / 1e9, 1),
+        "merged_quant_TFLOPs": round(merge_gflop / (ms_q * 1e-3) / 1e3, 2),
+        "merged_quant_transposed_us": round(ms_qt * 1e3, 2),
+        "work": "X 8192x4096, W 14336x4096 frozen, A 16x4096 / B 14336x16 FP32, MXFP4 W4A4; "
+                "fwd + STE bwd (dX, dA, dB); TFLOPs counts fwd + dX GEMMs and the rank-16 terms"}
 
 
 def cpu_baseline(w, rows):

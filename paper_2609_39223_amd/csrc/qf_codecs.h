@@ -44,17 +44,6 @@ __device__ __forceinline__ uint32_t bf16_rne(float f) {
   return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
 }
 
-// E2M1 magnitude code of v >= 0 (finite or +inf): nearest of {0,.5,1,1.5,2,3,4,6}, ties to
-// the even code, saturating at 6.  Below 1 the spacing is 0.5 (round 2v); from 1 up the
-// value has one fraction bit, so round the binary32 fraction to 1 bit on the bit pattern.
-__device__ __forceinline__ uint32_t e2m1_code(float v) {
-  if (v < 1.0f) return (uint32_t)__builtin_rintf(v * 2.0f);
-  uint32_t u = as_u32(v);
-  uint32_t r = u + 0x1FFFFFu + ((u >> 22) & 1u);
-  uint32_t m = (r >> 22) - 252u;          // (biased exp 127,128,129) x 2 + fraction bit - 252
-  return m < 7u ? m : 7u;
-}
-
 // E2M1 magnitude as binary32 (code 0..7).
 __device__ __forceinline__ float e2m1_value(uint32_t m) {
   uint32_t b = m >= 2u ? (m + 252u) << 22 : (m == 1u ? 0x3F000000u : 0u);
@@ -125,6 +114,37 @@ __device__ __forceinline__ uint32_t max_abs_bits8(const uint32_t h[8]) {
 // Each function quantizes and dequantizes this lane's 8 elements h[] (bf16 bits); the lanes
 // of one format block must run it together (cross-lane reductions).
 
+// ---- gfx950 FP4 conversions ----------------------------------------------------------------
+// v_cvt_scalef32_pk_fp4_{bf16,f32} encode two values as E2M1 codes of x / 2^s (nearest, ties to
+// the even code, saturating at 6, sign copied including -0; NaN encodes as magnitude 7), and
+// v_cvt_scalef32_pk_bf16_fp4 decodes two codes to bf16(+-V * 2^s); both use only the exponent
+// field of the FP32 scale (2^s; field 0 means 2^-127).  These equalities were checked on the
+// GPU for every bf16 input and scale exponents -127..127, and the quantizer parity tests pin
+// them against the oracle.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float e8m0_scale(uint32_t e) {     // 2^(e - 127), e in 0..254
+  return as_f32((e << 23) | 0x00400000u);
+}
+
+// Four E2M1 bytes (8 codes, element k in nibble k) of the bf16 words w[0..3] divided by 2^s.
+__device__ __forceinline__ uint32_t fp4_encode8(const uint32_t w[4], float scale) {
+  uint32_t cw = 0;
+  cw = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(cw, __builtin_bit_cast(bf16x2_t, w[0]), scale, 0);
+  cw = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(cw, __builtin_bit_cast(bf16x2_t, w[1]), scale, 1);
+  cw = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(cw, __builtin_bit_cast(bf16x2_t, w[2]), scale, 2);
+  cw = __builtin_amdgcn_cvt_scalef32_pk_fp4_bf16(cw, __builtin_bit_cast(bf16x2_t, w[3]), scale, 3);
+  return cw;
+}
+
+// bf16 words (two elements each) of the 8 codes in cw times 2^s.
+__device__ __forceinline__ void fp4_decode8(uint32_t cw, float scale, uint32_t w[4]) {
+  w[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(cw, scale, 0));
+  w[1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(cw, scale, 1));
+  w[2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(cw, scale, 2));
+  w[3] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(cw, scale, 3));
+}
+
 // NVFP4 (16-block = this lane and lane ^ 1): 4-bit codes cw (element k in nibble k), E4M3
 // block scale sc, x_hat bits xh.  S is the FP32 tensor scale g / (6 * 448), six_s = 6 S.
 __device__ __forceinline__ void nvfp4_chunk(const uint32_t h[8], float S, float six_s,
@@ -139,12 +159,22 @@ __device__ __forceinline__ void nvfp4_chunk(const uint32_t h[8], float S, float 
   }
   const float D = S * e4m3_value(sc);       // block decode scale s_FP32 * s_E4M3,b
   const float rcp = D != 0.0f ? 1.0f / D : 0.0f;
+  // magnitude codes of fl(|x| * rcp) (scale 2^0), then the sign bit of each input; D = 0
+  // gives magnitude 0 for every element (also for Inf / NaN inputs under a caller's g = 0)
+  uint32_t mc = 0;
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const float v0 = as_f32((h[2 * p] & 0x7FFFu) << 16) * rcp;
+    const float v1 = as_f32((h[2 * p + 1] & 0x7FFFu) << 16) * rcp;
+    const uint32_t c2 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, v0, v1, 1.0f, 0);
+    mc |= (c2 & 0xFFu) << (8 * p);
+  }
+  if (D == 0.0f) mc = 0;
   cw = 0;
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
     const uint32_t sign = h[k] >> 15;
-    uint32_t m = 0;
-    if (D != 0.0f) m = e2m1_code(as_f32((h[k] & 0x7FFFu) << 16) * rcp);
+    const uint32_t m = (mc >> (4 * k)) & 7u;
     cw |= ((sign << 3) | m) << (4 * k);
     const float mag = e2m1_value(m) * D;
     xh[k] = bf16_rne(sign ? -mag : mag);
@@ -163,19 +193,16 @@ __device__ __forceinline__ void mxfp4_chunk(const uint32_t h[8], uint32_t& cw, u
   const bool nonfinite = ab >= 0x7F80u;     // Inf or NaN somewhere in the block
   const uint32_t E = ab >> 7;               // biased exponent of the block max
   const uint32_t e = E >= 2u ? E - 2u : 0u; // scale code: floor(log2 a) - 2, clamped
-  const float up = as_f32((254u - e) << 23);  // 2^(127 - e): divides by the scale exactly
-  cw = 0;
+  const float sc = e8m0_scale(e);
+  const uint32_t w[4] = {h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                         h[6] | (h[7] << 16)};
+  cw = fp4_encode8(w, sc);                  // nearest E2M1 of x / 2^(e - 127)
+  uint32_t d[4];
+  fp4_decode8(cw, sc, d);                   // x_hat = +-V * 2^(e - 127)
 #pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    const uint32_t sign = h[k] >> 15;
-    const uint32_t m = e2m1_code(as_f32((h[k] & 0x7FFFu) << 16) * up);
-    // x_hat = +-V(m) * 2^(e-127) written directly as bf16 bits
-    uint32_t b;
-    if (m == 0u) b = 0u;
-    else if (e < 2u && m < 4u) b = m << (e + 5u);             // bf16 subnormal range
-    else b = (e << 7) - 128u + (m >= 2u ? 64u * m : 0u);
-    cw |= ((sign << 3) | m) << (4 * k);
-    xh[k] = b | (sign << 15);
+  for (int p = 0; p < 4; ++p) {
+    xh[2 * p] = d[p] & 0xFFFFu;
+    xh[2 * p + 1] = d[p] >> 16;
   }
   scale = e;
   if (nonfinite) {
