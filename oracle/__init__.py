@@ -360,3 +360,28 @@ def lora_quant_grouped(w: np.ndarray, B: np.ndarray, A: np.ndarray, scale: float
     E = w.shape[0]
     return np.stack([lora_quant(w[e], _expert_factor(B, e, 3), _expert_factor(A, e, 3), scale,
                                 fmt)["xhat"] for e in range(E)])
+
+
+# --------------------------------------------------------------------- QAD distillation loss
+def _log_softmax_f64(z: np.ndarray) -> np.ndarray:
+    m = z.max(axis=1, keepdims=True)
+    return z - (m + np.log(np.exp(z - m).sum(axis=1, keepdims=True)))
+
+
+def qad_kl(zt: np.ndarray, zs: np.ndarray):
+    """Token-averaged forward KL of Eq. qad-objective in FP64 from bf16 logits [L, V] of the
+    teacher (zt) and the student (zs): p = softmax over the vocabulary per token,
+    KL_t = sum_v p_T log(p_T / p_S), loss = mean_t KL_t.  Its gradient with respect to the
+    student's logits is (p_S - p_T) / L (the softmax Jacobian applied to -p_T / p_S).
+    Also returns the teacher-student top-1 agreement per token (first index among equal
+    maxima, compared on the bf16 logits).  Returns (loss, kl [L], grad [L, V], agree [L])."""
+    t = bf16_array_to_f64(zt)
+    s = bf16_array_to_f64(zs)
+    L = t.shape[0]
+    lt, ls = _log_softmax_f64(t), _log_softmax_f64(s)
+    pt, ps = np.exp(lt), np.exp(ls)
+    kl = (pt * (lt - ls)).sum(axis=1)
+    loss = float(kl.mean()) if L else 0.0
+    grad = (ps - pt) / max(L, 1)
+    agree = (t.argmax(axis=1) == s.argmax(axis=1)).astype(np.int32)
+    return loss, kl, grad, agree
