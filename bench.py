@@ -398,6 +398,9 @@ def other_rows(qf, torch, dev):
     del glayers
     torch.cuda.empty_cache()
 
+    # ---- QAD distillation loss: 8192 tokens over a 151936-token vocabulary ------------------
+    out["qad_kl_8k_v152k"] = kl_row(qf, torch, dev, gen)
+
     # ---- Q4_K export: quantize + pack W [14336, 4096], then the forward GEMM at M = 4096 ----
     Wq = _randn_bf16(torch, gen, (N, K), 0.02, row_scale=torch.exp(0.5 * torch.randn(N, generator=gen, device=dev)))
     Xq = _randn_bf16(torch, gen, (4096, K))
@@ -461,6 +464,37 @@ def lora_row(qf, torch, dev, gen):
         "merged_quant_transposed_us": round(ms_qt * 1e3, 2),
         "work": "X 8192x4096, W 14336x4096 frozen, A 16x4096 / B 14336x16 FP32, MXFP4 W4A4; "
                 "fwd + STE bwd (dX, dA, dB); TFLOPs counts fwd + dX GEMMs and the rank-16 terms"}
+
+
+def kl_row(qf, torch, dev, gen):
+    """Forward KL of Eq. qad-objective with its student-logit gradient and top-1 agreement, for
+    one 8K-token sequence over a 151936-token vocabulary (bf16 logits, teacher 2 N(0,1) with
+    three boosted tokens per row, student = teacher + N(0, 0.25))."""
+    L, V = 8192, 151936
+    t = torch.randn(L, V, generator=gen, device=dev) * 2
+    hot = torch.randint(0, V, (L, 3), generator=gen, device=dev)
+    t.scatter_add_(1, hot, torch.rand(L, 3, generator=gen, device=dev) * 8 + 6)
+    s = t + torch.randn(L, V, generator=gen, device=dev) * 0.5
+    zt, zs = t.to(torch.bfloat16), s.to(torch.bfloat16)
+    del t, s
+    kl = torch.empty(L, dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    agree = torch.empty(L, dtype=torch.int32, device=dev)
+    grad = torch.empty(L, V, dtype=torch.bfloat16, device=dev)
+    ms = _time(torch, lambda: qf.qad_kl(zt, zs, kl, loss=loss, grad=grad, agree=agree), reps=10)
+    ms_loss = _time(torch, lambda: qf.qad_kl(zt, zs, kl, loss=loss, agree=agree), reps=10)
+    n = L * V
+    out = {"ms": round(ms, 4), "tokens_per_s": round(L / (ms * 1e-3), 1),
+           "GBps_algorithmic": round(n * 6.0 / (ms * 1e-3) / 1e9, 1),
+           "frac_hbm": round(n * 6.0 / (ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+           "loss_only_ms": round(ms_loss, 4),
+           "loss_only_GBps": round(n * 4.0 / (ms_loss * 1e-3) / 1e9, 1),
+           "loss": round(float(loss.item()), 6),
+           "work": "L=8192 tokens, V=151936, bf16 logits; algorithmic bytes 6 per element "
+                   "(two logits read, gradient written); the kernel reads the logits twice"}
+    del zt, zs, grad
+    torch.cuda.empty_cache()
+    return out
 
 
 def cpu_baseline(w, rows):

@@ -369,6 +369,28 @@ QF_API qf_status qf_qlinear_grouped_lora_bwd_ste(const qf_grouped_desc* d, const
                                                  float* dB, void* ws, size_t ws_bytes,
                                                  qf_stream_t stream);
 
+/* ---------------------------------------------------------------------------------------
+ * QAD distillation loss (Sec. 3.3 "Quantization-aware distillation", Eq. qad-objective)
+ * ------------------------------------------------------------------------------------ */
+/*
+ * qf_qad_kl -- token-averaged forward KL between the teacher's and the student's softmax
+ * distributions over the vocabulary, its gradient with respect to the student's logits, and
+ * the teacher-student top-1 agreement (a training metric of Sec. 4).
+ *   zt, zs     bf16 logits [L, V] of the frozen teacher and of the student (row strides ldt,
+ *              lds, multiples of 8); V % 8 == 0; logits must be finite.
+ *   row_kl     FP32 [L], required: KL_t = sum_v p_T log(p_T / p_S) per token (FP32 online
+ *              log-sum-exp statistics; deterministic order).
+ *   loss       FP32 device scalar or NULL: (1/L) sum_t KL_t.
+ *   grad       bf16 [L, V] (row stride ldg) or NULL: grad_scale * (p_S - p_T); with
+ *              grad_scale = 1/L this is d loss / d z_S.
+ *   agree      int32 [L] or NULL: 1 where the first maximum of z_T and of z_S are at the
+ *              same index, else 0.
+ * L = 0 gives loss 0.
+ */
+QF_API qf_status qf_qad_kl(const uint16_t* zt, int64_t ldt, const uint16_t* zs, int64_t lds,
+                           int64_t L, int64_t V, float grad_scale, float* row_kl, float* loss,
+                           uint16_t* grad, int64_t ldg, int32_t* agree, qf_stream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -105,6 +105,8 @@ def lib() -> ctypes.CDLL:
             "qf_qlinear_lora_bwd_ste": ([ctypes.POINTER(QLinearDesc), ctypes.POINTER(LoRA), _P,
                                          _P, _P, _P, _P, _P, _P, ctypes.c_size_t, _P],
                                         ctypes.c_int),
+            "qf_qad_kl": ([_P, _I, _P, _I, _I, _I, ctypes.c_float, _P, _P, _P, _I, _P, _P],
+                          ctypes.c_int),
             "qf_grouped_lora_workspace_size": ([ctypes.POINTER(GroupedDesc), ctypes.POINTER(LoRA),
                                                 ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
             "qf_qlinear_grouped_lora_fwd": ([ctypes.POINTER(GroupedDesc), ctypes.POINTER(LoRA), _P,
@@ -348,3 +350,19 @@ def qlinear_grouped_lora_bwd_ste(desc, lo: LoRA, offsets, dY, X, W, dX, dA, dB, 
                                                  _ptr(offsets), _ptr(_bf16(dY)), _ptr(_bf16(X)),
                                                  _ptr(_bf16(W)), _ptr(_bf16(dX)), _ptr(dA),
                                                  _ptr(dB), _ptr(ws), ws.numel(), _stream()))
+
+
+# ------------------------------------------------------------------ QAD distillation loss
+def qad_kl(zt, zs, row_kl, loss=None, grad=None, agree=None, grad_scale=None):
+    """Forward KL of Eq. qad-objective per token (row_kl), its mean (loss), the student-logit
+    gradient grad_scale * (p_S - p_T) (default grad_scale = 1/L) and top-1 agreement."""
+    L, V, ldt = _rows(_bf16(zt))
+    L2, V2, lds = _rows(_bf16(zs))
+    if (L2, V2) != (L, V):
+        raise ValueError("teacher and student logits must have the same shape")
+    ldg = 0
+    if grad is not None:
+        _, _, ldg = _rows(_bf16(grad))
+    gs = (1.0 / L if L else 1.0) if grad_scale is None else float(grad_scale)
+    _check(lib().qf_qad_kl(_ptr(zt), ldt, _ptr(zs), lds, L, V, gs, _ptr(row_kl), _ptr(loss),
+                           _ptr(grad), ldg, _ptr(agree), _stream()))

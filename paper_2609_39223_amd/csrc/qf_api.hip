@@ -1067,4 +1067,23 @@ qf_status qf_qlinear_grouped_lora_bwd_ste(const qf_grouped_desc* d, const qf_lor
   return ok();
 }
 
+// ------------------------------------------------------------------ QAD distillation loss
+qf_status qf_qad_kl(const uint16_t* zt, int64_t ldt, const uint16_t* zs, int64_t lds, int64_t L,
+                    int64_t V, float grad_scale, float* row_kl, float* loss, uint16_t* grad,
+                    int64_t ldg, int32_t* agree, qf_stream_t stream) {
+  const char* fn = "qf_qad_kl";
+  if (L < 0 || V < 0) return fail(QF_ESHAPE, "%s: negative shape", fn);
+  if (V % 8) return fail(QF_ESHAPE, "%s: V=%lld is not a multiple of 8", fn, (long long)V);
+  if (L > 0 && V == 0) return fail(QF_ESHAPE, "%s: empty vocabulary", fn);
+  QF_TRY(check_mat("qf_qad_kl: zt", zt, L, V, ldt, true));
+  QF_TRY(check_mat("qf_qad_kl: zs", zs, L, V, lds, true));
+  QF_TRY(check_mat("qf_qad_kl: grad", grad, L, V, ldg, false));
+  if (L > 0 && !row_kl) return fail(QF_EINVAL, "%s: null row_kl", fn);
+  QF_TRY(check_out("qf_qad_kl: agree", agree));
+  QF_TRY(dev(qf::launch_qad_kl(zt, ldt, zs, lds, L, V, grad_scale, row_kl, loss, grad, ldg, agree,
+                               S(stream)),
+             "qad kl"));
+  return ok();
+}
+
 }  // extern "C"

@@ -127,4 +127,11 @@ hipError_t launch_lora_colsum(const uint16_t* Big, int64_t M, int64_t C, int64_t
 // Ft [z][r][N] = F[z]^T for `batch` FP32 [N, r] matrices stored back to back.
 hipError_t launch_transpose_f32(const float* F, int64_t N, int64_t r, int64_t batch, float* Ft,
                                 hipStream_t s);
+
+// ---- QAD distillation loss (qf_kl.hip) ---------------------------------------------------------
+// Per row of bf16 logits [L, V] (V % 8 == 0): row_kl[t], optional loss (mean), grad
+// (gscale (p_S - p_T), bf16) and agree (top-1 equality).
+hipError_t launch_qad_kl(const uint16_t* zt, int64_t ldt, const uint16_t* zs, int64_t lds_,
+                         int64_t L, int64_t V, float gscale, float* row_kl, float* loss,
+                         uint16_t* grad, int64_t ldg, int32_t* agree, hipStream_t s);
 }  // namespace qf

@@ -21,6 +21,12 @@ tensor shapes and value distributions of the layers it quantizes (Sec. 3.2, Sec.
                         popularity (Gumbel-top-8 sampling), hidden 3072, expert intermediate
                         1536: W_gu [128][3072][3072], W_d [128][3072][1536] ~ N(0,0.02).
 * ``q4k_weight``        W [14336,4096] ~ N(0,0.02) x per-row log-normal(0,0.5), X [4096,4096] ~ N(0,1).
+* ``qad_logits``        Teacher / student logits for the QAD loss (Sec. 3.3, Eq. qad-objective):
+                        L tokens over a vocabulary V (the paper's Qwen3 models: 151936),
+                        teacher z_T = 2 N(0,1) plus +6..+14 on 1..4 "preferred" tokens per row
+                        (peaked next-token distributions), student z_S = z_T + N(0, 0.5^2)
+                        (a quantization-perturbed copy: KL per token ~0.1, as in the paper's
+                        evaluation KL), both rounded to bf16.
 * ``lora_factors``      LoRA-QAD adapters of rank r on an [N, K] weight (Sec. 3.3; the paper's
                         ranks are 4, 16, 64, 256 and its memory table uses 16): FP32
                         A [r, K] ~ N(0, 1/K) and B [N, r] ~ N(0, (0.001 sqrt(K/r))^2), so a
@@ -170,3 +176,22 @@ def lora_factors(seed: int, N: int, K: int, r: int = 16, alpha: float | None = N
     B = (rng.standard_normal((N, r), dtype=np.float32) * np.float32(0.001 * np.sqrt(K / r)))
     a = 2.0 * r if alpha is None else float(alpha)
     return {"A": A.astype(np.float32), "B": B.astype(np.float32), "r": r, "scale": a / r}
+
+
+def qad_logits(seed: int, L: int, V: int = 151936) -> dict:
+    """bf16 teacher / student logits [L, V] (see the module docstring)."""
+    rng = np.random.default_rng(seed)
+    zt = np.empty((L, V), np.uint16)
+    zs = np.empty((L, V), np.uint16)
+    step = max(1, (1 << 22) // max(V, 1))
+    for r0 in range(0, L, step):
+        r1 = min(L, r0 + step)
+        t = rng.standard_normal((r1 - r0, V), dtype=np.float32) * np.float32(2.0)
+        for i in range(r1 - r0):
+            k = int(rng.integers(1, 5))
+            idx = rng.integers(0, V, size=k)
+            t[i, idx] += rng.uniform(6.0, 14.0, size=k).astype(np.float32)
+        s_ = t + rng.standard_normal((r1 - r0, V), dtype=np.float32) * np.float32(0.5)
+        zt[r0:r1] = to_bf16(t)
+        zs[r0:r1] = to_bf16(s_)
+    return {"zt": zt, "zs": zs, "L": L, "V": V}
