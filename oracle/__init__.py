@@ -10,7 +10,8 @@ Contents
   plain C codecs for E2M1, E4M3, E8M0, bfloat16, float16 and the three quantizers
   NVFP4 / MXFP4 / Q4_K (QATFactory Sec. 3.2.3, Tab. formats; Eqs. nvfp4-dequant,
   mxfp4-dequant, q4k-dequant), plus Q4_K block packing (Sec. 3.5, engine-native export)
-  and the LoRA merge W + s B A in binary32 (Sec. 3.3, Eqs. qad-lora, export-lora).
+  and the LoRA merge W + s B A in binary32 (Sec. 3.3, Eqs. qad-lora, export-lora), and a
+  Q4_K quantizer whose sub-block steps come from a search minimizing ||W - W_q||^2 (Sec. 4).
 * FP64 linear-layer references in this module: the forward O = A_hat W_hat^T
   (Eq. fakequant, written for row-major activations) and the straight-through backward
   dA = dO W_hat (Eq. activation-ste), dW = dO^T A_hat (Eqs. ste, activation-gradient-error).
@@ -85,6 +86,10 @@ def lib():
         L.or_q4k_unpack_block.argtypes = [_u8p, ctypes.POINTER(ctypes.c_uint16),
                                           ctypes.POINTER(ctypes.c_uint16), ip, ip, ip]
         L.or_q4k_unpack_block.restype = None
+        L.or_q4k_mse_quant.argtypes = [_u16p, _i64, _i64, _i64, _u8p, _u16p]
+        L.or_q4k_mse_quant.restype = None
+        L.or_q4k_mse_subblock.argtypes = [_f32p, _f32p, _f32p, ctypes.POINTER(ctypes.c_int)]
+        L.or_q4k_mse_subblock.restype = None
         L.or_lora_merge.argtypes = [_u16p, _i64, _i64, _i64, _f32p, _f32p, _i64, ctypes.c_float,
                                     _u16p]
         L.or_lora_merge.restype = None
@@ -385,3 +390,27 @@ def qad_kl(zt: np.ndarray, zs: np.ndarray):
     grad = (ps - pt) / max(L, 1)
     agree = (t.argmax(axis=1) == s.argmax(axis=1)).astype(np.int32)
     return loss, kl, grad, agree
+
+
+# ----------------------------------------------------------------- Q4_K with an MSE search
+def q4k_mse(x: np.ndarray) -> dict:
+    """Q4_K with searched sub-block steps (the scale search minimizes ||W - W_q||^2, the
+    objective of the paper's Q4_K PTQ baseline, Sec. 4): same 144-byte blocks and x_hat as
+    q4k(); the C function or_q4k_mse_quant states the search."""
+    x, R, K = _rows(x)
+    assert K % 256 == 0
+    packed = np.zeros((R, K // 256, 144), np.uint8)
+    xhat = np.zeros((R, K), np.uint16)
+    lib().or_q4k_mse_quant(_ptr(x, _u16p), R, K, K, _ptr(packed, _u8p), _ptr(xhat, _u16p))
+    return {"packed": packed, "xhat": xhat}
+
+
+def q4k_mse_subblock(x32) -> tuple:
+    """The search for one 32-element sub-block: (a, mu, codes)."""
+    xv = np.ascontiguousarray(x32, np.float32)
+    assert xv.shape == (32,)
+    a = np.zeros(1, np.float32)
+    mu = np.zeros(1, np.float32)
+    q = (ctypes.c_int * 32)()
+    lib().or_q4k_mse_subblock(_ptr(xv, _f32p), _ptr(a, _f32p), _ptr(mu, _f32p), q)
+    return float(a[0]), float(mu[0]), np.array(list(q))

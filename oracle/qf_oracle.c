@@ -498,4 +498,171 @@ void or_lora_merge(const uint16_t* w, int64_t N, int64_t K, int64_t ldw, const f
         }
 }
 
+/* ------------------------------------------------------------------------- */
+/* Q4_K with an MSE search of the sub-block scales (Sec. 4: PTQ searching for   */
+/* scales that minimize ||W - W_q||^2; the search below is this library's own)  */
+/* ------------------------------------------------------------------------- */
+/*
+ * FP32 sums over a 32-element sub-block are taken in one fixed order: four groups of 8
+ * consecutive elements, each summed from +0 in index order, then (g0 + g1) + (g2 + g3);
+ * super-block totals add the 8 sub-block sums as ((s0 + s1) + (s2 + s3)) + ((s4 + s5) +
+ * (s6 + s7)).  (The comparisons between candidates depend on the rounding of these sums, so
+ * the reading fixes their order.)
+ */
+static float sb_sum(const float* f) {
+    float g[4];
+    for (int c = 0; c < 4; ++c) {
+        float s = 0.0f;
+        for (int i = 0; i < 8; ++i) s += f[8 * c + i];
+        g[c] = s;
+    }
+    return (g[0] + g[1]) + (g[2] + g[3]);
+}
+
+static float clampf15(float v) { return v < 0.0f ? 0.0f : (v > 15.0f ? 15.0f : v); }
+
+/*
+ * One sub-block (x[32], signed zeros as +0): min-max anchors lo = min(0, min x), hi = max x,
+ * mu0 = 0 - lo.  Candidate k = 0..16 takes the step a_k = (hi - lo) / (14 + k/4), codes
+ * q = clamp(rne((x + mu0) * fl(1 / a_k)), 0, 15), then refits the step and offset to those
+ * codes by least squares (minimizing sum (x - (a q - mu))^2):
+ *     den = 32 Sqq - Sq^2,  a* = (32 Sqx - Sq Sx) / den,  mu* = (a* Sq - Sx) / 32
+ * (den = 0: keep a_k, mu0); mu* < 0 is moved to the constraint mu = 0 with a* = Sqx / Sqq; a
+ * refit with a* <= 0 keeps a_k, mu0.  a_k = 0 (a constant sub-block at lo) keeps (0, mu0).
+ * The candidate with the smallest error sum (x - fl(fl(a* q) - mu*))^2 wins (the first one
+ * on ties).  Outputs the winning (a, mu) and its codes.
+ */
+static void q4k_mse_subblock(const float* x, float* a_out, float* mu_out, int* q_out) {
+    float lo = 0.0f, hi = x[0];
+    for (int i = 0; i < 32; ++i) {
+        if (x[i] < lo) lo = x[i];
+        if (x[i] > hi) hi = x[i];
+    }
+    const float range = hi - lo, mu0 = 0.0f - lo;
+    const float sx = sb_sum(x);
+    float best_e = INFINITY, best_a = range / 15.0f, best_mu = mu0;
+    for (int i = 0; i < 32; ++i) q_out[i] = 0;
+    for (int k = 0; k <= 16; ++k) {
+        const float Dk = 14.0f + 0.25f * (float)k;
+        const float ak = range / Dk;
+        float q[32], ac = ak, mc = mu0;
+        if (ak == 0.0f) {
+            for (int i = 0; i < 32; ++i) q[i] = 0.0f;
+        } else {
+            const float r = 1.0f / ak;
+            float qq[32], qx[32];
+            for (int i = 0; i < 32; ++i) {
+                q[i] = clampf15((float)rne_int((x[i] + mu0) * r));
+                qq[i] = q[i] * q[i];
+                qx[i] = q[i] * x[i];
+            }
+            const float sq = sb_sum(q), sqq = sb_sum(qq), sqx = sb_sum(qx);
+            const float den = 32.0f * sqq - sq * sq;
+            if (den > 0.0f) {
+                ac = (32.0f * sqx - sq * sx) / den;
+                mc = (ac * sq - sx) / 32.0f;
+                if (mc < 0.0f) {
+                    mc = 0.0f;
+                    ac = sqx / sqq;
+                }
+                if (!(ac > 0.0f)) {
+                    ac = ak;
+                    mc = mu0;
+                }
+            }
+        }
+        float e2[32];
+        for (int i = 0; i < 32; ++i) {
+            const float e = x[i] - (ac * q[i] - mc);
+            e2[i] = e * e;
+        }
+        const float err = sb_sum(e2);
+        if (err < best_e) {
+            best_e = err;
+            best_a = ac;
+            best_mu = mc;
+            for (int i = 0; i < 32; ++i) q_out[i] = (int)q[i];
+        }
+    }
+    *a_out = best_a;
+    *mu_out = best_mu;
+}
+
+void or_q4k_mse_subblock(const float* x, float* a, float* mu, int* q) {
+    q4k_mse_subblock(x, a, mu, q);
+}
+
+/* Super-block from per-sub-block (a_j, mu_j): the 6-bit scale / min quantization and the
+ * final codes of the min-max reading (or_q4k_quant), plus the super-block's error sum of
+ * (x - fl(fl(t1 C) - t2))^2 in the fixed order. */
+static float q4k_finish(const float* x, const float* a, const float* mu, uint16_t* dh,
+                        uint16_t* mh, int* ls, int* lm, int* q, float* xf) {
+    float amx = a[0], mmx = mu[0];
+    for (int j = 1; j < 8; ++j) {
+        if (a[j] > amx) amx = a[j];
+        if (mu[j] > mmx) mmx = mu[j];
+    }
+    *dh = or_f16_from_f32(amx / 63.0f);
+    *mh = or_f16_from_f32(mmx / 63.0f);
+    const float d = or_f16_to_f32(*dh), dmin = or_f16_to_f32(*mh);
+    float s8[8];
+    for (int j = 0; j < 8; ++j) {
+        ls[j] = (d != 0.0f) ? clampi(rne_int(a[j] / d), 0, 63) : 0;
+        lm[j] = (dmin != 0.0f) ? clampi(rne_int(mu[j] / dmin), 0, 63) : 0;
+        const float t1 = d * (float)ls[j], t2 = dmin * (float)lm[j];
+        float e2[32];
+        for (int i = 0; i < 32; ++i) {
+            const float v = x[32 * j + i];
+            int c = 0;
+            if (t1 != 0.0f) c = clampi(rne_int((v + t2) / t1), 0, 15);
+            q[32 * j + i] = c;
+            xf[32 * j + i] = t1 * (float)c - t2;
+            const float e = v - xf[32 * j + i];
+            e2[i] = e * e;
+        }
+        s8[j] = sb_sum(e2);
+    }
+    return ((s8[0] + s8[1]) + (s8[2] + s8[3])) + ((s8[4] + s8[5]) + (s8[6] + s8[7]));
+}
+
+/*
+ * or_q4k_mse_quant -- Q4_K with the searched sub-block steps: per super-block, the search
+ * above gives (a_j, mu_j), q4k_finish quantizes them to 6 bits and recomputes the codes; the
+ * min-max reading does the same from its own (a_j, mu_j); the super-block keeps the search's
+ * result when its error sum is smaller, else the min-max one (so it is never worse).
+ */
+void or_q4k_mse_quant(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, uint8_t* packed,
+                      uint16_t* xhat) {
+    for (int64_t r = 0; r < R; ++r)
+        for (int64_t sb = 0; sb < K / 256; ++sb) {
+            const uint16_t* xs = x + r * ldx + sb * 256;
+            float xv[256];
+            for (int i = 0; i < 256; ++i) xv[i] = or_bf16_to_f32(xs[i]) + 0.0f;   /* -0 -> +0 */
+            float as[8], ms[8], am[8], mm[8];
+            int qtmp[32];
+            for (int j = 0; j < 8; ++j) {
+                q4k_mse_subblock(xv + 32 * j, &as[j], &ms[j], qtmp);
+                float lo = 0.0f, hi = xv[32 * j];
+                for (int i = 0; i < 32; ++i) {
+                    if (xv[32 * j + i] < lo) lo = xv[32 * j + i];
+                    if (xv[32 * j + i] > hi) hi = xv[32 * j + i];
+                }
+                am[j] = (hi - lo) / 15.0f;
+                mm[j] = 0.0f - lo;
+            }
+            uint16_t dh1, mh1, dh2, mh2;
+            int ls1[8], lm1[8], q1[256], ls2[8], lm2[8], q2[256];
+            float xf1[256], xf2[256];
+            const float e1 = q4k_finish(xv, as, ms, &dh1, &mh1, ls1, lm1, q1, xf1);
+            const float e2 = q4k_finish(xv, am, mm, &dh2, &mh2, ls2, lm2, q2, xf2);
+            const int use1 = e1 < e2;
+            if (packed)
+                q4k_pack(packed + (r * (K / 256) + sb) * 144, use1 ? dh1 : dh2, use1 ? mh1 : mh2,
+                         use1 ? ls1 : ls2, use1 ? lm1 : lm2, use1 ? q1 : q2);
+            if (xhat)
+                for (int i = 0; i < 256; ++i)
+                    xhat[r * K + sb * 256 + i] = or_bf16_from_f32(use1 ? xf1[i] : xf2[i]);
+        }
+}
+
 int or_version(void) { return 1; }
