@@ -410,6 +410,20 @@ def other_rows(qf, torch, dev):
     packed = torch.empty(N, K // 256, 144, dtype=torch.uint8, device=dev)
     ms_pack = _time(torch, lambda: qf.fakequant_q4k(Wq, packed, None), reps=10)
     ms_fwd = _time(torch, lambda: qf.qlinear_fwd(d, Xq, Wq, Yq, ws), reps=10)
+    xm = torch.empty(N, K, dtype=torch.bfloat16, device=dev)
+    x0 = torch.empty(N, K, dtype=torch.bfloat16, device=dev)
+    ms_mse = _time(torch, lambda: qf.fakequant_q4k_mse(Wq, packed, xm), reps=5)
+    qf.fakequant_q4k(Wq, None, x0)
+    torch.cuda.synchronize()
+    wf = Wq.float()
+    ratio = float(((wf - xm.float()) ** 2).sum() / ((wf - x0.float()) ** 2).sum())
+    out["q4k_mse_search"] = {
+        "us": round(ms_mse * 1e3, 1),
+        "GBps": round(N * K * (2 + 2 + 144 / 256) / (ms_mse * 1e-3) / 1e9, 1),
+        "sq_error_vs_min_max": round(ratio, 4),
+        "work": "W 14336x4096 (per-row log-normal scale) -> 144-byte blocks + x_hat with the "
+                "searched sub-block steps (17 candidates, least-squares refit); ALU-bound"}
+    del xm, x0, wf
     out["q4k_export_and_forward"] = {
         "pack_us": round(ms_pack * 1e3, 2),
         "pack_GBps": round(N * K * (2 + 144 / 256) / (ms_pack * 1e-3) / 1e9, 1),

@@ -126,6 +126,22 @@ QF_API qf_status qf_fakequant_mxfp4(const uint16_t* x, int64_t R, int64_t K, int
 QF_API qf_status qf_fakequant_q4k(const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
                            uint8_t* packed, uint16_t* xhat, qf_stream_t stream);
 
+/*
+ * qf_fakequant_q4k_mse -- Q4_K (same 144-byte blocks and x_hat convention as qf_fakequant_q4k)
+ * whose sub-block steps and offsets come from a search minimizing ||x - x_hat||^2, the
+ * objective of the Q4_K post-training baseline (Sec. 4 "Quantization-aware distillation":
+ * scales that minimize ||W - W_q||^2).  The search is this library's own: per sub-block of 32,
+ * 17 candidate steps (hi - lo) / (14 + k/4) (lo = min(0, min x), hi = max x) each give codes,
+ * to which step and offset are refitted by least squares (offset >= 0); the candidate with
+ * the smallest squared error wins.  Each super-block keeps the searched result or the
+ * min-max one (qf_fakequant_q4k), whichever decodes with the smaller error, so it is never
+ * worse.  FP32 sums over a sub-block: per 8 consecutive elements in order, then
+ * (g0 + g1) + (g2 + g3); over a super-block: ((s0 + s1) + (s2 + s3)) + ((s4 + s5) + (s6 + s7)).
+ *   x bf16 [R, K], K % 256 == 0; packed [R, K/256, 144] or NULL; xhat bf16 [R, K] or NULL.
+ */
+QF_API qf_status qf_fakequant_q4k_mse(const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
+                                      uint8_t* packed, uint16_t* xhat, qf_stream_t stream);
+
 /* ---------------------------------------------------------------------------------------
  * Quantization-aware linear layer (Eqs. fakequant, ste, activation-ste)
  * ------------------------------------------------------------------------------------ */

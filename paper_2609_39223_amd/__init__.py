@@ -71,6 +71,7 @@ def lib() -> ctypes.CDLL:
                                    ctypes.c_int),
             "qf_fakequant_mxfp4": ([_P, _I, _I, _I, _P, _P, _P, _P], ctypes.c_int),
             "qf_fakequant_q4k": ([_P, _I, _I, _I, _P, _P, _P], ctypes.c_int),
+            "qf_fakequant_q4k_mse": ([_P, _I, _I, _I, _P, _P, _P], ctypes.c_int),
             "qf_workspace_size": ([ctypes.POINTER(QLinearDesc), ctypes.POINTER(ctypes.c_size_t)],
                                   ctypes.c_int),
             "qf_qlinear_fwd": ([ctypes.POINTER(QLinearDesc), _P, _P, _P, _P, ctypes.c_size_t, _P],
@@ -183,6 +184,11 @@ def fakequant_mxfp4(x, codes=None, scales=None, xhat=None):
 def fakequant_q4k(x, packed=None, xhat=None):
     R, K, ld = _rows(_bf16(x))
     _check(lib().qf_fakequant_q4k(_ptr(x), R, K, ld, _ptr(packed), _ptr(xhat), _stream()))
+
+
+def fakequant_q4k_mse(x, packed=None, xhat=None):
+    R, K, ld = _rows(_bf16(x))
+    _check(lib().qf_fakequant_q4k_mse(_ptr(x), R, K, ld, _ptr(packed), _ptr(xhat), _stream()))
 
 
 def fakequant_transposed(x, fmt, out, amax=None):

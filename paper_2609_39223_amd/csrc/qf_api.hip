@@ -264,6 +264,15 @@ qf_status qf_fakequant_q4k(const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
   return ok();
 }
 
+qf_status qf_fakequant_q4k_mse(const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
+                               uint8_t* packed, uint16_t* xhat, qf_stream_t stream) {
+  QF_TRY(check_quant_input("qf_fakequant_q4k_mse", x, R, K, ldx, 256));
+  QF_TRY(check_out("qf_fakequant_q4k_mse: packed", packed));
+  QF_TRY(check_out("qf_fakequant_q4k_mse: xhat", xhat));
+  QF_TRY(dev(qf::launch_q4k_mse(x, R, K, ldx, packed, xhat, S(stream)), "q4k mse"));
+  return ok();
+}
+
 qf_status qf_fakequant_transposed(int fmt, const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
                                   const float* amax, uint16_t* out, int64_t ldo,
                                   qf_stream_t stream) {

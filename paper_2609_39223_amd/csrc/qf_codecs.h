@@ -259,6 +259,134 @@ __device__ __forceinline__ void q4k_chunk(const uint32_t h[8], Q4kChunk& r, uint
 }
 
 
+// ---- Q4_K with searched sub-block steps ------------------------------------------------------
+// Sums over a 32-element sub-block in one fixed order: this lane's 8 elements from +0 in
+// index order, then the quad tree (g0 + g1) + (g2 + g3) (lane ^ 1, then lane ^ 2; the same
+// value lands on all four lanes since each step adds a commutative pair).
+__device__ __forceinline__ float sub_sum(const float f[8]) {
+  float s = 0.0f;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) s += f[k];
+  s = s + xor1_f(s);
+  return s + xor2_f(s);
+}
+// Super-block total of per-sub-block sums (lane L holds sub-block L / 4):
+// ((s0 + s1) + (s2 + s3)) + ((s4 + s5) + (s6 + s7)).
+__device__ __forceinline__ float super_sum(float s) {
+  s = s + xor_swz_f<4>(s);
+  s = s + xor_swz_f<8>(s);
+  return s + xor_swz_f<16>(s);
+}
+
+// The final stage shared by both candidates of a super-block: 6-bit scale / min quantization
+// of (a, mu), codes of the min-max reading's last step, FP32 decode t1 C - t2 and the
+// super-block's squared-error sum.
+__device__ __forceinline__ float q4k_finish(const float xv[8], float a, float mu, Q4kChunk& r,
+                                            float xf[8]) {
+  float A = a, Mx = mu;
+  A = fmaxf(A, xor_swz_f<4>(A)); Mx = fmaxf(Mx, xor_swz_f<4>(Mx));
+  A = fmaxf(A, xor_swz_f<8>(A)); Mx = fmaxf(Mx, xor_swz_f<8>(Mx));
+  A = fmaxf(A, xor_swz_f<16>(A)); Mx = fmaxf(Mx, xor_swz_f<16>(Mx));
+  r.dh = f16_rne_sat(A / 63.0f);
+  r.mh = f16_rne_sat(Mx / 63.0f);
+  const float d = f16_value(r.dh), dmin = f16_value(r.mh);
+  r.ls = 0;
+  r.lm = 0;
+  if (d != 0.0f) r.ls = (uint32_t)fminf(fmaxf(__builtin_rintf(a / d), 0.0f), 63.0f);
+  if (dmin != 0.0f) r.lm = (uint32_t)fminf(fmaxf(__builtin_rintf(mu / dmin), 0.0f), 63.0f);
+  const float t1 = d * (float)r.ls;
+  const float t2 = dmin * (float)r.lm;
+  r.qlo = 0;
+  r.qhi = 0;
+  float e2[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    uint32_t q = 0;
+    if (t1 != 0.0f) q = (uint32_t)fminf(fmaxf(__builtin_rintf((xv[k] + t2) / t1), 0.0f), 15.0f);
+    if (k < 4) r.qlo |= q << (8 * k);
+    else r.qhi |= q << (8 * (k - 4));
+    xf[k] = t1 * (float)q - t2;
+    const float e = xv[k] - xf[k];
+    e2[k] = e * e;
+  }
+  return super_sum(sub_sum(e2));
+}
+
+// Q4_K whose sub-block (step, offset) come from a search of ||x - x_hat||^2: anchors lo =
+// min(0, min x), hi = max x, mu0 = -lo; candidate k = 0..16 quantizes with the step
+// (hi - lo) / (14 + k/4), refits step and offset to those codes by least squares (offset
+// constrained to >= 0; a degenerate or non-positive refit keeps the candidate), and the
+// candidate with the smallest error sum wins (the first on ties).  The super-block then keeps
+// the searched steps or the min-max ones (q4k_chunk), whichever gives the smaller final error.
+__device__ __forceinline__ void q4k_mse_chunk(const uint32_t h[8], Q4kChunk& r, uint32_t xh[8]) {
+  float xv[8];
+  float lo = 0.0f, hi = -__builtin_huge_valf();
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    xv[k] = as_f32(h[k] << 16) + 0.0f;      // signed zeros count as +0
+    lo = fminf(lo, xv[k]);
+    hi = fmaxf(hi, xv[k]);
+  }
+  lo = fminf(lo, xor1_f(lo)); hi = fmaxf(hi, xor1_f(hi));
+  lo = fminf(lo, xor2_f(lo)); hi = fmaxf(hi, xor2_f(hi));
+  const float range = hi - lo, mu0 = 0.0f - lo;
+  const float sx = sub_sum(xv);
+  float best_e = __builtin_huge_valf(), best_a = range / 15.0f, best_mu = mu0;
+#pragma unroll 1
+  for (int k = 0; k <= 16; ++k) {
+    const float Dk = 14.0f + 0.25f * (float)k;
+    const float ak = range / Dk;
+    float q[8], ac = ak, mc = mu0;
+    if (ak == 0.0f) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) q[i] = 0.0f;
+    } else {
+      const float rc = 1.0f / ak;
+      float qq[8], qx[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        q[i] = fminf(fmaxf(__builtin_rintf((xv[i] + mu0) * rc), 0.0f), 15.0f);
+        qq[i] = q[i] * q[i];
+        qx[i] = q[i] * xv[i];
+      }
+      const float sq = sub_sum(q), sqq = sub_sum(qq), sqx = sub_sum(qx);
+      const float den = 32.0f * sqq - sq * sq;
+      if (den > 0.0f) {
+        ac = (32.0f * sqx - sq * sx) / den;
+        mc = (ac * sq - sx) / 32.0f;
+        if (mc < 0.0f) {
+          mc = 0.0f;
+          ac = sqx / sqq;
+        }
+        if (!(ac > 0.0f)) {
+          ac = ak;
+          mc = mu0;
+        }
+      }
+    }
+    float e2[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float e = xv[i] - (ac * q[i] - mc);
+      e2[i] = e * e;
+    }
+    const float err = sub_sum(e2);
+    if (err < best_e) {
+      best_e = err;
+      best_a = ac;
+      best_mu = mc;
+    }
+  }
+  Q4kChunk rs, rm;
+  float xs[8], xm[8];
+  const float es = q4k_finish(xv, best_a, best_mu, rs, xs);
+  const float em = q4k_finish(xv, range / 15.0f, mu0, rm, xm);
+  const bool use_s = es < em;
+  r = use_s ? rs : rm;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) xh[k] = bf16_rne(use_s ? xs[k] : xm[k]);
+}
+
 // Packs one Q4_K super-block held by the 32 lanes of a half-wave (lane L = this lane's index
 // inside the super-block, elements 8L..8L+7) into the 144-byte llama.cpp block at blk: FP16 d
 // and dmin, twelve bytes of 6-bit scales / mins, then 128 bytes of codes (sub-block 2p in the

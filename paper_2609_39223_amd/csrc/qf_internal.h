@@ -20,6 +20,9 @@ hipError_t launch_mxfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, ui
                         uint8_t* scales, uint16_t* xhat, hipStream_t s);
 hipError_t launch_q4k(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, uint8_t* packed,
                       uint16_t* xhat, hipStream_t s);
+// Q4_K with searched sub-block steps (never a larger super-block error than launch_q4k's).
+hipError_t launch_q4k_mse(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, uint8_t* packed,
+                          uint16_t* xhat, hipStream_t s);
 
 // Batched variants over E equally shaped tensors (expert weights), one tensor scale each.
 hipError_t launch_amax_batched(const uint16_t* x, int64_t E, int64_t R, int64_t K,

@@ -149,7 +149,7 @@ __global__ __launch_bounds__(kThreads) void mxfp4_kernel(
 // ============================================================================= Q4_K
 // 32 lanes per 256-element super-block; lane L of the super-block holds elements 8L..8L+7,
 // i.e. sub-block j = L / 4.
-template <int RPT>
+template <int RPT, bool MSE>
 __global__ __launch_bounds__(kThreads) void q4k_kernel(const uint16_t* __restrict__ x, int64_t R,
                                                        int64_t K, int64_t ldx,
                                                        uint8_t* __restrict__ packed,
@@ -168,7 +168,8 @@ __global__ __launch_bounds__(kThreads) void q4k_kernel(const uint16_t* __restric
     uint32_t h[8], xh[8];
     unpack8(v, h);
     Q4kChunk q;
-    q4k_chunk(h, q, xh);
+    if (MSE) q4k_mse_chunk(h, q, xh);
+    else q4k_chunk(h, q, xh);
     q4k_store(q, L, ok && packed, packed ? packed + (r * (K / 256) + sb) * 144 : nullptr);
     if (ok && xhat) *reinterpret_cast<uint4*>(xhat + r * K + c * 8) = pack8(xh);
   }
@@ -328,7 +329,15 @@ hipError_t launch_mxfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, ui
 hipError_t launch_q4k(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, uint8_t* packed,
                       uint16_t* xhat, hipStream_t s) {
   if (R == 0 || K == 0) return hipSuccess;
-  hipLaunchKernelGGL(q4k_kernel<2>, row_grid(R, K, 2), dim3(kThreads), 0, s, x, R, K, ldx,
+  hipLaunchKernelGGL((q4k_kernel<2, false>), row_grid(R, K, 2), dim3(kThreads), 0, s, x, R, K,
+                     ldx, packed, xhat);
+  return hipGetLastError();
+}
+
+hipError_t launch_q4k_mse(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, uint8_t* packed,
+                          uint16_t* xhat, hipStream_t s) {
+  if (R == 0 || K == 0) return hipSuccess;
+  hipLaunchKernelGGL((q4k_kernel<1, true>), row_grid(R, K, 1), dim3(kThreads), 0, s, x, R, K, ldx,
                      packed, xhat);
   return hipGetLastError();
 }

@@ -183,6 +183,47 @@ def test_q4k_full_size_export_weight(qf):
     assert_same(run_q4k(qf, w["W"]), oracle.q4k(w["W"]), ("packed", "xhat"), "q4k 14336x4096")
 
 
+# -------------------------------------------------------------- Q4_K with an MSE search
+def run_q4k_mse(qf, x, ld=None):
+    R, K = x.shape
+    xd = to_dev(x) if ld is None else to_dev(_strided(x, ld))[:, :K]
+    packed = torch.empty(R, K // 256, 144, dtype=torch.uint8, device="cuda")
+    xhat = empty_bf16((R, K))
+    qf.fakequant_q4k_mse(xd, packed, xhat)
+    torch.cuda.synchronize()
+    return {"packed": from_dev(packed), "xhat": from_dev(xhat)}
+
+
+def test_q4k_mse_bit_exact(qf):
+    rng = np.random.default_rng(15)
+    cases = [
+        ("normal", workloads.normal_bf16(rng, (37, 512), 0.02), None),
+        ("heavy", workloads.to_bf16((rng.standard_t(3, size=(16, 1024)) * 0.02).astype(np.float32)), 1096),
+        ("wide", wide_range_bf16(rng, (9, 768), lo_exp=-20, hi_exp=10, zero_frac=0.05), None),
+        ("ints", workloads.to_bf16(rng.integers(-8, 9, size=(8, 256)).astype(np.float32)), None),
+    ]
+    x = cases[2][1]
+    x[0, :32] = 0                                      # all-zero sub-block
+    x[-1, 32:64] = 0x8000                              # all -0 sub-block
+    x[-1, 64:96] = 0x3F80                              # constant sub-block
+    for name, x, ld in cases:
+        assert_same(run_q4k_mse(qf, x, ld), oracle.q4k_mse(x), ("packed", "xhat"), f"q4k-mse {name}")
+
+
+def test_q4k_mse_exhaustive_bf16_inputs_below_limits(qf):
+    v = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    mag = np.abs((v.astype(np.uint32) << 16).view(np.float32))
+    sel = np.random.default_rng(9).permutation(v[mag < 2.0 ** 14])
+    x = sel[: len(sel) // 256 * 256].reshape(-1, 256)
+    assert_same(run_q4k_mse(qf, x), oracle.q4k_mse(x), ("packed", "xhat"), "q4k-mse exhaustive")
+
+
+def test_q4k_mse_export_weight_rows(qf):
+    w = workloads.q4k_weight(seed=0, n_scale=8)      # 1792 x 4096 rows of the export weight
+    assert_same(run_q4k_mse(qf, w["W"]), oracle.q4k_mse(w["W"]), ("packed", "xhat"),
+                "q4k-mse 1792x4096")
+
+
 # ------------------------------------------------------------------------------- amax
 def test_amax_and_running_accumulate(qf):
     rng = np.random.default_rng(6)
