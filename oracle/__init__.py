@@ -414,3 +414,56 @@ def q4k_mse_subblock(x32) -> tuple:
     q = (ctypes.c_int * 32)()
     lib().or_q4k_mse_subblock(_ptr(xv, _f32p), _ptr(a, _f32p), _ptr(mu, _f32p), q)
     return float(a[0]), float(mu[0]), np.array(list(q))
+
+
+# ------------------------------------------------------------ engine-native export (NVFP4/MXFP4)
+def export_fused(members, fmt: str, a_amax: float | None = None) -> dict:
+    """Export of a fused projection (Sec. 3.2.3 "Engine-specific scale sharing", Sec. 3.5):
+    the engine's fused weight is the row concatenation of the member weights (QKV, gate/up);
+    NVFP4 uses one tensor scale for it, from the amax over all members, and exports the
+    input-activation scale from the running activation amax (Sec. 3.2.3 NVFP4 paragraph:
+    S_act = amax / (6 * 448), the decode scale the engine applies).  MXFP4 has block scales
+    only.  Returns codes [N, K/2], scales, and for NVFP4 weight_scale_2 (S) and input_scale."""
+    W = np.concatenate([np.ascontiguousarray(m) for m in members], axis=0)
+    if fmt == "nvfp4":
+        q = nvfp4(W)
+        out = {"codes": q["codes"], "scales": q["scales"], "weight_scale_2": q["S"],
+               "amax": amax(W)}
+        out["input_scale"] = (float(np.float32(np.float32(a_amax) / np.float32(2688.0)))
+                              if a_amax is not None else None)
+        return out
+    if fmt == "mxfp4":
+        q = mxfp4(W)
+        return {"codes": q["codes"], "scales": q["scales"]}
+    raise ValueError(fmt)
+
+
+PAYLOAD_MAGIC = 0x31504651          # bytes "QFP1"
+
+
+def payload_layout(fmt: str, N: int, K: int) -> dict:
+    """Weight-sync payload of one layer (this library's format): a 64-byte header, then the
+    codes, the block scales and two FP32 scalars (weight_scale_2, input_scale; zeros for
+    MXFP4), each section starting at a multiple of 256 bytes."""
+    blk = {"nvfp4": 16, "mxfp4": 32}[fmt]
+    up = lambda v: (v + 255) // 256 * 256
+    off_codes = 256
+    off_scales = off_codes + up(N * K // 2)
+    off_scalars = off_scales + up(N * K // blk)
+    return {"codes": off_codes, "scales": off_scales, "scalars": off_scalars,
+            "total": off_scalars + 256, "blk": blk}
+
+
+def parse_payload(buf: np.ndarray) -> dict:
+    """Reads a payload back (header fields little-endian: u32 magic, u32 format, i64 N, i64 K,
+    u64 codes / scales / scalars offsets, u64 total size)."""
+    b = np.ascontiguousarray(buf, np.uint8)
+    magic, fmt = (int(v) for v in b[0:8].view("<u4"))
+    N, K = (int(v) for v in b[8:24].view("<i8"))
+    oc, osc, osr, total = (int(v) for v in b[24:56].view("<u8"))
+    name = {1: "nvfp4", 2: "mxfp4"}[int(fmt)]
+    blk = 16 if name == "nvfp4" else 32
+    return {"magic": int(magic), "fmt": name, "N": int(N), "K": int(K), "total": int(total),
+            "codes": b[oc:oc + N * K // 2].reshape(N, K // 2),
+            "scales": b[osc:osc + N * K // blk].reshape(N, K // blk),
+            "scalars": b[osr:osr + 8].view("<f4")}
