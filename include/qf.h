@@ -407,6 +407,54 @@ QF_API qf_status qf_qad_kl(const uint16_t* zt, int64_t ldt, const uint16_t* zs, 
                            int64_t L, int64_t V, float grad_scale, float* row_kl, float* loss,
                            uint16_t* grad, int64_t ldg, int32_t* agree, qf_stream_t stream);
 
+/* ---------------------------------------------------------------------------------------
+ * Engine-native export and weight sync (Sec. 3.5; Sec. 3.2.3 "Engine-specific scale sharing";
+ * Sec. 3.4 "Low-precision weight synchronization")
+ * ------------------------------------------------------------------------------------ */
+typedef struct {
+    const uint16_t* W;    /* bf16 [rows, K], row stride ldw (device) */
+    int64_t rows;
+    int64_t ldw;
+} qf_member;
+
+/*
+ * qf_export_fused -- export of a fused projection (attention QKV, MLP gate/up): the engine's
+ * fused weight is the row concatenation of the n member weights (1 <= n <= 8, common K).
+ *   fmt        QF_FMT_NVFP4 or QF_FMT_MXFP4.
+ *   codes      [N, K/2] (N = sum of rows; element 2i in the low nibble), required.
+ *   scales     [N, K/16] E4M3 (NVFP4) or [N, K/32] E8M0 (MXFP4), required.
+ *   NVFP4 only:
+ *   w_amax     device FP32 scalar, required: receives the tied amax g over all members.
+ *   weight_scale_2  device FP32 scalar or NULL: the tied tensor decode scale g / 2688 (one
+ *              for the fused matrix, as the engine uses it).
+ *   a_amax, input_scale  device FP32 scalars or NULL: input_scale = a_amax / 2688, the
+ *              static activation scale exported from the running activation amax (NVFP4
+ *              paragraph) -- the decode scale the activation quantizer uses for that amax.
+ * The codes and block scales equal those of qf_fakequant_nvfp4 / _mxfp4 on the concatenated
+ * weight, bit for bit.  Any output may point into a weight-sync payload (below).
+ */
+QF_API qf_status qf_export_fused(int fmt, const qf_member* members, int n, int64_t K,
+                                 uint8_t* codes, uint8_t* scales, float* w_amax,
+                                 float* weight_scale_2, const float* a_amax, float* input_scale,
+                                 qf_stream_t stream);
+
+/*
+ * Weight-sync payload of one layer (this library's format; the transport is the caller's):
+ * one contiguous byte buffer with a 64-byte header, then the codes, the block scales and two
+ * FP32 scalars {weight_scale_2, input_scale} (zeros for MXFP4), each section at a multiple of
+ * 256 bytes.  Header (little-endian): u32 magic 0x31504651 ("QFP1"), u32 format, i64 N,
+ * i64 K, u64 offsets of codes, scales and scalars, u64 total bytes, 8 bytes zero.
+ * qf_payload_layout_of (host only) returns the offsets and size; qf_export_fused (or the
+ * quantizers) write the sections in place; qf_payload_write_header writes the header and
+ * leaves the sections untouched.
+ */
+typedef struct {
+    uint64_t codes, scales, scalars, total;
+} qf_payload_layout;
+QF_API qf_status qf_payload_layout_of(int fmt, int64_t N, int64_t K, qf_payload_layout* out);
+QF_API qf_status qf_payload_write_header(int fmt, int64_t N, int64_t K, void* payload,
+                                         qf_stream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

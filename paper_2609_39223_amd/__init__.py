@@ -44,6 +44,15 @@ class LoRA(ctypes.Structure):
                 ("b_shared", ctypes.c_int32)]
 
 
+class Member(ctypes.Structure):
+    _fields_ = [("W", ctypes.c_void_p), ("rows", ctypes.c_int64), ("ldw", ctypes.c_int64)]
+
+
+class PayloadLayout(ctypes.Structure):
+    _fields_ = [("codes", ctypes.c_uint64), ("scales", ctypes.c_uint64),
+                ("scalars", ctypes.c_uint64), ("total", ctypes.c_uint64)]
+
+
 class GroupedDesc(ctypes.Structure):
     _fields_ = [("E", ctypes.c_int64), ("T", ctypes.c_int64), ("N", ctypes.c_int64),
                 ("K", ctypes.c_int64), ("wfmt", ctypes.c_int32), ("afmt", ctypes.c_int32),
@@ -108,6 +117,11 @@ def lib() -> ctypes.CDLL:
                                         ctypes.c_int),
             "qf_qad_kl": ([_P, _I, _P, _I, _I, _I, ctypes.c_float, _P, _P, _P, _I, _P, _P],
                           ctypes.c_int),
+            "qf_export_fused": ([ctypes.c_int, ctypes.POINTER(Member), ctypes.c_int, _I, _P, _P,
+                                 _P, _P, _P, _P, _P], ctypes.c_int),
+            "qf_payload_layout_of": ([ctypes.c_int, _I, _I, ctypes.POINTER(PayloadLayout)],
+                                     ctypes.c_int),
+            "qf_payload_write_header": ([ctypes.c_int, _I, _I, _P, _P], ctypes.c_int),
             "qf_grouped_lora_workspace_size": ([ctypes.POINTER(GroupedDesc), ctypes.POINTER(LoRA),
                                                 ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
             "qf_qlinear_grouped_lora_fwd": ([ctypes.POINTER(GroupedDesc), ctypes.POINTER(LoRA), _P,
@@ -372,3 +386,29 @@ def qad_kl(zt, zs, row_kl, loss=None, grad=None, agree=None, grad_scale=None):
     gs = (1.0 / L if L else 1.0) if grad_scale is None else float(grad_scale)
     _check(lib().qf_qad_kl(_ptr(zt), ldt, _ptr(zs), lds, L, V, gs, _ptr(row_kl), _ptr(loss),
                            _ptr(grad), ldg, _ptr(agree), _stream()))
+
+
+# --------------------------------------------------------------- engine-native export / sync
+def export_fused(members, fmt, codes, scales, w_amax=None, weight_scale_2=None, a_amax=None,
+                 input_scale=None):
+    """Fused-projection export: members are bf16 [rows_i, K] tensors (row-contiguous)."""
+    K = members[0].shape[1]
+    arr = (Member * len(members))()
+    for i, m in enumerate(members):
+        R, Km, ld = _rows(_bf16(m))
+        if Km != K:
+            raise ValueError("members must share K")
+        arr[i] = Member(_ptr(m), R, ld)
+    _check(lib().qf_export_fused(FMT[fmt], arr, len(members), K, _ptr(codes), _ptr(scales),
+                                 _ptr(w_amax), _ptr(weight_scale_2), _ptr(a_amax),
+                                 _ptr(input_scale), _stream()))
+
+
+def payload_layout(fmt, N, K) -> PayloadLayout:
+    L = PayloadLayout()
+    _check(lib().qf_payload_layout_of(FMT[fmt], N, K, ctypes.byref(L)))
+    return L
+
+
+def payload_write_header(fmt, N, K, payload):
+    _check(lib().qf_payload_write_header(FMT[fmt], N, K, _ptr(payload), _stream()))

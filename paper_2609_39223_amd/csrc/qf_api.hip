@@ -1095,4 +1095,99 @@ qf_status qf_qad_kl(const uint16_t* zt, int64_t ldt, const uint16_t* zs, int64_t
   return ok();
 }
 
+// --------------------------------------------------------------- engine-native export / sync
+namespace {
+
+constexpr uint32_t kPayloadMagic = 0x31504651u;   // "QFP1"
+
+qf_status payload_layout(int fmt, int64_t N, int64_t K, qf_payload_layout* L) {
+  if (fmt != QF_FMT_NVFP4 && fmt != QF_FMT_MXFP4)
+    return fail(QF_EINVAL, "payload: format must be NVFP4 or MXFP4");
+  if (N < 0 || K < 0) return fail(QF_ESHAPE, "payload: negative shape");
+  const int64_t blk = block_of(fmt);
+  if (K % blk) return fail(QF_ESHAPE, "payload: K=%lld is not a multiple of %lld", (long long)K,
+                           (long long)blk);
+  L->codes = 256;
+  L->scales = L->codes + up((size_t)N * K / 2);
+  L->scalars = L->scales + up((size_t)N * K / blk);
+  L->total = L->scalars + 256;
+  return QF_OK;
+}
+
+}  // namespace
+
+qf_status qf_payload_layout_of(int fmt, int64_t N, int64_t K, qf_payload_layout* out) {
+  if (!out) return fail(QF_EINVAL, "qf_payload_layout_of: null output");
+  QF_TRY(payload_layout(fmt, N, K, out));
+  return ok();
+}
+
+qf_status qf_payload_write_header(int fmt, int64_t N, int64_t K, void* payload,
+                                  qf_stream_t stream) {
+  qf_payload_layout L;
+  QF_TRY(payload_layout(fmt, N, K, &L));
+  if (!payload) return fail(QF_EINVAL, "qf_payload_write_header: null payload");
+  if ((uintptr_t)payload % kAlign)
+    return fail(QF_EALIGN, "qf_payload_write_header: payload not 256-byte aligned");
+  const uint64_t q[7] = {(uint64_t)N, (uint64_t)K, L.codes, L.scales, L.scalars, L.total, 0};
+  uint32_t w[16];
+  w[0] = kPayloadMagic;
+  w[1] = (uint32_t)fmt;
+  for (int i = 0; i < 7; ++i) {
+    w[2 + 2 * i] = (uint32_t)(q[i] & 0xFFFFFFFFu);
+    w[3 + 2 * i] = (uint32_t)(q[i] >> 32);
+  }
+  QF_TRY(dev(qf::launch_payload_header(payload, w, S(stream)), "payload header"));
+  return ok();
+}
+
+qf_status qf_export_fused(int fmt, const qf_member* members, int n, int64_t K, uint8_t* codes,
+                          uint8_t* scales, float* w_amax, float* weight_scale_2,
+                          const float* a_amax, float* input_scale, qf_stream_t stream) {
+  const char* fn = "qf_export_fused";
+  if (fmt != QF_FMT_NVFP4 && fmt != QF_FMT_MXFP4)
+    return fail(QF_EINVAL, "%s: format must be NVFP4 or MXFP4", fn);
+  if (!members || n < 1 || n > 8) return fail(QF_EINVAL, "%s: 1 to 8 members", fn);
+  const int64_t blk = block_of(fmt);
+  int64_t N = 0;
+  for (int i = 0; i < n; ++i) {
+    QF_TRY(check_quant_input(fn, members[i].W, members[i].rows, K, members[i].ldw, blk));
+    N += members[i].rows;
+  }
+  if (!codes || !scales) return fail(QF_EINVAL, "%s: codes and scales are required", fn);
+  QF_TRY(check_out("qf_export_fused: codes", codes));
+  hipStream_t s = S(stream);
+  if (fmt == QF_FMT_NVFP4) {
+    if (!w_amax) return fail(QF_EINVAL, "%s: NVFP4 needs w_amax", fn);
+    if (input_scale && !a_amax) return fail(QF_EINVAL, "%s: input_scale needs a_amax", fn);
+    QF_TRY(dev(qf::launch_fill_f32(w_amax, 1, 0.0f, s), "amax init"));
+    for (int i = 0; i < n; ++i)
+      QF_TRY(dev(qf::launch_amax(members[i].W, members[i].rows, K, members[i].ldw, w_amax, s),
+                 "tied amax"));
+    int64_t r0 = 0;
+    for (int i = 0; i < n; ++i) {
+      QF_TRY(dev(qf::launch_nvfp4(members[i].W, members[i].rows, K, members[i].ldw, w_amax,
+                                  nullptr, codes + r0 * (K / 2), scales + r0 * (K / 16), nullptr,
+                                  s),
+                 "nvfp4 member"));
+      r0 += members[i].rows;
+    }
+    if (weight_scale_2 || input_scale)
+      QF_TRY(dev(qf::launch_export_scalars(w_amax, a_amax, weight_scale_2, input_scale, s),
+                 "export scalars"));
+  } else {
+    if (w_amax || weight_scale_2 || input_scale)
+      return fail(QF_EINVAL, "%s: MXFP4 has no tensor-level scales", fn);
+    int64_t r0 = 0;
+    for (int i = 0; i < n; ++i) {
+      QF_TRY(dev(qf::launch_mxfp4(members[i].W, members[i].rows, K, members[i].ldw,
+                                  codes + r0 * (K / 2), scales + r0 * (K / 32), nullptr, s),
+                 "mxfp4 member"));
+      r0 += members[i].rows;
+    }
+  }
+  (void)N;
+  return ok();
+}
+
 }  // extern "C"

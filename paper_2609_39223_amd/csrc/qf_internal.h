@@ -137,4 +137,11 @@ hipError_t launch_transpose_f32(const float* F, int64_t N, int64_t r, int64_t ba
 hipError_t launch_qad_kl(const uint16_t* zt, int64_t ldt, const uint16_t* zs, int64_t lds_,
                          int64_t L, int64_t V, float gscale, float* row_kl, float* loss,
                          uint16_t* grad, int64_t ldg, int32_t* agree, hipStream_t s);
+
+// ---- export helpers (qf_export.hip) --------------------------------------------------------
+// ws2 = *g / 2688 and is = *a / 2688 (either output may be null; a is read only when is is set).
+hipError_t launch_export_scalars(const float* g, const float* a, float* ws2, float* is,
+                                 hipStream_t s);
+// Writes the 64-byte payload header (16 little-endian 32-bit words) to payload.
+hipError_t launch_payload_header(void* payload, const uint32_t words[16], hipStream_t s);
 }  // namespace qf

@@ -157,3 +157,28 @@ def test_lora_validation(L):
     assert L.qf_qlinear_lora_fwd(ctypes.byref(d), ctypes.byref(lo), P(256), P(256), P(256),
                                  P(256), ctypes.c_size_t(16), None) == QF_EINVAL
     assert b"workspace" in L.qf_last_error()
+
+
+class Member(ctypes.Structure):
+    _fields_ = [("W", ctypes.c_void_p), ("rows", ctypes.c_int64), ("ldw", ctypes.c_int64)]
+
+
+def test_export_validation(L):
+    m = (Member * 9)(*[Member(256, 8, 64) for _ in range(9)])
+    f = L.qf_export_fused
+    args = lambda fmt, n, w_amax=None, ws2=None, K=64: f(fmt, m, n, I64(K), P(256), P(512), w_amax,
+                                                         ws2, None, None, None)
+    assert args(2, 0) == QF_EINVAL                         # no members
+    assert args(2, 9) == QF_EINVAL                         # more than 8
+    assert args(3, 2) == QF_EINVAL                         # Q4_K is not an FP4 export format
+    assert args(2, 2, w_amax=P(1024)) == QF_EINVAL         # MXFP4 has no tensor scale
+    assert args(1, 2) == QF_EINVAL                         # NVFP4 needs w_amax
+    assert args(2, 2, K=48) == QF_ESHAPE                   # K % 32
+    class Lay(ctypes.Structure):
+        _fields_ = [("codes", ctypes.c_uint64), ("scales", ctypes.c_uint64),
+                    ("scalars", ctypes.c_uint64), ("total", ctypes.c_uint64)]
+    lay = Lay()
+    assert L.qf_payload_layout_of(1, I64(160), I64(512), ctypes.byref(lay)) == QF_OK
+    assert (lay.codes, lay.scales, lay.scalars) == (256, 256 + 40960, 256 + 40960 + 5120)
+    assert L.qf_payload_layout_of(3, I64(160), I64(512), ctypes.byref(lay)) == QF_EINVAL
+    assert L.qf_payload_write_header(1, I64(160), I64(512), P(128), None) == QF_EALIGN
