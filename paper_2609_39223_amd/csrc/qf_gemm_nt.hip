@@ -54,9 +54,6 @@ constexpr int kOpStage = BM * kRow;              // 32 KB: one operand, one stag
 constexpr int kStage = 2 * kOpStage;             // 64 KB: A then B
 constexpr int kGroupM = 8;
 constexpr int kXcds = 8;
-constexpr int kWaves = 8;
-constexpr int NJ = 2;                            // 32-column accumulator blocks per wavefront
-constexpr int NLD = 8;                           // direct-to-LDS loads per wavefront per stage
 constexpr int64_t kMaxSplitTiles = 128;          // split tiles of the last round, at most
 constexpr int kPitch16 = BN * 2 + 16;            // epilogue LDS row pitch, bf16 tile (528 B)
 constexpr int kPitch32 = BN * 4 + 32;            // epilogue LDS row pitch, FP32 half tile
@@ -136,13 +133,24 @@ __device__ __forceinline__ int remap_xcd(int bid, int nb) {
   return (bid % kXcds) * (full / kXcds) + bid / kXcds;
 }
 
-template <bool C_F32, int MODE, bool A_MN, bool B_MN>
-__global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
+// WAVES = 8: each wavefront owns a 128 x 64 sub-tile (4 x 2 accumulator blocks) and loads
+// one operand (8 loads per stage); operands stored [K][rows] (A_MN / B_MN) need this form.
+// WAVES = 4: each wavefront owns a 128 x 128 sub-tile (4 x 4 blocks, 256 accumulators in
+// AGPRs) and loads 64 rows of both operands (16 loads per stage); one wavefront per SIMD and a
+// third less LDS fragment traffic per MFMA (0.5 KB instead of 0.75 KB).  Both visit every
+// output element's k slices in the same order, so their results are bit-identical.
+template <bool C_F32, int MODE, bool A_MN, bool B_MN, int WAVES>
+__global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
+  static_assert(WAVES == 8 || (!A_MN && !B_MN), "operands stored [K][rows] need 8 wavefronts");
+  constexpr int NJ = WAVES == 8 ? 2 : 4;         // 32-column accumulator blocks per wavefront
+  constexpr int NLD = WAVES == 8 ? 8 : 16;       // direct-to-LDS loads per wavefront per stage
+  // stage s+1's loads: L0 in the last slice of step s-1, L1 in slice 0 and L2 in slice 1
+  constexpr int L0 = WAVES == 8 ? 3 : 6, L1 = WAVES == 8 ? 3 : 5, L2 = NLD - L0 - L1;
   __shared__ __attribute__((aligned(16))) char smem[kSmem];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (scalar) index
-  const int wm = w >> 2, wn = w & 3;
+  const int wm = WAVES == 8 ? w >> 2 : w >> 1, wn = WAVES == 8 ? w & 3 : w & 1;
   const int item = remap_xcd(blockIdx.x, gridDim.x);
   int bid = item, half = -1, pidx = 0;
   if (MODE == kDense && C_F32 && p.part != nullptr) {
@@ -195,47 +203,58 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
   const int64_t n_end = p.N, K = p.K;
 
   // ---- this lane's loads ----------------------------------------------------------------------
-  // Wavefront w loads operand w >> 2 (8 loads of 1 KB per stage, LDS offsets lbase + 1 KB q).
+  // WAVES = 8: wavefront w loads operand w >> 2, rows (or k-rows) of quarter w & 3, 8 loads of
+  // 1 KB per stage.  WAVES = 4: wavefront w loads quarter w of both operands, loads 0-7 for A
+  // and 8-15 for B.  Load q of quarter lw at LDS offset op * 32 KB + 8 KB lw + 1 KB (q % 8).
   // k-major operand ([rows][K], a stage is 256 rows x 128 B): load q covers tile rows
-  // R = 64 (w & 3) + 8 q .. R + 7, lane l lands at row R + l / 8, slot l % 8 and so fetches
+  // R = 64 lw + 8 (q % 8) .. R + 7, lane l lands at row R + l / 8, slot l % 8 and so fetches
   // logical chunk (l % 8) ^ ((row >> 1) % 8) = (l % 8) ^ ((4 (q % 2) + l / 16) % 8).
   // mn-major operand ([K][rows], a stage is 64 k-rows x 512 B): load q covers k-rows
-  // 16 (w & 3) + 2 q + {0, 1}; lane l lands at k-row 16 (w & 3) + 2 q + l / 32, 16-byte slot
-  // l % 32, and fetches logical chunk (l % 32) ^ (4 (k-row % 4)) (chunk c = columns 8c..8c+7).
-  const int op = w >> 2, lw = w & 3;
-  const bool mn = op ? B_MN : A_MN;              // wave-uniform
-  const int64_t ld = op ? p.ldb : p.lda;
-  const int64_t r0 = op ? n0 : m0;
-  const int64_t rlim = (op ? n_end : m_end) - r0 - 1;   // last valid tile row (k-major) / column
-  const char* gbase;
-  __amdgpu_buffer_rsrc_t rsrc;
-  int64_t sstride;                               // bytes from one stage to the next
+  // 16 lw + 2 q + {0, 1}; lane l lands at k-row 16 lw + 2 q + l / 32, 16-byte slot l % 32,
+  // and fetches logical chunk (l % 32) ^ (4 (k-row % 4)) (chunk c = columns 8c..8c+7).
+  const int lw = WAVES == 8 ? w & 3 : w;
+  const int wop = WAVES == 8 ? w >> 2 : 0;       // WAVES = 8: this wavefront's operand
+  auto op_of = [&](int q) { return WAVES == 8 ? wop : q >> 3; };
+  const char* gb[2];
+  __amdgpu_buffer_rsrc_t rs[2];
+  int64_t sstride = kRow;                        // bytes from one stage to the next
   uint32_t goff[NLD];
-  if (!mn) {
-    gbase = reinterpret_cast<const char*>((op ? Bp : p.A) + r0 * ld);
-    rsrc = make_rsrc(gbase, (rlim * ld + K) * 2);
-    sstride = kRow;
+  bool mn = false;
 #pragma unroll
-    for (int q = 0; q < NLD; ++q) {
-      const int64_t row = lw * 64 + q * 8 + (lane >> 3);
-      const int64_t rc = row < rlim ? row : rlim;
-      const int c = (lane & 7) ^ ((4 * (q & 1) + (lane >> 4)) & 7);
-      goff[q] = (uint32_t)((rc * ld + c * 8) * 2);
-    }
-  } else {
-    gbase = reinterpret_cast<const char*>((op ? Bp : p.A) + r0);
-    rsrc = make_rsrc(gbase, ((K - 1) * ld + rlim + 1) * 2);
-    sstride = (int64_t)BK * ld * 2;
-    const int clim = (int)(rlim / 8);            // last chunk holding valid columns
+  for (int op = 0; op < 2; ++op) {
+    if (WAVES == 8 && op != wop) continue;       // uniform
+    const bool omn = op ? B_MN : A_MN;
+    const int64_t ld = op ? p.ldb : p.lda;
+    const int64_t r0 = op ? n0 : m0;
+    const int64_t rlim = (op ? n_end : m_end) - r0 - 1;   // last valid row (k-major) / column
+    if (!omn) {
+      gb[op] = reinterpret_cast<const char*>((op ? Bp : p.A) + r0 * ld);
+      rs[op] = make_rsrc(gb[op], (rlim * ld + K) * 2);
 #pragma unroll
-    for (int q = 0; q < NLD; ++q) {
-      const int kr = lw * 16 + q * 2 + (lane >> 5);
-      int c = (lane & 31) ^ (4 * (kr & 3));
-      c = c < clim ? c : clim;
-      goff[q] = (uint32_t)(((int64_t)kr * ld + c * 8) * 2);
+      for (int q = 0; q < NLD; ++q) {
+        if (WAVES == 4 && (q >> 3) != op) continue;
+        const int qq = q & 7;
+        const int64_t row = lw * 64 + qq * 8 + (lane >> 3);
+        const int64_t rc = row < rlim ? row : rlim;
+        const int c = (lane & 7) ^ ((4 * (qq & 1) + (lane >> 4)) & 7);
+        goff[q] = (uint32_t)((rc * ld + c * 8) * 2);
+      }
+    } else {
+      mn = true;
+      gb[op] = reinterpret_cast<const char*>((op ? Bp : p.A) + r0);
+      rs[op] = make_rsrc(gb[op], ((K - 1) * ld + rlim + 1) * 2);
+      sstride = (int64_t)BK * ld * 2;
+      const int clim = (int)(rlim / 8);          // last chunk holding valid columns
+#pragma unroll
+      for (int q = 0; q < NLD; ++q) {
+        const int kr = lw * 16 + q * 2 + (lane >> 5);
+        int c = (lane & 31) ^ (4 * (kr & 3));
+        c = c < clim ? c : clim;
+        goff[q] = (uint32_t)(((int64_t)kr * ld + c * 8) * 2);
+      }
     }
   }
-  const int lbase = op * kOpStage + lw * 8192;   // load q adds 1 KB q
+  auto lds_of = [&](int q) { return op_of(q) * kOpStage + lw * 8192 + (q & 7) * 1024; };
 
   // ---- fragment offsets ----------------------------------------------------------------------
   // k-major: slice kk, fragment i at fo[kk] + i * 4096 (32 rows of 128 bytes); fragment rows
@@ -248,7 +267,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
   // is fo[f], plus (16 kk + 4 h) * 512 bytes for slice kk, half h.
   int foa[4], fob[4];
   {
-    const int ra = wm * 128 + (lane & 31), rb = wn * 64 + (lane & 31);
+    const int ra = wm * 128 + (lane & 31), rb = wn * (NJ * 32) + (lane & 31);
     const int sw = (lane >> 1) & 7;
     const int g = lane >> 4, j = (lane >> 2) & 3, a = lane & 3;
 #pragma unroll
@@ -258,7 +277,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
       const int rowj = 8 * (g >> 1) + j;
       if (A_MN) foa[x] = rowj * 512 + ((4 * ((wm * 4 + x) ^ j) + 2 * (g & 1) + (a >> 1)) << 4) + 8 * (a & 1);
       else foa[x] = ra * kRow + ((c ^ sw) << 4);
-      if (B_MN) fob[x] = kOpStage + rowj * 512 + ((4 * ((wn * 2 + x) ^ j) + 2 * (g & 1) + (a >> 1)) << 4) + 8 * (a & 1);
+      if (B_MN) fob[x] = kOpStage + rowj * 512 + ((4 * ((wn * NJ + x) ^ j) + 2 * (g & 1) + (a >> 1)) << 4) + 8 * (a & 1);
       else fob[x] = kOpStage + rb * kRow + ((c ^ sw) << 4);
     }
   }
@@ -283,9 +302,10 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
   auto dma = [&](int64_t s, int buf, int q) {
     int64_t se = s + krot;
     if (se >= ks1) se -= klen;
-    char* l = smem + buf * kStage + lbase + q * 1024;
-    if (QF_NT_GLOBAL_LDS) dma16_global(gbase + se * sstride + goff[q], l);
-    else dma16_buf(rsrc, goff[q], (uint32_t)(se * sstride), l);
+    char* l = smem + buf * kStage + lds_of(q);
+    const int op = op_of(q);
+    if (QF_NT_GLOBAL_LDS) dma16_global(gb[op] + se * sstride + goff[q], l);
+    else dma16_buf(rs[op], goff[q], (uint32_t)(se * sstride), l);
   };
   // Fragment read r of a slice, in the order the slice's MFMAs consume them: A0, B0, B1, A1..A3.
   auto frag = [&](const char* st, int kk, int f, bool is_b) -> bf16x8_t {
@@ -330,9 +350,9 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
       __builtin_amdgcn_sched_barrier(0);
     }
   };
-  // Loads are spread over the step: stage s+1's eight loads per wavefront go out 3 in the
-  // last slice of step s-1 (right after its barrier freed stage s-1's buffer), 3 in slice 0
-  // and 2 in slice 1 of step s; the barrier before slice 3 waits for them.
+  // Loads are spread over the step: stage s+1's loads go out L0 in the last slice of step s-1
+  // (right after its barrier freed stage s-1's buffer), L1 in slice 0 and L2 in slice 1 of
+  // step s; the barrier before slice 3 waits for them.
   auto step = [&](int64_t s, int64_t s_end, auto last) {
     constexpr bool LAST = decltype(last)::value;
     const int cur = (int)((s - ks0) & 1), nxt = cur ^ 1;
@@ -341,14 +361,15 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
     // not read again, and the epilogue's barrier drains them.
     const int64_t n1 = s + 1 < s_end ? s + 1 : s_end - 1;
     const int64_t n2 = s + 2 < s_end ? s + 2 : s_end - 1;
-    slice(std::true_type{}, std::true_type{}, fa[0], fb[0], cs, 1, fa[1], fb[1], n1, nxt, 3, 3);
-    slice(std::true_type{}, std::true_type{}, fa[1], fb[1], cs, 2, fa[0], fb[0], n1, nxt, 6, 2);
+    slice(std::true_type{}, std::true_type{}, fa[0], fb[0], cs, 1, fa[1], fb[1], n1, nxt, L0, L1);
+    slice(std::true_type{}, std::true_type{}, fa[1], fb[1], cs, 2, fa[0], fb[0], n1, nxt, L0 + L1,
+          L2);
     slice(std::true_type{}, std::false_type{}, fa[0], fb[0], cs, 3, fa[1], fb[1], 0, 0);
     __builtin_amdgcn_s_waitcnt(0);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     slice(std::integral_constant<bool, !LAST>{}, std::true_type{}, fa[1], fb[1],
-          smem + nxt * kStage, 0, fa[0], fb[0], n2, cur, 0, 3);
+          smem + nxt * kStage, 0, fa[0], fb[0], n2, cur, 0, L0);
   };
 
   const int64_t nfull = K / BK;                 // the K tail (dense, second half) follows it
@@ -359,13 +380,23 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
     for (int q = 0; q < NLD; ++q) dma(s0, 0, q);
     if (s0 + 1 < s1) {
 #pragma unroll
-      for (int q = 0; q < 3; ++q) dma(s0 + 1, 1, q);
+      for (int q = 0; q < L0; ++q) dma(s0 + 1, 1, q);
     }
     __builtin_amdgcn_s_waitcnt(0);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     read_all(smem, 0, fa[0], fb[0]);
-    for (int64_t s = s0; s < s1 - 1; ++s) step(s, s1, std::false_type{});
+    int64_t s = s0;
+    if (WAVES == 4) {
+      // two steps per iteration: with one loop-carried copy of the 256 accumulators the
+      // register allocator keeps them in place (a one-step loop body rotates them through
+      // other AGPRs at every back edge)
+      for (; s + 2 < s1; s += 2) {
+        step(s, s1, std::false_type{});
+        step(s + 1, s1, std::false_type{});
+      }
+    }
+    for (; s < s1 - 1; ++s) step(s, s1, std::false_type{});
     step(s1 - 1, s1, std::true_type{});
   }
   if (krem > 0) {
@@ -384,8 +415,8 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
         valid = nfull * BK + lw * 16 + q * 2 + (lane >> 5) < K;
       }
       uint4 v = make_uint4(0, 0, 0, 0);
-      if (valid) v = *reinterpret_cast<const uint4*>(gbase + nfull * sstride + goff[q]);
-      *reinterpret_cast<uint4*>(smem + lbase + q * 1024 + lane * 16) = v;
+      if (valid) v = *reinterpret_cast<const uint4*>(gb[op_of(q)] + nfull * sstride + goff[q]);
+      *reinterpret_cast<uint4*>(smem + lds_of(q) + lane * 16) = v;
     }
     __syncthreads();
 #pragma unroll
@@ -414,7 +445,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
     ldc = BN; em0 = 0; em_end = BM; en0 = 0; en_end = BN; vec = 1;
   }
   if (!C_F32) {
-    char* wbase = smem + (wm * 128 + 4 * (lane >> 5)) * kPitch16 + (wn * 64 + (lane & 31)) * 2;
+    char* wbase = smem + (wm * 128 + 4 * (lane >> 5)) * kPitch16 + (wn * NJ * 32 + (lane & 31)) * 2;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -426,9 +457,10 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
     __syncthreads();
     const int c8 = (tid & 31) * 8;
     const int64_t gcol = en0 + c8;
+    constexpr int kRowsPerPass = WAVES * 64 / 32;  // 32 lanes cover a row
 #pragma unroll 4
-    for (int it = 0; it < BM / 16; ++it) {
-      const int r = it * 16 + (tid >> 5);
+    for (int it = 0; it < BM / kRowsPerPass; ++it) {
+      const int r = it * kRowsPerPass + (tid >> 5);
       const int64_t grow = em0 + r;
       if (grow >= em_end || gcol >= en_end) continue;
       const uint4 v = *reinterpret_cast<const uint4*>(smem + r * kPitch16 + c8 * 2);
@@ -443,7 +475,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
     }
   } else {
     // FP32 tile (256 KB) in two halves of 128 rows: the wavefronts with wm == h write half h.
-    char* wbase = smem + 4 * (lane >> 5) * kPitch32 + (wn * 64 + (lane & 31)) * 4;
+    char* wbase = smem + 4 * (lane >> 5) * kPitch32 + (wn * NJ * 32 + (lane & 31)) * 4;
     const int c4 = (tid & 63) * 4;
     const int64_t gcol = en0 + c4;
 #pragma unroll
@@ -460,9 +492,10 @@ __global__ __launch_bounds__(kWaves * 64, 1) void gemm_nt_kernel(NtArgs p) {
                                         j * 128) = acc[i][j][v];
       }
       __syncthreads();
+      constexpr int kRowsPerPass32 = WAVES;       // 64 lanes cover a row
 #pragma unroll 4
-      for (int it = 0; it < 128 / 8; ++it) {
-        const int r = it * 8 + (tid >> 6);
+      for (int it = 0; it < 128 / kRowsPerPass32; ++it) {
+        const int r = it * kRowsPerPass32 + (tid >> 6);
         const int64_t grow = em0 + h * 128 + r;
         if (grow >= em_end || gcol >= en_end) continue;
         const uint4 v = *reinterpret_cast<const uint4*>(smem + r * kPitch32 + c4 * 4);
@@ -505,7 +538,7 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(NtArgs p) {
   }
 }
 
-// Blocks resident at once: one 512-lane block per CU.
+// Blocks resident at once: one block per CU (its LDS).
 int64_t resident_blocks() {
   int dev = 0, ncu = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
@@ -562,17 +595,17 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, in
     items = tiles + rem;
   }
   const dim3 grid((unsigned)items);
-  const dim3 blk(kWaves * 64);
+  const dim3 b8(8 * 64), b4(4 * 64);
   if (c_f32) {
-    if (a_mn && b_mn) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, true, true>), grid, blk, 0, s, a);
-    else if (b_mn) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, false, true>), grid, blk, 0, s, a);
-    else if (a_mn) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, true, false>), grid, blk, 0, s, a);
-    else hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, false, false>), grid, blk, 0, s, a);
+    if (a_mn && b_mn) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, true, true, 8>), grid, b8, 0, s, a);
+    else if (b_mn) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, false, true, 8>), grid, b8, 0, s, a);
+    else if (a_mn) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, true, false, 8>), grid, b8, 0, s, a);
+    else hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, false, false, 4>), grid, b4, 0, s, a);
   } else {
-    if (a_mn && b_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, true, true>), grid, blk, 0, s, a);
-    else if (b_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, false, true>), grid, blk, 0, s, a);
-    else if (a_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, true, false>), grid, blk, 0, s, a);
-    else hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, false, false>), grid, blk, 0, s, a);
+    if (a_mn && b_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, true, true, 8>), grid, b8, 0, s, a);
+    else if (b_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, false, true, 8>), grid, b8, 0, s, a);
+    else if (a_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, true, false, 8>), grid, b8, 0, s, a);
+    else hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, false, false, 4>), grid, b4, 0, s, a);
   }
   if (a.part != nullptr)
     hipLaunchKernelGGL(split_reduce_kernel, dim3(BM * BN / (256 * 4), (unsigned)rem), dim3(256),
@@ -593,8 +626,8 @@ hipError_t launch_grouped_nt_rows(int64_t E, int64_t T, int64_t N, int64_t K, co
   a.tiles_n = (int)((N + BN - 1) / BN);
   a.tiles_m = (int)((T + BM - 1) / BM + E);
   const dim3 grid((unsigned)(a.tiles_m * a.tiles_n));
-  if (b_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRows, false, true>), grid, dim3(kWaves * 64), 0, s, a);
-  else hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRows, false, false>), grid, dim3(kWaves * 64), 0, s, a);
+  if (b_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRows, false, true, 8>), grid, dim3(8 * 64), 0, s, a);
+  else hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRows, false, false, 4>), grid, dim3(4 * 64), 0, s, a);
   return hipGetLastError();
 }
 
@@ -611,7 +644,7 @@ hipError_t launch_grouped_nt_k(int64_t E, int64_t M, int64_t N, int64_t Kpad, co
   a.tiles_m = (int)((M + BM - 1) / BM);
   a.tiles_n = (int)((N + BN - 1) / BN);
   const dim3 grid((unsigned)(a.tiles_m * a.tiles_n * E));
-  hipLaunchKernelGGL((gemm_nt_kernel<true, kGroupK, false, false>), grid, dim3(kWaves * 64), 0, s, a);
+  hipLaunchKernelGGL((gemm_nt_kernel<true, kGroupK, false, false, 4>), grid, dim3(4 * 64), 0, s, a);
   return hipGetLastError();
 }
 
