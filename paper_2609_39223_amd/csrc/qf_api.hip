@@ -401,7 +401,6 @@ struct GroupedWs {
   uint16_t* ahat;   // [T, K]
   uint16_t* whatt;  // [E, K, N]: per-expert W_hat^T, right operand of dX in NT form
   int* kstart;      // [E+1]: expert e's tokens at padded columns [64 kstart[e], 64 kstart[e+1])
-  int* korder;      // [E]: experts in XCD-balanced order for the dW launch
   uint16_t* dyt;    // [N, Tpad]: dY^T, each expert's tokens padded to a multiple of 64
   uint16_t* at;     // [K, Tpad]: A_hat^T, same padding (dW operands in NT form)
 };
@@ -414,7 +413,7 @@ size_t grouped_ws_bytes(const qf_grouped_desc* d) {
   if (d->wfmt != QF_FMT_NONE) b += up((size_t)d->E * d->N * d->K * 2);
   if (d->afmt != QF_FMT_NONE) b += up((size_t)d->T * d->K * 2);
   b += up((size_t)d->E * d->N * d->K * 2);
-  b += up((size_t)(d->E + 1) * 4) + up((size_t)d->E * 4);
+  b += up((size_t)(d->E + 1) * 4);
   b += up((size_t)d->N * grouped_tpad(d) * 2) + up((size_t)d->K * grouped_tpad(d) * 2);
   return b;
 }
@@ -429,7 +428,6 @@ GroupedWs grouped_ws(const qf_grouped_desc* d, void* ws) {
   if (d->afmt != QF_FMT_NONE) { g.ahat = reinterpret_cast<uint16_t*>(p); p += up((size_t)d->T * d->K * 2); }
   g.whatt = reinterpret_cast<uint16_t*>(p); p += up((size_t)d->E * d->N * d->K * 2);
   g.kstart = reinterpret_cast<int*>(p); p += up((size_t)(d->E + 1) * 4);
-  g.korder = reinterpret_cast<int*>(p); p += up((size_t)d->E * 4);
   g.dyt = reinterpret_cast<uint16_t*>(p); p += up((size_t)d->N * grouped_tpad(d) * 2);
   g.at = reinterpret_cast<uint16_t*>(p);
   return g;
@@ -507,8 +505,7 @@ qf_status qf_qlinear_grouped_fwd(const qf_grouped_desc* d, const int64_t* group_
   GroupedWs g = grouped_ws(d, ws);
   const uint16_t *Wop, *Aop;
   QF_TRY(grouped_quantize(d, X, W, g, true, true, &Wop, &Aop, s));
-  QF_TRY(dev(qf::launch_grouped_prep(group_offsets, d->E, g.tile_start, g.order, g.kstart,
-                                    g.korder, s),
+  QF_TRY(dev(qf::launch_grouped_prep(group_offsets, d->E, g.tile_start, g.order, g.kstart, s),
              "prep"));
   QF_TRY(dev(qf::launch_grouped_nt_rows(d->E, d->T, d->N, d->K, group_offsets, g.tile_start, Aop,
                                         d->K, Wop, d->K, 0, d->N * d->K, Y, d->N, s),
@@ -535,8 +532,7 @@ qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int64_t* gr
   const bool fuse_w = dX && d->wfmt != QF_FMT_NONE && !reuse;
   const uint16_t *Wop, *Aop;
   QF_TRY(grouped_quantize(d, X, W, g, !reuse && dX && !fuse_w, false, &Wop, &Aop, s));
-  QF_TRY(dev(qf::launch_grouped_prep(group_offsets, d->E, g.tile_start, g.order, g.kstart,
-                                    g.korder, s),
+  QF_TRY(dev(qf::launch_grouped_prep(group_offsets, d->E, g.tile_start, g.order, g.kstart, s),
              "prep"));
   if (dX) {
     if (fuse_w) {
@@ -569,7 +565,7 @@ qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int64_t* gr
     QF_TRY(dev(qf::launch_quant_t_grouped(saved ? QF_FMT_NONE : d->afmt, saved ? g.ahat : X, d->T,
                                           d->K, group_offsets, g.kstart, d->E, g.at, tp, s),
                "quantize A (grouped, transposed)"));
-    QF_TRY(dev(qf::launch_grouped_nt_k(d->E, d->N, d->K, tp, g.kstart, g.korder, g.dyt, tp, g.at,
+    QF_TRY(dev(qf::launch_grouped_nt_k(d->E, d->N, d->K, tp, g.kstart, g.order, g.dyt, tp, g.at,
                                        tp, dW, d->K, d->N * d->K, s),
                "grouped dW"));
   }
@@ -999,8 +995,7 @@ qf_status qf_qlinear_grouped_lora_fwd(const qf_grouped_desc* d, const qf_lora* l
     QF_TRY(dev(qf::launch_mxfp4(X, d->T, d->K, d->K, nullptr, nullptr, g.ahat, s), "mxfp4"));
     Aop = g.ahat;
   }
-  QF_TRY(dev(qf::launch_grouped_prep(group_offsets, d->E, g.tile_start, g.order, nullptr, nullptr,
-                                    s),
+  QF_TRY(dev(qf::launch_grouped_prep(group_offsets, d->E, g.tile_start, g.order, nullptr, s),
              "prep"));
   QF_TRY(dev(qf::launch_grouped_nt_rows(d->E, d->T, d->N, d->K, group_offsets, g.tile_start, Aop,
                                         d->K, g.what, d->K, 0, d->N * d->K, Y, d->N, s),
@@ -1030,8 +1025,7 @@ qf_status qf_qlinear_grouped_lora_bwd_ste(const qf_grouped_desc* d, const qf_lor
   const bool reuse = (d->flags & QF_FLAG_REUSE_WS) != 0;
   const int64_t E = d->E, T = d->T, N = d->N, K = d->K, r = lora->r, rp = (r + 15) / 16 * 16;
   if (dX) {
-    QF_TRY(dev(qf::launch_grouped_prep(group_offsets, E, g.tile_start, g.order, nullptr, nullptr,
-                                      s),
+    QF_TRY(dev(qf::launch_grouped_prep(group_offsets, E, g.tile_start, g.order, nullptr, s),
                "prep"));
     if (reuse) {
       QF_TRY(dev(qf::launch_transpose_bf16(g.what, N, K, K, g.whatt, N, E, N * K, N * K, s),

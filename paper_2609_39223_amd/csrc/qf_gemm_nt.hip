@@ -75,7 +75,8 @@ struct NtArgs {
   int E;
   // grouped K (per-expert weight gradient): expert e contracts over k in
   // [BK kstart[e], BK kstart[e+1]) and writes C + e cstride; order[] lists experts by
-  // decreasing work, so the largest start first.
+  // decreasing work.  Every XCD owns the same contiguous eighth of each expert's tile grid
+  // and runs its share of the experts in that order (see the item mapping in the kernel).
   const int* kstart;
   const int* order;
   int64_t cstride;
@@ -173,9 +174,18 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
   if (MODE == kDense || MODE == kGroupK) {
     int t = bid;
     if (MODE == kGroupK) {
+      // Block b runs on XCD x = b % 8 as that XCD's item j = b / 8.  XCD x owns tiles
+      // [x tpe / 8, (x + 1) tpe / 8) of every expert; its items walk the experts in order[]
+      // (decreasing work), cmax = ceil(tpe / 8) items per expert, the surplus ones empty.  So
+      // the 8 XCDs carry equal work however skewed the routing is, and each XCD's CUs take
+      // the largest tiles first.
       const int tpe = p.tiles_m * p.tiles_n;
-      const int e = p.order[bid / tpe];
-      t = bid % tpe;
+      const int cmax = (tpe + kXcds - 1) / kXcds;
+      const int x = blockIdx.x % kXcds, j = blockIdx.x / kXcds;
+      const int lo = x * tpe / kXcds, hi = (x + 1) * tpe / kXcds;
+      t = lo + j % cmax;
+      if (t >= hi) return;                         // uniform over the block
+      const int e = p.order[j / cmax];
       ks0 = p.kstart[e];
       ks1 = p.kstart[e + 1];
       cofs = (int64_t)e * p.cstride;
@@ -188,8 +198,15 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
     m_end = p.M;
     n0 = (int64_t)((t % per_group) / gs) * BN;
   } else {
-    const int mt = bid / p.tiles_n, tn = bid % p.tiles_n;
-    if (mt >= p.tile_start[p.E]) return;         // uniform over the block
+    // The grid is sized for the most row tiles any routing can need; the real count is
+    // tile_start[E].  Block b runs on XCD x = b % 8 as its item j = b / 8, and XCD x takes the
+    // contiguous range [x per, (x + 1) per) of the real items (per = ceil(items / 8)), so the
+    // XCDs get equal shares and their 32 CUs share the expert weight panels in their L2.
+    const int items = p.tile_start[p.E] * p.tiles_n;
+    const int per = (items + kXcds - 1) / kXcds;
+    const int j = blockIdx.x / kXcds, it = (blockIdx.x % kXcds) * per + j;
+    if (j >= per || it >= items) return;         // uniform over the block
+    const int mt = it / p.tiles_n, tn = it % p.tiles_n;
     int lo = 0, hi = p.E;                        // tile_start[e] <= mt < tile_start[e+1]
     while (hi - lo > 1) {
       const int mid = (lo + hi) >> 1;
@@ -625,7 +642,8 @@ hipError_t launch_grouped_nt_rows(int64_t E, int64_t T, int64_t N, int64_t K, co
   a.vec_store = vec_store_ok(C, ldc, 2);
   a.tiles_n = (int)((N + BN - 1) / BN);
   a.tiles_m = (int)((T + BM - 1) / BM + E);
-  const dim3 grid((unsigned)(a.tiles_m * a.tiles_n));
+  const int64_t per = ((int64_t)a.tiles_m * a.tiles_n + kXcds - 1) / kXcds;
+  const dim3 grid((unsigned)(kXcds * per));
   if (b_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRows, false, true, 8>), grid, dim3(8 * 64), 0, s, a);
   else hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRows, false, false, 4>), grid, dim3(4 * 64), 0, s, a);
   return hipGetLastError();
@@ -643,7 +661,8 @@ hipError_t launch_grouped_nt_k(int64_t E, int64_t M, int64_t N, int64_t Kpad, co
   a.vec_store = vec_store_ok(C, ldc, 4) && (cstride * 4) % 16 == 0;
   a.tiles_m = (int)((M + BM - 1) / BM);
   a.tiles_n = (int)((N + BN - 1) / BN);
-  const dim3 grid((unsigned)(a.tiles_m * a.tiles_n * E));
+  const int64_t cmax = ((int64_t)a.tiles_m * a.tiles_n + kXcds - 1) / kXcds;
+  const dim3 grid((unsigned)(kXcds * E * cmax));
   hipLaunchKernelGGL((gemm_nt_kernel<true, kGroupK, false, false, 4>), grid, dim3(4 * 64), 0, s, a);
   return hipGetLastError();
 }

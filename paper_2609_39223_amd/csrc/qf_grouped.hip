@@ -11,7 +11,7 @@ namespace {
 constexpr int BM = 256;   // row tile of the NT GEMM's grouped-rows mode
 
 __global__ void grouped_prep_kernel(const int64_t* __restrict__ off, int E, int* tile_start,
-                                    int* order, int* kstart, int* korder) {
+                                    int* order, int* kstart) {
   __shared__ int cnt[1024], cnt64[1024];
   const int e = threadIdx.x;
   int64_t rows = 0;
@@ -36,27 +36,15 @@ __global__ void grouped_prep_kernel(const int64_t* __restrict__ off, int E, int*
       rank += (ri > rows) || (ri == rows && i < e);
     }
     order[rank] = e;
-    if (korder) {
-      // Balanced over the 8 XCDs for launches whose items run as 8 contiguous ranges (one per
-      // XCD): ranks are dealt in a snake (0..7 to XCDs 0..7, 8..15 to XCDs 7..0, ...), and
-      // each XCD's experts stay in decreasing order.  Needs E % 8 == 0 (else the plain order).
-      int pos = rank;
-      if (E % 8 == 0) {
-        const int k = rank / 8, i = rank % 8;
-        const int x = (k & 1) ? 7 - i : i;
-        pos = x * (E / 8) + k;
-      }
-      korder[pos] = e;
-    }
   }
 }
 
 }  // namespace
 
 hipError_t launch_grouped_prep(const int64_t* off, int64_t E, int* tile_start, int* order,
-                               int* kstart, int* korder, hipStream_t s) {
+                               int* kstart, hipStream_t s) {
   hipLaunchKernelGGL(grouped_prep_kernel, dim3(1), dim3(1024), 0, s, off, (int)E, tile_start,
-                     order, kstart, korder);
+                     order, kstart);
   return hipGetLastError();
 }
 

@@ -74,10 +74,9 @@ hipError_t launch_transpose_bf16(const uint16_t* in, int64_t R, int64_t C, int64
 // Grouped over experts (qf_grouped.hip; rows [off[e], off[e+1]) of the token-major operands belong to
 // expert e; the host never reads off).  launch_grouped_prep fills small device arrays:
 // tile_start[E+1] (prefix of per-expert 256-row tile counts), order[E] (experts by
-// decreasing row count) and, when non-null, kstart[E+1] (prefix of per-expert 64-row counts)
-// and korder[E] (the same experts dealt over 8 XCD ranges; see grouped_prep_kernel).
+// decreasing row count) and, when non-null, kstart[E+1] (prefix of per-expert 64-row counts).
 hipError_t launch_grouped_prep(const int64_t* off, int64_t E, int* tile_start, int* order,
-                               int* kstart, int* korder, hipStream_t s);
+                               int* kstart, hipStream_t s);
 
 // ---- LoRA-QAD (qf_lora.hip) ------------------------------------------------------------------
 // Low-rank factors of a merged weight W + scale * B A: A FP32 [r, K] (row stride K), B FP32

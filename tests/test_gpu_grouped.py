@@ -62,6 +62,28 @@ def test_grouped_matches_per_expert_loop(qf, wfmt, afmt):
             assert np.all(dW[e] == 0.0)
 
 
+def test_grouped_dw_tile_grid_split_over_xcds(qf):
+    """Per-expert dW grids of 5 x 3 tiles (ragged in both dimensions) are dealt to the 8 XCDs
+    in shares of 1 or 2 tiles; every expert's gradient is complete, empty experts are zero."""
+    rng = np.random.default_rng(7)
+    E, N, K = 5, 1032, 544
+    counts = np.array([0, 700, 65, 1, 2000])
+    offsets = np.concatenate([[0], np.cumsum(counts)])
+    T = int(offsets[-1])
+    X = workloads.normal_bf16(rng, (T, K))
+    W = np.stack([workloads.normal_bf16(rng, (N, K), 0.02) for _ in range(E)])
+    dY = workloads.normal_bf16(rng, (T, N))
+    Y, dX, dW = run_grouped(qf, offsets, X, W, dY, "nvfp4", "mxfp4")
+    ahat = oracle.fakequant(X, "mxfp4")
+    for e in range(E):
+        r0, r1 = offsets[e], offsets[e + 1]
+        if r1 > r0:
+            assert_close(dW[e].astype(np.float64), oracle.linear_dw(dY[r0:r1], ahat[r0:r1]),
+                         f"dW e={e}")
+        else:
+            assert np.all(dW[e] == 0.0)
+
+
 def test_grouped_zipf_routing_sampled(qf):
     """128 experts, top-8 Zipf(1.1) routing (reduced token count and width), sampled."""
     tok, offsets = workloads.moe_routing(seed=0, tokens=2048, experts=128, topk=8)
