@@ -44,6 +44,22 @@ __device__ __forceinline__ uint32_t bf16_rne(float f) {
   return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
 }
 
+// Two binary32 values -> bfloat16 pair (lo in bits 0-15), round to nearest even, with the
+// hardware conversion: equal to bf16_rne for every input except NaN (whose sign and payload
+// it keeps), so callers use it only on values that cannot be NaN.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t bf16x2_rne_nonnan(float lo, float hi) {
+  const f32x2_t v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
+
+// The two E2M1 codes in byte P of w (low nibble first) as signed binary32 values +-V, exact.
+template <int P>
+__device__ __forceinline__ f32x2_t e2m1_pair(uint32_t w) {
+  return __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, 1.0f, P);
+}
+
 // E2M1 magnitude as binary32 (code 0..7).
 __device__ __forceinline__ float e2m1_value(uint32_t m) {
   uint32_t b = m >= 2u ? (m + 252u) << 22 : (m == 1u ? 0x3F000000u : 0u);
@@ -170,14 +186,30 @@ __device__ __forceinline__ void nvfp4_chunk(const uint32_t h[8], float S, float 
     mc |= (c2 & 0xFFu) << (8 * p);
   }
   if (D == 0.0f) mc = 0;
-  cw = 0;
+  cw = mc;                                  // magnitudes leave bit 3 of each nibble clear
 #pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    const uint32_t sign = h[k] >> 15;
-    const uint32_t m = (mc >> (4 * k)) & 7u;
-    cw |= ((sign << 3) | m) << (4 * k);
-    const float mag = e2m1_value(m) * D;
-    xh[k] = bf16_rne(sign ? -mag : mag);
+  for (int k = 0; k < 8; ++k) cw |= (h[k] >> 15) << (4 * k + 3);
+  if (__builtin_isfinite(D)) {
+    // x_hat = bf16(+-V D): V from the hardware E2M1 decode (exact), one FP32 product, the
+    // hardware round-to-nearest-even pack.  |V D| <= 6 D is finite here, so this equals the
+    // bit-level path below.
+    const f32x2_t v0 = e2m1_pair<0>(cw), v1 = e2m1_pair<1>(cw);
+    const f32x2_t v2 = e2m1_pair<2>(cw), v3 = e2m1_pair<3>(cw);
+    const uint32_t p[4] = {bf16x2_rne_nonnan(v0.x * D, v0.y * D),
+                           bf16x2_rne_nonnan(v1.x * D, v1.y * D),
+                           bf16x2_rne_nonnan(v2.x * D, v2.y * D),
+                           bf16x2_rne_nonnan(v3.x * D, v3.y * D)};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      xh[2 * q] = p[q] & 0xFFFFu;
+      xh[2 * q + 1] = p[q] >> 16;
+    }
+  } else {                                  // tensor scale from a non-finite amax
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const float mag = e2m1_value((cw >> (4 * k)) & 7u) * D;
+      xh[k] = bf16_rne((cw >> (4 * k + 3)) & 1u ? -mag : mag);
+    }
   }
 }
 

@@ -35,24 +35,28 @@ __global__ void fill_f32_kernel(float* p, int64_t n, float v) {
 // max |x| as bf16 magnitude bits (NaN bit patterns sort above +inf), folded into *amax as the
 // binary32 pattern with an integer atomic max (order independent, so the result is exact and
 // deterministic).  grid.z indexes equally shaped tensors when batched (stride R*K elements).
+// A lane issues kAmaxRows 16-byte loads before it reduces them (a pass covers one row chunk of
+// kAmaxRows rows; the grid is sized for about one pass per lane), and a workgroup skips its
+// atomic when a relaxed read already shows a value at least as large (amax only grows).
+constexpr int kAmaxRows = 16;
 __global__ __launch_bounds__(kThreads) void amax_kernel(const uint16_t* __restrict__ x, int64_t R,
                                                         int64_t K, int64_t ldx, int64_t tstride,
                                                         float* __restrict__ amax) {
-  constexpr int RPT = 8;                      // rows per pass: 8 independent 16-byte loads
   const int64_t chunks = K >> 3;
   const uint16_t* xt = x + (int64_t)blockIdx.z * tstride;
   uint32_t m = 0;
   for (int64_t c = (int64_t)blockIdx.x * kThreads + threadIdx.x; c < chunks;
        c += (int64_t)gridDim.x * kThreads) {
-    for (int64_t r0 = (int64_t)blockIdx.y * RPT; r0 < R; r0 += (int64_t)gridDim.y * RPT) {
-      uint4 v[RPT];
+    for (int64_t r0 = (int64_t)blockIdx.y * kAmaxRows; r0 < R;
+         r0 += (int64_t)gridDim.y * kAmaxRows) {
+      uint4 v[kAmaxRows];
 #pragma unroll
-      for (int i = 0; i < RPT; ++i) {
+      for (int i = 0; i < kAmaxRows; ++i) {
         v[i] = make_uint4(0, 0, 0, 0);
         if (r0 + i < R) v[i] = *reinterpret_cast<const uint4*>(xt + (r0 + i) * ldx + c * 8);
       }
 #pragma unroll
-      for (int i = 0; i < RPT; ++i) {
+      for (int i = 0; i < kAmaxRows; ++i) {
         uint32_t h[8];
         unpack8(v[i], h);
         const uint32_t a = max_abs_bits8(h);
@@ -72,7 +76,10 @@ __global__ __launch_bounds__(kThreads) void amax_kernel(const uint16_t* __restri
   if (threadIdx.x == 0) {
     uint32_t b = wmax[0];
     for (int i = 1; i < kThreads / 64; ++i) b = wmax[i] > b ? wmax[i] : b;
-    if (b != 0u) atomicMax(reinterpret_cast<unsigned int*>(amax + blockIdx.z), b << 16);
+    unsigned int* dst = reinterpret_cast<unsigned int*>(amax + blockIdx.z);
+    if (b != 0u &&
+        __hip_atomic_load(dst, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < (b << 16))
+      atomicMax(dst, b << 16);
   }
 }
 
@@ -263,13 +270,15 @@ hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s) {
   return hipGetLastError();
 }
 
-// At most ~1000 blocks (one atomic each) for one tensor: 8 rows per pass, grid-strided.
+// Grid of amax_kernel: up to 64 x 256 chunks per row pass and kAmaxRows rows per lane pass,
+// at most ~2048 workgroups over all E tensors (so most lanes make one or a few passes).
 static dim3 amax_grid(int64_t R, int64_t K, int64_t E) {
   const int64_t chunks = K >> 3;
   int64_t gx = (chunks + kThreads - 1) / kThreads;
   if (gx > 64) gx = 64;
-  int64_t gy = (R + 7) / 8;
-  const int64_t cap = (1024 + gx - 1) / gx;
+  int64_t gy = (R + kAmaxRows - 1) / kAmaxRows;
+  int64_t cap = 2048 / (gx * E);
+  if (cap < 1) cap = 1;
   if (gy > cap) gy = cap;
   if (gy < 1) gy = 1;
   return dim3((unsigned)gx, (unsigned)gy, (unsigned)E);
@@ -286,10 +295,8 @@ hipError_t launch_amax(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, flo
 hipError_t launch_amax_batched(const uint16_t* x, int64_t E, int64_t R, int64_t K, float* amax,
                                hipStream_t s) {
   if (E == 0 || R == 0 || K == 0) return hipSuccess;
-  dim3 grid = amax_grid(R, K, E);
-  const int64_t gy = (R + 7) / 8 < 16 ? (R + 7) / 8 : 16;
-  grid.y = (unsigned)(gy < 1 ? 1 : gy);
-  hipLaunchKernelGGL(amax_kernel, grid, dim3(kThreads), 0, s, x, R, K, K, R * K, amax);
+  hipLaunchKernelGGL(amax_kernel, amax_grid(R, K, E), dim3(kThreads), 0, s, x, R, K, K, R * K,
+                     amax);
   return hipGetLastError();
 }
 
