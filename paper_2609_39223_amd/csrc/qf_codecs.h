@@ -251,6 +251,38 @@ __device__ __forceinline__ void mxfp4_chunk(const uint32_t h[8], uint32_t& cw, u
 struct Q4kChunk {
   uint32_t dh, mh, ls, lm, qlo, qhi;
 };
+
+// Q4_K element codes q[k] = min(max(rint(fl(a[k] / t)), 0), 15) for a normal t > 0.  With
+// rt = 1 / t from v_rcp_f32 (within 1 ulp), y = fl(a rt) is within 2.4e-7 |a / t| of
+// fl(a / t): within 4e-6 for |a / t| <= 16, and further out both clamp alike, so whenever y
+// lies more than 1e-5 from a half-integer both round to the same integer.  A chunk with any
+// element closer than that (or a non-finite y) takes the exact quotients for all eight.
+__device__ __forceinline__ void q4_codes8(const float a[8], float t, uint32_t q[8]) {
+  const float rt = __builtin_amdgcn_rcpf(t);
+  float y[8];
+  bool exact = false;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    y[k] = a[k] * rt;
+    exact |= !(__builtin_fabsf(__builtin_amdgcn_fractf(y[k]) - 0.5f) > 1e-5f);
+  }
+  if (exact) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) y[k] = a[k] / t;
+  }
+#pragma unroll
+  for (int k = 0; k < 8; ++k) q[k] = (uint32_t)fminf(fmaxf(__builtin_rintf(y[k]), 0.0f), 15.0f);
+}
+
+// Q4_K 6-bit sub-block code min(max(rint(fl(a / t)), 0), 63) for a normal t > 0: as above,
+// y = fl(a / v_rcp(t)) is within 1.6e-5 of fl(a / t) for |a / t| <= 64, so a margin of 1e-4
+// around half-integers decides; closer, the exact quotient.
+__device__ __forceinline__ uint32_t q6_code(float a, float t) {
+  float y = a * __builtin_amdgcn_rcpf(t);
+  if (!(__builtin_fabsf(__builtin_amdgcn_fractf(y) - 0.5f) > 1e-4f)) y = a / t;
+  return (uint32_t)fminf(fmaxf(__builtin_rintf(y), 0.0f), 63.0f);
+}
+
 __device__ __forceinline__ void q4k_chunk(const uint32_t h[8], Q4kChunk& r, uint32_t xh[8]) {
   float xv[8];
   float lo = 0.0f, hi = -__builtin_huge_valf();
@@ -273,20 +305,31 @@ __device__ __forceinline__ void q4k_chunk(const uint32_t h[8], Q4kChunk& r, uint
   const float d = f16_value(r.dh), dmin = f16_value(r.mh);
   r.ls = 0;
   r.lm = 0;
-  if (d != 0.0f) r.ls = (uint32_t)fminf(fmaxf(__builtin_rintf(a / d), 0.0f), 63.0f);
-  if (dmin != 0.0f) r.lm = (uint32_t)fminf(fmaxf(__builtin_rintf(mu / dmin), 0.0f), 63.0f);
+  if (d != 0.0f) r.ls = q6_code(a, d);
+  if (dmin != 0.0f) r.lm = q6_code(mu, dmin);
   const float t1 = d * (float)r.ls;
   const float t2 = dmin * (float)r.lm;
   r.qlo = 0;
   r.qhi = 0;
+  uint32_t qv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  if (t1 != 0.0f) {
+    float av[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) av[k] = xv[k] + t2;
+    q4_codes8(av, t1, qv);
+  }
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
-    uint32_t q = 0;
-    if (t1 != 0.0f) q = (uint32_t)fminf(fmaxf(__builtin_rintf((xv[k] + t2) / t1), 0.0f), 15.0f);
-    if (k < 4) r.qlo |= q << (8 * k);
-    else r.qhi |= q << (8 * (k - 4));
-    const float prod = t1 * (float)q;
-    xh[k] = bf16_rne(prod - t2);
+    if (k < 4) r.qlo |= qv[k] << (8 * k);
+    else r.qhi |= qv[k] << (8 * (k - 4));
+  }
+  // t1 q - t2 is finite for every input (t1, t2 come from FP16 scales), so the hardware pack
+  // rounds it exactly as bf16_rne would
+#pragma unroll
+  for (int k = 0; k < 8; k += 2) {
+    const uint32_t p = bf16x2_rne_nonnan(t1 * (float)qv[k] - t2, t1 * (float)qv[k + 1] - t2);
+    xh[k] = p & 0xFFFFu;
+    xh[k + 1] = p >> 16;
   }
 }
 
@@ -324,17 +367,23 @@ __device__ __forceinline__ float q4k_finish(const float xv[8], float a, float mu
   const float d = f16_value(r.dh), dmin = f16_value(r.mh);
   r.ls = 0;
   r.lm = 0;
-  if (d != 0.0f) r.ls = (uint32_t)fminf(fmaxf(__builtin_rintf(a / d), 0.0f), 63.0f);
-  if (dmin != 0.0f) r.lm = (uint32_t)fminf(fmaxf(__builtin_rintf(mu / dmin), 0.0f), 63.0f);
+  if (d != 0.0f) r.ls = q6_code(a, d);
+  if (dmin != 0.0f) r.lm = q6_code(mu, dmin);
   const float t1 = d * (float)r.ls;
   const float t2 = dmin * (float)r.lm;
   r.qlo = 0;
   r.qhi = 0;
   float e2[8];
+  uint32_t qv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  if (t1 != 0.0f) {
+    float av[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) av[k] = xv[k] + t2;
+    q4_codes8(av, t1, qv);
+  }
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
-    uint32_t q = 0;
-    if (t1 != 0.0f) q = (uint32_t)fminf(fmaxf(__builtin_rintf((xv[k] + t2) / t1), 0.0f), 15.0f);
+    const uint32_t q = qv[k];
     if (k < 4) r.qlo |= q << (8 * k);
     else r.qhi |= q << (8 * (k - 4));
     xf[k] = t1 * (float)q - t2;

@@ -178,6 +178,29 @@ def test_q4k_exhaustive_bf16_inputs_below_limits(qf):
         assert_same(run_q4k(qf, x), oracle.q4k(x), ("packed", "xhat"), f"q4k below {lim}")
 
 
+def q4k_tie_rows():
+    """Super-blocks whose element quotients (x + t2) / t1 land exactly on half-integers: the
+    first sub-block spans [-1/32, 29.5] (step 63/32, so d = 1/32), the other seven span
+    [0, 15] (ls = 32, t1 = 1, t2 = 0) and hold k + 1/2 values (rounding ties)."""
+    rng = np.random.default_rng(11)
+    rows = []
+    for r in range(6):
+        subs = [np.concatenate([[29.5, -0.03125], rng.integers(0, 59, 30) * 0.5])]
+        subs += [np.concatenate([[0.0, 15.0], rng.integers(0, 15, 30) + 0.5]) for _ in range(7)]
+        row = np.concatenate([rng.permutation(s) for s in subs]).astype(np.float32)
+        rows.append(-row[::-1].copy() if r % 2 else row)
+    return (np.stack(rows).view(np.uint32) >> 16).astype(np.uint16)
+
+
+def test_q4k_exact_rounding_ties(qf):
+    x = q4k_tie_rows()
+    ref = oracle.q4k(x)
+    d, dmin, ls, lm, q = oracle.q4k_unpack_block(ref["packed"][0, 0])
+    assert d == 0x2800 and ls[1:] == [32] * 7                 # t1 = 1 in sub-blocks 1-7
+    assert_same(run_q4k(qf, x), ref, ("packed", "xhat"), "q4k ties")
+    assert_same(run_q4k_mse(qf, x), oracle.q4k_mse(x), ("packed", "xhat"), "q4k-mse ties")
+
+
 def test_q4k_full_size_export_weight(qf):
     w = workloads.q4k_weight(seed=0, scale=64)
     assert_same(run_q4k(qf, w["W"]), oracle.q4k(w["W"]), ("packed", "xhat"), "q4k 14336x4096")
