@@ -47,6 +47,7 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef short v8i16 __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int BM = 256, BN = 256, BK = 64;
 constexpr int kRow = BK * 2;                     // 128 bytes per LDS row
@@ -122,10 +123,28 @@ __device__ __forceinline__ v4i16 lds_tr16(const char* p) {
       (__attribute__((address_space(3))) v4i16*)(__attribute__((address_space(3))) char*)(p));
 }
 
-__device__ __forceinline__ uint32_t bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7FFFFFFFu) > 0x7F800000u) return 0x7FC0u;
-  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+// Workgroup barrier that orders LDS accesses only: outstanding global stores are not waited
+// for (a plain __syncthreads() would drain them).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// 16-byte store of an output row segment.  Output tiles go out non-temporally: they are not
+// read again by this launch, and as ordinary stores their lines displace operand panels in L2
+// (measured 2-5 % slower on whole launches); split partials, read back right away, stay cached.
+__device__ __forceinline__ void store_c16(void* dst, uint4 v, bool nt) {
+  if (nt) __builtin_nontemporal_store(u32x4_t{v.x, v.y, v.z, v.w}, reinterpret_cast<u32x4_t*>(dst));
+  else *reinterpret_cast<uint4*>(dst) = v;
+}
+
+// Two FP32 values -> packed bf16 pair (lo in bits 0-15), round to nearest even.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const f32x2_t v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
 
 __device__ __forceinline__ int remap_xcd(int bid, int nb) {
@@ -356,7 +375,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
     constexpr int NM = 4 * NJ, NR = 4 + NJ;
 #pragma unroll
     for (int t = 0; t < NM; ++t) {
-      acc[t / NJ][t % NJ] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[t / NJ], b[t % NJ],
+      acc[t / NJ][t % NJ] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[t % NJ], a[t / NJ],
                                                                     acc[t / NJ][t % NJ], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
       if (READS && t < NR) read_one(rst, rkk, t, ra, rb);
@@ -444,14 +463,15 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
       for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < NJ; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[0][i], fb[0][j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[0][j], fa[0][i], acc[i][j], 0, 0, 0);
     }
   }
 
   // ---- epilogue: the tile goes through LDS and leaves as whole-row 16-byte stores ----------
-  // Accumulator element v of block (i, j) sits at row 8 (v / 4) + 4 (lane / 32) + v % 4, column
-  // lane % 32 of that 32 x 32 block.  Rows are padded so that the two half-waves of a write
-  // (rows 4 apart) land 16 banks apart.
+  // Each MFMA takes the B fragment as its first operand, so accumulator block (i, j) holds the
+  // transposed product: element v sits at row lane % 32 of the block and column
+  // 8 (v / 4) + 4 (lane / 32) + v % 4, i.e. a lane owns four consecutive columns of one row per
+  // group v / 4, written to LDS with one 8-byte (bf16) or 16-byte (FP32) store.
   __syncthreads();                               // every wavefront is done with the operands
   // Destination: the output tile, or (split halves) a dense 256 x 256 FP32 partial.
   char* Cp = reinterpret_cast<char*>(p.C) + cofs * (C_F32 ? 4 : 2);
@@ -461,17 +481,22 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
     Cp = reinterpret_cast<char*>(p.part + (int64_t)pidx * BM * BN);
     ldc = BN; em0 = 0; em_end = BM; en0 = 0; en_end = BN; vec = 1;
   }
+  const int er = wm * 128 + (lane & 31);          // this lane's row in block (0, *)
+  const int ec = wn * (NJ * 32) + 4 * (lane >> 5);  // its first column in block (*, 0), group 0
   if (!C_F32) {
-    char* wbase = smem + (wm * 128 + 4 * (lane >> 5)) * kPitch16 + (wn * NJ * 32 + (lane & 31)) * 2;
+    // bf16 pairs by the hardware pack (round to nearest even; a NaN result stays a quiet NaN)
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < NJ; ++j)
 #pragma unroll
-        for (int v = 0; v < 16; ++v)
-          *reinterpret_cast<uint16_t*>(wbase + (i * 32 + 8 * (v >> 2) + (v & 3)) * kPitch16 +
-                                       j * 64) = (uint16_t)bf16_rne(acc[i][j][v]);
-    __syncthreads();
+        for (int g = 0; g < 4; ++g) {
+          const f32x16_t& a = acc[i][j];
+          const uint2 w = make_uint2(pack_bf16x2(a[4 * g], a[4 * g + 1]),
+                                     pack_bf16x2(a[4 * g + 2], a[4 * g + 3]));
+          *reinterpret_cast<uint2*>(smem + (er + 32 * i) * kPitch16 + (ec + 32 * j + 8 * g) * 2) = w;
+        }
+    lds_barrier();
     const int c8 = (tid & 31) * 8;
     const int64_t gcol = en0 + c8;
     constexpr int kRowsPerPass = WAVES * 64 / 32;  // 32 lanes cover a row
@@ -483,7 +508,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
       const uint4 v = *reinterpret_cast<const uint4*>(smem + r * kPitch16 + c8 * 2);
       uint16_t* dst = reinterpret_cast<uint16_t*>(Cp) + grow * ldc + gcol;
       if (vec && gcol + 8 <= en_end) {
-        *reinterpret_cast<uint4*>(dst) = v;
+        store_c16(dst, v, half < 0);
       } else {
         const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
         for (int e = 0; e < 8 && gcol + e < en_end; ++e)
@@ -491,34 +516,35 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
       }
     }
   } else {
-    // FP32 tile (256 KB) in two halves of 128 rows: the wavefronts with wm == h write half h.
-    char* wbase = smem + 4 * (lane >> 5) * kPitch32 + (wn * NJ * 32 + (lane & 31)) * 4;
+    // FP32 tile (256 KB) in two halves: in half h every wavefront writes its row blocks 2h and
+    // 2h + 1, so LDS row q (0..127) holds tile row (q / 64) * 128 + 64 h + q % 64.
     const int c4 = (tid & 63) * 4;
     const int64_t gcol = en0 + c4;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      if (h) __syncthreads();                    // half 0 has been read out
-      if (wm == h) {
+      if (h) lds_barrier();                      // half 0 has been read out of LDS
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+      for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
-          for (int j = 0; j < NJ; ++j)
+        for (int j = 0; j < NJ; ++j)
 #pragma unroll
-            for (int v = 0; v < 16; ++v)
-              *reinterpret_cast<float*>(wbase + (i * 32 + 8 * (v >> 2) + (v & 3)) * kPitch32 +
-                                        j * 128) = acc[i][j][v];
-      }
-      __syncthreads();
+          for (int g = 0; g < 4; ++g) {
+            const f32x16_t& a = acc[2 * h + ii][j];
+            const int q = wm * 64 + ii * 32 + (lane & 31);
+            *reinterpret_cast<float4*>(smem + q * kPitch32 + (ec + 32 * j + 8 * g) * 4) =
+                make_float4(a[4 * g], a[4 * g + 1], a[4 * g + 2], a[4 * g + 3]);
+          }
+      lds_barrier();
       constexpr int kRowsPerPass32 = WAVES;       // 64 lanes cover a row
 #pragma unroll 4
       for (int it = 0; it < 128 / kRowsPerPass32; ++it) {
-        const int r = it * kRowsPerPass32 + (tid >> 6);
-        const int64_t grow = em0 + h * 128 + r;
+        const int q = it * kRowsPerPass32 + (tid >> 6);
+        const int64_t grow = em0 + (q >> 6) * 128 + 64 * h + (q & 63);
         if (grow >= em_end || gcol >= en_end) continue;
-        const uint4 v = *reinterpret_cast<const uint4*>(smem + r * kPitch32 + c4 * 4);
+        const uint4 v = *reinterpret_cast<const uint4*>(smem + q * kPitch32 + c4 * 4);
         float* dst = reinterpret_cast<float*>(Cp) + grow * ldc + gcol;
         if (vec && gcol + 4 <= en_end) {
-          *reinterpret_cast<uint4*>(dst) = v;
+          store_c16(dst, v, half < 0);
         } else {
           const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
           for (int e = 0; e < 4 && gcol + e < en_end; ++e) dst[e] = __uint_as_float(wv[e]);
