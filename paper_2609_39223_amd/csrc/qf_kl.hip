@@ -6,7 +6,10 @@
 //   pass 1  online base-2 statistics of both rows, with a = z log2(e):
 //             m = max a,  S = sum 2^(a - m)                         (teacher and student)
 //             Q = sum 2^(a_T - m_T) (z_T - z_S)                      (teacher-weighted gap)
-//           and the first index of each row's maximum logit.  Then, in natural units,
+//           and the first index of each row's maximum logit.  Each 8-logit chunk updates the
+//           maxima from its raw maximum (z -> z log2(e) is monotone), each exponent is one
+//           FMA (z log2(e) - m), and the index search runs only when a chunk's maximum beats
+//           the lane's running one.  Then, in natural units,
 //             lse = ln2 (m + log2 S),   KL = Q / S_T + lse_S - lse_T
 //           (sum_v p_T (log p_T - log p_S) with log p = z - lse).
 //   pass 2  grad[v] = scale (2^(a_S - c_S) - 2^(a_T - c_T)), c = m + log2 S, i.e.
@@ -60,6 +63,29 @@ __device__ __forceinline__ ArgMax amax_merge(ArgMax x, ArgMax y) {
   return x;
 }
 
+// The 8 bf16 logits of a 16-byte chunk as FP32 (element k in half k % 2 of dword k / 2).
+__device__ __forceinline__ void unpack8_f32(uint4 v, float x[8]) {
+  const uint32_t d[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    x[2 * q] = as_f32(d[q] << 16);
+    x[2 * q + 1] = as_f32(d[q] & 0xFFFF0000u);
+  }
+}
+
+__device__ __forceinline__ float max8(const float x[8]) {
+  return fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])),
+               fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+}
+
+// First k with x[k] == m (m is the maximum of x, so one exists).
+__device__ __forceinline__ int first_eq8(const float x[8], float m) {
+  int k0 = 7;
+#pragma unroll
+  for (int k = 6; k >= 0; --k) k0 = x[k] == m ? k : k0;
+  return k0;
+}
+
 template <int NT>
 __global__ __launch_bounds__(NT) void qad_kl_kernel(const uint16_t* __restrict__ zt, int64_t ldt,
                                                     const uint16_t* __restrict__ zs, int64_t lds_,
@@ -98,31 +124,23 @@ __global__ __launch_bounds__(NT) void qad_kl_kernel(const uint16_t* __restrict__
     for (int u = 0; u < kUnroll; ++u) {
       const int64_t c = c0 + (int64_t)u * NT;
       if (c >= chunks) break;
-      uint32_t ht[8], hs[8];
-      unpack8(vt[u], ht);
-      unpack8(vs[u], hs);
       float xt[8], xs[8];
-      float cmt = -__builtin_huge_valf(), cms = -__builtin_huge_valf();
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        xt[k] = as_f32(ht[k] << 16);
-        xs[k] = as_f32(hs[k] << 16);
-        if (xt[k] > at.v) { at.v = xt[k]; at.i = c * 8 + k; }
-        if (xs[k] > as.v) { as.v = xs[k]; as.i = c * 8 + k; }
-        cmt = fmaxf(cmt, xt[k] * kLog2e);
-        cms = fmaxf(cms, xs[k] * kLog2e);
-      }
+      unpack8_f32(vt[u], xt);
+      unpack8_f32(vs[u], xs);
+      const float mt = max8(xt), ms = max8(xs);
+      if (mt > at.v) at = ArgMax{mt, c * 8 + first_eq8(xt, mt)};
+      if (ms > as.v) as = ArgMax{ms, c * 8 + first_eq8(xs, ms)};
       // rescale the running sums to the new maxima, then add the chunk
-      const float nmt = fmaxf(st.m, cmt), nms = fmaxf(ss.m, cms);
+      const float nmt = fmaxf(st.m, mt * kLog2e), nms = fmaxf(ss.m, ms * kLog2e);
       const float ft = st.m == nmt ? 1.0f : exp2_safe(st.m - nmt);
       const float fs = ss.m == nms ? 1.0f : exp2_safe(ss.m - nms);
       float S_t = st.S * ft, Q_t = st.Q * ft, S_s = ss.S * fs;
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        const float et = exp2_safe(xt[k] * kLog2e - nmt);
+        const float et = exp2_safe(__builtin_fmaf(xt[k], kLog2e, -nmt));
         S_t += et;
-        Q_t += et * (xt[k] - xs[k]);
-        S_s += exp2_safe(xs[k] * kLog2e - nms);
+        Q_t = __builtin_fmaf(et, xt[k] - xs[k], Q_t);
+        S_s += exp2_safe(__builtin_fmaf(xs[k], kLog2e, -nms));
       }
       st = Stat{nmt, S_t, Q_t};
       ss = Stat{nms, S_s, 0.0f};
@@ -168,6 +186,10 @@ __global__ __launch_bounds__(NT) void qad_kl_kernel(const uint16_t* __restrict__
   __syncthreads();
   const float ct = row_c[0], cs = row_c[1];
   uint16_t* pg = grad + row * ldg;
+  // Finite row statistics make every probability finite, so the hardware bf16 pack rounds
+  // exactly as bf16_rne; rows with non-finite logits keep the bit-level rounding (uniform per
+  // workgroup).
+  const bool finite = __builtin_isfinite(ct) && __builtin_isfinite(cs);
   for (int64_t c0 = t; c0 < chunks; c0 += (int64_t)NT * kUnroll) {
     uint4 vt[kUnroll], vs[kUnroll];
 #pragma unroll
@@ -184,17 +206,24 @@ __global__ __launch_bounds__(NT) void qad_kl_kernel(const uint16_t* __restrict__
     for (int u = 0; u < kUnroll; ++u) {
       const int64_t c = c0 + (int64_t)u * NT;
       if (c >= chunks) break;
-      uint32_t ht[8], hs[8], go[8];
-      unpack8(vt[u], ht);
-      unpack8(vs[u], hs);
+      float xt[8], xs[8], g[8];
+      unpack8_f32(vt[u], xt);
+      unpack8_f32(vs[u], xs);
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        const float p_t = exp2_safe(as_f32(ht[k] << 16) * kLog2e - ct);
-        const float p_s = exp2_safe(as_f32(hs[k] << 16) * kLog2e - cs);
-        go[k] = bf16_rne(gscale * (p_s - p_t));
+        const float p_t = exp2_safe(__builtin_fmaf(xt[k], kLog2e, -ct));
+        const float p_s = exp2_safe(__builtin_fmaf(xs[k], kLog2e, -cs));
+        g[k] = gscale * (p_s - p_t);
       }
-      const uint4 o = pack8(go);
-      const u32x4 ov = {o.x, o.y, o.z, o.w};
+      uint32_t o[4];
+      if (finite) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) o[q] = bf16x2_rne_nonnan(g[2 * q], g[2 * q + 1]);
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) o[q] = bf16_rne(g[2 * q]) | (bf16_rne(g[2 * q + 1]) << 16);
+      }
+      const u32x4 ov = {o[0], o[1], o[2], o[3]};
       __builtin_nontemporal_store(ov, reinterpret_cast<u32x4*>(pg + c * 8));
     }
   }
