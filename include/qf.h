@@ -168,7 +168,8 @@ typedef struct {
 QF_API qf_status qf_workspace_size(const qf_qlinear_desc* d, size_t* bytes);
 
 /*
- * qf_qlinear_fwd -- Y = A_hat W_hat^T (bf16 output, FP32 accumulation on MFMA).
+ * qf_qlinear_fwd -- Y = A_hat W_hat^T (bf16 output rounded to nearest even from FP32
+ * accumulation on MFMA; NaN sums give quiet NaNs).
  *   X bf16 [M, K], W bf16 [N, K], Y bf16 [M, N]; ws >= qf_workspace_size bytes, 256-aligned.
  * The workspace receives W_hat (and A_hat when afmt != NONE) as bf16; it also holds the
  * transposed operands the backward builds (W_hat^T, A_hat^T, dY^T), so one workspace serves
@@ -249,7 +250,8 @@ QF_API qf_status qf_transpose_bf16(const uint16_t* in, int64_t R, int64_t C, int
  * qf_gemm_bf16 -- C[M, N] = sum_k opA(m, k) * opB(n, k), FP32 accumulation.
  *   a_kmajor = 1: A stored [M, K] (k contiguous, row stride lda); 0: stored [K, M].
  *   b_kmajor = 1: B stored [N, K] (k contiguous, row stride ldb); 0: stored [K, N].
- *   c_f32 = 1: C is FP32, else bf16; row stride ldc.
+ *   c_f32 = 1: C is FP32, else bf16 (FP32 sums rounded to nearest even; a NaN sum gives a
+ *   quiet NaN whose sign and payload bits are unspecified); row stride ldc.
  * Forward = (1, 1); dX = dY W_hat is (1, 0); dW = dY^T A_hat is (0, 0).
  */
 QF_API qf_status qf_gemm_bf16(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
