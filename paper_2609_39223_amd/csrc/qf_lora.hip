@@ -221,17 +221,35 @@ __global__ void group_prefix_kernel(const int64_t* __restrict__ off, int E, int 
 }
 
 // ============================================================================ row-dot
-// P[m][j0 + jj] = sum_k X[m][k] F[j0 + jj][k] for jj < 16: X bf16 [M, K] (row stride ldx),
+// P[m][j0 + j] = sum_k X[m][k] F[j0 + j][k] for j < 16: X bf16 [M, K] (row stride ldx),
 // F FP32 [r, K] (row stride ldf), P FP32 [M, ldp] with ldp >= r rounded up to 16 (the ranks
-// past r get zeros).  A block of 4 waves takes
-// 16 rows (4 per wave); each step covers 512 columns (8 per lane): the F slab [16][512] is
-// staged in LDS in two planes of 4 columns so every lane's 16-byte reads are contiguous
-// across the wave.  After the K loop each lane holds 4 x 16 partial sums, which a
-// recursive-halving exchange (63 shuffles, fixed pairing) reduces so that lane l ends with
-// output l = (row l / 16, rank l % 16).  Grouped: a block's 16 rows come from one expert's
-// chunk and use F + e * fstride.
-constexpr int kRowsPerWave = 4;
-constexpr int kStepK = 512;
+// past r get zeros).  On v_mfma_f32_16x16x32_bf16: each FP32 factor value f is split into
+// bf16 hi = rn(f) and lo = rn(f - hi) (|f - hi - lo| <= 2^-18 |f|; f - hi is exact), and the
+// row block accumulates X hi + X lo in FP32 (X is bf16, exact as an MFMA operand).  A block of
+// 4 waves covers 16 rows x 16 ranks; wave w takes the 32-deep k steps w, w + 4, ..., each lane
+// loading its 8 consecutive k of one X row (A operand: row lane % 16, k 8 (lane / 16) + 0..7)
+// and of one F row (B operand: rank lane % 16).  The waves' 16 x 16 partials are added in wave
+// order through LDS, so the sums are deterministic.  Grouped: a block's 16 rows come from one
+// expert's chunk and use F + e * fstride.
+constexpr int kRowBlock = 16;
+constexpr int kDotUnroll = 4;                         // k steps in flight per wave
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// hi / lo bf16 halves of 8 FP32 values (round to nearest even; the inputs are finite factors).
+__device__ __forceinline__ void split_bf16x8(const float f[8], bf16x8_t& hi, bf16x8_t& lo) {
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    h[q] = bf16x2_rne_nonnan(f[2 * q], f[2 * q + 1]);
+    const float r0 = f[2 * q] - as_f32(h[q] << 16);
+    const float r1 = f[2 * q + 1] - as_f32(h[q] & 0xFFFF0000u);
+    l[q] = bf16x2_rne_nonnan(r0, r1);
+  }
+  hi = __builtin_bit_cast(bf16x8_t, make_uint4(h[0], h[1], h[2], h[3]));
+  lo = __builtin_bit_cast(bf16x8_t, make_uint4(l[0], l[1], l[2], l[3]));
+}
 
 __global__ __launch_bounds__(kThreads) void lora_rowdot_kernel(const uint16_t* __restrict__ X,
                                                                int64_t M, int64_t K, int64_t ldx,
@@ -240,78 +258,60 @@ __global__ __launch_bounds__(kThreads) void lora_rowdot_kernel(const uint16_t* _
                                                                float* __restrict__ P,
                                                                int64_t ldp, Groups g,
                                                                int64_t fstride) {
-  __shared__ float4 fs[kRC * 2 * 64];                 // [jj][plane][lane] x 4 columns
+  __shared__ f32x4_t red[4][64];
   const int t = threadIdx.x, lane = t & 63;
   const int wv = __builtin_amdgcn_readfirstlane(t >> 6);
-  const int j0 = blockIdx.y * kRC;
-  const int nj = r - j0 < kRC ? r - j0 : kRC;
-  int64_t m0 = (int64_t)blockIdx.x * (4 * kRowsPerWave) + wv * kRowsPerWave;
+  const int j0 = blockIdx.y * kRowBlock;
+  int64_t m0 = (int64_t)blockIdx.x * kRowBlock;
   if (g.off) {                                        // uniform over the block
     const int y = blockIdx.x;
     if (y >= g.pre[g.E]) return;
     const int e = find_group(g.pre, g.E, y);
-    m0 = g.off[e] + (int64_t)(y - g.pre[e]) * (4 * kRowsPerWave) + wv * kRowsPerWave;
+    m0 = g.off[e] + (int64_t)(y - g.pre[e]) * kRowBlock;
     M = g.off[e + 1];
     F += e * fstride;
   }
-  float acc[kRowsPerWave][kRC];
+  const int row = lane & 15, kq = (lane >> 4) * 8;
+  const bool rok = m0 + row < M, jok = j0 + row < r;  // A row / B rank of this lane
+  const uint16_t* xp = X + (rok ? m0 + row : m0) * ldx + kq;
+  const float* fp = F + (int64_t)(jok ? j0 + row : 0) * ldf + kq;
+  f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int64_t k0 = (int64_t)wv * 32; k0 < K; k0 += 4 * 32 * kDotUnroll) {
+    uint4 xa[kDotUnroll];
+    float4 fa[kDotUnroll][2];
 #pragma unroll
-  for (int i = 0; i < kRowsPerWave; ++i)
-#pragma unroll
-    for (int j = 0; j < kRC; ++j) acc[i][j] = 0.0f;
-
-  for (int64_t k0 = 0; k0 < K; k0 += kStepK) {
-    const int64_t kc = k0 + lane * 8;
-    uint4 xv[kRowsPerWave];
-#pragma unroll
-    for (int i = 0; i < kRowsPerWave; ++i) {
-      xv[i] = make_uint4(0, 0, 0, 0);
-      if (m0 + i < M && kc < K) xv[i] = *reinterpret_cast<const uint4*>(X + (m0 + i) * ldx + kc);
-    }
-    __syncthreads();                                  // previous slab fully read
-#pragma unroll
-    for (int q = 0; q < (kRC * 2 * 64) / kThreads; ++q) {
-      const int idx = t + q * kThreads;               // (jj, lane', plane) in global order
-      const int jj = idx >> 7, l = (idx >> 1) & 63, pl = idx & 1;
-      const int64_t kk = k0 + l * 8 + pl * 4;
-      float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-      if (jj < nj && kk < K) v = *reinterpret_cast<const float4*>(F + (int64_t)(j0 + jj) * ldf + kk);
-      fs[(jj * 2 + pl) * 64 + l] = v;
-    }
-    __syncthreads();
-    float xf[kRowsPerWave][8];
-#pragma unroll
-    for (int i = 0; i < kRowsPerWave; ++i) {
-      uint32_t h[8];
-      unpack8(xv[i], h);
-#pragma unroll
-      for (int k = 0; k < 8; ++k) xf[i][k] = as_f32(h[k] << 16);
+    for (int u = 0; u < kDotUnroll; ++u) {            // all loads first
+      const int64_t k = k0 + u * 4 * 32;
+      const bool kin = k + kq < K;                    // K % 8 == 0: a lane's 8 are all in or out
+      xa[u] = make_uint4(0, 0, 0, 0);
+      fa[u][0] = fa[u][1] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      if (kin && rok) xa[u] = *reinterpret_cast<const uint4*>(xp + k);
+      if (kin && jok) {
+        fa[u][0] = *reinterpret_cast<const float4*>(fp + k);
+        fa[u][1] = *reinterpret_cast<const float4*>(fp + k + 4);
+      }
     }
 #pragma unroll
-    for (int jj = 0; jj < kRC; ++jj) {
-      const float4 lo = fs[(jj * 2) * 64 + lane], hi = fs[(jj * 2 + 1) * 64 + lane];
-      const float f[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-#pragma unroll
-      for (int i = 0; i < kRowsPerWave; ++i)
-#pragma unroll
-        for (int k = 0; k < 8; ++k) acc[i][jj] = __builtin_fmaf(xf[i][k], f[k], acc[i][jj]);
+    for (int u = 0; u < kDotUnroll; ++u) {
+      const float f[8] = {fa[u][0].x, fa[u][0].y, fa[u][0].z, fa[u][0].w,
+                          fa[u][1].x, fa[u][1].y, fa[u][1].z, fa[u][1].w};
+      bf16x8_t hi, lo;
+      split_bf16x8(f, hi, lo);
+      const bf16x8_t a = __builtin_bit_cast(bf16x8_t, xa[u]);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, hi, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, lo, acc, 0, 0, 0);
     }
   }
-  // recursive halving over the 64 lanes: value index v = 16 i + jj
-  float* v = &acc[0][0];
+  red[wv][lane] = acc;
+  __syncthreads();
+  if (wv != 0) return;
+  const f32x4_t s = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
+  // D[i][j]: lane holds rows 4 (lane / 16) + v, rank lane % 16
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) {
-    const bool upper = (lane & o) != 0;
-#pragma unroll
-    for (int q = 0; q < o; ++q) {
-      const float send = upper ? v[q] : v[q + o];
-      const float keep = upper ? v[q + o] : v[q];
-      v[q] = keep + __shfl_xor(send, o, 64);
-    }
+  for (int v = 0; v < 4; ++v) {
+    const int64_t m = m0 + 4 * (lane >> 4) + v;
+    if (m < M) P[m * ldp + j0 + (lane & 15)] = s[v];   // ranks past r: zeros (F rows read as 0)
   }
-  const int64_t m = m0 + (lane >> 4);
-  const int jj = lane & 15;
-  if (m < M) P[m * ldp + j0 + jj] = v[0];          // ranks past r: zeros (F rows read as 0)
 }
 
 // ======================================================================== column sums
@@ -504,9 +504,9 @@ hipError_t launch_lora_rowdot(const uint16_t* X, int64_t M, int64_t K, int64_t l
                               int64_t ldf, int64_t r, float* P, int64_t ldp, const int64_t* off,
                               const int* pre, int64_t E, int64_t fstride, hipStream_t s) {
   if (M == 0 || r == 0) return hipSuccess;
-  constexpr int64_t rows = 4 * kRowsPerWave;
+  constexpr int64_t rows = kRowBlock;
   const int64_t blocks = off ? M / rows + E : (M + rows - 1) / rows;
-  const dim3 grid((unsigned)blocks, (unsigned)((r + kRC - 1) / kRC));
+  const dim3 grid((unsigned)blocks, (unsigned)((r + kRowBlock - 1) / kRowBlock));
   hipLaunchKernelGGL(lora_rowdot_kernel, grid, dim3(kThreads), 0, s, X, M, K, ldx, F, ldf, (int)r,
                      P, ldp, Groups{off, pre, (int)E}, fstride);
   return hipGetLastError();
