@@ -315,14 +315,31 @@ __global__ __launch_bounds__(kThreads) void lora_rowdot_kernel(const uint16_t* _
 }
 
 // ======================================================================== column sums
-// part[s][j0 + jj][c] = sum over rows m of split s of Big[m][c] Sm[m][j0 + jj], jj < 16:
-// Big bf16 [M, C] (row stride ldb), Sm FP32 [M, lds_].  A block covers 256 columns (4 per
-// lane) of one row split; each of its 4 waves takes every fourth group of 4 rows (4 loads in
-// flight per lane), and the waves' partials are added in wave order through LDS, 8 ranks at a
-// time.  part is [splits][r][C] FP32.  Sm's row stride is a multiple of 16 with zeros past
-// rank r (as the row-dot writes it), so a rank pass reads 16 values unconditionally.
-// Grouped: split y is chunk y - pre[e] (rows_per_split rows) of expert e.
-constexpr int kColRows = 4;
+// part[s][j0 + j][c] = sum over rows m of split s of Big[m][c] Sm[m][j0 + j], j < 16:
+// Big bf16 [M, C] (row stride ldb), Sm FP32 [M, lds_] (row stride a multiple of 16, zeros
+// past rank r, as the row-dot writes it).  On v_mfma_f32_16x16x32_bf16 as D[j][c] =
+// sum_m Sm^T[j][m] Big[m][c], with Sm split into bf16 hi + lo like the row-dot's factor.  A
+// block covers 256 columns of one row split and one 16-rank block; per 32-row step it stages
+// the Big tile [32][256] (row pitch 544 bytes) and Sm^T [16][32] in LDS (double-buffered, the
+// next step's global loads in flight while the current one computes).  Wave w owns columns
+// 64 w .. 64 w + 63 as four 16-column MFMA blocks: the A operand (rank lane % 16, rows
+// 8 (lane / 16) + 0..7) is read from Sm^T, the B operand (column lane % 16, the same rows)
+// with two ds_read_b64_tr_b16 per block.  Waves own disjoint columns, so no cross-wave sum.
+// part is [splits][r][C] FP32.  Grouped: split y is chunk y - pre[e] (rows_per_split rows)
+// of expert e.
+constexpr int kColTile = 256;                         // columns per block
+constexpr int kColStep = 32;                          // rows per step
+constexpr int kColPitch = kColTile * 2 + 32;          // Big tile row pitch in LDS (bytes)
+
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+typedef short v8i16_t __attribute__((ext_vector_type(8)));
+
+// ds_read_b64_tr_b16: within each group of 16 lanes, source lane 4 j + a gives the address of
+// row kb + j, columns c0 + 4 a .. + 3; output lane L receives rows kb .. kb + 3 of column c0 + L.
+__device__ __forceinline__ v4i16_t lds_tr16(const char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) v4i16_t*)(__attribute__((address_space(3))) char*)(p));
+}
 
 __global__ __launch_bounds__(kThreads) void lora_colsum_kernel(const uint16_t* __restrict__ Big,
                                                                int64_t M, int64_t C, int64_t ldb,
@@ -331,15 +348,14 @@ __global__ __launch_bounds__(kThreads) void lora_colsum_kernel(const uint16_t* _
                                                                int64_t rows_per_split,
                                                                float* __restrict__ part,
                                                                Groups g) {
-  __shared__ float4 red[4 * 8 * 64];                  // [wave][rank of the half][lane] x 4 cols
+  __shared__ __attribute__((aligned(16))) char tile[2][kColStep * kColPitch];
+  __shared__ __attribute__((aligned(16))) float smt[2][kRC * kColStep];   // [j][m]
   const int t = threadIdx.x, lane = t & 63;
   const int wv = __builtin_amdgcn_readfirstlane(t >> 6);
   const int j0 = blockIdx.z * kRC;
   const int nj = r - j0 < kRC ? r - j0 : kRC;
   const int64_t s = blockIdx.y;
-  const int64_t cb = (int64_t)blockIdx.x * 256;
-  const int64_t c = cb + lane * 4;
-  const bool c_ok = c < C;
+  const int64_t cb = (int64_t)blockIdx.x * kColTile;
   int64_t mb = s * rows_per_split, end = M;
   if (g.off) {                                        // uniform over the block
     if (s >= g.pre[g.E]) return;
@@ -348,54 +364,85 @@ __global__ __launch_bounds__(kThreads) void lora_colsum_kernel(const uint16_t* _
     end = g.off[e + 1];
   }
   const int64_t me = mb + rows_per_split < end ? mb + rows_per_split : end;
-  float acc[4][kRC];
+  // staging: thread t loads Big rows t / 32 + 8 q (q < 4), 16-byte chunk t % 32, and Sm row
+  // t / 8, ranks 2 (t % 8) + {0, 1}
+  const int srow = t >> 5, schunk = t & 31;
+  const int64_t scol = cb + schunk * 8;
+  const bool scol_ok = scol < C;                      // C % 4 == 0, chunks of 8 may be partial
+  const int mrow = t >> 3, mj = 2 * (t & 7);
+  uint4 bv[4];
+  float2 sv;
+  auto load = [&](int64_t m0) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < kRC; ++j) acc[i][j] = 0.0f;
-  for (int64_t m0 = mb + wv * kColRows; m0 < me; m0 += 4 * kColRows) {
-    uint2 bv[kColRows];
-#pragma unroll
-    for (int q = 0; q < kColRows; ++q) {
-      bv[q] = make_uint2(0, 0);
-      if (c_ok && m0 + q < me) bv[q] = *reinterpret_cast<const uint2*>(Big + (m0 + q) * ldb + c);
-    }
-#pragma unroll
-    for (int q = 0; q < kColRows; ++q) {
-      if (m0 + q >= me) break;                        // uniform over the wave
-      const float x[4] = {as_f32(bv[q].x << 16), as_f32(bv[q].x & 0xFFFF0000u),
-                          as_f32(bv[q].y << 16), as_f32(bv[q].y & 0xFFFF0000u)};
-      const float4* sm = reinterpret_cast<const float4*>(Sm + (m0 + q) * lds_ + j0);
-      float sv[kRC];
-#pragma unroll
-      for (int u = 0; u < kRC / 4; ++u) {
-        const float4 f = sm[u];
-        sv[4 * u] = f.x; sv[4 * u + 1] = f.y; sv[4 * u + 2] = f.z; sv[4 * u + 3] = f.w;
+    for (int q = 0; q < 4; ++q) {
+      const int64_t m = m0 + srow + 8 * q;
+      bv[q] = make_uint4(0, 0, 0, 0);
+      if (m < me) {
+        if (scol + 8 <= C) {
+          bv[q] = *reinterpret_cast<const uint4*>(Big + m * ldb + scol);
+        } else if (scol_ok) {                         // 4 valid columns
+          const uint2 h = *reinterpret_cast<const uint2*>(Big + m * ldb + scol);
+          bv[q] = make_uint4(h.x, h.y, 0, 0);
+        }
       }
+    }
+    sv = make_float2(0.0f, 0.0f);
+    if (m0 + mrow < me) sv = *reinterpret_cast<const float2*>(Sm + (m0 + mrow) * lds_ + j0 + mj);
+  };
+  auto store = [&](int b) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+    for (int q = 0; q < 4; ++q)
+      *reinterpret_cast<uint4*>(tile[b] + (srow + 8 * q) * kColPitch + schunk * 16) = bv[q];
+    smt[b][mj * kColStep + mrow] = sv.x;
+    smt[b][(mj + 1) * kColStep + mrow] = sv.y;
+  };
+  // fragment addresses: A from Sm^T row lane % 16, columns 8 (lane / 16) + 0..7; B per
+  // column block cb4: rows 8 (lane / 16) + 4 h + (lane % 16) / 4, columns 16 cb4 + 4 (lane % 4)
+  const int grp = lane >> 4, lj = (lane & 15) >> 2, la = lane & 3;
+  const int a_off = (lane & 15) * kColStep + 8 * grp;
+  const int b_off = (8 * grp + lj) * kColPitch + (wv * 64 + 4 * la) * 2;
+  f32x4_t acc[4];
 #pragma unroll
-        for (int j = 0; j < kRC; ++j) acc[i][j] = __builtin_fmaf(x[i], sv[j], acc[i][j]);
+  for (int i = 0; i < 4; ++i) acc[i] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+  if (mb < me) {
+    load(mb);
+    store(0);
+    __syncthreads();
+    int b = 0;
+    for (int64_t m0 = mb; m0 < me; m0 += kColStep) {
+      const bool more = m0 + kColStep < me;           // uniform
+      if (more) load(m0 + kColStep);
+      const float4 a0 = *reinterpret_cast<const float4*>(&smt[b][a_off]);
+      const float4 a1 = *reinterpret_cast<const float4*>(&smt[b][a_off + 4]);
+      const float f[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+      bf16x8_t hi, lo;
+      split_bf16x8(f, hi, lo);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const char* p = tile[b] + b_off + i * 32;
+        const v4i16_t r0 = lds_tr16(p);
+        const v4i16_t r1 = lds_tr16(p + 4 * kColPitch);
+        const v8i16_t v = __builtin_shufflevector(r0, r1, 0, 1, 2, 3, 4, 5, 6, 7);
+        const bf16x8_t bb = __builtin_bit_cast(bf16x8_t, v);
+        acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, bb, acc[i], 0, 0, 0);
+        acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, bb, acc[i], 0, 0, 0);
+      }
+      if (more) {
+        store(b ^ 1);
+        __syncthreads();                              // next tile published
+        b ^= 1;
+      }
     }
   }
-  // wave partials -> LDS (4 columns per lane as one 16-byte write), then thread t sums column
-  // cb + t over the waves in order, 8 ranks per half
+  // D[j][c]: lane holds ranks 4 (lane / 16) + v of column lane % 16 of each block
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    if (h) __syncthreads();
+  for (int i = 0; i < 4; ++i) {
+    const int64_t c = cb + wv * 64 + i * 16 + (lane & 15);
+    if (c >= C) continue;
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
-      red[(wv * 8 + j) * 64 + lane] =
-          make_float4(acc[0][8 * h + j], acc[1][8 * h + j], acc[2][8 * h + j], acc[3][8 * h + j]);
-    __syncthreads();
-    const float* rf = reinterpret_cast<const float*>(red);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int jj = 8 * h + j;
-      float v = rf[(0 * 8 + j) * 256 + t];
-#pragma unroll
-      for (int w = 1; w < 4; ++w) v += rf[(w * 8 + j) * 256 + t];
-      if (jj < nj && cb + t < C) part[(s * r + j0 + jj) * C + cb + t] = v;
+    for (int v = 0; v < 4; ++v) {
+      const int jj = 4 * grp + v;
+      if (jj < nj) part[(s * r + j0 + jj) * C + c] = acc[i][v];
     }
   }
 }
@@ -415,8 +462,18 @@ __global__ void lora_finish_kernel(const float* __restrict__ part, int64_t split
     s1 = per_group ? g.pre[e + 1] : g.pre[g.E];
     out += (int64_t)e * C * r;
   }
+  // splits added in order; eight loads in flight per batch
+  const int64_t stride = C * r;
   float acc = 0.0f;
-  for (int64_t s = s0; s < s1; ++s) acc += part[s * C * r + idx];
+  int64_t s = s0;
+  for (; s + 8 <= s1; s += 8) {
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = part[(s + i) * stride + idx];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc += v[i];
+  }
+  for (; s < s1; ++s) acc += part[s * stride + idx];
   const float v = scale * acc;
   const int64_t j = idx / C, c = idx % C;
   if (transposed) out[idx] = v;
