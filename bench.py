@@ -42,6 +42,10 @@ def parse():
                    help="token rows in the CPU oracle's bounded sample of the step")
     p.add_argument("--main-only", action="store_true",
                    help="time only the MXFP4 MLP up-projection step (used for counter runs)")
+    p.add_argument("--rows", default=None,
+                   help="run only these secondary row groups (comma-separated: quant, dense, moe, "
+                        "lora, moe_lora, kl, q4k) and print them as one JSON object; no step timing "
+                        "(used for per-row kernel traces)")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain 1 GiB device-to-device copy (reference for the "
                         "HBM byte counters) and exit")
@@ -93,6 +97,10 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     qf.lib()
+    if args.rows:
+        print(json.dumps({"rows": other_rows(qf, torch, dev, set(args.rows.split(",")))}),
+              flush=True)
+        return
     w = workloads.mlp_up(seed=0)
     M, N, K = w["M"], w["N"], w["K"]
 
@@ -260,176 +268,187 @@ def _randn_bf16(torch, gen, shape, std=1.0, col_scale=None, row_scale=None):
     return z.to(torch.bfloat16)
 
 
-def other_rows(qf, torch, dev):
+def other_rows(qf, torch, dev, only=None):
     """Throughput of the remaining hot-path steps on their own workloads (seeded synthetic
     data drawn on the GPU): every quantizer and the amax pass over W-shaped tensors through
     rotating buffers, the transpose, the 9B-class dense layer at 32K tokens (NVFP4 weights,
     tied QKV and gate/up scales), the 128-expert grouped layer (NVFP4 weights, Zipf(1.1)
     top-8 routing), the LoRA-QAD layer (rank-16 adapter on the MLP up-projection) and the
     Q4_K export packing + forward GEMM."""
+    def want(name):
+        return only is None or name in only
+
     import workloads
     gen = torch.Generator(device="cuda")
     gen.manual_seed(0)
     out = {}
     N, K = 14336, 4096
-    nbuf = 10
-    bufs = [_randn_bf16(torch, gen, (N, K), 0.02) for _ in range(nbuf)]
-    codes = torch.empty(N, K // 2, dtype=torch.uint8, device=dev)
-    sc16 = torch.empty(N, K // 16, dtype=torch.uint8, device=dev)
-    sc32 = torch.empty(N, K // 32, dtype=torch.uint8, device=dev)
-    packed = torch.empty(N, K // 256, 144, dtype=torch.uint8, device=dev)
-    xh = torch.empty(N, K, dtype=torch.int16, device=dev)
-    amax = torch.zeros(1, dtype=torch.float32, device=dev)
-    s_out = torch.zeros(1, dtype=torch.float32, device=dev)
-    tr = torch.empty(K, N, dtype=torch.int16, device=dev)
-    it = [0]
+    if want("quant"):
+        nbuf = 10
+        bufs = [_randn_bf16(torch, gen, (N, K), 0.02) for _ in range(nbuf)]
+        codes = torch.empty(N, K // 2, dtype=torch.uint8, device=dev)
+        sc16 = torch.empty(N, K // 16, dtype=torch.uint8, device=dev)
+        sc32 = torch.empty(N, K // 32, dtype=torch.uint8, device=dev)
+        packed = torch.empty(N, K // 256, 144, dtype=torch.uint8, device=dev)
+        xh = torch.empty(N, K, dtype=torch.int16, device=dev)
+        amax = torch.zeros(1, dtype=torch.float32, device=dev)
+        s_out = torch.zeros(1, dtype=torch.float32, device=dev)
+        tr = torch.empty(K, N, dtype=torch.int16, device=dev)
+        it = [0]
 
-    def nxt():
-        it[0] += 1
-        return bufs[it[0] % nbuf]
+        def nxt():
+            it[0] += 1
+            return bufs[it[0] % nbuf]
 
-    def gbps(fn, bpe):
-        ms = _time(torch, fn, reps=3 * nbuf)
-        g = N * K * bpe / (ms * 1e-3) / 1e9
-        return {"us": round(ms * 1e3, 2), "GBps": round(g, 1), "frac_hbm": round(g / PEAK_HBM_GBPS, 4),
-                "bytes_per_elem": bpe}
+        def gbps(fn, bpe):
+            ms = _time(torch, fn, reps=3 * nbuf)
+            g = N * K * bpe / (ms * 1e-3) / 1e9
+            return {"us": round(ms * 1e3, 2), "GBps": round(g, 1), "frac_hbm": round(g / PEAK_HBM_GBPS, 4),
+                    "bytes_per_elem": bpe}
 
-    out["a1_amax"] = gbps(lambda: qf.amax(nxt(), amax), 2.0)
-    out["nvfp4_amax_computed"] = gbps(
-        lambda: qf.fakequant_nvfp4(nxt(), amax, qf.AMAX_COMPUTE, s_out, codes, sc16, xh), 4.5625)
-    out["nvfp4_amax_given"] = gbps(
-        lambda: qf.fakequant_nvfp4(nxt(), amax, qf.AMAX_GIVEN, s_out, codes, sc16, xh), 4.5625)
-    out["mxfp4"] = gbps(lambda: qf.fakequant_mxfp4(nxt(), codes, sc32, xh), 4.53125)
-    out["mxfp4_xhat_only"] = gbps(lambda: qf.fakequant_mxfp4(nxt(), None, None, xh), 4.0)
-    out["q4k_pack"] = gbps(lambda: qf.fakequant_q4k(nxt(), packed, xh), 4.5625)
-    out["transpose"] = gbps(lambda: qf.transpose_bf16(nxt(), tr), 4.0)
-    for k in list(out):
-        out[k]["tensor"] = f"{N}x{K}"
-    del bufs, codes, sc16, sc32, packed, xh, tr
+        out["a1_amax"] = gbps(lambda: qf.amax(nxt(), amax), 2.0)
+        out["nvfp4_amax_computed"] = gbps(
+            lambda: qf.fakequant_nvfp4(nxt(), amax, qf.AMAX_COMPUTE, s_out, codes, sc16, xh), 4.5625)
+        out["nvfp4_amax_given"] = gbps(
+            lambda: qf.fakequant_nvfp4(nxt(), amax, qf.AMAX_GIVEN, s_out, codes, sc16, xh), 4.5625)
+        out["mxfp4"] = gbps(lambda: qf.fakequant_mxfp4(nxt(), codes, sc32, xh), 4.53125)
+        out["mxfp4_xhat_only"] = gbps(lambda: qf.fakequant_mxfp4(nxt(), None, None, xh), 4.0)
+        out["q4k_pack"] = gbps(lambda: qf.fakequant_q4k(nxt(), packed, xh), 4.5625)
+        out["transpose"] = gbps(lambda: qf.transpose_bf16(nxt(), tr), 4.0)
+        for k in list(out):
+            out[k]["tensor"] = f"{N}x{K}"
+        del bufs, codes, sc16, sc32, packed, xh, tr
 
-    # ---- 9B-class dense layer at 32K tokens: QKV, O, gate/up, down (NVFP4 weights) ---------
-    T = 32768
-    layer = []
-    flops = 0.0
-    for name, n, k in workloads.DENSE_LINEARS:
-        tau = torch.from_numpy(np.abs(np.random.default_rng(k).standard_t(3.0, size=k))
-                               .astype(np.float32)).to(dev)
-        Xl = _randn_bf16(torch, gen, (T, k), col_scale=tau)
-        Wl = _randn_bf16(torch, gen, (n, k), 0.02)
-        dYl = _randn_bf16(torch, gen, (T, n))
-        d = qf.qlinear_desc(T, n, k, "nvfp4", "none")
-        layer.append((d, Xl, Wl, dYl, torch.empty(T, n, dtype=torch.bfloat16, device=dev),
-                      torch.empty(T, k, dtype=torch.bfloat16, device=dev),
-                      torch.empty(n, k, dtype=torch.float32, device=dev), qf.workspace(d)))
-        flops += 3 * 2.0 * T * n * k
+    if want("dense"):
+        # ---- 9B-class dense layer at 32K tokens: QKV, O, gate/up, down (NVFP4 weights) ---------
+        T = 32768
+        layer = []
+        flops = 0.0
+        for name, n, k in workloads.DENSE_LINEARS:
+            tau = torch.from_numpy(np.abs(np.random.default_rng(k).standard_t(3.0, size=k))
+                                   .astype(np.float32)).to(dev)
+            Xl = _randn_bf16(torch, gen, (T, k), col_scale=tau)
+            Wl = _randn_bf16(torch, gen, (n, k), 0.02)
+            dYl = _randn_bf16(torch, gen, (T, n))
+            d = qf.qlinear_desc(T, n, k, "nvfp4", "none")
+            layer.append((d, Xl, Wl, dYl, torch.empty(T, n, dtype=torch.bfloat16, device=dev),
+                          torch.empty(T, k, dtype=torch.bfloat16, device=dev),
+                          torch.empty(n, k, dtype=torch.float32, device=dev), qf.workspace(d)))
+            flops += 3 * 2.0 * T * n * k
 
-    def dense_step():
-        for d, Xl, Wl, dYl, Yl, dXl, dWl, ws in layer:
-            qf.qlinear_fwd(d, Xl, Wl, Yl, ws)
-            qf.qlinear_bwd_ste(d, dYl, Xl, Wl, dXl, dWl, ws)
+        def dense_step():
+            for d, Xl, Wl, dYl, Yl, dXl, dWl, ws in layer:
+                qf.qlinear_fwd(d, Xl, Wl, Yl, ws)
+                qf.qlinear_bwd_ste(d, dYl, Xl, Wl, dXl, dWl, ws)
 
-    ms = _time(torch, dense_step, reps=3, warm=1)
-    out["dense_layer_32k_nvfp4"] = {"ms": round(ms, 3), "TFLOPs": round(flops / (ms * 1e-3) / 1e12, 1),
-                                    "work": "T=32768, QKV 6144, O 4096, gate/up 24576, down 4096x12288, fwd + STE bwd"}
-    del layer
-    torch.cuda.empty_cache()
+        ms = _time(torch, dense_step, reps=3, warm=1)
+        out["dense_layer_32k_nvfp4"] = {"ms": round(ms, 3), "TFLOPs": round(flops / (ms * 1e-3) / 1e12, 1),
+                                        "work": "T=32768, QKV 6144, O 4096, gate/up 24576, down 4096x12288, fwd + STE bwd"}
+        del layer
+        torch.cuda.empty_cache()
 
-    # ---- 128-expert grouped layer, Zipf(1.1) top-8 routing of 32768 tokens -------------------
-    _, offsets = workloads.moe_routing(seed=0, tokens=32768, experts=128, topk=8)
-    E, Tm, H, I = 128, int(offsets[-1]), 3072, 1536
-    off = torch.from_numpy(offsets).to(dev)
-    gflops = 0.0
-    glayers = []
-    for n, k in ((2 * I, H), (H, I)):
-        Xg = _randn_bf16(torch, gen, (Tm, k))
-        Wg = _randn_bf16(torch, gen, (E * n, k), 0.02)
-        dYg = _randn_bf16(torch, gen, (Tm, n))
-        d = qf.grouped_desc(E, Tm, n, k, "nvfp4", "none")
-        glayers.append((d, Xg, Wg, dYg, torch.empty(Tm, n, dtype=torch.bfloat16, device=dev),
-                        torch.empty(Tm, k, dtype=torch.bfloat16, device=dev),
-                        torch.empty(E, n, k, dtype=torch.float32, device=dev), qf.grouped_workspace(d)))
-        gflops += 3 * 2.0 * Tm * n * k
+    if want("moe"):
+        # ---- 128-expert grouped layer, Zipf(1.1) top-8 routing of 32768 tokens -------------------
+        _, offsets = workloads.moe_routing(seed=0, tokens=32768, experts=128, topk=8)
+        E, Tm, H, I = 128, int(offsets[-1]), 3072, 1536
+        off = torch.from_numpy(offsets).to(dev)
+        gflops = 0.0
+        glayers = []
+        for n, k in ((2 * I, H), (H, I)):
+            Xg = _randn_bf16(torch, gen, (Tm, k))
+            Wg = _randn_bf16(torch, gen, (E * n, k), 0.02)
+            dYg = _randn_bf16(torch, gen, (Tm, n))
+            d = qf.grouped_desc(E, Tm, n, k, "nvfp4", "none")
+            glayers.append((d, Xg, Wg, dYg, torch.empty(Tm, n, dtype=torch.bfloat16, device=dev),
+                            torch.empty(Tm, k, dtype=torch.bfloat16, device=dev),
+                            torch.empty(E, n, k, dtype=torch.float32, device=dev), qf.grouped_workspace(d)))
+            gflops += 3 * 2.0 * Tm * n * k
 
-    def moe_step():
-        for d, Xg, Wg, dYg, Yg, dXg, dWg, ws in glayers:
-            qf.qlinear_grouped_fwd(d, off, Xg, Wg, Yg, ws)
-            qf.qlinear_grouped_bwd_ste(d, off, dYg, Xg, Wg, dXg, dWg, ws)
+        def moe_step():
+            for d, Xg, Wg, dYg, Yg, dXg, dWg, ws in glayers:
+                qf.qlinear_grouped_fwd(d, off, Xg, Wg, Yg, ws)
+                qf.qlinear_grouped_bwd_ste(d, off, dYg, Xg, Wg, dXg, dWg, ws)
 
-    ms = _time(torch, moe_step, reps=3, warm=1)
-    cnt = np.diff(offsets)
-    out["moe_grouped_nvfp4"] = {"ms": round(ms, 3), "TFLOPs": round(gflops / (ms * 1e-3) / 1e12, 1),
-                                "work": f"128 experts, {Tm} routed rows (per expert {cnt.min()}..{cnt.max()}), "
-                                        "gate/up 3072->3072 + down 1536->3072, fwd + STE bwd"}
-    del glayers
-    torch.cuda.empty_cache()
+        ms = _time(torch, moe_step, reps=3, warm=1)
+        cnt = np.diff(offsets)
+        out["moe_grouped_nvfp4"] = {"ms": round(ms, 3), "TFLOPs": round(gflops / (ms * 1e-3) / 1e12, 1),
+                                    "work": f"128 experts, {Tm} routed rows (per expert {cnt.min()}..{cnt.max()}), "
+                                            "gate/up 3072->3072 + down 1536->3072, fwd + STE bwd"}
+        del glayers
+        torch.cuda.empty_cache()
 
-    # ---- LoRA-QAD: the MXFP4 W4A4 MLP up-projection with a rank-16 adapter -------------------
-    out["lora_mlp_up_r16"] = lora_row(qf, torch, dev, gen)
+    if want("lora"):
+        # ---- LoRA-QAD: the MXFP4 W4A4 MLP up-projection with a rank-16 adapter -------------------
+        out["lora_mlp_up_r16"] = lora_row(qf, torch, dev, gen)
 
-    # ---- MoE LoRA-QAD: the same 128 experts with rank-16 adapters in the hybrid layout ------
-    _, offsets = workloads.moe_routing(seed=0, tokens=32768, experts=128, topk=8)
-    off = torch.from_numpy(offsets).to(dev)
-    r = 16
-    glayers = []
-    for n, k, shared in ((2 * I, H, "A"), (H, I, "B")):
-        Xg = _randn_bf16(torch, gen, (Tm, k))
-        Wg = _randn_bf16(torch, gen, (E * n, k), 0.02)
-        dYg = _randn_bf16(torch, gen, (Tm, n))
-        Ag = torch.randn((r, k) if shared == "A" else (E, r, k), generator=gen, device=dev) / np.sqrt(k)
-        Bg = torch.randn((n, r) if shared == "B" else (E, n, r), generator=gen, device=dev) * (0.001 * np.sqrt(k / r))
-        lo = qf.lora(Ag.contiguous(), Bg.contiguous(), 2.0, a_shared=shared == "A",
-                     b_shared=shared == "B")
-        d = qf.grouped_desc(E, Tm, n, k, "nvfp4", "none")
-        glayers.append((d, lo, Xg, Wg, dYg, torch.empty(Tm, n, dtype=torch.bfloat16, device=dev),
-                        torch.empty(Tm, k, dtype=torch.bfloat16, device=dev),
-                        torch.empty_like(Ag), torch.empty_like(Bg), qf.grouped_lora_workspace(d, lo)))
+    if want("moe_lora"):
+        # ---- MoE LoRA-QAD: the same 128 experts with rank-16 adapters in the hybrid layout ------
+        _, offsets = workloads.moe_routing(seed=0, tokens=32768, experts=128, topk=8)
+        E, Tm, H, I = 128, int(offsets[-1]), 3072, 1536
+        off = torch.from_numpy(offsets).to(dev)
+        r = 16
+        glayers = []
+        for n, k, shared in ((2 * I, H, "A"), (H, I, "B")):
+            Xg = _randn_bf16(torch, gen, (Tm, k))
+            Wg = _randn_bf16(torch, gen, (E * n, k), 0.02)
+            dYg = _randn_bf16(torch, gen, (Tm, n))
+            Ag = torch.randn((r, k) if shared == "A" else (E, r, k), generator=gen, device=dev) / np.sqrt(k)
+            Bg = torch.randn((n, r) if shared == "B" else (E, n, r), generator=gen, device=dev) * (0.001 * np.sqrt(k / r))
+            lo = qf.lora(Ag.contiguous(), Bg.contiguous(), 2.0, a_shared=shared == "A",
+                         b_shared=shared == "B")
+            d = qf.grouped_desc(E, Tm, n, k, "nvfp4", "none")
+            glayers.append((d, lo, Xg, Wg, dYg, torch.empty(Tm, n, dtype=torch.bfloat16, device=dev),
+                            torch.empty(Tm, k, dtype=torch.bfloat16, device=dev),
+                            torch.empty_like(Ag), torch.empty_like(Bg), qf.grouped_lora_workspace(d, lo)))
 
-    def moe_lora_step():
-        for d, lo, Xg, Wg, dYg, Yg, dXg, dAg, dBg, ws in glayers:
-            qf.qlinear_grouped_lora_fwd(d, lo, off, Xg, Wg, Yg, ws)
-            qf.qlinear_grouped_lora_bwd_ste(d, lo, off, dYg, Xg, Wg, dXg, dAg, dBg, ws)
+        def moe_lora_step():
+            for d, lo, Xg, Wg, dYg, Yg, dXg, dAg, dBg, ws in glayers:
+                qf.qlinear_grouped_lora_fwd(d, lo, off, Xg, Wg, Yg, ws)
+                qf.qlinear_grouped_lora_bwd_ste(d, lo, off, dYg, Xg, Wg, dXg, dAg, dBg, ws)
 
-    ms = _time(torch, moe_lora_step, reps=3, warm=1)
-    gf = 2 * 2.0 * Tm * (2 * I * H + H * I)
-    out["moe_lora_nvfp4_r16"] = {"ms": round(ms, 3), "TFLOPs": round(gf / (ms * 1e-3) / 1e12, 1),
-                                 "work": "the 128-expert layer above with frozen expert weights and "
-                                         "rank-16 adapters (gate/up: A shared, down: B shared), fwd + "
-                                         "STE bwd (dX, dA, dB); TFLOPs counts fwd + dX GEMMs"}
-    del glayers
-    torch.cuda.empty_cache()
+        ms = _time(torch, moe_lora_step, reps=3, warm=1)
+        gf = 2 * 2.0 * Tm * (2 * I * H + H * I)
+        out["moe_lora_nvfp4_r16"] = {"ms": round(ms, 3), "TFLOPs": round(gf / (ms * 1e-3) / 1e12, 1),
+                                     "work": "the 128-expert layer above with frozen expert weights and "
+                                             "rank-16 adapters (gate/up: A shared, down: B shared), fwd + "
+                                             "STE bwd (dX, dA, dB); TFLOPs counts fwd + dX GEMMs"}
+        del glayers
+        torch.cuda.empty_cache()
 
-    # ---- QAD distillation loss: 8192 tokens over a 151936-token vocabulary ------------------
-    out["qad_kl_8k_v152k"] = kl_row(qf, torch, dev, gen)
+    if want("kl"):
+        # ---- QAD distillation loss: 8192 tokens over a 151936-token vocabulary ------------------
+        out["qad_kl_8k_v152k"] = kl_row(qf, torch, dev, gen)
 
-    # ---- Q4_K export: quantize + pack W [14336, 4096], then the forward GEMM at M = 4096 ----
-    Wq = _randn_bf16(torch, gen, (N, K), 0.02, row_scale=torch.exp(0.5 * torch.randn(N, generator=gen, device=dev)))
-    Xq = _randn_bf16(torch, gen, (4096, K))
-    d = qf.qlinear_desc(4096, N, K, "q4k", "none")
-    ws = qf.workspace(d)
-    Yq = torch.empty(4096, N, dtype=torch.bfloat16, device=dev)
-    packed = torch.empty(N, K // 256, 144, dtype=torch.uint8, device=dev)
-    ms_pack = _time(torch, lambda: qf.fakequant_q4k(Wq, packed, None), reps=10)
-    ms_fwd = _time(torch, lambda: qf.qlinear_fwd(d, Xq, Wq, Yq, ws), reps=10)
-    xm = torch.empty(N, K, dtype=torch.bfloat16, device=dev)
-    x0 = torch.empty(N, K, dtype=torch.bfloat16, device=dev)
-    ms_mse = _time(torch, lambda: qf.fakequant_q4k_mse(Wq, packed, xm), reps=5)
-    qf.fakequant_q4k(Wq, None, x0)
-    torch.cuda.synchronize()
-    wf = Wq.float()
-    ratio = float(((wf - xm.float()) ** 2).sum() / ((wf - x0.float()) ** 2).sum())
-    out["q4k_mse_search"] = {
-        "us": round(ms_mse * 1e3, 1),
-        "GBps": round(N * K * (2 + 2 + 144 / 256) / (ms_mse * 1e-3) / 1e9, 1),
-        "sq_error_vs_min_max": round(ratio, 4),
-        "work": "W 14336x4096 (per-row log-normal scale) -> 144-byte blocks + x_hat with the "
-                "searched sub-block steps (17 candidates, least-squares refit); ALU-bound"}
-    del xm, x0, wf
-    out["q4k_export_and_forward"] = {
-        "pack_us": round(ms_pack * 1e3, 2),
-        "pack_GBps": round(N * K * (2 + 144 / 256) / (ms_pack * 1e-3) / 1e9, 1),
-        "forward_ms": round(ms_fwd, 4),
-        "forward_TFLOPs": round(2.0 * 4096 * N * K / (ms_fwd * 1e-3) / 1e12, 1),
-        "work": "W 14336x4096 (per-row log-normal scale) -> 144-byte blocks; Y = X Q(W)^T, X 4096x4096"}
+    if want("q4k"):
+        # ---- Q4_K export: quantize + pack W [14336, 4096], then the forward GEMM at M = 4096 ----
+        Wq = _randn_bf16(torch, gen, (N, K), 0.02, row_scale=torch.exp(0.5 * torch.randn(N, generator=gen, device=dev)))
+        Xq = _randn_bf16(torch, gen, (4096, K))
+        d = qf.qlinear_desc(4096, N, K, "q4k", "none")
+        ws = qf.workspace(d)
+        Yq = torch.empty(4096, N, dtype=torch.bfloat16, device=dev)
+        packed = torch.empty(N, K // 256, 144, dtype=torch.uint8, device=dev)
+        ms_pack = _time(torch, lambda: qf.fakequant_q4k(Wq, packed, None), reps=10)
+        ms_fwd = _time(torch, lambda: qf.qlinear_fwd(d, Xq, Wq, Yq, ws), reps=10)
+        xm = torch.empty(N, K, dtype=torch.bfloat16, device=dev)
+        x0 = torch.empty(N, K, dtype=torch.bfloat16, device=dev)
+        ms_mse = _time(torch, lambda: qf.fakequant_q4k_mse(Wq, packed, xm), reps=5)
+        qf.fakequant_q4k(Wq, None, x0)
+        torch.cuda.synchronize()
+        wf = Wq.float()
+        ratio = float(((wf - xm.float()) ** 2).sum() / ((wf - x0.float()) ** 2).sum())
+        out["q4k_mse_search"] = {
+            "us": round(ms_mse * 1e3, 1),
+            "GBps": round(N * K * (2 + 2 + 144 / 256) / (ms_mse * 1e-3) / 1e9, 1),
+            "sq_error_vs_min_max": round(ratio, 4),
+            "work": "W 14336x4096 (per-row log-normal scale) -> 144-byte blocks + x_hat with the "
+                    "searched sub-block steps (17 candidates, least-squares refit); ALU-bound"}
+        del xm, x0, wf
+        out["q4k_export_and_forward"] = {
+            "pack_us": round(ms_pack * 1e3, 2),
+            "pack_GBps": round(N * K * (2 + 144 / 256) / (ms_pack * 1e-3) / 1e9, 1),
+            "forward_ms": round(ms_fwd, 4),
+            "forward_TFLOPs": round(2.0 * 4096 * N * K / (ms_fwd * 1e-3) / 1e12, 1),
+            "work": "W 14336x4096 (per-row log-normal scale) -> 144-byte blocks; Y = X Q(W)^T, X 4096x4096"}
     return out
 
 

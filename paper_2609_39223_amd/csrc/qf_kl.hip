@@ -233,8 +233,16 @@ __global__ __launch_bounds__(NT) void qad_kl_kernel(const uint16_t* __restrict__
 __global__ __launch_bounds__(256) void mean_kernel(const float* __restrict__ x, int64_t n,
                                                    float* __restrict__ out) {
   __shared__ float part[256];
-  float acc = 0.0f;
-  for (int64_t i = threadIdx.x; i < n; i += 256) acc += x[i];
+  float acc = 0.0f;                                   // x[t], x[t + 256], ... in order,
+  int64_t i = threadIdx.x;                            // eight loads in flight per batch
+  for (; i + 7 * 256 < n; i += 8 * 256) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = x[i + u * 256];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc += v[u];
+  }
+  for (; i < n; i += 256) acc += x[i];
   part[threadIdx.x] = acc;
   __syncthreads();
   for (int s = 128; s >= 1; s >>= 1) {
