@@ -108,13 +108,20 @@ qf_status fakequant_to(int fmt, const uint16_t* x, int64_t R, int64_t K, int64_t
   }
 }
 
+// Row stride (elements) of a workspace operand whose rows hold `cols` bf16 values.  Byte strides
+// that are multiples of 32 KB put every row of a GEMM tile on the same memory channels and L2
+// sets (an NT GEMM over 64 KB strides measured ~5 % slower than over 64 KB + 256 B; 16 KB
+// strides showed no difference), so those rows get 128 more elements.
+int64_t ws_ld(int64_t cols) { return cols % 16384 == 0 ? cols + 128 : cols; }
+
 // Workspace of one linear layer (256-byte aligned regions):
 //   scal   256 B   weight amax scratch
 //   what   [N, K]  W_hat (forward operand), when wfmt != NONE
 //   ahat   [M, K]  A_hat, when afmt != NONE
 //   whatt  [K, N]  W_hat^T (or W^T): right operand of dX = dY W_hat in NT form
-//   ahatt  [K, M]  A_hat^T (or X^T): right operand of dW = dY^T A_hat in NT form
-//   dyt    [N, M]  dY^T: left operand of dW
+//   ahatt  [K, M]  A_hat^T (or X^T): right operand of dW = dY^T A_hat in NT form (row stride
+//                  ws_ld(M))
+//   dyt    [N, M]  dY^T: left operand of dW (row stride ws_ld(M))
 //   part   FP32 partial tiles of the dW GEMM's split last round (qf::gemm_nt_split_bytes)
 struct LinearWs {
   float* scal;
@@ -131,7 +138,8 @@ size_t linear_ws_bytes(const qf_qlinear_desc* d) {
   size_t b = kAlign;
   if (d->wfmt != QF_FMT_NONE) b += up(N * K * 2);
   if (d->afmt != QF_FMT_NONE) b += up(M * K * 2);
-  b += up(K * N * 2) + up(K * M * 2) + up(N * M * 2);
+  const size_t ldm = (size_t)ws_ld(d->M);
+  b += up(K * N * 2) + up(K * ldm * 2) + up(N * ldm * 2);
   b += up(qf::gemm_nt_split_bytes(d->N, d->K));
   return b;
 }
@@ -144,9 +152,10 @@ LinearWs linear_ws(const qf_qlinear_desc* d, void* ws) {
   p += kAlign;
   if (d->wfmt != QF_FMT_NONE) { w.what = reinterpret_cast<uint16_t*>(p); p += up(N * K * 2); }
   if (d->afmt != QF_FMT_NONE) { w.ahat = reinterpret_cast<uint16_t*>(p); p += up(M * K * 2); }
+  const size_t ldm = (size_t)ws_ld(d->M);
   w.whatt = reinterpret_cast<uint16_t*>(p); p += up(K * N * 2);
-  w.ahatt = reinterpret_cast<uint16_t*>(p); p += up(K * M * 2);
-  w.dyt = reinterpret_cast<uint16_t*>(p); p += up(N * M * 2);
+  w.ahatt = reinterpret_cast<uint16_t*>(p); p += up(K * ldm * 2);
+  w.dyt = reinterpret_cast<uint16_t*>(p); p += up(N * ldm * 2);
   w.part = reinterpret_cast<float*>(p);
   return w;
 }
@@ -357,18 +366,19 @@ qf_status qf_qlinear_bwd_ste(const qf_qlinear_desc* d, const uint16_t* dY, const
                  "dX gemm"));
     }
     if (dW) {  // dW[N, K] = (dY^T)[N, M] (A_hat^T)[K, M]^T
-      QF_TRY(dev(qf::launch_transpose_bf16(dY, d->M, d->N, dm.ldy, w.dyt, d->M, 1, 0, 0, s),
+      const int64_t ldm = ws_ld(d->M);
+      QF_TRY(dev(qf::launch_transpose_bf16(dY, d->M, d->N, dm.ldy, w.dyt, ldm, 1, 0, 0, s),
                  "transpose dY"));
       if (d->afmt != QF_FMT_NONE && !reuse) {
         QF_TRY(dev(qf::launch_quant_t(d->afmt, X, d->M, d->K, dm.ldx, 1, 0, d->a_amax, w.ahatt,
-                                      d->M, 0, s), "quantize X (transposed)"));
+                                      ldm, 0, s), "quantize X (transposed)"));
       } else {
         const uint16_t* src = d->afmt != QF_FMT_NONE ? w.ahat : X;
         const int64_t ld = d->afmt != QF_FMT_NONE ? d->K : dm.ldx;
-        QF_TRY(dev(qf::launch_transpose_bf16(src, d->M, d->K, ld, w.ahatt, d->M, 1, 0, 0, s),
+        QF_TRY(dev(qf::launch_transpose_bf16(src, d->M, d->K, ld, w.ahatt, ldm, 1, 0, 0, s),
                    "transpose A_hat"));
       }
-      QF_TRY(dev(qf::launch_gemm_nt(d->N, d->K, d->M, w.dyt, d->M, 0, w.ahatt, d->M, 0, dW, d->K,
+      QF_TRY(dev(qf::launch_gemm_nt(d->N, d->K, d->M, w.dyt, ldm, 0, w.ahatt, ldm, 0, dW, d->K,
                                     1, w.part, s),
                  "dW gemm"));
     }
@@ -401,8 +411,9 @@ struct GroupedWs {
   uint16_t* ahat;   // [T, K]
   uint16_t* whatt;  // [E, K, N]: per-expert W_hat^T, right operand of dX in NT form
   int* kstart;      // [E+1]: expert e's tokens at padded columns [64 kstart[e], 64 kstart[e+1])
-  uint16_t* dyt;    // [N, Tpad]: dY^T, each expert's tokens padded to a multiple of 64
-  uint16_t* at;     // [K, Tpad]: A_hat^T, same padding (dW operands in NT form)
+  uint16_t* dyt;    // [N, Tpad] (row stride ws_ld(Tpad)): dY^T, each expert's tokens padded
+                    // to a multiple of 64
+  uint16_t* at;     // [K, Tpad] (same row stride): A_hat^T, same padding (dW operands, NT form)
 };
 
 // Padded token count: each expert's rows rounded up to a multiple of 64.
@@ -414,7 +425,8 @@ size_t grouped_ws_bytes(const qf_grouped_desc* d) {
   if (d->afmt != QF_FMT_NONE) b += up((size_t)d->T * d->K * 2);
   b += up((size_t)d->E * d->N * d->K * 2);
   b += up((size_t)(d->E + 1) * 4);
-  b += up((size_t)d->N * grouped_tpad(d) * 2) + up((size_t)d->K * grouped_tpad(d) * 2);
+  const size_t ldt = (size_t)ws_ld(grouped_tpad(d));
+  b += up((size_t)d->N * ldt * 2) + up((size_t)d->K * ldt * 2);
   return b;
 }
 
@@ -428,7 +440,7 @@ GroupedWs grouped_ws(const qf_grouped_desc* d, void* ws) {
   if (d->afmt != QF_FMT_NONE) { g.ahat = reinterpret_cast<uint16_t*>(p); p += up((size_t)d->T * d->K * 2); }
   g.whatt = reinterpret_cast<uint16_t*>(p); p += up((size_t)d->E * d->N * d->K * 2);
   g.kstart = reinterpret_cast<int*>(p); p += up((size_t)(d->E + 1) * 4);
-  g.dyt = reinterpret_cast<uint16_t*>(p); p += up((size_t)d->N * grouped_tpad(d) * 2);
+  g.dyt = reinterpret_cast<uint16_t*>(p); p += up((size_t)d->N * ws_ld(grouped_tpad(d)) * 2);
   g.at = reinterpret_cast<uint16_t*>(p);
   return g;
 }
@@ -557,16 +569,16 @@ qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int64_t* gr
   if (dW) {
     // dW_e = dY_e^T A_hat_e as one NT launch over padded, transposed token columns: expert e
     // contracts over its own 64-aligned column range (zeros past its last token).
-    const int64_t tp = grouped_tpad(d);
+    const int64_t tp = grouped_tpad(d), ldt = ws_ld(tp);
     QF_TRY(dev(qf::launch_quant_t_grouped(QF_FMT_NONE, dY, d->T, d->N, group_offsets, g.kstart,
-                                          d->E, g.dyt, tp, s),
+                                          d->E, g.dyt, ldt, s),
                "transpose dY (grouped)"));
     const bool saved = d->afmt != QF_FMT_NONE && reuse;
     QF_TRY(dev(qf::launch_quant_t_grouped(saved ? QF_FMT_NONE : d->afmt, saved ? g.ahat : X, d->T,
-                                          d->K, group_offsets, g.kstart, d->E, g.at, tp, s),
+                                          d->K, group_offsets, g.kstart, d->E, g.at, ldt, s),
                "quantize A (grouped, transposed)"));
-    QF_TRY(dev(qf::launch_grouped_nt_k(d->E, d->N, d->K, tp, g.kstart, g.order, g.dyt, tp, g.at,
-                                       tp, dW, d->K, d->N * d->K, s),
+    QF_TRY(dev(qf::launch_grouped_nt_k(d->E, d->N, d->K, tp, g.kstart, g.order, g.dyt, ldt, g.at,
+                                       ldt, dW, d->K, d->N * d->K, s),
                "grouped dW"));
   }
   return ok();
