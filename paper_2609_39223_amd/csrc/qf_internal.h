@@ -108,14 +108,17 @@ hipError_t launch_lora_quant_t(int fmt, const LoraOperand& L, const uint16_t* w,
 // rows for the row-dot, 1024 for the column sum) deals expert-aligned chunks to blocks; off
 // null = one group.  pre[e] = sum over experts before e of ceil(rows / q).
 hipError_t launch_group_prefix(const int64_t* off, int64_t E, int q, int* pre, hipStream_t s);
-// P[m][j] = sum_k X[m][k] F[j][k]: X bf16 [M, K] (ldx), F FP32 [r, K] (ldf, multiple of 4,
-// 16-byte aligned; grouped: expert e uses F + e * fstride), P FP32 [M, ldp] with ldp = r
-// rounded up to 16 (zeros past r).  K a multiple of 8.
+// P[m][j] = sum_k X[m][k] F[j][k]: X bf16 [M, K] (ldx a multiple of 8, 16-byte aligned), F FP32
+// [r, K] (ldf, multiple of 4, 16-byte aligned; grouped: expert e uses F + e * fstride), P FP32
+// [M, ldp] with ldp = r rounded up to 16 (zeros past r).  K a multiple of 8.  Both run on MFMA
+// with the FP32 factor split into bf16 hi + lo (within the floating-point tolerance, not the
+// FP32 FMA chain's rounding).
 hipError_t launch_lora_rowdot(const uint16_t* X, int64_t M, int64_t K, int64_t ldx, const float* F,
                               int64_t ldf, int64_t r, float* P, int64_t ldp, const int64_t* off,
                               const int* pre, int64_t E, int64_t fstride, hipStream_t s);
 // out = scale * sum_m Big[m][c] Sm[m][j] as out[c][j] (or out[j][c] when transposed): Big bf16
-// [M, C] (ldb, C a multiple of 4), Sm FP32 [M, lds_] as the row-dot writes it (lds_ = r
+// [M, C] (16-byte aligned, ldb a multiple of 8, C a multiple of 4), Sm FP32 [M, lds_] as the
+// row-dot writes it (lds_ = r
 // rounded up to 16, zeros past r, 16-byte aligned); `part` holds lora_colsum_part_bytes(M, C,
 // r) bytes (grouped: lora_colsum_grouped_part_bytes) of row-chunk partials, summed in a fixed
 // order.  Grouped with per_group: out + e * C * r receives expert e's rows only; grouped
