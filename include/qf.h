@@ -356,6 +356,9 @@ QF_API qf_status qf_qlinear_lora_fwd(const qf_qlinear_desc* d, const qf_lora* lo
  *   dB = scale G A^T    FP32 [N, r]       dA = scale B^T G    FP32 [r, K]
  * (overwritten; either may be NULL), and dX = dY W_hat (Eq. activation-ste; bf16 [M, K], may
  * be NULL).  G itself is never formed: dB = scale dY^T (A_hat A^T), dA = scale (dY B)^T A_hat.
+ * The rank-r products accumulate in FP32 on the matrix cores, each FP32 factor (and rank-r
+ * intermediate) taken as the sum of two bf16 halves (relative error below 2^-17 per value), in
+ * a fixed order, so the gradients are deterministic.
  */
 QF_API qf_status qf_qlinear_lora_bwd_ste(const qf_qlinear_desc* d, const qf_lora* lora,
                                          const uint16_t* dY, const uint16_t* X,
