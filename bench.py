@@ -84,8 +84,8 @@ def copy_calibration():
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the multi-GPU path is "
-              "not part of this build", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the layer has no "
+              "multi-GPU path", file=sys.stderr)
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()

@@ -50,7 +50,7 @@ typedef enum {
     QF_EINVAL = 1,   /* null required pointer, bad enum, aliasing that the call forbids */
     QF_ESHAPE = 2,   /* negative size, K not a multiple of the format's block, ld < K   */
     QF_EALIGN = 3,   /* pointer not 16-byte aligned or ld not a multiple of 8          */
-    QF_ENOTSUP = 4,  /* valid request that this build does not implement               */
+    QF_ENOTSUP = 4,  /* valid request that the library does not implement             */
     QF_EDEVICE = 5   /* a HIP launch failed (message carries the HIP error string)      */
 } qf_status;
 
