@@ -717,6 +717,30 @@ qf_status lora_weight_amax(const qf_qlinear_desc* d, const qf::LoraOperand& L, c
   return QF_OK;
 }
 
+// NVFP4 without a given amax needs the merged tensor's amax before any block scale.  Rather
+// than merging twice (an amax pass, then the quantizer), the merged bf16 tensor m = bf16(W +
+// scale B A) is written once to `tmp` [N, K] and the amax and the quantizer read it: the same m
+// values through the same codec, so the output is bit-identical.  Transposed: out [K, N].
+bool lora_merge_once(const qf_qlinear_desc* d) { return d->wfmt == QF_FMT_NVFP4 && !d->w_amax; }
+
+qf_status lora_quant_via_merged(const qf_qlinear_desc* d, const qf::LoraOperand& L,
+                                const uint16_t* W, int64_t ldw, uint16_t* tmp, float* scratch,
+                                uint16_t* out, bool transposed, hipStream_t s) {
+  const int64_t N = d->N, K = d->K;
+  QF_TRY(dev(qf::launch_lora_quant(QF_FMT_NONE, L, W, N, K, ldw, 1, 0, nullptr, nullptr, nullptr,
+                                   nullptr, nullptr, tmp, s),
+             "merge"));
+  QF_TRY(dev(qf::launch_fill_f32(scratch, 1, 0.0f, s), "amax init"));
+  QF_TRY(dev(qf::launch_amax(tmp, N, K, K, scratch, s), "amax of the merged weight"));
+  if (transposed)
+    QF_TRY(dev(qf::launch_quant_t(QF_FMT_NVFP4, tmp, N, K, K, 1, 0, scratch, out, N, 0, s),
+               "quantize merged weight (transposed)"));
+  else
+    QF_TRY(dev(qf::launch_nvfp4(tmp, N, K, K, scratch, nullptr, nullptr, nullptr, out, s),
+               "quantize merged weight"));
+  return QF_OK;
+}
+
 }  // namespace
 
 qf_status qf_lora_amax(const uint16_t* W, int64_t N, int64_t K, int64_t ldw, const qf_lora* lora,
@@ -809,11 +833,15 @@ qf_status qf_qlinear_lora_fwd(const qf_qlinear_desc* d, const qf_lora* lora, con
   hipStream_t s = S(stream);
   LoraWs w = lora_ws(d, lora->r, ws);
   const qf::LoraOperand L = lora_op(lora);
-  const float* g;
-  QF_TRY(lora_weight_amax(d, L, W, dm.ldw, w.scal, &g, s));
-  QF_TRY(dev(qf::launch_lora_quant(d->wfmt, L, W, d->N, d->K, dm.ldw, 1, 0, g, nullptr, nullptr,
-                                   nullptr, nullptr, w.what, s),
-             "merged quantize"));
+  if (lora_merge_once(d)) {           // W_hat^T's region is free in the forward
+    QF_TRY(lora_quant_via_merged(d, L, W, dm.ldw, w.whatt, w.scal, w.what, false, s));
+  } else {
+    const float* g;
+    QF_TRY(lora_weight_amax(d, L, W, dm.ldw, w.scal, &g, s));
+    QF_TRY(dev(qf::launch_lora_quant(d->wfmt, L, W, d->N, d->K, dm.ldw, 1, 0, g, nullptr, nullptr,
+                                     nullptr, nullptr, w.what, s),
+               "merged quantize"));
+  }
   const uint16_t* Aop = X;
   int64_t lda = dm.ldx;
   if (d->afmt != QF_FMT_NONE) {
@@ -852,6 +880,8 @@ qf_status qf_qlinear_lora_bwd_ste(const qf_qlinear_desc* d, const qf_lora* lora,
     if (reuse) {
       QF_TRY(dev(qf::launch_transpose_bf16(w.what, N, K, K, w.whatt, N, 1, 0, 0, s),
                  "transpose W_hat"));
+    } else if (lora_merge_once(d)) {    // W_hat's region is free without a saved forward
+      QF_TRY(lora_quant_via_merged(d, L, W, dm.ldw, w.what, w.scal, w.whatt, true, s));
     } else {
       const float* g;
       QF_TRY(lora_weight_amax(d, L, W, dm.ldw, w.scal, &g, s));
@@ -973,6 +1003,29 @@ qf_status glora_amax(const qf_grouped_desc* d, const qf::LoraOperand& L, const u
   return QF_OK;
 }
 
+// As lora_quant_via_merged, per expert: the merged experts go to `tmp` [E, N, K] once, then the
+// per-expert amax and NVFP4 quantizer (row-major into out [E, N, K], or transposed into
+// out [E, K, N]) read them.
+bool glora_merge_once(const qf_grouped_desc* d) { return d->wfmt == QF_FMT_NVFP4 && !d->w_amax; }
+
+qf_status glora_quant_via_merged(const qf_grouped_desc* d, const qf::LoraOperand& L,
+                                 const uint16_t* W, uint16_t* tmp, float* scratch, uint16_t* out,
+                                 bool transposed, hipStream_t s) {
+  const int64_t E = d->E, N = d->N, K = d->K;
+  QF_TRY(dev(qf::launch_lora_quant(QF_FMT_NONE, L, W, N, K, K, E, N * K, nullptr, nullptr,
+                                   nullptr, nullptr, nullptr, tmp, s),
+             "merge (experts)"));
+  QF_TRY(dev(qf::launch_fill_f32(scratch, E, 0.0f, s), "amax init"));
+  QF_TRY(dev(qf::launch_amax_batched(tmp, E, N, K, scratch, s), "amax of the merged experts"));
+  if (transposed)
+    QF_TRY(dev(qf::launch_quant_t(QF_FMT_NVFP4, tmp, N, K, K, E, N * K, scratch, out, N, N * K, s),
+               "quantize merged experts (transposed)"));
+  else
+    QF_TRY(dev(qf::launch_nvfp4_batched(tmp, E, N, K, scratch, out, s),
+               "quantize merged experts"));
+  return QF_OK;
+}
+
 }  // namespace
 
 qf_status qf_grouped_lora_workspace_size(const qf_grouped_desc* d, const qf_lora* lora,
@@ -997,11 +1050,15 @@ qf_status qf_qlinear_grouped_lora_fwd(const qf_grouped_desc* d, const qf_lora* l
   hipStream_t s = S(stream);
   GroupedLoraWs g = glora_ws(d, lora->r, lora->b_shared, ws);
   const qf::LoraOperand L = glora_op(d, lora);
-  const float* gp;
-  QF_TRY(glora_amax(d, L, W, g.wamax, &gp, s));
-  QF_TRY(dev(qf::launch_lora_quant(d->wfmt, L, W, d->N, d->K, d->K, d->E, d->N * d->K, gp,
-                                   nullptr, nullptr, nullptr, nullptr, g.what, s),
-             "merged quantize (experts)"));
+  if (glora_merge_once(d)) {          // the experts' W_hat^T region is free in the forward
+    QF_TRY(glora_quant_via_merged(d, L, W, g.whatt, g.wamax, g.what, false, s));
+  } else {
+    const float* gp;
+    QF_TRY(glora_amax(d, L, W, g.wamax, &gp, s));
+    QF_TRY(dev(qf::launch_lora_quant(d->wfmt, L, W, d->N, d->K, d->K, d->E, d->N * d->K, gp,
+                                     nullptr, nullptr, nullptr, nullptr, g.what, s),
+               "merged quantize (experts)"));
+  }
   const uint16_t* Aop = X;
   if (d->afmt == QF_FMT_MXFP4) {
     QF_TRY(dev(qf::launch_mxfp4(X, d->T, d->K, d->K, nullptr, nullptr, g.ahat, s), "mxfp4"));
@@ -1042,6 +1099,8 @@ qf_status qf_qlinear_grouped_lora_bwd_ste(const qf_grouped_desc* d, const qf_lor
     if (reuse) {
       QF_TRY(dev(qf::launch_transpose_bf16(g.what, N, K, K, g.whatt, N, E, N * K, N * K, s),
                  "transpose expert W_hat"));
+    } else if (glora_merge_once(d)) {   // W_hat's region is free without a saved forward
+      QF_TRY(glora_quant_via_merged(d, L, W, g.what, g.wamax, g.whatt, true, s));
     } else {
       const float* gp;
       QF_TRY(glora_amax(d, L, W, g.wamax, &gp, s));
