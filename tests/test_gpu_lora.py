@@ -226,8 +226,10 @@ def test_lora_layer_partial_outputs_and_zero_tokens(qf):
     assert np.all(from_dev(dA) == 0.0) and np.all(from_dev(dB) == 0.0)
 
 
-def test_lora_layer_zero_adapter_matches_plain_layer(qf):
+@pytest.mark.parametrize("wfmt", ["mxfp4", "nvfp4"])
+def test_lora_layer_zero_adapter_matches_plain_layer(qf, wfmt):
     # B = 0 (the adapter's initialization): forward and dX equal the plain layer's bit for bit
+    # (NVFP4: the merged tensor is stored once, then its amax and quantizer run over it)
     rng = np.random.default_rng(51)
     M, N, K, r = 256, 264, 512, 16
     X = workloads.normal_bf16(rng, (M, K))
@@ -235,8 +237,8 @@ def test_lora_layer_zero_adapter_matches_plain_layer(qf):
     dY = workloads.normal_bf16(rng, (M, N))
     f = _factors(51, N, K, r)
     f["B"][:] = 0.0
-    Y, dX, dA, dB = _lora_layer(qf, X, W, dY, f, "mxfp4", "mxfp4")
-    d = qf.qlinear_desc(M, N, K, "mxfp4", "mxfp4")
+    Y, dX, dA, dB = _lora_layer(qf, X, W, dY, f, wfmt, "mxfp4")
+    d = qf.qlinear_desc(M, N, K, wfmt, "mxfp4")
     ws = qf.workspace(d)
     Y0, dX0 = empty_bf16((M, N)), empty_bf16((M, K))
     Xd, Wd = to_dev(X), to_dev(W)
