@@ -84,6 +84,28 @@ def test_grouped_dw_tile_grid_split_over_xcds(qf):
             assert np.all(dW[e] == 0.0)
 
 
+def test_grouped_padded_token_count_multiple_of_16384(qf):
+    """Two experts whose 64-aligned padded token count is exactly 16384: the dW operands sit
+    in the workspace with a row stride of 16384 + 128 elements."""
+    rng = np.random.default_rng(23)
+    E, N, K = 2, 136, 256
+    counts = np.array([8000, 8195])                # (16195 + 63 * 2 + 63) // 64 * 64 == 16384
+    offsets = np.concatenate([[0], np.cumsum(counts)])
+    T = int(offsets[-1])
+    X = workloads.normal_bf16(rng, (T, K))
+    W = np.stack([workloads.normal_bf16(rng, (N, K), 0.02 * (e + 1)) for e in range(E)])
+    dY = workloads.normal_bf16(rng, (T, N))
+    Y, dX, dW = run_grouped(qf, offsets, X, W, dY, "mxfp4", "mxfp4")
+    ahat = oracle.fakequant(X, "mxfp4")
+    for e in range(E):
+        r0, r1 = offsets[e], offsets[e + 1]
+        what = oracle.fakequant(W[e], "mxfp4")
+        assert_close(bf16_to_f64(Y[r0:r1]), oracle.linear_fwd(ahat[r0:r1], what), f"Y e={e}")
+        assert_close(bf16_to_f64(dX[r0:r1]), oracle.linear_dx(dY[r0:r1], what), f"dX e={e}")
+        assert_close(dW[e].astype(np.float64), oracle.linear_dw(dY[r0:r1], ahat[r0:r1]),
+                     f"dW e={e}")
+
+
 def test_grouped_zipf_routing_sampled(qf):
     """128 experts, top-8 Zipf(1.1) routing (reduced token count and width), sampled."""
     tok, offsets = workloads.moe_routing(seed=0, tokens=2048, experts=128, topk=8)

@@ -222,6 +222,53 @@ def test_layer_backward_with_m_not_multiple_of_8(qf):
     assert_close(dW.astype(np.float64), oracle.linear_dw(w["dY"], ahat), "dW")
 
 
+@pytest.mark.parametrize("wfmt,afmt,reuse", [("mxfp4", "mxfp4", False), ("nvfp4", "none", False),
+                                             ("mxfp4", "mxfp4", True)])
+def test_layer_token_count_multiple_of_16384(qf, wfmt, afmt, reuse):
+    """16384 tokens: the dW operands dY^T and A_hat^T sit in the workspace with a row stride of
+    16384 + 128 elements (byte strides that are multiples of 32 KB get padded)."""
+    rng = np.random.default_rng(21)
+    M, N, K = 16384, 264, 512
+    w = {"X": _rand_bf16(rng, (M, K)), "W": _rand_bf16(rng, (N, K), 0.02),
+         "dY": _rand_bf16(rng, (M, N))}
+    Y, dX, dW = _layer(qf, w, wfmt, afmt, reuse=reuse)
+    what = oracle.fakequant(w["W"], wfmt)
+    ahat = oracle.fakequant(w["X"], afmt)
+    assert_close(bf16_to_f64(Y), oracle.linear_fwd(ahat, what), "Y")
+    assert_close(bf16_to_f64(dX), oracle.linear_dx(w["dY"], what), "dX")
+    assert_close(dW.astype(np.float64), oracle.linear_dw(w["dY"], ahat), "dW")
+
+
+def test_dense_down_projection_32k_tokens_sampled(qf):
+    """The 9B-class layer's down projection at 32K tokens (32768 x 4096 x 12288, NVFP4 weights,
+    bf16 activations with heavy-tailed column scales) in the launch configuration the benchmark
+    times (row stride 32768 + 128 for the dW operands), checked on sampled entries."""
+    rng = np.random.default_rng(22)
+    M, N, K = 32768, 4096, 12288
+    tau = np.abs(rng.standard_t(3.0, size=K)).astype(np.float32)
+    w = {"X": workloads.normal_bf16(rng, (M, K), 1.0, col_scale=tau),
+         "W": workloads.normal_bf16(rng, (N, K), 0.02),
+         "dY": workloads.normal_bf16(rng, (M, N), 1.0)}
+    Y, dX, dW = _layer(qf, w, "nvfp4", "none")
+    wq = oracle.nvfp4(w["W"])["xhat"]
+    n = 2048
+
+    def sampled(a, ai, b, bi):                    # chunked: rows are up to 32768 long
+        return np.concatenate([oracle.dot_rows(a, ai[c:c + 256], b, bi[c:c + 256])
+                               for c in range(0, len(ai), 256)])
+
+    i, j = rng.integers(0, M, n), rng.integers(0, N, n)
+    assert_close(bf16_to_f64(Y[i, j]), sampled(w["X"], i, wq, j), "Y sampled")
+    wqT = np.ascontiguousarray(wq.T)
+    i, k = rng.integers(0, M, n), rng.integers(0, K, n)
+    assert_close(bf16_to_f64(dX[i, k]), sampled(w["dY"], i, wqT, k), "dX sampled")
+    del wqT, Y, dX
+    dYT = np.ascontiguousarray(w["dY"].T)
+    xT = np.ascontiguousarray(w["X"].T)
+    j, k = rng.integers(0, N, n), rng.integers(0, K, n)
+    assert_close(dW[j, k].astype(np.float64), sampled(dYT, j, xT, k), "dW sampled")
+
+
 def test_nt_gemm_pipeline_depths(qf):
     # K from below one stage to many stages, with and without a partial last stage
     rng = np.random.default_rng(13)
