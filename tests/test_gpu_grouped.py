@@ -125,6 +125,44 @@ def test_grouped_zipf_routing_sampled(qf):
         assert_close(dW[e].astype(np.float64), oracle.linear_dw(dY[r0:r1], X[r0:r1]), f"dW e={e}")
 
 
+def test_moe_down_projection_full_size_sampled(qf):
+    """The MoE layer's down projection at full size (128 experts, Zipf(1.1) top-8 routing of
+    32768 tokens = 262144 rows, 1536 -> 3072, NVFP4 weights) in the launch configuration the
+    benchmark times; entries sampled in the largest, smallest and three other experts."""
+    _, offsets = workloads.moe_routing(seed=0, tokens=32768, experts=128, topk=8)
+    E, N, K = 128, 3072, 1536
+    T = int(offsets[-1])
+    rng = np.random.default_rng(24)
+    X = workloads.normal_bf16(rng, (T, K))
+    W = workloads.normal_bf16(rng, (E * N, K), 0.02).reshape(E, N, K)
+    dY = workloads.normal_bf16(rng, (T, N))
+    d = qf.grouped_desc(E, T, N, K, "nvfp4", "none")
+    ws = qf.grouped_workspace(d)
+    off = torch.from_numpy(offsets.astype(np.int64)).cuda()
+    Xd, Wd, dYd = to_dev(X), to_dev(W.reshape(E * N, K)), to_dev(dY)
+    Yd, dXd = empty_bf16((T, N)), empty_bf16((T, K))
+    dWd = torch.empty((E, N, K), dtype=torch.float32, device="cuda")
+    qf.qlinear_grouped_fwd(d, off, Xd, Wd, Yd, ws)
+    qf.qlinear_grouped_bwd_ste(d, off, dYd, Xd, Wd, dXd, dWd, ws)
+    torch.cuda.synchronize()
+    Y, dX = from_dev(Yd), from_dev(dXd)
+    cnt = np.diff(offsets)
+    experts = [int(np.argmax(cnt)), int(np.argmin(cnt))] + [int(e) for e in rng.choice(E, 3)]
+    n = 1024
+    for e in experts:
+        r0, r1 = int(offsets[e]), int(offsets[e + 1])
+        what = oracle.nvfp4(W[e])["xhat"]
+        i, j, k = rng.integers(r0, r1, n), rng.integers(0, N, n), rng.integers(0, K, n)
+        assert_close(bf16_to_f64(Y[i, j]), oracle.dot_rows(X, i, what, j), f"Y e={e}")
+        assert_close(bf16_to_f64(dX[i, k]), oracle.dot_rows(dY, i, np.ascontiguousarray(what.T), k),
+                     f"dX e={e}")
+        dW = from_dev(dWd[e])
+        j, k = rng.integers(0, N, n), rng.integers(0, K, n)
+        dYT = np.ascontiguousarray(dY[r0:r1].T)
+        XT = np.ascontiguousarray(X[r0:r1].T)
+        assert_close(dW[j, k].astype(np.float64), oracle.dot_rows(dYT, j, XT, k), f"dW e={e}")
+
+
 @pytest.mark.parametrize("wfmt", ["nvfp4", "mxfp4", "q4k"])
 def test_grouped_transposing_quantizer_matches_saved_operands(qf, wfmt):
     """Expert W_hat^T straight from the transposing quantizer (per-expert NVFP4 scales) equals

@@ -186,6 +186,26 @@ def test_mlp_up_mxfp4_full_size_sampled(qf):
     assert_close(dW[j, k].astype(np.float64), oracle.dot_rows(dYT, j, xqT, k), "dW sampled")
 
 
+def test_q4k_export_weight_forward_full_size_sampled(qf):
+    """The Q4_K export weight (14336 x 4096, per-row log-normal scales) and its forward GEMM at
+    X 4096 x 4096, in the launch configuration the benchmark times, on sampled entries + rows."""
+    w = workloads.q4k_weight(seed=0)
+    M, N, K = w["M"], w["N"], w["K"]
+    X, W = to_dev(w["X"]), to_dev(w["W"])
+    d = qf.qlinear_desc(M, N, K, "q4k", "none")
+    ws = qf.workspace(d)
+    Yd = empty_bf16((M, N))
+    qf.qlinear_fwd(d, X, W, Yd, ws)
+    torch.cuda.synchronize()
+    Y = from_dev(Yd)
+    wq = oracle.q4k(w["W"])["xhat"]
+    rng = np.random.default_rng(25)
+    i, j = rng.integers(0, M, 1 << 14), rng.integers(0, N, 1 << 14)
+    assert_close(bf16_to_f64(Y[i, j]), oracle.dot_rows(w["X"], i, wq, j), "Y sampled")
+    r = rng.integers(0, M, 2)
+    assert_close(bf16_to_f64(Y[r]), oracle.linear_fwd(w["X"][r], wq), "Y rows")
+
+
 def test_linear_determinism(qf):
     rng = np.random.default_rng(10)
     w = {"X": _rand_bf16(rng, (512, 1024)), "W": _rand_bf16(rng, (768, 1024), 0.02),
