@@ -145,15 +145,15 @@ def main():
     xhatt = torch.empty(K, M, dtype=torch.int16, device=dev)
     dYt = torch.empty(N, M, dtype=torch.int16, device=dev)
     gws = qf.gemm_workspace(N, K, 1)        # dW's split last round, as in the layer call
-    phases = ["quant_W", "quant_X", "gemm_fwd", "quant_W_transposed", "gemm_dX", "transpose_dY",
+    # (the dX GEMM also writes dY^T, the left operand of dW, as the layer's backward does)
+    phases = ["quant_W", "quant_X", "gemm_fwd", "quant_W_transposed", "gemm_dX_and_dY_transposed",
               "quant_X_transposed", "gemm_dW"]
     calls = [
         lambda: qf.fakequant_mxfp4(W, None, None, what),
         lambda: qf.fakequant_mxfp4(X, None, None, xhat),
         lambda: qf.gemm_bf16(M, N, K, xhat, K, 1, what, K, 1, Y, N, 0),
         lambda: qf.fakequant_transposed(W, "mxfp4", whatt),
-        lambda: qf.gemm_bf16(M, K, N, dY, N, 1, whatt, N, 1, dX, K, 0),
-        lambda: qf.transpose_bf16(dY, dYt),
+        lambda: qf.gemm_bf16_at(M, K, N, dY, N, whatt, N, dX, K, dYt, M),
         lambda: qf.fakequant_transposed(X, "mxfp4", xhatt),
         lambda: qf.gemm_bf16(N, K, M, dYt, M, 1, xhatt, M, 1, dW, K, 1, ws=gws),
     ]

@@ -259,6 +259,20 @@ QF_API qf_status qf_gemm_bf16(int64_t M, int64_t N, int64_t K, const uint16_t* A
                        int64_t ldc, int c_f32, qf_stream_t stream);
 
 /*
+ * qf_gemm_bf16_at -- qf_gemm_bf16 with A [M, K] and B [N, K] k-contiguous and a bf16 C, that
+ * also writes A^T: at[k * ldat + m] = A[m, k] for m < M, k < K (other elements of `at` are
+ * left alone).  The layer backward's dX = dY W_hat (Eq. activation-ste) uses it to produce
+ * dY^T, the left operand of dW = dY^T A_hat (Eq. ste), from the dY tiles the GEMM stages in
+ * LDS anyway, instead of a separate transpose pass over dY.  C and `at` are bit-identical to
+ * qf_gemm_bf16 and qf_transpose_bf16.
+ *   M and K multiples of 8; ldat >= M, a multiple of 4 and below 2^24; at 16-byte aligned
+ *   device memory owned by the caller (needed when M and K are nonzero).
+ */
+QF_API qf_status qf_gemm_bf16_at(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
+                                 const uint16_t* B, int64_t ldb, uint16_t* C, int64_t ldc,
+                                 uint16_t* at, int64_t ldat, qf_stream_t stream);
+
+/*
  * qf_gemm_workspace_size / qf_gemm_bf16_ws -- qf_gemm_bf16 with a caller workspace.  With
  * k-contiguous A and B and an FP32 C (the dW product), a last round of output tiles that
  * would leave at least half of the compute units idle is computed as two K-halves into the

@@ -100,6 +100,7 @@ def lib() -> ctypes.CDLL:
                                        ctypes.c_int),
             "qf_gemm_bf16_ws": ([_I, _I, _I, _P, _I, ctypes.c_int, _P, _I, ctypes.c_int, _P, _I,
                                  ctypes.c_int, _P, ctypes.c_size_t, _P], ctypes.c_int),
+            "qf_gemm_bf16_at": ([_I, _I, _I, _P, _I, _P, _I, _P, _I, _P, _I, _P], ctypes.c_int),
             "qf_fakequant_transposed": ([ctypes.c_int, _P, _I, _I, _I, _P, _P, _I, _P],
                                         ctypes.c_int),
             "qf_lora_amax": ([_P, _I, _I, _I, ctypes.POINTER(LoRA), _P, ctypes.c_int, _P],
@@ -275,6 +276,12 @@ def gemm_bf16(M, N, K, A, lda, a_kmajor, B, ldb, b_kmajor, C, ldc, c_f32, ws=Non
                                      ldb, int(b_kmajor), _ptr(C), ldc, int(c_f32), _ptr(ws),
                                      ws.numel() * ws.element_size(), _stream()))
     return C
+
+
+def gemm_bf16_at(M, N, K, A, lda, B, ldb, C, ldc, at, ldat):
+    _check(lib().qf_gemm_bf16_at(M, N, K, _ptr(_bf16(A)), lda, _ptr(_bf16(B)), ldb,
+                                 _ptr(_bf16(C)), ldc, _ptr(_bf16(at)), ldat, _stream()))
+    return C, at
 
 
 def gemm_workspace(M, N, c_f32, device="cuda"):

@@ -345,6 +345,10 @@ qf_status qf_qlinear_bwd_ste(const qf_qlinear_desc* d, const uint16_t* dY, const
   if (d->M % 8 == 0) {
     // NT form: transposed operands through the workspace.  Without saved x_hat operands the
     // transposed ones come straight from the transposing quantizer (one pass over W and X).
+    // dY^T (left operand of dW) is written by the dX GEMM from the dY tiles it stages anyway
+    // when both gradients are asked for; otherwise by the transpose kernel.
+    const int64_t ldm = ws_ld(d->M);
+    const bool dyt_by_dx = dX != nullptr && dW != nullptr && ldm < qf::kGemmAtMaxLd;
     if (dX) {  // dX[M, K] = dY[M, N] (W_hat^T)[K, N]^T
       if (d->wfmt != QF_FMT_NONE && !reuse) {
         const float* g = d->w_amax;
@@ -362,13 +366,13 @@ qf_status qf_qlinear_bwd_ste(const qf_qlinear_desc* d, const uint16_t* dY, const
                    "transpose W_hat"));
       }
       QF_TRY(dev(qf::launch_gemm_nt(d->M, d->K, d->N, dY, dm.ldy, 0, w.whatt, d->N, 0, dX,
-                                    dm.ldx, 0, nullptr, s),
+                                    dm.ldx, 0, nullptr, s, dyt_by_dx ? w.dyt : nullptr, ldm),
                  "dX gemm"));
     }
     if (dW) {  // dW[N, K] = (dY^T)[N, M] (A_hat^T)[K, M]^T
-      const int64_t ldm = ws_ld(d->M);
-      QF_TRY(dev(qf::launch_transpose_bf16(dY, d->M, d->N, dm.ldy, w.dyt, ldm, 1, 0, 0, s),
-                 "transpose dY"));
+      if (!dyt_by_dx)
+        QF_TRY(dev(qf::launch_transpose_bf16(dY, d->M, d->N, dm.ldy, w.dyt, ldm, 1, 0, 0, s),
+                   "transpose dY"));
       if (d->afmt != QF_FMT_NONE && !reuse) {
         QF_TRY(dev(qf::launch_quant_t(d->afmt, X, d->M, d->K, dm.ldx, 1, 0, d->a_amax, w.ahatt,
                                       ldm, 0, s), "quantize X (transposed)"));
@@ -612,6 +616,30 @@ qf_status qf_gemm_bf16_ws(int64_t M, int64_t N, int64_t K, const uint16_t* A, in
   QF_TRY(dev(qf::launch_gemm_nt(M, N, K, A, lda, !a_kmajor, B, ldb, !b_kmajor, C, ldc, c_f32,
                                 part, S(stream)),
              "gemm"));
+  return ok();
+}
+
+qf_status qf_gemm_bf16_at(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
+                          const uint16_t* B, int64_t ldb, uint16_t* C, int64_t ldc, uint16_t* at,
+                          int64_t ldat, qf_stream_t stream) {
+  if (M < 0 || N < 0 || K < 0) return fail(QF_ESHAPE, "qf_gemm_bf16_at: negative shape");
+  if (M % 8 || K % 8) return fail(QF_ESHAPE, "qf_gemm_bf16_at: M and K must be multiples of 8");
+  QF_TRY(check_mat("qf_gemm_bf16_at: A", A, M, K, lda, true));
+  QF_TRY(check_mat("qf_gemm_bf16_at: B", B, N, K, ldb, true));
+  if (M > 0 && N > 0) {
+    if (!C) return fail(QF_EINVAL, "qf_gemm_bf16_at: null C");
+    if (ldc < N) return fail(QF_ESHAPE, "qf_gemm_bf16_at: ldc < N");
+    if (!aligned16(C)) return fail(QF_EALIGN, "qf_gemm_bf16_at: C not 16-byte aligned");
+  }
+  if (M > 0 && K > 0) {
+    if (!at) return fail(QF_EINVAL, "qf_gemm_bf16_at: null at");
+    if (ldat < M || ldat % 4 || ldat >= qf::kGemmAtMaxLd)
+      return fail(QF_ESHAPE, "qf_gemm_bf16_at: ldat must be >= M, a multiple of 4 and < 2^24");
+    if ((uintptr_t)at % 16) return fail(QF_EALIGN, "qf_gemm_bf16_at: at not 16-byte aligned");
+  }
+  QF_TRY(dev(qf::launch_gemm_nt(M, N, K, A, lda, 0, B, ldb, 0, C, ldc, 0, nullptr, S(stream),
+                                at, ldat),
+             "gemm (A^T output)"));
   return ok();
 }
 

@@ -48,6 +48,7 @@ typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef short v8i16 __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2_t __attribute__((ext_vector_type(2)));
 
 constexpr int BM = 256, BN = 256, BK = 64;
 constexpr int kRow = BK * 2;                     // 128 bytes per LDS row
@@ -61,7 +62,8 @@ constexpr int kPitch32 = BN * 4 + 32;            // epilogue LDS row pitch, FP32
 constexpr int kSmemEpi = (BM * kPitch16 > 128 * kPitch32) ? BM * kPitch16 : 128 * kPitch32;
 constexpr int kSmem = (2 * kStage > kSmemEpi) ? 2 * kStage : kSmemEpi;
 
-enum Mode { kDense = 0, kGroupRows = 1, kGroupK = 2 };
+// kDenseAT: dense, and the launch also writes A^T (see NtArgs::at).
+enum Mode { kDense = 0, kGroupRows = 1, kGroupK = 2, kDenseAT = 3 };
 
 struct NtArgs {
   const uint16_t* A;
@@ -90,6 +92,12 @@ struct NtArgs {
   float* part;
   int split_from, full_per_xcd, split_per_xcd;
   int64_t split_stage;
+  // kDenseAT: A^T [K][M] (row stride ldat) is written as a by-product of the main loop.  Tile
+  // (tm, tn) owns the k stages s with s % tiles_n == tn of its 256-row panel and writes them
+  // from LDS while they are resident, so every stage of every panel is written exactly once
+  // and no kernel re-reads A to transpose it.
+  uint16_t* at;
+  int64_t ldat;
 };
 
 #define QF_LDS(p) ((__attribute__((address_space(3))) void*)(p))
@@ -171,9 +179,11 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
   const int lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (scalar) index
   const int wm = WAVES == 8 ? w >> 2 : w >> 1, wn = WAVES == 8 ? w & 3 : w & 1;
+  constexpr bool DENSE = MODE == kDense || MODE == kDenseAT;
+  static_assert(MODE != kDenseAT || (!C_F32 && WAVES == 4), "A^T output: bf16 four-wavefront form");
   const int item = remap_xcd(blockIdx.x, gridDim.x);
   int bid = item, half = -1, pidx = 0;
-  if (MODE == kDense && C_F32 && p.part != nullptr) {
+  if (DENSE && C_F32 && p.part != nullptr) {
     const int per_xcd = p.full_per_xcd + 2 * p.split_per_xcd;
     const int x = item / per_xcd, j = item % per_xcd;
     if (j < p.full_per_xcd) {
@@ -190,7 +200,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
   int64_t m0, m_end, n0;
   int64_t ks0 = 0, ks1 = p.K / BK;               // stage range of this item
   int64_t cofs = 0;                              // element offset of this item's C
-  if (MODE == kDense || MODE == kGroupK) {
+  if (DENSE || MODE == kGroupK) {
     int t = bid;
     if (MODE == kGroupK) {
       // Block b runs on XCD x = b % 8 as that XCD's item j = b / 8.  XCD x owns tiles
@@ -335,7 +345,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
   if (half == 0) ks1 = p.split_stage;
   const int64_t klen = ks1 > ks0 ? ks1 - ks0 : 1;
   const int64_t krot = (int64_t)(blockIdx.x % kXcds) * (klen / kXcds);
-  auto dma = [&](int64_t s, int buf, int q) {
+  auto dma = [&](int64_t s, int buf, int q) __attribute__((always_inline)) {
     int64_t se = s + krot;
     if (se >= ks1) se -= klen;
     char* l = smem + buf * kStage + lds_of(q);
@@ -344,7 +354,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
     else dma16_buf(rs[op], goff[q], (uint32_t)(se * sstride), l);
   };
   // Fragment read r of a slice, in the order the slice's MFMAs consume them: A0, B0, B1, A1..A3.
-  auto frag = [&](const char* st, int kk, int f, bool is_b) -> bf16x8_t {
+  auto frag = [&](const char* st, int kk, int f, bool is_b) __attribute__((always_inline)) -> bf16x8_t {
     const bool mnf = is_b ? B_MN : A_MN;
     if (!mnf) {
       const int* fo = is_b ? fob : foa;
@@ -356,21 +366,75 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
     const v8i16 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
     return __builtin_bit_cast(bf16x8_t, v);
   };
-  auto read_one = [&](const char* st, int kk, int r, bf16x8_t* a, bf16x8_t* b) {
+  auto read_one = [&](const char* st, int kk, int r, bf16x8_t* a, bf16x8_t* b) __attribute__((always_inline)) {
     if (r == 0) a[0] = frag(st, kk, 0, false);
     else if (r <= NJ) b[r - 1] = frag(st, kk, r - 1, true);
     else a[r - NJ] = frag(st, kk, r - NJ, false);
   };
-  auto read_all = [&](const char* st, int kk, bf16x8_t* a, bf16x8_t* b) {
+  auto read_all = [&](const char* st, int kk, bf16x8_t* a, bf16x8_t* b) __attribute__((always_inline)) {
 #pragma unroll
     for (int r = 0; r < 4 + NJ; ++r) read_one(st, kk, r, a, b);
   };
+  // ---- A^T output (kDenseAT) ---------------------------------------------------------------------
+  // A stage's A^T is 16 pieces: piece u is k columns 4 u .. 4 u + 3 over the tile's 256 rows, so
+  // each of its rows of A^T is written as whole 128-byte lines, each line by one store.  Piece
+  // u of global stage se belongs to tile column (16 se + u) mod tiles_n, so with tiles_n >= 8 a
+  // tile has at most two pieces per stage.  at_read gathers this lane's part of piece u from
+  // the stage in LDS (rows r0 .. r0 + 3, r0 = 64 w + 4 (l % 16), of k column kc = 4 u + l / 16;
+  // four 2-byte reads through the row swizzle) before the step's barrier; at_store writes
+  // those 8 bytes to A^T row se * 64 + kc, columns m0 + r0 .. +3, after it, so the store has a
+  // whole step to complete before the next barrier's wait.  Stores go through a buffer
+  // resource over the stage's rows of A^T: lanes with rows past the operand or columns at or
+  // past kvalid get an offset beyond its range, which the hardware drops.  (Plain LDS reads:
+  // the transposing read builtin makes the compiler wait for every direct-to-LDS load in
+  // flight first.)
+  const int64_t at_tn = n0 / BN;                 // this tile's column
+  const int at_r = w * 64 + 4 * (lane & 15), at_c = lane >> 4;
+  // (the four values stay unpacked until the store: packing them at the read would make the
+  // wavefront wait for the reads there)
+  auto at_read = [&](const char* st, int u) __attribute__((always_inline)) -> u32x4_t {
+    const int kc = 4 * u + at_c;
+    u32x4_t h;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int row = at_r + e;
+      h[e] = *reinterpret_cast<const uint16_t*>(
+          st + row * kRow + ((((kc >> 3) ^ (row >> 1)) & 7) << 4) + (kc & 7) * 2);
+    }
+    return h;
+  };
+  // byte offset of this lane's 8 bytes of piece 0 within a stage's rows of A^T (below 2^31)
+  const int at_off = (int)(((int64_t)at_c * p.ldat + m0 + at_r) * 2);
+  const int at_ld8 = (int)(p.ldat * 8);          // bytes of 4 rows of A^T
+  const bool at_rok = m0 + at_r < m_end;
+  auto at_store = [&](int64_t se, int kvalid, int u, u32x4_t h) __attribute__((always_inline)) {
+    const u32x2_t v = {h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
+    const bool ok = at_rok && 4 * u + at_c < kvalid;
+    const int off = ok ? at_off + u * at_ld8 : 0x7FFFFFF8;
+    __builtin_amdgcn_raw_buffer_store_b64(
+        v, make_rsrc(p.at + se * BK * p.ldat, (int64_t)kvalid * p.ldat * 2), off, 0, 0);
+  };
+  // first piece of stage se owned by this tile, (tn - 16 se) mod tiles_n (>= 16: none); the
+  // second is at + tiles_n.  In the loop it is stepped, not divided: stage se + 1's is
+  // this one minus 16 mod tiles_n.
+  auto at_first = [&](int64_t se) -> int {
+    const int64_t t = p.tiles_n;
+    return (int)((at_tn - (se * 16) % t + t) % t);
+  };
+  int at_u = 0;
+  int at_u_wrap = 0, at_d = 0;
+  if (MODE == kDenseAT) {
+    at_u_wrap = at_first(ks0);                   // the stage after the wrap to ks0
+    at_d = (int)(16 % p.tiles_n);
+  }
   // One 16-deep slice of MFMAs from (a, b), with the fragment reads of the next slice (from
   // rst / rkk into ra, rb) and, if LOADS, the direct-to-LDS loads of stage ls into buffer
   // lbuf, issued one per MFMA.  The scheduling fences keep that interleave.
+  // extra(t) runs after MFMA t (kDenseAT: the A^T reads and stores).
+  auto noextra = [](int) {};
   auto slice = [&](auto reads, auto loads, const bf16x8_t* a, const bf16x8_t* b,
                    const char* rst, int rkk, bf16x8_t* ra, bf16x8_t* rb, int64_t ls, int lbuf,
-                   int qa = 0, int nq = 0) {
+                   int qa, int nq, auto extra) __attribute__((always_inline)) {
     constexpr bool READS = decltype(reads)::value, LOADS = decltype(loads)::value;
     constexpr int NM = 4 * NJ, NR = 4 + NJ;
 #pragma unroll
@@ -383,13 +447,14 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
         // loads [qa, qa + nq) of stage ls, one per MFMA from the first
         if (t < nq) dma(ls, lbuf, qa + t);
       }
+      extra(t);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
   // Loads are spread over the step: stage s+1's loads go out L0 in the last slice of step s-1
   // (right after its barrier freed stage s-1's buffer), L1 in slice 0 and L2 in slice 1 of
   // step s; the barrier before slice 3 waits for them.
-  auto step = [&](int64_t s, int64_t s_end, auto last) {
+  auto step = [&](int64_t s, int64_t s_end, auto last) __attribute__((always_inline)) {
     constexpr bool LAST = decltype(last)::value;
     const int cur = (int)((s - ks0) & 1), nxt = cur ^ 1;
     const char* cs = smem + cur * kStage;
@@ -397,15 +462,44 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
     // not read again, and the epilogue's barrier drains them.
     const int64_t n1 = s + 1 < s_end ? s + 1 : s_end - 1;
     const int64_t n2 = s + 2 < s_end ? s + 2 : s_end - 1;
-    slice(std::true_type{}, std::true_type{}, fa[0], fb[0], cs, 1, fa[1], fb[1], n1, nxt, L0, L1);
+    // kDenseAT: this tile's A^T pieces of the stage (at most two, u0 and u0 + tiles_n) are
+    // read in slice 1, while the stage is resident, and stored in slice 3, after the barrier.
+    int64_t se = 0;
+    int u0 = 16, u1 = 16;
+    u32x4_t v0 = {0, 0, 0, 0}, v1 = {0, 0, 0, 0};
+    if (MODE == kDenseAT) {
+      se = s + krot;
+      if (se >= ks1) se -= klen;
+      if (s != ks0) {                            // at_u holds the previous stage's piece
+        at_u = se == ks0 ? at_u_wrap : at_u - at_d;
+        if (at_u < 0) at_u += p.tiles_n;
+      }
+      u0 = at_u;
+      u1 = u0 + p.tiles_n;
+    }
+    auto at_rd = [&](int t) __attribute__((always_inline)) {
+      if (MODE == kDenseAT && t == 8) {
+        if (u0 < 16) v0 = at_read(cs, u0);
+        if (u1 < 16) v1 = at_read(cs, u1);
+      }
+    };
+    auto at_st = [&](int t) __attribute__((always_inline)) {
+      if (MODE == kDenseAT && t == 8) {
+        if (u0 < 16) at_store(se, BK, u0, v0);
+        if (u1 < 16) at_store(se, BK, u1, v1);
+      }
+    };
+    slice(std::true_type{}, std::true_type{}, fa[0], fb[0], cs, 1, fa[1], fb[1], n1, nxt, L0, L1,
+          noextra);
     slice(std::true_type{}, std::true_type{}, fa[1], fb[1], cs, 2, fa[0], fb[0], n1, nxt, L0 + L1,
-          L2);
-    slice(std::true_type{}, std::false_type{}, fa[0], fb[0], cs, 3, fa[1], fb[1], 0, 0);
+          L2, at_rd);
+    slice(std::true_type{}, std::false_type{}, fa[0], fb[0], cs, 3, fa[1], fb[1], 0, 0, 0, 0,
+          noextra);
     __builtin_amdgcn_s_waitcnt(0);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     slice(std::integral_constant<bool, !LAST>{}, std::true_type{}, fa[1], fb[1],
-          smem + nxt * kStage, 0, fa[0], fb[0], n2, cur, 0, L0);
+          smem + nxt * kStage, 0, fa[0], fb[0], n2, cur, 0, L0, at_st);
   };
 
   const int64_t nfull = K / BK;                 // the K tail (dense, second half) follows it
@@ -423,6 +517,11 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
     __builtin_amdgcn_sched_barrier(0);
     read_all(smem, 0, fa[0], fb[0]);
     int64_t s = s0;
+    if (MODE == kDenseAT) {
+      int64_t se = s0 + krot;
+      if (se >= ks1) se -= klen;
+      at_u = at_first(se);
+    }
     if (WAVES == 4) {
       // two steps per iteration: with one loop-carried copy of the 256 accumulators the
       // register allocator keeps them in place (a one-step loop body rotates them through
@@ -455,6 +554,10 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
       *reinterpret_cast<uint4*>(smem + lds_of(q) + lane * 16) = v;
     }
     __syncthreads();
+    if (MODE == kDenseAT) {                      // the tail stage, same ownership
+      for (int u = at_first(nfull); u < 16; u += p.tiles_n)
+        at_store(nfull, (int)krem, u, at_read(smem, u));
+    }
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
       if (kk * 16 >= krem) break;                // uniform: the rest of the stage is zeros
@@ -612,12 +715,27 @@ size_t gemm_nt_split_bytes(int64_t M, int64_t N) {
 
 hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
                           int a_mn, const uint16_t* B, int64_t ldb, int b_mn, void* C,
-                          int64_t ldc, int c_f32, float* part, hipStream_t s) {
+                          int64_t ldc, int c_f32, float* part, hipStream_t s, uint16_t* at,
+                          int64_t ldat) {
+  // (a stage's 64 rows of A^T, 128 ldat bytes, stay below 2^31: 32-bit store offsets)
+  if (at != nullptr && (c_f32 || a_mn || b_mn || M % 8 != 0 || ldat < M || ldat % 4 != 0 ||
+                        ldat >= kGemmAtMaxLd || reinterpret_cast<uintptr_t>(at) % 8 != 0))
+    return hipErrorInvalidValue;
+  if (at != nullptr && (N == 0 || (N + BN - 1) / BN < 8)) {
+    // no tiles, or fewer than 8 tile columns (a tile would own more than two A^T pieces per
+    // stage): the transpose kernel writes A^T instead
+    if (M > 0 && K > 0) {
+      const hipError_t e = launch_transpose_bf16(A, M, K, lda, at, ldat, 1, 0, 0, s);
+      if (e != hipSuccess) return e;
+    }
+    at = nullptr;
+  }
   if (M == 0 || N == 0) return hipSuccess;
   if (!nt_offsets_fit(K, lda, ldb, a_mn, b_mn)) return hipErrorInvalidValue;
   NtArgs a{};
   a.A = A; a.B = B; a.C = C; a.lda = lda; a.ldb = ldb; a.ldc = ldc;
   a.M = M; a.N = N; a.K = K;
+  a.at = at; a.ldat = ldat;
   a.vec_store = vec_store_ok(C, ldc, c_f32 ? 4 : 2);
   a.tiles_m = (int)((M + BM - 1) / BM);
   a.tiles_n = (int)((N + BN - 1) / BN);
@@ -648,6 +766,7 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, in
     if (a_mn && b_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, true, true, 8>), grid, b8, 0, s, a);
     else if (b_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, false, true, 8>), grid, b8, 0, s, a);
     else if (a_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, true, false, 8>), grid, b8, 0, s, a);
+    else if (at != nullptr) hipLaunchKernelGGL((gemm_nt_kernel<false, kDenseAT, false, false, 4>), grid, b4, 0, s, a);
     else hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, false, false, 4>), grid, b4, 0, s, a);
   }
   if (a.part != nullptr)

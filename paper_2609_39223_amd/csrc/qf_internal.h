@@ -46,10 +46,15 @@ hipError_t launch_quant_t_grouped(int fmt, const uint16_t* x, int64_t T, int64_t
 // ---- GEMMs --------------------------------------------------------------------------------
 // NT GEMM (qf_gemm_nt.hip): C[m, n] = sum_k A(m, k) B(n, k).  A is [M][K] (k contiguous) or,
 // with a_mn, [K][M] (m contiguous); likewise B [N][K] or [K][N] with b_mn.  Row strides and
-// K multiples of 8.
+// K multiples of 8.  With `at` (bf16 C, both operands k-major, M % 8 == 0, M <= ldat <
+// kGemmAtMaxLd, ldat a multiple of 4, at 8-byte aligned) the launch also writes A^T [K][M]
+// (row stride ldat): from the tiles it stages anyway when N spans at least 8 tile columns,
+// else with the transpose kernel; other arguments give hipErrorInvalidValue.
+constexpr int64_t kGemmAtMaxLd = (int64_t)1 << 24;
 hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
                           int a_mn, const uint16_t* B, int64_t ldb, int b_mn, void* C,
-                          int64_t ldc, int c_f32, float* part, hipStream_t s);
+                          int64_t ldc, int c_f32, float* part, hipStream_t s,
+                          uint16_t* at = nullptr, int64_t ldat = 0);
 // Bytes of the FP32 partial buffer `part` an [M, N] FP32-output launch may use (a K-split
 // of the last partial round of tiles).  part may be null: no split.
 size_t gemm_nt_split_bytes(int64_t M, int64_t N);

@@ -49,6 +49,28 @@ def test_gemm_layouts_ragged(qf, a_km, b_km, c32, M, N, K):
     assert_close(got, oracle.linear_fwd(A, B), f"gemm a_km={a_km} b_km={b_km}")
 
 
+@pytest.mark.parametrize("M,N,K", [(264, 2056, 200), (512, 64, 136), (1032, 2304, 4104),
+                                   (8, 2048, 8), (64, 0, 72), (2048, 4096, 1024)])
+def test_gemm_with_transposed_a_output(qf, M, N, K):
+    """qf_gemm_bf16_at: C bit-identical to qf_gemm_bf16 and at = A^T exactly, padding columns
+    untouched (8 or 9 tile columns: A^T from the GEMM's staged tiles, ragged last stage and
+    rows; 1 tile column or N = 0: from the transpose kernel)."""
+    rng = np.random.default_rng(M * 5 + N + K)
+    A, B = _rand_bf16(rng, (M, K)), _rand_bf16(rng, (N, K))
+    Ad, Bd = to_dev(A), to_dev(B)
+    ldat = M + 12
+    at = torch.full((K, ldat), 0x1234, dtype=torch.int16, device="cuda")
+    C = empty_bf16((M, N))
+    qf.gemm_bf16_at(M, N, K, Ad, K, Bd, K, C, N, at, ldat)
+    C2 = empty_bf16((M, N))
+    qf.gemm_bf16(M, N, K, Ad, K, 1, Bd, K, 1, C2, N, 0)
+    torch.cuda.synchronize()
+    assert np.array_equal(from_dev(C).view(np.uint16), from_dev(C2).view(np.uint16))
+    a_t = from_dev(at).view(np.uint16)
+    assert np.array_equal(a_t[:, :M], A.T)
+    assert np.all(a_t[:, M:] == 0x1234)
+
+
 def test_gemm_zero_depth_writes_zeros(qf):
     C = torch.full((64, 64), 7.0, dtype=torch.float32, device="cuda")
     A = torch.zeros(64, 8, dtype=torch.int16, device="cuda")
@@ -257,6 +279,30 @@ def test_layer_token_count_multiple_of_16384(qf, wfmt, afmt, reuse):
     assert_close(bf16_to_f64(Y), oracle.linear_fwd(ahat, what), "Y")
     assert_close(bf16_to_f64(dX), oracle.linear_dx(w["dY"], what), "dX")
     assert_close(dW.astype(np.float64), oracle.linear_dw(w["dY"], ahat), "dW")
+
+
+@pytest.mark.parametrize("M,N,K", [(512, 264, 768), (1032, 1000, 544), (16384, 136, 1280),
+                                   (8, 72, 32), (2048, 64, 2304)])
+def test_dw_alone_equals_dw_with_dx(qf, M, N, K):
+    """dY^T for dW comes from the dX GEMM (which writes it from the dY tiles it stages) when
+    both gradients are asked for, from the transpose kernel when dW alone is: bit-identical
+    dW (tile columns that own 0 to several stages, a ragged last stage, padded strides)."""
+    rng = np.random.default_rng(M + N + K)
+    w = {"X": _rand_bf16(rng, (M, K)), "W": _rand_bf16(rng, (N, K), 0.02),
+         "dY": _rand_bf16(rng, (M, N))}
+    X, W, dY = to_dev(w["X"]), to_dev(w["W"]), to_dev(w["dY"])
+    d = qf.qlinear_desc(M, N, K, "mxfp4", "mxfp4")
+    outs = []
+    for want_dx in (True, False):
+        ws = qf.workspace(d)
+        dX = empty_bf16((M, K)) if want_dx else None
+        dW = torch.full((N, K), 7.0, dtype=torch.float32, device="cuda")
+        qf.qlinear_bwd_ste(d, dY, X, W, dX, dW, ws)
+        torch.cuda.synchronize()
+        outs.append(from_dev(dW))
+    assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
+    ahat = oracle.mxfp4(w["X"])["xhat"]
+    assert_close(outs[0].astype(np.float64), oracle.linear_dw(w["dY"], ahat), "dW")
 
 
 def test_dense_down_projection_32k_tokens_sampled(qf):
