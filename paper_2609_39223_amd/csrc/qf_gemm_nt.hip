@@ -7,9 +7,12 @@
 //   dX          = dY W_hat             A = dY [M, N],      B = W_hat^T [K, N]
 //   dW          = dY^T A_hat           A = dY^T [N, M],    B = A_hat^T [K, M]
 //
-// Design (256 x 256 block tile, 512 lanes = 8 wavefronts, two per SIMD):
-//  - Each wavefront owns a 128 x 64 sub-tile as 4 x 2 v_mfma_f32_32x32x16_bf16 accumulators;
-//    the second wavefront on a SIMD issues MFMAs while the first waits.
+// Design (256 x 256 block tile):
+//  - k-contiguous operands (every layer product): 4 wavefronts, one per SIMD, each owning a
+//    128 x 128 sub-tile as 4 x 4 v_mfma_f32_32x32x16_bf16 accumulators (256 AGPRs).  Operands
+//    stored with K as rows: 8 wavefronts, two per SIMD, 128 x 64 each (4 x 2 accumulators).
+//    The bullets below describe the eight-wavefront load split; the four-wavefront form loads
+//    64 rows of both operands per wavefront (see the kernel).
 //  - K advances in 64-deep stages, double-buffered in LDS (2 x 64 KB).  A stage row is 128
 //    bytes, so every global request is a whole 128-byte cache line (32-deep stages fetch half
 //    lines and double the L2 request count).
@@ -32,6 +35,10 @@
 //    different banks) and writes whole rows with 16-byte stores; FP32 tiles go in two halves.
 //  - Block ids are remapped so each XCD (own L2) works on a contiguous group of tiles, and
 //    each XCD walks K from its own rotated start (HBM channel spread).
+//  - Optionally (kDenseAT, the backward's dX = dY W_hat) the launch also writes A^T: each
+//    staged k stage of A is split into 16 pieces of 4 k-rows, each owned by one tile of the
+//    row panel, which gathers its piece from LDS before the step's barrier and stores it as
+//    whole 128-byte rows after it.  That replaces a separate transpose pass over dY.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
