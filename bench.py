@@ -57,15 +57,16 @@ def measured_traffic(launch):
     (copy-calibrated), or None when no summary covers it or the kernel source has changed since
     the counters were taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "gemm_nt_wgrad_mlp_up_traffic.json")
+    path = os.path.join(ROOT, "profiles", "gemm_nt_mlp_up_step_traffic.json")
     try:
         rec = json.load(open(path))
         src = open(os.path.join(ROOT, rec["source"]), "rb").read()
-    except (OSError, ValueError, KeyError):
+        entry = rec["launches"].get(launch)
+    except (OSError, ValueError, KeyError, AttributeError):
         return None
-    if rec.get("launch") != launch or hashlib.sha256(src).hexdigest() != rec["source_sha256"]:
+    if entry is None or hashlib.sha256(src).hexdigest() != rec["source_sha256"]:
         return None
-    return rec["bytes"]
+    return entry["bytes"]
 
 
 def copy_calibration():
