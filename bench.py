@@ -35,8 +35,9 @@ PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=10)
-    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--steps", type=int, default=20)
+    # untimed: the GPU clock under back-to-back GEMMs settles over the first ~10 steps
+    p.add_argument("--warmup", type=int, default=25)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-rows", type=int, default=256,
                    help="token rows in the CPU oracle's bounded sample of the step")
