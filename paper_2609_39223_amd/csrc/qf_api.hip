@@ -550,6 +550,12 @@ qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int64_t* gr
   QF_TRY(grouped_quantize(d, X, W, g, !reuse && dX && !fuse_w, false, &Wop, &Aop, s));
   QF_TRY(dev(qf::launch_grouped_prep(group_offsets, d->E, g.tile_start, g.order, g.kstart, s),
              "prep"));
+  // dY^T in the padded layout of dW is written by the dX launch from the dY tiles it stages
+  // when both gradients are asked for and dX spans at least 8 tile columns (K >= 1793);
+  // otherwise by the grouped transposer
+  const int64_t tp = grouped_tpad(d), ldt = ws_ld(tp);
+  const bool dyt_by_dx = dX != nullptr && dW != nullptr && (d->K + 255) / 256 >= 8 &&
+                         ldt < qf::kGemmAtMaxLd;
   if (dX) {
     if (fuse_w) {
       const float* gp = d->w_amax;
@@ -567,16 +573,17 @@ qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int64_t* gr
                  "transpose expert W_hat"));
     }
     QF_TRY(dev(qf::launch_grouped_nt_rows(d->E, d->T, d->K, d->N, group_offsets, g.tile_start, dY,
-                                          d->N, g.whatt, d->N, 0, d->N * d->K, dX, d->K, s),
+                                          d->N, g.whatt, d->N, 0, d->N * d->K, dX, d->K, s,
+                                          dyt_by_dx ? g.dyt : nullptr, ldt, g.kstart),
                "grouped dX"));
   }
   if (dW) {
     // dW_e = dY_e^T A_hat_e as one NT launch over padded, transposed token columns: expert e
     // contracts over its own 64-aligned column range (zeros past its last token).
-    const int64_t tp = grouped_tpad(d), ldt = ws_ld(tp);
-    QF_TRY(dev(qf::launch_quant_t_grouped(QF_FMT_NONE, dY, d->T, d->N, group_offsets, g.kstart,
-                                          d->E, g.dyt, ldt, s),
-               "transpose dY (grouped)"));
+    if (!dyt_by_dx)
+      QF_TRY(dev(qf::launch_quant_t_grouped(QF_FMT_NONE, dY, d->T, d->N, group_offsets, g.kstart,
+                                            d->E, g.dyt, ldt, s),
+                 "transpose dY (grouped)"));
     const bool saved = d->afmt != QF_FMT_NONE && reuse;
     QF_TRY(dev(qf::launch_quant_t_grouped(saved ? QF_FMT_NONE : d->afmt, saved ? g.ahat : X, d->T,
                                           d->K, group_offsets, g.kstart, d->E, g.at, ldt, s),

@@ -69,8 +69,8 @@ constexpr int kPitch32 = BN * 4 + 32;            // epilogue LDS row pitch, FP32
 constexpr int kSmemEpi = (BM * kPitch16 > 128 * kPitch32) ? BM * kPitch16 : 128 * kPitch32;
 constexpr int kSmem = (2 * kStage > kSmemEpi) ? 2 * kStage : kSmemEpi;
 
-// kDenseAT: dense, and the launch also writes A^T (see NtArgs::at).
-enum Mode { kDense = 0, kGroupRows = 1, kGroupK = 2, kDenseAT = 3 };
+// kDenseAT / kGroupRowsAT: dense / grouped rows, and the launch also writes A^T (NtArgs::at).
+enum Mode { kDense = 0, kGroupRows = 1, kGroupK = 2, kDenseAT = 3, kGroupRowsAT = 4 };
 
 struct NtArgs {
   const uint16_t* A;
@@ -99,10 +99,10 @@ struct NtArgs {
   float* part;
   int split_from, full_per_xcd, split_per_xcd;
   int64_t split_stage;
-  // kDenseAT: A^T [K][M] (row stride ldat) is written as a by-product of the main loop.  Tile
-  // (tm, tn) owns the k stages s with s % tiles_n == tn of its 256-row panel and writes them
-  // from LDS while they are resident, so every stage of every panel is written exactly once
-  // and no kernel re-reads A to transpose it.
+  // kDenseAT / kGroupRowsAT: A^T (row stride ldat) is written as a by-product of the main
+  // loop, from the A tiles in LDS (see the kernel).  Dense: A^T [K][M].  Grouped rows: the
+  // padded layout of the grouped weight gradient, expert e's rows at columns 64 kstart[e] + i
+  // and zeros up to 64 kstart[e+1].
   uint16_t* at;
   int64_t ldat;
 };
@@ -187,7 +187,8 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform (scalar) index
   const int wm = WAVES == 8 ? w >> 2 : w >> 1, wn = WAVES == 8 ? w & 3 : w & 1;
   constexpr bool DENSE = MODE == kDense || MODE == kDenseAT;
-  static_assert(MODE != kDenseAT || (!C_F32 && WAVES == 4), "A^T output: bf16 four-wavefront form");
+  constexpr bool AT = MODE == kDenseAT || MODE == kGroupRowsAT;
+  static_assert(!AT || (!C_F32 && WAVES == 4 && !A_MN && !B_MN), "A^T output: bf16 4-wave form");
   const int item = remap_xcd(blockIdx.x, gridDim.x);
   int bid = item, half = -1, pidx = 0;
   if (DENSE && C_F32 && p.part != nullptr) {
@@ -207,6 +208,9 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
   int64_t m0, m_end, n0;
   int64_t ks0 = 0, ks1 = p.K / BK;               // stage range of this item
   int64_t cofs = 0;                              // element offset of this item's C
+  // A^T columns of this tile's first row and the end of its A^T range: rows whose column is
+  // below at_end but lie past the operand get zeros (grouped padding)
+  int64_t at_col0 = 0, at_end = 0;
   if (DENSE || MODE == kGroupK) {
     int t = bid;
     if (MODE == kGroupK) {
@@ -233,6 +237,8 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
     m0 = (int64_t)(first + (t % per_group) % gs) * BM;
     m_end = p.M;
     n0 = (int64_t)((t % per_group) / gs) * BN;
+    at_col0 = m0;
+    at_end = m_end;
   } else {
     // The grid is sized for the most row tiles any routing can need; the real count is
     // tile_start[E].  Block b runs on XCD x = b % 8 as its item j = b / 8, and XCD x takes the
@@ -251,6 +257,10 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
     m0 = p.off[lo] + (int64_t)(mt - p.tile_start[lo]) * BM;
     m_end = p.off[lo + 1];
     n0 = (int64_t)tn * BN;
+    if (AT) {
+      at_col0 = 64 * (int64_t)p.kstart[lo] + (m0 - p.off[lo]);
+      at_end = 64 * (int64_t)p.kstart[lo + 1];
+    }
     Bp += (int64_t)lo * p.bstride;
   }
   const int64_t n_end = p.N, K = p.K;
@@ -411,12 +421,13 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
     return h;
   };
   // byte offset of this lane's 8 bytes of piece 0 within a stage's rows of A^T (below 2^31)
-  const int at_off = (int)(((int64_t)at_c * p.ldat + m0 + at_r) * 2);
+  const int at_off = (int)(((int64_t)at_c * p.ldat + at_col0 + at_r) * 2);
   const int at_ld8 = (int)(p.ldat * 8);          // bytes of 4 rows of A^T
-  const bool at_rok = m0 + at_r < m_end;
+  const bool at_rok = m0 + at_r < m_end;          // data rows
+  const bool at_zok = at_col0 + at_r < at_end;     // data or zero-padding columns
   auto at_store = [&](int64_t se, int kvalid, int u, u32x4_t h) __attribute__((always_inline)) {
-    const u32x2_t v = {h[0] | (h[1] << 16), h[2] | (h[3] << 16)};
-    const bool ok = at_rok && 4 * u + at_c < kvalid;
+    const u32x2_t v = at_rok ? u32x2_t{h[0] | (h[1] << 16), h[2] | (h[3] << 16)} : u32x2_t{0, 0};
+    const bool ok = at_zok && 4 * u + at_c < kvalid;
     const int off = ok ? at_off + u * at_ld8 : 0x7FFFFFF8;
     __builtin_amdgcn_raw_buffer_store_b64(
         v, make_rsrc(p.at + se * BK * p.ldat, (int64_t)kvalid * p.ldat * 2), off, 0, 0);
@@ -430,7 +441,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
   };
   int at_u = 0;
   int at_u_wrap = 0, at_d = 0;
-  if (MODE == kDenseAT) {
+  if (AT) {
     at_u_wrap = at_first(ks0);                   // the stage after the wrap to ks0
     at_d = (int)(16 % p.tiles_n);
   }
@@ -474,7 +485,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
     int64_t se = 0;
     int u0 = 16, u1 = 16;
     u32x4_t v0 = {0, 0, 0, 0}, v1 = {0, 0, 0, 0};
-    if (MODE == kDenseAT) {
+    if (AT) {
       se = s + krot;
       if (se >= ks1) se -= klen;
       if (s != ks0) {                            // at_u holds the previous stage's piece
@@ -485,13 +496,13 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
       u1 = u0 + p.tiles_n;
     }
     auto at_rd = [&](int t) __attribute__((always_inline)) {
-      if (MODE == kDenseAT && t == 8) {
+      if (AT && t == 8) {
         if (u0 < 16) v0 = at_read(cs, u0);
         if (u1 < 16) v1 = at_read(cs, u1);
       }
     };
     auto at_st = [&](int t) __attribute__((always_inline)) {
-      if (MODE == kDenseAT && t == 8) {
+      if (AT && t == 8) {
         if (u0 < 16) at_store(se, BK, u0, v0);
         if (u1 < 16) at_store(se, BK, u1, v1);
       }
@@ -524,7 +535,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
     __builtin_amdgcn_sched_barrier(0);
     read_all(smem, 0, fa[0], fb[0]);
     int64_t s = s0;
-    if (MODE == kDenseAT) {
+    if (AT) {
       int64_t se = s0 + krot;
       if (se >= ks1) se -= klen;
       at_u = at_first(se);
@@ -561,7 +572,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
       *reinterpret_cast<uint4*>(smem + lds_of(q) + lane * 16) = v;
     }
     __syncthreads();
-    if (MODE == kDenseAT) {                      // the tail stage, same ownership
+    if (AT) {                      // the tail stage, same ownership
       for (int u = at_first(nfull); u < 16; u += p.tiles_n)
         at_store(nfull, (int)krem, u, at_read(smem, u));
     }
@@ -785,18 +796,24 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, in
 hipError_t launch_grouped_nt_rows(int64_t E, int64_t T, int64_t N, int64_t K, const int64_t* off,
                                   const int* tile_start, const uint16_t* A, int64_t lda,
                                   const uint16_t* B, int64_t ldb, int b_mn, int64_t bstride,
-                                  uint16_t* C, int64_t ldc, hipStream_t s) {
+                                  uint16_t* C, int64_t ldc, hipStream_t s, uint16_t* at,
+                                  int64_t ldat, const int* kstart) {
+  if (at != nullptr && (b_mn || (N + BN - 1) / BN < 8 || kstart == nullptr || ldat % 4 != 0 ||
+                        ldat >= kGemmAtMaxLd || reinterpret_cast<uintptr_t>(at) % 8 != 0))
+    return hipErrorInvalidValue;
   if (T == 0 || N == 0 || E == 0) return hipSuccess;
   if (!nt_offsets_fit(K, lda, ldb, false, b_mn)) return hipErrorInvalidValue;
   NtArgs a{};
   a.A = A; a.B = B; a.C = C; a.lda = lda; a.ldb = ldb; a.ldc = ldc; a.bstride = bstride;
   a.M = T; a.N = N; a.K = K; a.off = off; a.tile_start = tile_start; a.E = (int)E;
+  a.at = at; a.ldat = ldat; a.kstart = kstart;
   a.vec_store = vec_store_ok(C, ldc, 2);
   a.tiles_n = (int)((N + BN - 1) / BN);
   a.tiles_m = (int)((T + BM - 1) / BM + E);
   const int64_t per = ((int64_t)a.tiles_m * a.tiles_n + kXcds - 1) / kXcds;
   const dim3 grid((unsigned)(kXcds * per));
   if (b_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRows, false, true, 8>), grid, dim3(8 * 64), 0, s, a);
+  else if (at != nullptr) hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRowsAT, false, false, 4>), grid, dim3(4 * 64), 0, s, a);
   else hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRows, false, false, 4>), grid, dim3(4 * 64), 0, s, a);
   return hipGetLastError();
 }

@@ -65,11 +65,16 @@ hipError_t launch_grouped_nt_k(int64_t E, int64_t M, int64_t N, int64_t Kpad, co
                                 const uint16_t* B, int64_t ldb, float* C, int64_t ldc,
                                 int64_t cstride, hipStream_t s);
 // Grouped NT: rows [off[e], off[e+1]) of A use B + e * bstride ([N][K], k contiguous, or
-// [K][N] with b_mn).
+// [K][N] with b_mn).  With `at` (k-contiguous B, N spanning at least 8 tile columns, kstart
+// from launch_grouped_prep, ldat a multiple of 4 below kGemmAtMaxLd, at 8-byte aligned) the
+// launch also writes A^T in the padded layout of the grouped weight gradient: row k, column
+// 64 kstart[e] + i holds A[off[e] + i][k], zeros up to 64 kstart[e+1].
 hipError_t launch_grouped_nt_rows(int64_t E, int64_t T, int64_t N, int64_t K, const int64_t* off,
                                   const int* tile_start, const uint16_t* A, int64_t lda,
                                   const uint16_t* B, int64_t ldb, int b_mn, int64_t bstride,
-                                  uint16_t* C, int64_t ldc, hipStream_t s);
+                                  uint16_t* C, int64_t ldc, hipStream_t s,
+                                  uint16_t* at = nullptr, int64_t ldat = 0,
+                                  const int* kstart = nullptr);
 // bf16 transpose (qf_transpose.hip): out[c][r] = in[r][c] for `batch` matrices spaced ibs / obs
 // elements apart; R and C multiples of 8.
 hipError_t launch_transpose_bf16(const uint16_t* in, int64_t R, int64_t C, int64_t ldi,

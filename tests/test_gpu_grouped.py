@@ -84,6 +84,40 @@ def test_grouped_dw_tile_grid_split_over_xcds(qf):
             assert np.all(dW[e] == 0.0)
 
 
+def test_grouped_dw_alone_equals_dw_with_dx(qf):
+    """With 8 or more tile columns in dX the grouped dX launch writes the padded dY^T for dW
+    (zeros past each expert's last token, written by the tile holding its last rows); asked
+    for alone, dW takes it from the grouped transposer: bit-identical dW, equal to the oracle."""
+    rng = np.random.default_rng(26)
+    E, N, K = 5, 136, 2048
+    counts = np.array([0, 300, 1, 513, 77])
+    offsets = np.concatenate([[0], np.cumsum(counts)])
+    T = int(offsets[-1])
+    X = workloads.normal_bf16(rng, (T, K))
+    W = np.stack([workloads.normal_bf16(rng, (N, K), 0.02 * (e + 1)) for e in range(E)])
+    dY = workloads.normal_bf16(rng, (T, N))
+    d = qf.grouped_desc(E, T, N, K, "nvfp4", "none")
+    off = torch.from_numpy(offsets.astype(np.int64)).cuda()
+    Xd, Wd, dYd = to_dev(X), to_dev(W.reshape(E * N, K)), to_dev(dY)
+    outs = []
+    for want_dx in (True, False):
+        ws = qf.grouped_workspace(d)
+        ws.fill_(0x5A)                              # stale workspace bytes must not leak in
+        dX = empty_bf16((T, K)) if want_dx else None
+        dW = torch.full((E, N, K), 7.0, dtype=torch.float32, device="cuda")
+        qf.qlinear_grouped_bwd_ste(d, off, dYd, Xd, Wd, dX, dW, ws)
+        torch.cuda.synchronize()
+        outs.append(from_dev(dW))
+    assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
+    for e in range(E):
+        r0, r1 = offsets[e], offsets[e + 1]
+        if r1 > r0:
+            assert_close(outs[0][e].astype(np.float64), oracle.linear_dw(dY[r0:r1], X[r0:r1]),
+                         f"dW e={e}")
+        else:
+            assert np.all(outs[0][e] == 0.0)
+
+
 def test_grouped_padded_token_count_multiple_of_16384(qf):
     """Two experts whose 64-aligned padded token count is exactly 16384: the dW operands sit
     in the workspace with a row stride of 16384 + 128 elements."""
@@ -125,12 +159,14 @@ def test_grouped_zipf_routing_sampled(qf):
         assert_close(dW[e].astype(np.float64), oracle.linear_dw(dY[r0:r1], X[r0:r1]), f"dW e={e}")
 
 
-def test_moe_down_projection_full_size_sampled(qf):
-    """The MoE layer's down projection at full size (128 experts, Zipf(1.1) top-8 routing of
-    32768 tokens = 262144 rows, 1536 -> 3072, NVFP4 weights) in the launch configuration the
-    benchmark times; entries sampled in the largest, smallest and three other experts."""
+@pytest.mark.parametrize("N,K", [(3072, 1536), (3072, 3072)])
+def test_moe_projection_full_size_sampled(qf, N, K):
+    """The MoE layer's projections at full size (128 experts, Zipf(1.1) top-8 routing of
+    32768 tokens = 262144 rows; down 1536 -> 3072 and gate/up 3072 -> 3072, whose dX launch
+    also writes the padded dY^T; NVFP4 weights) in the launch configuration the benchmark
+    times; entries sampled in the largest, smallest and three other experts."""
     _, offsets = workloads.moe_routing(seed=0, tokens=32768, experts=128, topk=8)
-    E, N, K = 128, 3072, 1536
+    E = 128
     T = int(offsets[-1])
     rng = np.random.default_rng(24)
     X = workloads.normal_bf16(rng, (T, K))
