@@ -35,10 +35,12 @@
 //    different banks) and writes whole rows with 16-byte stores; FP32 tiles go in two halves.
 //  - Block ids are remapped so each XCD (own L2) works on a contiguous group of tiles, and
 //    each XCD walks K from its own rotated start (HBM channel spread).
-//  - Optionally (kDenseAT, the backward's dX = dY W_hat) the launch also writes A^T: each
-//    staged k stage of A is split into 16 pieces of 4 k-rows, each owned by one tile of the
-//    row panel, which gathers its piece from LDS before the step's barrier and stores it as
-//    whole 128-byte rows after it.  That replaces a separate transpose pass over dY.
+//  - Optionally (kDenseAT / kGroupRowsAT, the backward's dX = dY W_hat, dense or per expert)
+//    the launch also writes A^T: each staged k stage of A is split into 16 pieces of 4 k-rows,
+//    each owned by one tile of the row panel, which gathers its piece from LDS before the
+//    step's barrier and stores it as whole 128-byte rows after it.  That replaces a separate
+//    transpose pass over dY (grouped: into the padded per-expert columns of the weight
+//    gradient, zeros included).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -392,17 +394,19 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
 #pragma unroll
     for (int r = 0; r < 4 + NJ; ++r) read_one(st, kk, r, a, b);
   };
-  // ---- A^T output (kDenseAT) ---------------------------------------------------------------------
+  // ---- A^T output (kDenseAT, kGroupRowsAT) ---------------------------------------------------
   // A stage's A^T is 16 pieces: piece u is k columns 4 u .. 4 u + 3 over the tile's 256 rows, so
   // each of its rows of A^T is written as whole 128-byte lines, each line by one store.  Piece
   // u of global stage se belongs to tile column (16 se + u) mod tiles_n, so with tiles_n >= 8 a
   // tile has at most two pieces per stage.  at_read gathers this lane's part of piece u from
   // the stage in LDS (rows r0 .. r0 + 3, r0 = 64 w + 4 (l % 16), of k column kc = 4 u + l / 16;
   // four 2-byte reads through the row swizzle) before the step's barrier; at_store writes
-  // those 8 bytes to A^T row se * 64 + kc, columns m0 + r0 .. +3, after it, so the store has a
-  // whole step to complete before the next barrier's wait.  Stores go through a buffer
-  // resource over the stage's rows of A^T: lanes with rows past the operand or columns at or
-  // past kvalid get an offset beyond its range, which the hardware drops.  (Plain LDS reads:
+  // those 8 bytes to A^T row se * 64 + kc, columns at_col0 + r0 .. +3 (at_col0 = m0 dense, the
+  // padded column of the tile's first row grouped), after it, so the store has a whole step to
+  // complete before the next barrier's wait.  Rows past the operand store zeros while their
+  // column is below at_end (an expert's padding) and nothing beyond it.  Stores go through a
+  // buffer resource over the stage's rows of A^T: lanes with nothing to store (or columns at
+  // or past kvalid) get an offset beyond its range, which the hardware drops.  (Plain LDS reads:
   // the transposing read builtin makes the compiler wait for every direct-to-LDS load in
   // flight first.)
   const int64_t at_tn = n0 / BN;                 // this tile's column
@@ -448,7 +452,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
   // One 16-deep slice of MFMAs from (a, b), with the fragment reads of the next slice (from
   // rst / rkk into ra, rb) and, if LOADS, the direct-to-LDS loads of stage ls into buffer
   // lbuf, issued one per MFMA.  The scheduling fences keep that interleave.
-  // extra(t) runs after MFMA t (kDenseAT: the A^T reads and stores).
+  // extra(t) runs after MFMA t (the A^T modes: the A^T reads and stores).
   auto noextra = [](int) {};
   auto slice = [&](auto reads, auto loads, const bf16x8_t* a, const bf16x8_t* b,
                    const char* rst, int rkk, bf16x8_t* ra, bf16x8_t* rb, int64_t ls, int lbuf,
@@ -480,7 +484,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
     // not read again, and the epilogue's barrier drains them.
     const int64_t n1 = s + 1 < s_end ? s + 1 : s_end - 1;
     const int64_t n2 = s + 2 < s_end ? s + 2 : s_end - 1;
-    // kDenseAT: this tile's A^T pieces of the stage (at most two, u0 and u0 + tiles_n) are
+    // A^T modes: this tile's A^T pieces of the stage (at most two, u0 and u0 + tiles_n) are
     // read in slice 1, while the stage is resident, and stored in slice 3, after the barrier.
     int64_t se = 0;
     int u0 = 16, u1 = 16;
