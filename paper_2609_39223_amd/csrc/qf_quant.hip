@@ -284,11 +284,13 @@ static dim3 amax_grid(int64_t R, int64_t K, int64_t E) {
   return dim3((unsigned)gx, (unsigned)gy, (unsigned)E);
 }
 
-// The amax is a max over all elements, so a contiguous tensor whose rows do not fill the
-// workgroups' lanes (K / 8 chunks not a multiple of kThreads) is read as rows of 8 kThreads
-// elements when its size allows (expert weights 3072 x 3072 and 3072 x 1536: a quarter of
-// the lanes would idle).
-static void amax_view(int64_t& R, int64_t& K) {
+// A contiguous tensor whose rows do not fill the workgroups' lanes (K / 8 chunks not a
+// multiple of kThreads) is read as rows of 8 kThreads elements when its size allows (expert
+// weights 3072 x 3072 and 3072 x 1536: a quarter of the lanes would idle).  Valid wherever
+// the result does not depend on where rows break: the amax (a max over all elements), and the
+// batched NVFP4 x_hat (16-element blocks along rows of a multiple of 16, one scale per
+// tensor).
+static void contiguous_row_view(int64_t& R, int64_t& K) {
   const int64_t row = 8 * kThreads;
   if ((K >> 3) % kThreads != 0 && (R * K) % row == 0) {
     R = R * K / row;
@@ -300,7 +302,7 @@ hipError_t launch_amax(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, flo
                        hipStream_t s) {
   if (R == 0 || K == 0) return hipSuccess;
   if (ldx == K) {
-    amax_view(R, K);
+    contiguous_row_view(R, K);
     ldx = K;
   }
   hipLaunchKernelGGL(amax_kernel, amax_grid(R, K, 1), dim3(kThreads), 0, s, x, R, K, ldx,
@@ -311,7 +313,7 @@ hipError_t launch_amax(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, flo
 hipError_t launch_amax_batched(const uint16_t* x, int64_t E, int64_t R, int64_t K, float* amax,
                                hipStream_t s) {
   if (E == 0 || R == 0 || K == 0) return hipSuccess;
-  amax_view(R, K);                               // tensors are contiguous, R * K apart
+  contiguous_row_view(R, K);                     // tensors are contiguous, R * K apart
   hipLaunchKernelGGL(amax_kernel, amax_grid(R, K, E), dim3(kThreads), 0, s, x, R, K, K, R * K,
                      amax);
   return hipGetLastError();
@@ -335,6 +337,10 @@ hipError_t launch_nvfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, co
 hipError_t launch_nvfp4_batched(const uint16_t* x, int64_t E, int64_t R, int64_t K,
                                 const float* g, uint16_t* xhat, hipStream_t s) {
   if (E == 0 || R == 0 || K == 0) return hipSuccess;
+  // Blocks of 16 lie along the contiguous rows and the scale g[z] covers the whole tensor, so
+  // each (contiguous) tensor may be read as rows of 2048 elements: same blocks, same x_hat,
+  // and every lane busy where K / 8 chunks would leave some idle.
+  contiguous_row_view(R, K);
   dim3 grid = row_grid(R, K, kRowsPerThread);
   grid.z = (unsigned)E;
   hipLaunchKernelGGL(nvfp4_kernel<kRowsPerThread>, grid, dim3(kThreads), 0, s, x, R, K, K,
