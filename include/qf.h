@@ -78,7 +78,9 @@ QF_API const char* qf_last_error(void);
  *   accumulate = 0: *amax = g.   accumulate = 1: *amax = max(*amax, g) -- the running
  *   activation amax of Sec. 3.2.3 (NVFP4 paragraph), and the way to build a tied-scale group
  *   ("Engine-specific scale sharing": call once per member).
- * NaN inputs make *amax NaN.  R = 0 or K = 0 leaves a zero (accumulate = 0) or unchanged value.
+ * K may be any size (no block constraint; ldx >= K, ldx % 8 == 0): elements past K in a row
+ * are never read.  NaN inputs make *amax NaN.  R = 0 or K = 0 leaves a zero (accumulate = 0)
+ * or unchanged value.
  */
 QF_API qf_status qf_amax(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, float* amax,
                   int accumulate, qf_stream_t stream);

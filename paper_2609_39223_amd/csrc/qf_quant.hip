@@ -42,18 +42,28 @@ constexpr int kAmaxRows = 16;
 __global__ __launch_bounds__(kThreads) void amax_kernel(const uint16_t* __restrict__ x, int64_t R,
                                                         int64_t K, int64_t ldx, int64_t tstride,
                                                         float* __restrict__ amax) {
-  const int64_t chunks = K >> 3;
+  const int64_t chunks = (K + 7) >> 3;           // a last partial chunk holds K % 8 elements
   const uint16_t* xt = x + (int64_t)blockIdx.z * tstride;
   uint32_t m = 0;
   for (int64_t c = (int64_t)blockIdx.x * kThreads + threadIdx.x; c < chunks;
        c += (int64_t)gridDim.x * kThreads) {
+    const bool whole = c * 8 + 8 <= K;
     for (int64_t r0 = (int64_t)blockIdx.y * kAmaxRows; r0 < R;
          r0 += (int64_t)gridDim.y * kAmaxRows) {
       uint4 v[kAmaxRows];
 #pragma unroll
       for (int i = 0; i < kAmaxRows; ++i) {
         v[i] = make_uint4(0, 0, 0, 0);
-        if (r0 + i < R) v[i] = *reinterpret_cast<const uint4*>(xt + (r0 + i) * ldx + c * 8);
+        if (r0 + i < R) {
+          const uint16_t* src = xt + (r0 + i) * ldx + c * 8;
+          if (whole) {
+            v[i] = *reinterpret_cast<const uint4*>(src);
+          } else {                                  // the row's last K % 8 elements only
+            uint32_t h[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+            for (int e = 0; e < (int)(K - c * 8); ++e) h[e] = src[e];
+            v[i] = pack8(h);
+          }
+        }
       }
 #pragma unroll
       for (int i = 0; i < kAmaxRows; ++i) {
@@ -273,7 +283,7 @@ hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s) {
 // Grid of amax_kernel: up to 64 x 256 chunks per row pass and kAmaxRows rows per lane pass,
 // at most ~2048 workgroups over all E tensors (so most lanes make one or a few passes).
 static dim3 amax_grid(int64_t R, int64_t K, int64_t E) {
-  const int64_t chunks = K >> 3;
+  const int64_t chunks = (K + 7) >> 3;
   int64_t gx = (chunks + kThreads - 1) / kThreads;
   if (gx > 64) gx = 64;
   int64_t gy = (R + kAmaxRows - 1) / kAmaxRows;

@@ -264,6 +264,40 @@ def test_amax_and_running_accumulate(qf):
     assert float(out.item()) == max(oracle.amax(a), oracle.amax(b))
 
 
+@pytest.mark.parametrize("K,col", [(12, 10), (5, 4), (1, 0), (1003, 1001)])
+def test_amax_row_tail_not_multiple_of_8(qf, K, col):
+    """K % 8 != 0 inside a wider row stride: the row's last K % 8 elements count (the maximum
+    sits there) and the padding past K (larger still) is never read."""
+    rng = np.random.default_rng(K)
+    R, ld = 37, (K + 7) // 8 * 8 + 8
+    x = (rng.standard_normal((R, ld)) * 0.5).astype(np.float32)
+    x[:, K:] = 1e30                               # padding: must not be read
+    x[17, col] = -7.25                            # the maximum |x| among the K columns
+    u = x.view(np.uint32)
+    buf = ((u + (((u >> 16) & 1) + 0x7FFF)) >> 16).astype(np.uint16)
+    out = torch.full((1,), 123.0, dtype=torch.float32, device="cuda")
+    xd = to_dev(buf)[:, :K]
+    qf.amax(xd, out, accumulate=False)
+    torch.cuda.synchronize()
+    assert float(out.item()) == oracle.amax(np.ascontiguousarray(buf[:, :K])) == 7.25
+
+
+def test_q4k_handworked_block_bit_exact(qf):
+    """The hand-worked super-block of the golden fixture: the kernel's 144 bytes equal the
+    bytes worked out by hand (6-bit scale / min rounding, scale-bit and nibble layout)."""
+    from tests.test_oracle_quant import _handworked_q4k_block
+    x, _, _, _, _, blk = _handworked_q4k_block()
+    xr = np.repeat(x, 3, axis=0)                  # a few rows, one super-block each
+    packed = torch.empty(3, 1, 144, dtype=torch.uint8, device="cuda")
+    xhat = empty_bf16((3, 256))
+    qf.fakequant_q4k(to_dev(xr), packed, xhat)
+    torch.cuda.synchronize()
+    got = from_dev(packed)
+    for r in range(3):
+        assert bytes(got[r, 0]) == blk
+    np.testing.assert_array_equal(from_dev(xhat), oracle.q4k(xr)["xhat"])
+
+
 def test_determinism_two_runs(qf):
     w = workloads.mlp_up(seed=1, scale=8, n_scale=8)
     a = run_nvfp4(qf, w["X"])

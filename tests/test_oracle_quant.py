@@ -327,6 +327,52 @@ def test_q4k_scale_field_matches_hand_worked_layout():
             assert blk[16 + 32 * c + l] == q[64 * c + l] | (q[64 * c + 32 + l] << 4)
 
 
+def _handworked_q4k_block():
+    """The hand-worked super-block of tests/golden/q4k_block_handworked.txt: input bf16 bits,
+    listed FP16 d / dmin, 6-bit scales and mins, and the expected 144 bytes."""
+    rows = [l.split() for l in open(os.path.join(GOLDEN, "q4k_block_handworked.txt"))
+            if l.strip() and not l.startswith("#")]
+    vals = rows[:8]
+    x = np.zeros((1, 256), np.uint16)
+    for j, line in enumerate(vals):
+        assert len(line) == 32
+        for i, t in enumerate(line):
+            v = np.float32(int(t) * 2.0 ** -13)
+            u = int(np.array([v]).view(np.uint32)[0])
+            assert u & 0xFFFF == 0, "fixture value not exact in bf16"
+            x[0, 32 * j + i] = (u >> 16) | (0x8000 if t.startswith("-") else 0)
+    dh, mh = (int(v, 16) for v in rows[8])
+    ls = [int(v) for v in rows[9]]
+    lm = [int(v) for v in rows[10]]
+    blk = bytes(int(v, 16) for r in rows[11:] for v in r)
+    assert len(blk) == 144
+    return x, dh, mh, ls, lm, blk
+
+
+def test_q4k_handworked_block_bytes():
+    # Every field and byte of this block was worked out by hand from the reading (nearest 6-bit
+    # scale and min, ties to even) and the public block layout; a truncated or half-up 6-bit
+    # rounding, a swapped nibble or sub-block, or a misplaced scale bit changes the bytes.
+    x, dh, mh, ls, lm, blk = _handworked_q4k_block()
+    q = oracle.q4k(x)
+    got = bytes(q["packed"].reshape(-1))
+    assert got[0:4] == blk[0:4], "d / dmin"
+    assert got[4:16] == blk[4:16], "scale bytes"
+    assert got[16:] == blk[16:], "code bytes"
+    d2, m2, ls2, lm2, q2 = oracle.q4k_unpack_block(q["packed"][0, 0])
+    assert (d2, m2, ls2, lm2) == (dh, mh, ls, lm)
+    assert q2 == [(i % 32 + i // 32) % 16 for i in range(256)]
+    # x_hat follows Eq. q4k-dequant from the listed fields (d = dmin = 2^-10 here, so every
+    # t1 q - t2 is a multiple of 2^-10 below 1024 of them: exact in FP32, rounded once to bf16)
+    xh = bf16_to_f64(q["xhat"][0])
+    for i in range(256):
+        j = i // 32
+        want = np.float32((ls[j] * q2[i] - lm[j]) * 2.0 ** -10)
+        u = int(np.array([want]).view(np.uint32)[0])
+        u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+        assert q["xhat"][0, i] == u, (i, xh[i], float(want))
+
+
 def test_q4k_dequant_of_packed_bytes_reproduces_xhat():
     x = _q4k_inputs(seed=1)
     q = oracle.q4k(x)
@@ -359,9 +405,16 @@ def test_q4k_superblock_scales_match_numpy_float16():
     want_m = (mu.max(-1) / np.float32(63)).astype(np.float32).astype(np.float16).astype(np.float64)
     np.testing.assert_array_equal(d, want_d)
     np.testing.assert_array_equal(m, want_m)
-    # 6-bit scale/min reproduce each sub-block's step and offset to within half a step
+    # the 6-bit scale reproduces each sub-block's step to within half a step of d
     unclamped = ls < 63
     assert np.all(np.abs(d[..., None] * ls - a)[unclamped] <= d[..., None].repeat(8, -1)[unclamped] / 2 * (1 + 1e-6))
+    # and the 6-bit min reproduces each offset to within half a step of dmin (nearest, not
+    # truncated: about half of these offsets sit more than half a step above a multiple)
+    unclamped = (lm < 63) & (m[..., None] > 0)
+    mm = m[..., None].repeat(8, -1)
+    assert np.all(np.abs(mm * lm - mu)[unclamped] <= mm[unclamped] / 2 * (1 + 1e-6))
+    frac = (mu / np.where(mm > 0, mm, 1))[unclamped] % 1.0
+    assert np.count_nonzero(frac > 0.55) > 10    # the check above covers round-up cases
 
 
 def test_q4k_codes_are_nearest_grid_points():
