@@ -1,19 +1,22 @@
-"""Benchmark: one quantization-aware linear layer step (fake quant + BF16 MFMA GEMMs,
-forward + straight-through backward) on one MI355X.
+"""Benchmark: the 9B-class transformer layer at 32K tokens through the quantization-aware
+linear layer (NVFP4 weight fake quant + BF16 MFMA GEMMs, forward + straight-through backward)
+on one MI355X.
 
-Workload (default): the 8B-class MLP up-projection with MXFP4 weights and activations,
-X [8192, 4096], W [14336, 4096], dY [8192, 14336] (seeded synthetic bf16, see workloads/).
-One step is the layer's two C-ABI calls, qf_qlinear_fwd then qf_qlinear_bwd_ste, which run
-the whole hot path:
-    forward:  Q(W) -> W_hat, Q(X) -> X_hat (MXFP4 quantize-dequantize), Y = X_hat W_hat^T
-    backward: Q(W) -> W_hat^T and Q(X) -> X_hat^T (transposing quantizer: the quantized
-              tensors are transient, as in the paper), dY^T, dX = dY W_hat,
-              dW = dY^T X_hat (FP32); all three products are NT GEMMs
-`value` is the step's throughput in TFLOP/s over the three GEMMs' 3 * 2MNK flops, with the
-quantization time inside the step.  A second pass issues the same kernels one C-ABI call at a
-time, each bracketed by HIP events on the stream it runs on: that gives the per-kernel
-durations of the roofline record.  The fake-quant kernel bandwidth is measured separately
-over rotating input buffers (>1 GB) so the 256 MB MALL cannot serve repeated reads.
+Workload (the headline): one 32768-token sequence through a 9B-class dense layer's four fused
+linears -- QKV 4096 -> 6144 (4096 + 1024 + 1024, one tied tensor scale), O 4096 -> 4096,
+gate/up 4096 -> 2 x 12288 (tied), down 12288 -> 4096 -- seven projections, NVFP4 weight-only;
+activations x = z |tau_c| with z ~ N(0,1) and heavy-tailed per-channel tau_c ~ Student-t(3),
+weights ~ N(0, 0.02), upstream gradients ~ N(0,1) (seeded, drawn on the GPU).  One step is
+the eight C-ABI calls qf_qlinear_fwd + qf_qlinear_bwd_ste of the four linears, which run the
+whole hot path per linear:
+    forward:  amax(W) -> g, Q(W) -> W_hat (NVFP4 quantize-dequantize), Y = X W_hat^T
+    backward: amax(W), Q(W) -> W_hat^T (transposing quantizer), dX = dY W_hat with dY^T as a
+              by-product, X^T, dW = dY^T X (FP32); all three products are NT GEMMs
+`value` is the step's throughput in TFLOP/s over the 21 GEMMs' 3 * 2MNK flops (37.93 TF),
+quantization and transposes inside the step.  A second pass issues the same kernels one
+C-ABI call at a time, each bracketed by HIP events on the stream it runs on: that gives the
+per-kernel durations of the roofline record.  Rows time the other configurations (the MXFP4
+MLP up-projection, the quantizers over rotating buffers, the MoE layer, Q4_K export, ...).
 
 Prints ONE JSON line.  Only --gpus 1 is supported.
 """
@@ -30,44 +33,49 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense BF16 MFMA
 PEAK_HBM_GBPS = 8000.0        # MI355X HBM3E
+METRIC = "fake-quant GB/s and fused fake-quant+BF16 GEMM TFLOP/s (fwd+bwd), 1 MI355X"
 
 
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=20)
-    # untimed: the GPU clock under back-to-back GEMMs settles over the first ~10 steps
-    p.add_argument("--warmup", type=int, default=25)
+    # untimed: the GPU clock under back-to-back GEMMs settles over the first steps
+    p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-rows", type=int, default=256,
+    p.add_argument("--cpu-rows", type=int, default=32,
                    help="token rows in the CPU oracle's bounded sample of the step")
     p.add_argument("--main-only", action="store_true",
-                   help="time only the MXFP4 MLP up-projection step (used for counter runs)")
+                   help="time only the headline step and its per-call pass (no rows, no CPU "
+                        "baseline)")
+    p.add_argument("--phases-once", action="store_true",
+                   help="issue the headline's per-call pass once, with no warm-up or timing "
+                        "(dispatch order = phase order; used for the HBM counter runs)")
     p.add_argument("--rows", default=None,
-                   help="run only these secondary row groups (comma-separated: quant, dense, moe, "
-                        "lora, moe_lora, kl, q4k) and print them as one JSON object; no step timing "
-                        "(used for per-row kernel traces)")
+                   help="run only these secondary row groups (comma-separated: mlp_up, quant, "
+                        "moe, lora, moe_lora, kl, q4k) and print them as one JSON object; no "
+                        "headline step (used for per-row kernel traces)")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain 1 GiB device-to-device copy (reference for the "
                         "HBM byte counters) and exit")
     return p.parse_args()
 
 
-def measured_traffic(launch):
-    """HBM bytes per launch of `launch` from the committed FETCH_SIZE/WRITE_SIZE counter summary
-    (copy-calibrated), or None when no summary covers it or the kernel source has changed since
-    the counters were taken."""
+def measured_traffic(profile, launch):
+    """HBM bytes per launch of `launch` from a committed FETCH_SIZE / WRITE_SIZE counter
+    summary (copy-calibrated) under profiles/, or None when none covers it or a kernel source
+    has changed since the counters were taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "gemm_nt_mlp_up_step_traffic.json")
+    path = os.path.join(ROOT, "profiles", profile)
     try:
         rec = json.load(open(path))
-        src = open(os.path.join(ROOT, rec["source"]), "rb").read()
+        for src, sha in rec["sources"].items():
+            if hashlib.sha256(open(os.path.join(ROOT, src), "rb").read()).hexdigest() != sha:
+                return None
         entry = rec["launches"].get(launch)
     except (OSError, ValueError, KeyError, AttributeError):
         return None
-    if entry is None or hashlib.sha256(src).hexdigest() != rec["source_sha256"]:
-        return None
-    return entry["bytes"]
+    return None if entry is None else entry["bytes"]
 
 
 def copy_calibration():
@@ -83,6 +91,51 @@ def copy_calibration():
     print(json.dumps({"copy_calibration_bytes": 1 << 30, "repeats": 5}), flush=True)
 
 
+def dense_layer_inputs(torch, dev, gen):
+    """The 9B-class layer's four fused linears at T = 32768 (seeded draws on the GPU)."""
+    import workloads
+    T = 32768
+    lins = []
+    for name, n, k in workloads.DENSE_LINEARS:
+        tau = torch.from_numpy(np.abs(np.random.default_rng(k).standard_t(3.0, size=k))
+                               .astype(np.float32)).to(dev)
+        X = _randn_bf16(torch, gen, (T, k), col_scale=tau)
+        W = _randn_bf16(torch, gen, (n, k), 0.02)
+        dY = _randn_bf16(torch, gen, (T, n))
+        lins.append({"name": name, "T": T, "N": n, "K": k, "X": X, "W": W, "dY": dY})
+    return lins
+
+
+def dense_phase_calls(qf, torch, dev, lin):
+    """The kernels one linear's qf_qlinear_fwd + qf_qlinear_bwd_ste launch (NVFP4 weights,
+    W computed amax, bf16 activations), one C-ABI call each, in the layer's order."""
+    T, N, K = lin["T"], lin["N"], lin["K"]
+    X, W, dY = lin["X"], lin["W"], lin["dY"]
+    ldm = T + 128 if T % 16384 == 0 else T        # the layer workspace's padded stride
+    g = torch.zeros(1, dtype=torch.float32, device=dev)
+    what = torch.empty(N, K, dtype=torch.bfloat16, device=dev)
+    whatt = torch.empty(K, N, dtype=torch.bfloat16, device=dev)
+    xt = torch.empty(K, ldm, dtype=torch.bfloat16, device=dev)
+    dyt = torch.empty(N, ldm, dtype=torch.bfloat16, device=dev)
+    Y = torch.empty(T, N, dtype=torch.bfloat16, device=dev)
+    dX = torch.empty(T, K, dtype=torch.bfloat16, device=dev)
+    dW = torch.empty(N, K, dtype=torch.float32, device=dev)
+    gws = qf.gemm_workspace(N, K, 1)
+    nm = lin["name"]
+    return [
+        (f"{nm}.amax_W", 0.0, lambda: qf.amax(W, g)),
+        (f"{nm}.quant_W", 0.0, lambda: qf.fakequant_nvfp4(W, g, qf.AMAX_GIVEN, None, None, None, what)),
+        (f"{nm}.gemm_fwd", 2.0 * T * N * K, lambda: qf.gemm_bf16(T, N, K, X, K, 1, what, K, 1, Y, N, 0)),
+        (f"{nm}.amax_W_bwd", 0.0, lambda: qf.amax(W, g)),
+        (f"{nm}.quant_W_transposed", 0.0, lambda: qf.fakequant_transposed(W, "nvfp4", whatt, amax=g)),
+        (f"{nm}.gemm_dX_and_dY_transposed", 2.0 * T * N * K,
+         lambda: qf.gemm_bf16_at(T, K, N, dY, N, whatt, N, dX, K, dyt, ldm)),
+        (f"{nm}.transpose_X", 0.0, lambda: qf.transpose_bf16(X, xt)),
+        (f"{nm}.gemm_dW", 2.0 * T * N * K,
+         lambda: qf.gemm_bf16(N, K, T, dyt, ldm, 1, xt, ldm, 1, dW, K, 1, ws=gws)),
+    ]
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -94,7 +147,6 @@ def main():
         return
     import torch
     import paper_2609_39223_amd as qf
-    import workloads
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -103,24 +155,36 @@ def main():
         print(json.dumps({"rows": other_rows(qf, torch, dev, set(args.rows.split(",")))}),
               flush=True)
         return
-    w = workloads.mlp_up(seed=0)
-    M, N, K = w["M"], w["N"], w["K"]
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(0)
+    lins = dense_layer_inputs(torch, dev, gen)
 
-    def up(a):
-        return torch.from_numpy(a.view(np.int16)).to(dev)
+    if args.phases_once:
+        calls = [c for lin in lins for c in dense_phase_calls(qf, torch, dev, lin)]
+        torch.cuda.synchronize()
+        for name, _, fn in calls:
+            print(name, flush=True)
+            fn()
+            torch.cuda.synchronize()
+        print(json.dumps({"phases_once": [c[0] for c in calls]}), flush=True)
+        return
 
-    X, W, dY = up(w["X"]), up(w["W"]), up(w["dY"])
-    Y = torch.empty(M, N, dtype=torch.int16, device=dev)
-    dX = torch.empty(M, K, dtype=torch.int16, device=dev)
-    dW = torch.empty(N, K, dtype=torch.float32, device=dev)
-
-    # ---- the timed step: the layer's two C-ABI calls, forward then STE backward ------------
-    desc = qf.qlinear_desc(M, N, K, "mxfp4", "mxfp4")
-    ws = qf.workspace(desc)
+    # ---- the timed step: the four linears' C-ABI calls, forward then STE backward ---------
+    layer = []
+    flops = 0.0
+    for lin in lins:
+        T, N, K = lin["T"], lin["N"], lin["K"]
+        d = qf.qlinear_desc(T, N, K, "nvfp4", "none")
+        layer.append((d, lin["X"], lin["W"], lin["dY"],
+                      torch.empty(T, N, dtype=torch.bfloat16, device=dev),
+                      torch.empty(T, K, dtype=torch.bfloat16, device=dev),
+                      torch.empty(N, K, dtype=torch.float32, device=dev), qf.workspace(d)))
+        flops += 3 * 2.0 * T * N * K
 
     def layer_step():
-        qf.qlinear_fwd(desc, X, W, Y, ws)
-        qf.qlinear_bwd_ste(desc, dY, X, W, dX, dW, ws)
+        for d, X, W, dY, Y, dX, dW, ws in layer:
+            qf.qlinear_fwd(d, X, W, Y, ws)
+            qf.qlinear_bwd_ste(d, dY, X, W, dX, dW, ws)
 
     for _ in range(args.warmup):
         layer_step()
@@ -135,19 +199,118 @@ def main():
     wall = time.perf_counter() - t0
     step_ms = [sev[i].elapsed_time(sev[i + 1]) for i in range(args.steps)]
     ms_step = float(np.mean(step_ms))
-    gemm_flops = 2.0 * M * N * K
-    tflops = 3 * gemm_flops / (ms_step * 1e-3) / 1e12
-    del ws
+    tflops = flops / (ms_step * 1e-3) / 1e12
+    del layer
+    torch.cuda.empty_cache()
 
-    # ---- per-launch breakdown: the same kernels the two calls issue, one C-ABI call each, so
-    # every launch is bracketed by HIP events on the stream it runs on ------------------------
+    # ---- per-call pass: the same kernels, one C-ABI call each, each bracketed by HIP events
+    # on the stream it runs on (torch's current stream, where the binding launches) --------
+    calls = [c for lin in lins for c in dense_phase_calls(qf, torch, dev, lin)]
+    reps = max(3, args.steps // 4)
+
+    def one_pass(ev=None):
+        for i, (_, _, fn) in enumerate(calls):
+            if ev is not None:
+                ev[i].record()
+            fn()
+        if ev is not None:
+            ev[len(calls)].record()
+
+    for _ in range(2):
+        one_pass()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)] for _ in range(reps)]
+    for r in range(reps):
+        one_pass(evs[r])
+    torch.cuda.synchronize()
+    per = np.zeros(len(calls))
+    for ev in evs:
+        per += [ev[i].elapsed_time(ev[i + 1]) for i in range(len(calls))]
+    per /= reps
+    phases = {c[0]: round(float(per[i]), 4) for i, c in enumerate(calls)}
+    gemms = [(c[0], c[1], float(per[i])) for i, c in enumerate(calls) if c[1] > 0]
+    dom, dom_flops, dom_ms = max(gemms, key=lambda t: t[2])
+    achieved = dom_flops / (dom_ms * 1e-3) / 1e12
+    gemm_ms = sum(t[2] for t in gemms)
+    del calls
+    torch.cuda.empty_cache()
+
+    rows = None
+    if not args.main_only:
+        del lins
+        torch.cuda.empty_cache()
+        rows = other_rows(qf, torch, dev)
+    cpu = None
+    if not args.no_cpu_baseline and not args.main_only:
+        cpu = cpu_baseline(args.cpu_rows)
+
+    out = {
+        "metric": METRIC,
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded on the GPU: x = N(0,1) * |Student-t(3)| per channel, "
+                "N(0,0.02) weights, N(0,1) upstream gradients)",
+        "config": {"workload": "dense_9b_layer_32k_nvfp4: one 32768-token sequence, hidden "
+                               "4096, QKV 4096->6144 (tied scale), O 4096->4096, gate/up "
+                               "4096->2x12288 (tied scale), down 12288->4096; NVFP4 weight-only "
+                               "fake quant, all seven projections fwd + STE bwd",
+                   "T": 32768, "linears": [[n, k] for _, n, k in __import__("workloads").DENSE_LINEARS],
+                   "wfmt": "nvfp4", "afmt": "none", "step_tflop": round(flops / 1e12, 3)},
+        "roofline": {"bound": "mfma", "kernel": "gemm_nt_kernel", "launch": dom,
+                     "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": measured_traffic("dense_layer_32k_nvfp4_traffic.json", dom),
+                     "traffic_unit": "bytes per launch",
+                     "launch_ms": round(dom_ms, 4), "launch_flop": dom_flops},
+        "gemm_share": {"gemm_ms": round(gemm_ms, 4), "phases_sum_ms": round(float(per.sum()), 4),
+                       "gemm_TFLOPs": round(flops / (gemm_ms * 1e-3) / 1e12, 1)},
+        "phases_ms": phases,
+        "wall_s_timed": round(wall, 3),
+        "rows": rows,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+def mlp_up_row(qf, torch, dev):
+    """The MXFP4 W4A4 MLP up-projection (X 8192x4096, W 14336x4096, dY 8192x14336, seeded on
+    the host): the layer's two C-ABI calls per step (20 steps after 10 untimed), the per-call
+    breakdown with its roofline record, and the MXFP4 quantizer over rotating buffers."""
+    import workloads
+    w = workloads.mlp_up(seed=0)
+    M, N, K = w["M"], w["N"], w["K"]
+
+    def up(a):
+        return torch.from_numpy(a.view(np.int16)).to(dev)
+
+    X, W, dY = up(w["X"]), up(w["W"]), up(w["dY"])
+    Y = torch.empty(M, N, dtype=torch.int16, device=dev)
+    dX = torch.empty(M, K, dtype=torch.int16, device=dev)
+    dW = torch.empty(N, K, dtype=torch.float32, device=dev)
+    desc = qf.qlinear_desc(M, N, K, "mxfp4", "mxfp4")
+    ws = qf.workspace(desc)
+
+    def layer_step():
+        qf.qlinear_fwd(desc, X, W, Y, ws)
+        qf.qlinear_bwd_ste(desc, dY, X, W, dX, dW, ws)
+
+    ms_step = _time(torch, layer_step, reps=20, warm=10)
+    gemm_flops = 2.0 * M * N * K
+    del ws
     what = torch.empty(N, K, dtype=torch.int16, device=dev)
     xhat = torch.empty(M, K, dtype=torch.int16, device=dev)
     whatt = torch.empty(K, N, dtype=torch.int16, device=dev)
     xhatt = torch.empty(K, M, dtype=torch.int16, device=dev)
     dYt = torch.empty(N, M, dtype=torch.int16, device=dev)
-    gws = qf.gemm_workspace(N, K, 1)        # dW's split last round, as in the layer call
-    # (the dX GEMM also writes dY^T, the left operand of dW, as the layer's backward does)
+    gws = qf.gemm_workspace(N, K, 1)
     phases = ["quant_W", "quant_X", "gemm_fwd", "quant_W_transposed", "gemm_dX_and_dY_transposed",
               "quant_X_transposed", "gemm_dW"]
     calls = [
@@ -159,6 +322,7 @@ def main():
         lambda: qf.fakequant_transposed(X, "mxfp4", xhatt),
         lambda: qf.gemm_bf16(N, K, M, dYt, M, 1, xhatt, M, 1, dW, K, 1, ws=gws),
     ]
+    steps = 10
 
     def step(ev=None):
         for i, c in enumerate(calls):
@@ -168,82 +332,31 @@ def main():
         if ev is not None:
             ev[len(calls)].record()
 
-    for _ in range(args.warmup):
+    for _ in range(5):
         step()
     torch.cuda.synchronize()
     events = [[torch.cuda.Event(enable_timing=True) for _ in range(len(phases) + 1)]
-              for _ in range(args.steps)]
-    for s_ in range(args.steps):
+              for _ in range(steps)]
+    for s_ in range(steps):
         step(events[s_])
     torch.cuda.synchronize()
     per_phase = np.zeros(len(phases))
     for ev in events:
         per_phase += [ev[i].elapsed_time(ev[i + 1]) for i in range(len(phases))]
-    per_phase /= args.steps
+    per_phase /= steps
     gemm_ms = {p: float(per_phase[i]) for i, p in enumerate(phases) if p.startswith("gemm")}
     dom = max(gemm_ms, key=gemm_ms.get)
     achieved = gemm_flops / (gemm_ms[dom] * 1e-3) / 1e12
-
-    # ---- fake-quant bandwidth over rotating buffers (W-shaped, > 1 GB in total) -----------
-    nbuf = 10
-    bufs = [torch.empty_like(W) for _ in range(nbuf)]
-    for b in bufs:   # finite bf16 payloads of N(0, 0.02)-like magnitude
-        b.copy_((torch.randn(N, K, device=dev) * 0.02).to(torch.bfloat16).view(torch.int16))
-    codes = torch.empty(N, K // 2, dtype=torch.uint8, device=dev)
-    scales = torch.empty(N, K // 32, dtype=torch.uint8, device=dev)
-    outs = torch.empty(N, K, dtype=torch.int16, device=dev)
-    for b in bufs[:2]:
-        qf.fakequant_mxfp4(b, codes, scales, outs)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    reps = 3 * nbuf
-    e0.record()
-    for i in range(reps):
-        qf.fakequant_mxfp4(bufs[i % nbuf], codes, scales, outs)
-    e1.record()
-    torch.cuda.synchronize()
-    q_ms = e0.elapsed_time(e1) / reps
-    q_bytes = N * K * (2 + 2 + 0.5 + 1.0 / 32)
-    q_gbps = q_bytes / (q_ms * 1e-3) / 1e9
-    del bufs
-
     del X, W, dY, what, xhat, whatt, xhatt, dYt, Y, dX, dW, gws
     torch.cuda.empty_cache()
-    rows = None if args.main_only else other_rows(qf, torch, dev)
-
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(w, args.cpu_rows)
-
-    out = {
-        "metric": "fake-quant GB/s and fused fake-quant+BF16 GEMM TFLOP/s (fwd+bwd), 1 MI355X",
-        "value": round(tflops, 2),
-        "unit": "TFLOP/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 4),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic (seeded N(0,1) activations with 41 outlier channels x20, N(0,0.02) weights)",
-        "config": {"workload": "mlp_up_mxfp4_w4a4: X 8192x4096, W 14336x4096, fwd + STE bwd",
-                   "M": M, "N": N, "K": K, "wfmt": "mxfp4", "afmt": "mxfp4"},
-        "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
-                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": measured_traffic(dom), "traffic_unit": "bytes per launch"},
-        "phases_ms": {p: round(float(per_phase[i]), 4) for i, p in enumerate(phases)},
-        "phases_sum_ms": round(float(per_phase.sum()), 4),
-        "fakequant": {"kernel": "mxfp4 (codes+scales+x_hat)", "tensor": f"{N}x{K}",
-                      "GBps": round(q_gbps, 1), "frac_hbm": round(q_gbps / PEAK_HBM_GBPS, 4),
-                      "us": round(q_ms * 1e3, 2), "bytes_per_elem": 4.53125},
-        "wall_s_timed": round(wall, 3),
-        "rows": rows,
-        "cpu_baseline": cpu,
-    }
-    print(json.dumps(out), flush=True)
+    return {"ms": round(ms_step, 4), "TFLOPs": round(3 * gemm_flops / (ms_step * 1e-3) / 1e12, 1),
+            "roofline": {"bound": "mfma", "launch": dom, "achieved": round(achieved, 2),
+                         "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                         "traffic": measured_traffic("gemm_nt_mlp_up_step_traffic.json", dom)},
+            "phases_ms": {p: round(float(per_phase[i]), 4) for i, p in enumerate(phases)},
+            "work": "MXFP4 W4A4 MLP up-projection X 8192x4096, W 14336x4096, dY 8192x14336; "
+                    "fwd + STE bwd (20 steps after 10 untimed)"}
 
 
 def _time(torch, fn, reps=10, warm=2):
@@ -271,12 +384,11 @@ def _randn_bf16(torch, gen, shape, std=1.0, col_scale=None, row_scale=None):
 
 
 def other_rows(qf, torch, dev, only=None):
-    """Throughput of the remaining hot-path steps on their own workloads (seeded synthetic
-    data drawn on the GPU): every quantizer and the amax pass over W-shaped tensors through
-    rotating buffers, the transpose, the 9B-class dense layer at 32K tokens (NVFP4 weights,
-    tied QKV and gate/up scales), the 128-expert grouped layer (NVFP4 weights, Zipf(1.1)
-    top-8 routing), the LoRA-QAD layer (rank-16 adapter on the MLP up-projection) and the
-    Q4_K export packing + forward GEMM."""
+    """Throughput of the other configurations on their own workloads (seeded synthetic data):
+    the MXFP4 W4A4 MLP up-projection step, every quantizer and the amax pass over W-shaped
+    tensors through rotating buffers, the transpose, the 128-expert grouped layer (NVFP4
+    weights, Zipf(1.1) top-8 routing), the LoRA-QAD layers, the QAD loss and the Q4_K export
+    packing + forward GEMM."""
     def want(name):
         return only is None or name in only
 
@@ -321,33 +433,9 @@ def other_rows(qf, torch, dev, only=None):
             out[k]["tensor"] = f"{N}x{K}"
         del bufs, codes, sc16, sc32, packed, xh, tr
 
-    if want("dense"):
-        # ---- 9B-class dense layer at 32K tokens: QKV, O, gate/up, down (NVFP4 weights) ---------
-        T = 32768
-        layer = []
-        flops = 0.0
-        for name, n, k in workloads.DENSE_LINEARS:
-            tau = torch.from_numpy(np.abs(np.random.default_rng(k).standard_t(3.0, size=k))
-                                   .astype(np.float32)).to(dev)
-            Xl = _randn_bf16(torch, gen, (T, k), col_scale=tau)
-            Wl = _randn_bf16(torch, gen, (n, k), 0.02)
-            dYl = _randn_bf16(torch, gen, (T, n))
-            d = qf.qlinear_desc(T, n, k, "nvfp4", "none")
-            layer.append((d, Xl, Wl, dYl, torch.empty(T, n, dtype=torch.bfloat16, device=dev),
-                          torch.empty(T, k, dtype=torch.bfloat16, device=dev),
-                          torch.empty(n, k, dtype=torch.float32, device=dev), qf.workspace(d)))
-            flops += 3 * 2.0 * T * n * k
-
-        def dense_step():
-            for d, Xl, Wl, dYl, Yl, dXl, dWl, ws in layer:
-                qf.qlinear_fwd(d, Xl, Wl, Yl, ws)
-                qf.qlinear_bwd_ste(d, dYl, Xl, Wl, dXl, dWl, ws)
-
-        ms = _time(torch, dense_step, reps=3, warm=1)
-        out["dense_layer_32k_nvfp4"] = {"ms": round(ms, 3), "TFLOPs": round(flops / (ms * 1e-3) / 1e12, 1),
-                                        "work": "T=32768, QKV 6144, O 4096, gate/up 24576, down 4096x12288, fwd + STE bwd"}
-        del layer
-        torch.cuda.empty_cache()
+    if want("mlp_up"):
+        # ---- the MXFP4 W4A4 MLP up-projection (8B-class) -------------------------------------
+        out["mlp_up_mxfp4"] = mlp_up_row(qf, torch, dev)
 
     if want("moe"):
         # ---- 128-expert grouped layer, Zipf(1.1) top-8 routing of 32768 tokens -------------------
@@ -371,7 +459,7 @@ def other_rows(qf, torch, dev, only=None):
                 qf.qlinear_grouped_fwd(d, off, Xg, Wg, Yg, ws)
                 qf.qlinear_grouped_bwd_ste(d, off, dYg, Xg, Wg, dXg, dWg, ws)
 
-        ms = _time(torch, moe_step, reps=3, warm=1)
+        ms = _time(torch, moe_step, reps=10, warm=5)
         cnt = np.diff(offsets)
         out["moe_grouped_nvfp4"] = {"ms": round(ms, 3), "TFLOPs": round(gflops / (ms * 1e-3) / 1e12, 1),
                                     "work": f"128 experts, {Tm} routed rows (per expert {cnt.min()}..{cnt.max()}), "
@@ -532,30 +620,86 @@ def kl_row(qf, torch, dev, gen):
     return out
 
 
-def cpu_baseline(w, rows):
-    """The CPU oracle on a bounded sample of the same step: `rows` token rows of X and dY
-    (full W): MXFP4 fake quant of W and of the sampled X rows, then the three FP64 products
-    restricted to those rows.  Throughput counts the sample's 3 * 2 * rows * N * K flops."""
+def cpu_baseline(rows):
+    """The CPU oracle (test infrastructure, as it stands) on a bounded sample of the headline
+    step, on the host's cores (threads over row chunks, each an oracle call; numpy's BLAS for
+    the FP64 products):
+      - NVFP4 fake quant with the tensor amax computed (codes, scales, S and x_hat) of the 9B
+        layer's four weights, all 193 M elements, on all threads; and of the QKV weight's first
+        2048 rows on one thread -> GB/s of the 4.5625-byte model;
+      - the FP64 products of `rows` token rows through the four linears (their rows of Y and
+        dX and their rank-`rows` share of dW: 3 * 2 * rows * N * K flops per linear), on one
+        thread and on all threads -> GFLOP/s.
+    `value` is the sample's GEMM flops over the all-thread time of its quantization + GEMMs
+    (TFLOP/s); `full_step_s_estimate` extrapolates the full 32768-token step."""
+    from concurrent.futures import ThreadPoolExecutor
+
     import oracle
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        cores = 1
-    M, N, K = w["M"], w["N"], w["K"]
-    Xs, dYs = w["X"][:rows], w["dY"][:rows]
-    t0 = time.perf_counter()
-    wq = oracle.mxfp4(w["W"])["xhat"]
-    xq = oracle.mxfp4(Xs)["xhat"]
-    oracle.linear_fwd(xq, wq)
-    oracle.linear_dx(dYs, wq)
-    oracle.linear_dw(dYs, xq)
-    dt = time.perf_counter() - t0
-    flops = 3 * 2.0 * rows * N * K
-    return {"value": round(flops / dt / 1e12, 5), "unit": "TFLOP/s", "cores": int(cores),
-            "kind": "oracle", "seconds": round(dt, 2),
-            "sample": f"{rows} of {M} token rows (full {N}x{K} weight quantized), MXFP4 W4A4 "
-                      "fwd + dX + dW in FP64"}
+    import workloads
+    from threadpoolctl import threadpool_limits
+
+    ncpu = os.cpu_count() or 1
+    threads = max(1, min(ncpu, int(os.environ.get("OMP_NUM_THREADS", ncpu))))
+    rng = np.random.default_rng(0)
+    lins = []
+    for name, n, k in workloads.DENSE_LINEARS:
+        tau = np.abs(rng.standard_t(3.0, size=k)).astype(np.float32)
+        lins.append({"name": name, "N": n, "K": k,
+                     "W": workloads.normal_bf16(rng, (n, k), 0.02),
+                     "X": workloads.normal_bf16(rng, (rows, k), 1.0, col_scale=tau),
+                     "dY": workloads.normal_bf16(rng, (rows, n), 1.0)})
+    nel = sum(l["N"] * l["K"] for l in lins)
+
+    def quant_rows(W, g, r0, r1):
+        return oracle.nvfp4(np.ascontiguousarray(W[r0:r1]), amax_in=g)["xhat"]
+
+    # one thread: the QKV weight's first 2048 rows (its tensor amax over the whole weight)
+    W0 = lins[0]["W"]
+    t = time.perf_counter()
+    g0 = oracle.amax(W0)
+    quant_rows(W0, g0, 0, 2048)
+    q1_s = time.perf_counter() - t
+    q1_gbps = 2048 * W0.shape[1] * 4.5625 / q1_s / 1e9
+    # all threads: every weight in full, chunks of 256 rows
+    t = time.perf_counter()
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        for l in lins:
+            g = oracle.amax(l["W"])
+            parts = list(ex.map(lambda r0: quant_rows(l["W"], g, r0, min(l["N"], r0 + 256)),
+                                range(0, l["N"], 256)))
+            l["what"] = np.concatenate(parts)
+    qn_s = time.perf_counter() - t
+    qn_gbps = nel * 4.5625 / qn_s / 1e9
+
+    def gemms():
+        for l in lins:
+            oracle.linear_fwd(l["X"], l["what"])
+            oracle.linear_dx(l["dY"], l["what"])
+            oracle.linear_dw(l["dY"], l["X"])
+
+    flops = sum(3 * 2.0 * rows * l["N"] * l["K"] for l in lins)
+    with threadpool_limits(limits=1):
+        t = time.perf_counter()
+        gemms()
+        g1_s = time.perf_counter() - t
+    with threadpool_limits(limits=threads):
+        t = time.perf_counter()
+        gemms()
+        gn_s = time.perf_counter() - t
+    full_flops = sum(3 * 2.0 * 32768 * l["N"] * l["K"] for l in lins)
+    return {"value": round(flops / (qn_s + gn_s) / 1e12, 6), "unit": "TFLOP/s",
+            "cores": threads, "host_cpu_count": ncpu, "kind": "oracle",
+            "sample": f"{rows} of 32768 token rows through the 9B layer's four linears (FP64 "
+                      f"fwd, dX, dW share) after NVFP4 fake quant of all four full weights "
+                      f"({nel / 1e6:.0f} M elements)",
+            "fakequant_nvfp4": {"GBps_1_thread": round(q1_gbps, 4), "s_1_thread": round(q1_s, 2),
+                                "elements_1_thread": 2048 * W0.shape[1],
+                                "GBps_all_threads": round(qn_gbps, 4), "s_all_threads": round(qn_s, 2),
+                                "elements_all_threads": nel, "bytes_per_elem": 4.5625},
+            "gemm_fp64": {"GFLOPs_1_thread": round(flops / g1_s / 1e9, 2), "s_1_thread": round(g1_s, 2),
+                          "GFLOPs_all_threads": round(flops / gn_s / 1e9, 2),
+                          "s_all_threads": round(gn_s, 2), "flop": flops},
+            "full_step_s_estimate": round(qn_s + full_flops / (flops / gn_s), 1)}
 
 
 if __name__ == "__main__":

@@ -206,6 +206,74 @@ def test_mlp_up_mxfp4_full_size_sampled(qf):
     xqT = np.ascontiguousarray(xq.T)
     j, k = rng.integers(0, N, n // 4), rng.integers(0, K, n // 4)
     assert_close(dW[j, k].astype(np.float64), oracle.dot_rows(dYT, j, xqT, k), "dW sampled")
+    # two whole rows of each gradient
+    r = rng.integers(0, M, 2)
+    assert_close(bf16_to_f64(dX[r]), oracle.linear_dx(w["dY"][r], wq), "dX rows")
+    j = rng.integers(0, N, 2)
+    assert_close(dW[j].astype(np.float64), oracle.linear_fwd(dYT[j], xqT), "dW rows")
+
+
+def _nvfp4_xhat_threaded(W, g):
+    """The oracle's NVFP4 x_hat of W with the tensor amax g, over row chunks in threads (each
+    chunk one oracle call; the block scales depend on g and the block only)."""
+    from concurrent.futures import ThreadPoolExecutor
+    chunks = range(0, W.shape[0], 512)
+    with ThreadPoolExecutor(max_workers=16) as ex:
+        parts = ex.map(lambda r0: oracle.nvfp4(np.ascontiguousarray(W[r0:r0 + 512]), amax_in=g)["xhat"],
+                       chunks)
+        return np.concatenate(list(parts))
+
+
+@pytest.mark.parametrize("name,members", [("qkv", (4096, 1024, 1024)), ("o", (4096,)),
+                                          ("gate_up", (12288, 12288))])
+def test_dense_layer_32k_tokens_sampled(qf, name, members):
+    """The 9B-class layer's QKV, O and gate/up projections at 32768 tokens (NVFP4 weights,
+    heavy-tailed activations) in the launch configuration the benchmark times.  A fused
+    projection's tensor scale is tied over its members (Sec. 3.2.3 "Engine-specific scale
+    sharing"): g is built with qf_amax over the member weights (overwrite, then accumulate) and
+    handed to the layer, which must give what the oracle gives for the same g.  Sampled
+    entries of Y, dX and dW plus two whole rows of each."""
+    T, K = 32768, 4096
+    N = sum(members)
+    rng = np.random.default_rng(40 + N)
+    tau = np.abs(rng.standard_t(3.0, size=K)).astype(np.float32)
+    w = {"X": workloads.normal_bf16(rng, (T, K), 1.0, col_scale=tau),
+         "W": workloads.normal_bf16(rng, (N, K), 0.02),
+         "dY": workloads.normal_bf16(rng, (T, N), 1.0)}
+    Wd = to_dev(w["W"])
+    g = torch.zeros(1, dtype=torch.float32, device="cuda")
+    r0 = 0
+    for i, m in enumerate(members):
+        qf.amax(Wd[r0:r0 + m], g, accumulate=i > 0)
+        r0 += m
+    torch.cuda.synchronize()
+    g_ref = max(oracle.amax(np.ascontiguousarray(w["W"][a:a + m]))
+                for a, m in zip(np.cumsum((0,) + members[:-1]), members))
+    assert float(g.item()) == g_ref == oracle.amax(w["W"])
+    Y, dX, dW = _layer(qf, w, "nvfp4", "none", w_amax=g)
+    del Wd
+    wq = _nvfp4_xhat_threaded(w["W"], g_ref)
+    n = 1 << 12
+
+    def sampled(a, ai, b, bi):
+        return np.concatenate([oracle.dot_rows(a, ai[c:c + 256], b, bi[c:c + 256])
+                               for c in range(0, len(ai), 256)])
+
+    i, j = rng.integers(0, T, n), rng.integers(0, N, n)
+    assert_close(bf16_to_f64(Y[i, j]), sampled(w["X"], i, wq, j), f"{name} Y sampled")
+    r = rng.integers(0, T, 2)
+    assert_close(bf16_to_f64(Y[r]), oracle.linear_fwd(w["X"][r], wq), f"{name} Y rows")
+    wqT = np.ascontiguousarray(wq.T)
+    i, k = rng.integers(0, T, n), rng.integers(0, K, n)
+    assert_close(bf16_to_f64(dX[i, k]), sampled(w["dY"], i, wqT, k), f"{name} dX sampled")
+    assert_close(bf16_to_f64(dX[r]), oracle.linear_dx(w["dY"][r], wq), f"{name} dX rows")
+    del wqT, Y, dX
+    dYT = np.ascontiguousarray(w["dY"].T)
+    xT = np.ascontiguousarray(w["X"].T)
+    j, k = rng.integers(0, N, n), rng.integers(0, K, n)
+    assert_close(dW[j, k].astype(np.float64), sampled(dYT, j, xT, k), f"{name} dW sampled")
+    j = rng.integers(0, N, 2)
+    assert_close(dW[j].astype(np.float64), oracle.linear_fwd(dYT[j], xT), f"{name} dW rows")
 
 
 def test_q4k_export_weight_forward_full_size_sampled(qf):
