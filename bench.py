@@ -107,12 +107,18 @@ def dense_layer_inputs(torch, dev, gen):
 
 
 def dense_phase_calls(qf, torch, dev, lin):
-    """The kernels one linear's qf_qlinear_fwd + qf_qlinear_bwd_ste launch (NVFP4 weights,
-    W computed amax, bf16 activations), one C-ABI call each, in the layer's order."""
+    """The kernels one linear's qf_qlinear_fwd + qf_qlinear_bwd_ste launch with a saved buffer
+    (NVFP4 weights, W's amax computed, bf16 activations), one C-ABI call each, in the layer's
+    order: the forward quantizes W once into its packed form (codes, scales, S; the saved
+    operand) and its bf16 W_hat, then runs the GEMM; the backward dequantizes the packed W
+    straight into W_hat^T."""
     T, N, K = lin["T"], lin["N"], lin["K"]
     X, W, dY = lin["X"], lin["W"], lin["dY"]
     ldm = T + 128 if T % 16384 == 0 else T        # the layer workspace's padded stride
     g = torch.zeros(1, dtype=torch.float32, device=dev)
+    S = torch.zeros(1, dtype=torch.float32, device=dev)
+    codes = torch.empty(N, K // 2, dtype=torch.uint8, device=dev)
+    scales = torch.empty(N, K // 16, dtype=torch.uint8, device=dev)
     what = torch.empty(N, K, dtype=torch.bfloat16, device=dev)
     whatt = torch.empty(K, N, dtype=torch.bfloat16, device=dev)
     xt = torch.empty(K, ldm, dtype=torch.bfloat16, device=dev)
@@ -124,10 +130,12 @@ def dense_phase_calls(qf, torch, dev, lin):
     nm = lin["name"]
     return [
         (f"{nm}.amax_W", 0.0, lambda: qf.amax(W, g)),
-        (f"{nm}.quant_W", 0.0, lambda: qf.fakequant_nvfp4(W, g, qf.AMAX_GIVEN, None, None, None, what)),
-        (f"{nm}.gemm_fwd", 2.0 * T * N * K, lambda: qf.gemm_bf16(T, N, K, X, K, 1, what, K, 1, Y, N, 0)),
-        (f"{nm}.amax_W_bwd", 0.0, lambda: qf.amax(W, g)),
-        (f"{nm}.quant_W_transposed", 0.0, lambda: qf.fakequant_transposed(W, "nvfp4", whatt, amax=g)),
+        (f"{nm}.quant_W", 0.0,
+         lambda: qf.fakequant_nvfp4(W, g, qf.AMAX_GIVEN, S, codes, scales, what)),
+        (f"{nm}.gemm_fwd", 2.0 * T * N * K,
+         lambda: qf.gemm_bf16(T, N, K, X, K, 1, what, K, 1, Y, N, 0)),
+        (f"{nm}.dequant_W_transposed", 0.0,
+         lambda: qf.dequantize_transposed("nvfp4", codes, scales, S, N, K, whatt)),
         (f"{nm}.gemm_dX_and_dY_transposed", 2.0 * T * N * K,
          lambda: qf.gemm_bf16_at(T, K, N, dY, N, whatt, N, dX, K, dyt, ldm)),
         (f"{nm}.transpose_X", 0.0, lambda: qf.transpose_bf16(X, xt)),
@@ -178,17 +186,20 @@ def main():
         layer.append((d, lin["X"], lin["W"], lin["dY"],
                       torch.empty(T, N, dtype=torch.bfloat16, device=dev),
                       torch.empty(T, K, dtype=torch.bfloat16, device=dev),
-                      torch.empty(N, K, dtype=torch.float32, device=dev), qf.workspace(d)))
+                      torch.empty(N, K, dtype=torch.float32, device=dev), qf.workspace(d),
+                      qf.saved_buffer(d)))
         flops += 3 * 2.0 * T * N * K
 
     def layer_step():
-        for d, X, W, dY, Y, dX, dW, ws in layer:
-            qf.qlinear_fwd(d, X, W, Y, ws)
-            qf.qlinear_bwd_ste(d, dY, X, W, dX, dW, ws)
+        # forward saves the packed W_hat; the backward dequantizes it (Sec. 3.2.1)
+        for d, X, W, dY, Y, dX, dW, ws, sv in layer:
+            qf.qlinear_fwd(d, X, W, Y, ws, saved=sv)
+            qf.qlinear_bwd_ste(d, dY, X, W, dX, dW, ws, saved=sv)
 
     for _ in range(args.warmup):
         layer_step()
     torch.cuda.synchronize()
+    ab = fused_ab(qf, torch, layer)
     sev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     t0 = time.perf_counter()
     sev[0].record()
@@ -273,11 +284,37 @@ def main():
         "gemm_share": {"gemm_ms": round(gemm_ms, 4), "phases_sum_ms": round(float(per.sum()), 4),
                        "gemm_TFLOPs": round(flops / (gemm_ms * 1e-3) / 1e12, 1)},
         "phases_ms": phases,
+        "fused_decode_ab": ab,
         "wall_s_timed": round(wall, 3),
         "rows": rows,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def fused_ab(qf, torch, layer, reps=10):
+    """Same-run A/B of the layer calls: the forward that decodes the packed weight inside the
+    GEMM (QF_FLAG_DECODE_IN_GEMM) against the default one that writes W_hat in bf16 and runs a
+    plain GEMM, and the backward from the saved packed operands against the one that
+    quantizes W again."""
+    out = {}
+    tot = {"fwd_fused": 0.0, "fwd_materialized": 0.0, "bwd_from_saved": 0.0,
+           "bwd_requantize": 0.0}
+    for d, X, W, dY, Y, dX, dW, ws, sv in layer:
+        df = qf.qlinear_desc(d.M, d.N, d.K, "nvfp4", "none", flags=qf.FLAG_DECODE_IN_GEMM)
+        r = {"fwd_fused": _time(torch, lambda: qf.qlinear_fwd(df, X, W, Y, ws, saved=sv), reps, 2),
+             "fwd_materialized": _time(torch, lambda: qf.qlinear_fwd(d, X, W, Y, ws, saved=sv),
+                                       reps, 2),
+             "bwd_from_saved": _time(torch, lambda: qf.qlinear_bwd_ste(d, dY, X, W, dX, dW, ws,
+                                                                       saved=sv), reps, 2),
+             "bwd_requantize": _time(torch, lambda: qf.qlinear_bwd_ste(d, dY, X, W, dX, dW, ws),
+                                     reps, 2)}
+        qf.qlinear_fwd(d, X, W, Y, ws, saved=sv)      # leave the saved buffer consistent
+        for k in tot:
+            tot[k] += r[k]
+        out[f"{d.N}x{d.K}"] = {k: round(v, 4) for k, v in r.items()}
+    out["total_ms"] = {k: round(v, 4) for k, v in tot.items()}
+    return out
 
 
 def mlp_up_row(qf, torch, dev):
@@ -297,29 +334,35 @@ def mlp_up_row(qf, torch, dev):
     dW = torch.empty(N, K, dtype=torch.float32, device=dev)
     desc = qf.qlinear_desc(M, N, K, "mxfp4", "mxfp4")
     ws = qf.workspace(desc)
+    sv = qf.saved_buffer(desc)
 
     def layer_step():
-        qf.qlinear_fwd(desc, X, W, Y, ws)
-        qf.qlinear_bwd_ste(desc, dY, X, W, dX, dW, ws)
+        qf.qlinear_fwd(desc, X, W, Y, ws, saved=sv)
+        qf.qlinear_bwd_ste(desc, dY, X, W, dX, dW, ws, saved=sv)
 
     ms_step = _time(torch, layer_step, reps=20, warm=10)
     gemm_flops = 2.0 * M * N * K
-    del ws
-    what = torch.empty(N, K, dtype=torch.int16, device=dev)
+    del ws, sv
+    wc = torch.empty(N, K // 2, dtype=torch.uint8, device=dev)
+    wsc = torch.empty(N, K // 32, dtype=torch.uint8, device=dev)
+    xc = torch.empty(M, K // 2, dtype=torch.uint8, device=dev)
+    xsc = torch.empty(M, K // 32, dtype=torch.uint8, device=dev)
     xhat = torch.empty(M, K, dtype=torch.int16, device=dev)
+    what = torch.empty(N, K, dtype=torch.int16, device=dev)
     whatt = torch.empty(K, N, dtype=torch.int16, device=dev)
     xhatt = torch.empty(K, M, dtype=torch.int16, device=dev)
     dYt = torch.empty(N, M, dtype=torch.int16, device=dev)
     gws = qf.gemm_workspace(N, K, 1)
-    phases = ["quant_W", "quant_X", "gemm_fwd", "quant_W_transposed", "gemm_dX_and_dY_transposed",
-              "quant_X_transposed", "gemm_dW"]
+    # the kernels of the two layer calls with a saved buffer, one C-ABI call each
+    phases = ["quant_W", "quant_X", "gemm_fwd", "dequant_W_transposed",
+              "gemm_dX_and_dY_transposed", "dequant_X_transposed", "gemm_dW"]
     calls = [
-        lambda: qf.fakequant_mxfp4(W, None, None, what),
-        lambda: qf.fakequant_mxfp4(X, None, None, xhat),
+        lambda: qf.fakequant_mxfp4(W, wc, wsc, what),
+        lambda: qf.fakequant_mxfp4(X, xc, xsc, xhat),
         lambda: qf.gemm_bf16(M, N, K, xhat, K, 1, what, K, 1, Y, N, 0),
-        lambda: qf.fakequant_transposed(W, "mxfp4", whatt),
+        lambda: qf.dequantize_transposed("mxfp4", wc, wsc, None, N, K, whatt),
         lambda: qf.gemm_bf16_at(M, K, N, dY, N, whatt, N, dX, K, dYt, M),
-        lambda: qf.fakequant_transposed(X, "mxfp4", xhatt),
+        lambda: qf.dequantize_transposed("mxfp4", xc, xsc, None, M, K, xhatt),
         lambda: qf.gemm_bf16(N, K, M, dYt, M, 1, xhatt, M, 1, dW, K, 1, ws=gws),
     ]
     steps = 10
@@ -347,7 +390,7 @@ def mlp_up_row(qf, torch, dev):
     gemm_ms = {p: float(per_phase[i]) for i, p in enumerate(phases) if p.startswith("gemm")}
     dom = max(gemm_ms, key=gemm_ms.get)
     achieved = gemm_flops / (gemm_ms[dom] * 1e-3) / 1e12
-    del X, W, dY, what, xhat, whatt, xhatt, dYt, Y, dX, dW, gws
+    del X, W, dY, wc, wsc, xc, xsc, xhat, what, whatt, xhatt, dYt, Y, dX, dW, gws
     torch.cuda.empty_cache()
     return {"ms": round(ms_step, 4), "TFLOPs": round(3 * gemm_flops / (ms_step * 1e-3) / 1e12, 1),
             "roofline": {"bound": "mfma", "launch": dom, "achieved": round(achieved, 2),

@@ -149,9 +149,15 @@ QF_API qf_status qf_fakequant_q4k_mse(const uint16_t* x, int64_t R, int64_t K, i
  * ------------------------------------------------------------------------------------ */
 
 /* flags */
-#define QF_FLAG_REUSE_WS 1u /* backward: the workspace still holds W_hat / A_hat written by the
-                               forward on the same X, W, desc (skips re-quantization; the
-                               bits are identical either way) */
+#define QF_FLAG_REUSE_WS 1u /* backward without a saved buffer: the workspace still holds the
+                               packed W_hat and the A_hat that a forward with no saved buffer
+                               wrote on the same X, W, desc (skips re-quantization; the bits are
+                               identical either way) */
+#define QF_FLAG_DECODE_IN_GEMM 2u /* forward: decode the packed weight inside the GEMM's
+                               prologue instead of writing W_hat in bf16 to the workspace and
+                               running a plain bf16 GEMM (identical Y; K a multiple of 64, else
+                               the flag is ignored).  Not the default: on MI355X the decoded
+                               tiles' LDS writes cost more than the bf16 W_hat pass saves */
 
 typedef struct {
     int64_t M, N, K;      /* X [M, K], W [N, K], Y [M, N]                                  */
@@ -170,25 +176,48 @@ typedef struct {
 QF_API qf_status qf_workspace_size(const qf_qlinear_desc* d, size_t* bytes);
 
 /*
- * qf_qlinear_fwd -- Y = A_hat W_hat^T (bf16 output rounded to nearest even from FP32
- * accumulation on MFMA; NaN sums give quiet NaNs).
+ * qf_saved_size -- bytes of the `saved` buffer of qf_qlinear_fwd / qf_qlinear_bwd_ste (host
+ * only): the packed quantized weight and, when afmt != NONE, the packed activation -- the
+ * transient quantized operands of Sec. 3.2.1, kept between the forward and the backward in
+ * their deployment form (0.5625 bytes per element for NVFP4 / Q4_K, 0.53125 for MXFP4).
+ * Layout, each region 256-byte aligned, W's then X's: NVFP4 = {256 B holding the FP32 tensor
+ * decode scale S = g / 2688, codes [R, K/2], E4M3 scales [R, K/16]}; MXFP4 = {codes [R, K/2],
+ * E8M0 scales [R, K/32]}; Q4_K = {blocks [R, K/256, 144]}; codes and scales as the quantizers
+ * write them.
+ */
+QF_API qf_status qf_saved_size(const qf_qlinear_desc* d, size_t* bytes);
+
+/*
+ * qf_qlinear_fwd -- Y = A_hat W_hat^T (Eq. fakequant; bf16 output rounded to nearest even from
+ * FP32 accumulation on MFMA; NaN sums give quiet NaNs).
  *   X bf16 [M, K], W bf16 [N, K], Y bf16 [M, N]; ws >= qf_workspace_size bytes, 256-aligned.
- * The workspace receives W_hat (and A_hat when afmt != NONE) as bf16; it also holds the
- * transposed operands the backward builds (W_hat^T, A_hat^T, dY^T), so one workspace serves
- * both calls.
+ *   saved  device buffer of qf_saved_size(d) bytes, 256-byte aligned, or NULL: receives the
+ *          packed W_hat (and A_hat) for the backward; NULL keeps the packed W_hat in the
+ *          workspace instead.
+ * W is quantized once into its packed codes and scales (Q(W), kept in `saved` or the
+ * workspace) and its bf16 W_hat = Q^-1(Q(W)) (the workspace), and Y = A_hat W_hat^T on the bf16
+ * MFMA GEMM.  With QF_FLAG_DECODE_IN_GEMM the GEMM instead decodes W_hat from the packed codes
+ * in its prologue, stage by stage, into the LDS tiles it multiplies (bit for bit the same
+ * x_hat), and no bf16 W_hat goes to memory.  A_hat (afmt != NONE) is quantized to bf16 in the
+ * workspace (and to its packed form in `saved`).
  */
 QF_API qf_status qf_qlinear_fwd(const qf_qlinear_desc* d, const uint16_t* X, const uint16_t* W,
-                         uint16_t* Y, void* ws, size_t ws_bytes, qf_stream_t stream);
+                                uint16_t* Y, void* saved, void* ws, size_t ws_bytes,
+                                qf_stream_t stream);
 
 /*
  * qf_qlinear_bwd_ste -- straight-through backward.
  *   dX = dY W_hat      bf16 [M, K]  (Eq. activation-ste)        dX may be NULL
  *   dW = dY^T A_hat    FP32 [N, K]  (Eq. ste; A_hat = X when afmt == NONE)  dW may be NULL
  * dY is bf16 [M, N] and is not quantized.  dW is overwritten (not accumulated).
+ *   saved  the forward's saved buffer (same d, X, W), or NULL: W_hat and A_hat are then
+ *          dequantized from their packed form straight into the transposed GEMM operands
+ *          (no amax pass, no re-quantization); NULL re-quantizes W and X (or, with
+ *          QF_FLAG_REUSE_WS, reuses the workspace).  The gradients are bit-identical either way.
  */
 QF_API qf_status qf_qlinear_bwd_ste(const qf_qlinear_desc* d, const uint16_t* dY, const uint16_t* X,
-                             const uint16_t* W, uint16_t* dX, float* dW, void* ws,
-                             size_t ws_bytes, qf_stream_t stream);
+                                    const uint16_t* W, const void* saved, uint16_t* dX, float* dW,
+                                    void* ws, size_t ws_bytes, qf_stream_t stream);
 
 /* ---------------------------------------------------------------------------------------
  * Grouped (mixture-of-experts) variant (Sec. 3.3 "Mixture-of-experts adaptation")
@@ -222,6 +251,23 @@ QF_API qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int6
                                      const uint16_t* dY, const uint16_t* X, const uint16_t* W,
                                      uint16_t* dX, float* dW, void* ws, size_t ws_bytes,
                                      qf_stream_t stream);
+
+/* ---------------------------------------------------------------------------------------
+ * Host-only validation (Sec. 3.2.2: the quantizer interface's preconditions).  Each runs the
+ * checks the corresponding entry point runs before it launches anything -- shapes, block
+ * multiples, formats, alignment, workspace size -- and returns the status and
+ * qf_last_error() message that call would return, without touching the device or reading
+ * any tensor.  Pointers are only checked for NULL and alignment.
+ * ------------------------------------------------------------------------------------ */
+/* A quantizer call: fmt QF_FMT_NVFP4 / MXFP4 / Q4K on x [R, K] with row stride ldx. */
+QF_API qf_status qf_validate_fakequant(int fmt, const void* x, int64_t R, int64_t K, int64_t ldx);
+/* A layer call pair: d with X, W, Y (dY has Y's shape and stride), saved and ws of ws_bytes. */
+QF_API qf_status qf_validate_qlinear(const qf_qlinear_desc* d, const void* X, const void* W,
+                                     const void* Y, const void* saved, const void* ws,
+                                     size_t ws_bytes);
+/* A grouped call pair: d with X [T, K], W [E, N, K], Y [T, N] and ws of ws_bytes. */
+QF_API qf_status qf_validate_grouped(const qf_grouped_desc* d, const void* X, const void* W,
+                                     const void* Y, const void* ws, size_t ws_bytes);
 
 /*
  * qf_fakequant_transposed -- quantize + dequantize with transposed output: out[k][r] =
@@ -273,6 +319,35 @@ QF_API qf_status qf_gemm_bf16(int64_t M, int64_t N, int64_t K, const uint16_t* A
 QF_API qf_status qf_gemm_bf16_at(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
                                  const uint16_t* B, int64_t ldb, uint16_t* C, int64_t ldc,
                                  uint16_t* at, int64_t ldat, qf_stream_t stream);
+
+/*
+ * qf_gemm_packed_b -- C[M, N] = A W_hat^T with W_hat decoded inside the GEMM from the packed
+ * weight (the layer forward's product, Eq. fakequant with Q^-1 in the GEMM's prologue): each
+ * 64-deep stage of the B tile is decoded from codes and scales by the quantizers' own decode
+ * and written to LDS, so C equals qf_gemm_bf16 on the bf16 x_hat of qf_fakequant_* bit for bit.
+ *   A      bf16 [M, K], k contiguous, row stride lda.
+ *   fmt    QF_FMT_NVFP4 (codes [N, K/2], E4M3 scales [N, K/16], S = the FP32 tensor decode
+ *          scale g / 2688 on the device, as qf_fakequant_nvfp4's s_out), QF_FMT_MXFP4 (codes,
+ *          E8M0 scales [N, K/32]; S ignored) or QF_FMT_Q4K (blocks [N, K/256, 144] in codes;
+ *          scales and S ignored), each dense row-major as the quantizers write them.
+ *   C      bf16 [M, N], row stride ldc.
+ *   K a multiple of 64 (Q4K: 256); codes / scales 16-byte aligned.
+ */
+QF_API qf_status qf_gemm_packed_b(int64_t M, int64_t N, int64_t K, const uint16_t* A,
+                                  int64_t lda, int fmt, const uint8_t* codes,
+                                  const uint8_t* scales, const float* S, uint16_t* C,
+                                  int64_t ldc, qf_stream_t stream);
+
+/*
+ * qf_dequantize_transposed -- out[k][r] = x_hat[r][k] decoded from a packed [R, K] tensor
+ * (Eqs. nvfp4-dequant, mxfp4-dequant, q4k-dequant; the layer backward's transposed operands
+ * from the saved buffer): bit for bit qf_fakequant_transposed of the tensor the codes came
+ * from.  fmt, codes, scales, S as for qf_gemm_packed_b; R % 8 == 0; out bf16 [K, R] with row
+ * stride ldo >= R (ldo % 8 == 0), 16-byte aligned.
+ */
+QF_API qf_status qf_dequantize_transposed(int fmt, const uint8_t* codes, const uint8_t* scales,
+                                          const float* S, int64_t R, int64_t K, uint16_t* out,
+                                          int64_t ldo, qf_stream_t stream);
 
 /*
  * qf_gemm_workspace_size / qf_gemm_bf16_ws -- qf_gemm_bf16 with a caller workspace.  With

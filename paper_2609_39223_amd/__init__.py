@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libqf.so")
 FMT = {"none": 0, "nvfp4": 1, "mxfp4": 2, "q4k": 3}
 AMAX_COMPUTE, AMAX_GIVEN = 0, 1
 FLAG_REUSE_WS = 1
+FLAG_DECODE_IN_GEMM = 2
 STATUS = {0: "QF_OK", 1: "QF_EINVAL", 2: "QF_ESHAPE", 3: "QF_EALIGN", 4: "QF_ENOTSUP",
           5: "QF_EDEVICE"}
 
@@ -83,10 +84,21 @@ def lib() -> ctypes.CDLL:
             "qf_fakequant_q4k_mse": ([_P, _I, _I, _I, _P, _P, _P], ctypes.c_int),
             "qf_workspace_size": ([ctypes.POINTER(QLinearDesc), ctypes.POINTER(ctypes.c_size_t)],
                                   ctypes.c_int),
-            "qf_qlinear_fwd": ([ctypes.POINTER(QLinearDesc), _P, _P, _P, _P, ctypes.c_size_t, _P],
-                               ctypes.c_int),
-            "qf_qlinear_bwd_ste": ([ctypes.POINTER(QLinearDesc), _P, _P, _P, _P, _P, _P,
+            "qf_saved_size": ([ctypes.POINTER(QLinearDesc), ctypes.POINTER(ctypes.c_size_t)],
+                              ctypes.c_int),
+            "qf_qlinear_fwd": ([ctypes.POINTER(QLinearDesc), _P, _P, _P, _P, _P, ctypes.c_size_t,
+                                _P], ctypes.c_int),
+            "qf_qlinear_bwd_ste": ([ctypes.POINTER(QLinearDesc), _P, _P, _P, _P, _P, _P, _P,
                                     ctypes.c_size_t, _P], ctypes.c_int),
+            "qf_gemm_packed_b": ([_I, _I, _I, _P, _I, ctypes.c_int, _P, _P, _P, _P, _I, _P],
+                                 ctypes.c_int),
+            "qf_dequantize_transposed": ([ctypes.c_int, _P, _P, _P, _I, _I, _P, _I, _P],
+                                         ctypes.c_int),
+            "qf_validate_fakequant": ([ctypes.c_int, _P, _I, _I, _I], ctypes.c_int),
+            "qf_validate_qlinear": ([ctypes.POINTER(QLinearDesc), _P, _P, _P, _P, _P,
+                                     ctypes.c_size_t], ctypes.c_int),
+            "qf_validate_grouped": ([ctypes.POINTER(GroupedDesc), _P, _P, _P, _P,
+                                     ctypes.c_size_t], ctypes.c_int),
             "qf_grouped_workspace_size": ([ctypes.POINTER(GroupedDesc),
                                            ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
             "qf_qlinear_grouped_fwd": ([ctypes.POINTER(GroupedDesc), _P, _P, _P, _P, _P,
@@ -233,16 +245,27 @@ def workspace(desc: QLinearDesc, device="cuda"):
     return torch.empty(max(workspace_size(desc), 256), dtype=torch.uint8, device=device)
 
 
-def qlinear_fwd(desc, X, W, Y, ws):
+def saved_size(desc: QLinearDesc) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().qf_saved_size(ctypes.byref(desc), ctypes.byref(n)))
+    return n.value
+
+
+def saved_buffer(desc: QLinearDesc, device="cuda"):
+    """A device buffer for the layer's saved (packed) operands, qf_saved_size bytes."""
+    return torch.empty(max(saved_size(desc), 256), dtype=torch.uint8, device=device)
+
+
+def qlinear_fwd(desc, X, W, Y, ws, saved=None):
     _check(lib().qf_qlinear_fwd(ctypes.byref(desc), _ptr(_bf16(X)), _ptr(_bf16(W)),
-                                _ptr(_bf16(Y)), _ptr(ws), ws.numel(), _stream()))
+                                _ptr(_bf16(Y)), _ptr(saved), _ptr(ws), ws.numel(), _stream()))
     return Y
 
 
-def qlinear_bwd_ste(desc, dY, X, W, dX, dW, ws):
+def qlinear_bwd_ste(desc, dY, X, W, dX, dW, ws, saved=None):
     _check(lib().qf_qlinear_bwd_ste(ctypes.byref(desc), _ptr(_bf16(dY)), _ptr(_bf16(X)),
-                                    _ptr(_bf16(W)), _ptr(_bf16(dX)), _ptr(dW), _ptr(ws),
-                                    ws.numel(), _stream()))
+                                    _ptr(_bf16(W)), _ptr(saved), _ptr(_bf16(dX)), _ptr(dW),
+                                    _ptr(ws), ws.numel(), _stream()))
 
 
 def grouped_desc(E, T, N, K, wfmt="nvfp4", afmt="none", w_amax=None, flags=0) -> GroupedDesc:
@@ -282,6 +305,22 @@ def gemm_bf16_at(M, N, K, A, lda, B, ldb, C, ldc, at, ldat):
     _check(lib().qf_gemm_bf16_at(M, N, K, _ptr(_bf16(A)), lda, _ptr(_bf16(B)), ldb,
                                  _ptr(_bf16(C)), ldc, _ptr(_bf16(at)), ldat, _stream()))
     return C, at
+
+
+def gemm_packed_b(M, N, K, A, lda, fmt, codes, scales, S, C, ldc):
+    """qf_gemm_packed_b: C = A W_hat^T with W_hat decoded inside the GEMM from packed codes."""
+    _check(lib().qf_gemm_packed_b(M, N, K, _ptr(_bf16(A)), lda, FMT[fmt], _ptr(codes),
+                                  _ptr(scales), _ptr(S), _ptr(_bf16(C)), ldc, _stream()))
+    return C
+
+
+def dequantize_transposed(fmt, codes, scales, S, R, K, out):
+    """qf_dequantize_transposed: out[k][r] = x_hat[r][k] from packed codes (out [K, >=R])."""
+    if out.dim() != 2 or out.shape[0] != K or out.shape[1] < R or out.stride(1) != 1:
+        raise ValueError("out must be a [K, >=R] row-contiguous tensor")
+    _check(lib().qf_dequantize_transposed(FMT[fmt], _ptr(codes), _ptr(scales), _ptr(S), R, K,
+                                          _ptr(_bf16(out)), out.stride(0), _stream()))
+    return out
 
 
 def gemm_workspace(M, N, c_f32, device="cuda"):

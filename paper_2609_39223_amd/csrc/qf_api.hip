@@ -108,6 +108,49 @@ qf_status fakequant_to(int fmt, const uint16_t* x, int64_t R, int64_t K, int64_t
   }
 }
 
+// A quantized operand in packed form: codes [R][K/2] + block scales [R][K/B] + (NVFP4) the
+// tensor decode scale S = g / 2688 in its own 256-byte slot; Q4_K: blocks [R][K/256][144] in
+// `codes`.  This is the layer's saved form of W_hat / A_hat (0.5625 bytes per element).
+struct Packed {
+  uint8_t* codes;
+  uint8_t* scales;
+  float* S;
+};
+
+size_t packed_bytes(int fmt, int64_t R, int64_t K) {
+  const size_t r = R, k = K;
+  switch (fmt) {
+    case QF_FMT_NVFP4: return kAlign + up(r * k / 2) + up(r * k / 16);
+    case QF_FMT_MXFP4: return up(r * k / 2) + up(r * k / 32);
+    case QF_FMT_Q4K: return up(r * (k / 256) * 144);
+    default: return 0;
+  }
+}
+
+// Carve a packed operand of format fmt out of p (advances p).
+Packed carve_packed(int fmt, int64_t R, int64_t K, char*& p) {
+  Packed q{};
+  const size_t r = R, k = K;
+  if (fmt == QF_FMT_NVFP4) { q.S = reinterpret_cast<float*>(p); p += kAlign; }
+  if (fmt == QF_FMT_NONE) return q;
+  q.codes = reinterpret_cast<uint8_t*>(p);
+  if (fmt == QF_FMT_Q4K) { p += up(r * (k / 256) * 144); return q; }
+  p += up(r * k / 2);
+  q.scales = reinterpret_cast<uint8_t*>(p);
+  p += up(r * k / (fmt == QF_FMT_NVFP4 ? 16 : 32));
+  return q;
+}
+
+// The saved operands of one layer call: packed W_hat, then packed A_hat when afmt != NONE.
+size_t saved_bytes(const qf_qlinear_desc* d) {
+  return packed_bytes(d->wfmt, d->N, d->K) + packed_bytes(d->afmt, d->M, d->K);
+}
+void saved_layout(const qf_qlinear_desc* d, void* saved, Packed* w, Packed* a) {
+  char* p = static_cast<char*>(saved);
+  *w = carve_packed(d->wfmt, d->N, d->K, p);
+  *a = carve_packed(d->afmt, d->M, d->K, p);
+}
+
 // Row stride (elements) of a workspace operand whose rows hold `cols` bf16 values.  Byte strides
 // that are multiples of 32 KB put every row of a GEMM tile on the same memory channels and L2
 // sets (an NT GEMM over 64 KB strides measured ~5 % slower than over 64 KB + 256 B; 16 KB
@@ -116,7 +159,10 @@ int64_t ws_ld(int64_t cols) { return cols % 16384 == 0 ? cols + 128 : cols; }
 
 // Workspace of one linear layer (256-byte aligned regions):
 //   scal   256 B   weight amax scratch
-//   what   [N, K]  W_hat (forward operand), when wfmt != NONE
+//   wpk    packed W_hat (when wfmt != NONE): the forward's GEMM operand (decoded inside the
+//                  GEMM), kept for a QF_FLAG_REUSE_WS backward when no saved buffer is given
+//   what   [N, K]  W_hat in bf16 (when wfmt != NONE): the operand of a materializing forward
+//                  and of the token-count-not-a-multiple-of-8 backward
 //   ahat   [M, K]  A_hat, when afmt != NONE
 //   whatt  [K, N]  W_hat^T (or W^T): right operand of dX = dY W_hat in NT form
 //   ahatt  [K, M]  A_hat^T (or X^T): right operand of dW = dY^T A_hat in NT form (row stride
@@ -125,6 +171,7 @@ int64_t ws_ld(int64_t cols) { return cols % 16384 == 0 ? cols + 128 : cols; }
 //   part   FP32 partial tiles of the dW GEMM's split last round (qf::gemm_nt_split_bytes)
 struct LinearWs {
   float* scal;
+  Packed wpk;
   uint16_t* what;
   uint16_t* ahat;
   uint16_t* whatt;
@@ -136,7 +183,7 @@ struct LinearWs {
 size_t linear_ws_bytes(const qf_qlinear_desc* d) {
   const size_t M = d->M, N = d->N, K = d->K;
   size_t b = kAlign;
-  if (d->wfmt != QF_FMT_NONE) b += up(N * K * 2);
+  if (d->wfmt != QF_FMT_NONE) b += packed_bytes(d->wfmt, d->N, d->K) + up(N * K * 2);
   if (d->afmt != QF_FMT_NONE) b += up(M * K * 2);
   const size_t ldm = (size_t)ws_ld(d->M);
   b += up(K * N * 2) + up(K * ldm * 2) + up(N * ldm * 2);
@@ -150,7 +197,10 @@ LinearWs linear_ws(const qf_qlinear_desc* d, void* ws) {
   LinearWs w{};
   w.scal = reinterpret_cast<float*>(p);
   p += kAlign;
-  if (d->wfmt != QF_FMT_NONE) { w.what = reinterpret_cast<uint16_t*>(p); p += up(N * K * 2); }
+  if (d->wfmt != QF_FMT_NONE) {
+    w.wpk = carve_packed(d->wfmt, d->N, d->K, p);
+    w.what = reinterpret_cast<uint16_t*>(p); p += up(N * K * 2);
+  }
   if (d->afmt != QF_FMT_NONE) { w.ahat = reinterpret_cast<uint16_t*>(p); p += up(M * K * 2); }
   const size_t ldm = (size_t)ws_ld(d->M);
   w.whatt = reinterpret_cast<uint16_t*>(p); p += up(K * N * 2);
@@ -211,11 +261,79 @@ qf_status quantize_operands(const qf_qlinear_desc* d, const Dims& dm, const uint
   return QF_OK;
 }
 
+// Quantize x [R, K] into its packed form pk (codes, block scales, NVFP4 decode scale S) and,
+// when xhat is non-null, its bf16 x_hat.  NVFP4: g_given (device) when non-null, else the
+// tensor amax computed into g_scratch.
+qf_status quantize_packed(int fmt, const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
+                          const float* g_given, float* g_scratch, const Packed& pk,
+                          uint16_t* xhat, hipStream_t s) {
+  switch (fmt) {
+    case QF_FMT_NVFP4: {
+      const float* g = g_given;
+      if (!g) {
+        QF_TRY(dev(qf::launch_fill_f32(g_scratch, 1, 0.0f, s), "amax init"));
+        QF_TRY(dev(qf::launch_amax(x, R, K, ldx, g_scratch, s), "amax"));
+        g = g_scratch;
+      }
+      return dev(qf::launch_nvfp4(x, R, K, ldx, g, pk.S, pk.codes, pk.scales, xhat, s), "nvfp4");
+    }
+    case QF_FMT_MXFP4:
+      return dev(qf::launch_mxfp4(x, R, K, ldx, pk.codes, pk.scales, xhat, s), "mxfp4");
+    case QF_FMT_Q4K:
+      return dev(qf::launch_q4k(x, R, K, ldx, pk.codes, xhat, s), "q4k");
+    default:
+      return fail(QF_EINVAL, "bad format %d", fmt);
+  }
+}
+
+// The forward decodes the packed weight inside the GEMM when the caller asks for it
+// (QF_FLAG_DECODE_IN_GEMM) and K is a multiple of the GEMM's 64-deep stages; otherwise it
+// writes the bf16 W_hat (the packed operand is written either way).
+bool fused_forward(const qf_qlinear_desc* d) {
+  return d->wfmt != QF_FMT_NONE && (d->flags & QF_FLAG_DECODE_IN_GEMM) != 0 && d->K > 0 &&
+         d->K % 64 == 0 && d->N > 0;
+}
+
+qf_status linear_forward(const char* fn, const qf_qlinear_desc* d, const Dims& dm,
+                         const uint16_t* X, const uint16_t* W, uint16_t* Y, const LinearWs& w,
+                         const Packed& pw, const Packed* pa, hipStream_t s) {
+  const bool fused = fused_forward(d);
+  const uint16_t* Wop = W;
+  int64_t ldw_op = dm.ldw;
+  if (d->wfmt != QF_FMT_NONE) {
+    QF_TRY(quantize_packed(d->wfmt, W, d->N, d->K, dm.ldw, d->w_amax, w.scal, pw,
+                           fused ? nullptr : w.what, s));
+    Wop = w.what;
+    ldw_op = d->K;
+  }
+  const uint16_t* Aop = X;
+  int64_t lda_op = dm.ldx;
+  if (d->afmt != QF_FMT_NONE) {
+    if (pa) QF_TRY(quantize_packed(d->afmt, X, d->M, d->K, dm.ldx, d->a_amax, nullptr, *pa, w.ahat, s));
+    else QF_TRY(fakequant_to(d->afmt, X, d->M, d->K, dm.ldx, d->a_amax, nullptr, w.ahat, s));
+    Aop = w.ahat;
+    lda_op = d->K;
+  }
+  if (fused)
+    return dev(qf::launch_gemm_nt_packed_b(d->M, d->N, d->K, Aop, lda_op, d->wfmt, pw.codes,
+                                           pw.scales, pw.S, Y, dm.ldy, s),
+               fn);
+  return dev(qf::launch_gemm_nt(d->M, d->N, d->K, Aop, lda_op, 0, Wop, ldw_op, 0, Y, dm.ldy, 0,
+                                nullptr, s),
+             fn);
+}
+
+qf_status check_saved(const char* fn, const void* saved) {
+  if (saved && (uintptr_t)saved % kAlign)
+    return fail(QF_EALIGN, "%s: saved buffer not 256-byte aligned", fn);
+  return QF_OK;
+}
+
 }  // namespace
 
 extern "C" {
 
-int qf_version(void) { return 100; }
+int qf_version(void) { return 200; }
 
 const char* qf_last_error(void) { return g_err; }
 
@@ -307,28 +425,35 @@ qf_status qf_workspace_size(const qf_qlinear_desc* d, size_t* bytes) {
   return ok();
 }
 
+qf_status qf_saved_size(const qf_qlinear_desc* d, size_t* bytes) {
+  Dims dm;
+  QF_TRY(check_desc("qf_saved_size", d, &dm));
+  if (!bytes) return fail(QF_EINVAL, "qf_saved_size: null output");
+  *bytes = saved_bytes(d);
+  return ok();
+}
+
 qf_status qf_qlinear_fwd(const qf_qlinear_desc* d, const uint16_t* X, const uint16_t* W,
-                         uint16_t* Y, void* ws, size_t ws_bytes, qf_stream_t stream) {
+                         uint16_t* Y, void* saved, void* ws, size_t ws_bytes,
+                         qf_stream_t stream) {
   Dims dm;
   QF_TRY(check_desc("qf_qlinear_fwd", d, &dm));
   QF_TRY(check_mat("qf_qlinear_fwd: X", X, d->M, d->K, dm.ldx, true));
   QF_TRY(check_mat("qf_qlinear_fwd: W", W, d->N, d->K, dm.ldw, true));
   QF_TRY(check_mat("qf_qlinear_fwd: Y", Y, d->M, d->N, dm.ldy, true));
+  QF_TRY(check_saved("qf_qlinear_fwd", saved));
   QF_TRY(check_ws("qf_qlinear_fwd", linear_ws_bytes(d), ws, ws_bytes));
-  hipStream_t s = S(stream);
   LinearWs w = linear_ws(d, ws);
-  const uint16_t *Wop, *Aop;
-  int64_t ldw_op, lda_op;
-  QF_TRY(quantize_operands(d, dm, X, W, w, true, true, &Wop, &ldw_op, &Aop, &lda_op, s));
-  QF_TRY(dev(qf::launch_gemm_nt(d->M, d->N, d->K, Aop, lda_op, 0, Wop, ldw_op, 0, Y, dm.ldy, 0,
-                                nullptr, s),
-             "forward gemm"));
+  Packed pw = w.wpk, pa{};
+  if (saved) saved_layout(d, saved, &pw, &pa);
+  QF_TRY(linear_forward("forward gemm", d, dm, X, W, Y, w, pw, saved ? &pa : nullptr,
+                        S(stream)));
   return ok();
 }
 
 qf_status qf_qlinear_bwd_ste(const qf_qlinear_desc* d, const uint16_t* dY, const uint16_t* X,
-                             const uint16_t* W, uint16_t* dX, float* dW, void* ws,
-                             size_t ws_bytes, qf_stream_t stream) {
+                             const uint16_t* W, const void* saved, uint16_t* dX, float* dW,
+                             void* ws, size_t ws_bytes, qf_stream_t stream) {
   Dims dm;
   QF_TRY(check_desc("qf_qlinear_bwd_ste", d, &dm));
   QF_TRY(check_mat("qf_qlinear_bwd_ste: dY", dY, d->M, d->N, dm.ldy, true));
@@ -336,34 +461,41 @@ qf_status qf_qlinear_bwd_ste(const qf_qlinear_desc* d, const uint16_t* dY, const
   QF_TRY(check_mat("qf_qlinear_bwd_ste: W", W, d->N, d->K, dm.ldw, dX != nullptr));
   QF_TRY(check_mat("qf_qlinear_bwd_ste: dX", dX, d->M, d->K, dm.ldx, false));
   QF_TRY(check_out("qf_qlinear_bwd_ste: dW", dW));
+  QF_TRY(check_saved("qf_qlinear_bwd_ste", saved));
   QF_TRY(check_ws("qf_qlinear_bwd_ste", linear_ws_bytes(d), ws, ws_bytes));
   hipStream_t s = S(stream);
   LinearWs w = linear_ws(d, ws);
   const bool reuse = (d->flags & QF_FLAG_REUSE_WS) != 0;
-  const uint16_t *Wop, *Aop;
-  int64_t ldw_op, lda_op;
+  // Packed W_hat / A_hat of the forward: from `saved`, else (QF_FLAG_REUSE_WS) W_hat from the
+  // workspace's packed region; otherwise the operands are quantized again (identical bits).
+  Packed sw{}, sa{};
+  if (saved) saved_layout(d, const_cast<void*>(saved), &sw, &sa);
+  const Packed* src_w = saved ? &sw : (reuse ? &w.wpk : nullptr);
   if (d->M % 8 == 0) {
-    // NT form: transposed operands through the workspace.  Without saved x_hat operands the
-    // transposed ones come straight from the transposing quantizer (one pass over W and X).
-    // dY^T (left operand of dW) is written by the dX GEMM from the dY tiles it stages anyway
-    // when both gradients are asked for; otherwise by the transpose kernel.
+    // NT form: transposed operands through the workspace.  W_hat^T comes from the packed
+    // operand (transposing dequantizer) or straight from the transposing quantizer (one pass
+    // over W).  dY^T (left operand of dW) is written by the dX GEMM from the dY tiles it stages
+    // anyway when both gradients are asked for; otherwise by the transpose kernel.
     const int64_t ldm = ws_ld(d->M);
     const bool dyt_by_dx = dX != nullptr && dW != nullptr && ldm < qf::kGemmAtMaxLd;
     if (dX) {  // dX[M, K] = dY[M, N] (W_hat^T)[K, N]^T
-      if (d->wfmt != QF_FMT_NONE && !reuse) {
-        const float* g = d->w_amax;
-        if (d->wfmt == QF_FMT_NVFP4 && !g) {
-          QF_TRY(dev(qf::launch_fill_f32(w.scal, 1, 0.0f, s), "amax init"));
-          QF_TRY(dev(qf::launch_amax(W, d->N, d->K, dm.ldw, w.scal, s), "amax"));
-          g = w.scal;
+      if (d->wfmt != QF_FMT_NONE) {
+        if (src_w) {
+          QF_TRY(dev(qf::launch_dequant_t(d->wfmt, src_w->codes, src_w->scales, src_w->S, d->N,
+                                          d->K, w.whatt, d->N, s), "dequantize W (transposed)"));
+        } else {
+          const float* g = d->w_amax;
+          if (d->wfmt == QF_FMT_NVFP4 && !g) {
+            QF_TRY(dev(qf::launch_fill_f32(w.scal, 1, 0.0f, s), "amax init"));
+            QF_TRY(dev(qf::launch_amax(W, d->N, d->K, dm.ldw, w.scal, s), "amax"));
+            g = w.scal;
+          }
+          QF_TRY(dev(qf::launch_quant_t(d->wfmt, W, d->N, d->K, dm.ldw, 1, 0, g, w.whatt, d->N, 0,
+                                        s), "quantize W (transposed)"));
         }
-        QF_TRY(dev(qf::launch_quant_t(d->wfmt, W, d->N, d->K, dm.ldw, 1, 0, g, w.whatt, d->N, 0,
-                                      s), "quantize W (transposed)"));
       } else {
-        const uint16_t* src = d->wfmt != QF_FMT_NONE ? w.what : W;
-        const int64_t ld = d->wfmt != QF_FMT_NONE ? d->K : dm.ldw;
-        QF_TRY(dev(qf::launch_transpose_bf16(src, d->N, d->K, ld, w.whatt, d->N, 1, 0, 0, s),
-                   "transpose W_hat"));
+        QF_TRY(dev(qf::launch_transpose_bf16(W, d->N, d->K, dm.ldw, w.whatt, d->N, 1, 0, 0, s),
+                   "transpose W"));
       }
       QF_TRY(dev(qf::launch_gemm_nt(d->M, d->K, d->N, dY, dm.ldy, 0, w.whatt, d->N, 0, dX,
                                     dm.ldx, 0, nullptr, s, dyt_by_dx ? w.dyt : nullptr, ldm),
@@ -373,7 +505,10 @@ qf_status qf_qlinear_bwd_ste(const qf_qlinear_desc* d, const uint16_t* dY, const
       if (!dyt_by_dx)
         QF_TRY(dev(qf::launch_transpose_bf16(dY, d->M, d->N, dm.ldy, w.dyt, ldm, 1, 0, 0, s),
                    "transpose dY"));
-      if (d->afmt != QF_FMT_NONE && !reuse) {
+      if (d->afmt != QF_FMT_NONE && saved) {
+        QF_TRY(dev(qf::launch_dequant_t(d->afmt, sa.codes, sa.scales, sa.S, d->M, d->K, w.ahatt,
+                                        ldm, s), "dequantize X (transposed)"));
+      } else if (d->afmt != QF_FMT_NONE && !reuse) {
         QF_TRY(dev(qf::launch_quant_t(d->afmt, X, d->M, d->K, dm.ldx, 1, 0, d->a_amax, w.ahatt,
                                       ldm, 0, s), "quantize X (transposed)"));
       } else {
@@ -389,8 +524,12 @@ qf_status qf_qlinear_bwd_ste(const qf_qlinear_desc* d, const uint16_t* dY, const
   } else {
     // Token count not a multiple of 8 (no 16-byte transposed rows): the NT kernel reads
     // W_hat [N, K], dY [M, N] and A_hat [M, K] in place as operands stored [K'][*], through
-    // transposing LDS reads (slower than the transposed operands, correct for any M).
-    QF_TRY(quantize_operands(d, dm, X, W, w, !reuse && dX != nullptr, !reuse && dW != nullptr,
+    // transposing LDS reads (slower than the transposed operands, correct for any M).  W_hat is
+    // quantized again into the workspace (the forward may have left only its packed form);
+    // A_hat is the forward's with QF_FLAG_REUSE_WS.
+    const uint16_t *Wop, *Aop;
+    int64_t ldw_op, lda_op;
+    QF_TRY(quantize_operands(d, dm, X, W, w, dX != nullptr, !reuse && dW != nullptr,
                              &Wop, &ldw_op, &Aop, &lda_op, s));
     if (dX)  // dX[M, K] = dY[M, N] W_hat[N, K]
       QF_TRY(dev(qf::launch_gemm_nt(d->M, d->K, d->N, dY, dm.ldy, 0, Wop, ldw_op, 1, dX, dm.ldx,
@@ -1287,6 +1426,83 @@ qf_status qf_export_fused(int fmt, const qf_member* members, int n, int64_t K, u
     }
   }
   (void)N;
+  return ok();
+}
+
+// ---------------------------------------------------------- packed-operand building blocks
+qf_status qf_gemm_packed_b(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
+                           int fmt, const uint8_t* codes, const uint8_t* scales, const float* Sp,
+                           uint16_t* C, int64_t ldc, qf_stream_t stream) {
+  const char* fn = "qf_gemm_packed_b";
+  if (fmt != QF_FMT_NVFP4 && fmt != QF_FMT_MXFP4 && fmt != QF_FMT_Q4K)
+    return fail(QF_EINVAL, "%s: bad format %d", fn, fmt);
+  if (M < 0 || N < 0 || K < 0) return fail(QF_ESHAPE, "%s: negative shape", fn);
+  if (K % (fmt == QF_FMT_Q4K ? 256 : 64))
+    return fail(QF_ESHAPE, "%s: K=%lld is not a multiple of %d", fn, (long long)K,
+                fmt == QF_FMT_Q4K ? 256 : 64);
+  QF_TRY(check_mat("qf_gemm_packed_b: A", A, M, K, lda, true));
+  QF_TRY(check_mat("qf_gemm_packed_b: C", C, M, N, ldc, true));
+  if (M == 0 || N == 0) return ok();
+  if (!codes || (fmt != QF_FMT_Q4K && !scales) || (fmt == QF_FMT_NVFP4 && !Sp))
+    return fail(QF_EINVAL, "%s: null packed operand", fn);
+  QF_TRY(check_out("qf_gemm_packed_b: codes", codes));
+  QF_TRY(check_out("qf_gemm_packed_b: scales", scales));
+  QF_TRY(dev(qf::launch_gemm_nt_packed_b(M, N, K, A, lda, fmt, codes, scales, Sp, C, ldc,
+                                         S(stream)), fn));
+  return ok();
+}
+
+qf_status qf_dequantize_transposed(int fmt, const uint8_t* codes, const uint8_t* scales,
+                                   const float* Sp, int64_t R, int64_t K, uint16_t* out,
+                                   int64_t ldo, qf_stream_t stream) {
+  const char* fn = "qf_dequantize_transposed";
+  if (fmt != QF_FMT_NVFP4 && fmt != QF_FMT_MXFP4 && fmt != QF_FMT_Q4K)
+    return fail(QF_EINVAL, "%s: bad format %d", fn, fmt);
+  if (R < 0 || K < 0) return fail(QF_ESHAPE, "%s: negative shape", fn);
+  if (K % block_of(fmt)) return fail(QF_ESHAPE, "%s: K=%lld is not a multiple of %lld", fn,
+                                     (long long)K, (long long)block_of(fmt));
+  if (R % 8) return fail(QF_ESHAPE, "%s: R=%lld is not a multiple of 8", fn, (long long)R);
+  if (R == 0 || K == 0) return ok();
+  if (!codes || (fmt != QF_FMT_Q4K && !scales) || (fmt == QF_FMT_NVFP4 && !Sp))
+    return fail(QF_EINVAL, "%s: null packed operand", fn);
+  QF_TRY(check_out("qf_dequantize_transposed: codes", codes));
+  QF_TRY(check_mat("qf_dequantize_transposed: out", out, K, R, ldo, true));
+  QF_TRY(dev(qf::launch_dequant_t(fmt, codes, scales, Sp, R, K, out, ldo, S(stream)), fn));
+  return ok();
+}
+
+// ------------------------------------------------------------------- host-only validation
+qf_status qf_validate_fakequant(int fmt, const void* x, int64_t R, int64_t K, int64_t ldx) {
+  const char* fn = "qf_validate_fakequant";
+  if (fmt != QF_FMT_NVFP4 && fmt != QF_FMT_MXFP4 && fmt != QF_FMT_Q4K)
+    return fail(QF_EINVAL, "%s: bad format %d", fn, fmt);
+  QF_TRY(check_quant_input(fn, static_cast<const uint16_t*>(x), R, K, ldx, block_of(fmt)));
+  return ok();
+}
+
+qf_status qf_validate_qlinear(const qf_qlinear_desc* d, const void* X, const void* W,
+                              const void* Y, const void* saved, const void* ws, size_t ws_bytes) {
+  const char* fn = "qf_validate_qlinear";
+  Dims dm;
+  QF_TRY(check_desc(fn, d, &dm));
+  QF_TRY(check_mat("qf_validate_qlinear: X", X, d->M, d->K, dm.ldx, true));
+  QF_TRY(check_mat("qf_validate_qlinear: W", W, d->N, d->K, dm.ldw, true));
+  QF_TRY(check_mat("qf_validate_qlinear: Y", Y, d->M, d->N, dm.ldy, true));
+  QF_TRY(check_saved(fn, saved));
+  QF_TRY(check_ws(fn, linear_ws_bytes(d), const_cast<void*>(ws), ws_bytes));
+  return ok();
+}
+
+qf_status qf_validate_grouped(const qf_grouped_desc* d, const void* X, const void* W,
+                              const void* Y, const void* ws, size_t ws_bytes) {
+  const char* fn = "qf_validate_grouped";
+  // (the device offsets are the call's own argument; only their presence is checked there)
+  static const int64_t kOffsetsPresent = 0;
+  QF_TRY(check_grouped(fn, d, &kOffsetsPresent));
+  QF_TRY(check_mat("qf_validate_grouped: X", X, d->T, d->K, d->K, true));
+  QF_TRY(check_mat("qf_validate_grouped: W", W, d->E * d->N, d->K, d->K, true));
+  QF_TRY(check_mat("qf_validate_grouped: Y", Y, d->T, d->N, d->N, true));
+  QF_TRY(check_ws(fn, grouped_ws_bytes(d), const_cast<void*>(ws), ws_bytes));
   return ok();
 }
 

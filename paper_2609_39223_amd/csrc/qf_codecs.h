@@ -161,6 +161,72 @@ __device__ __forceinline__ void fp4_decode8(uint32_t cw, float scale, uint32_t w
   w[3] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(cw, scale, 3));
 }
 
+// ---- decoders of packed codes (Eqs. nvfp4-dequant, mxfp4-dequant, q4k-dequant) ------------
+// Each returns the bf16 x_hat of 8 consecutive elements as 4 words (element 2q in the low half
+// of word q).  The quantizers below produce their x_hat through the same functions, and the
+// packed-operand GEMM prologue and the transposing dequantizer decode with them too, so x_hat
+// is bit-identical wherever it is formed.
+
+// NVFP4: 8 codes cw (element k in nibble k: bit 3 sign, bits 0-2 magnitude) of blocks whose
+// decode scale is D = fl(S * s_E4M3): x_hat = bf16(fl(+-V * D)).
+// For a finite D: V from the hardware E2M1 decode (exact), one FP32 product, the hardware
+// round-to-nearest-even pack (|V D| <= 6 D is finite, so the pack rounds as bf16_rne would).
+__device__ __forceinline__ void nvfp4_decode8_finite(uint32_t cw, float D, uint32_t w[4]) {
+  const f32x2_t v0 = e2m1_pair<0>(cw), v1 = e2m1_pair<1>(cw);
+  const f32x2_t v2 = e2m1_pair<2>(cw), v3 = e2m1_pair<3>(cw);
+  w[0] = bf16x2_rne_nonnan(v0.x * D, v0.y * D);
+  w[1] = bf16x2_rne_nonnan(v1.x * D, v1.y * D);
+  w[2] = bf16x2_rne_nonnan(v2.x * D, v2.y * D);
+  w[3] = bf16x2_rne_nonnan(v3.x * D, v3.y * D);
+}
+// D = fl(S * s_E4M3) is finite exactly when the tensor scale S is (s_E4M3 <= 480), so a caller
+// holding one S for many blocks may test S once and call nvfp4_decode8_finite.
+__device__ __forceinline__ void nvfp4_decode8(uint32_t cw, float D, uint32_t w[4]) {
+  if (__builtin_isfinite(D)) {
+    nvfp4_decode8_finite(cw, D, w);
+  } else {                                  // tensor scale from a non-finite amax
+    uint32_t xh[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const float mag = e2m1_value((cw >> (4 * k)) & 7u) * D;
+      xh[k] = bf16_rne((cw >> (4 * k + 3)) & 1u ? -mag : mag);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) w[q] = xh[2 * q] | (xh[2 * q + 1] << 16);
+  }
+}
+
+// The NVFP4 block decode scale D = fl(S * s_E4M3) of E4M3 code sc under tensor scale S.
+__device__ __forceinline__ float nvfp4_block_scale(float S, uint32_t sc) {
+  return S * e4m3_value(sc);
+}
+
+// MXFP4: 8 codes of a block with E8M0 scale code e: x_hat = +-V * 2^(e - 127); a block whose
+// scale code is 0xFF (it held Inf / NaN) decodes to NaN (0x7FC0).
+__device__ __forceinline__ void mxfp4_decode8(uint32_t cw, uint32_t e, uint32_t w[4]) {
+  fp4_decode8(cw, e8m0_scale(e), w);
+  const bool nan = e == 0xFFu;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) w[q] = nan ? 0x7FC07FC0u : w[q];
+}
+
+// Q4_K: 8 unsigned codes q (one per byte: element k in byte k % 4 of qw[k / 4]) of a sub-block
+// with step t1 = fl(d s6) and offset t2 = fl(dmin m6): x_hat = bf16(fl(t1 q - t2)).  t1 q is
+// exact (at most 21 significant bits, far from the FP32 range limits), so a fused multiply-add
+// rounds t1 q - t2 exactly once, as the separate product and difference do.
+__device__ __forceinline__ void q4k_decode8(const uint32_t qw[2], float t1, float t2,
+                                           uint32_t w[4]) {
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    const float a0 = __builtin_fmaf(t1, (float)(qw[p] & 0xFFu), -t2);
+    const float a1 = __builtin_fmaf(t1, (float)((qw[p] >> 8) & 0xFFu), -t2);
+    const float a2 = __builtin_fmaf(t1, (float)((qw[p] >> 16) & 0xFFu), -t2);
+    const float a3 = __builtin_fmaf(t1, (float)(qw[p] >> 24), -t2);
+    w[2 * p] = bf16x2_rne_nonnan(a0, a1);
+    w[2 * p + 1] = bf16x2_rne_nonnan(a2, a3);
+  }
+}
+
 // NVFP4 (16-block = this lane and lane ^ 1): 4-bit codes cw (element k in nibble k), E4M3
 // block scale sc, x_hat bits xh.  S is the FP32 tensor scale g / (6 * 448), six_s = 6 S.
 __device__ __forceinline__ void nvfp4_chunk(const uint32_t h[8], float S, float six_s,
@@ -173,7 +239,7 @@ __device__ __forceinline__ void nvfp4_chunk(const uint32_t h[8], float S, float 
     const float t = as_f32(ab << 16) / six_s;   // t_b = a_b / (6 S)
     sc = e4m3_code(t);
   }
-  const float D = S * e4m3_value(sc);       // block decode scale s_FP32 * s_E4M3,b
+  const float D = nvfp4_block_scale(S, sc); // block decode scale s_FP32 * s_E4M3,b
   const float rcp = D != 0.0f ? 1.0f / D : 0.0f;
   // magnitude codes of fl(|x| * rcp) (scale 2^0), then the sign bit of each input; D = 0
   // gives magnitude 0 for every element (also for Inf / NaN inputs under a caller's g = 0)
@@ -189,27 +255,12 @@ __device__ __forceinline__ void nvfp4_chunk(const uint32_t h[8], float S, float 
   cw = mc;                                  // magnitudes leave bit 3 of each nibble clear
 #pragma unroll
   for (int k = 0; k < 8; ++k) cw |= (h[k] >> 15) << (4 * k + 3);
-  if (__builtin_isfinite(D)) {
-    // x_hat = bf16(+-V D): V from the hardware E2M1 decode (exact), one FP32 product, the
-    // hardware round-to-nearest-even pack.  |V D| <= 6 D is finite here, so this equals the
-    // bit-level path below.
-    const f32x2_t v0 = e2m1_pair<0>(cw), v1 = e2m1_pair<1>(cw);
-    const f32x2_t v2 = e2m1_pair<2>(cw), v3 = e2m1_pair<3>(cw);
-    const uint32_t p[4] = {bf16x2_rne_nonnan(v0.x * D, v0.y * D),
-                           bf16x2_rne_nonnan(v1.x * D, v1.y * D),
-                           bf16x2_rne_nonnan(v2.x * D, v2.y * D),
-                           bf16x2_rne_nonnan(v3.x * D, v3.y * D)};
+  uint32_t p[4];
+  nvfp4_decode8(cw, D, p);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      xh[2 * q] = p[q] & 0xFFFFu;
-      xh[2 * q + 1] = p[q] >> 16;
-    }
-  } else {                                  // tensor scale from a non-finite amax
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const float mag = e2m1_value((cw >> (4 * k)) & 7u) * D;
-      xh[k] = bf16_rne((cw >> (4 * k + 3)) & 1u ? -mag : mag);
-    }
+  for (int q = 0; q < 4; ++q) {
+    xh[2 * q] = p[q] & 0xFFFFu;
+    xh[2 * q + 1] = p[q] >> 16;
   }
 }
 
@@ -229,19 +280,17 @@ __device__ __forceinline__ void mxfp4_chunk(const uint32_t h[8], uint32_t& cw, u
   const uint32_t w[4] = {h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
                          h[6] | (h[7] << 16)};
   cw = fp4_encode8(w, sc);                  // nearest E2M1 of x / 2^(e - 127)
-  uint32_t d[4];
-  fp4_decode8(cw, sc, d);                   // x_hat = +-V * 2^(e - 127)
-#pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    xh[2 * p] = d[p] & 0xFFFFu;
-    xh[2 * p + 1] = d[p] >> 16;
-  }
   scale = e;
   if (nonfinite) {
     cw = 0;
     scale = 0xFFu;
+  }
+  uint32_t d[4];
+  mxfp4_decode8(cw, scale, d);              // x_hat = +-V * 2^(e - 127), or NaN
 #pragma unroll
-    for (int k = 0; k < 8; ++k) xh[k] = 0x7FC0u;
+  for (int p = 0; p < 4; ++p) {
+    xh[2 * p] = d[p] & 0xFFFFu;
+    xh[2 * p + 1] = d[p] >> 16;
   }
 }
 
@@ -325,11 +374,13 @@ __device__ __forceinline__ void q4k_chunk(const uint32_t h[8], Q4kChunk& r, uint
   }
   // t1 q - t2 is finite for every input (t1, t2 come from FP16 scales), so the hardware pack
   // rounds it exactly as bf16_rne would
+  const uint32_t qw[2] = {r.qlo, r.qhi};
+  uint32_t p[4];
+  q4k_decode8(qw, t1, t2, p);
 #pragma unroll
-  for (int k = 0; k < 8; k += 2) {
-    const uint32_t p = bf16x2_rne_nonnan(t1 * (float)qv[k] - t2, t1 * (float)qv[k + 1] - t2);
-    xh[k] = p & 0xFFFFu;
-    xh[k + 1] = p >> 16;
+  for (int k = 0; k < 4; ++k) {
+    xh[2 * k] = p[k] & 0xFFFFu;
+    xh[2 * k + 1] = p[k] >> 16;
   }
 }
 

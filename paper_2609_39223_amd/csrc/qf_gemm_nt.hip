@@ -47,6 +47,8 @@
 #include <algorithm>
 #include <type_traits>
 
+#include "qf.h"
+#include "qf_codecs.h"
 #include "qf_internal.h"
 
 namespace qf {
@@ -107,6 +109,13 @@ struct NtArgs {
   // and zeros up to 64 kstart[e+1].
   uint16_t* at;
   int64_t ldat;
+  // Packed B (the forward's weight, gemm_nt_kernel's BQ != 0): NVFP4 / MXFP4 codes [N][K/2]
+  // (element 2i in the low nibble) and block scales [N][K/16 | K/32], NVFP4's tensor decode
+  // scale S at bq_S; or Q4_K blocks [N][K/256][144] at bq_codes.  Each stage's B tile is
+  // decoded from these in the main loop (K a multiple of 64).
+  const uint8_t* bq_codes;
+  const uint8_t* bq_scales;
+  const float* bq_S;
 };
 
 #define QF_LDS(p) ((__attribute__((address_space(3))) void*)(p))
@@ -176,13 +185,25 @@ __device__ __forceinline__ int remap_xcd(int bid, int nb) {
 // AGPRs) and loads 64 rows of both operands (16 loads per stage); one wavefront per SIMD and a
 // third less LDS fragment traffic per MFMA (0.5 KB instead of 0.75 KB).  Both visit every
 // output element's k slices in the same order, so their results are bit-identical.
-template <bool C_F32, int MODE, bool A_MN, bool B_MN, int WAVES>
+//
+// BQ != 0 (QF_FMT_NVFP4 / MXFP4 / Q4K; four wavefronts, dense, k-contiguous, bf16 C): B is the
+// packed quantized weight instead of a bf16 matrix.  Each lane owns one B row of its
+// wavefront's 64 (row 64 w + lane) and, one step ahead, loads that row's codes and scales for
+// a stage into registers (32 bytes of codes plus 4 / 2 scale bytes, or the Q4_K block's 16-byte
+// header and 32 code bytes); in the next step it decodes them with the quantizers' own decode
+// functions (so the B tile holds x_hat bit for bit) and writes the 8 chunks into the stage's
+// LDS buffer with 16-byte writes, interleaved with that step's MFMAs, before the barrier that
+// publishes the stage.  A keeps its direct-to-LDS loads.
+template <bool C_F32, int MODE, bool A_MN, bool B_MN, int WAVES, int BQ = 0>
 __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
   static_assert(WAVES == 8 || (!A_MN && !B_MN), "operands stored [K][rows] need 8 wavefronts");
+  static_assert(BQ == 0 || (WAVES == 4 && MODE == kDense && !C_F32),
+                "packed B: the four-wavefront dense bf16 form");
   constexpr int NJ = WAVES == 8 ? 2 : 4;         // 32-column accumulator blocks per wavefront
-  constexpr int NLD = WAVES == 8 ? 8 : 16;       // direct-to-LDS loads per wavefront per stage
+  // direct-to-LDS loads per wavefront per stage (packed B: A's only)
+  constexpr int NLD = (WAVES == 8 || BQ != 0) ? 8 : 16;
   // stage s+1's loads: L0 in the last slice of step s-1, L1 in slice 0 and L2 in slice 1
-  constexpr int L0 = WAVES == 8 ? 3 : 6, L1 = WAVES == 8 ? 3 : 5, L2 = NLD - L0 - L1;
+  constexpr int L0 = NLD == 8 ? 3 : 6, L1 = NLD == 8 ? 3 : 5, L2 = NLD - L0 - L1;
   __shared__ __attribute__((aligned(16))) char smem[kSmem];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -288,6 +309,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
 #pragma unroll
   for (int op = 0; op < 2; ++op) {
     if (WAVES == 8 && op != wop) continue;       // uniform
+    if (BQ != 0 && op == 1) continue;            // packed B: decoded through registers
     const bool omn = op ? B_MN : A_MN;
     const int64_t ld = op ? p.ldb : p.lda;
     const int64_t r0 = op ? n0 : m0;
@@ -320,6 +342,177 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
     }
   }
   auto lds_of = [&](int q) { return op_of(q) * kOpStage + lw * 8192 + (q & 7) * 1024; };
+
+  // ---- packed B (BQ != 0): this lane's row and its per-stage loads -------------------------
+  // Row brow = 64 w + lane of the tile (rows past N decode the last valid row; their outputs
+  // are never stored).  Registers of one stage: c0, c1 = the 32 code bytes (element 2i in the
+  // low nibble; Q4_K: byte l holds sub-block 2g's element l low and 2g+1's high), sc = the
+  // block scales (NVFP4 4 bytes, MXFP4 2) or hd = the Q4_K block header (d, dmin, 12 scale bytes).
+  struct BqRegs {
+    uint4 c0, c1, hd;
+    uint32_t sc;
+  };
+  const int brow = lw * 64 + lane;
+  const uint8_t* bq_row = nullptr;
+  const uint8_t* bq_srow = nullptr;
+  float bq_S = 0.0f;
+  if (BQ != 0) {
+    const int64_t gr = n0 + brow < n_end ? n0 + brow : n_end - 1;
+    if (BQ == QF_FMT_Q4K) {
+      bq_row = p.bq_codes + gr * (K / 256) * 144;
+    } else {
+      bq_row = p.bq_codes + gr * (K / 2);
+      bq_srow = p.bq_scales + gr * (K / (BQ == QF_FMT_NVFP4 ? 16 : 32));
+    }
+    if (BQ == QF_FMT_NVFP4) bq_S = p.bq_S[0];    // the quantizer's S = fl(g / 2688)
+  }
+  auto bq_load = [&](int64_t se, BqRegs& r) __attribute__((always_inline)) {
+    if (BQ == QF_FMT_Q4K) {
+      const uint8_t* blk = bq_row + (se >> 2) * 144;
+      r.hd = *reinterpret_cast<const uint4*>(blk);
+      r.c0 = *reinterpret_cast<const uint4*>(blk + 16 + 32 * (se & 3));
+      r.c1 = *reinterpret_cast<const uint4*>(blk + 32 + 32 * (se & 3));
+    } else {
+      r.c0 = *reinterpret_cast<const uint4*>(bq_row + se * 32);
+      r.c1 = *reinterpret_cast<const uint4*>(bq_row + se * 32 + 16);
+      if (BQ == QF_FMT_NVFP4) r.sc = *reinterpret_cast<const uint32_t*>(bq_srow + se * 4);
+      else r.sc = *reinterpret_cast<const uint16_t*>(bq_srow + se * 2);
+    }
+  };
+  // x_hat of logical chunk c (elements 8c .. 8c+7 of the stage) into LDS buffer buf.
+  auto bq_decode = [&](const BqRegs& r, int64_t se, int c, int buf) __attribute__((always_inline)) {
+    const uint32_t cw[8] = {r.c0.x, r.c0.y, r.c0.z, r.c0.w, r.c1.x, r.c1.y, r.c1.z, r.c1.w};
+    uint32_t o[4];
+    if (BQ == QF_FMT_NVFP4) {
+      // (with a non-finite tensor scale the decoded NaN operands may differ from the
+      // quantizer's x_hat in NaN sign and payload only, which the NaN sums do not show)
+      codec::nvfp4_decode8_finite(
+          cw[c], codec::nvfp4_block_scale(bq_S, (r.sc >> (8 * (c >> 1))) & 0xFFu), o);
+    } else if (BQ == QF_FMT_MXFP4) {
+      codec::mxfp4_decode8(cw[c], (r.sc >> (8 * (c >> 2))) & 0xFFu, o);
+    } else {
+      // sub-block j = 2 (se % 4) + (c >= 4): its 6-bit scale and min from the header
+      const int j = 2 * (int)(se & 3) + (c >> 2);
+      const int jj = j & 3, sh = 8 * jj;
+      uint32_t ls, lm;
+      if (j < 4) {
+        ls = (r.hd.y >> sh) & 63u;
+        lm = (r.hd.z >> sh) & 63u;
+      } else {
+        ls = ((r.hd.w >> sh) & 15u) | (((r.hd.y >> (sh + 6)) & 3u) << 4);
+        lm = ((r.hd.w >> (sh + 4)) & 15u) | (((r.hd.z >> (sh + 6)) & 3u) << 4);
+      }
+      const float t1 = codec::f16_value(r.hd.x & 0xFFFFu) * (float)ls;
+      const float t2 = codec::f16_value(r.hd.x >> 16) * (float)lm;
+      const int b = (c & 3) * 2;                  // code bytes 8 (c % 4) .. +7
+      const uint32_t sh4 = c >= 4 ? 4u : 0u;      // sub-block 2g + 1 in the high nibbles
+      const uint32_t qw[2] = {(cw[b] >> sh4) & 0x0F0F0F0Fu, (cw[b + 1] >> sh4) & 0x0F0F0F0Fu};
+      codec::q4k_decode8(qw, t1, t2, o);
+    }
+    *reinterpret_cast<uint4*>(smem + buf * kStage + kOpStage + brow * kRow +
+                              ((c ^ ((brow >> 1) & 7)) << 4)) = make_uint4(o[0], o[1], o[2], o[3]);
+  };
+  BqRegs bq_cur{}, bq_nxt{};
+  // The main loop decodes a stage as a chain of small operations, one after each MFMA of the
+  // step's first three slices, so that no gap between two MFMAs holds more than a few VALU
+  // instructions (one wavefront per SIMD: nothing else issues while this one decodes).
+  //   NVFP4, 48 operations: per chunk c, the block decode scale D (even c), the four element
+  //          pairs (E2M1 -> FP32, x D, bf16 pack), the 16-byte LDS write.
+  //   MXFP4, 24 (every other MFMA): per chunk, pairs 0-1 with the E8M0 scale, pairs 2-3, the
+  //          NaN-block select and the write.
+  //   Q4_K, 43: the super-block's d and dmin, the two sub-blocks' step t1 and offset t2, then
+  //          per chunk four element pairs (the first also extracts the chunk's nibbles) and
+  //          the write.
+  // The arithmetic is the decode functions' (codec::*_decode8), split up.
+  float bq_D = 0.0f, bq_d = 0.0f, bq_dmin = 0.0f, bq_t1[2] = {0.0f, 0.0f}, bq_t2[2] = {0.0f, 0.0f};
+  uint32_t bq_o[4] = {0, 0, 0, 0}, bq_qw[2] = {0, 0}, bq_e = 0;
+  auto bq_word = [&](const BqRegs& r, int c) __attribute__((always_inline)) -> uint32_t {
+    switch (c) {
+      case 0: return r.c0.x; case 1: return r.c0.y; case 2: return r.c0.z; case 3: return r.c0.w;
+      case 4: return r.c1.x; case 5: return r.c1.y; case 6: return r.c1.z; default: return r.c1.w;
+    }
+  };
+  auto bq_store = [&](int c, int buf) __attribute__((always_inline)) {
+    *reinterpret_cast<uint4*>(smem + buf * kStage + kOpStage + brow * kRow +
+                              ((c ^ ((brow >> 1) & 7)) << 4)) =
+        make_uint4(bq_o[0], bq_o[1], bq_o[2], bq_o[3]);
+  };
+  constexpr int kBqOps = BQ == QF_FMT_NVFP4 ? 48 : BQ == QF_FMT_MXFP4 ? 24 : 43;
+  auto bq_op = [&](const BqRegs& r, int64_t se, int u, int buf) __attribute__((always_inline)) {
+    if (BQ == QF_FMT_NVFP4) {
+      const int c = u / 6, k = u % 6;
+      const uint32_t cw = bq_word(r, c);
+      if (k == 0) {
+        if ((c & 1) == 0) bq_D = codec::nvfp4_block_scale(bq_S, (r.sc >> (8 * (c >> 1))) & 0xFFu);
+      } else if (k <= 4) {
+        // (with a non-finite tensor scale the decoded NaN operands may differ from the
+        // quantizer's x_hat in NaN sign and payload only, which the NaN sums do not show)
+        codec::f32x2_t v;
+        switch (k) {
+          case 1: v = codec::e2m1_pair<0>(cw); break;
+          case 2: v = codec::e2m1_pair<1>(cw); break;
+          case 3: v = codec::e2m1_pair<2>(cw); break;
+          default: v = codec::e2m1_pair<3>(cw); break;
+        }
+        bq_o[k - 1] = codec::bf16x2_rne_nonnan(v.x * bq_D, v.y * bq_D);
+      } else {
+        bq_store(c, buf);
+      }
+    } else if (BQ == QF_FMT_MXFP4) {
+      const int c = u / 3, k = u % 3;
+      const uint32_t cw = bq_word(r, c);
+      if (k == 0) bq_e = (r.sc >> (8 * (c >> 2))) & 0xFFu;
+      const float sc = codec::e8m0_scale(bq_e);
+      if (k == 0) {
+        bq_o[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(cw, sc, 0));
+        bq_o[1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(cw, sc, 1));
+      } else if (k == 1) {
+        bq_o[2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(cw, sc, 2));
+        bq_o[3] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(cw, sc, 3));
+      } else {
+        const bool nan = bq_e == 0xFFu;                // (codec::mxfp4_decode8's NaN block)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) bq_o[q] = nan ? 0x7FC07FC0u : bq_o[q];
+        bq_store(c, buf);
+      }
+    } else {
+      if (u == 0) {
+        bq_d = codec::f16_value(r.hd.x & 0xFFFFu);        // d and dmin of the super-block
+        bq_dmin = codec::f16_value(r.hd.x >> 16);
+      } else if (u < 3) {
+        // sub-block j = 2 (se % 4) + u - 1: its 6-bit scale and min from the header
+        const int j = 2 * (int)(se & 3) + u - 1;
+        const int sh = 8 * (j & 3);
+        uint32_t ls, lm;
+        if (j < 4) {
+          ls = (r.hd.y >> sh) & 63u;
+          lm = (r.hd.z >> sh) & 63u;
+        } else {
+          ls = ((r.hd.w >> sh) & 15u) | (((r.hd.y >> (sh + 6)) & 3u) << 4);
+          lm = ((r.hd.w >> (sh + 4)) & 15u) | (((r.hd.z >> (sh + 6)) & 3u) << 4);
+        }
+        bq_t1[u - 1] = bq_d * (float)ls;
+        bq_t2[u - 1] = bq_dmin * (float)lm;
+      } else {
+        const int c = (u - 3) / 5, k = (u - 3) % 5, h = c >> 2;
+        if (k == 0) {
+          const int b = (c & 3) * 2;                // code bytes 8 (c % 4) .. +7
+          const uint32_t sh4 = h ? 4u : 0u;         // sub-block 2g + 1 in the high nibbles
+          bq_qw[0] = (bq_word(r, b) >> sh4) & 0x0F0F0F0Fu;
+          bq_qw[1] = (bq_word(r, b + 1) >> sh4) & 0x0F0F0F0Fu;
+        }
+        if (k < 4) {
+          // elements 2k, 2k + 1: bf16(fl(t1 q - t2)) as in codec::q4k_decode8
+          const uint32_t q = bq_qw[k >> 1] >> (16 * (k & 1));
+          const float a0 = __builtin_fmaf(bq_t1[h], (float)(q & 0xFFu), -bq_t2[h]);
+          const float a1 = __builtin_fmaf(bq_t1[h], (float)((q >> 8) & 0xFFu), -bq_t2[h]);
+          bq_o[k] = codec::bf16x2_rne_nonnan(a0, a1);
+        } else {
+          bq_store(c, buf);
+        }
+      }
+    }
+  };
 
   // ---- fragment offsets ----------------------------------------------------------------------
   // k-major: slice kk, fragment i at fo[kk] + i * 4096 (32 rows of 128 bytes); fragment rows
@@ -511,25 +704,66 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
         if (u1 < 16) at_store(se, BK, u1, v1);
       }
     };
+    // Packed B: stage s+2's registers are loaded in slice 0 (they have the rest of the step,
+    // up to the barrier's wait), and stage s+1's (loaded one step earlier) are decoded into
+    // buffer nxt in small operations spread over slices 0-2.
+    int64_t se1 = 0, se2 = 0;
+    if (BQ != 0) {
+      se1 = n1 + krot;
+      if (se1 >= ks1) se1 -= klen;
+      se2 = n2 + krot;
+      if (se2 >= ks1) se2 -= klen;
+    }
+    // slot g (0..47) = the MFMA of slices 0-2 that the operation follows
+    auto bq_slot = [&](int g) __attribute__((always_inline)) {
+      if (BQ != 0) {
+        if (g == 1) bq_load(se2, bq_nxt);
+        if (BQ == QF_FMT_MXFP4) {
+          if ((g & 1) == 0 && g / 2 < kBqOps) bq_op(bq_cur, se1, g / 2, nxt);
+        } else if (g < kBqOps) {
+          bq_op(bq_cur, se1, g, nxt);
+        }
+      }
+    };
+    auto bq0 = [&](int t) __attribute__((always_inline)) { bq_slot(t); };
+    auto bq1 = [&](int t) __attribute__((always_inline)) {
+      bq_slot(16 + t);
+      at_rd(t);
+    };
+    auto bq2 = [&](int t) __attribute__((always_inline)) { bq_slot(32 + t); };
     slice(std::true_type{}, std::true_type{}, fa[0], fb[0], cs, 1, fa[1], fb[1], n1, nxt, L0, L1,
-          noextra);
+          bq0);
     slice(std::true_type{}, std::true_type{}, fa[1], fb[1], cs, 2, fa[0], fb[0], n1, nxt, L0 + L1,
-          L2, at_rd);
+          L2, bq1);
     slice(std::true_type{}, std::false_type{}, fa[0], fb[0], cs, 3, fa[1], fb[1], 0, 0, 0, 0,
-          noextra);
+          bq2);
     __builtin_amdgcn_s_waitcnt(0);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
+    if (BQ != 0) bq_cur = bq_nxt;               // complete: the wait above covered its loads
     slice(std::integral_constant<bool, !LAST>{}, std::true_type{}, fa[1], fb[1],
           smem + nxt * kStage, 0, fa[0], fb[0], n2, cur, 0, L0, at_st);
   };
 
   const int64_t nfull = K / BK;                 // the K tail (dense, second half) follows it
-  const int64_t krem = (half == 0 || MODE == kGroupK) ? 0 : K % BK;
+  // (packed B: K is a multiple of BK, checked on the host)
+  const int64_t krem = (half == 0 || MODE == kGroupK || BQ != 0) ? 0 : K % BK;
   const int64_t s0 = ks0, s1 = ks1;
   if (s1 > s0) {
 #pragma unroll
     for (int q = 0; q < NLD; ++q) dma(s0, 0, q);
+    if (BQ != 0) {
+      // stage s0's B decoded now; stage s0+1's registers for the first step
+      auto se_of = [&](int64_t st) {
+        int64_t se = st + krot;
+        return se >= ks1 ? se - klen : se;
+      };
+      BqRegs first;
+      bq_load(se_of(s0), first);
+      bq_load(se_of(s0 + 1 < s1 ? s0 + 1 : s1 - 1), bq_cur);
+#pragma unroll
+      for (int c = 0; c < 8; ++c) bq_decode(first, se_of(s0), c, 0);
+    }
     if (s0 + 1 < s1) {
 #pragma unroll
       for (int q = 0; q < L0; ++q) dma(s0 + 1, 1, q);
@@ -794,6 +1028,39 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, in
   if (a.part != nullptr)
     hipLaunchKernelGGL(split_reduce_kernel, dim3(BM * BN / (256 * 4), (unsigned)rem), dim3(256),
                        0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_nt_packed_b(int64_t M, int64_t N, int64_t K, const uint16_t* A,
+                                   int64_t lda, int bfmt, const uint8_t* codes,
+                                   const uint8_t* scales, const float* S, uint16_t* C,
+                                   int64_t ldc, hipStream_t s) {
+  if (K % BK != 0 || (bfmt == QF_FMT_Q4K && K % 256 != 0) || codes == nullptr ||
+      (bfmt != QF_FMT_Q4K && scales == nullptr) || (bfmt == QF_FMT_NVFP4 && S == nullptr))
+    return hipErrorInvalidValue;
+  if (M == 0 || N == 0) return hipSuccess;
+  if (!nt_offsets_fit(K, lda, K)) return hipErrorInvalidValue;
+  NtArgs a{};
+  a.A = A; a.B = nullptr; a.C = C; a.lda = lda; a.ldb = K; a.ldc = ldc;
+  a.M = M; a.N = N; a.K = K;
+  a.bq_codes = codes; a.bq_scales = scales; a.bq_S = S;
+  a.vec_store = vec_store_ok(C, ldc, 2);
+  a.tiles_m = (int)((M + BM - 1) / BM);
+  a.tiles_n = (int)((N + BN - 1) / BN);
+  const dim3 grid((unsigned)((int64_t)a.tiles_m * a.tiles_n)), b4(4 * 64);
+  switch (bfmt) {
+    case QF_FMT_NVFP4:
+      hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, false, false, 4, QF_FMT_NVFP4>), grid, b4, 0, s, a);
+      break;
+    case QF_FMT_MXFP4:
+      hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, false, false, 4, QF_FMT_MXFP4>), grid, b4, 0, s, a);
+      break;
+    case QF_FMT_Q4K:
+      hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, false, false, 4, QF_FMT_Q4K>), grid, b4, 0, s, a);
+      break;
+    default:
+      return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

@@ -36,6 +36,14 @@ hipError_t launch_nvfp4_batched(const uint16_t* x, int64_t E, int64_t R, int64_t
 hipError_t launch_quant_t(int fmt, const uint16_t* x, int64_t R, int64_t K, int64_t ldx,
                           int64_t batch, int64_t xbs, const float* g, uint16_t* out, int64_t ldo,
                           int64_t obs, hipStream_t s);
+// Dequantize with transposed output from packed codes: out[k][r] = x_hat[r][k] (bf16, row
+// stride ldo) of a [R, K] tensor stored as codes [R][K/2] + scales [R][K/16 | K/32] (NVFP4
+// with its tensor decode scale S = g / 2688 at S) or Q4_K blocks [R][K/256][144] (in
+// `codes`); bit-identical to launch_quant_t's x_hat of the tensor those codes came from.
+// R and K multiples of 8 (Q4K: K of 256).
+hipError_t launch_dequant_t(int fmt, const uint8_t* codes, const uint8_t* scales,
+                            const float* S, int64_t R, int64_t K, uint16_t* out, int64_t ldo,
+                            hipStream_t s);
 // Grouped, transposed, 64-padded: rows [off[e], off[e+1]) of x [T, K] (fmt NONE or MXFP4)
 // land as columns [64 kstart[e], 64 kstart[e+1]) of out [K, ldo] (x_hat^T), zeros past each
 // expert's last row.  kstart from launch_grouped_prep.
@@ -55,6 +63,14 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, in
                           int a_mn, const uint16_t* B, int64_t ldb, int b_mn, void* C,
                           int64_t ldc, int c_f32, float* part, hipStream_t s,
                           uint16_t* at = nullptr, int64_t ldat = 0);
+// The forward Y[M, N] = A W_hat^T (bf16 C) with W_hat decoded inside the GEMM from the packed
+// weight (bfmt NVFP4 / MXFP4: codes [N][K/2] + scales [N][K/16 | K/32] + NVFP4 tensor decode
+// scale S = g / 2688 at S; Q4K: blocks [N][K/256][144] in `codes`).  K a multiple of 64 (Q4K:
+// 256); A k-major; codes and scales rows 16-byte aligned (base pointers 16-byte aligned).
+hipError_t launch_gemm_nt_packed_b(int64_t M, int64_t N, int64_t K, const uint16_t* A,
+                                   int64_t lda, int bfmt, const uint8_t* codes,
+                                   const uint8_t* scales, const float* S, uint16_t* C,
+                                   int64_t ldc, hipStream_t s);
 // Bytes of the FP32 partial buffer `part` an [M, N] FP32-output launch may use (a K-split
 // of the last partial round of tiles).  part may be null: no split.
 size_t gemm_nt_split_bytes(int64_t M, int64_t N);

@@ -266,6 +266,78 @@ __global__ __launch_bounds__(kThreads) void quant_t_kernel(const uint16_t* __res
   store_tile_transposed(tile, t, out, ldo, c0, oc0, K, GROUPED ? INT64_MAX : R);
 }
 
+// ============================================ dequantize from packed codes, transposed output
+// out[k][r] = x_hat[r][k] of a tensor stored as packed codes (the layer's saved operands): the
+// tile and store of quant_t_kernel, with each lane's chunk decoded from its 4 code bytes and
+// block scale (Q4_K: 8 code bytes of its super-block plus the block header) by the quantizers'
+// own decode functions, so the output equals quant_t_kernel's for the tensor the codes came
+// from, bit for bit.  NVFP4 takes the stored tensor decode scale S.  R and K multiples of 8.
+template <int FMT>
+__global__ __launch_bounds__(kThreads) void dequant_t_kernel(const uint8_t* __restrict__ codes,
+                                                             const uint8_t* __restrict__ scales,
+                                                             const float* __restrict__ Sp,
+                                                             int64_t R, int64_t K,
+                                                             uint16_t* __restrict__ out,
+                                                             int64_t ldo) {
+  __shared__ uint4 tile[kTR * (kTC / 8)];
+  const int t = threadIdx.x;
+  const int64_t c0 = (int64_t)blockIdx.x * kTC, r0 = (int64_t)blockIdx.y * kTR;
+  const float S = FMT == QF_FMT_NVFP4 ? Sp[0] : 0.0f;
+  uint32_t cw[8], sc[8];
+  uint4 hd[8];
+  const int cc = t & 31;
+  const int64_t gc = c0 + cc * 8;                 // first element of this lane's chunk
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {                   // all loads first
+    const int64_t gr = r0 + i * 8 + (t >> 5);
+    cw[i] = 0; sc[i] = 0; hd[i] = make_uint4(0, 0, 0, 0);
+    if (gr < R && gc < K) {
+      if (FMT == QF_FMT_Q4K) {
+        // element e = 8 cc of super-block gc / 256: code bytes 32 (e / 64) + e % 32 .. +7,
+        // low nibbles for e % 64 < 32, high nibbles otherwise
+        const uint8_t* blk = codes + (gr * (K / 256) + gc / 256) * 144;
+        hd[i] = *reinterpret_cast<const uint4*>(blk);
+        const int e = (int)(gc % 256);
+        const uint2 q = *reinterpret_cast<const uint2*>(blk + 16 + 32 * (e / 64) + e % 32);
+        const uint32_t sh = (e % 64) >= 32 ? 4u : 0u;
+        cw[i] = (q.x >> sh) & 0x0F0F0F0Fu;
+        sc[i] = (q.y >> sh) & 0x0F0F0F0Fu;        // (the second 4 codes)
+      } else {
+        cw[i] = *reinterpret_cast<const uint32_t*>(codes + gr * (K / 2) + gc / 2);
+        sc[i] = scales[gr * (K / (FMT == QF_FMT_NVFP4 ? 16 : 32)) + gc / (FMT == QF_FMT_NVFP4 ? 16 : 32)];
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int row = i * 8 + (t >> 5);
+    uint32_t w[4];
+    if (FMT == QF_FMT_NVFP4) {
+      nvfp4_decode8(cw[i], nvfp4_block_scale(S, sc[i]), w);
+    } else if (FMT == QF_FMT_MXFP4) {
+      mxfp4_decode8(cw[i], sc[i], w);
+    } else {
+      // sub-block j = e / 32 (e = 8 cc): its 6-bit scale and min from the header bytes 4-15
+      const int j = cc >> 2, jj = j & 3, sh = 8 * jj;
+      uint32_t ls, lm;
+      if (j < 4) {
+        ls = (hd[i].y >> sh) & 63u;
+        lm = (hd[i].z >> sh) & 63u;
+      } else {
+        ls = ((hd[i].w >> sh) & 15u) | (((hd[i].y >> (sh + 6)) & 3u) << 4);
+        lm = ((hd[i].w >> (sh + 4)) & 15u) | (((hd[i].z >> (sh + 6)) & 3u) << 4);
+      }
+      const float t1 = f16_value(hd[i].x & 0xFFFFu) * (float)ls;
+      const float t2 = f16_value(hd[i].x >> 16) * (float)lm;
+      const uint32_t qw[2] = {cw[i], sc[i]};
+      q4k_decode8(qw, t1, t2, w);
+    }
+    tile[row * 32 + tslot(row, cc)] = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+  __syncthreads();
+  store_tile_transposed(tile, t, out, ldo, c0, r0, K, R);
+}
+
 inline dim3 row_grid(int64_t R, int64_t K, int rpt) {
   const int64_t chunks = K >> 3;
   return dim3((unsigned)((chunks + kThreads - 1) / kThreads), (unsigned)((R + rpt - 1) / rpt), 1);
@@ -410,6 +482,30 @@ hipError_t launch_quant_t(int fmt, const uint16_t* x, int64_t R, int64_t K, int6
   if (R == 0 || K == 0 || batch == 0) return hipSuccess;
   return launch_quant_t_impl<false>(fmt, x, R, K, ldx, batch, xbs, g, out, ldo, obs, nullptr,
                                     nullptr, 0, (R + kTR - 1) / kTR, s);
+}
+
+hipError_t launch_dequant_t(int fmt, const uint8_t* codes, const uint8_t* scales,
+                            const float* S, int64_t R, int64_t K, uint16_t* out, int64_t ldo,
+                            hipStream_t s) {
+  if (R == 0 || K == 0) return hipSuccess;
+  const dim3 grid((unsigned)((K + kTC - 1) / kTC), (unsigned)((R + kTR - 1) / kTR));
+  switch (fmt) {
+    case QF_FMT_NVFP4:
+      hipLaunchKernelGGL(dequant_t_kernel<QF_FMT_NVFP4>, grid, dim3(kThreads), 0, s, codes, scales,
+                         S, R, K, out, ldo);
+      break;
+    case QF_FMT_MXFP4:
+      hipLaunchKernelGGL(dequant_t_kernel<QF_FMT_MXFP4>, grid, dim3(kThreads), 0, s, codes, scales,
+                         S, R, K, out, ldo);
+      break;
+    case QF_FMT_Q4K:
+      hipLaunchKernelGGL(dequant_t_kernel<QF_FMT_Q4K>, grid, dim3(kThreads), 0, s, codes, scales,
+                         S, R, K, out, ldo);
+      break;
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_quant_t_grouped(int fmt, const uint16_t* x, int64_t T, int64_t K,

@@ -100,9 +100,60 @@ def test_workspace_size_and_desc_validation(L):
     for dd, w in zip(bad, want):
         assert L.qf_workspace_size(ctypes.byref(dd), ctypes.byref(n)) == w
     # too-small workspace is rejected before any launch
-    assert L.qf_qlinear_fwd(ctypes.byref(d), P(256), P(256), P(256), P(256), ctypes.c_size_t(16),
-                            None) == QF_EINVAL
+    assert L.qf_qlinear_fwd(ctypes.byref(d), P(256), P(256), P(256), None, P(256),
+                            ctypes.c_size_t(16), None) == QF_EINVAL
     assert b"workspace" in L.qf_last_error()
+    # a misaligned saved buffer too
+    assert L.qf_qlinear_fwd(ctypes.byref(d), P(256), P(256), P(256), P(272), P(256),
+                            ctypes.c_size_t(1 << 40), None) == QF_EALIGN
+    assert b"saved" in L.qf_last_error()
+
+
+def test_saved_size_is_the_packed_operands(L):
+    """qf_saved_size: packed W (and A when quantized), each region 256-byte aligned:
+    NVFP4 256 B (S) + codes K/2 + E4M3 scales K/16 per row; MXFP4 codes + K/32 scales;
+    Q4_K 144 bytes per 256 elements (Sec. 3.2.1's transient operands in deployment form)."""
+    def up(v):
+        return (v + 255) // 256 * 256
+    n = ctypes.c_size_t()
+    M, N, K = 264, 520, 512
+    cases = [(1, 0, 256 + up(N * K // 2) + up(N * K // 16)),
+             (2, 2, up(N * K // 2) + up(N * K // 32) + up(M * K // 2) + up(M * K // 32)),
+             (3, 0, up(N * (K // 256) * 144)),
+             (1, 1, 256 + up(N * K // 2) + up(N * K // 16) + 256 + up(M * K // 2) + up(M * K // 16)),
+             (0, 0, 0)]
+    for wf, af, want in cases:
+        d = Desc(M, N, K, 0, 0, 0, wf, af, None, P(256) if af == 1 else None, 0)
+        assert L.qf_saved_size(ctypes.byref(d), ctypes.byref(n)) == QF_OK
+        assert n.value == want, (wf, af)
+        assert n.value <= 0.5625 * (N + (M if af else 0)) * K + 3 * 256 + 2 * 256
+
+
+def test_validate_calls_mirror_the_entry_points(L):
+    """qf_validate_*: host-only checks that return what the call itself would, without a
+    launch (every case here would fail before one)."""
+    v = L.qf_validate_fakequant
+    assert v(1, P(256), I64(4), I64(64), I64(64)) == QF_OK
+    assert v(2, P(256), I64(4), I64(48), I64(48)) == QF_ESHAPE        # K % 32
+    assert b"multiple" in L.qf_last_error()
+    assert v(3, P(256), I64(4), I64(512), I64(512)) == QF_OK
+    assert v(3, P(256), I64(4), I64(384), I64(384)) == QF_ESHAPE      # K % 256
+    assert v(9, P(256), I64(4), I64(64), I64(64)) == QF_EINVAL        # format
+    assert v(1, P(264), I64(4), I64(64), I64(64)) == QF_EALIGN
+    assert v(1, None, I64(4), I64(64), I64(64)) == QF_EINVAL
+    n = ctypes.c_size_t()
+    d = Desc(256, 512, 512, 0, 0, 0, 2, 2, None, None, 0)
+    assert L.qf_workspace_size(ctypes.byref(d), ctypes.byref(n)) == QF_OK
+    vq = L.qf_validate_qlinear
+    vq.argtypes = [ctypes.POINTER(Desc), P, P, P, P, P, ctypes.c_size_t]
+    assert vq(ctypes.byref(d), P(256), P(512), P(768), P(1024), P(4096), n.value) == QF_OK
+    assert vq(ctypes.byref(d), P(256), P(512), P(768), P(1024), P(4096), n.value - 1) == QF_EINVAL
+    assert vq(ctypes.byref(d), P(256), P(512), P(768), P(1040), P(4096), n.value) == QF_EALIGN
+    assert vq(ctypes.byref(d), P(256), None, P(768), None, P(4096), n.value) == QF_EINVAL
+    bad = Desc(256, 512, 500, 0, 0, 0, 1, 0, None, None, 0)
+    assert vq(ctypes.byref(bad), P(256), P(512), P(768), None, P(4096), 1 << 40) == QF_ESHAPE
+    nv_act = Desc(256, 512, 512, 0, 0, 0, 1, 1, None, None, 0)        # NVFP4 A needs a_amax
+    assert vq(ctypes.byref(nv_act), P(256), P(512), P(768), None, P(4096), 1 << 40) == QF_EINVAL
 
 
 def test_gemm_validation(L):
