@@ -206,6 +206,22 @@ QF_API qf_status qf_qlinear_fwd(const qf_qlinear_desc* d, const uint16_t* X, con
                                 qf_stream_t stream);
 
 /*
+ * qf_qlinear_fwd_noalloc -- qf_qlinear_fwd without a workspace argument, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation).  Same kernels and bit-identical Y.  The quantized operands (W_hat,
+ * A_hat) and the amax scalar live in a static device array of QF_NOALLOC_SCRATCH_BYTES that
+ * the library holds on every device it runs on until the process ends; the call allocates and
+ * frees nothing.  Limit: 256 + 2 N K (when wfmt != NONE) + 2 M K (when afmt != NONE) bytes,
+ * each operand rounded up to 256, at most QF_NOALLOC_SCRATCH_BYTES (QF_ESHAPE beyond it).
+ * Every call on one device shares that device's array and leaves its contents behind: calls
+ * that overlap on one device (different streams, or threads) race and must be serialized by
+ * the caller.  No QF_FLAG_REUSE_WS backward can follow this call (there is no workspace).
+ */
+#define QF_NOALLOC_SCRATCH_BYTES (64u << 20)
+QF_API qf_status qf_qlinear_fwd_noalloc(const qf_qlinear_desc* d, const uint16_t* X,
+                                        const uint16_t* W, uint16_t* Y, qf_stream_t stream);
+
+/*
  * qf_qlinear_bwd_ste -- straight-through backward.
  *   dX = dY W_hat      bf16 [M, K]  (Eq. activation-ste)        dX may be NULL
  *   dW = dY^T A_hat    FP32 [N, K]  (Eq. ste; A_hat = X when afmt == NONE)  dW may be NULL

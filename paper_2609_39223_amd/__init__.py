@@ -88,6 +88,8 @@ def lib() -> ctypes.CDLL:
                               ctypes.c_int),
             "qf_qlinear_fwd": ([ctypes.POINTER(QLinearDesc), _P, _P, _P, _P, _P, ctypes.c_size_t,
                                 _P], ctypes.c_int),
+            "qf_qlinear_fwd_noalloc": ([ctypes.POINTER(QLinearDesc), _P, _P, _P, _P],
+                                       ctypes.c_int),
             "qf_qlinear_bwd_ste": ([ctypes.POINTER(QLinearDesc), _P, _P, _P, _P, _P, _P, _P,
                                     ctypes.c_size_t, _P], ctypes.c_int),
             "qf_gemm_packed_b": ([_I, _I, _I, _P, _I, ctypes.c_int, _P, _P, _P, _P, _I, _P],
@@ -259,6 +261,13 @@ def saved_buffer(desc: QLinearDesc, device="cuda"):
 def qlinear_fwd(desc, X, W, Y, ws, saved=None):
     _check(lib().qf_qlinear_fwd(ctypes.byref(desc), _ptr(_bf16(X)), _ptr(_bf16(W)),
                                 _ptr(_bf16(Y)), _ptr(saved), _ptr(ws), ws.numel(), _stream()))
+    return Y
+
+
+def qlinear_fwd_noalloc(desc, X, W, Y):
+    """qf_qlinear_fwd_noalloc: the forward with the library's static device scratch."""
+    _check(lib().qf_qlinear_fwd_noalloc(ctypes.byref(desc), _ptr(_bf16(X)), _ptr(_bf16(W)),
+                                        _ptr(_bf16(Y)), _stream()))
     return Y
 
 

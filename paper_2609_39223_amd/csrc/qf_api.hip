@@ -6,6 +6,8 @@
 #include <stdint.h>
 #include <stdio.h>
 
+#include <mutex>
+
 #include "qf.h"
 #include "qf_internal.h"
 
@@ -448,6 +450,80 @@ qf_status qf_qlinear_fwd(const qf_qlinear_desc* d, const uint16_t* X, const uint
   if (saved) saved_layout(d, saved, &pw, &pa);
   QF_TRY(linear_forward("forward gemm", d, dm, X, W, Y, w, pw, saved ? &pa : nullptr,
                         S(stream)));
+  return ok();
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------- allocation-free forward
+// The forward's quantized operands (W_hat, A_hat and the amax scalar) in a file-scope device
+// array instead of a caller workspace.  Each device the library runs on holds its own copy at
+// its own address, for the life of the process.  Host code never passes `scratch` itself (in
+// host code that name is a stand-in, not a device address): it passes the address that
+// hipGetSymbolAddress returns for the current device, looked up once per device.
+namespace {
+
+static __device__ __align__(256) char scratch[QF_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+qf_status scratch_of_current_device(void** out) {
+  int dev_id = 0;
+  QF_TRY(dev(hipGetDevice(&dev_id), "hipGetDevice"));
+  if (dev_id < 0 || dev_id >= kMaxDevices)
+    return fail(QF_ENOTSUP, "device %d beyond the %d the library tracks", dev_id, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev_id]) {
+    void* p = nullptr;
+    QF_TRY(dev(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)"));
+    if (!p || (uintptr_t)p % kAlign) return fail(QF_EDEVICE, "scratch address not usable");
+    g_scratch_ptr[dev_id] = p;
+  }
+  *out = g_scratch_ptr[dev_id];
+  return QF_OK;
+}
+
+// Bytes of the forward's operands: the scalar slot, W_hat [N, K] and A_hat [M, K] (bf16).
+size_t fwd_operand_bytes(const qf_qlinear_desc* d) {
+  const size_t M = d->M, N = d->N, K = d->K;
+  size_t b = kAlign;
+  if (d->wfmt != QF_FMT_NONE) b += up(N * K * 2);
+  if (d->afmt != QF_FMT_NONE) b += up(M * K * 2);
+  return b;
+}
+
+}  // namespace
+
+extern "C" {
+
+qf_status qf_qlinear_fwd_noalloc(const qf_qlinear_desc* d, const uint16_t* X, const uint16_t* W,
+                                 uint16_t* Y, qf_stream_t stream) {
+  Dims dm;
+  QF_TRY(check_desc("qf_qlinear_fwd_noalloc", d, &dm));
+  QF_TRY(check_mat("qf_qlinear_fwd_noalloc: X", X, d->M, d->K, dm.ldx, true));
+  QF_TRY(check_mat("qf_qlinear_fwd_noalloc: W", W, d->N, d->K, dm.ldw, true));
+  QF_TRY(check_mat("qf_qlinear_fwd_noalloc: Y", Y, d->M, d->N, dm.ldy, true));
+  const size_t need = fwd_operand_bytes(d);
+  if (need > (size_t)QF_NOALLOC_SCRATCH_BYTES)
+    return fail(QF_ESHAPE, "qf_qlinear_fwd_noalloc: the quantized operands need %zu bytes, "
+                "beyond the %zu-byte static scratch", need, (size_t)QF_NOALLOC_SCRATCH_BYTES);
+  void* base = nullptr;
+  QF_TRY(scratch_of_current_device(&base));
+  char* p = static_cast<char*>(base);
+  LinearWs w{};
+  w.scal = reinterpret_cast<float*>(p);   // the amax slot is rewritten (zero fill + max) per call
+  p += kAlign;
+  if (d->wfmt != QF_FMT_NONE) { w.what = reinterpret_cast<uint16_t*>(p); p += up((size_t)d->N * d->K * 2); }
+  if (d->afmt != QF_FMT_NONE) w.ahat = reinterpret_cast<uint16_t*>(p);
+  hipStream_t s = S(stream);
+  const uint16_t *Wop, *Aop;
+  int64_t ldw_op, lda_op;
+  QF_TRY(quantize_operands(d, dm, X, W, w, true, true, &Wop, &ldw_op, &Aop, &lda_op, s));
+  QF_TRY(dev(qf::launch_gemm_nt(d->M, d->N, d->K, Aop, lda_op, 0, Wop, ldw_op, 0, Y, dm.ldy, 0,
+                                nullptr, s),
+             "forward gemm"));
   return ok();
 }
 
