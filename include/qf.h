@@ -366,6 +366,28 @@ QF_API qf_status qf_dequantize_transposed(int fmt, const uint8_t* codes, const u
                                           int64_t ldo, qf_stream_t stream);
 
 /*
+ * Fragment-major B operand: B [N, K] stored as the v_mfma_f32_32x32x16_bf16 operands of 32-row
+ * by 16-column blocks, blocks ordered row-block-major: element (n, k) at
+ *   ((n / 32) (K / 16) + k / 16) * 512 + ((n % 32) + 32 ((k / 8) % 2)) * 8 + k % 8,
+ * rows past N (up to the next multiple of 32) zero.  A GEMM reading B in this form loads each
+ * wavefront's operand of one 16-deep slice as one contiguous 1 KB block straight into the
+ * matrix cores' registers and stages only A in LDS (half of the LDS traffic of the k-contiguous
+ * form).  K % 16 == 0 for the layout, K % 64 == 0 for the GEMM.
+ * qf_fragment_bytes: bytes of the layout (host only).
+ * qf_pack_fragments: out (fragment-major) from B [N, K] row-major with row stride ldb
+ *   (16-byte aligned, ldb % 8 == 0).
+ * qf_gemm_bf16_fragb: C[M, N] = A B^T with A [M, K] k-contiguous (row stride lda) and B in the
+ *   fragment-major layout; bf16 or FP32 C as qf_gemm_bf16_ws (same split of a partial last round
+ *   with the workspace); bit-identical to qf_gemm_bf16 on the row-major B.
+ */
+QF_API qf_status qf_fragment_bytes(int64_t N, int64_t K, size_t* bytes);
+QF_API qf_status qf_pack_fragments(const uint16_t* B, int64_t N, int64_t K, int64_t ldb,
+                                   uint16_t* out, qf_stream_t stream);
+QF_API qf_status qf_gemm_bf16_fragb(int64_t M, int64_t N, int64_t K, const uint16_t* A,
+                                    int64_t lda, const uint16_t* Bf, void* C, int64_t ldc,
+                                    int c_f32, void* ws, size_t ws_bytes, qf_stream_t stream);
+
+/*
  * qf_gemm_workspace_size / qf_gemm_bf16_ws -- qf_gemm_bf16 with a caller workspace.  With
  * k-contiguous A and B and an FP32 C (the dW product), a last round of output tiles that
  * would leave at least half of the compute units idle is computed as two K-halves into the

@@ -92,6 +92,10 @@ def lib() -> ctypes.CDLL:
                                        ctypes.c_int),
             "qf_qlinear_bwd_ste": ([ctypes.POINTER(QLinearDesc), _P, _P, _P, _P, _P, _P, _P,
                                     ctypes.c_size_t, _P], ctypes.c_int),
+            "qf_fragment_bytes": ([_I, _I, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
+            "qf_pack_fragments": ([_P, _I, _I, _I, _P, _P], ctypes.c_int),
+            "qf_gemm_bf16_fragb": ([_I, _I, _I, _P, _I, _P, _P, _I, ctypes.c_int, _P,
+                                    ctypes.c_size_t, _P], ctypes.c_int),
             "qf_gemm_packed_b": ([_I, _I, _I, _P, _I, ctypes.c_int, _P, _P, _P, _P, _I, _P],
                                  ctypes.c_int),
             "qf_dequantize_transposed": ([ctypes.c_int, _P, _P, _P, _I, _I, _P, _I, _P],
@@ -314,6 +318,27 @@ def gemm_bf16_at(M, N, K, A, lda, B, ldb, C, ldc, at, ldat):
     _check(lib().qf_gemm_bf16_at(M, N, K, _ptr(_bf16(A)), lda, _ptr(_bf16(B)), ldb,
                                  _ptr(_bf16(C)), ldc, _ptr(_bf16(at)), ldat, _stream()))
     return C, at
+
+
+def fragment_bytes(N, K) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().qf_fragment_bytes(N, K, ctypes.byref(n)))
+    return n.value
+
+
+def pack_fragments(B, out):
+    """qf_pack_fragments: out (a flat 16-bit tensor of fragment_bytes(N, K) bytes) from B [N, K]."""
+    N, K, ld = _rows(_bf16(B))
+    _check(lib().qf_pack_fragments(_ptr(_bf16(B)), N, K, ld, _ptr(out), _stream()))
+    return out
+
+
+def gemm_bf16_fragb(M, N, K, A, lda, Bf, C, ldc, c_f32, ws=None):
+    """qf_gemm_bf16_fragb: C = A B^T with B in the fragment-major layout."""
+    _check(lib().qf_gemm_bf16_fragb(M, N, K, _ptr(_bf16(A)), lda, _ptr(Bf), _ptr(C), ldc,
+                                    int(c_f32), _ptr(ws), 0 if ws is None else ws.numel(),
+                                    _stream()))
+    return C
 
 
 def gemm_packed_b(M, N, K, A, lda, fmt, codes, scales, S, C, ldc):

@@ -1505,6 +1505,50 @@ qf_status qf_export_fused(int fmt, const qf_member* members, int n, int64_t K, u
   return ok();
 }
 
+// ------------------------------------------------------------- fragment-major B operands
+qf_status qf_fragment_bytes(int64_t N, int64_t K, size_t* bytes) {
+  if (N < 0 || K < 0) return fail(QF_ESHAPE, "qf_fragment_bytes: negative shape");
+  if (K % 16) return fail(QF_ESHAPE, "qf_fragment_bytes: K=%lld is not a multiple of 16", (long long)K);
+  if (!bytes) return fail(QF_EINVAL, "qf_fragment_bytes: null output");
+  *bytes = qf::gemm_frag_bytes(N, K);
+  return ok();
+}
+
+qf_status qf_pack_fragments(const uint16_t* B, int64_t N, int64_t K, int64_t ldb, uint16_t* out,
+                            qf_stream_t stream) {
+  const char* fn = "qf_pack_fragments";
+  if (N < 0 || K < 0) return fail(QF_ESHAPE, "%s: negative shape", fn);
+  if (K % 16) return fail(QF_ESHAPE, "%s: K=%lld is not a multiple of 16", fn, (long long)K);
+  QF_TRY(check_mat("qf_pack_fragments: B", B, N, K, ldb, true));
+  if (N == 0 || K == 0) return ok();
+  if (!out) return fail(QF_EINVAL, "%s: null output", fn);
+  QF_TRY(check_out("qf_pack_fragments: out", out));
+  QF_TRY(dev(qf::launch_frag_pack(B, N, K, ldb, out, S(stream)), fn));
+  return ok();
+}
+
+qf_status qf_gemm_bf16_fragb(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
+                             const uint16_t* Bf, void* C, int64_t ldc, int c_f32, void* ws,
+                             size_t ws_bytes, qf_stream_t stream) {
+  const char* fn = "qf_gemm_bf16_fragb";
+  if (M < 0 || N < 0 || K < 0) return fail(QF_ESHAPE, "%s: negative shape", fn);
+  if (K % 64) return fail(QF_ESHAPE, "%s: K=%lld is not a multiple of 64", fn, (long long)K);
+  if (c_f32 != 0 && c_f32 != 1) return fail(QF_EINVAL, "%s: c_f32 must be 0/1", fn);
+  QF_TRY(check_mat("qf_gemm_bf16_fragb: A", A, M, K, lda, true));
+  if (!C && M > 0 && N > 0) return fail(QF_EINVAL, "%s: null C", fn);
+  if (ldc < N) return fail(QF_ESHAPE, "%s: ldc < N", fn);
+  if (M == 0 || N == 0) return ok();
+  if (!Bf) return fail(QF_EINVAL, "%s: null B", fn);
+  QF_TRY(check_out("qf_gemm_bf16_fragb: B", Bf));
+  float* part = nullptr;
+  if (c_f32 && ws) {
+    if ((uintptr_t)ws % kAlign) return fail(QF_EALIGN, "%s: workspace not 256-byte aligned", fn);
+    if (ws_bytes >= qf::gemm_nt_split_bytes(M, N)) part = static_cast<float*>(ws);
+  }
+  QF_TRY(dev(qf::launch_gemm_nt_bf(M, N, K, A, lda, Bf, C, ldc, c_f32, part, S(stream)), fn));
+  return ok();
+}
+
 // ---------------------------------------------------------- packed-operand building blocks
 qf_status qf_gemm_packed_b(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
                            int fmt, const uint8_t* codes, const uint8_t* scales, const float* Sp,

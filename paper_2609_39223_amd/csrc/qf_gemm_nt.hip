@@ -73,6 +73,13 @@ constexpr int kPitch32 = BN * 4 + 32;            // epilogue LDS row pitch, FP32
 constexpr int kSmemEpi = (BM * kPitch16 > 128 * kPitch32) ? BM * kPitch16 : 128 * kPitch32;
 constexpr int kSmem = (2 * kStage > kSmemEpi) ? 2 * kStage : kSmemEpi;
 
+// Fragment-major layout of a B operand [N, K] (K a multiple of 16): block (nb, kb) holds rows
+// 32 nb .. 32 nb + 31 and columns 16 kb .. 16 kb + 15 as the 64 lanes' MFMA operands of
+// v_mfma_f32_32x32x16_bf16 (lane L: row 32 nb + L % 32, columns 16 kb + 8 (L / 32) .. +7, 16
+// bytes), blocks ordered nb-major: element (n, k) at
+//   ((n / 32) (K / 16) + k / 16) kBfBlock + ((n % 32) + 32 ((k / 8) % 2)) 8 + k % 8,
+// rows past N zero.  A wavefront's operand of one slice and block is one contiguous 1 KB load.
+constexpr int kBfBlock = 512;                    // elements per block (64 lanes x 8)
 // kDenseAT / kGroupRowsAT: dense / grouped rows, and the launch also writes A^T (NtArgs::at).
 enum Mode { kDense = 0, kGroupRows = 1, kGroupK = 2, kDenseAT = 3, kGroupRowsAT = 4 };
 
@@ -194,16 +201,29 @@ __device__ __forceinline__ int remap_xcd(int bid, int nb) {
 // functions (so the B tile holds x_hat bit for bit) and writes the 8 chunks into the stage's
 // LDS buffer with 16-byte writes, interleaved with that step's MFMAs, before the barrier that
 // publishes the stage.  A keeps its direct-to-LDS loads.
-template <bool C_F32, int MODE, bool A_MN, bool B_MN, int WAVES, int BQ = 0>
+//
+// BF (four wavefronts, k-contiguous A, dense modes, K a multiple of 64): B comes in the
+// fragment-major layout (see kBfBlock) straight from memory into the MFMA operand registers,
+// one fully coalesced 1 KB load per 32-row block and 16-deep slice, and never enters LDS: LDS
+// then carries only A (its direct-to-LDS copies and fragment reads), half of the traffic of
+// the form above, which is the budget the MFMAs wait on.  Each B fragment of stage s+1 is
+// loaded right after the last MFMA that uses the same register for stage s, so it has a whole
+// step to arrive; A's copies of stage s+1 all go out at the start of step s, ahead of every B
+// load of the step, and the barrier waits for them while leaving that step's B loads in flight.
+template <bool C_F32, int MODE, bool A_MN, bool B_MN, int WAVES, int BQ = 0, bool BF = false>
 __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
   static_assert(WAVES == 8 || (!A_MN && !B_MN), "operands stored [K][rows] need 8 wavefronts");
   static_assert(BQ == 0 || (WAVES == 4 && MODE == kDense && !C_F32),
                 "packed B: the four-wavefront dense bf16 form");
+  static_assert(!BF || (WAVES == 4 && BQ == 0 && (MODE == kDense || MODE == kDenseAT)),
+                "fragment-major B: the four-wavefront dense forms");
   constexpr int NJ = WAVES == 8 ? 2 : 4;         // 32-column accumulator blocks per wavefront
-  // direct-to-LDS loads per wavefront per stage (packed B: A's only)
-  constexpr int NLD = (WAVES == 8 || BQ != 0) ? 8 : 16;
+  // direct-to-LDS loads per wavefront per stage (packed or fragment-major B: A's only)
+  constexpr int NLD = (WAVES == 8 || BQ != 0 || BF) ? 8 : 16;
   // stage s+1's loads: L0 in the last slice of step s-1, L1 in slice 0 and L2 in slice 1
-  constexpr int L0 = NLD == 8 ? 3 : 6, L1 = NLD == 8 ? 3 : 5, L2 = NLD - L0 - L1;
+  // (fragment-major B: all of A's in slice 0)
+  constexpr int L0 = BF ? 0 : NLD == 8 ? 3 : 6, L1 = BF ? 8 : NLD == 8 ? 3 : 5;
+  constexpr int L2 = NLD - L0 - L1;
   __shared__ __attribute__((aligned(16))) char smem[kSmem];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -309,7 +329,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
 #pragma unroll
   for (int op = 0; op < 2; ++op) {
     if (WAVES == 8 && op != wop) continue;       // uniform
-    if (BQ != 0 && op == 1) continue;            // packed B: decoded through registers
+    if ((BQ != 0 || BF) && op == 1) continue;    // packed / fragment-major B: registers
     const bool omn = op ? B_MN : A_MN;
     const int64_t ld = op ? p.ldb : p.lda;
     const int64_t r0 = op ? n0 : m0;
@@ -546,6 +566,23 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
 #pragma unroll
     for (int j = 0; j < NJ; ++j) acc[i][j] = f32x16_t{};
   bf16x8_t fa[2][4], fb[2][NJ];
+  // Fragment-major B (BF): fbr[kk][j] holds the B fragment of 16-deep slice kk and 32-row
+  // block j of this wavefront's 128 columns for the stage in use.  Block j's fragments start at
+  // bf_base[j]; slice kk of global stage se is kBfBlock elements further per (4 se + kk).
+  bf16x8_t fbr[BF ? 4 : 1][BF ? 4 : 1];
+  const uint16_t* bf_base[BF ? 4 : 1];
+  if (BF) {
+    const int64_t nblocks = (p.N + 31) / 32, kblocks = p.K / 16;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      int64_t nb = (n0 + wn * 128) / 32 + j;
+      nb = nb < nblocks ? nb : nblocks - 1;      // blocks past N: outputs never stored
+      bf_base[j] = p.B + (nb * kblocks) * kBfBlock + lane * 8;
+    }
+  }
+  auto bf_load = [&](int64_t se, int kk, int j) __attribute__((always_inline)) {
+    if (BF) fbr[kk][j] = *reinterpret_cast<const bf16x8_t*>(bf_base[j] + (se * 4 + kk) * kBfBlock);
+  };
 
   // K order: the stages of this item's range [ks0, ks1) are visited rotated by an offset that
   // depends on the XCD (blockIdx.x % 8).  The 32 CUs of an XCD stay in step, so the panels
@@ -580,7 +617,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
   };
   auto read_one = [&](const char* st, int kk, int r, bf16x8_t* a, bf16x8_t* b) __attribute__((always_inline)) {
     if (r == 0) a[0] = frag(st, kk, 0, false);
-    else if (r <= NJ) b[r - 1] = frag(st, kk, r - 1, true);
+    else if (r <= NJ) { if (!BF) b[r - 1] = frag(st, kk, r - 1, true); }
     else a[r - NJ] = frag(st, kk, r - NJ, false);
   };
   auto read_all = [&](const char* st, int kk, bf16x8_t* a, bf16x8_t* b) __attribute__((always_inline)) {
@@ -708,7 +745,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
     // up to the barrier's wait), and stage s+1's (loaded one step earlier) are decoded into
     // buffer nxt in small operations spread over slices 0-2.
     int64_t se1 = 0, se2 = 0;
-    if (BQ != 0) {
+    if (BQ != 0 || BF) {
       se1 = n1 + krot;
       if (se1 >= ks1) se1 -= klen;
       se2 = n2 + krot;
@@ -725,33 +762,65 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
         }
       }
     };
-    auto bq0 = [&](int t) __attribute__((always_inline)) { bq_slot(t); };
+    // Fragment-major B: after MFMA t = 12 + j of slice kk (the last one using fbr[kk][j]), that
+    // register is loaded with stage s+1's fragment (not in the last step).
+    auto bf_hook = [&](int kk, int t) __attribute__((always_inline)) {
+      if (BF && !LAST && t >= 12) bf_load(se1, kk, t - 12);
+    };
+    auto bq0 = [&](int t) __attribute__((always_inline)) {
+      bq_slot(t);
+      bf_hook(0, t);
+    };
     auto bq1 = [&](int t) __attribute__((always_inline)) {
       bq_slot(16 + t);
       at_rd(t);
+      bf_hook(1, t);
     };
-    auto bq2 = [&](int t) __attribute__((always_inline)) { bq_slot(32 + t); };
-    slice(std::true_type{}, std::true_type{}, fa[0], fb[0], cs, 1, fa[1], fb[1], n1, nxt, L0, L1,
-          bq0);
-    slice(std::true_type{}, std::true_type{}, fa[1], fb[1], cs, 2, fa[0], fb[0], n1, nxt, L0 + L1,
-          L2, bq1);
-    slice(std::true_type{}, std::false_type{}, fa[0], fb[0], cs, 3, fa[1], fb[1], 0, 0, 0, 0,
-          bq2);
-    __builtin_amdgcn_s_waitcnt(0);
+    auto bq2 = [&](int t) __attribute__((always_inline)) {
+      bq_slot(32 + t);
+      bf_hook(2, t);
+    };
+    auto bq3 = [&](int t) __attribute__((always_inline)) {
+      at_st(t);
+      bf_hook(3, t);
+    };
+    slice(std::true_type{}, std::true_type{}, fa[0], BF ? fbr[0] : fb[0], cs, 1, fa[1], fb[1], n1,
+          nxt, L0, L1, bq0);
+    slice(std::true_type{}, std::true_type{}, fa[1], BF ? fbr[1 % (BF ? 4 : 1)] : fb[1], cs, 2,
+          fa[0], fb[0], n1, nxt, L0 + L1, L2, bq1);
+    slice(std::true_type{}, std::false_type{}, fa[0], BF ? fbr[2 % (BF ? 4 : 1)] : fb[0], cs, 3,
+          fa[1], fb[1], 0, 0, 0, 0, bq2);
+    if (BF && !LAST) {
+      // A's copies of stage s+1 and everything before them; the 12 B loads issued after them in
+      // slices 0-2 stay in flight (vmcnt(12); expcnt not waited; lgkmcnt(0): this wavefront's
+      // reads of stage s are done before the barrier lets stage s+2's copies overwrite it)
+      __builtin_amdgcn_s_waitcnt(12 | (7 << 4) | (0 << 8));
+    } else {
+      __builtin_amdgcn_s_waitcnt(0);
+    }
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     if (BQ != 0) bq_cur = bq_nxt;               // complete: the wait above covered its loads
-    slice(std::integral_constant<bool, !LAST>{}, std::true_type{}, fa[1], fb[1],
-          smem + nxt * kStage, 0, fa[0], fb[0], n2, cur, 0, L0, at_st);
+    slice(std::integral_constant<bool, !LAST>{}, std::true_type{}, fa[1],
+          BF ? fbr[3 % (BF ? 4 : 1)] : fb[1], smem + nxt * kStage, 0, fa[0], fb[0], n2, cur, 0,
+          L0, bq3);
   };
 
   const int64_t nfull = K / BK;                 // the K tail (dense, second half) follows it
-  // (packed B: K is a multiple of BK, checked on the host)
-  const int64_t krem = (half == 0 || MODE == kGroupK || BQ != 0) ? 0 : K % BK;
+  // (packed or fragment-major B: K is a multiple of BK, checked on the host)
+  const int64_t krem = (half == 0 || MODE == kGroupK || BQ != 0 || BF) ? 0 : K % BK;
   const int64_t s0 = ks0, s1 = ks1;
   if (s1 > s0) {
 #pragma unroll
     for (int q = 0; q < NLD; ++q) dma(s0, 0, q);
+    if (BF) {
+      int64_t se = s0 + krot;
+      if (se >= ks1) se -= klen;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) bf_load(se, kk, j);
+    }
     if (BQ != 0) {
       // stage s0's B decoded now; stage s0+1's registers for the first step
       auto se_of = [&](int64_t st) {
@@ -969,13 +1038,18 @@ size_t gemm_nt_split_bytes(int64_t M, int64_t N) {
   return (size_t)(2 * std::min<int64_t>(tiles, kMaxSplitTiles)) * BM * BN * sizeof(float);
 }
 
-hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
-                          int a_mn, const uint16_t* B, int64_t ldb, int b_mn, void* C,
-                          int64_t ldc, int c_f32, float* part, hipStream_t s, uint16_t* at,
-                          int64_t ldat) {
+namespace {
+
+// Shared launch of the dense NT GEMM: bf = B in the fragment-major layout (a_mn = b_mn = 0,
+// K a multiple of 64).
+hipError_t launch_dense(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda, int a_mn,
+                        const uint16_t* B, int64_t ldb, int b_mn, bool bf, void* C, int64_t ldc,
+                        int c_f32, float* part, hipStream_t s, uint16_t* at, int64_t ldat) {
   // (a stage's 64 rows of A^T, 128 ldat bytes, stay below 2^31: 32-bit store offsets)
   if (at != nullptr && (c_f32 || a_mn || b_mn || M % 8 != 0 || ldat < M || ldat % 4 != 0 ||
                         ldat >= kGemmAtMaxLd || reinterpret_cast<uintptr_t>(at) % 8 != 0))
+    return hipErrorInvalidValue;
+  if (bf && (a_mn || b_mn || K % BK != 0 || reinterpret_cast<uintptr_t>(B) % 16 != 0))
     return hipErrorInvalidValue;
   if (at != nullptr && (N == 0 || (N + BN - 1) / BN < 8)) {
     // no tiles, or fewer than 8 tile columns (a tile would own more than two A^T pieces per
@@ -987,7 +1061,7 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, in
     at = nullptr;
   }
   if (M == 0 || N == 0) return hipSuccess;
-  if (!nt_offsets_fit(K, lda, ldb, a_mn, b_mn)) return hipErrorInvalidValue;
+  if (!nt_offsets_fit(K, lda, bf ? K : ldb, a_mn, b_mn)) return hipErrorInvalidValue;
   NtArgs a{};
   a.A = A; a.B = B; a.C = C; a.lda = lda; a.ldb = ldb; a.ldc = ldc;
   a.M = M; a.N = N; a.K = K;
@@ -1013,7 +1087,11 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, in
   }
   const dim3 grid((unsigned)items);
   const dim3 b8(8 * 64), b4(4 * 64);
-  if (c_f32) {
+  if (bf) {
+    if (c_f32) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, false, false, 4, 0, true>), grid, b4, 0, s, a);
+    else if (at != nullptr) hipLaunchKernelGGL((gemm_nt_kernel<false, kDenseAT, false, false, 4, 0, true>), grid, b4, 0, s, a);
+    else hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, false, false, 4, 0, true>), grid, b4, 0, s, a);
+  } else if (c_f32) {
     if (a_mn && b_mn) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, true, true, 8>), grid, b8, 0, s, a);
     else if (b_mn) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, false, true, 8>), grid, b8, 0, s, a);
     else if (a_mn) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, true, false, 8>), grid, b8, 0, s, a);
@@ -1029,6 +1107,52 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, in
     hipLaunchKernelGGL(split_reduce_kernel, dim3(BM * BN / (256 * 4), (unsigned)rem), dim3(256),
                        0, s, a);
   return hipGetLastError();
+}
+
+// Row-major bf16 B [N, K] (row stride ld) -> fragment-major (kBfBlock): one lane per 16-byte
+// operand; rows past N (to the next multiple of 32) are zeros.
+__global__ __launch_bounds__(256) void frag_pack_kernel(const uint16_t* __restrict__ B, int64_t N,
+                                                        int64_t K, int64_t ld,
+                                                        uint16_t* __restrict__ out,
+                                                        int64_t total) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;   // 16-byte operand index
+  if (i >= total) return;
+  const int64_t blk = i / 64, L = i % 64;
+  const int64_t kblocks = K / 16;
+  const int64_t nb = blk / kblocks, kb = blk % kblocks;
+  const int64_t n = nb * 32 + L % 32, k = kb * 16 + 8 * (L / 32);
+  uint4 v = make_uint4(0, 0, 0, 0);
+  if (n < N) v = *reinterpret_cast<const uint4*>(B + n * ld + k);
+  *reinterpret_cast<uint4*>(out + i * 8) = v;
+}
+
+}  // namespace
+
+size_t gemm_frag_bytes(int64_t N, int64_t K) { return (size_t)((N + 31) / 32) * 32 * K * 2; }
+
+hipError_t launch_frag_pack(const uint16_t* B, int64_t N, int64_t K, int64_t ld, uint16_t* out,
+                            hipStream_t s) {
+  if (N == 0 || K == 0) return hipSuccess;
+  if (K % 16 || ld % 8 || reinterpret_cast<uintptr_t>(B) % 16 || reinterpret_cast<uintptr_t>(out) % 16)
+    return hipErrorInvalidValue;
+  const int64_t total = (N + 31) / 32 * (K / 16) * 64;
+  hipLaunchKernelGGL(frag_pack_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, B,
+                     N, K, ld, out, total);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
+                          int a_mn, const uint16_t* B, int64_t ldb, int b_mn, void* C,
+                          int64_t ldc, int c_f32, float* part, hipStream_t s, uint16_t* at,
+                          int64_t ldat) {
+  return launch_dense(M, N, K, A, lda, a_mn, B, ldb, b_mn, false, C, ldc, c_f32, part, s, at,
+                      ldat);
+}
+
+hipError_t launch_gemm_nt_bf(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
+                             const uint16_t* Bf, void* C, int64_t ldc, int c_f32, float* part,
+                             hipStream_t s, uint16_t* at, int64_t ldat) {
+  return launch_dense(M, N, K, A, lda, 0, Bf, K, 0, true, C, ldc, c_f32, part, s, at, ldat);
 }
 
 hipError_t launch_gemm_nt_packed_b(int64_t M, int64_t N, int64_t K, const uint16_t* A,

@@ -63,6 +63,17 @@ hipError_t launch_gemm_nt(int64_t M, int64_t N, int64_t K, const uint16_t* A, in
                           int a_mn, const uint16_t* B, int64_t ldb, int b_mn, void* C,
                           int64_t ldc, int c_f32, float* part, hipStream_t s,
                           uint16_t* at = nullptr, int64_t ldat = 0);
+// The same product with B [N, K] given in the fragment-major layout the MFMA operands use
+// (launch_frag_pack writes it from a row-major matrix; gemm_frag_bytes(N, K) bytes, rows padded
+// to a multiple of 32 with zeros): B's fragments go from memory straight into registers and only
+// A is staged in LDS.  A k-major; K a multiple of 64; Bf 16-byte aligned.  Results equal
+// launch_gemm_nt's on the row-major B bit for bit.
+hipError_t launch_gemm_nt_bf(int64_t M, int64_t N, int64_t K, const uint16_t* A, int64_t lda,
+                             const uint16_t* Bf, void* C, int64_t ldc, int c_f32, float* part,
+                             hipStream_t s, uint16_t* at = nullptr, int64_t ldat = 0);
+size_t gemm_frag_bytes(int64_t N, int64_t K);
+hipError_t launch_frag_pack(const uint16_t* B, int64_t N, int64_t K, int64_t ld, uint16_t* out,
+                            hipStream_t s);
 // The forward Y[M, N] = A W_hat^T (bf16 C) with W_hat decoded inside the GEMM from the packed
 // weight (bfmt NVFP4 / MXFP4: codes [N][K/2] + scales [N][K/16 | K/32] + NVFP4 tensor decode
 // scale S = g / 2688 at S; Q4K: blocks [N][K/256][144] in `codes`).  K a multiple of 64 (Q4K:
