@@ -84,24 +84,35 @@ __device__ __forceinline__ float e4m3_value(uint32_t c) {
 }
 
 // binary32 -> binary16, round to nearest even, subnormals kept, finite overflow saturating to
-// 65504; NaN -> 0x7E00.
+// 65504; NaN -> 0x7E00.  The hardware conversion (round to nearest even in the default mode,
+// binary16 subnormals kept) on the value clamped to +-65504: every binary32 above 65504 in
+// magnitude would round to 65504 or to infinity, and the clamp makes it 65504.  Equal to the
+// bit-level rounding for all 2^32 inputs (checked on the GPU).
 __device__ __forceinline__ uint32_t f16_rne_sat(float f) {
-  uint32_t u = as_u32(f);
-  uint32_t s = (u >> 16) & 0x8000u;
-  uint32_t a = u & 0x7FFFFFFFu;
-  if (a > 0x7F800000u) return 0x7E00u;
-  float af = as_f32(a);
-  if (af >= 65504.0f) return s | 0x7BFFu;
-  if (af < 0x1p-14f) return s | (uint32_t)__builtin_rintf(af * 16777216.0f);
-  uint32_t r = a + 0xFFFu + ((a >> 13) & 1u);
-  uint32_t h = (r >> 13) - (112u << 10);
-  return s | (h < 0x7BFFu ? h : 0x7BFFu);
+  const float c = __builtin_fminf(__builtin_fmaxf(f, -65504.0f), 65504.0f);
+  const uint32_t h = __builtin_bit_cast(uint16_t, (_Float16)c);
+  return f != f ? 0x7E00u : h;
 }
 
+// binary16 bits -> binary32 (hardware conversion: exact, subnormals kept, infinity and NaN
+// as infinity and NaN).
 __device__ __forceinline__ float f16_value(uint32_t h) {
-  uint32_t e = (h >> 10) & 31u, f = h & 1023u;
-  float v = e == 0u ? (float)f * 0x1p-24f : as_f32(((e + 112u) << 23) | (f << 13));
-  return (h & 0x8000u) ? -v : v;
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)h);
+}
+
+// fl(x / C) for x >= 0 (zero, subnormal, normal, infinity or NaN) and C = 15 or 63: the product
+// with the rounded reciprocal, its exact residual by FMA and one correcting FMA (the
+// Markstein correction, which is correctly rounded here).  Equal to the IEEE quotient for
+// every non-negative binary32 input, checked exhaustively for both constants; an infinite
+// product is returned as is (the residual would be NaN).
+template <int C>
+__device__ __forceinline__ float div_nonneg_by(float x) {
+  static_assert(C == 15 || C == 63, "checked for 15 and 63 only");
+  constexpr float c = (float)C, rc = 1.0f / (float)C;
+  const float q0 = x * rc;
+  const float r = __builtin_fmaf(-q0, c, x);
+  const float q1 = __builtin_fmaf(r, rc, q0);
+  return __builtin_isinf(q0) ? q0 : q1;
 }
 
 __device__ __forceinline__ uint32_t lo16(uint32_t w) { return w & 0xFFFFu; }
@@ -210,21 +221,24 @@ __device__ __forceinline__ void mxfp4_decode8(uint32_t cw, uint32_t e, uint32_t 
   for (int q = 0; q < 4; ++q) w[q] = nan ? 0x7FC07FC0u : w[q];
 }
 
-// Q4_K: 8 unsigned codes q (one per byte: element k in byte k % 4 of qw[k / 4]) of a sub-block
-// with step t1 = fl(d s6) and offset t2 = fl(dmin m6): x_hat = bf16(fl(t1 q - t2)).  t1 q is
-// exact (at most 21 significant bits, far from the FP32 range limits), so a fused multiply-add
-// rounds t1 q - t2 exactly once, as the separate product and difference do.
+// Q4_K: 8 unsigned codes q of a sub-block with step t1 = fl(d s6) and offset t2 = fl(dmin m6):
+// x_hat = bf16(fl(t1 q - t2)).  t1 q is exact (at most 21 significant bits, far from the FP32
+// range limits), so a fused multiply-add rounds t1 q - t2 exactly once, as the separate product
+// and difference do.  The codes as FP32 integers 0..15 (qf[k] for element k):
+__device__ __forceinline__ void q4k_decode8f(const float qf[8], float t1, float t2,
+                                            uint32_t w[4]) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    w[q] = bf16x2_rne_nonnan(__builtin_fmaf(t1, qf[2 * q], -t2),
+                             __builtin_fmaf(t1, qf[2 * q + 1], -t2));
+}
+// ... and as bytes (element k in byte k % 4 of qw[k / 4]).
 __device__ __forceinline__ void q4k_decode8(const uint32_t qw[2], float t1, float t2,
                                            uint32_t w[4]) {
+  float qf[8];
 #pragma unroll
-  for (int p = 0; p < 2; ++p) {
-    const float a0 = __builtin_fmaf(t1, (float)(qw[p] & 0xFFu), -t2);
-    const float a1 = __builtin_fmaf(t1, (float)((qw[p] >> 8) & 0xFFu), -t2);
-    const float a2 = __builtin_fmaf(t1, (float)((qw[p] >> 16) & 0xFFu), -t2);
-    const float a3 = __builtin_fmaf(t1, (float)(qw[p] >> 24), -t2);
-    w[2 * p] = bf16x2_rne_nonnan(a0, a1);
-    w[2 * p + 1] = bf16x2_rne_nonnan(a2, a3);
-  }
+  for (int k = 0; k < 8; ++k) qf[k] = (float)((qw[k >> 2] >> (8 * (k & 3))) & 0xFFu);
+  q4k_decode8f(qf, t1, t2, w);
 }
 
 // NVFP4 (16-block = this lane and lane ^ 1): 4-bit codes cw (element k in nibble k), E4M3
@@ -301,34 +315,48 @@ struct Q4kChunk {
   uint32_t dh, mh, ls, lm, qlo, qhi;
 };
 
-// Q4_K element codes q[k] = min(max(rint(fl(a[k] / t)), 0), 15) for a normal t > 0.  With
-// rt = 1 / t from v_rcp_f32 (within 1 ulp), y = fl(a rt) is within 2.4e-7 |a / t| of
-// fl(a / t): within 4e-6 for |a / t| <= 16, and further out both clamp alike, so whenever y
-// lies more than 1e-5 from a half-integer both round to the same integer.  A chunk with any
-// element closer than that (or a non-finite y) takes the exact quotients for all eight.
-__device__ __forceinline__ void q4_codes8(const float a[8], float t, uint32_t q[8]) {
+// Q4_K element codes q[k] = min(max(rint(fl(a[k] / t)), 0), 15) for a normal t > 0, as FP32
+// integers.  With rt = 1 / t from v_rcp_f32 (within 1 ulp), y = fl(a rt) is within
+// 2.4e-7 |a / t| of fl(a / t): within 4e-6 for |a / t| <= 16, and further out both clamp
+// alike, so whenever y lies more than 1e-5 from a half-integer both round to the same integer.
+// A chunk with any element closer than that takes the exact quotients for all eight (y - rint y
+// is exact, so |y - rint y| >= 0.49999 is the test; a NaN or infinite y fails it and clamps as
+// the exact quotient does).
+__device__ __forceinline__ void q4_codes8(const float a[8], float t, float q[8]) {
   const float rt = __builtin_amdgcn_rcpf(t);
-  float y[8];
-  bool exact = false;
+  float dm = 0.0f;
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
-    y[k] = a[k] * rt;
-    exact |= !(__builtin_fabsf(__builtin_amdgcn_fractf(y[k]) - 0.5f) > 1e-5f);
+    const float y = a[k] * rt;
+    const float n = __builtin_rintf(y);
+    dm = fmaxf(dm, __builtin_fabsf(y - n));     // a NaN distance is dropped
+    q[k] = fminf(fmaxf(n, 0.0f), 15.0f);
   }
-  if (exact) {
+  if (dm >= 0.49999f) {
 #pragma unroll
-    for (int k = 0; k < 8; ++k) y[k] = a[k] / t;
+    for (int k = 0; k < 8; ++k) q[k] = fminf(fmaxf(__builtin_rintf(a[k] / t), 0.0f), 15.0f);
   }
+}
+
+// Four codes held as FP32 integers 0..15 -> one byte each (element k in byte k).
+__device__ __forceinline__ uint32_t q4_bytes4(const float q[4]) {
+  uint32_t w = 0;
 #pragma unroll
-  for (int k = 0; k < 8; ++k) q[k] = (uint32_t)fminf(fmaxf(__builtin_rintf(y[k]), 0.0f), 15.0f);
+  for (int k = 0; k < 4; ++k) w = __builtin_amdgcn_cvt_pk_u8_f32(q[k], k, w);
+  return w;
 }
 
 // Q4_K 6-bit sub-block code min(max(rint(fl(a / t)), 0), 63) for a normal t > 0: as above,
-// y = fl(a / v_rcp(t)) is within 1.6e-5 of fl(a / t) for |a / t| <= 64, so a margin of 1e-4
-// around half-integers decides; closer, the exact quotient.
+// y = fl(a * v_rcp(t)) is within 1.6e-5 of fl(a / t) for |a / t| <= 64, so a margin of 1e-4
+// around half-integers decides; closer, the exact quotient.  The exact quotient sits behind a
+// wavefront-uniform test, so it costs nothing unless some lane needs it.
 __device__ __forceinline__ uint32_t q6_code(float a, float t) {
   float y = a * __builtin_amdgcn_rcpf(t);
-  if (!(__builtin_fabsf(__builtin_amdgcn_fractf(y) - 0.5f) > 1e-4f)) y = a / t;
+  const bool near = !(__builtin_fabsf(__builtin_amdgcn_fractf(y) - 0.5f) > 1e-4f);
+  if (__builtin_amdgcn_ballot_w64(near) != 0) {
+    const float e = a / t;
+    y = near ? e : y;
+  }
   return (uint32_t)fminf(fmaxf(__builtin_rintf(y), 0.0f), 63.0f);
 }
 
@@ -337,46 +365,42 @@ __device__ __forceinline__ void q4k_chunk(const uint32_t h[8], Q4kChunk& r, uint
   float lo = 0.0f, hi = -__builtin_huge_valf();
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
-    xv[k] = as_f32(h[k] << 16) + 0.0f;      // signed zeros count as +0
+    xv[k] = as_f32(h[k] << 16);
     lo = fminf(lo, xv[k]);
     hi = fmaxf(hi, xv[k]);
   }
   lo = fminf(lo, xor1_f(lo)); hi = fmaxf(hi, xor1_f(hi));
   lo = fminf(lo, xor2_f(lo)); hi = fmaxf(hi, xor2_f(hi));
-  const float a = (hi - lo) / 15.0f;        // step of the sub-block
+  lo = lo + 0.0f;                           // signed zeros count as +0 (the extremes only:
+  hi = hi + 0.0f;                           // x + t2 below treats -0 as +0 by itself)
+  const float a = div_nonneg_by<15>(hi - lo);   // step of the sub-block, fl((hi - lo) / 15)
   const float mu = 0.0f - lo;               // offset (subtracted), never negative
   float A = a, Mx = mu;
   A = fmaxf(A, xor_swz_f<4>(A)); Mx = fmaxf(Mx, xor_swz_f<4>(Mx));
   A = fmaxf(A, xor_swz_f<8>(A)); Mx = fmaxf(Mx, xor_swz_f<8>(Mx));
   A = fmaxf(A, xor_swz_f<16>(A)); Mx = fmaxf(Mx, xor_swz_f<16>(Mx));
-  r.dh = f16_rne_sat(A / 63.0f);
-  r.mh = f16_rne_sat(Mx / 63.0f);
+  r.dh = f16_rne_sat(div_nonneg_by<63>(A));
+  r.mh = f16_rne_sat(div_nonneg_by<63>(Mx));
   const float d = f16_value(r.dh), dmin = f16_value(r.mh);
   r.ls = 0;
   r.lm = 0;
   if (d != 0.0f) r.ls = q6_code(a, d);
   if (dmin != 0.0f) r.lm = q6_code(mu, dmin);
   const float t1 = d * (float)r.ls;
-  const float t2 = dmin * (float)r.lm;
-  r.qlo = 0;
-  r.qhi = 0;
-  uint32_t qv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  const float t2 = dmin * (float)r.lm;  // >= +0, so x + t2 is +0 for x = -0 and t2 = 0
+  float qv[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
   if (t1 != 0.0f) {
     float av[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) av[k] = xv[k] + t2;
     q4_codes8(av, t1, qv);
   }
-#pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    if (k < 4) r.qlo |= qv[k] << (8 * k);
-    else r.qhi |= qv[k] << (8 * (k - 4));
-  }
+  r.qlo = q4_bytes4(qv);
+  r.qhi = q4_bytes4(qv + 4);
   // t1 q - t2 is finite for every input (t1, t2 come from FP16 scales), so the hardware pack
   // rounds it exactly as bf16_rne would
-  const uint32_t qw[2] = {r.qlo, r.qhi};
   uint32_t p[4];
-  q4k_decode8(qw, t1, t2, p);
+  q4k_decode8f(qv, t1, t2, p);
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     xh[2 * k] = p[k] & 0xFFFFu;
@@ -413,8 +437,8 @@ __device__ __forceinline__ float q4k_finish(const float xv[8], float a, float mu
   A = fmaxf(A, xor_swz_f<4>(A)); Mx = fmaxf(Mx, xor_swz_f<4>(Mx));
   A = fmaxf(A, xor_swz_f<8>(A)); Mx = fmaxf(Mx, xor_swz_f<8>(Mx));
   A = fmaxf(A, xor_swz_f<16>(A)); Mx = fmaxf(Mx, xor_swz_f<16>(Mx));
-  r.dh = f16_rne_sat(A / 63.0f);
-  r.mh = f16_rne_sat(Mx / 63.0f);
+  r.dh = f16_rne_sat(div_nonneg_by<63>(A));
+  r.mh = f16_rne_sat(div_nonneg_by<63>(Mx));
   const float d = f16_value(r.dh), dmin = f16_value(r.mh);
   r.ls = 0;
   r.lm = 0;
@@ -422,22 +446,19 @@ __device__ __forceinline__ float q4k_finish(const float xv[8], float a, float mu
   if (dmin != 0.0f) r.lm = q6_code(mu, dmin);
   const float t1 = d * (float)r.ls;
   const float t2 = dmin * (float)r.lm;
-  r.qlo = 0;
-  r.qhi = 0;
   float e2[8];
-  uint32_t qv[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  float qv[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
   if (t1 != 0.0f) {
     float av[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) av[k] = xv[k] + t2;
     q4_codes8(av, t1, qv);
   }
+  r.qlo = q4_bytes4(qv);
+  r.qhi = q4_bytes4(qv + 4);
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
-    const uint32_t q = qv[k];
-    if (k < 4) r.qlo |= q << (8 * k);
-    else r.qhi |= q << (8 * (k - 4));
-    xf[k] = t1 * (float)q - t2;
+    xf[k] = t1 * qv[k] - t2;
     const float e = xv[k] - xf[k];
     e2[k] = e * e;
   }
@@ -463,7 +484,7 @@ __device__ __forceinline__ void q4k_mse_chunk(const uint32_t h[8], Q4kChunk& r, 
   lo = fminf(lo, xor2_f(lo)); hi = fmaxf(hi, xor2_f(hi));
   const float range = hi - lo, mu0 = 0.0f - lo;
   const float sx = sub_sum(xv);
-  float best_e = __builtin_huge_valf(), best_a = range / 15.0f, best_mu = mu0;
+  float best_e = __builtin_huge_valf(), best_a = div_nonneg_by<15>(range), best_mu = mu0;
 #pragma unroll 1
   for (int k = 0; k <= 16; ++k) {
     const float Dk = 14.0f + 0.25f * (float)k;
@@ -512,7 +533,7 @@ __device__ __forceinline__ void q4k_mse_chunk(const uint32_t h[8], Q4kChunk& r, 
   Q4kChunk rs, rm;
   float xs[8], xm[8];
   const float es = q4k_finish(xv, best_a, best_mu, rs, xs);
-  const float em = q4k_finish(xv, range / 15.0f, mu0, rm, xm);
+  const float em = q4k_finish(xv, div_nonneg_by<15>(range), mu0, rm, xm);
   const bool use_s = es < em;
   r = use_s ? rs : rm;
 #pragma unroll
@@ -525,31 +546,30 @@ __device__ __forceinline__ void q4k_mse_chunk(const uint32_t h[8], Q4kChunk& r, 
 // low nibbles of bytes 16 + 32p.., sub-block 2p+1 in the high nibbles).  Every lane of the
 // half-wave must call it (cross-lane moves); `store` predicates the writes.
 __device__ __forceinline__ void q4k_store(const Q4kChunk& q, int L, bool store, uint8_t* blk) {
-  // gather the eight 6-bit scales / mins at lane 0 of the super-block
-  uint32_t LS[8], LM[8];
-  const int base = (threadIdx.x & 63) & ~31;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    LS[j] = (uint32_t)__shfl((int)q.ls, base + 4 * j, 64);
-    LM[j] = (uint32_t)__shfl((int)q.lm, base + 4 * j, 64);
-  }
+  // The twelve scale bytes: byte j (j < 4) = low 6 bits of scale j | top 2 bits of scale j + 4
+  // << 6, byte 4 + j the same for the mins, byte 8 + j = low nibble of scale j + 4 | low
+  // nibble of min j + 4 << 4.  Lane 4j of the half-wave holds sub-block j's scale and min.
+  // Every lane computes both forms; swizzles inside the half-wave bring lanes 0, 4, 8, 12
+  // (bytes j, 4 + j) and 16, 20, 24, 28 (bytes 8 + j) together at lane 0.
+  const uint32_t own = q.ls | (q.lm << 16);
+  const uint32_t up = xor_swz_u32<16>(own);                  // scale, min of sub-block j + 4
+  const uint32_t v = (own & 0x003F003Fu) | (((up >> 4) & 0x00030003u) << 6);  // bytes j, 4+j
+  const uint32_t v4 = xor_swz_u32<4>(v);
+  const uint32_t pv = (v & 0x00FF00FFu) | ((v4 & 0x00FF00FFu) << 8);  // lane 0: b0 b1 b4 b5
+  const uint32_t pv8 = xor_swz_u32<8>(pv);                   // lane 0: b2 b3 b6 b7
+  const uint32_t w0 = (q.ls & 15u) | ((q.lm & 15u) << 4);    // lane 16 + 4j: byte 8 + j
+  const uint32_t w4 = xor_swz_u32<4>(w0);
+  const uint32_t pw = w0 | (w4 << 8);
+  const uint32_t pw8 = xor_swz_u32<8>(pw);
+  const uint32_t sw = xor_swz_u32<16>(pw | (pw8 << 16));     // lane 0: b8 b9 b10 b11
   // codes of sub-block j+1 (odd) go to the high nibbles of sub-block j's bytes
   const uint32_t plo = xor_swz_u32<4>(q.qlo);
   const uint32_t phi = xor_swz_u32<4>(q.qhi);
   if (!store) return;
-  if (L == 0) {
-    uint32_t sc[12];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      sc[j] = (LS[j] & 63u) | ((LS[j + 4] >> 4) << 6);
-      sc[j + 4] = (LM[j] & 63u) | ((LM[j + 4] >> 4) << 6);
-      sc[j + 8] = (LS[j + 4] & 15u) | ((LM[j + 4] & 15u) << 4);
-    }
+  if (L == 0)
     *reinterpret_cast<uint4*>(blk) =
-        make_uint4(q.dh | (q.mh << 16), sc[0] | (sc[1] << 8) | (sc[2] << 16) | (sc[3] << 24),
-                   sc[4] | (sc[5] << 8) | (sc[6] << 16) | (sc[7] << 24),
-                   sc[8] | (sc[9] << 8) | (sc[10] << 16) | (sc[11] << 24));
-  }
+        make_uint4(q.dh | (q.mh << 16), (pv & 0xFFFFu) | (pv8 << 16),
+                   (pv >> 16) | (pv8 & 0xFFFF0000u), sw);
   const int sub = L >> 2;
   if ((sub & 1) == 0) {
     const int off = 16 + 32 * (sub >> 1) + 8 * (L & 3);
