@@ -95,8 +95,7 @@ qf_status fakequant_to(int fmt, const uint16_t* x, int64_t R, int64_t K, int64_t
     case QF_FMT_NVFP4: {
       const float* g = g_given;
       if (!g) {
-        QF_TRY(dev(qf::launch_fill_f32(g_scratch, 1, 0.0f, s), "amax init"));
-        QF_TRY(dev(qf::launch_amax(x, R, K, ldx, g_scratch, s), "amax"));
+        QF_TRY(dev(qf::launch_amax(x, R, K, ldx, g_scratch, false, s), "amax"));
         g = g_scratch;
       }
       return dev(qf::launch_nvfp4(x, R, K, ldx, g, nullptr, nullptr, nullptr, out, s), "nvfp4");
@@ -273,8 +272,7 @@ qf_status quantize_packed(int fmt, const uint16_t* x, int64_t R, int64_t K, int6
     case QF_FMT_NVFP4: {
       const float* g = g_given;
       if (!g) {
-        QF_TRY(dev(qf::launch_fill_f32(g_scratch, 1, 0.0f, s), "amax init"));
-        QF_TRY(dev(qf::launch_amax(x, R, K, ldx, g_scratch, s), "amax"));
+        QF_TRY(dev(qf::launch_amax(x, R, K, ldx, g_scratch, false, s), "amax"));
         g = g_scratch;
       }
       return dev(qf::launch_nvfp4(x, R, K, ldx, g, pk.S, pk.codes, pk.scales, xhat, s), "nvfp4");
@@ -344,8 +342,7 @@ qf_status qf_amax(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, float* a
   QF_TRY(check_mat("qf_amax: x", x, R, K, ldx, true));
   if (!amax) return fail(QF_EINVAL, "qf_amax: null amax");
   if (accumulate != 0 && accumulate != 1) return fail(QF_EINVAL, "qf_amax: accumulate must be 0/1");
-  if (!accumulate) QF_TRY(dev(qf::launch_fill_f32(amax, 1, 0.0f, S(stream)), "amax init"));
-  QF_TRY(dev(qf::launch_amax(x, R, K, ldx, amax, S(stream)), "amax"));
+  QF_TRY(dev(qf::launch_amax(x, R, K, ldx, amax, accumulate != 0, S(stream)), "amax"));
   return ok();
 }
 
@@ -362,8 +359,7 @@ qf_status qf_fakequant_nvfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ld
   QF_TRY(check_out("qf_fakequant_nvfp4: xhat", xhat));
   hipStream_t s = S(stream);
   if (amax_mode == QF_AMAX_COMPUTE) {
-    QF_TRY(dev(qf::launch_fill_f32(amax, 1, 0.0f, s), "amax init"));
-    QF_TRY(dev(qf::launch_amax(x, R, K, ldx, amax, s), "amax"));
+    QF_TRY(dev(qf::launch_amax(x, R, K, ldx, amax, false, s), "amax"));
   }
   if (R == 0 || K == 0) {
     if (s_out) QF_TRY(dev(qf::launch_fill_f32(s_out, 1, 0.0f, s), "S"));
@@ -562,8 +558,7 @@ qf_status qf_qlinear_bwd_ste(const qf_qlinear_desc* d, const uint16_t* dY, const
         } else {
           const float* g = d->w_amax;
           if (d->wfmt == QF_FMT_NVFP4 && !g) {
-            QF_TRY(dev(qf::launch_fill_f32(w.scal, 1, 0.0f, s), "amax init"));
-            QF_TRY(dev(qf::launch_amax(W, d->N, d->K, dm.ldw, w.scal, s), "amax"));
+            QF_TRY(dev(qf::launch_amax(W, d->N, d->K, dm.ldw, w.scal, false, s), "amax"));
             g = w.scal;
           }
           QF_TRY(dev(qf::launch_quant_t(d->wfmt, W, d->N, d->K, dm.ldw, 1, 0, g, w.whatt, d->N, 0,
@@ -690,8 +685,7 @@ qf_status grouped_quantize(const qf_grouped_desc* d, const uint16_t* X, const ui
         case QF_FMT_NVFP4: {
           const float* gp = d->w_amax;
           if (!gp) {
-            QF_TRY(dev(qf::launch_fill_f32(g.wamax, d->E, 0.0f, s), "amax init"));
-            QF_TRY(dev(qf::launch_amax_batched(W, d->E, R, K, g.wamax, s), "amax"));
+            QF_TRY(dev(qf::launch_amax_batched(W, d->E, R, K, g.wamax, false, s), "amax"));
             gp = g.wamax;
           }
           QF_TRY(dev(qf::launch_nvfp4_batched(W, d->E, R, K, gp, g.what, s), "nvfp4"));
@@ -775,8 +769,7 @@ qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int64_t* gr
     if (fuse_w) {
       const float* gp = d->w_amax;
       if (d->wfmt == QF_FMT_NVFP4 && !gp) {
-        QF_TRY(dev(qf::launch_fill_f32(g.wamax, d->E, 0.0f, s), "amax init"));
-        QF_TRY(dev(qf::launch_amax_batched(W, d->E, d->N, d->K, g.wamax, s), "amax"));
+        QF_TRY(dev(qf::launch_amax_batched(W, d->E, d->N, d->K, g.wamax, false, s), "amax"));
         gp = g.wamax;
       }
       QF_TRY(dev(qf::launch_quant_t(d->wfmt, W, d->N, d->K, d->K, d->E, d->N * d->K, gp, g.whatt,
@@ -980,8 +973,7 @@ qf_status lora_quant_via_merged(const qf_qlinear_desc* d, const qf::LoraOperand&
   QF_TRY(dev(qf::launch_lora_quant(QF_FMT_NONE, L, W, N, K, ldw, 1, 0, nullptr, nullptr, nullptr,
                                    nullptr, nullptr, tmp, s),
              "merge"));
-  QF_TRY(dev(qf::launch_fill_f32(scratch, 1, 0.0f, s), "amax init"));
-  QF_TRY(dev(qf::launch_amax(tmp, N, K, K, scratch, s), "amax of the merged weight"));
+  QF_TRY(dev(qf::launch_amax(tmp, N, K, K, scratch, false, s), "amax of the merged weight"));
   if (transposed)
     QF_TRY(dev(qf::launch_quant_t(QF_FMT_NVFP4, tmp, N, K, K, 1, 0, scratch, out, N, 0, s),
                "quantize merged weight (transposed)"));
@@ -1265,8 +1257,7 @@ qf_status glora_quant_via_merged(const qf_grouped_desc* d, const qf::LoraOperand
   QF_TRY(dev(qf::launch_lora_quant(QF_FMT_NONE, L, W, N, K, K, E, N * K, nullptr, nullptr,
                                    nullptr, nullptr, nullptr, tmp, s),
              "merge (experts)"));
-  QF_TRY(dev(qf::launch_fill_f32(scratch, E, 0.0f, s), "amax init"));
-  QF_TRY(dev(qf::launch_amax_batched(tmp, E, N, K, scratch, s), "amax of the merged experts"));
+  QF_TRY(dev(qf::launch_amax_batched(tmp, E, N, K, scratch, false, s), "amax of the merged experts"));
   if (transposed)
     QF_TRY(dev(qf::launch_quant_t(QF_FMT_NVFP4, tmp, N, K, K, E, N * K, scratch, out, N, N * K, s),
                "quantize merged experts (transposed)"));
@@ -1475,9 +1466,9 @@ qf_status qf_export_fused(int fmt, const qf_member* members, int n, int64_t K, u
   if (fmt == QF_FMT_NVFP4) {
     if (!w_amax) return fail(QF_EINVAL, "%s: NVFP4 needs w_amax", fn);
     if (input_scale && !a_amax) return fail(QF_EINVAL, "%s: input_scale needs a_amax", fn);
-    QF_TRY(dev(qf::launch_fill_f32(w_amax, 1, 0.0f, s), "amax init"));
-    for (int i = 0; i < n; ++i)
-      QF_TRY(dev(qf::launch_amax(members[i].W, members[i].rows, K, members[i].ldw, w_amax, s),
+    for (int i = 0; i < n; ++i)       // the first member sets g, the others fold into it
+      QF_TRY(dev(qf::launch_amax(members[i].W, members[i].rows, K, members[i].ldw, w_amax,
+                                 i > 0, s),
                  "tied amax"));
     int64_t r0 = 0;
     for (int i = 0; i < n; ++i) {

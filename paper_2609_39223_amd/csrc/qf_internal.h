@@ -10,8 +10,10 @@ namespace qf {
 // ---- quantizers (qf_quant.hip) ----------------------------------------------------------
 // Writes v to p[0..n) with a kernel (no memset nodes, so callers may capture it in a graph).
 hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s);
+// Tensor amax into *amax (accumulate: max(*amax, amax), compared as bits); one dispatch, no
+// clearing kernel before it (an empty tensor: a one-element fill unless accumulating).
 hipError_t launch_amax(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, float* amax,
-                       hipStream_t s);
+                       bool accumulate, hipStream_t s);
 // g: device scalar holding the tensor amax to use; s_out may be null.
 hipError_t launch_nvfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, const float* g,
                         float* s_out, uint8_t* codes, uint8_t* scales, uint16_t* xhat,
@@ -26,7 +28,7 @@ hipError_t launch_q4k_mse(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, 
 
 // Batched variants over E equally shaped tensors (expert weights), one tensor scale each.
 hipError_t launch_amax_batched(const uint16_t* x, int64_t E, int64_t R, int64_t K,
-                               float* amax, hipStream_t s);
+                               float* amax, bool accumulate, hipStream_t s);
 hipError_t launch_nvfp4_batched(const uint16_t* x, int64_t E, int64_t R, int64_t K,
                                 const float* g, uint16_t* xhat, hipStream_t s);
 

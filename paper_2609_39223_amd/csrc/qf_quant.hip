@@ -15,6 +15,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 #include "qf.h"
 #include "qf_codecs.h"
 #include "qf_internal.h"
@@ -32,18 +34,112 @@ __global__ void fill_f32_kernel(float* p, int64_t n, float v) {
   if (i < n) p[i] = v;
 }
 
-// max |x| as bf16 magnitude bits (NaN bit patterns sort above +inf), folded into *amax as the
-// binary32 pattern with an integer atomic max (order independent, so the result is exact and
-// deterministic).  grid.z indexes equally shaped tensors when batched (stride R*K elements).
-// A lane issues kAmaxRows 16-byte loads before it reduces them (a pass covers one row chunk of
-// kAmaxRows rows; the grid is sized for about one pass per lane), and a workgroup skips its
-// atomic when a relaxed read already shows a value at least as large (amax only grows).
+// ---- tensor amax --------------------------------------------------------------------------
+// max |x| as bf16 magnitude bits (NaN bit patterns sort above +inf), reduced per workgroup and
+// folded into a reduction slot with an integer atomic max (order independent, so the result is
+// exact and deterministic).  Each 64-bit slot holds the running maximum (binary32 bits) and a
+// ticket count of the workgroups that have folded theirs in; the workgroup that takes the last ticket
+// writes the result (*amax = m, or max(*amax, m) when accumulating, compared as bits) and
+// returns the slot to zero.  Slots start at zero when the library loads, so no pass needs a
+// clearing dispatch.  The host hands each pass its own slot (one per tensor of a batch) from a
+// ring of kAmaxSlots, so passes running concurrently on different streams do not share one
+// unless kAmaxSlots slots are taken in between.
+constexpr uint32_t kAmaxSlots = 4096;
+// low word: the running maximum (binary32 bits); high word: the ticket count
+__device__ uint64_t g_amax_slot[kAmaxSlots];
+
+// Called by thread 0 of every workgroup of a pass with the workgroup's maximum b.
+__device__ __forceinline__ void amax_fold(uint32_t b, uint32_t slot, uint32_t nblocks,
+                                          float* amax, int accumulate) {
+  uint64_t* sl = &g_amax_slot[slot % kAmaxSlots];
+  const uint32_t v = b << 16;
+  // Device-scope atomics are performed at the device's coherence point.  The fold is
+  // acknowledged before the ticket is taken (the wait), so every fold precedes the last ticket,
+  // and the ticket's returned word carries the maximum of all of them; no cache write-back is
+  // needed for that (a release ordering would write back this XCD's L2 in every workgroup).
+  if (v != 0u)
+    __hip_atomic_fetch_max(reinterpret_cast<uint32_t*>(sl), v, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+  __builtin_amdgcn_s_waitcnt(0x0F70);            // vmcnt(0): the fold is acknowledged
+  const uint64_t old =
+      __hip_atomic_fetch_add(sl, 1ull << 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if ((uint32_t)(old >> 32) != nblocks - 1) return;
+  const uint32_t m = (uint32_t)old;
+  uint32_t* out = reinterpret_cast<uint32_t*>(amax);
+  const uint32_t prev = accumulate ? *out : 0u;
+  *out = prev > m ? prev : m;
+  __hip_atomic_store(sl, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Block-wide maximum of m, then the fold by thread 0.
+__device__ __forceinline__ void amax_block_fold(uint32_t m, uint32_t slot, uint32_t nblocks,
+                                                float* amax, int accumulate) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const uint32_t o = (uint32_t)__shfl_xor((int)m, off, 64);
+    m = o > m ? o : m;
+  }
+  __shared__ uint32_t wmax[kThreads / 64];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  if (lane == 0) wmax[wid] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t b = wmax[0];
+    for (int i = 1; i < kThreads / 64; ++i) b = wmax[i] > b ? wmax[i] : b;
+    amax_fold(b, slot, nblocks, amax, accumulate);
+  }
+}
+
+// max |x| over the eight bf16 of a 16-byte chunk, as magnitude bits
+__device__ __forceinline__ uint32_t max_abs_chunk(const uint4& v) {
+  const uint32_t w[4] = {v.x & 0x7FFF7FFFu, v.y & 0x7FFF7FFFu, v.z & 0x7FFF7FFFu,
+                         v.w & 0x7FFF7FFFu};
+  uint32_t m = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t a = w[q] & 0xFFFFu, b = w[q] >> 16;
+    m = a > m ? a : m;
+    m = b > m ? b : m;
+  }
+  return m;
+}
+
+// Contiguous tensors (n 16-byte chunks each, tensor z at chunk z * n): a grid-stride loop with
+// kAmaxFlatLoads loads in flight per lane; about one workgroup per CU over all tensors.
+constexpr int kAmaxFlatLoads = 8;
+__global__ __launch_bounds__(kThreads) void amax_flat_kernel(const uint4* __restrict__ x,
+                                                             int64_t n, uint32_t slot0,
+                                                             float* __restrict__ amax,
+                                                             int accumulate) {
+  const uint4* xt = x + (int64_t)blockIdx.z * n;
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  uint32_t m = 0;
+  for (int64_t base = (int64_t)blockIdx.x * kThreads + threadIdx.x; base < n;
+       base += stride * kAmaxFlatLoads) {
+    uint4 v[kAmaxFlatLoads];
+#pragma unroll
+    for (int j = 0; j < kAmaxFlatLoads; ++j) {
+      const int64_t i = base + j * stride;
+      v[j] = i < n ? xt[i] : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < kAmaxFlatLoads; ++j) {
+      const uint32_t a = max_abs_chunk(v[j]);
+      m = a > m ? a : m;
+    }
+  }
+  amax_block_fold(m, slot0 + blockIdx.z, gridDim.x, amax + blockIdx.z, accumulate);
+}
+
+// Strided rows or a row length that is not a multiple of 8: chunks along K (a last partial
+// chunk holds K % 8 elements), kAmaxRows rows per lane pass (all loads issued before the
+// reduction); the grid is sized for about one pass per lane.
 constexpr int kAmaxRows = 16;
-__global__ __launch_bounds__(kThreads) void amax_kernel(const uint16_t* __restrict__ x, int64_t R,
-                                                        int64_t K, int64_t ldx, int64_t tstride,
-                                                        float* __restrict__ amax) {
-  const int64_t chunks = (K + 7) >> 3;           // a last partial chunk holds K % 8 elements
-  const uint16_t* xt = x + (int64_t)blockIdx.z * tstride;
+__global__ __launch_bounds__(kThreads) void amax_rows_kernel(const uint16_t* __restrict__ x,
+                                                             int64_t R, int64_t K, int64_t ldx,
+                                                             uint32_t slot, float* __restrict__ amax,
+                                                             int accumulate) {
+  const int64_t chunks = (K + 7) >> 3;
   uint32_t m = 0;
   for (int64_t c = (int64_t)blockIdx.x * kThreads + threadIdx.x; c < chunks;
        c += (int64_t)gridDim.x * kThreads) {
@@ -55,7 +151,7 @@ __global__ __launch_bounds__(kThreads) void amax_kernel(const uint16_t* __restri
       for (int i = 0; i < kAmaxRows; ++i) {
         v[i] = make_uint4(0, 0, 0, 0);
         if (r0 + i < R) {
-          const uint16_t* src = xt + (r0 + i) * ldx + c * 8;
+          const uint16_t* src = x + (r0 + i) * ldx + c * 8;
           if (whole) {
             v[i] = *reinterpret_cast<const uint4*>(src);
           } else {                                  // the row's last K % 8 elements only
@@ -67,30 +163,12 @@ __global__ __launch_bounds__(kThreads) void amax_kernel(const uint16_t* __restri
       }
 #pragma unroll
       for (int i = 0; i < kAmaxRows; ++i) {
-        uint32_t h[8];
-        unpack8(v[i], h);
-        const uint32_t a = max_abs_bits8(h);
+        const uint32_t a = max_abs_chunk(v[i]);
         m = a > m ? a : m;
       }
     }
   }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    uint32_t o = (uint32_t)__shfl_xor((int)m, off, 64);
-    m = o > m ? o : m;
-  }
-  __shared__ uint32_t wmax[kThreads / 64];
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  if (lane == 0) wmax[wid] = m;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t b = wmax[0];
-    for (int i = 1; i < kThreads / 64; ++i) b = wmax[i] > b ? wmax[i] : b;
-    unsigned int* dst = reinterpret_cast<unsigned int*>(amax + blockIdx.z);
-    if (b != 0u &&
-        __hip_atomic_load(dst, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < (b << 16))
-      atomicMax(dst, b << 16);
-  }
+  amax_block_fold(m, slot, gridDim.x * gridDim.y, amax, accumulate);
 }
 
 // ============================================================================= NVFP4
@@ -352,26 +430,11 @@ hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Grid of amax_kernel: up to 64 x 256 chunks per row pass and kAmaxRows rows per lane pass,
-// at most ~2048 workgroups over all E tensors (so most lanes make one or a few passes).
-static dim3 amax_grid(int64_t R, int64_t K, int64_t E) {
-  const int64_t chunks = (K + 7) >> 3;
-  int64_t gx = (chunks + kThreads - 1) / kThreads;
-  if (gx > 64) gx = 64;
-  int64_t gy = (R + kAmaxRows - 1) / kAmaxRows;
-  int64_t cap = 2048 / (gx * E);
-  if (cap < 1) cap = 1;
-  if (gy > cap) gy = cap;
-  if (gy < 1) gy = 1;
-  return dim3((unsigned)gx, (unsigned)gy, (unsigned)E);
-}
-
 // A contiguous tensor whose rows do not fill the workgroups' lanes (K / 8 chunks not a
 // multiple of kThreads) is read as rows of 8 kThreads elements when its size allows (expert
 // weights 3072 x 3072 and 3072 x 1536: a quarter of the lanes would idle).  Valid wherever
-// the result does not depend on where rows break: the amax (a max over all elements), and the
-// batched NVFP4 x_hat (16-element blocks along rows of a multiple of 16, one scale per
-// tensor).
+// the result does not depend on where rows break: the batched NVFP4 x_hat (16-element blocks
+// along rows of a multiple of 16, one scale per tensor).
 static void contiguous_row_view(int64_t& R, int64_t& K) {
   const int64_t row = 8 * kThreads;
   if ((K >> 3) % kThreads != 0 && (R * K) % row == 0) {
@@ -380,24 +443,55 @@ static void contiguous_row_view(int64_t& R, int64_t& K) {
   }
 }
 
+// The next `count` reduction slots of the ring (one per tensor of a pass).
+static uint32_t take_amax_slots(uint32_t count) {
+  static std::atomic<uint32_t> next{0};
+  return next.fetch_add(count, std::memory_order_relaxed) % kAmaxSlots;
+}
+
+// About one workgroup per CU over all E tensors, none idle.
+static unsigned amax_flat_grid(int64_t n, int64_t E) {
+  int64_t gx = 256 / E;
+  if (gx < 1) gx = 1;
+  const int64_t need = (n + kThreads * kAmaxFlatLoads - 1) / (kThreads * kAmaxFlatLoads);
+  if (gx > need) gx = need;
+  return (unsigned)(gx < 1 ? 1 : gx);
+}
+
 hipError_t launch_amax(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, float* amax,
-                       hipStream_t s) {
-  if (R == 0 || K == 0) return hipSuccess;
-  if (ldx == K) {
-    contiguous_row_view(R, K);
-    ldx = K;
+                       bool accumulate, hipStream_t s) {
+  if (R == 0 || K == 0)
+    return accumulate ? hipSuccess : launch_fill_f32(amax, 1, 0.0f, s);
+  const uint32_t slot = take_amax_slots(1);
+  if (ldx == K && K % 8 == 0) {
+    const int64_t n = R * K / 8;
+    hipLaunchKernelGGL(amax_flat_kernel, dim3(amax_flat_grid(n, 1)), dim3(kThreads), 0, s,
+                       reinterpret_cast<const uint4*>(x), n, slot, amax, (int)accumulate);
+  } else {
+    const int64_t chunks = (K + 7) >> 3;
+    int64_t gx = (chunks + kThreads - 1) / kThreads;
+    if (gx > 64) gx = 64;
+    int64_t gy = (R + kAmaxRows - 1) / kAmaxRows;
+    const int64_t cap = 2048 / gx;
+    if (gy > cap) gy = cap;
+    if (gy < 1) gy = 1;
+    hipLaunchKernelGGL(amax_rows_kernel, dim3((unsigned)gx, (unsigned)gy), dim3(kThreads), 0, s,
+                       x, R, K, ldx, slot, amax, (int)accumulate);
   }
-  hipLaunchKernelGGL(amax_kernel, amax_grid(R, K, 1), dim3(kThreads), 0, s, x, R, K, ldx,
-                     (int64_t)0, amax);
   return hipGetLastError();
 }
 
 hipError_t launch_amax_batched(const uint16_t* x, int64_t E, int64_t R, int64_t K, float* amax,
-                               hipStream_t s) {
-  if (E == 0 || R == 0 || K == 0) return hipSuccess;
-  contiguous_row_view(R, K);                     // tensors are contiguous, R * K apart
-  hipLaunchKernelGGL(amax_kernel, amax_grid(R, K, E), dim3(kThreads), 0, s, x, R, K, K, R * K,
-                     amax);
+                               bool accumulate, hipStream_t s) {
+  if (E == 0) return hipSuccess;
+  if (R == 0 || K == 0)
+    return accumulate ? hipSuccess : launch_fill_f32(amax, E, 0.0f, s);
+  // tensors are contiguous, R * K apart; R * K is a multiple of 8 for the block formats
+  const int64_t n = R * K / 8;
+  const uint32_t slot0 = take_amax_slots((uint32_t)E);
+  hipLaunchKernelGGL(amax_flat_kernel, dim3(amax_flat_grid(n, E), 1, (unsigned)E),
+                     dim3(kThreads), 0, s, reinterpret_cast<const uint4*>(x), n, slot0, amax,
+                     (int)accumulate);
   return hipGetLastError();
 }
 

@@ -264,6 +264,51 @@ def test_amax_and_running_accumulate(qf):
     assert float(out.item()) == max(oracle.amax(a), oracle.amax(b))
 
 
+def test_amax_passes_do_not_see_each_other(qf):
+    """Each amax pass folds into a reduction slot that its last workgroup clears: a pass over a
+    small tensor right after one over a large tensor returns the small amax (no carry-over, no
+    clearing dispatch), whatever the output held before; contiguous (flat) and strided (rows)
+    tensors, a zero tensor, a NaN, and more passes than the slot ring holds."""
+    rng = np.random.default_rng(11)
+    big = wide_range_bf16(rng, (300, 1024), lo_exp=-3, hi_exp=12)
+    small = wide_range_bf16(rng, (64, 4096), lo_exp=-8, hi_exp=-2)
+    strided = wide_range_bf16(rng, (37, 520), lo_exp=-6, hi_exp=0)
+    zero = np.zeros((16, 256), np.uint16)
+    nan = small.copy()
+    nan[5, 7] = 0x7FC1
+    dev = {k: to_dev(v) for k, v in dict(big=big, small=small, zero=zero, nan=nan).items()}
+    sd = to_dev(np.pad(strided, ((0, 0), (0, 8))))[:, :520]
+    want = {"big": oracle.amax(big), "small": oracle.amax(small), "zero": 0.0,
+            "strided": oracle.amax(strided)}
+    out = torch.full((1,), 1e30, dtype=torch.float32, device="cuda")
+    order = ["big", "small", "strided", "big", "zero", "strided", "small"] * 700   # > 4096 passes
+    got = torch.empty(len(order), dtype=torch.float32, device="cuda")
+    for i, k in enumerate(order):
+        qf.amax(sd if k == "strided" else dev[k], out, accumulate=False)
+        got[i] = out[0]
+    torch.cuda.synchronize()
+    g = got.cpu().numpy()
+    for i, k in enumerate(order):
+        assert g[i] == want[k], (i, k, g[i], want[k])
+    qf.amax(dev["nan"], out, accumulate=False)
+    torch.cuda.synchronize()
+    assert np.isnan(out.item())
+    qf.amax(dev["small"], out, accumulate=False)      # the NaN pass left its slot clear too
+    torch.cuda.synchronize()
+    assert out.item() == want["small"]
+
+
+def test_amax_empty_tensor(qf):
+    out = torch.full((1,), 5.0, dtype=torch.float32, device="cuda")
+    x = torch.empty((0, 64), dtype=torch.int16, device="cuda")
+    qf.amax(x, out, accumulate=True)
+    torch.cuda.synchronize()
+    assert out.item() == 5.0
+    qf.amax(x, out, accumulate=False)
+    torch.cuda.synchronize()
+    assert out.item() == 0.0
+
+
 @pytest.mark.parametrize("K,col", [(12, 10), (5, 4), (1, 0), (1003, 1001)])
 def test_amax_row_tail_not_multiple_of_8(qf, K, col):
     """K % 8 != 0 inside a wider row stride: the row's last K % 8 elements count (the maximum
