@@ -494,13 +494,15 @@ def other_rows(qf, torch, dev, only=None):
             d = qf.grouped_desc(E, Tm, n, k, "nvfp4", "none")
             glayers.append((d, Xg, Wg, dYg, torch.empty(Tm, n, dtype=torch.bfloat16, device=dev),
                             torch.empty(Tm, k, dtype=torch.bfloat16, device=dev),
-                            torch.empty(E, n, k, dtype=torch.float32, device=dev), qf.grouped_workspace(d)))
+                            torch.empty(E, n, k, dtype=torch.float32, device=dev), qf.grouped_workspace(d),
+                            qf.grouped_saved_buffer(d)))
             gflops += 3 * 2.0 * Tm * n * k
 
         def moe_step():
-            for d, Xg, Wg, dYg, Yg, dXg, dWg, ws in glayers:
-                qf.qlinear_grouped_fwd(d, off, Xg, Wg, Yg, ws)
-                qf.qlinear_grouped_bwd_ste(d, off, dYg, Xg, Wg, dXg, dWg, ws)
+            # the forward saves the experts' packed W_hat; the backward dequantizes it
+            for d, Xg, Wg, dYg, Yg, dXg, dWg, ws, sv in glayers:
+                qf.qlinear_grouped_fwd(d, off, Xg, Wg, Yg, ws, saved=sv)
+                qf.qlinear_grouped_bwd_ste(d, off, dYg, Xg, Wg, dXg, dWg, ws, saved=sv)
 
         ms = _time(torch, moe_step, reps=10, warm=5)
         cnt = np.diff(offsets)

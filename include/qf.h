@@ -250,23 +250,39 @@ typedef struct {
 QF_API qf_status qf_grouped_workspace_size(const qf_grouped_desc* d, size_t* bytes);
 
 /*
+ * qf_grouped_saved_size -- bytes of the grouped layer's saved operand (Sec. 3.2.1, Sec. 3.3):
+ * the experts' packed W_hat back to back, 0.5625 bytes per element for NVFP4.  Layout, each
+ * region 256-byte aligned: NVFP4 = {S [E] (the experts' tensor decode scales), codes [E N, K/2],
+ * E4M3 scales [E N, K/16]}; MXFP4 = {codes [E N, K/2], E8M0 scales [E N, K/32]}; Q4_K = {blocks
+ * [E N, K/256, 144]}; 0 for an unquantized weight.  Expert e's rows are rows e N .. e N + N - 1.
+ * The activations are not saved: the backward forms A_hat's transposed, expert-padded operand
+ * from X in one pass, which reads no more than a dequantization of packed codes would.
+ */
+QF_API qf_status qf_grouped_saved_size(const qf_grouped_desc* d, size_t* bytes);
+
+/*
  * qf_qlinear_grouped_fwd -- for every expert e, rows [off[e], off[e+1]) of X:
  *   Y_e = A_hat_e W_hat_e^T with W_hat_e = Q^-1(Q(W[e])), one tensor scale per expert.
  *   group_offsets: DEVICE int64 [E+1], non-decreasing, off[0] = 0, off[E] = T (the host never
  *   reads it).  X bf16 [T, K], W bf16 [E, N, K], Y bf16 [T, N].
+ *   saved: NULL, or a 256-byte aligned device buffer of qf_grouped_saved_size bytes that
+ *   receives the experts' packed W_hat (written by the same quantizer launch as W_hat).
  */
 QF_API qf_status qf_qlinear_grouped_fwd(const qf_grouped_desc* d, const int64_t* group_offsets,
-                                 const uint16_t* X, const uint16_t* W, uint16_t* Y, void* ws,
-                                 size_t ws_bytes, qf_stream_t stream);
+                                 const uint16_t* X, const uint16_t* W, uint16_t* Y, void* saved,
+                                 void* ws, size_t ws_bytes, qf_stream_t stream);
 
 /*
  * qf_qlinear_grouped_bwd_ste -- per expert: dX_e = dY_e W_hat_e (bf16 [T, K], may be NULL),
  *   dW_e = dY_e^T A_hat_e (FP32 [E, N, K], may be NULL; experts with no rows get zeros).
+ *   saved: the forward's saved buffer (the experts' W_hat^T are dequantized from it: no amax
+ *   pass, no re-quantization), or NULL (W is quantized again, or with QF_FLAG_REUSE_WS the
+ *   workspace's W_hat is used).  The gradients are bit-identical either way.
  */
 QF_API qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int64_t* group_offsets,
                                      const uint16_t* dY, const uint16_t* X, const uint16_t* W,
-                                     uint16_t* dX, float* dW, void* ws, size_t ws_bytes,
-                                     qf_stream_t stream);
+                                     const void* saved, uint16_t* dX, float* dW, void* ws,
+                                     size_t ws_bytes, qf_stream_t stream);
 
 /* ---------------------------------------------------------------------------------------
  * Host-only validation (Sec. 3.2.2: the quantizer interface's preconditions).  Each runs the
@@ -281,9 +297,10 @@ QF_API qf_status qf_validate_fakequant(int fmt, const void* x, int64_t R, int64_
 QF_API qf_status qf_validate_qlinear(const qf_qlinear_desc* d, const void* X, const void* W,
                                      const void* Y, const void* saved, const void* ws,
                                      size_t ws_bytes);
-/* A grouped call pair: d with X [T, K], W [E, N, K], Y [T, N] and ws of ws_bytes. */
+/* A grouped call pair: d with X [T, K], W [E, N, K], Y [T, N], saved and ws of ws_bytes. */
 QF_API qf_status qf_validate_grouped(const qf_grouped_desc* d, const void* X, const void* W,
-                                     const void* Y, const void* ws, size_t ws_bytes);
+                                     const void* Y, const void* saved, const void* ws,
+                                     size_t ws_bytes);
 
 /*
  * qf_fakequant_transposed -- quantize + dequantize with transposed output: out[k][r] =

@@ -103,14 +103,16 @@ def lib() -> ctypes.CDLL:
             "qf_validate_fakequant": ([ctypes.c_int, _P, _I, _I, _I], ctypes.c_int),
             "qf_validate_qlinear": ([ctypes.POINTER(QLinearDesc), _P, _P, _P, _P, _P,
                                      ctypes.c_size_t], ctypes.c_int),
-            "qf_validate_grouped": ([ctypes.POINTER(GroupedDesc), _P, _P, _P, _P,
+            "qf_validate_grouped": ([ctypes.POINTER(GroupedDesc), _P, _P, _P, _P, _P,
                                      ctypes.c_size_t], ctypes.c_int),
             "qf_grouped_workspace_size": ([ctypes.POINTER(GroupedDesc),
                                            ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
-            "qf_qlinear_grouped_fwd": ([ctypes.POINTER(GroupedDesc), _P, _P, _P, _P, _P,
+            "qf_grouped_saved_size": ([ctypes.POINTER(GroupedDesc),
+                                       ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
+            "qf_qlinear_grouped_fwd": ([ctypes.POINTER(GroupedDesc), _P, _P, _P, _P, _P, _P,
                                         ctypes.c_size_t, _P], ctypes.c_int),
             "qf_qlinear_grouped_bwd_ste": ([ctypes.POINTER(GroupedDesc), _P, _P, _P, _P, _P, _P,
-                                            _P, ctypes.c_size_t, _P], ctypes.c_int),
+                                            _P, _P, ctypes.c_size_t, _P], ctypes.c_int),
             "qf_gemm_bf16": ([_I, _I, _I, _P, _I, ctypes.c_int, _P, _I, ctypes.c_int, _P, _I,
                               ctypes.c_int, _P], ctypes.c_int),
             "qf_transpose_bf16": ([_P, _I, _I, _I, _P, _I, _P], ctypes.c_int),
@@ -291,16 +293,28 @@ def grouped_workspace(desc: GroupedDesc, device="cuda"):
     return torch.empty(max(n.value, 256), dtype=torch.uint8, device=device)
 
 
-def qlinear_grouped_fwd(desc, offsets, X, W, Y, ws):
+def grouped_saved_size(desc: GroupedDesc) -> int:
+    n = ctypes.c_size_t()
+    _check(lib().qf_grouped_saved_size(ctypes.byref(desc), ctypes.byref(n)))
+    return n.value
+
+
+def grouped_saved_buffer(desc: GroupedDesc, device="cuda"):
+    """A device buffer for the grouped layer's saved operand (the experts' packed W_hat)."""
+    return torch.empty(max(grouped_saved_size(desc), 256), dtype=torch.uint8, device=device)
+
+
+def qlinear_grouped_fwd(desc, offsets, X, W, Y, ws, saved=None):
     _check(lib().qf_qlinear_grouped_fwd(ctypes.byref(desc), _ptr(offsets), _ptr(_bf16(X)),
-                                        _ptr(_bf16(W)), _ptr(_bf16(Y)), _ptr(ws), ws.numel(),
-                                        _stream()))
+                                        _ptr(_bf16(W)), _ptr(_bf16(Y)), _ptr(saved), _ptr(ws),
+                                        ws.numel(), _stream()))
 
 
-def qlinear_grouped_bwd_ste(desc, offsets, dY, X, W, dX, dW, ws):
+def qlinear_grouped_bwd_ste(desc, offsets, dY, X, W, dX, dW, ws, saved=None):
     _check(lib().qf_qlinear_grouped_bwd_ste(ctypes.byref(desc), _ptr(offsets), _ptr(_bf16(dY)),
-                                            _ptr(_bf16(X)), _ptr(_bf16(W)), _ptr(_bf16(dX)),
-                                            _ptr(dW), _ptr(ws), ws.numel(), _stream()))
+                                            _ptr(_bf16(X)), _ptr(_bf16(W)), _ptr(saved),
+                                            _ptr(_bf16(dX)), _ptr(dW), _ptr(ws), ws.numel(),
+                                            _stream()))
 
 
 def gemm_bf16(M, N, K, A, lda, a_kmajor, B, ldb, b_kmajor, C, ldc, c_f32, ws=None):

@@ -110,7 +110,8 @@ qf_status fakequant_to(int fmt, const uint16_t* x, int64_t R, int64_t K, int64_t
 }
 
 // A quantized operand in packed form: codes [R][K/2] + block scales [R][K/B] + (NVFP4) the
-// tensor decode scale S = g / 2688 in its own 256-byte slot; Q4_K: blocks [R][K/256][144] in
+// tensor decode scale S = g / 2688 in its own 256-byte slot (nS scales, one per tensor, for
+// the experts of a grouped layer stored back to back); Q4_K: blocks [R][K/256][144] in
 // `codes`.  This is the layer's saved form of W_hat / A_hat (0.5625 bytes per element).
 struct Packed {
   uint8_t* codes;
@@ -118,10 +119,10 @@ struct Packed {
   float* S;
 };
 
-size_t packed_bytes(int fmt, int64_t R, int64_t K) {
+size_t packed_bytes(int fmt, int64_t R, int64_t K, int64_t nS = 1) {
   const size_t r = R, k = K;
   switch (fmt) {
-    case QF_FMT_NVFP4: return kAlign + up(r * k / 2) + up(r * k / 16);
+    case QF_FMT_NVFP4: return up((size_t)nS * 4) + up(r * k / 2) + up(r * k / 16);
     case QF_FMT_MXFP4: return up(r * k / 2) + up(r * k / 32);
     case QF_FMT_Q4K: return up(r * (k / 256) * 144);
     default: return 0;
@@ -129,10 +130,10 @@ size_t packed_bytes(int fmt, int64_t R, int64_t K) {
 }
 
 // Carve a packed operand of format fmt out of p (advances p).
-Packed carve_packed(int fmt, int64_t R, int64_t K, char*& p) {
+Packed carve_packed(int fmt, int64_t R, int64_t K, char*& p, int64_t nS = 1) {
   Packed q{};
   const size_t r = R, k = K;
-  if (fmt == QF_FMT_NVFP4) { q.S = reinterpret_cast<float*>(p); p += kAlign; }
+  if (fmt == QF_FMT_NVFP4) { q.S = reinterpret_cast<float*>(p); p += up((size_t)nS * 4); }
   if (fmt == QF_FMT_NONE) return q;
   q.codes = reinterpret_cast<uint8_t*>(p);
   if (fmt == QF_FMT_Q4K) { p += up(r * (k / 256) * 144); return q; }
@@ -659,6 +660,16 @@ GroupedWs grouped_ws(const qf_grouped_desc* d, void* ws) {
   return g;
 }
 
+// The grouped layer's saved operand: the experts' packed W_hat back to back, one tensor
+// decode scale per expert (NVFP4); nothing for an unquantized weight.
+size_t grouped_saved_bytes(const qf_grouped_desc* d) {
+  return packed_bytes(d->wfmt, d->E * d->N, d->K, d->E);
+}
+Packed grouped_saved_layout(const qf_grouped_desc* d, void* saved) {
+  char* p = static_cast<char*>(saved);
+  return carve_packed(d->wfmt, d->E * d->N, d->K, p, d->E);
+}
+
 qf_status check_grouped(const char* fn, const qf_grouped_desc* d, const int64_t* off) {
   if (!d) return fail(QF_EINVAL, "%s: null descriptor", fn);
   if (d->E < 0 || d->T < 0 || d->N < 0 || d->K < 0) return fail(QF_ESHAPE, "%s: negative shape", fn);
@@ -673,12 +684,14 @@ qf_status check_grouped(const char* fn, const qf_grouped_desc* d, const int64_t*
   return QF_OK;
 }
 
+// W_hat (and, with pk, the experts' packed W_hat in the same launch) and A_hat.
 qf_status grouped_quantize(const qf_grouped_desc* d, const uint16_t* X, const uint16_t* W,
                            const GroupedWs& g, bool do_w, bool do_a, const uint16_t** Wop,
-                           const uint16_t** Aop, hipStream_t s) {
+                           const uint16_t** Aop, hipStream_t s, const Packed* pk = nullptr) {
   *Wop = W;
   *Aop = X;
   const int64_t R = d->N, K = d->K;
+  const Packed q = pk ? *pk : Packed{};
   if (d->wfmt != QF_FMT_NONE) {
     if (do_w) {
       switch (d->wfmt) {
@@ -688,14 +701,16 @@ qf_status grouped_quantize(const qf_grouped_desc* d, const uint16_t* X, const ui
             QF_TRY(dev(qf::launch_amax_batched(W, d->E, R, K, g.wamax, false, s), "amax"));
             gp = g.wamax;
           }
-          QF_TRY(dev(qf::launch_nvfp4_batched(W, d->E, R, K, gp, g.what, s), "nvfp4"));
+          QF_TRY(dev(qf::launch_nvfp4_batched(W, d->E, R, K, gp, q.S, q.codes, q.scales, g.what,
+                                              s),
+                     "nvfp4"));
           break;
         }
         case QF_FMT_MXFP4:
-          QF_TRY(dev(qf::launch_mxfp4(W, d->E * R, K, K, nullptr, nullptr, g.what, s), "mxfp4"));
+          QF_TRY(dev(qf::launch_mxfp4(W, d->E * R, K, K, q.codes, q.scales, g.what, s), "mxfp4"));
           break;
         case QF_FMT_Q4K:
-          QF_TRY(dev(qf::launch_q4k(W, d->E * R, K, K, nullptr, g.what, s), "q4k"));
+          QF_TRY(dev(qf::launch_q4k(W, d->E * R, K, K, q.codes, g.what, s), "q4k"));
           break;
       }
     }
@@ -717,19 +732,28 @@ qf_status qf_grouped_workspace_size(const qf_grouped_desc* d, size_t* bytes) {
   return ok();
 }
 
+qf_status qf_grouped_saved_size(const qf_grouped_desc* d, size_t* bytes) {
+  QF_TRY(check_grouped("qf_grouped_saved_size", d, (const int64_t*)1));
+  if (!bytes) return fail(QF_EINVAL, "qf_grouped_saved_size: null output");
+  *bytes = grouped_saved_bytes(d);
+  return ok();
+}
+
 qf_status qf_qlinear_grouped_fwd(const qf_grouped_desc* d, const int64_t* group_offsets,
-                                 const uint16_t* X, const uint16_t* W, uint16_t* Y, void* ws,
-                                 size_t ws_bytes, qf_stream_t stream) {
+                                 const uint16_t* X, const uint16_t* W, uint16_t* Y, void* saved,
+                                 void* ws, size_t ws_bytes, qf_stream_t stream) {
   QF_TRY(check_grouped("qf_qlinear_grouped_fwd", d, group_offsets));
   QF_TRY(check_mat("qf_qlinear_grouped_fwd: X", X, d->T, d->K, d->K, true));
   QF_TRY(check_mat("qf_qlinear_grouped_fwd: W", W, d->E * d->N, d->K, d->K, true));
   QF_TRY(check_mat("qf_qlinear_grouped_fwd: Y", Y, d->T, d->N, d->N, true));
+  QF_TRY(check_saved("qf_qlinear_grouped_fwd", saved));
   QF_TRY(check_ws("qf_qlinear_grouped_fwd", grouped_ws_bytes(d), ws, ws_bytes));
   if (d->E == 0) return ok();
   hipStream_t s = S(stream);
   GroupedWs g = grouped_ws(d, ws);
   const uint16_t *Wop, *Aop;
-  QF_TRY(grouped_quantize(d, X, W, g, true, true, &Wop, &Aop, s));
+  const Packed pk = saved ? grouped_saved_layout(d, saved) : Packed{};
+  QF_TRY(grouped_quantize(d, X, W, g, true, true, &Wop, &Aop, s, saved ? &pk : nullptr));
   QF_TRY(dev(qf::launch_grouped_prep(group_offsets, d->E, g.tile_start, g.order, g.kstart, s),
              "prep"));
   QF_TRY(dev(qf::launch_grouped_nt_rows(d->E, d->T, d->N, d->K, group_offsets, g.tile_start, Aop,
@@ -740,23 +764,27 @@ qf_status qf_qlinear_grouped_fwd(const qf_grouped_desc* d, const int64_t* group_
 
 qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int64_t* group_offsets,
                                      const uint16_t* dY, const uint16_t* X, const uint16_t* W,
-                                     uint16_t* dX, float* dW, void* ws, size_t ws_bytes,
-                                     qf_stream_t stream) {
+                                     const void* saved, uint16_t* dX, float* dW, void* ws,
+                                     size_t ws_bytes, qf_stream_t stream) {
   QF_TRY(check_grouped("qf_qlinear_grouped_bwd_ste", d, group_offsets));
   QF_TRY(check_mat("qf_qlinear_grouped_bwd_ste: dY", dY, d->T, d->N, d->N, true));
   QF_TRY(check_mat("qf_qlinear_grouped_bwd_ste: X", X, d->T, d->K, d->K, dW != nullptr));
   QF_TRY(check_mat("qf_qlinear_grouped_bwd_ste: W", W, d->E * d->N, d->K, d->K, dX != nullptr));
   QF_TRY(check_mat("qf_qlinear_grouped_bwd_ste: dX", dX, d->T, d->K, d->K, false));
   QF_TRY(check_out("qf_qlinear_grouped_bwd_ste: dW", dW));
+  QF_TRY(check_saved("qf_qlinear_grouped_bwd_ste", saved));
   QF_TRY(check_ws("qf_qlinear_grouped_bwd_ste", grouped_ws_bytes(d), ws, ws_bytes));
   if (d->E == 0) return ok();
   hipStream_t s = S(stream);
   GroupedWs g = grouped_ws(d, ws);
   const bool reuse = (d->flags & QF_FLAG_REUSE_WS) != 0;
-  // Without a saved W_hat, the experts' W_hat^T comes straight from the transposing quantizer.
-  const bool fuse_w = dX && d->wfmt != QF_FMT_NONE && !reuse;
+  // The experts' W_hat^T: dequantized from the saved packed experts, or straight from the
+  // transposing quantizer, or (QF_FLAG_REUSE_WS) transposed from the workspace's W_hat.
+  const bool from_saved = dX && d->wfmt != QF_FMT_NONE && saved != nullptr;
+  const bool fuse_w = dX && d->wfmt != QF_FMT_NONE && !reuse && !from_saved;
   const uint16_t *Wop, *Aop;
-  QF_TRY(grouped_quantize(d, X, W, g, !reuse && dX && !fuse_w, false, &Wop, &Aop, s));
+  QF_TRY(grouped_quantize(d, X, W, g, !reuse && dX && !fuse_w && !from_saved, false, &Wop,
+                          &Aop, s));
   QF_TRY(dev(qf::launch_grouped_prep(group_offsets, d->E, g.tile_start, g.order, g.kstart, s),
              "prep"));
   // dY^T in the padded layout of dW is written by the dX launch from the dY tiles it stages
@@ -766,7 +794,12 @@ qf_status qf_qlinear_grouped_bwd_ste(const qf_grouped_desc* d, const int64_t* gr
   const bool dyt_by_dx = dX != nullptr && dW != nullptr && (d->K + 255) / 256 >= 8 &&
                          ldt < qf::kGemmAtMaxLd;
   if (dX) {
-    if (fuse_w) {
+    if (from_saved) {
+      const Packed pk = grouped_saved_layout(d, const_cast<void*>(saved));
+      QF_TRY(dev(qf::launch_dequant_t(d->wfmt, pk.codes, pk.scales, pk.S, d->N, d->K, g.whatt,
+                                      d->N, s, d->E, d->N * d->K),
+                 "dequantize saved expert W (transposed)"));
+    } else if (fuse_w) {
       const float* gp = d->w_amax;
       if (d->wfmt == QF_FMT_NVFP4 && !gp) {
         QF_TRY(dev(qf::launch_amax_batched(W, d->E, d->N, d->K, g.wamax, false, s), "amax"));
@@ -1262,7 +1295,7 @@ qf_status glora_quant_via_merged(const qf_grouped_desc* d, const qf::LoraOperand
     QF_TRY(dev(qf::launch_quant_t(QF_FMT_NVFP4, tmp, N, K, K, E, N * K, scratch, out, N, N * K, s),
                "quantize merged experts (transposed)"));
   else
-    QF_TRY(dev(qf::launch_nvfp4_batched(tmp, E, N, K, scratch, out, s),
+    QF_TRY(dev(qf::launch_nvfp4_batched(tmp, E, N, K, scratch, nullptr, nullptr, nullptr, out, s),
                "quantize merged experts"));
   return QF_OK;
 }
@@ -1605,7 +1638,8 @@ qf_status qf_validate_qlinear(const qf_qlinear_desc* d, const void* X, const voi
 }
 
 qf_status qf_validate_grouped(const qf_grouped_desc* d, const void* X, const void* W,
-                              const void* Y, const void* ws, size_t ws_bytes) {
+                              const void* Y, const void* saved, const void* ws,
+                              size_t ws_bytes) {
   const char* fn = "qf_validate_grouped";
   // (the device offsets are the call's own argument; only their presence is checked there)
   static const int64_t kOffsetsPresent = 0;
@@ -1613,6 +1647,7 @@ qf_status qf_validate_grouped(const qf_grouped_desc* d, const void* X, const voi
   QF_TRY(check_mat("qf_validate_grouped: X", X, d->T, d->K, d->K, true));
   QF_TRY(check_mat("qf_validate_grouped: W", W, d->E * d->N, d->K, d->K, true));
   QF_TRY(check_mat("qf_validate_grouped: Y", Y, d->T, d->N, d->N, true));
+  QF_TRY(check_saved(fn, saved));
   QF_TRY(check_ws(fn, grouped_ws_bytes(d), const_cast<void*>(ws), ws_bytes));
   return ok();
 }

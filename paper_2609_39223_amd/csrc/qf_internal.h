@@ -29,8 +29,11 @@ hipError_t launch_q4k_mse(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, 
 // Batched variants over E equally shaped tensors (expert weights), one tensor scale each.
 hipError_t launch_amax_batched(const uint16_t* x, int64_t E, int64_t R, int64_t K,
                                float* amax, bool accumulate, hipStream_t s);
+// NVFP4 of tensor z with g[z]: x_hat and, when non-null, S[z], codes and scales of all E tensors
+// back to back (tensor z's after tensor z - 1's).
 hipError_t launch_nvfp4_batched(const uint16_t* x, int64_t E, int64_t R, int64_t K,
-                                const float* g, uint16_t* xhat, hipStream_t s);
+                                const float* g, float* s_out, uint8_t* codes, uint8_t* scales,
+                                uint16_t* xhat, hipStream_t s);
 
 // Quantize-dequantize with transposed output: out[k][r] = x_hat[r][k] (bf16, row stride ldo)
 // for `batch` tensors spaced xbs / obs elements apart (NVFP4: tensor amax g[z] per tensor).
@@ -43,9 +46,11 @@ hipError_t launch_quant_t(int fmt, const uint16_t* x, int64_t R, int64_t K, int6
 // with its tensor decode scale S = g / 2688 at S) or Q4_K blocks [R][K/256][144] (in
 // `codes`); bit-identical to launch_quant_t's x_hat of the tensor those codes came from.
 // R and K multiples of 8 (Q4K: K of 256).
+// batch > 1: that many [R, K] tensors stored back to back (decode scale S[z]), tensor z's
+// output obs elements after tensor z - 1's.
 hipError_t launch_dequant_t(int fmt, const uint8_t* codes, const uint8_t* scales,
                             const float* S, int64_t R, int64_t K, uint16_t* out, int64_t ldo,
-                            hipStream_t s);
+                            hipStream_t s, int64_t batch = 1, int64_t obs = 0);
 // Grouped, transposed, 64-padded: rows [off[e], off[e+1]) of x [T, K] (fmt NONE or MXFP4)
 // land as columns [64 kstart[e], 64 kstart[e+1]) of out [K, ldo] (x_hat^T), zeros past each
 // expert's last row.  kstart from launch_grouped_prep.

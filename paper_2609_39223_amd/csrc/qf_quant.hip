@@ -356,11 +356,22 @@ __global__ __launch_bounds__(kThreads) void dequant_t_kernel(const uint8_t* __re
                                                              const float* __restrict__ Sp,
                                                              int64_t R, int64_t K,
                                                              uint16_t* __restrict__ out,
-                                                             int64_t ldo) {
+                                                             int64_t ldo, int64_t obs) {
   __shared__ uint4 tile[kTR * (kTC / 8)];
   const int t = threadIdx.x;
   const int64_t c0 = (int64_t)blockIdx.x * kTC, r0 = (int64_t)blockIdx.y * kTR;
-  const float S = FMT == QF_FMT_NVFP4 ? Sp[0] : 0.0f;
+  // grid.z indexes equally shaped tensors stored back to back (expert weights): tensor z's
+  // codes / scales / blocks follow the z before it, its decode scale is Sp[z], and its output
+  // starts obs elements after tensor z - 1's
+  const int64_t z = blockIdx.z;
+  if (FMT == QF_FMT_Q4K) {
+    codes += z * R * (K / 256) * 144;
+  } else {
+    codes += z * R * (K / 2);
+    scales += z * R * (K / (FMT == QF_FMT_NVFP4 ? 16 : 32));
+  }
+  out += z * obs;
+  const float S = FMT == QF_FMT_NVFP4 ? Sp[z] : 0.0f;
   uint32_t cw[8], sc[8];
   uint4 hd[8];
   const int cc = t & 31;
@@ -511,16 +522,18 @@ hipError_t launch_nvfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, co
 }
 
 hipError_t launch_nvfp4_batched(const uint16_t* x, int64_t E, int64_t R, int64_t K,
-                                const float* g, uint16_t* xhat, hipStream_t s) {
+                                const float* g, float* s_out, uint8_t* codes, uint8_t* scales,
+                                uint16_t* xhat, hipStream_t s) {
   if (E == 0 || R == 0 || K == 0) return hipSuccess;
   // Blocks of 16 lie along the contiguous rows and the scale g[z] covers the whole tensor, so
-  // each (contiguous) tensor may be read as rows of 2048 elements: same blocks, same x_hat,
-  // and every lane busy where K / 8 chunks would leave some idle.
+  // each (contiguous) tensor may be read as rows of 2048 elements: same blocks, same codes,
+  // scales and x_hat at the same offsets, and every lane busy where K / 8 chunks would leave
+  // some idle.
   contiguous_row_view(R, K);
   dim3 grid = row_grid(R, K, kRowsPerThread);
   grid.z = (unsigned)E;
   hipLaunchKernelGGL(nvfp4_kernel<kRowsPerThread>, grid, dim3(kThreads), 0, s, x, R, K, K,
-                     R * K, g, (float*)nullptr, (uint8_t*)nullptr, (uint8_t*)nullptr, xhat);
+                     R * K, g, s_out, codes, scales, xhat);
   return hipGetLastError();
 }
 
@@ -580,22 +593,19 @@ hipError_t launch_quant_t(int fmt, const uint16_t* x, int64_t R, int64_t K, int6
 
 hipError_t launch_dequant_t(int fmt, const uint8_t* codes, const uint8_t* scales,
                             const float* S, int64_t R, int64_t K, uint16_t* out, int64_t ldo,
-                            hipStream_t s) {
-  if (R == 0 || K == 0) return hipSuccess;
-  const dim3 grid((unsigned)((K + kTC - 1) / kTC), (unsigned)((R + kTR - 1) / kTR));
+                            hipStream_t s, int64_t batch, int64_t obs) {
+  if (R == 0 || K == 0 || batch == 0) return hipSuccess;
+  const dim3 grid((unsigned)((K + kTC - 1) / kTC), (unsigned)((R + kTR - 1) / kTR),
+                  (unsigned)batch);
   switch (fmt) {
-    case QF_FMT_NVFP4:
-      hipLaunchKernelGGL(dequant_t_kernel<QF_FMT_NVFP4>, grid, dim3(kThreads), 0, s, codes, scales,
-                         S, R, K, out, ldo);
-      break;
-    case QF_FMT_MXFP4:
-      hipLaunchKernelGGL(dequant_t_kernel<QF_FMT_MXFP4>, grid, dim3(kThreads), 0, s, codes, scales,
-                         S, R, K, out, ldo);
-      break;
-    case QF_FMT_Q4K:
-      hipLaunchKernelGGL(dequant_t_kernel<QF_FMT_Q4K>, grid, dim3(kThreads), 0, s, codes, scales,
-                         S, R, K, out, ldo);
-      break;
+#define QF_DQ(F)                                                                               \
+  hipLaunchKernelGGL(dequant_t_kernel<F>, grid, dim3(kThreads), 0, s, codes, scales, S, R, K, \
+                     out, ldo, obs);                                                           \
+  break;
+    case QF_FMT_NVFP4: QF_DQ(QF_FMT_NVFP4)
+    case QF_FMT_MXFP4: QF_DQ(QF_FMT_MXFP4)
+    case QF_FMT_Q4K: QF_DQ(QF_FMT_Q4K)
+#undef QF_DQ
     default:
       return hipErrorInvalidValue;
   }

@@ -129,6 +129,37 @@ def test_saved_size_is_the_packed_operands(L):
         assert n.value <= 0.5625 * (N + (M if af else 0)) * K + 3 * 256 + 2 * 256
 
 
+class GDesc(ctypes.Structure):
+    _fields_ = [("E", ctypes.c_int64), ("T", ctypes.c_int64), ("N", ctypes.c_int64),
+                ("K", ctypes.c_int64), ("wfmt", ctypes.c_int32), ("afmt", ctypes.c_int32),
+                ("w_amax", ctypes.c_void_p), ("flags", ctypes.c_uint32)]
+
+
+def test_grouped_saved_size_and_validation(L):
+    """qf_grouped_saved_size: the experts' packed W_hat back to back (NVFP4: one FP32 decode
+    scale per expert in a 256-byte aligned region, then codes and E4M3 scales of all E N rows);
+    qf_validate_grouped checks the saved buffer's alignment as the calls do."""
+    def up(v):
+        return (v + 255) // 256 * 256
+    n = ctypes.c_size_t()
+    E, T, N, K = 128, 1000, 3072, 1536
+    for wf, want in [(1, up(4 * E) + up(E * N * K // 2) + up(E * N * K // 16)),
+                     (2, up(E * N * K // 2) + up(E * N * K // 32)),
+                     (3, up(E * N * (K // 256) * 144)), (0, 0)]:
+        d = GDesc(E, T, N, K, wf, 0, None, 0)
+        assert L.qf_grouped_saved_size(ctypes.byref(d), ctypes.byref(n)) == QF_OK
+        assert n.value == want, wf
+    d = GDesc(E, T, N, K, 1, 0, None, 0)
+    assert L.qf_grouped_workspace_size(ctypes.byref(d), ctypes.byref(n)) == QF_OK
+    vg = L.qf_validate_grouped
+    vg.argtypes = [ctypes.POINTER(GDesc), P, P, P, P, P, ctypes.c_size_t]
+    assert vg(ctypes.byref(d), P(256), P(512), P(768), P(1024), P(4096), n.value) == QF_OK
+    assert vg(ctypes.byref(d), P(256), P(512), P(768), None, P(4096), n.value) == QF_OK
+    assert vg(ctypes.byref(d), P(256), P(512), P(768), P(1040), P(4096), n.value) == QF_EALIGN
+    assert b"saved" in L.qf_last_error()
+    assert vg(ctypes.byref(d), P(256), P(512), P(768), P(1024), P(4096), n.value - 1) == QF_EINVAL
+
+
 def test_validate_calls_mirror_the_entry_points(L):
     """qf_validate_*: host-only checks that return what the call itself would, without a
     launch (every case here would fail before one)."""

@@ -21,19 +21,22 @@ def qf():
     return qf
 
 
-def run_grouped(qf, offsets, X, W, dY, wfmt, afmt, reuse=False):
+def run_grouped(qf, offsets, X, W, dY, wfmt, afmt, reuse=False, saved=False):
+    """Forward + backward; the backward re-quantizes W (default), reuses the forward's
+    workspace (reuse) or dequantizes the forward's saved packed experts (saved)."""
     E, N, K = W.shape
     T = X.shape[0]
     d = qf.grouped_desc(E, T, N, K, wfmt, afmt)
     ws = qf.grouped_workspace(d)
+    sv = qf.grouped_saved_buffer(d) if saved else None
     off = torch.from_numpy(offsets.astype(np.int64)).cuda()
     Xd, Wd, dYd = to_dev(X), to_dev(W.reshape(E * N, K)), to_dev(dY)
     Y, dX = empty_bf16((T, N)), empty_bf16((T, K))
     dW = torch.full((E, N, K), 7.0, dtype=torch.float32, device="cuda")
-    qf.qlinear_grouped_fwd(d, off, Xd, Wd, Y, ws)
+    qf.qlinear_grouped_fwd(d, off, Xd, Wd, Y, ws, saved=sv)
     if reuse:
         d = qf.grouped_desc(E, T, N, K, wfmt, afmt, flags=qf.FLAG_REUSE_WS)
-    qf.qlinear_grouped_bwd_ste(d, off, dYd, Xd, Wd, dX, dW, ws)
+    qf.qlinear_grouped_bwd_ste(d, off, dYd, Xd, Wd, dX, dW, ws, saved=sv)
     torch.cuda.synchronize()
     return from_dev(Y), from_dev(dX), from_dev(dW)
 
@@ -174,12 +177,13 @@ def test_moe_projection_full_size_sampled(qf, N, K):
     dY = workloads.normal_bf16(rng, (T, N))
     d = qf.grouped_desc(E, T, N, K, "nvfp4", "none")
     ws = qf.grouped_workspace(d)
+    sv = qf.grouped_saved_buffer(d)                 # as the benchmark: backward from saved
     off = torch.from_numpy(offsets.astype(np.int64)).cuda()
     Xd, Wd, dYd = to_dev(X), to_dev(W.reshape(E * N, K)), to_dev(dY)
     Yd, dXd = empty_bf16((T, N)), empty_bf16((T, K))
     dWd = torch.empty((E, N, K), dtype=torch.float32, device="cuda")
-    qf.qlinear_grouped_fwd(d, off, Xd, Wd, Yd, ws)
-    qf.qlinear_grouped_bwd_ste(d, off, dYd, Xd, Wd, dXd, dWd, ws)
+    qf.qlinear_grouped_fwd(d, off, Xd, Wd, Yd, ws, saved=sv)
+    qf.qlinear_grouped_bwd_ste(d, off, dYd, Xd, Wd, dXd, dWd, ws, saved=sv)
     torch.cuda.synchronize()
     Y, dX = from_dev(Yd), from_dev(dXd)
     cnt = np.diff(offsets)
@@ -215,3 +219,65 @@ def test_grouped_transposing_quantizer_matches_saved_operands(qf, wfmt):
     _, dX2, dW2 = run_grouped(qf, offsets, X, W, dY, wfmt, "none", reuse=True)
     assert np.array_equal(dX.view(np.uint16), dX2.view(np.uint16))
     assert np.array_equal(dW.view(np.uint32), dW2.view(np.uint32))
+
+
+@pytest.mark.parametrize("wfmt,afmt", [("nvfp4", "none"), ("mxfp4", "mxfp4"), ("q4k", "none")])
+def test_grouped_saved_experts_and_backward_from_them(qf, wfmt, afmt):
+    """The grouped forward's saved operand holds every expert's packed W_hat (NVFP4: codes, E4M3
+    scales and the expert's own S; MXFP4; Q4_K blocks) bit for bit as the oracle packs it, and
+    the backward that dequantizes it gives the same dX and dW bits as the backward that
+    re-quantizes W and the one that reuses the workspace."""
+    rng = np.random.default_rng(29)
+    E, N, K = 5, 264, 768
+    counts = np.array([70, 0, 258, 9, 300])
+    offsets = np.concatenate([[0], np.cumsum(counts)])
+    T = int(offsets[-1])
+    X = workloads.normal_bf16(rng, (T, K))
+    W = np.stack([workloads.normal_bf16(rng, (N, K), 0.02 * (e + 1)) for e in range(E)])
+    dY = workloads.normal_bf16(rng, (T, N))
+    d = qf.grouped_desc(E, T, N, K, wfmt, afmt)
+    sv = torch.full((qf.grouped_saved_size(d),), 0xA5, dtype=torch.uint8, device="cuda")
+    Y = empty_bf16((T, N))
+    qf.qlinear_grouped_fwd(d, torch.from_numpy(offsets.astype(np.int64)).cuda(), to_dev(X),
+                           to_dev(W.reshape(E * N, K)), Y, qf.grouped_workspace(d), saved=sv)
+    torch.cuda.synchronize()
+    buf = from_dev(sv)
+
+    def up(v):
+        return (v + 255) // 256 * 256
+    o = 0
+    if wfmt == "nvfp4":
+        S = buf[:4 * E].view(np.float32)
+        o = up(4 * E)
+    refs = [{"nvfp4": oracle.nvfp4, "mxfp4": oracle.mxfp4, "q4k": oracle.q4k}[wfmt](W[e])
+            for e in range(E)]
+    if wfmt == "q4k":
+        blk = buf[o:o + E * N * (K // 256) * 144].reshape(E, N, K // 256, 144)
+        for e in range(E):
+            np.testing.assert_array_equal(blk[e], refs[e]["packed"], err_msg=f"blocks e={e}")
+    else:
+        B = 16 if wfmt == "nvfp4" else 32
+        codes = buf[o:o + E * N * K // 2].reshape(E, N, K // 2)
+        o += up(E * N * K // 2)
+        scales = buf[o:o + E * N * K // B].reshape(E, N, K // B)
+        assert o + up(E * N * K // B) == qf.grouped_saved_size(d)
+        for e in range(E):
+            np.testing.assert_array_equal(codes[e], refs[e]["codes"], err_msg=f"codes e={e}")
+            np.testing.assert_array_equal(scales[e], refs[e]["scales"], err_msg=f"scales e={e}")
+            if wfmt == "nvfp4":
+                assert S[e] == refs[e]["S"], e
+    outs = [run_grouped(qf, offsets, X, W, dY, wfmt, afmt, saved=True),
+            run_grouped(qf, offsets, X, W, dY, wfmt, afmt),
+            run_grouped(qf, offsets, X, W, dY, wfmt, afmt, reuse=True)]
+    for name, (_, dX, dW) in zip(("requantize", "reuse"), outs[1:]):
+        assert np.array_equal(outs[0][1].view(np.uint16), dX.view(np.uint16)), f"dX vs {name}"
+        assert np.array_equal(outs[0][2].view(np.uint32), dW.view(np.uint32)), f"dW vs {name}"
+    ahat = oracle.fakequant(X, afmt)
+    _, dX, dW = outs[0]
+    for e in range(E):
+        r0, r1 = offsets[e], offsets[e + 1]
+        if r1 > r0:
+            assert_close(bf16_to_f64(dX[r0:r1]), oracle.linear_dx(dY[r0:r1], refs[e]["xhat"]),
+                         f"dX e={e}")
+            assert_close(dW[e].astype(np.float64), oracle.linear_dw(dY[r0:r1], ahat[r0:r1]),
+                         f"dW e={e}")
