@@ -108,10 +108,12 @@ def dense_layer_inputs(torch, dev, gen):
 
 def dense_phase_calls(qf, torch, dev, lin):
     """The kernels one linear's qf_qlinear_fwd + qf_qlinear_bwd_ste launch with a saved buffer
-    (NVFP4 weights, W's amax computed, bf16 activations), one C-ABI call each, in the layer's
-    order: the forward quantizes W once into its packed form (codes, scales, S; the saved
-    operand) and its bf16 W_hat, then runs the GEMM; the backward dequantizes the packed W
-    straight into W_hat^T."""
+    and the workspace kept (QF_FLAG_REUSE_WS; NVFP4 weights, W's amax computed, bf16
+    activations), one C-ABI call each, in the layer's order: the forward quantizes W once into
+    its packed form (codes, scales, S; the saved operand) and its bf16 W_hat, then runs the GEMM,
+    which also writes X^T for weights of at most 8192 rows; the backward dequantizes the packed
+    W straight into W_hat^T, its dX GEMM also writes dY^T, and it transposes X itself for the
+    wider weight."""
     T, N, K = lin["T"], lin["N"], lin["K"]
     X, W, dY = lin["X"], lin["W"], lin["dY"]
     ldm = T + 128 if T % 16384 == 0 else T        # the layer workspace's padded stride
@@ -128,20 +130,28 @@ def dense_phase_calls(qf, torch, dev, lin):
     dW = torch.empty(N, K, dtype=torch.float32, device=dev)
     gws = qf.gemm_workspace(N, K, 1)
     nm = lin["name"]
-    return [
+    calls = [
         (f"{nm}.amax_W", 0.0, lambda: qf.amax(W, g)),
         (f"{nm}.quant_W", 0.0,
          lambda: qf.fakequant_nvfp4(W, g, qf.AMAX_GIVEN, S, codes, scales, what)),
-        (f"{nm}.gemm_fwd", 2.0 * T * N * K,
-         lambda: qf.gemm_bf16(T, N, K, X, K, 1, what, K, 1, Y, N, 0)),
+    ]
+    if (N + 255) // 256 <= 32:     # the layer's forward GEMM also writes X^T (kept workspace)
+        calls.append((f"{nm}.gemm_fwd_and_X_transposed", 2.0 * T * N * K,
+                      lambda: qf.gemm_bf16_at(T, N, K, X, K, what, K, Y, N, xt, ldm)))
+    else:                          # ... else the backward transposes X
+        calls.append((f"{nm}.gemm_fwd", 2.0 * T * N * K,
+                      lambda: qf.gemm_bf16(T, N, K, X, K, 1, what, K, 1, Y, N, 0)))
+    calls += [
         (f"{nm}.dequant_W_transposed", 0.0,
          lambda: qf.dequantize_transposed("nvfp4", codes, scales, S, N, K, whatt)),
         (f"{nm}.gemm_dX_and_dY_transposed", 2.0 * T * N * K,
          lambda: qf.gemm_bf16_at(T, K, N, dY, N, whatt, N, dX, K, dyt, ldm)),
-        (f"{nm}.transpose_X", 0.0, lambda: qf.transpose_bf16(X, xt)),
-        (f"{nm}.gemm_dW", 2.0 * T * N * K,
-         lambda: qf.gemm_bf16(N, K, T, dyt, ldm, 1, xt, ldm, 1, dW, K, 1, ws=gws)),
     ]
+    if (N + 255) // 256 > 32:
+        calls.append((f"{nm}.transpose_X", 0.0, lambda: qf.transpose_bf16(X, xt)))
+    calls.append((f"{nm}.gemm_dW", 2.0 * T * N * K,
+                  lambda: qf.gemm_bf16(N, K, T, dyt, ldm, 1, xt, ldm, 1, dW, K, 1, ws=gws)))
+    return calls
 
 
 def main():
@@ -182,7 +192,8 @@ def main():
     flops = 0.0
     for lin in lins:
         T, N, K = lin["T"], lin["N"], lin["K"]
-        d = qf.qlinear_desc(T, N, K, "nvfp4", "none")
+        # the workspace is kept from forward to backward: the forward GEMM also writes X^T
+        d = qf.qlinear_desc(T, N, K, "nvfp4", "none", flags=qf.FLAG_REUSE_WS)
         layer.append((d, lin["X"], lin["W"], lin["dY"],
                       torch.empty(T, N, dtype=torch.bfloat16, device=dev),
                       torch.empty(T, K, dtype=torch.bfloat16, device=dev),
@@ -295,19 +306,25 @@ def main():
 def fused_ab(qf, torch, layer, reps=10):
     """Same-run A/B of the layer calls: the forward that decodes the packed weight inside the
     GEMM (QF_FLAG_DECODE_IN_GEMM) against the default one that writes W_hat in bf16 and runs a
-    plain GEMM, and the backward from the saved packed operands against the one that
-    quantizes W again."""
+    plain GEMM (and the same writing X^T for a kept workspace), and the backward from the saved
+    packed operands (with and without the forward's X^T) against the one that quantizes W
+    again."""
     out = {}
-    tot = {"fwd_fused": 0.0, "fwd_materialized": 0.0, "bwd_from_saved": 0.0,
-           "bwd_requantize": 0.0}
+    tot = {"fwd_fused": 0.0, "fwd_materialized": 0.0, "fwd_materialized_writing_Xt": 0.0,
+           "bwd_from_saved": 0.0, "bwd_from_saved_and_Xt": 0.0, "bwd_requantize": 0.0}
     for d, X, W, dY, Y, dX, dW, ws, sv in layer:
         df = qf.qlinear_desc(d.M, d.N, d.K, "nvfp4", "none", flags=qf.FLAG_DECODE_IN_GEMM)
+        d0 = qf.qlinear_desc(d.M, d.N, d.K, "nvfp4", "none")     # no workspace kept
         r = {"fwd_fused": _time(torch, lambda: qf.qlinear_fwd(df, X, W, Y, ws, saved=sv), reps, 2),
-             "fwd_materialized": _time(torch, lambda: qf.qlinear_fwd(d, X, W, Y, ws, saved=sv),
+             "fwd_materialized": _time(torch, lambda: qf.qlinear_fwd(d0, X, W, Y, ws, saved=sv),
                                        reps, 2),
-             "bwd_from_saved": _time(torch, lambda: qf.qlinear_bwd_ste(d, dY, X, W, dX, dW, ws,
+             "fwd_materialized_writing_Xt": _time(
+                 torch, lambda: qf.qlinear_fwd(d, X, W, Y, ws, saved=sv), reps, 2),
+             "bwd_from_saved": _time(torch, lambda: qf.qlinear_bwd_ste(d0, dY, X, W, dX, dW, ws,
                                                                        saved=sv), reps, 2),
-             "bwd_requantize": _time(torch, lambda: qf.qlinear_bwd_ste(d, dY, X, W, dX, dW, ws),
+             "bwd_from_saved_and_Xt": _time(
+                 torch, lambda: qf.qlinear_bwd_ste(d, dY, X, W, dX, dW, ws, saved=sv), reps, 2),
+             "bwd_requantize": _time(torch, lambda: qf.qlinear_bwd_ste(d0, dY, X, W, dX, dW, ws),
                                      reps, 2)}
         qf.qlinear_fwd(d, X, W, Y, ws, saved=sv)      # leave the saved buffer consistent
         for k in tot:

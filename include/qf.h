@@ -149,10 +149,13 @@ QF_API qf_status qf_fakequant_q4k_mse(const uint16_t* x, int64_t R, int64_t K, i
  * ------------------------------------------------------------------------------------ */
 
 /* flags */
-#define QF_FLAG_REUSE_WS 1u /* backward without a saved buffer: the workspace still holds the
-                               packed W_hat and the A_hat that a forward with no saved buffer
-                               wrote on the same X, W, desc (skips re-quantization; the bits are
-                               identical either way) */
+#define QF_FLAG_REUSE_WS 1u /* the caller keeps the workspace from the forward to the backward
+                               (same X, W, desc and flags).  The forward then also writes A_hat^T
+                               (X^T for unquantized activations) into it from the A tiles its
+                               GEMM stages (M % 8 == 0, N <= 8192), and the backward takes dW's
+                               operand from there instead of transposing or quantizing X; without a
+                               saved buffer it also takes the packed W_hat and A_hat from the
+                               workspace.  The bits are identical either way */
 #define QF_FLAG_DECODE_IN_GEMM 2u /* forward: decode the packed weight inside the GEMM's
                                prologue instead of writing W_hat in bf16 to the workspace and
                                running a plain bf16 GEMM (identical Y; K a multiple of 64, else

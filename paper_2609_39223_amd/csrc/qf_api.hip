@@ -295,6 +295,18 @@ bool fused_forward(const qf_qlinear_desc* d) {
          d->K % 64 == 0 && d->N > 0;
 }
 
+// Whether a forward with this descriptor leaves A_hat^T [K, ws_ld(M)] in the workspace (for a
+// QF_FLAG_REUSE_WS backward): the materialized forward on a token count that is a multiple of
+// 8 (the NT backward's case), with at most 32 output tile columns.  Writing A^T costs the
+// forward GEMM a few microseconds per round of tiles plus the pieces it writes; measured at 32K
+// tokens (same box) it saves 0.18 / 0.03 / 0.01 ms net for the 4096 x 12288, 4096 x 4096 and
+// 6144 x 4096 weights (16-24 tile columns) and loses 0.06 ms for the 24576 x 4096 one (96
+// columns, 48 rounds), where the backward's transpose (0.12 ms) is the cheaper route.
+bool forward_writes_at(const qf_qlinear_desc* d) {
+  return (d->flags & QF_FLAG_REUSE_WS) != 0 && !fused_forward(d) && d->M % 8 == 0 &&
+         ws_ld(d->M) < qf::kGemmAtMaxLd && (d->N + 255) / 256 <= 32;
+}
+
 qf_status linear_forward(const char* fn, const qf_qlinear_desc* d, const Dims& dm,
                          const uint16_t* X, const uint16_t* W, uint16_t* Y, const LinearWs& w,
                          const Packed& pw, const Packed* pa, hipStream_t s) {
@@ -319,8 +331,12 @@ qf_status linear_forward(const char* fn, const qf_qlinear_desc* d, const Dims& d
     return dev(qf::launch_gemm_nt_packed_b(d->M, d->N, d->K, Aop, lda_op, d->wfmt, pw.codes,
                                            pw.scales, pw.S, Y, dm.ldy, s),
                fn);
+  // With the workspace kept for the backward, the GEMM also writes A_hat^T (X^T when the
+  // activations are not quantized), the backward dW's right operand, from the A tiles it
+  // stages anyway.
+  const bool at = forward_writes_at(d);
   return dev(qf::launch_gemm_nt(d->M, d->N, d->K, Aop, lda_op, 0, Wop, ldw_op, 0, Y, dm.ldy, 0,
-                                nullptr, s),
+                                nullptr, s, at ? w.ahatt : nullptr, ws_ld(d->M)),
              fn);
 }
 
@@ -510,7 +526,7 @@ qf_status qf_qlinear_fwd_noalloc(const qf_qlinear_desc* d, const uint16_t* X, co
   QF_TRY(scratch_of_current_device(&base));
   char* p = static_cast<char*>(base);
   LinearWs w{};
-  w.scal = reinterpret_cast<float*>(p);   // the amax slot is rewritten (zero fill + max) per call
+  w.scal = reinterpret_cast<float*>(p);   // the amax slot is rewritten per call
   p += kAlign;
   if (d->wfmt != QF_FMT_NONE) { w.what = reinterpret_cast<uint16_t*>(p); p += up((size_t)d->N * d->K * 2); }
   if (d->afmt != QF_FMT_NONE) w.ahat = reinterpret_cast<uint16_t*>(p);
@@ -577,7 +593,9 @@ qf_status qf_qlinear_bwd_ste(const qf_qlinear_desc* d, const uint16_t* dY, const
       if (!dyt_by_dx)
         QF_TRY(dev(qf::launch_transpose_bf16(dY, d->M, d->N, dm.ldy, w.dyt, ldm, 1, 0, 0, s),
                    "transpose dY"));
-      if (d->afmt != QF_FMT_NONE && saved) {
+      if (forward_writes_at(d)) {
+        // A_hat^T is in the workspace already: the forward's GEMM wrote it
+      } else if (d->afmt != QF_FMT_NONE && saved) {
         QF_TRY(dev(qf::launch_dequant_t(d->afmt, sa.codes, sa.scales, sa.S, d->M, d->K, w.ahatt,
                                         ldm, s), "dequantize X (transposed)"));
       } else if (d->afmt != QF_FMT_NONE && !reuse) {

@@ -95,14 +95,13 @@ def test_gemm_strided_output_leaves_padding(qf):
 def _layer(qf, w, wfmt, afmt, flags=0, w_amax=None, a_amax=None, reuse=False):
     M, N, K = w["X"].shape[0], w["W"].shape[0], w["W"].shape[1]
     X, W, dY = to_dev(w["X"]), to_dev(w["W"]), to_dev(w["dY"])
-    d = qf.qlinear_desc(M, N, K, wfmt, afmt, w_amax=w_amax, a_amax=a_amax, flags=0)
+    # reuse: the workspace is kept from the forward to the backward (both calls carry the flag)
+    d = qf.qlinear_desc(M, N, K, wfmt, afmt, w_amax=w_amax, a_amax=a_amax,
+                        flags=qf.FLAG_REUSE_WS if reuse else 0)
     ws = qf.workspace(d)
     Y, dX = empty_bf16((M, N)), empty_bf16((M, K))
     dW = torch.empty(N, K, dtype=torch.float32, device="cuda")
     qf.qlinear_fwd(d, X, W, Y, ws)
-    if reuse:
-        d = qf.qlinear_desc(M, N, K, wfmt, afmt, w_amax=w_amax, a_amax=a_amax,
-                            flags=qf.FLAG_REUSE_WS)
     qf.qlinear_bwd_ste(d, dY, X, W, dX, dW, ws)
     torch.cuda.synchronize()
     return from_dev(Y), from_dev(dX), from_dev(dW)
@@ -423,8 +422,10 @@ def test_nt_gemm_pipeline_depths(qf):
                                            ("mxfp4", "none", 8, 256)])
 def test_transposing_quantizer_matches_saved_operands(qf, wfmt, afmt, M, K):
     """The backward quantizes W (and X) straight into the transposed NT operands; with
-    QF_FLAG_REUSE_WS it instead transposes the forward's saved x_hat.  Both routes feed the
-    same GEMMs, so dX and dW must agree bit for bit (ragged tiles in every direction)."""
+    QF_FLAG_REUSE_WS it takes W_hat^T from the workspace's packed W_hat and A_hat^T from the
+    forward GEMM, which wrote it from its staged A tiles (M = 8: from the transpose kernel).
+    Both routes feed the same GEMMs, so dX and dW must agree bit for bit (ragged tiles in every
+    direction)."""
     rng = np.random.default_rng(12)
     N = 264
     w = {"X": _rand_bf16(rng, (M, K)), "W": _rand_bf16(rng, (N, K), 0.02),
