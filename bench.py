@@ -493,6 +493,27 @@ def other_rows(qf, torch, dev, only=None):
             out[k]["tensor"] = f"{N}x{K}"
         del bufs, codes, sc16, sc32, packed, xh, tr
 
+    if want("single"):
+        # ---- the single NVFP4 linear (W 512x512, X 256x512): a latency-bound correctness shape --
+        w = workloads.single_linear(seed=0)
+        X1, W1, dY1 = (torch.from_numpy(w[k].view(np.int16)).to(dev) for k in ("X", "W", "dY"))
+        d1 = qf.qlinear_desc(256, 512, 512, "nvfp4", "none")
+        ws1, sv1 = qf.workspace(d1), qf.saved_buffer(d1)
+        Y1 = torch.empty(256, 512, dtype=torch.bfloat16, device=dev)
+        dX1 = torch.empty(256, 512, dtype=torch.bfloat16, device=dev)
+        dW1 = torch.empty(512, 512, dtype=torch.float32, device=dev)
+
+        def single_step():
+            qf.qlinear_fwd(d1, X1, W1, Y1, ws1, saved=sv1)
+            qf.qlinear_bwd_ste(d1, dY1, X1, W1, dX1, dW1, ws1, saved=sv1)
+
+        ms = _time(torch, single_step, reps=200, warm=20)
+        out["single_linear_nvfp4"] = {
+            "us": round(ms * 1e3, 2), "fwd_us": round(_time(
+                torch, lambda: qf.qlinear_fwd(d1, X1, W1, Y1, ws1, saved=sv1), 200, 20) * 1e3, 2),
+            "work": "X 256x512, W 512x512 NVFP4 (amax computed), fwd + STE bwd: 0.403 GFLOP; "
+                    "launch-latency bound"}
+
     if want("mlp_up"):
         # ---- the MXFP4 W4A4 MLP up-projection (8B-class) -------------------------------------
         out["mlp_up_mxfp4"] = mlp_up_row(qf, torch, dev)
