@@ -413,7 +413,7 @@ def mlp_up_row(qf, torch, dev):
             "roofline": {"bound": "mfma", "launch": dom, "achieved": round(achieved, 2),
                          "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                          "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                         "traffic": measured_traffic("gemm_nt_mlp_up_step_traffic.json", dom)},
+                         "traffic": None},       # HBM counters are kept for the headline workload
             "phases_ms": {p: round(float(per_phase[i]), 4) for i, p in enumerate(phases)},
             "work": "MXFP4 W4A4 MLP up-projection X 8192x4096, W 14336x4096, dY 8192x14336; "
                     "fwd + STE bwd (20 steps after 10 untimed)"}
