@@ -382,7 +382,13 @@ qf_status qf_fakequant_nvfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ld
     if (s_out) QF_TRY(dev(qf::launch_fill_f32(s_out, 1, 0.0f, s), "S"));
     return ok();
   }
-  QF_TRY(dev(qf::launch_nvfp4(x, R, K, ldx, amax, s_out, codes, scales, xhat, s), "nvfp4"));
+  // After this call's own amax pass, a tensor that fits the 256 MB last-level cache is still
+  // there: the quantizer then writes with non-temporal stores so its outputs do not evict it,
+  // and its read of x is served from the cache.  A tensor read from HBM anyway keeps plain
+  // stores, which are faster there.
+  const bool stream_out = amax_mode == QF_AMAX_COMPUTE && R * K * 2 <= (int64_t(160) << 20);
+  QF_TRY(dev(qf::launch_nvfp4(x, R, K, ldx, amax, s_out, codes, scales, xhat, s, stream_out),
+             "nvfp4"));
   return ok();
 }
 

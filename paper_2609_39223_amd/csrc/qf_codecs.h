@@ -68,13 +68,15 @@ __device__ __forceinline__ float e2m1_value(uint32_t m) {
 
 // OCP E4M3 ("FN", bias 7, max 448) code of t >= 0: round to nearest even, saturating at
 // 448 (code 0x7E); NaN -> 0x7F.
+// Both candidate codes are formed and one is selected (no branch).
 __device__ __forceinline__ uint32_t e4m3_code(float t) {
-  if (!(t < 448.0f)) return t != t ? 0x7Fu : 0x7Eu;
-  if (t < 0x1p-6f) return (uint32_t)__builtin_rintf(t * 512.0f);   // subnormals m * 2^-9
-  uint32_t u = as_u32(t);
-  uint32_t r = u + 0x7FFFFu + ((u >> 20) & 1u);
-  uint32_t c = (r >> 20) - (120u << 3);
-  return c < 0x7Eu ? c : 0x7Eu;
+  const uint32_t sub = (uint32_t)__builtin_rintf(t * 512.0f);     // subnormals m * 2^-9
+  const uint32_t u = as_u32(t);
+  const uint32_t r = u + 0x7FFFFu + ((u >> 20) & 1u);
+  uint32_t c = (r >> 20) - (120u << 3);                              // normals
+  c = c < 0x7Eu ? c : 0x7Eu;
+  c = t < 0x1p-6f ? sub : c;
+  return t < 448.0f ? c : (t != t ? 0x7Fu : 0x7Eu);
 }
 
 __device__ __forceinline__ float e4m3_value(uint32_t c) {
@@ -241,41 +243,100 @@ __device__ __forceinline__ void q4k_decode8(const uint32_t qw[2], float t1, floa
   q4k_decode8f(qf, t1, t2, w);
 }
 
-// NVFP4 (16-block = this lane and lane ^ 1): 4-bit codes cw (element k in nibble k), E4M3
-// block scale sc, x_hat bits xh.  S is the FP32 tensor scale g / (6 * 448), six_s = 6 S.
-__device__ __forceinline__ void nvfp4_chunk(const uint32_t h[8], float S, float six_s,
-                                            uint32_t& cw, uint32_t& sc, uint32_t xh[8]) {
-  uint32_t ab = max_abs_bits8(h);
+// The block decode scale D = fl(S * s_E4M3) of every E4M3 code under one tensor scale S, with
+// its reciprocal fl(1 / D) (0 where D = 0), as the NVFP4 encoder uses them: computed per call
+// (Nvfp4Direct), or read from a 128-entry table of all codes (Nvfp4Table) that a workgroup
+// fills once with nvfp4_fill_table (same operations, so the same values).
+__device__ __forceinline__ f32x2_t nvfp4_scale_pair(float S, uint32_t sc) {
+  const float D = nvfp4_block_scale(S, sc);
+  return f32x2_t{D, D != 0.0f ? 1.0f / D : 0.0f};
+}
+struct Nvfp4Direct {
+  float S;
+  __device__ __forceinline__ f32x2_t operator()(uint32_t sc) const { return nvfp4_scale_pair(S, sc); }
+};
+struct Nvfp4Table {
+  const f32x2_t* tab;                       // 128 entries (codes 0x00..0x7F), LDS
+  __device__ __forceinline__ f32x2_t operator()(uint32_t sc) const { return tab[sc]; }
+};
+// Threads 0..127 of a workgroup each write one entry; the caller synchronizes before use.
+__device__ __forceinline__ void nvfp4_fill_table(float S, f32x2_t* tab, int t) {
+  if (t < 128) tab[t] = nvfp4_scale_pair(S, (uint32_t)t);
+}
+
+// NVFP4 steps for a 16-block held by this lane and lane ^ 1 (both lanes call each step):
+// the block's max |x| as bf16 magnitude bits ...
+__device__ __forceinline__ uint32_t nvfp4_block_max(const uint32_t h[8]) {
+  const uint32_t ab = max_abs_bits8(h);
   const uint32_t o = xor1_u32(ab);         // partner lane holds the other 8 of the 16-block
-  ab = o > ab ? o : ab;
-  sc = 0;
-  if (S != 0.0f) {
-    const float t = as_f32(ab << 16) / six_s;   // t_b = a_b / (6 S)
-    sc = e4m3_code(t);
-  }
-  const float D = nvfp4_block_scale(S, sc); // block decode scale s_FP32 * s_E4M3,b
-  const float rcp = D != 0.0f ? 1.0f / D : 0.0f;
-  // magnitude codes of fl(|x| * rcp) (scale 2^0), then the sign bit of each input; D = 0
-  // gives magnitude 0 for every element (also for Inf / NaN inputs under a caller's g = 0)
-  uint32_t mc = 0;
-#pragma unroll
-  for (int p = 0; p < 4; ++p) {
-    const float v0 = as_f32((h[2 * p] & 0x7FFFu) << 16) * rcp;
-    const float v1 = as_f32((h[2 * p + 1] & 0x7FFFu) << 16) * rcp;
-    const uint32_t c2 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, v0, v1, 1.0f, 0);
-    mc |= (c2 & 0xFFu) << (8 * p);
-  }
-  if (D == 0.0f) mc = 0;
-  cw = mc;                                  // magnitudes leave bit 3 of each nibble clear
-#pragma unroll
-  for (int k = 0; k < 8; ++k) cw |= (h[k] >> 15) << (4 * k + 3);
+  return o > ab ? o : ab;
+}
+// ... its E4M3 scale code from t_b = a_b / (6 S) (S is the FP32 tensor scale g / (6 * 448),
+// six_s = 6 S; S = 0 gives code 0) ...
+__device__ __forceinline__ uint32_t nvfp4_scale_code(uint32_t ab, float S, float six_s) {
+  return S != 0.0f ? e4m3_code(as_f32(ab << 16) / six_s) : 0u;
+}
+// ... and the 4-bit codes cw (element k in nibble k) and x_hat bits xh of this lane's 8
+// elements h under scale code sc, with bs(sc) giving the block's (D, 1 / D).
+template <class BlockScale>
+__device__ __forceinline__ void nvfp4_encode(const uint32_t h[8], uint32_t ab, uint32_t sc,
+                                             const BlockScale& bs, uint32_t& cw, uint32_t xh[8]) {
+  const f32x2_t dr = bs(sc);
+  const float D = dr.x, rcp = dr.y;         // block decode scale s_FP32 * s_E4M3,b, 1 / D
+  const uint32_t w[4] = {h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                         h[6] | (h[7] << 16)};
   uint32_t p[4];
-  nvfp4_decode8(cw, D, p);
+  if (ab < 0x7F80u && __builtin_isfinite(rcp) && __builtin_isfinite(D)) {
+    // A finite block under a finite reciprocal (0 when D = 0): fl(x * rcp) is the signed
+    // fl(|x| * rcp) (-0 for x = -0), and the conversion copies the sign bit, so each code is
+    // the sign of x over the magnitude code of fl(|x| * rcp), as defined.
+    uint32_t c = 0;
+    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, as_f32(w[0] << 16) * rcp,
+                                                 as_f32(w[0] & 0xFFFF0000u) * rcp, 1.0f, 0);
+    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, as_f32(w[1] << 16) * rcp,
+                                                 as_f32(w[1] & 0xFFFF0000u) * rcp, 1.0f, 1);
+    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, as_f32(w[2] << 16) * rcp,
+                                                 as_f32(w[2] & 0xFFFF0000u) * rcp, 1.0f, 2);
+    c = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(c, as_f32(w[3] << 16) * rcp,
+                                                 as_f32(w[3] & 0xFFFF0000u) * rcp, 1.0f, 3);
+    cw = c;
+    nvfp4_decode8_finite(cw, D, p);
+  } else {
+    // magnitude codes of fl(|x| * rcp) (scale 2^0), then the sign bit of each input; D = 0
+    // gives magnitude 0 for every element (also for Inf / NaN inputs under a caller's g = 0)
+    uint32_t mc = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float v0 = as_f32((h[2 * q] & 0x7FFFu) << 16) * rcp;
+      const float v1 = as_f32((h[2 * q + 1] & 0x7FFFu) << 16) * rcp;
+      const uint32_t c2 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, v0, v1, 1.0f, 0);
+      mc |= (c2 & 0xFFu) << (8 * q);
+    }
+    if (D == 0.0f) mc = 0;
+    cw = mc;                                // magnitudes leave bit 3 of each nibble clear
+#pragma unroll
+    for (int k = 0; k < 8; ++k) cw |= (h[k] >> 15) << (4 * k + 3);
+    nvfp4_decode8(cw, D, p);
+  }
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     xh[2 * q] = p[q] & 0xFFFFu;
     xh[2 * q + 1] = p[q] >> 16;
   }
+}
+
+// NVFP4 of one chunk: codes cw, E4M3 block scale sc, x_hat bits xh.
+template <class BlockScale>
+__device__ __forceinline__ void nvfp4_chunk(const uint32_t h[8], float S, float six_s,
+                                            const BlockScale& bs, uint32_t& cw, uint32_t& sc,
+                                            uint32_t xh[8]) {
+  const uint32_t ab = nvfp4_block_max(h);
+  sc = nvfp4_scale_code(ab, S, six_s);
+  nvfp4_encode(h, ab, sc, bs, cw, xh);
+}
+__device__ __forceinline__ void nvfp4_chunk(const uint32_t h[8], float S, float six_s,
+                                            uint32_t& cw, uint32_t& sc, uint32_t xh[8]) {
+  nvfp4_chunk(h, S, six_s, Nvfp4Direct{S}, cw, sc, xh);
 }
 
 // MXFP4 (32-block = the 4 lanes of a quad): codes cw, E8M0 scale code e (0xFF for a block

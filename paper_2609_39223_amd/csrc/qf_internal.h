@@ -14,10 +14,12 @@ hipError_t launch_fill_f32(float* p, int64_t n, float v, hipStream_t s);
 // clearing kernel before it (an empty tensor: a one-element fill unless accumulating).
 hipError_t launch_amax(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, float* amax,
                        bool accumulate, hipStream_t s);
-// g: device scalar holding the tensor amax to use; s_out may be null.
+// g: device scalar holding the tensor amax to use; s_out may be null.  stream_out: write the
+// outputs with non-temporal stores (for a call right after an amax pass over the same input
+// that fits the last-level cache, whose lines the outputs then do not evict).
 hipError_t launch_nvfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, const float* g,
                         float* s_out, uint8_t* codes, uint8_t* scales, uint16_t* xhat,
-                        hipStream_t s);
+                        hipStream_t s, bool stream_out = false);
 hipError_t launch_mxfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, uint8_t* codes,
                         uint8_t* scales, uint16_t* xhat, hipStream_t s);
 hipError_t launch_q4k(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, uint8_t* packed,

@@ -171,10 +171,26 @@ __global__ __launch_bounds__(kThreads) void amax_rows_kernel(const uint16_t* __r
   amax_block_fold(m, slot, gridDim.x * gridDim.y, amax, accumulate);
 }
 
+// Plain or non-temporal stores of 4 and 16 bytes (aligned).
+template <bool NT>
+__device__ __forceinline__ void store_u32(void* p, uint32_t v) {
+  if (NT) __builtin_nontemporal_store(v, reinterpret_cast<uint32_t*>(p));
+  else *reinterpret_cast<uint32_t*>(p) = v;
+}
+template <bool NT>
+__device__ __forceinline__ void store_u128(void* p, uint4 v) {
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  if (NT) __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w}, reinterpret_cast<u32x4*>(p));
+  else *reinterpret_cast<uint4*>(p) = v;
+}
+
 // ============================================================================= NVFP4
 // grid.z indexes batched tensors (expert weights): tensor z uses g[z] and element offset
 // z * tstride (input) / z * R * K (outputs).
-template <int RPT>
+// STREAM: the outputs are written with non-temporal stores, which do not allocate in the
+// last-level cache, so an input read just before (by the amax pass) stays there for this
+// kernel's read.
+template <int RPT, bool STREAM>
 __global__ __launch_bounds__(kThreads) void nvfp4_kernel(
     const uint16_t* __restrict__ x, int64_t R, int64_t K, int64_t ldx, int64_t tstride,
     const float* __restrict__ gptr, float* __restrict__ s_out, uint8_t* __restrict__ codes,
@@ -196,17 +212,55 @@ __global__ __launch_bounds__(kThreads) void nvfp4_kernel(
     vin[i] = make_uint4(0, 0, 0, 0);
     if (col_ok && r < R) vin[i] = *reinterpret_cast<const uint4*>(xt + r * ldx + c * 8);
   }
+  __shared__ f32x2_t tab[128];              // (D, 1 / D) of every E4M3 code under this S
+  nvfp4_fill_table(S, tab, threadIdx.x);
+  __syncthreads();
+  const Nvfp4Table bs{tab};
+  // The two lanes of a block pair split the scale codes: the even lane encodes rows 0, 2, ..
+  // and the odd lane rows 1, 3, .. of this thread's RPT, and each takes the other's over DPP.
+  static_assert(RPT % 2 == 0, "rows are taken in pairs");
+  // With K a multiple of 64 each group of 8 lanes (4 blocks) lies wholly inside or outside a
+  // row and its 4 scale bytes start at a multiple of 4 (for an aligned scales pointer): one
+  // word store per group; otherwise one byte per block.
+  const bool wide_scales = scales && (K & 63) == 0 && (reinterpret_cast<uintptr_t>(scales) & 3) == 0;
+  const bool odd = (threadIdx.x & 1) != 0;
+  const uint32_t odd_mask = 0u - (threadIdx.x & 1u);
+  uint32_t ab[RPT], scs[RPT];
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    uint32_t h[8];
+    unpack8(vin[i], h);
+    ab[i] = nvfp4_block_max(h);
+  }
+#pragma unroll
+  for (int i = 0; i < RPT; i += 2) {
+    // (a mask select: a conditional on the array index would put ab[] in memory)
+    const uint32_t a = ab[i] ^ ((ab[i] ^ ab[i + 1]) & odd_mask);
+    const uint32_t mine = nvfp4_scale_code(a, S, six_s);
+    const uint32_t theirs = xor1_u32(mine);
+    scs[i] = odd ? theirs : mine;
+    scs[i + 1] = odd ? mine : theirs;
+  }
 #pragma unroll
   for (int i = 0; i < RPT; ++i) {
     const int64_t r = (int64_t)blockIdx.y * RPT + i;
     const bool ok = col_ok && r < R;
-    uint32_t h[8], cw, sc, xh[8];
+    uint32_t h[8], cw, xh[8];
+    const uint32_t sc = scs[i];
     unpack8(vin[i], h);
-    nvfp4_chunk(h, S, six_s, cw, sc, xh);
+    nvfp4_encode(h, ab[i], sc, bs, cw, xh);
+    // lane 8j gathers the scale bytes of its 4 blocks (lanes 8j, +2, +4, +6) into one word
+    uint32_t s4 = sc | (xor2_u32(sc) << 8);
+    s4 |= xor_swz_u32<4>(s4) << 16;
     if (ok) {
-      if (codes) *reinterpret_cast<uint32_t*>(codes + obase / 2 + r * (K / 2) + c * 4) = cw;
-      if (scales && (c & 1) == 0) scales[obase / 16 + r * (K / 16) + c / 2] = (uint8_t)sc;
-      if (xhat) *reinterpret_cast<uint4*>(xhat + obase + r * K + c * 8) = pack8(xh);
+      if (codes) store_u32<STREAM>(codes + obase / 2 + r * (K / 2) + c * 4, cw);
+      uint8_t* srow = scales + obase / 16 + r * (K / 16);
+      if (wide_scales) {
+        if ((c & 7) == 0) store_u32<STREAM>(srow + c / 2, s4);
+      } else if (scales && (c & 1) == 0) {
+        srow[c / 2] = (uint8_t)sc;
+      }
+      if (xhat) store_u128<STREAM>(xhat + obase + r * K + c * 8, pack8(xh));
     }
   }
 }
@@ -510,14 +564,16 @@ constexpr int kRowsPerThread = 4;
 
 hipError_t launch_nvfp4(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, const float* g,
                         float* s_out, uint8_t* codes, uint8_t* scales, uint16_t* xhat,
-                        hipStream_t s) {
-  if (R == 0 || K == 0) {
-    if (s_out) return hipSuccess;  // nothing to quantize; S is left to the caller
-    return hipSuccess;
-  }
-  hipLaunchKernelGGL(nvfp4_kernel<kRowsPerThread>, row_grid(R, K, kRowsPerThread),
-                     dim3(kThreads), 0, s, x, R, K, ldx, (int64_t)0, g, s_out, codes, scales,
-                     xhat);
+                        hipStream_t s, bool stream_out) {
+  if (R == 0 || K == 0) return hipSuccess;  // nothing to quantize; S is left to the caller
+  if (stream_out)
+    hipLaunchKernelGGL((nvfp4_kernel<kRowsPerThread, true>), row_grid(R, K, kRowsPerThread),
+                       dim3(kThreads), 0, s, x, R, K, ldx, (int64_t)0, g, s_out, codes, scales,
+                       xhat);
+  else
+    hipLaunchKernelGGL((nvfp4_kernel<kRowsPerThread, false>), row_grid(R, K, kRowsPerThread),
+                       dim3(kThreads), 0, s, x, R, K, ldx, (int64_t)0, g, s_out, codes, scales,
+                       xhat);
   return hipGetLastError();
 }
 
@@ -532,7 +588,7 @@ hipError_t launch_nvfp4_batched(const uint16_t* x, int64_t E, int64_t R, int64_t
   contiguous_row_view(R, K);
   dim3 grid = row_grid(R, K, kRowsPerThread);
   grid.z = (unsigned)E;
-  hipLaunchKernelGGL(nvfp4_kernel<kRowsPerThread>, grid, dim3(kThreads), 0, s, x, R, K, K,
+  hipLaunchKernelGGL((nvfp4_kernel<kRowsPerThread, false>), grid, dim3(kThreads), 0, s, x, R, K, K,
                      R * K, g, s_out, codes, scales, xhat);
   return hipGetLastError();
 }
