@@ -649,6 +649,18 @@ constexpr int kTR = 64, kTC = 256;
 
 __device__ __forceinline__ int tslot(int r, int c) { return c ^ (((r >> 3) & 7) << 1); }
 
+// Output row j (0..7) of the transposed 8 x 8 block of 16-bit values whose input row i is
+// w[i] (element 2q + h in half h of word q): word d holds input rows 2d and 2d + 1.
+__device__ __forceinline__ uint4 block_row_transposed(const uint32_t w[8][4], int j) {
+  uint32_t o[4];
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    const uint32_t lo = w[2 * d][j >> 1], hi = w[2 * d + 1][j >> 1];
+    o[d] = __builtin_amdgcn_perm(hi, lo, (j & 1) ? 0x07060302u : 0x05040100u);
+  }
+  return make_uint4(o[0], o[1], o[2], o[3]);
+}
+
 // out[c0 + k][oc0 + r] = tile(r, k) for the 64 x 256 tile in LDS (after a barrier); output rows
 // at or past K and output columns at or past col_end are skipped (both multiples of 8).
 __device__ __forceinline__ void store_tile_transposed(const uint4* tile, int t, uint16_t* out,
@@ -667,14 +679,26 @@ __device__ __forceinline__ void store_tile_transposed(const uint4* tile, int t, 
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     if (orow0 + j >= K) break;
-    uint32_t o[4];
-#pragma unroll
-    for (int d = 0; d < 4; ++d) {
-      const uint32_t lo = w[2 * d][j >> 1], hi = w[2 * d + 1][j >> 1];
-      o[d] = (j & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
-    }
-    *reinterpret_cast<uint4*>(out + (orow0 + j) * ldo + ocol) = make_uint4(o[0], o[1], o[2], o[3]);
+    *reinterpret_cast<uint4*>(out + (orow0 + j) * ldo + ocol) = block_row_transposed(w, j);
   }
+}
+
+// Tile origin of the grouped transposes (64-row tiles, grid.y = y): expert e's rows
+// [off[e], off[e+1]) go to the 64-aligned output columns starting at 64 kstart[e], so tile y
+// reads input rows [r0, r_end) and writes output columns from oc0 (the columns past the
+// expert's last row as zeros).  False for the tiles past the last expert's (uniform per block).
+__device__ __forceinline__ bool grouped_tile(int y, const int64_t* off, const int* kstart, int E,
+                                             int64_t& r0, int64_t& r_end, int64_t& oc0) {
+  if (y >= kstart[E]) return false;
+  int lo = 0, hi = E;                            // kstart[e] <= y < kstart[e+1]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (kstart[mid] <= y) lo = mid; else hi = mid;
+  }
+  r0 = off[lo] + (int64_t)(y - kstart[lo]) * kTR;
+  r_end = off[lo + 1];
+  oc0 = (int64_t)y * kTR;
+  return true;
 }
 
 }  // namespace codec

@@ -346,20 +346,7 @@ __global__ __launch_bounds__(kThreads) void quant_t_kernel(const uint16_t* __res
   const int64_t c0 = (int64_t)blockIdx.x * kTC;
   // Input rows [r0, r_end) of this tile; output columns start at oc0.
   int64_t r0 = (int64_t)blockIdx.y * kTR, r_end = R, oc0 = r0;
-  if (GROUPED) {
-    // Expert e's rows [off[e], off[e+1]) go to the 64-aligned output columns starting at
-    // 64 kstart[e]; the columns past its last row are written as zeros.
-    const int y = blockIdx.y;
-    if (y >= kstart[E]) return;                  // uniform over the block
-    int lo = 0, hi = E;                          // kstart[e] <= y < kstart[e+1]
-    while (hi - lo > 1) {
-      const int mid = (lo + hi) >> 1;
-      if (kstart[mid] <= y) lo = mid; else hi = mid;
-    }
-    r0 = off[lo] + (int64_t)(y - kstart[lo]) * kTR;
-    r_end = off[lo + 1];
-    oc0 = (int64_t)y * kTR;
-  }
+  if (GROUPED && !grouped_tile(blockIdx.y, off, kstart, E, r0, r_end, oc0)) return;
   x += (int64_t)blockIdx.z * xbs;
   out += (int64_t)blockIdx.z * obs;
   float S = 0.0f, six_s = 0.0f;
@@ -622,13 +609,15 @@ hipError_t launch_quant_t_impl(int fmt, const uint16_t* x, int64_t R, int64_t K,
                                int64_t batch, int64_t xbs, const float* g, uint16_t* out,
                                int64_t ldo, int64_t obs, const int64_t* off, const int* kstart,
                                int E, int64_t ytiles, hipStream_t s) {
+  if (fmt == QF_FMT_NONE)                   // plain transposes: the register-only form
+    return GROUPED ? launch_transpose_grouped(x, R, K, off, kstart, E, ytiles, out, ldo, s)
+                   : launch_transpose_bf16(x, R, K, ldx, out, ldo, batch, xbs, obs, s);
   const dim3 grid((unsigned)((K + kTC - 1) / kTC), (unsigned)ytiles, (unsigned)batch);
   switch (fmt) {
 #define QF_QT(F)                                                                            \
   hipLaunchKernelGGL((quant_t_kernel<F, GROUPED>), grid, dim3(kThreads), 0, s, x, R, K, ldx, \
                      xbs, g, out, ldo, obs, off, kstart, E);                                 \
   break;
-    case QF_FMT_NONE: QF_QT(QF_FMT_NONE)
     case QF_FMT_NVFP4: QF_QT(QF_FMT_NVFP4)
     case QF_FMT_MXFP4: QF_QT(QF_FMT_MXFP4)
     case QF_FMT_Q4K: QF_QT(QF_FMT_Q4K)
