@@ -303,12 +303,16 @@ __device__ __forceinline__ void nvfp4_encode(const uint32_t h[8], uint32_t ab, u
     nvfp4_decode8_finite(cw, D, p);
   } else {
     // magnitude codes of fl(|x| * rcp) (scale 2^0), then the sign bit of each input; D = 0
-    // gives magnitude 0 for every element (also for Inf / NaN inputs under a caller's g = 0)
+    // gives magnitude 0 for every element (also for Inf / NaN inputs under a caller's g = 0).
+    // A NaN product (a NaN input, or 0 * Inf where fl(1 / D) overflows for a D below 2^-128)
+    // encodes magnitude 0: no E2M1 value is nearest to it (the conversion would give 7).
     uint32_t mc = 0;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const float v0 = as_f32((h[2 * q] & 0x7FFFu) << 16) * rcp;
-      const float v1 = as_f32((h[2 * q + 1] & 0x7FFFu) << 16) * rcp;
+      float v0 = as_f32((h[2 * q] & 0x7FFFu) << 16) * rcp;
+      float v1 = as_f32((h[2 * q + 1] & 0x7FFFu) << 16) * rcp;
+      v0 = v0 != v0 ? 0.0f : v0;
+      v1 = v1 != v1 ? 0.0f : v1;
       const uint32_t c2 = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, v0, v1, 1.0f, 0);
       mc |= (c2 & 0xFFu) << (8 * q);
     }

@@ -138,6 +138,23 @@ def test_nvfp4_wide_range_ragged_and_amax(qf):
             assert got["S"] == want["S"] and got["amax"] == oracle.amax(x)
 
 
+def test_nvfp4_scales_whose_reciprocal_overflows(qf):
+    """Block decode scales below 2^-128 (tensor amax among the float denormals, computed from a
+    tensor of bf16 denormals or supplied by the caller): fl(1 / D) overflows, zeros scale to
+    0 * Inf and encode as magnitude 0 as the oracle's nearest-value rule gives; every other
+    element saturates at 6."""
+    v = np.arange(0x80, dtype=np.uint16)                  # +0, the positive bf16 denormals
+    x = np.concatenate([v, v | 0x8000]).reshape(-1, 64)   # and their negatives (-0 included)
+    got, want = run_nvfp4(qf, x), oracle.nvfp4(x)
+    assert_same(got, want, ("codes", "scales", "xhat"), "nvfp4 denormal tensor")
+    assert got["S"] == want["S"] and got["amax"] == oracle.amax(x)
+    xf = all_bf16_blocks(16, finite_only=True, seed=5).reshape(-1, 64)[:256]
+    for g in [1.0e-39, 1.0e-41, 3.0e-44, 1.4e-45]:
+        g32 = float(np.float32(g))
+        assert_same(run_nvfp4(qf, xf, amax_in=g32), oracle.nvfp4(xf, amax_in=g32),
+                    ("codes", "scales", "xhat"), f"nvfp4 g={g}")
+
+
 def test_nvfp4_zero_tensor(qf):
     x = np.zeros((4, 64), np.uint16)
     x[2, 5] = 0x8000
