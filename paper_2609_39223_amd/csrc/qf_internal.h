@@ -116,12 +116,6 @@ hipError_t launch_grouped_nt_rows(int64_t E, int64_t T, int64_t N, int64_t K, co
 hipError_t launch_transpose_bf16(const uint16_t* in, int64_t R, int64_t C, int64_t ldi,
                                  uint16_t* out, int64_t ldo, int64_t batch, int64_t ibs,
                                  int64_t obs, hipStream_t s);
-// Grouped bf16 transpose (qf_transpose.hip) into the padded layout of the grouped weight
-// gradient: out[k][64 kstart[e] + i] = x[off[e] + i][k] (x: [T][K] contiguous), zeros up to
-// 64 kstart[e+1]; ytiles >= kstart[E] 64-row tiles are launched (the rest exit).
-hipError_t launch_transpose_grouped(const uint16_t* x, int64_t T, int64_t K, const int64_t* off,
-                                    const int* kstart, int E, int64_t ytiles, uint16_t* out,
-                                    int64_t ldo, hipStream_t s);
 
 // Grouped over experts (qf_grouped.hip; rows [off[e], off[e+1]) of the token-major operands belong to
 // expert e; the host never reads off).  launch_grouped_prep fills small device arrays:

@@ -609,15 +609,17 @@ hipError_t launch_quant_t_impl(int fmt, const uint16_t* x, int64_t R, int64_t K,
                                int64_t batch, int64_t xbs, const float* g, uint16_t* out,
                                int64_t ldo, int64_t obs, const int64_t* off, const int* kstart,
                                int E, int64_t ytiles, hipStream_t s) {
-  if (fmt == QF_FMT_NONE)                   // plain transposes: the register-only form
-    return GROUPED ? launch_transpose_grouped(x, R, K, off, kstart, E, ytiles, out, ldo, s)
-                   : launch_transpose_bf16(x, R, K, ldx, out, ldo, batch, xbs, obs, s);
+  // Plain dense transposes take the register-only form; the grouped ones (expert rows padded
+  // to 64) keep the LDS tile, faster there (600 against 625 us for 262144 x 3072).
+  if (fmt == QF_FMT_NONE && !GROUPED)
+    return launch_transpose_bf16(x, R, K, ldx, out, ldo, batch, xbs, obs, s);
   const dim3 grid((unsigned)((K + kTC - 1) / kTC), (unsigned)ytiles, (unsigned)batch);
   switch (fmt) {
 #define QF_QT(F)                                                                            \
   hipLaunchKernelGGL((quant_t_kernel<F, GROUPED>), grid, dim3(kThreads), 0, s, x, R, K, ldx, \
                      xbs, g, out, ldo, obs, off, kstart, E);                                 \
   break;
+    case QF_FMT_NONE: QF_QT(QF_FMT_NONE)
     case QF_FMT_NVFP4: QF_QT(QF_FMT_NVFP4)
     case QF_FMT_MXFP4: QF_QT(QF_FMT_MXFP4)
     case QF_FMT_Q4K: QF_QT(QF_FMT_Q4K)

@@ -1,5 +1,4 @@
-// bf16 matrix transposes for gfx950: out[c][r] = in[r][c], batched, and the grouped form that
-// lays each expert's rows out as the 64-aligned column range of the grouped weight gradient.
+// bf16 matrix transpose for gfx950: out[c][r] = in[r][c], optionally batched.
 //
 // The backward GEMMs of the quantization-aware layer run in NT form, which needs dY^T and the
 // transposed operands.  Register-only form, no LDS: a 256-thread workgroup covers a 64 x 256
@@ -8,7 +7,9 @@
 // block in registers and writes it as 8 output rows of 16 bytes (the 8 lanes with the same b
 // write 128 contiguous bytes of each).  Non-temporal stores: the output is not read again by
 // the launch.  Tile shapes from 32 x 512 to 256 x 256 through LDS (eight variants) measured
-// 47-58 us at 14336 x 4096 against 47.5 us for this form, which needs no barrier.
+// 47-58 us at 14336 x 4096 against 47.5 us for this form, which needs no barrier.  (The grouped
+// transposes of the expert layer keep the LDS tile of the transposing quantizer: this form
+// measured 625 against 600 us there.)
 // R and C must be multiples of 8 (16-byte chunks).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -60,14 +61,6 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(const uint16_t* __r
                  out + (int64_t)blockIdx.z * obs, ldo, r0, R);
 }
 
-__global__ __launch_bounds__(256) void transpose_grouped_kernel(
-    const uint16_t* __restrict__ x, int64_t K, const int64_t* __restrict__ off,
-    const int* __restrict__ kstart, int E, uint16_t* __restrict__ out, int64_t ldo) {
-  int64_t r0, r_end, oc0;
-  if (!grouped_tile(blockIdx.y, off, kstart, E, r0, r_end, oc0)) return;
-  transpose_tile(x, K, r0, r_end, (int64_t)blockIdx.x * kTC, K, out, ldo, oc0, INT64_MAX);
-}
-
 }  // namespace
 
 hipError_t launch_transpose_bf16(const uint16_t* in, int64_t R, int64_t C, int64_t ldi,
@@ -78,16 +71,6 @@ hipError_t launch_transpose_bf16(const uint16_t* in, int64_t R, int64_t C, int64
                   (unsigned)batch);
   hipLaunchKernelGGL(transpose_bf16_kernel, grid, dim3(256), 0, s, in, R, C, ldi, out, ldo, ibs,
                      obs);
-  return hipGetLastError();
-}
-
-hipError_t launch_transpose_grouped(const uint16_t* x, int64_t T, int64_t K, const int64_t* off,
-                                    const int* kstart, int E, int64_t ytiles, uint16_t* out,
-                                    int64_t ldo, hipStream_t s) {
-  if (T == 0 || K == 0 || E == 0) return hipSuccess;
-  const dim3 grid((unsigned)((K + kTC - 1) / kTC), (unsigned)ytiles, 1);
-  hipLaunchKernelGGL(transpose_grouped_kernel, grid, dim3(256), 0, s, x, K, off, kstart, E, out,
-                     ldo);
   return hipGetLastError();
 }
 
