@@ -508,11 +508,30 @@ def other_rows(qf, torch, dev, only=None):
             qf.qlinear_bwd_ste(d1, dY1, X1, W1, dX1, dW1, ws1, saved=sv1)
 
         ms = _time(torch, single_step, reps=200, warm=20)
+        # the same calls captured once in a HIP graph and replayed (the launch floor); the
+        # replay's outputs are checked against the eager calls' first
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            single_step()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        ref = (Y1.clone(), dX1.clone(), dW1.clone())
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            single_step()
+        graph.replay()
+        torch.cuda.synchronize()
+        same = all(torch.equal(a, b) for a, b in zip(ref, (Y1, dX1, dW1)))
+        gms = _time(torch, graph.replay, reps=500, warm=20)
         out["single_linear_nvfp4"] = {
             "us": round(ms * 1e3, 2), "fwd_us": round(_time(
                 torch, lambda: qf.qlinear_fwd(d1, X1, W1, Y1, ws1, saved=sv1), 200, 20) * 1e3, 2),
+            "graph_us": round(gms * 1e3, 2), "graph_matches_eager": same,
             "work": "X 256x512, W 512x512 NVFP4 (amax computed), fwd + STE bwd: 0.403 GFLOP; "
-                    "launch-latency bound"}
+                    "bound by its chain of small dependent kernels on the GPU (graph_us: the same "
+                    "calls replayed from a HIP graph, no faster, so not by host launches)"}
+        del graph
 
     if want("mlp_up"):
         # ---- the MXFP4 W4A4 MLP up-projection (8B-class) -------------------------------------
