@@ -53,7 +53,7 @@ def parse():
                         "(dispatch order = phase order; used for the HBM counter runs)")
     p.add_argument("--rows", default=None,
                    help="run only these secondary row groups (comma-separated: mlp_up, quant, "
-                        "moe, lora, moe_lora, kl, q4k) and print them as one JSON object; no "
+                        "moe, lora, moe_lora, kl, q4k, single, blas) and print them as one JSON object; no "
                         "headline step (used for per-row kernel traces)")
     p.add_argument("--copy-calibration", action="store_true",
                    help="only run a plain 1 GiB device-to-device copy (reference for the "
@@ -641,6 +641,27 @@ def other_rows(qf, torch, dev, only=None):
             "forward_ms": round(ms_fwd, 4),
             "forward_TFLOPs": round(2.0 * 4096 * N * K / (ms_fwd * 1e-3) / 1e12, 1),
             "work": "W 14336x4096 (per-row log-normal scale) -> 144-byte blocks; Y = X Q(W)^T, X 4096x4096"}
+
+    if want("blas"):
+        # ---- context: this library's NT GEMM against hipBLASLt (torch's F.linear) on the 9B
+        # layer's forward shapes and the MLP up shape, same operands, same run -------------------
+        import torch.nn.functional as F
+        shapes = {"qkv": (32768, 6144, 4096), "o": (32768, 4096, 4096), "gate_up": (32768, 24576, 4096),
+                  "down": (32768, 4096, 12288), "mlp_up": (8192, 14336, 4096)}
+        ctx = {}
+        for name, (M, Nn, Kk) in shapes.items():
+            A = _randn_bf16(torch, gen, (M, Kk))
+            B = _randn_bf16(torch, gen, (Nn, Kk), 0.02)
+            C = torch.empty(M, Nn, dtype=torch.bfloat16, device=dev)
+            ws = qf.gemm_workspace(M, Nn, 0)
+            ours = _time(torch, lambda: qf.gemm_bf16(M, Nn, Kk, A, Kk, 1, B, Kk, 1, C, Nn, 0, ws=ws), reps=10, warm=3)
+            blas = _time(torch, lambda: F.linear(A, B), reps=10, warm=3)
+            f = 2.0 * M * Nn * Kk
+            ctx[name] = {"shape": f"{M}x{Nn}x{Kk}", "ours_ms": round(ours, 4), "hipblaslt_ms": round(blas, 4),
+                         "ours_TFLOPs": round(f / (ours * 1e-3) / 1e12, 1),
+                         "hipblaslt_TFLOPs": round(f / (blas * 1e-3) / 1e12, 1)}
+            del A, B, C, ws
+        out["gemm_vs_hipblaslt"] = ctx
     return out
 
 
