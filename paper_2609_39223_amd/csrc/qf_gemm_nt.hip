@@ -212,7 +212,11 @@ __device__ __forceinline__ int remap_xcd(int bid, int nb) {
 // loaded right after the last MFMA that uses the same register for stage s, so it has a whole
 // step to arrive; A's copies of stage s+1 all go out at the start of step s, ahead of every B
 // load of the step, and the barrier waits for them while leaving that step's B loads in flight.
-template <bool C_F32, int MODE, bool A_MN, bool B_MN, int WAVES, int BQ = 0, bool BF = false>
+//
+// AT2 (A^T modes): a tile may own two A^T pieces per stage (fewer than 16 tile columns); without
+// it the launch has at least 16 and a tile owns at most one.
+template <bool C_F32, int MODE, bool A_MN, bool B_MN, int WAVES, int BQ = 0, bool BF = false,
+          bool AT2 = false>
 __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
   static_assert(WAVES == 8 || (!A_MN && !B_MN), "operands stored [K][rows] need 8 wavefronts");
   static_assert(BQ == 0 || (WAVES == 4 && MODE == kDense && !C_F32),
@@ -251,7 +255,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
 
   const uint16_t* Bp = p.B;
   int64_t m0, m_end, n0;
-  int64_t ks0 = 0, ks1 = p.K / BK;               // stage range of this item
+  int ks0 = 0, ks1 = (int)(p.K / BK);            // stage range of this item
   int64_t cofs = 0;                              // element offset of this item's C
   // A^T columns of this tile's first row and the end of its A^T range: rows whose column is
   // below at_end but lie past the operand get zeros (grouped padding)
@@ -592,17 +596,23 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
   // with row strides that are large powers of two, k-aligned requests from all CUs otherwise
   // pile onto the same HBM channels.  Each tile's sum order is fixed, so results are
   // deterministic.
-  if (half == 1) ks0 = p.split_stage;
-  if (half == 0) ks1 = p.split_stage;
-  const int64_t klen = ks1 > ks0 ? ks1 - ks0 : 1;
-  const int64_t krot = (int64_t)(blockIdx.x % kXcds) * (klen / kXcds);
-  auto dma = [&](int64_t s, int buf, int q) __attribute__((always_inline)) {
-    int64_t se = s + krot;
-    if (se >= ks1) se -= klen;
+  // (Stage indices are 32-bit: fewer scalar instructions in the main loop's issue slots.)
+  if (half == 1) ks0 = (int)p.split_stage;
+  if (half == 0) ks1 = (int)p.split_stage;
+  const int klen = ks1 > ks0 ? ks1 - ks0 : 1;
+  const int krot = (int)(blockIdx.x % kXcds) * (klen / kXcds);
+  // global stage of loop stage s
+  auto gstage = [&](int s) __attribute__((always_inline)) -> int {
+    const int se = s + krot;
+    return se >= ks1 ? se - klen : se;
+  };
+  const uint32_t sstride32 = (uint32_t)sstride;
+  // load q of global stage se into buffer buf
+  auto dma = [&](int se, int buf, int q) __attribute__((always_inline)) {
     char* l = smem + buf * kStage + lds_of(q);
     const int op = op_of(q);
-    if (QF_NT_GLOBAL_LDS) dma16_global(gb[op] + se * sstride + goff[q], l);
-    else dma16_buf(rs[op], goff[q], (uint32_t)(se * sstride), l);
+    if (QF_NT_GLOBAL_LDS) dma16_global(gb[op] + (int64_t)se * sstride + goff[q], l);
+    else dma16_buf(rs[op], goff[q], (uint32_t)se * sstride32, l);
   };
   // Fragment read r of a slice, in the order the slice's MFMAs consume them: A0, B0, B1, A1..A3.
   auto frag = [&](const char* st, int kk, int f, bool is_b) __attribute__((always_inline)) -> bf16x8_t {
@@ -681,13 +691,40 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
     at_u_wrap = at_first(ks0);                   // the stage after the wrap to ks0
     at_d = (int)(16 % p.tiles_n);
   }
+  // The main loop's form of at_read / at_store, split into small pieces that go into the
+  // issue slots between MFMAs (with one wavefront per SIMD a slot has room for a few
+  // instructions only; more stall the MFMA stream).  With kc = 4 u + at_c (at_c < 4),
+  // kc >> 3 = u >> 1 and kc & 7 = 4 (u & 1) + at_c, so element e of piece u sits at
+  // at_lb[e] + ((u >> 1) << 4 ^ at_sw[e >> 1]) + 8 (u & 1) in the stage (rows at_r + e share
+  // (row >> 1) & 7 in pairs).  at_read2 reads elements e0, e0 + 1 of piece u (u < 16) from
+  // buffer buf.
+  int at_lb[4], at_sw[2];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) at_lb[e] = (at_r + e) * kRow + at_c * 2;
+#pragma unroll
+  for (int e = 0; e < 2; ++e) at_sw[e] = (((at_r + 2 * e) >> 1) & 7) << 4;
+  auto at_read2 = [&](int buf, int u, int e0, u32x4_t& h) __attribute__((always_inline)) {
+    const int xs = (u >> 1) << 4, ad = buf * kStage + ((u & 1) << 3);
+    const int x = xs ^ at_sw[e0 >> 1];
+    h[e0] = *reinterpret_cast<const uint16_t*>(smem + at_lb[e0] + x + ad);
+    h[e0 + 1] = *reinterpret_cast<const uint16_t*>(smem + at_lb[e0 + 1] + x + ad);
+  };
+  // bytes of a stage's rows of A^T (below 2^31: ldat < 2^24)
+  const uint32_t at_sbytes = (uint32_t)(BK * p.ldat * 2);
+  auto at_pack = [&](const u32x4_t& h) __attribute__((always_inline)) -> u32x2_t {
+    return at_rok ? u32x2_t{h[0] | (h[1] << 16), h[2] | (h[3] << 16)} : u32x2_t{0, 0};
+  };
+  auto at_put = [&](__amdgpu_buffer_rsrc_t r, int u, u32x2_t v) __attribute__((always_inline)) {
+    const int off = at_zok && u < 16 ? at_off + u * at_ld8 : 0x7FFFFFF8;
+    __builtin_amdgcn_raw_buffer_store_b64(v, r, off, 0, 0);
+  };
+  constexpr bool at_two = AT && AT2;             // a second piece per stage is possible
   // One 16-deep slice of MFMAs from (a, b), with the fragment reads of the next slice (from
-  // rst / rkk into ra, rb) and, if LOADS, the direct-to-LDS loads of stage ls into buffer
-  // lbuf, issued one per MFMA.  The scheduling fences keep that interleave.
-  // extra(t) runs after MFMA t (the A^T modes: the A^T reads and stores).
-  auto noextra = [](int) {};
+  // rst / rkk into ra, rb) and, if LOADS, the direct-to-LDS loads of global stage ls into
+  // buffer lbuf, issued one per MFMA.  The scheduling fences keep that interleave.
+  // extra(t) runs after MFMA t (the A^T reads and stores, the packed-B decode, index updates).
   auto slice = [&](auto reads, auto loads, const bf16x8_t* a, const bf16x8_t* b,
-                   const char* rst, int rkk, bf16x8_t* ra, bf16x8_t* rb, int64_t ls, int lbuf,
+                   const char* rst, int rkk, bf16x8_t* ra, bf16x8_t* rb, int ls, int lbuf,
                    int qa, int nq, auto extra) __attribute__((always_inline)) {
     constexpr bool READS = decltype(reads)::value, LOADS = decltype(loads)::value;
     constexpr int NM = 4 * NJ, NR = 4 + NJ;
@@ -707,91 +744,101 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
   };
   // Loads are spread over the step: stage s+1's loads go out L0 in the last slice of step s-1
   // (right after its barrier freed stage s-1's buffer), L1 in slice 0 and L2 in slice 1 of
-  // step s; the barrier before slice 3 waits for them.
-  auto step = [&](int64_t s, int64_t s_end, auto last) __attribute__((always_inline)) {
-    constexpr bool LAST = decltype(last)::value;
-    const int cur = (int)((s - ks0) & 1), nxt = cur ^ 1;
+  // step s; the barrier before slice 3 waits for them.  A step knows the global stages of
+  // loop stages s and s+1 (e_cur, e_nx1, handed on by the step before) and works out that of
+  // s+2 (e_nx2) in a free slot of slice 2.  LD1 / LD2: loop stages s+1 / s+2 exist (no copies
+  // are issued for stages past the end, so the epilogue does not wait for any).  cur: the
+  // buffer holding stage s.
+  int e_cur = 0, e_nx1 = 0;
+  auto step = [&](int s, int s_end, auto last, auto ld1, auto ld2, int cur)
+      __attribute__((always_inline)) {
+    constexpr bool LAST = decltype(last)::value, LD1 = decltype(ld1)::value;
+    constexpr bool LD2 = decltype(ld2)::value;
+    const int nxt = cur ^ 1;
     const char* cs = smem + cur * kStage;
-    // Stages past the end are clamped to the last one: their copies land in a buffer that is
-    // not read again, and the epilogue's barrier drains them.
-    const int64_t n1 = s + 1 < s_end ? s + 1 : s_end - 1;
-    const int64_t n2 = s + 2 < s_end ? s + 2 : s_end - 1;
-    // A^T modes: this tile's A^T pieces of the stage (at most two, u0 and u0 + tiles_n) are
-    // read in slice 1, while the stage is resident, and stored in slice 3, after the barrier.
-    int64_t se = 0;
-    int u0 = 16, u1 = 16;
-    u32x4_t v0 = {0, 0, 0, 0}, v1 = {0, 0, 0, 0};
-    if (AT) {
-      se = s + krot;
-      if (se >= ks1) se -= klen;
-      if (s != ks0) {                            // at_u holds the previous stage's piece
-        at_u = se == ks0 ? at_u_wrap : at_u - at_d;
-        if (at_u < 0) at_u += p.tiles_n;
-      }
-      u0 = at_u;
-      u1 = u0 + p.tiles_n;
-    }
-    auto at_rd = [&](int t) __attribute__((always_inline)) {
-      if (AT && t == 8) {
-        if (u0 < 16) v0 = at_read(cs, u0);
-        if (u1 < 16) v1 = at_read(cs, u1);
-      }
+    // packed or fragment-major B use stage s+2's index from slice 0 on
+    constexpr bool EARLY = BQ != 0 || BF;
+    int e_nx2 = 0;
+    auto calc_nx2 = [&]() __attribute__((always_inline)) {
+      e_nx2 = gstage(s + 2 < s_end ? s + 2 : s_end - 1);
     };
-    auto at_st = [&](int t) __attribute__((always_inline)) {
-      if (AT && t == 8) {
-        if (u0 < 16) at_store(se, BK, u0, v0);
-        if (u1 < 16) at_store(se, BK, u1, v1);
+    if (EARLY) calc_nx2();
+    // A^T modes: this tile's A^T pieces of the stage (u0 and, with fewer than 16 tile columns,
+    // u0 + tiles_n; >= 16: none) are read in slice 1, while the stage is resident, and stored
+    // in slice 3, after the barrier; at_u then moves on to stage s+1's piece.
+    const int u0 = at_u, u1 = at_u + p.tiles_n;
+    u32x4_t v0 = {0, 0, 0, 0}, v1 = {0, 0, 0, 0};
+    u32x2_t w0 = {0, 0}, w1 = {0, 0};
+    // the main loop's stores cover a full stage (kvalid = BK) of A^T rows
+    __amdgpu_buffer_rsrc_t at_rs;
+    const char* at_base = nullptr;
+    auto at_hook1 = [&](int t) __attribute__((always_inline)) {
+      if (!AT) return;
+      if (t == 8) at_read2(cur, u0 & 15, 0, v0);
+      if (t == 9) at_read2(cur, u0 & 15, 2, v0);
+      if (at_two && t == 10) at_read2(cur, u1 & 15, 0, v1);
+      if (at_two && t == 11) at_read2(cur, u1 & 15, 2, v1);
+    };
+    auto at_hook2 = [&](int t) __attribute__((always_inline)) {
+      if (AT && t == 12)
+        at_base = reinterpret_cast<const char*>(p.at) + (uint64_t)(uint32_t)e_cur * at_sbytes;
+      if (AT && t == 13) at_rs = make_rsrc(at_base, (int64_t)at_sbytes);
+    };
+    auto at_hook3 = [&](int t) __attribute__((always_inline)) {
+      if (!AT) return;
+      if (t == 8) w0 = at_pack(v0);
+      if (t == 9) at_put(at_rs, u0, w0);
+      if (at_two && t == 10) w1 = at_pack(v1);
+      if (at_two && t == 11) at_put(at_rs, u1, w1);
+      if (!LAST && t == 13) {
+        int u = e_nx1 == ks0 ? at_u_wrap : at_u - at_d;
+        at_u = u < 0 ? u + p.tiles_n : u;
       }
     };
     // Packed B: stage s+2's registers are loaded in slice 0 (they have the rest of the step,
     // up to the barrier's wait), and stage s+1's (loaded one step earlier) are decoded into
     // buffer nxt in small operations spread over slices 0-2.
-    int64_t se1 = 0, se2 = 0;
-    if (BQ != 0 || BF) {
-      se1 = n1 + krot;
-      if (se1 >= ks1) se1 -= klen;
-      se2 = n2 + krot;
-      if (se2 >= ks1) se2 -= klen;
-    }
     // slot g (0..47) = the MFMA of slices 0-2 that the operation follows
     auto bq_slot = [&](int g) __attribute__((always_inline)) {
       if (BQ != 0) {
-        if (g == 1) bq_load(se2, bq_nxt);
+        if (g == 1) bq_load(e_nx2, bq_nxt);
         if (BQ == QF_FMT_MXFP4) {
-          if ((g & 1) == 0 && g / 2 < kBqOps) bq_op(bq_cur, se1, g / 2, nxt);
+          if ((g & 1) == 0 && g / 2 < kBqOps) bq_op(bq_cur, e_nx1, g / 2, nxt);
         } else if (g < kBqOps) {
-          bq_op(bq_cur, se1, g, nxt);
+          bq_op(bq_cur, e_nx1, g, nxt);
         }
       }
     };
     // Fragment-major B: after MFMA t = 12 + j of slice kk (the last one using fbr[kk][j]), that
     // register is loaded with stage s+1's fragment (not in the last step).
     auto bf_hook = [&](int kk, int t) __attribute__((always_inline)) {
-      if (BF && !LAST && t >= 12) bf_load(se1, kk, t - 12);
+      if (BF && !LAST && t >= 12) bf_load(e_nx1, kk, t - 12);
     };
-    auto bq0 = [&](int t) __attribute__((always_inline)) {
+    auto hook0 = [&](int t) __attribute__((always_inline)) {
       bq_slot(t);
       bf_hook(0, t);
     };
-    auto bq1 = [&](int t) __attribute__((always_inline)) {
+    auto hook1 = [&](int t) __attribute__((always_inline)) {
       bq_slot(16 + t);
-      at_rd(t);
+      at_hook1(t);
       bf_hook(1, t);
     };
-    auto bq2 = [&](int t) __attribute__((always_inline)) {
+    auto hook2 = [&](int t) __attribute__((always_inline)) {
       bq_slot(32 + t);
+      at_hook2(t);
+      if (!EARLY && t == 2 * NJ + 1) calc_nx2();   // a free slot (slices hold 4 NJ MFMAs)
       bf_hook(2, t);
     };
-    auto bq3 = [&](int t) __attribute__((always_inline)) {
-      at_st(t);
+    auto hook3 = [&](int t) __attribute__((always_inline)) {
+      at_hook3(t);
       bf_hook(3, t);
     };
-    slice(std::true_type{}, std::true_type{}, fa[0], BF ? fbr[0] : fb[0], cs, 1, fa[1], fb[1], n1,
-          nxt, L0, L1, bq0);
-    slice(std::true_type{}, std::true_type{}, fa[1], BF ? fbr[1 % (BF ? 4 : 1)] : fb[1], cs, 2,
-          fa[0], fb[0], n1, nxt, L0 + L1, L2, bq1);
+    slice(std::true_type{}, std::integral_constant<bool, LD1>{}, fa[0], BF ? fbr[0] : fb[0], cs,
+          1, fa[1], fb[1], e_nx1, nxt, L0, L1, hook0);
+    slice(std::true_type{}, std::integral_constant<bool, LD1>{}, fa[1],
+          BF ? fbr[1 % (BF ? 4 : 1)] : fb[1], cs, 2, fa[0], fb[0], e_nx1, nxt, L0 + L1, L2, hook1);
     slice(std::true_type{}, std::false_type{}, fa[0], BF ? fbr[2 % (BF ? 4 : 1)] : fb[0], cs, 3,
-          fa[1], fb[1], 0, 0, 0, 0, bq2);
+          fa[1], fb[1], 0, 0, 0, 0, hook2);
     if (BF && !LAST) {
       // A's copies of stage s+1 and everything before them; the 12 B loads issued after them in
       // slices 0-2 stay in flight (vmcnt(12); expcnt not waited; lgkmcnt(0): this wavefront's
@@ -803,63 +850,63 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     if (BQ != 0) bq_cur = bq_nxt;               // complete: the wait above covered its loads
-    slice(std::integral_constant<bool, !LAST>{}, std::true_type{}, fa[1],
-          BF ? fbr[3 % (BF ? 4 : 1)] : fb[1], smem + nxt * kStage, 0, fa[0], fb[0], n2, cur, 0,
-          L0, bq3);
+    slice(std::integral_constant<bool, !LAST>{}, std::integral_constant<bool, LD2>{}, fa[1],
+          BF ? fbr[3 % (BF ? 4 : 1)] : fb[1], smem + nxt * kStage, 0, fa[0], fb[0], e_nx2, cur, 0,
+          L0, hook3);
+    e_cur = e_nx1;
+    e_nx1 = e_nx2;
   };
 
   const int64_t nfull = K / BK;                 // the K tail (dense, second half) follows it
   // (packed or fragment-major B: K is a multiple of BK, checked on the host)
   const int64_t krem = (half == 0 || MODE == kGroupK || BQ != 0 || BF) ? 0 : K % BK;
-  const int64_t s0 = ks0, s1 = ks1;
+  const int s0 = ks0, s1 = ks1;
   if (s1 > s0) {
+    e_cur = gstage(s0);
+    e_nx1 = gstage(s0 + 1 < s1 ? s0 + 1 : s1 - 1);
 #pragma unroll
-    for (int q = 0; q < NLD; ++q) dma(s0, 0, q);
+    for (int q = 0; q < NLD; ++q) dma(e_cur, 0, q);
     if (BF) {
-      int64_t se = s0 + krot;
-      if (se >= ks1) se -= klen;
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) bf_load(se, kk, j);
+        for (int j = 0; j < 4; ++j) bf_load(e_cur, kk, j);
     }
     if (BQ != 0) {
       // stage s0's B decoded now; stage s0+1's registers for the first step
-      auto se_of = [&](int64_t st) {
-        int64_t se = st + krot;
-        return se >= ks1 ? se - klen : se;
-      };
       BqRegs first;
-      bq_load(se_of(s0), first);
-      bq_load(se_of(s0 + 1 < s1 ? s0 + 1 : s1 - 1), bq_cur);
+      bq_load(e_cur, first);
+      bq_load(e_nx1, bq_cur);
 #pragma unroll
-      for (int c = 0; c < 8; ++c) bq_decode(first, se_of(s0), c, 0);
+      for (int c = 0; c < 8; ++c) bq_decode(first, e_cur, c, 0);
     }
     if (s0 + 1 < s1) {
 #pragma unroll
-      for (int q = 0; q < L0; ++q) dma(s0 + 1, 1, q);
+      for (int q = 0; q < L0; ++q) dma(e_nx1, 1, q);
     }
     __builtin_amdgcn_s_waitcnt(0);
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     read_all(smem, 0, fa[0], fb[0]);
-    int64_t s = s0;
-    if (AT) {
-      int64_t se = s0 + krot;
-      if (se >= ks1) se -= klen;
-      at_u = at_first(se);
-    }
+    int s = s0;
+    if (AT) at_u = at_first(e_cur);
+    const std::true_type T{};
+    const std::false_type F{};
     if (WAVES == 4) {
       // two steps per iteration: with one loop-carried copy of the 256 accumulators the
       // register allocator keeps them in place (a one-step loop body rotates them through
       // other AGPRs at every back edge)
-      for (; s + 2 < s1; s += 2) {
-        step(s, s1, std::false_type{});
-        step(s + 1, s1, std::false_type{});
+      for (; s + 3 < s1; s += 2) {
+        step(s, s1, F, T, T, 0);
+        step(s + 1, s1, F, T, T, 1);
       }
     }
-    for (; s < s1 - 1; ++s) step(s, s1, std::false_type{});
-    step(s1 - 1, s1, std::true_type{});
+    for (; s + 2 < s1; ++s) step(s, s1, F, T, T, (s - s0) & 1);
+    if (s + 1 < s1) {
+      step(s, s1, F, T, F, (s - s0) & 1);
+      ++s;
+    }
+    step(s, s1, T, F, F, (s - s0) & 1);
   }
   if (krem > 0) {
     // Partial last stage: masked loads through registers into buffer 0.  The wait + barrier
@@ -1091,7 +1138,7 @@ hipError_t launch_dense(int64_t M, int64_t N, int64_t K, const uint16_t* A, int6
   const dim3 b8(8 * 64), b4(4 * 64);
   if (bf) {
     if (c_f32) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, false, false, 4, 0, true>), grid, b4, 0, s, a);
-    else if (at != nullptr) hipLaunchKernelGGL((gemm_nt_kernel<false, kDenseAT, false, false, 4, 0, true>), grid, b4, 0, s, a);
+    else if (at != nullptr) hipLaunchKernelGGL((gemm_nt_kernel<false, kDenseAT, false, false, 4, 0, true, true>), grid, b4, 0, s, a);
     else hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, false, false, 4, 0, true>), grid, b4, 0, s, a);
   } else if (c_f32) {
     if (a_mn && b_mn) hipLaunchKernelGGL((gemm_nt_kernel<true, kDense, true, true, 8>), grid, b8, 0, s, a);
@@ -1102,6 +1149,7 @@ hipError_t launch_dense(int64_t M, int64_t N, int64_t K, const uint16_t* A, int6
     if (a_mn && b_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, true, true, 8>), grid, b8, 0, s, a);
     else if (b_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, false, true, 8>), grid, b8, 0, s, a);
     else if (a_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, true, false, 8>), grid, b8, 0, s, a);
+    else if (at != nullptr && a.tiles_n < 16) hipLaunchKernelGGL((gemm_nt_kernel<false, kDenseAT, false, false, 4, 0, false, true>), grid, b4, 0, s, a);
     else if (at != nullptr) hipLaunchKernelGGL((gemm_nt_kernel<false, kDenseAT, false, false, 4>), grid, b4, 0, s, a);
     else hipLaunchKernelGGL((gemm_nt_kernel<false, kDense, false, false, 4>), grid, b4, 0, s, a);
   }
@@ -1210,6 +1258,7 @@ hipError_t launch_grouped_nt_rows(int64_t E, int64_t T, int64_t N, int64_t K, co
   const int64_t per = ((int64_t)a.tiles_m * a.tiles_n + kXcds - 1) / kXcds;
   const dim3 grid((unsigned)(kXcds * per));
   if (b_mn) hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRows, false, true, 8>), grid, dim3(8 * 64), 0, s, a);
+  else if (at != nullptr && a.tiles_n < 16) hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRowsAT, false, false, 4, 0, false, true>), grid, dim3(4 * 64), 0, s, a);
   else if (at != nullptr) hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRowsAT, false, false, 4>), grid, dim3(4 * 64), 0, s, a);
   else hipLaunchKernelGGL((gemm_nt_kernel<false, kGroupRows, false, false, 4>), grid, dim3(4 * 64), 0, s, a);
   return hipGetLastError();
