@@ -716,7 +716,7 @@ __global__ __launch_bounds__(WAVES * 64, 1) void gemm_nt_kernel(NtArgs p) {
   };
   auto at_put = [&](__amdgpu_buffer_rsrc_t r, int u, u32x2_t v) __attribute__((always_inline)) {
     const int off = at_zok && u < 16 ? at_off + u * at_ld8 : 0x7FFFFFF8;
-    __builtin_amdgcn_raw_buffer_store_b64(v, r, off, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b64(v, r, off, 0, 2);   // non-temporal
   };
   constexpr bool at_two = AT && AT2;             // a second piece per stage is possible
   // One 16-deep slice of MFMAs from (a, b), with the fragment reads of the next slice (from
