@@ -50,11 +50,13 @@ def test_gemm_layouts_ragged(qf, a_km, b_km, c32, M, N, K):
 
 
 @pytest.mark.parametrize("M,N,K", [(264, 2056, 200), (512, 64, 136), (1032, 2304, 4104),
-                                   (8, 2048, 8), (64, 0, 72), (2048, 4096, 1024)])
+                                   (8, 2048, 8), (64, 0, 72), (2048, 4096, 1024),
+                                   (520, 3840, 2056)])
 def test_gemm_with_transposed_a_output(qf, M, N, K):
     """qf_gemm_bf16_at: C bit-identical to qf_gemm_bf16 and at = A^T exactly, padding columns
-    untouched (8 or 9 tile columns: A^T from the GEMM's staged tiles, ragged last stage and
-    rows; 1 tile column or N = 0: from the transpose kernel)."""
+    untouched (8, 9 or 15 tile columns: A^T from the GEMM's staged tiles, up to two pieces per
+    tile and stage; 16: at most one; ragged last stage and rows; 1 tile column or N = 0: from
+    the transpose kernel)."""
     rng = np.random.default_rng(M * 5 + N + K)
     A, B = _rand_bf16(rng, (M, K)), _rand_bf16(rng, (N, K))
     Ad, Bd = to_dev(A), to_dev(B)
