@@ -87,12 +87,14 @@ def test_grouped_dw_tile_grid_split_over_xcds(qf):
             assert np.all(dW[e] == 0.0)
 
 
-def test_grouped_dw_alone_equals_dw_with_dx(qf):
+@pytest.mark.parametrize("K", [2048, 4096])
+def test_grouped_dw_alone_equals_dw_with_dx(qf, K):
     """With 8 or more tile columns in dX the grouped dX launch writes the padded dY^T for dW
-    (zeros past each expert's last token, written by the tile holding its last rows); asked
-    for alone, dW takes it from the grouped transposer: bit-identical dW, equal to the oracle."""
+    (zeros past each expert's last token, written by the tile holding its last rows; 8 tile
+    columns: up to two pieces per tile and stage, 16: one); asked for alone, dW takes it from
+    the grouped transposer: bit-identical dW, equal to the oracle, and dX equal to the oracle."""
     rng = np.random.default_rng(26)
-    E, N, K = 5, 136, 2048
+    E, N = 5, 136
     counts = np.array([0, 300, 1, 513, 77])
     offsets = np.concatenate([[0], np.cumsum(counts)])
     T = int(offsets[-1])
@@ -103,6 +105,7 @@ def test_grouped_dw_alone_equals_dw_with_dx(qf):
     off = torch.from_numpy(offsets.astype(np.int64)).cuda()
     Xd, Wd, dYd = to_dev(X), to_dev(W.reshape(E * N, K)), to_dev(dY)
     outs = []
+    dx_got = None
     for want_dx in (True, False):
         ws = qf.grouped_workspace(d)
         ws.fill_(0x5A)                              # stale workspace bytes must not leak in
@@ -111,12 +114,16 @@ def test_grouped_dw_alone_equals_dw_with_dx(qf):
         qf.qlinear_grouped_bwd_ste(d, off, dYd, Xd, Wd, dX, dW, ws)
         torch.cuda.synchronize()
         outs.append(from_dev(dW))
+        if want_dx:
+            dx_got = bf16_to_f64(from_dev(dX))
     assert np.array_equal(outs[0].view(np.uint32), outs[1].view(np.uint32))
     for e in range(E):
         r0, r1 = offsets[e], offsets[e + 1]
         if r1 > r0:
             assert_close(outs[0][e].astype(np.float64), oracle.linear_dw(dY[r0:r1], X[r0:r1]),
                          f"dW e={e}")
+            what = oracle.fakequant(W[e], "nvfp4")       # one tensor scale per expert
+            assert_close(dx_got[r0:r1], oracle.linear_dx(dY[r0:r1], what), f"dX e={e}")
         else:
             assert np.all(outs[0][e] == 0.0)
 
