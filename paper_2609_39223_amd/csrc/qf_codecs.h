@@ -474,6 +474,105 @@ __device__ __forceinline__ void q4k_chunk(const uint32_t h[8], Q4kChunk& r, uint
 }
 
 
+// ---- Q4_K, sixteen elements per lane ---------------------------------------------------------
+// The row quantizer's form: lane L of a group of 16 holds elements 16 L .. 16 L + 15 of a
+// super-block (sub-block L / 2, its half L % 2), so a sub-block's extremes take one lane
+// exchange and the per-sub-block work (step, offset, 6-bit codes, FP16 scales, block header) is
+// shared by twice as many elements as in q4k_chunk.  Every value comes from the same operations
+// as there (minima and maxima do not depend on the order of their reductions), so the codes,
+// scales and x_hat are the same bits.
+// DPP row mirrors: lane i <-> 7 - i inside each 8 lanes, 15 - i inside each 16.
+__device__ __forceinline__ uint32_t half_mirror_u32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false);
+}
+__device__ __forceinline__ uint32_t mirror_u32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, false);
+}
+// Maximum over a group of 16 lanes of a value that lanes 2j and 2j + 1 hold alike: quads by
+// lane ^ 2, then the two quads of each 8 by the half mirror, then the two 8s by the mirror.
+__device__ __forceinline__ float max16_pairs(float v) {
+  v = fmaxf(v, as_f32(xor2_u32(as_u32(v))));
+  v = fmaxf(v, as_f32(half_mirror_u32(as_u32(v))));
+  return fmaxf(v, as_f32(mirror_u32(as_u32(v))));
+}
+
+struct Q4kChunk16 {
+  uint32_t dh, mh, ls, lm, q[4];            // q: the 16 codes, element k in byte k % 4 of q[k / 4]
+};
+
+// h: the lane's 16 bf16 inputs; xw: x_hat as 8 words of bf16 pairs (element 2i in the low half).
+__device__ __forceinline__ void q4k_chunk16(const uint32_t h[16], Q4kChunk16& r, uint32_t xw[8]) {
+  float xv[16];
+  float lo = 0.0f, hi = -__builtin_huge_valf();
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    xv[k] = as_f32(h[k] << 16);
+    lo = fminf(lo, xv[k]);
+    hi = fmaxf(hi, xv[k]);
+  }
+  lo = fminf(lo, xor1_f(lo)); hi = fmaxf(hi, xor1_f(hi));
+  lo = lo + 0.0f;                           // signed zeros count as +0 (as in q4k_chunk)
+  hi = hi + 0.0f;
+  const float a = div_nonneg_by<15>(hi - lo);   // step of the sub-block, fl((hi - lo) / 15)
+  const float mu = 0.0f - lo;               // offset (subtracted), never negative
+  const float A = max16_pairs(a), Mx = max16_pairs(mu);
+  r.dh = f16_rne_sat(div_nonneg_by<63>(A));
+  r.mh = f16_rne_sat(div_nonneg_by<63>(Mx));
+  const float d = f16_value(r.dh), dmin = f16_value(r.mh);
+  r.ls = 0;
+  r.lm = 0;
+  if (d != 0.0f) r.ls = q6_code(a, d);
+  if (dmin != 0.0f) r.lm = q6_code(mu, dmin);
+  const float t1 = d * (float)r.ls;
+  const float t2 = dmin * (float)r.lm;
+  float qv[16];
+#pragma unroll
+  for (int k = 0; k < 16; ++k) qv[k] = 0.0f;
+  if (t1 != 0.0f) {
+    float av[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) av[k] = xv[k] + t2;
+    q4_codes8(av, t1, qv);
+    q4_codes8(av + 8, t1, qv + 8);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) r.q[i] = q4_bytes4(qv + 4 * i);
+  q4k_decode8f(qv, t1, t2, xw);
+  q4k_decode8f(qv + 8, t1, t2, xw + 4);
+}
+
+// Packs the super-block held by 16 lanes (lane L: sub-block L / 2, half L % 2) into its 144-byte
+// block at blk, in the layout q4k_store writes.  Every lane of the group must call it
+// (cross-lane moves); `store` predicates the writes.
+__device__ __forceinline__ void q4k_store16(const Q4kChunk16& q, int L, bool store, uint8_t* blk) {
+  // Lane 2j holds sub-block j's scale and min.  Bytes j and 4 + j come together at lane 2j,
+  // pairs of them at lanes 0 and 4 (lane ^ 2), all eight at lane 0 (lane ^ 4); bytes 8 + j
+  // start at lane 8 + 2j and meet at lane 8, then lane 0.
+  const uint32_t own = q.ls | (q.lm << 16);
+  const uint32_t up = xor_swz_u32<8>(own);                   // scale, min of sub-block j + 4
+  const uint32_t v = (own & 0x003F003Fu) | (((up >> 4) & 0x00030003u) << 6);  // bytes j, 4+j
+  const uint32_t v2 = xor2_u32(v);
+  const uint32_t pv = (v & 0x00FF00FFu) | ((v2 & 0x00FF00FFu) << 8);  // lane 0: b0 b1 b4 b5
+  const uint32_t pv4 = xor_swz_u32<4>(pv);                   // lane 0: b2 b3 b6 b7
+  const uint32_t w0 = (q.ls & 15u) | ((q.lm & 15u) << 4);    // lane 8 + 2j: byte 8 + j
+  const uint32_t pw = w0 | (xor2_u32(w0) << 8);              // lane 8: b8 b9, lane 12: b10 b11
+  const uint32_t pw4 = xor_swz_u32<4>(pw);
+  const uint32_t sw = xor_swz_u32<8>(pw | (pw4 << 16));      // lane 0: b8 b9 b10 b11
+  // codes of the odd sub-block (lane L ^ 2) go to the high nibbles of the even one's bytes
+  uint32_t pq[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) pq[i] = xor2_u32(q.q[i]);
+  if (!store) return;
+  if (L == 0)
+    *reinterpret_cast<uint4*>(blk) =
+        make_uint4(q.dh | (q.mh << 16), (pv & 0xFFFFu) | (pv4 << 16),
+                   (pv >> 16) | (pv4 & 0xFFFF0000u), sw);
+  if ((L & 2) == 0)
+    *reinterpret_cast<uint4*>(blk + 16 + 32 * (L >> 2) + 16 * (L & 1)) =
+        make_uint4(q.q[0] | (pq[0] << 4), q.q[1] | (pq[1] << 4), q.q[2] | (pq[2] << 4),
+                   q.q[3] | (pq[3] << 4));
+}
+
 // ---- Q4_K with searched sub-block steps ------------------------------------------------------
 // Sums over a 32-element sub-block in one fixed order: this lane's 8 elements from +0 in
 // index order, then the quad tree (g0 + g1) + (g2 + g3) (lane ^ 1, then lane ^ 2; the same

@@ -184,14 +184,16 @@ def test_q4k_wide_range_edge_blocks_and_ragged(qf):
         assert_same(run_q4k(qf, x, ld), oracle.q4k(x), ("packed", "xhat"), f"q4k {R}x{K}")
 
 
-def test_q4k_exhaustive_bf16_inputs_below_limits(qf):
+@pytest.mark.parametrize("width", [256, 1024])
+def test_q4k_exhaustive_bf16_inputs_below_limits(qf, width):
     # every bf16 pattern with magnitude below 2^100 (super-block ranges stay finite in FP32),
-    # then every pattern below 2^14 (scales inside the FP16 range), in shuffled blocks
+    # then every pattern below 2^14 (scales inside the FP16 range), in shuffled blocks; rows of
+    # 256 and of 1024 elements (the row quantizer's two forms: 8 and 16 elements per lane)
     v = np.arange(65536, dtype=np.uint32).astype(np.uint16)
     for lim, seed in ((2.0 ** 100, 7), (2.0 ** 14, 8)):
         mag = np.abs((v.astype(np.uint32) << 16).view(np.float32))
         sel = np.random.default_rng(seed).permutation(v[mag < lim])
-        x = sel[: len(sel) // 256 * 256].reshape(-1, 256)
+        x = sel[: len(sel) // width * width].reshape(-1, width)
         assert_same(run_q4k(qf, x), oracle.q4k(x), ("packed", "xhat"), f"q4k below {lim}")
 
 
@@ -216,6 +218,12 @@ def test_q4k_exact_rounding_ties(qf):
     assert d == 0x2800 and ls[1:] == [32] * 7                 # t1 = 1 in sub-blocks 1-7
     assert_same(run_q4k(qf, x), ref, ("packed", "xhat"), "q4k ties")
     assert_same(run_q4k_mse(qf, x), oracle.q4k_mse(x), ("packed", "xhat"), "q4k-mse ties")
+
+
+def test_q4k_exact_rounding_ties_1024_wide_rows(qf):
+    # the tie rows laid end to end as rows of 1024 elements (the 16-elements-per-lane form)
+    x = np.tile(q4k_tie_rows(), (2, 1))[:8].reshape(2, 1024)
+    assert_same(run_q4k(qf, x), oracle.q4k(x), ("packed", "xhat"), "q4k ties, 1024-wide rows")
 
 
 def test_q4k_full_size_export_weight(qf):
