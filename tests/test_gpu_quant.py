@@ -176,7 +176,10 @@ def test_nvfp4_full_size_weights(qf):
 # -------------------------------------------------------------------------------- Q4_K
 def test_q4k_wide_range_edge_blocks_and_ragged(qf):
     rng = np.random.default_rng(5)
-    for R, K, ld in [(1, 256, None), (9, 768, None), (40, 4096, 4352), (3, 8448, None)]:
+    # (K a multiple of 1024 takes the 16-element form: 7 x 2048 and 5 x 3072 leave whole
+    # wavefronts of a workgroup past the row end, and odd row counts a half-used row pair)
+    for R, K, ld in [(1, 256, None), (9, 768, None), (40, 4096, 4352), (3, 8448, None),
+                     (7, 2048, None), (5, 3072, 3200)]:
         x = wide_range_bf16(rng, (R, K), lo_exp=-20, hi_exp=10, zero_frac=0.05)
         x[0, :32] = 0                                  # all-zero sub-block
         x[-1, 32:64] = 0x8000                          # all -0 sub-block
