@@ -36,39 +36,59 @@ __global__ void fill_f32_kernel(float* p, int64_t n, float v) {
 
 // ---- tensor amax --------------------------------------------------------------------------
 // max |x| as bf16 magnitude bits (NaN bit patterns sort above +inf), reduced per workgroup and
-// folded into a reduction slot with an integer atomic max (order independent, so the result is
-// exact and deterministic).  Each 64-bit slot holds the running maximum (binary32 bits) and a
-// ticket count of the workgroups that have folded theirs in; the workgroup that takes the last ticket
-// writes the result (*amax = m, or max(*amax, m) when accumulating, compared as bits) and
-// returns the slot to zero.  Slots start at zero when the library loads, so no pass needs a
-// clearing dispatch.  The host hands each pass its own slot (one per tensor of a batch) from a
-// ring of kAmaxSlots, so passes running concurrently on different streams do not share one
-// unless kAmaxSlots slots are taken in between.
-constexpr uint32_t kAmaxSlots = 4096;
-// low word: the running maximum (binary32 bits); high word: the ticket count
-__device__ uint64_t g_amax_slot[kAmaxSlots];
+// folded with integer atomic maxima (order independent, so the result is exact and
+// deterministic).  A fold word is 64 bits: the running maximum (binary32 bits) in the low word
+// and a ticket count of the contributors that have folded theirs in in the high word; the
+// contributor that takes the last ticket holds the maximum of all of them and returns the word
+// to zero.  Words start at zero when the library loads, so no pass needs a clearing dispatch.
+// A pass folds in two levels: workgroup i into first-level word i mod kAmaxSub, the last
+// workgroup of each of those into the top word, whose last contributor writes the result
+// (*amax = m, or max(*amax, m) when accumulating, compared as bits).  Every word sits on a
+// 256-byte line of its own: device-scope atomics on one line are performed one after another,
+// and a single word per pass cost ~2 us more at the end of a 14336 x 4096 pass.  The host hands
+// each pass its own slot (one per tensor of a batch) from a ring of kAmaxSlots, so passes
+// running concurrently on different streams do not share one unless kAmaxSlots slots are taken
+// in between.
+constexpr uint32_t kAmaxSlots = 1024;
+constexpr uint32_t kAmaxSub = 8;                     // first-level words per slot
+constexpr uint32_t kAmaxLine = 32;                   // 64-bit words per 256-byte line
+// slot s: first-level words at lines 9s .. 9s+7, the top word at line 9s+8
+__device__ uint64_t g_amax_slot[kAmaxSlots * (kAmaxSub + 1) * kAmaxLine];
 
-// Called by thread 0 of every workgroup of a pass with the workgroup's maximum b.
-__device__ __forceinline__ void amax_fold(uint32_t b, uint32_t slot, uint32_t nblocks,
-                                          float* amax, int accumulate) {
-  uint64_t* sl = &g_amax_slot[slot % kAmaxSlots];
-  const uint32_t v = b << 16;
-  // Device-scope atomics are performed at the device's coherence point.  The fold is
-  // acknowledged before the ticket is taken (the wait), so every fold precedes the last ticket,
-  // and the ticket's returned word carries the maximum of all of them; no cache write-back is
-  // needed for that (a release ordering would write back this XCD's L2 in every workgroup).
+// Folds v into word w as one of n contributors.  Returns true for the last one, with the
+// maximum of all n in m, after clearing the word.  Device-scope atomics are performed at the
+// device's coherence point.  The fold is acknowledged before the ticket is taken (the wait), so
+// every fold precedes the last ticket, and the ticket's returned word carries the maximum of all
+// of them; no cache write-back is needed for that (a release ordering would write back this
+// XCD's L2 in every workgroup).
+__device__ __forceinline__ bool fold_word(uint64_t* w, uint32_t v, uint32_t n, uint32_t& m) {
   if (v != 0u)
-    __hip_atomic_fetch_max(reinterpret_cast<uint32_t*>(sl), v, __ATOMIC_RELAXED,
+    __hip_atomic_fetch_max(reinterpret_cast<uint32_t*>(w), v, __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
   __builtin_amdgcn_s_waitcnt(0x0F70);            // vmcnt(0): the fold is acknowledged
   const uint64_t old =
-      __hip_atomic_fetch_add(sl, 1ull << 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  if ((uint32_t)(old >> 32) != nblocks - 1) return;
-  const uint32_t m = (uint32_t)old;
+      __hip_atomic_fetch_add(w, 1ull << 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if ((uint32_t)(old >> 32) != n - 1u) return false;
+  m = (uint32_t)old;
+  __hip_atomic_store(w, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return true;
+}
+
+// Called by thread 0 of every workgroup of a pass with the workgroup's maximum b.  The pass's
+// nblocks workgroups are those of one grid z plane, numbered x + y * gridDim.x.
+__device__ __forceinline__ void amax_fold(uint32_t b, uint32_t slot, uint32_t nblocks,
+                                          float* amax, int accumulate) {
+  uint64_t* rec = &g_amax_slot[(slot % kAmaxSlots) * (kAmaxSub + 1) * kAmaxLine];
+  const uint32_t i = blockIdx.x + blockIdx.y * gridDim.x;
+  const uint32_t sub = i % kAmaxSub;
+  uint32_t m;
+  if (!fold_word(rec + sub * kAmaxLine, b << 16, (nblocks - sub + kAmaxSub - 1u) / kAmaxSub, m))
+    return;
+  if (!fold_word(rec + kAmaxSub * kAmaxLine, m, nblocks < kAmaxSub ? nblocks : kAmaxSub, m))
+    return;
   uint32_t* out = reinterpret_cast<uint32_t*>(amax);
   const uint32_t prev = accumulate ? *out : 0u;
   *out = prev > m ? prev : m;
-  __hip_atomic_store(sl, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Block-wide maximum of m, then the fold by thread 0.

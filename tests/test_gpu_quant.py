@@ -309,7 +309,7 @@ def test_amax_passes_do_not_see_each_other(qf):
     want = {"big": oracle.amax(big), "small": oracle.amax(small), "zero": 0.0,
             "strided": oracle.amax(strided)}
     out = torch.full((1,), 1e30, dtype=torch.float32, device="cuda")
-    order = ["big", "small", "strided", "big", "zero", "strided", "small"] * 700   # > 4096 passes
+    order = ["big", "small", "strided", "big", "zero", "strided", "small"] * 700   # 4900: round the ring
     got = torch.empty(len(order), dtype=torch.float32, device="cuda")
     for i, k in enumerate(order):
         qf.amax(sd if k == "strided" else dev[k], out, accumulate=False)
