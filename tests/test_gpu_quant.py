@@ -355,6 +355,30 @@ def test_amax_row_tail_not_multiple_of_8(qf, K, col):
     assert float(out.item()) == oracle.amax(np.ascontiguousarray(buf[:, :K])) == 7.25
 
 
+@pytest.mark.parametrize("R", [100, 600])
+def test_amax_rows_two_dimensional_grid(qf, R):
+    """Strided rows 2999 wide run the row kernel on a grid with two workgroup columns and 7 or 38
+    workgroup rows; its workgroups fold in two levels by their linear index. The maximum is
+    planted in one workgroup's region at a time (both columns, first / middle / last row band,
+    the row's ragged tail) and must come out every time."""
+    K, ld = 2999, 3008
+    rng = np.random.default_rng(R)
+    base = (rng.uniform(-0.9, 0.9, (R, ld))).astype(np.float32)
+    base[:, K:] = 1e30                            # padding: must not be read
+    bands = (R + 15) // 16
+    spots = [(3, 7 * 8 + 2), (3, (256 + 7) * 8 + 2), (16 * (bands // 2) + 5, 11),
+             (R - 1, 2100), (R - 1, K - 1), (16 * (bands - 1), K - 3)]
+    out = torch.full((1,), 55.0, dtype=torch.float32, device="cuda")
+    for r, c in spots:
+        x = base.copy()
+        x[r, c] = -9.5
+        u = x.view(np.uint32)
+        buf = ((u + (((u >> 16) & 1) + 0x7FFF)) >> 16).astype(np.uint16)
+        qf.amax(to_dev(buf)[:, :K], out, accumulate=False)
+        torch.cuda.synchronize()
+        assert float(out.item()) == oracle.amax(np.ascontiguousarray(buf[:, :K])) == 9.5, (r, c)
+
+
 def test_q4k_handworked_block_bit_exact(qf):
     """The hand-worked super-block of the golden fixture: the kernel's 144 bytes equal the
     bytes worked out by hand (6-bit scale / min rounding, scale-bit and nibble layout)."""
