@@ -81,9 +81,10 @@ QF_API const char* qf_last_error(void);
  * K may be any size (no block constraint; ldx >= K, ldx % 8 == 0): elements past K in a row
  * are never read.  NaN inputs make *amax NaN.  R = 0 or K = 0 leaves a zero (accumulate = 0)
  * or unchanged value.  One kernel dispatch (no clearing dispatch before it): the workgroups
- * fold into one of 4096 per-device reduction slots, taken in turn per pass and left clear by
- * the pass's last workgroup, so passes on different streams run independently unless 4096
- * further passes start while one is still in flight.  Graph-capturable (no memset nodes).
+ * fold into one of 1024 per-device reduction slots, taken in turn per pass (one per tensor of
+ * a batch; grouped calls allow at most 1024 experts) and left clear by the pass's last
+ * workgroups, so passes on different streams run independently unless 1024 further slots are
+ * taken while one is still in flight.  Graph-capturable (no memset nodes).
  */
 QF_API qf_status qf_amax(const uint16_t* x, int64_t R, int64_t K, int64_t ldx, float* amax,
                   int accumulate, qf_stream_t stream);
